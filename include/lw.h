@@ -1,0 +1,142 @@
+/*
+ * lw.h — C ABI of the fused dequantize x matrix-vector library for MI355X (gfx950).
+ *
+ * The operation is the decode step of a transformer run with block-quantized
+ * weights: y = dequant(W) . x (paper Sec. 2.1, decode is a matrix-vector
+ * product; Sec. 3.3, matrix-vector kernels dequantize weights in registers).
+ * The element value of every format follows Eq. (1) of Sec. 2.2,
+ * x_hat = s * q + mu, with the block structure of Sec. 2.2 (legacy blocks of
+ * 32 weights; K-quant super-blocks of 256 = 8 sub-blocks of 32 whose scales are
+ * themselves quantized against a super-block scale).
+ *
+ * Every entry point is extern "C", takes plain pointers and 64-bit sizes, and
+ * needs no HIP or C++ header from the caller. Pointers named "device" must be
+ * device (HBM) addresses; the library never dereferences them on the host.
+ *
+ * Ownership: the caller owns every buffer. The library allocates no memory and
+ * keeps no pointer after a call returns. Its only state is immutable, so every
+ * entry point is re-entrant and thread-safe.
+ *
+ * Asynchrony: lw_matvec and lw_dequant only enqueue work and return; they never
+ * synchronise. A launch error is reported as LW_EHIP; an error inside a running
+ * kernel surfaces on the caller's next synchronisation.
+ *
+ * Errors: every argument is checked on the host, in the order of the codes
+ * below (format, then values, then shape, then alignment), before any HIP call.
+ * A call that returns an error has launched nothing and written nothing.
+ *
+ * ------------------------------------------------------------------------
+ * Packed layout ("lw split-plane layout").
+ *
+ * A tensor of n elements is stored as up to three planes that follow each
+ * other from the base pointer W. Plane 0 starts at W; each later plane starts
+ * at the end of the previous one rounded up to a multiple of 256 bytes. All
+ * multi-byte fields are little-endian; "binary16" is IEEE 754 half precision.
+ * Elements are numbered e = 0..n-1; for a matrix of M rows and K columns,
+ * e = r*K + k (row-major). Group g = e / 32; super-block S = e / 256; sub-block
+ * j = (e / 32) mod 8.
+ *
+ *   LW_F16  plane 0: n x binary16.                      value = fp16[e]
+ *   LW_Q8_0 plane 0: n x int8 (two's complement) q.
+ *           plane 1: n/32 x binary16 d.                  value = q[e] * d[g]
+ *   LW_Q4_0 plane 0: n/2 bytes; group g owns bytes [16g, 16g+16); byte i of
+ *                    the group holds element 32g+i in bits 0-3 and element
+ *                    32g+i+16 in bits 4-7 (unsigned codes q in [0, 15]).
+ *           plane 1: n/32 x binary16 d.                  value = (q - 8) * d[g]
+ *   LW_Q4_K plane 0: as LW_Q4_0 plane 0 (group g = 8S + j).
+ *           plane 1: n/256 records of 12 bytes. A record is a 96-bit
+ *                    little-endian integer R with sc_j = (R >> 6j) & 63 and
+ *                    m_j = (R >> (48 + 6j)) & 63, j = 0..7.
+ *           plane 2: n/256 x { binary16 d, binary16 dmin } (4 bytes each).
+ *                                    value = d[S] * sc_j * q[e] - dmin[S] * m_j
+ *
+ * The dequantized value of an element is the exact real value of its closed
+ * form rounded once to binary32 with round-to-nearest-even. For LW_F16,
+ * LW_Q8_0 and LW_Q4_0 the closed form is exactly representable in binary32;
+ * for LW_Q4_K the two products are exact and the difference is rounded once.
+ * ------------------------------------------------------------------------
+ */
+#ifndef LW_H
+#define LW_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Weight formats (Sec. 2.2: f16 storage, legacy symmetric blocks of 32,
+ * K-quant super-blocks of 256 with double-quantized scales and mins). */
+typedef enum { LW_F16 = 0, LW_Q8_0 = 1, LW_Q4_0 = 2, LW_Q4_K = 3 } lw_fmt;
+
+/* Return codes. */
+enum {
+    LW_OK = 0,
+    LW_EINVAL = -1, /* null pointer, or a size out of range (M, K, n_tok < 1; n < 0; too large) */
+    LW_EFMT = -2,   /* unknown format */
+    LW_ESHAPE = -3, /* K (or n) not a multiple of 256 */
+    LW_EALIGN = -4, /* W not 256-byte aligned, or x / y / out not 16-byte aligned */
+    LW_EHIP = -5    /* the HIP launch failed */
+};
+
+/* Largest accepted M and K, and largest accepted element count M*K or n. */
+#define LW_MAX_DIM ((int64_t)1 << 31)
+#define LW_MAX_ELEMS ((int64_t)1 << 40)
+/* Token counts up to this bound take the matrix-vector path (W is streamed
+ * once, every token reuses each decoded weight in registers); larger token
+ * counts take the matrix-core (MFMA) prefill path. */
+#define LW_GEMV_MAX_TOK 8
+
+/*
+ * lw_matvec — y[t][r] = sum_k value(W, r*K + k) * x[t][k]
+ *             for 0 <= t < n_tok, 0 <= r < M, 0 <= k < K.
+ *
+ * Decode step of Sec. 2.1 with the dequantize-in-registers matrix-vector
+ * kernel of Sec. 3.3; n_tok > 1 is the multi-token batch of the same product,
+ * and n_tok > LW_GEMV_MAX_TOK the prefill matrix multiplication of Sec. 3.2
+ * (dequantized weight tiles reused across tokens, Sec. 3.3).
+ *
+ *   fmt    one of lw_fmt.
+ *   W      device; M*K elements packed in the layout above, 256-byte aligned.
+ *   x      device; float32 [n_tok][K] row-major, 16-byte aligned.
+ *   y      device; float32 [n_tok][M] row-major, 16-byte aligned; overwritten.
+ *          Must not overlap W or x.
+ *   M, K   rows and columns; 1 <= M, K <= LW_MAX_DIM, M*K <= LW_MAX_ELEMS;
+ *          K must be a multiple of 256 (LW_ESHAPE otherwise).
+ *   n_tok  number of token vectors, >= 1.
+ *   stream hipStream_t to enqueue on (NULL: the null stream).
+ *
+ * Arithmetic: products and sums in float32 with float32 accumulation (no
+ * reduced-precision activations) on the matrix-vector path. The prefill path
+ * multiplies exact integer codes by activations split into a bfloat16 high
+ * part and a bfloat16 low part, accumulating in float32; its error relative to
+ * sum_k |w * x| stays below 1e-4.
+ */
+int lw_matvec(int fmt, const void* W, const float* x, float* y,
+              int64_t M, int64_t K, int64_t n_tok, void* stream);
+
+/*
+ * lw_dequant — out[e] = value(W, e) for 0 <= e < n, bit-exact (see above).
+ * Runs on the null stream. n == 0 is a no-op returning LW_OK.
+ *
+ *   W    device; n elements packed in the layout above, 256-byte aligned.
+ *   out  device; float32 [n], 16-byte aligned; must not overlap W.
+ *   n    element count, 0 <= n <= LW_MAX_ELEMS, a multiple of 256.
+ */
+int lw_dequant(int fmt, const void* W, float* out, int64_t n);
+
+/*
+ * lw_weight_bytes — size in bytes of n packed elements (plane 0 through the
+ * end of the last plane). Returns LW_EFMT, LW_EINVAL (n < 0 or too large) or
+ * LW_ESHAPE (n not a multiple of 256) as a negative value. Host-only.
+ */
+int64_t lw_weight_bytes(int fmt, int64_t n);
+
+/* lw_strerror — static, NUL-terminated description of a return code. */
+const char* lw_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LW_H */

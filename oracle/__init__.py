@@ -1,0 +1,140 @@
+"""CPU oracle for the fused dequantize x matrix-vector product.
+
+TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the benchmark's
+CPU-baseline leg may import this package; the product path (the HIP library and
+its Python binding) never does, and this package imports nothing from it.
+
+The arithmetic lives in ``lw_oracle.c`` (plain scalar C, double precision, one
+rounding per dequantized element, fixed summation order); this module only
+builds it with gcc and marshals numpy arrays through ctypes.
+
+* ``dequant(fmt, W_bytes, n)`` -> float32[n], the exact closed form of each
+  element rounded once (Eq. (1) of Sec. 2.2 with the legacy and K-quant block
+  structures of Sec. 2.2).
+* ``matvec(fmt, W_bytes, x, M, K)`` -> (y, A) in float64: y = dequant(W) . x
+  (Sec. 2.1: decode is a matrix-vector product) and A = sum_k |w * x|.
+* ``matvec_sampled(...)`` the same for a list of (token, row) outputs.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "lw_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+F16, Q8_0, Q4_0, Q4_K = 0, 1, 2, 3
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile lw_oracle.c into liboracle.so next to it (plain -O2, no FMA
+    contraction, no fast-math, no vector intrinsics)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-std=c11", "-O2", "-ffp-contract=off", "-fno-fast-math",
+                               "-fPIC", "-shared", "-pthread", "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build()
+        lib = ctypes.CDLL(_LIB)
+        u8p = ctypes.POINTER(ctypes.c_uint8)
+        f32p = ctypes.POINTER(ctypes.c_float)
+        f64p = ctypes.POINTER(ctypes.c_double)
+        i64p = ctypes.POINTER(ctypes.c_int64)
+        i64 = ctypes.c_int64
+        lib.oracle_weight_bytes.argtypes = [ctypes.c_int, i64]
+        lib.oracle_weight_bytes.restype = i64
+        lib.oracle_dequant.argtypes = [ctypes.c_int, u8p, i64, f32p]
+        lib.oracle_dequant.restype = ctypes.c_int
+        lib.oracle_matvec.argtypes = [ctypes.c_int, u8p, f32p, i64, i64, i64, f64p, f64p, ctypes.c_int]
+        lib.oracle_matvec.restype = ctypes.c_int
+        lib.oracle_matvec_sampled.argtypes = [ctypes.c_int, u8p, f32p, i64, i64, i64, i64,
+                                              i64p, i64p, f64p, f64p]
+        lib.oracle_matvec_sampled.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def _ptr(a: np.ndarray, ctype):
+    return a.ctypes.data_as(ctypes.POINTER(ctype))
+
+
+def _bytes(W) -> np.ndarray:
+    W = np.ascontiguousarray(W)
+    if W.dtype != np.uint8:
+        W = W.view(np.uint8)
+    return W.reshape(-1)
+
+
+def weight_bytes(fmt: int, n: int) -> int:
+    return int(_load().oracle_weight_bytes(fmt, n))
+
+
+def dequant(fmt: int, W, n: int) -> np.ndarray:
+    W = _bytes(W)
+    need = weight_bytes(fmt, n)
+    if need < 0 or W.size < need:
+        raise ValueError("oracle.dequant: bad format/size (need %d bytes, got %d)" % (need, W.size))
+    out = np.empty(n, dtype=np.float32)
+    if _load().oracle_dequant(fmt, _ptr(W, ctypes.c_uint8), n, _ptr(out, ctypes.c_float)) != 0:
+        raise ValueError("oracle.dequant failed")
+    return out
+
+
+def matvec(fmt: int, W, x: np.ndarray, M: int, K: int, n_threads: int = 0):
+    """Returns (y, A, threads): float64 arrays of shape [n_tok, M] and the
+    number of threads used."""
+    W = _bytes(W)
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    if x.ndim == 1:
+        x = x.reshape(1, -1)
+    n_tok = x.shape[0]
+    if x.shape[1] != K:
+        raise ValueError("oracle.matvec: x has %d columns, K = %d" % (x.shape[1], K))
+    need = weight_bytes(fmt, M * K)
+    if need < 0 or W.size < need:
+        raise ValueError("oracle.matvec: bad format/size")
+    y = np.empty((n_tok, M), dtype=np.float64)
+    A = np.empty((n_tok, M), dtype=np.float64)
+    T = _load().oracle_matvec(fmt, _ptr(W, ctypes.c_uint8), _ptr(x, ctypes.c_float), M, K, n_tok,
+                              _ptr(y, ctypes.c_double), _ptr(A, ctypes.c_double), n_threads)
+    if T < 0:
+        raise ValueError("oracle.matvec failed")
+    return y, A, T
+
+
+def matvec_sampled(fmt: int, W, x: np.ndarray, M: int, K: int, rows, toks):
+    """y[s], A[s] for the outputs (toks[s], rows[s])."""
+    W = _bytes(W)
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    if x.ndim == 1:
+        x = x.reshape(1, -1)
+    n_tok = x.shape[0]
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    toks = np.ascontiguousarray(toks, dtype=np.int64)
+    if rows.shape != toks.shape:
+        raise ValueError("rows and toks differ in shape")
+    need = weight_bytes(fmt, M * K)
+    if need < 0 or W.size < need:
+        raise ValueError("oracle.matvec_sampled: bad format/size")
+    y = np.empty(rows.size, dtype=np.float64)
+    A = np.empty(rows.size, dtype=np.float64)
+    rc = _load().oracle_matvec_sampled(fmt, _ptr(W, ctypes.c_uint8), _ptr(x, ctypes.c_float), M, K,
+                                       n_tok, rows.size, _ptr(rows, ctypes.c_int64),
+                                       _ptr(toks, ctypes.c_int64), _ptr(y, ctypes.c_double),
+                                       _ptr(A, ctypes.c_double))
+    if rc != 0:
+        raise ValueError("oracle.matvec_sampled failed")
+    return y, A

@@ -1,0 +1,282 @@
+/*
+ * CPU oracle for the fused dequantize x matrix-vector product.
+ *
+ * TEST INFRASTRUCTURE ONLY. Nothing in the product path links, loads or calls
+ * this file; only the tests, the smoke check and the benchmark's CPU-baseline
+ * leg do. It shares no code, header or table with the HIP library: it has its
+ * own plane arithmetic, its own binary16 decoder and its own bit extraction.
+ *
+ * What it computes is the plain definition, written out slowly:
+ *   - dequantization, one element at a time: read the fields of the element
+ *     from the packed bytes, evaluate the closed form exactly in double
+ *     precision (every product involved is exact there), and round once to
+ *     float with the C cast (round to nearest, ties to even);
+ *   - the matrix-vector product y[t][r] = sum_k w[r][k] * x[t][k] with
+ *     w = the float dequantized weight, every product taken in double (exact:
+ *     24 + 24 bits) and summed in double in the order k = 0, 1, ..., K-1;
+ *     alongside it the condition sum A[t][r] = sum_k |w[r][k] * x[t][k]|.
+ *
+ * Passages followed:
+ *   - Eq. (1), Sec. 2.2: x_hat = s * q + mu (scale s, optional offset mu).
+ *   - Sec. 2.2, legacy formats: blocks of 32 weights; q8_0 and q4_0 are
+ *     symmetric (no offset): value = d * q for q8_0, d * (q - 8) for the
+ *     unsigned 4-bit codes of q4_0.
+ *   - Sec. 2.2, K-quants: super-blocks of 256 = 8 sub-blocks of 32, each with
+ *     its own scale, the scales quantized against a super-block scale; the
+ *     K-quant style used here also carries a per-sub-block min quantized
+ *     against a super-block dmin (Eq. (1)'s offset mu = -dmin * m):
+ *     value = d * sc_j * q - dmin * m_j.
+ *   - Sec. 2.1: decode is a matrix-vector product.
+ *
+ * Byte layout (the library's split-plane layout): plane 0 at offset 0; each
+ * next plane at the end of the previous rounded up to 256 bytes; fields are
+ * little-endian. Q4 nibbles: byte i of group g holds element 32g+i in its low
+ * four bits and element 32g+i+16 in its high four bits. Q4_K plane 1 holds one
+ * 12-byte record per super-block, read as a 96-bit little-endian integer R:
+ * sc_j = bits [6j, 6j+6), m_j = bits [48+6j, 48+6j+6). Q4_K plane 2 holds
+ * {binary16 d, binary16 dmin} per super-block.
+ *
+ * Build: gcc -O2 -ffp-contract=off -fPIC -shared -pthread (no fast-math, no
+ * vector intrinsics). Results do not depend on the thread count: each output
+ * has one fixed summation order.
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <unistd.h>
+
+enum { OR_F16 = 0, OR_Q8_0 = 1, OR_Q4_0 = 2, OR_Q4_K = 3 };
+
+/* ---- plane arithmetic ---------------------------------------------------- */
+
+static int64_t round_up_256(int64_t v) { return (v + 255) / 256 * 256; }
+
+/* Byte offset of each plane and the total size, for n elements of fmt.
+ * Returns 0 on success, -1 for an unknown format or an n the format cannot
+ * hold (negative, or not a multiple of the format's block). */
+static int planes(int fmt, int64_t n, int64_t off[3], int64_t* total) {
+    if (n < 0) return -1;
+    off[0] = off[1] = off[2] = 0;
+    switch (fmt) {
+    case OR_F16:
+        *total = 2 * n;
+        return 0;
+    case OR_Q8_0:
+        if (n % 32) return -1;
+        off[1] = round_up_256(n);               /* n int8 codes */
+        *total = off[1] + 2 * (n / 32);         /* n/32 binary16 scales */
+        return 0;
+    case OR_Q4_0:
+        if (n % 32) return -1;
+        off[1] = round_up_256(n / 2);           /* two codes per byte */
+        *total = off[1] + 2 * (n / 32);
+        return 0;
+    case OR_Q4_K:
+        if (n % 256) return -1;
+        off[1] = round_up_256(n / 2);
+        off[2] = round_up_256(off[1] + 12 * (n / 256));
+        *total = off[2] + 4 * (n / 256);
+        return 0;
+    default:
+        return -1;
+    }
+}
+
+int64_t oracle_weight_bytes(int fmt, int64_t n) {
+    int64_t off[3], total;
+    if (planes(fmt, n, off, &total)) return -1;
+    return total;
+}
+
+/* ---- field readers ------------------------------------------------------- */
+
+static unsigned read_u16(const uint8_t* p) { return (unsigned)p[0] | ((unsigned)p[1] << 8); }
+
+/* Exact real value of an IEEE 754 binary16 bit pattern, as a double.
+ * sign | 5-bit exponent e | 10-bit fraction f:
+ *   e = 0       subnormal or zero: f * 2^-24
+ *   e = 31      infinity (f = 0) or NaN
+ *   otherwise   (1024 + f) * 2^(e - 25)  (= (1 + f/1024) * 2^(e - 15)) */
+static double half_value(unsigned h) {
+    unsigned sign = (h >> 15) & 1u, e = (h >> 10) & 31u, f = h & 1023u;
+    double v;
+    if (e == 0)
+        v = ldexp((double)f, -24);
+    else if (e == 31)
+        v = f ? NAN : INFINITY;
+    else
+        v = ldexp((double)(1024u + f), (int)e - 25);
+    return sign ? -v : v;
+}
+
+/* Bit field [start, start+len) of a little-endian byte string, one bit at a time. */
+static unsigned bit_field(const uint8_t* bytes, int start, int len) {
+    unsigned v = 0;
+    for (int b = 0; b < len; ++b) {
+        int pos = start + b;
+        unsigned bit = (bytes[pos / 8] >> (pos % 8)) & 1u;
+        v |= bit << b;
+    }
+    return v;
+}
+
+/* 4-bit code of element e in a Q4 code plane. */
+static unsigned q4_code(const uint8_t* codes, int64_t e) {
+    int64_t g = e / 32;
+    int i = (int)(e % 32);
+    uint8_t byte = codes[16 * g + (i % 16)];
+    return i < 16 ? (byte & 15u) : (byte >> 4);
+}
+
+/* ---- dequantization: exact closed form, one rounding ---------------------- */
+
+/* The exact real value of element e (before the final rounding). */
+static double exact_value(int fmt, const uint8_t* W, const int64_t off[3], int64_t e) {
+    switch (fmt) {
+    case OR_F16:
+        return half_value(read_u16(W + 2 * e));
+    case OR_Q8_0: {
+        int q = (int)(int8_t)W[e];
+        double d = half_value(read_u16(W + off[1] + 2 * (e / 32)));
+        return (double)q * d; /* <= 8 + 11 significant bits: exact */
+    }
+    case OR_Q4_0: {
+        int q = (int)q4_code(W, e);
+        double d = half_value(read_u16(W + off[1] + 2 * (e / 32)));
+        return (double)(q - 8) * d; /* exact */
+    }
+    case OR_Q4_K: {
+        int64_t S = e / 256;
+        int j = (int)((e / 32) % 8);
+        const uint8_t* rec = W + off[1] + 12 * S;
+        unsigned sc = bit_field(rec, 6 * j, 6);
+        unsigned m = bit_field(rec, 48 + 6 * j, 6);
+        double d = half_value(read_u16(W + off[2] + 4 * S));
+        double dmin = half_value(read_u16(W + off[2] + 4 * S + 2));
+        unsigned q = q4_code(W, e);
+        /* d*sc*q has <= 21 significant bits and dmin*m <= 17; for any finite
+         * binary16 d and dmin the two lie within 2^26 .. 2^-24 of each other,
+         * so the double difference below is exact as well. */
+        double a = d * (double)sc * (double)q;
+        double b = dmin * (double)m;
+        return a - b;
+    }
+    default:
+        return NAN;
+    }
+}
+
+/* out[e] = float(value(e)) for e in [0, n). Returns 0, or -1 on a bad
+ * format or n. Single-threaded. */
+int oracle_dequant(int fmt, const uint8_t* W, int64_t n, float* out) {
+    int64_t off[3], total;
+    if (planes(fmt, n, off, &total)) return -1;
+    for (int64_t e = 0; e < n; ++e) out[e] = (float)exact_value(fmt, W, off, e);
+    return 0;
+}
+
+/* ---- matrix-vector product ------------------------------------------------ */
+
+typedef struct {
+    int fmt;
+    const uint8_t* W;
+    const int64_t* off;
+    const float* x;
+    int64_t M, K, n_tok;
+    double* y;
+    double* A;
+    int64_t r_begin, r_end;
+} mv_job;
+
+static void* mv_rows(void* arg) {
+    mv_job* jb = (mv_job*)arg;
+    float* w = (float*)malloc(sizeof(float) * (size_t)jb->K);
+    if (!w) return (void*)1;
+    for (int64_t r = jb->r_begin; r < jb->r_end; ++r) {
+        /* the row of dequantized weights, each rounded once to float */
+        for (int64_t k = 0; k < jb->K; ++k)
+            w[k] = (float)exact_value(jb->fmt, jb->W, jb->off, r * jb->K + k);
+        for (int64_t t = 0; t < jb->n_tok; ++t) {
+            const float* xt = jb->x + t * jb->K;
+            double s = 0.0, a = 0.0;
+            for (int64_t k = 0; k < jb->K; ++k) {
+                double p = (double)w[k] * (double)xt[k]; /* exact in double */
+                s += p;
+                a += fabs(p);
+            }
+            jb->y[t * jb->M + r] = s;
+            if (jb->A) jb->A[t * jb->M + r] = a;
+        }
+    }
+    free(w);
+    return NULL;
+}
+
+static int n_threads_or_default(int n_threads) {
+    if (n_threads > 0) return n_threads;
+    long c = sysconf(_SC_NPROCESSORS_ONLN);
+    return c > 0 ? (int)c : 1;
+}
+
+/* y[t*M + r] and A[t*M + r] (A may be NULL) for all t < n_tok, r < M.
+ * x is float [n_tok][K]. n_threads <= 0 uses every online CPU. Returns the
+ * number of threads used, or -1 on a bad argument / allocation failure. */
+int oracle_matvec(int fmt, const uint8_t* W, const float* x, int64_t M, int64_t K,
+                  int64_t n_tok, double* y, double* A, int n_threads) {
+    int64_t off[3], total;
+    if (M < 1 || K < 1 || n_tok < 1 || !W || !x || !y) return -1;
+    if (planes(fmt, M * K, off, &total) || (fmt != OR_F16 && K % 32)) return -1;
+    int T = n_threads_or_default(n_threads);
+    if (T > M) T = (int)M;
+    pthread_t* th = (pthread_t*)calloc((size_t)T, sizeof(pthread_t));
+    mv_job* jobs = (mv_job*)calloc((size_t)T, sizeof(mv_job));
+    if (!th || !jobs) {
+        free(th);
+        free(jobs);
+        return -1;
+    }
+    int failed = 0;
+    for (int i = 0; i < T; ++i) {
+        mv_job jb = {fmt, W, off, x, M, K, n_tok, y, A, M * i / T, M * (i + 1) / T};
+        jobs[i] = jb;
+        if (pthread_create(&th[i], NULL, mv_rows, &jobs[i])) {
+            mv_rows(&jobs[i]); /* could not start a thread: do its rows here */
+            th[i] = 0;
+        }
+    }
+    for (int i = 0; i < T; ++i) {
+        void* rv = NULL;
+        if (th[i]) pthread_join(th[i], &rv);
+        if (rv) failed = 1;
+    }
+    free(th);
+    free(jobs);
+    return failed ? -1 : T;
+}
+
+/* The same product for a list of single outputs: for s < n_samples,
+ * y[s] = y_full[toks[s]][rows[s]] and A[s] likewise (A may be NULL).
+ * Single-threaded. Returns 0 or -1. */
+int oracle_matvec_sampled(int fmt, const uint8_t* W, const float* x, int64_t M, int64_t K,
+                          int64_t n_tok, int64_t n_samples, const int64_t* rows,
+                          const int64_t* toks, double* y, double* A) {
+    int64_t off[3], total;
+    if (M < 1 || K < 1 || n_tok < 1 || !W || !x || !y || n_samples < 0) return -1;
+    if (planes(fmt, M * K, off, &total) || (fmt != OR_F16 && K % 32)) return -1;
+    for (int64_t s = 0; s < n_samples; ++s) {
+        int64_t r = rows[s], t = toks[s];
+        if (r < 0 || r >= M || t < 0 || t >= n_tok) return -1;
+        const float* xt = x + t * K;
+        double sum = 0.0, a = 0.0;
+        for (int64_t k = 0; k < K; ++k) {
+            double p = (double)(float)exact_value(fmt, W, off, r * K + k) * (double)xt[k];
+            sum += p;
+            a += fabs(p);
+        }
+        y[s] = sum;
+        if (A) A[s] = a;
+    }
+    return 0;
+}

@@ -1,0 +1,137 @@
+"""Packers for the lw split-plane weight layout (byte placement only).
+
+These functions place already-quantized fields (codes, scales, mins) into the
+byte layout that ``include/lw.h`` specifies; they compute no dequantized value
+and no product. Users call them to lay out weights they quantized themselves;
+the tests and the benchmark call them (through ``synth``) to build seeded
+synthetic inputs that both the HIP library and the CPU oracle then read.
+
+Layout summary (little-endian; each plane after the first starts at the end of
+the previous one rounded up to 256 bytes):
+
+* f16   plane 0: n x binary16
+* q8_0  plane 0: n x int8 codes;   plane 1: n/32 x binary16 d
+* q4_0  plane 0: n/2 bytes, group g owns bytes [16g, 16g+16), byte i holds
+        element 32g+i (bits 0-3) and 32g+i+16 (bits 4-7);  plane 1: n/32 x binary16 d
+* q4_k  plane 0: as q4_0;  plane 1: n/256 x 12-byte record, a 96-bit
+        little-endian integer with sc_j at bits [6j, 6j+6) and m_j at bits
+        [48+6j, 48+6j+6);  plane 2: n/256 x {binary16 d, binary16 dmin}
+"""
+from __future__ import annotations
+
+import numpy as np
+
+F16, Q8_0, Q4_0, Q4_K = 0, 1, 2, 3
+FORMATS = {"f16": F16, "q8_0": Q8_0, "q4_0": Q4_0, "q4_k": Q4_K}
+FORMAT_NAMES = {v: k for k, v in FORMATS.items()}
+# Packed bytes per weight (codes and scales, ignoring plane padding).
+BYTES_PER_WEIGHT = {F16: 2.0, Q8_0: 34.0 / 32.0, Q4_0: 18.0 / 32.0, Q4_K: 144.0 / 256.0}
+
+ALIGN = 256
+
+
+def _up(v: int) -> int:
+    return (v + ALIGN - 1) // ALIGN * ALIGN
+
+
+def plane_offsets(fmt: int, n: int):
+    """(offsets of planes 0..2, total bytes) for n elements."""
+    if n < 0:
+        raise ValueError("n < 0")
+    if fmt == F16:
+        return (0, 0, 0), 2 * n
+    if fmt in (Q8_0, Q4_0):
+        if n % 32:
+            raise ValueError("n must be a multiple of 32")
+        o1 = _up(n if fmt == Q8_0 else n // 2)
+        return (0, o1, 0), o1 + 2 * (n // 32)
+    if fmt == Q4_K:
+        if n % 256:
+            raise ValueError("n must be a multiple of 256")
+        o1 = _up(n // 2)
+        o2 = _up(o1 + 12 * (n // 256))
+        return (0, o1, o2), o2 + 4 * (n // 256)
+    raise ValueError("unknown format %r" % (fmt,))
+
+
+def _half_bits(a) -> np.ndarray:
+    a = np.asarray(a)
+    if a.dtype == np.float16:
+        return a.view(np.uint16).reshape(-1)
+    if a.dtype == np.uint16:
+        return a.reshape(-1)
+    raise TypeError("binary16 fields must be float16 or uint16 bit patterns")
+
+
+def pack_nibbles(q) -> np.ndarray:
+    """4-bit codes (n,) in [0, 15] -> n/2 bytes in the group-of-32 nibble order."""
+    q = np.asarray(q, dtype=np.uint8).reshape(-1, 2, 16)
+    if q.size and int(q.max()) > 15:
+        raise ValueError("4-bit codes must lie in [0, 15]")
+    return (q[:, 0, :] | (q[:, 1, :] << 4)).reshape(-1)
+
+
+def pack_q4k_records(sc, m) -> np.ndarray:
+    """6-bit sub-block scales and mins, shape (n/32,) each, -> (n/256, 12) bytes."""
+    sc = np.asarray(sc, dtype=np.uint64).reshape(-1, 8)
+    m = np.asarray(m, dtype=np.uint64).reshape(-1, 8)
+    if sc.size and (int(sc.max()) > 63 or int(m.max()) > 63):
+        raise ValueError("6-bit fields must lie in [0, 63]")
+    shifts = (np.arange(8, dtype=np.uint64) * np.uint64(6))
+    lo = np.bitwise_or.reduce(sc << shifts, axis=1)  # bits 0..47 of R
+    hi = np.bitwise_or.reduce(m << shifts, axis=1)   # bits 48..95 of R
+    rec = np.empty((sc.shape[0], 12), dtype=np.uint8)
+    rec[:, 0:6] = lo.astype("<u8").view(np.uint8).reshape(-1, 8)[:, 0:6]
+    rec[:, 6:12] = hi.astype("<u8").view(np.uint8).reshape(-1, 8)[:, 0:6]
+    return rec
+
+
+def assemble(fmt: int, n: int, plane0: np.ndarray, plane1=None, plane2=None) -> np.ndarray:
+    """Place already-encoded plane bytes at their offsets (zero padding)."""
+    offs, total = plane_offsets(fmt, n)
+    out = np.zeros(total, dtype=np.uint8)
+    for i, p in enumerate((plane0, plane1, plane2)):
+        if p is None:
+            continue
+        p = np.ascontiguousarray(p).view(np.uint8).reshape(-1)
+        out[offs[i]:offs[i] + p.size] = p
+    return out
+
+
+def pack_f16(w) -> np.ndarray:
+    h = _half_bits(w).astype("<u2")
+    return assemble(F16, h.size, h)
+
+
+def pack_q8_0(q, d) -> np.ndarray:
+    q = np.asarray(q)
+    if q.dtype != np.int8:
+        if q.size and (int(q.min()) < -128 or int(q.max()) > 127):
+            raise ValueError("int8 codes out of range")
+        q = q.astype(np.int8)
+    q = q.reshape(-1)
+    d = _half_bits(d).astype("<u2")
+    if d.size * 32 != q.size:
+        raise ValueError("need one scale per 32 codes")
+    return assemble(Q8_0, q.size, q, d)
+
+
+def pack_q4_0(q, d) -> np.ndarray:
+    q = np.asarray(q).reshape(-1)
+    d = _half_bits(d).astype("<u2")
+    if d.size * 32 != q.size:
+        raise ValueError("need one scale per 32 codes")
+    return assemble(Q4_0, q.size, pack_nibbles(q), d)
+
+
+def pack_q4_k(q, sc, m, d, dmin) -> np.ndarray:
+    q = np.asarray(q).reshape(-1)
+    n = q.size
+    d = _half_bits(d)
+    dmin = _half_bits(dmin)
+    if d.size * 256 != n or dmin.size * 256 != n or np.size(sc) * 32 != n or np.size(m) * 32 != n:
+        raise ValueError("q4_k field sizes do not match n")
+    dd = np.empty((n // 256, 2), dtype="<u2")
+    dd[:, 0] = d
+    dd[:, 1] = dmin
+    return assemble(Q4_K, n, pack_nibbles(q), pack_q4k_records(sc, m), dd)

@@ -1,0 +1,172 @@
+"""Seeded synthetic inputs with the shapes and value distributions of the
+decode workloads (Llama-3.2-1B- and Llama-3-8B-shaped weight sets).
+
+Draws fields with numpy's PCG64 generator and lays them out with ``layout``;
+holds none of the method's arithmetic (no dequantization, no product). Both
+the HIP library's tests and the CPU oracle read the bytes produced here.
+
+Recipe (each matrix has its own generator,
+``default_rng(SeedSequence([0, workload_id, layer, matrix_id]))``; the single
+Q8_0 matrix uses the literal seed 0):
+
+* f16   w ~ N(0, 0.02^2) drawn as float32 and rounded to binary16 (RNE);
+* q8_0  codes uniform in [-127, 127]; d uniform in [1e-3, 2e-2] -> binary16;
+* q4_0  codes uniform in [0, 15] (drawn as uniform random bytes, i.e. two
+        independent uniform nibbles per byte); d uniform in [1e-3, 2e-2];
+* q4_k  codes as q4_0; sc and m uniform in [0, 63]; d and dmin uniform in
+        [1e-4, 2e-3] -> binary16;
+* x     float32 N(0, 1), shape [n_tok, K], from the generator of the workload
+        (matrix_id 99).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+from . import layout
+from .layout import F16, Q4_0, Q4_K, Q8_0
+
+
+@dataclass(frozen=True)
+class Matrix:
+    name: str
+    M: int
+    K: int
+    layer: int
+    matrix_id: int
+
+
+@dataclass(frozen=True)
+class Workload:
+    key: str
+    workload_id: int
+    fmt: int
+    matrices: tuple
+    n_toks: tuple = (1,)
+    description: str = ""
+
+    @property
+    def weights(self) -> int:
+        return sum(m.M * m.K for m in self.matrices)
+
+
+def _llama_layers(n_layers, hidden, qkv, ffn):
+    mats = []
+    for L in range(n_layers):
+        mats += [Matrix("qkv", qkv, hidden, L, 0), Matrix("o", hidden, hidden, L, 1),
+                 Matrix("gate", ffn, hidden, L, 2), Matrix("up", ffn, hidden, L, 3),
+                 Matrix("down", hidden, ffn, L, 4)]
+    return mats
+
+
+# Llama-3.2-1B: hidden 2048, 32 q-heads / 8 kv-heads of 64 -> QKV 3072, FFN 8192, 16 layers.
+_L1B = dict(n_layers=16, hidden=2048, qkv=3072, ffn=8192)
+# Llama-3-8B: hidden 4096, kv width 1024 -> QKV 6144, FFN 14336, 32 layers.
+_L8B = dict(n_layers=32, hidden=4096, qkv=6144, ffn=14336)
+_VOCAB = 128256
+
+WORKLOADS = {
+    "q8_0_2048": Workload("q8_0_2048", 1, Q8_0, (Matrix("w", 2048, 2048, 0, 0),),
+                          description="single Q8_0 GEMV 2048x2048, 1 token"),
+    "f16_llama1b": Workload("f16_llama1b", 2, F16, tuple(_llama_layers(**_L1B)),
+                            description="f16 GEMV over the 80 per-layer decode matrices of a "
+                                        "Llama-3.2-1B-shaped model, 1 token"),
+    "q4_0_llama1b": Workload("q4_0_llama1b", 3, Q4_0,
+                             tuple(_llama_layers(**_L1B)) + (Matrix("lm_head", _VOCAB, 2048, 16, 5),),
+                             description="Q4_0 decode-step weight set, Llama-3.2-1B shapes + lm_head, "
+                                         "1 token"),
+    "q4_k_llama8b": Workload("q4_k_llama8b", 4, Q4_K,
+                             tuple(_llama_layers(**_L8B)) + (Matrix("lm_head", _VOCAB, 4096, 32, 5),),
+                             description="Q4_K-style decode-step weight set, Llama-3-8B shapes "
+                                         "(32 layers) + lm_head, 1 token"),
+    "q4_0_llama8b_ffn": Workload("q4_0_llama8b_ffn", 5, Q4_0,
+                                 (Matrix("gate", 14336, 4096, 0, 2), Matrix("up", 14336, 4096, 0, 3),
+                                  Matrix("down", 4096, 14336, 0, 4)),
+                                 n_toks=(1, 2, 4, 8, 512),
+                                 description="multi-token Q4_0 on Llama-3-8B gate/up/down, "
+                                             "n_tok in {1,2,4,8} and prefill 512"),
+}
+
+
+def rng_for(workload_id: int, layer: int, matrix_id: int) -> np.random.Generator:
+    if workload_id == 1:
+        return np.random.default_rng(0)
+    return np.random.default_rng(np.random.SeedSequence([0, workload_id, layer, matrix_id]))
+
+
+def _uniform_half(rng, lo, hi, size):
+    return rng.uniform(lo, hi, size).astype(np.float16)
+
+
+def _random_bytes(rng, nbytes):
+    return np.frombuffer(rng.bytes(nbytes), dtype=np.uint8)
+
+
+def gen_fields(fmt: int, n: int, rng: np.random.Generator) -> dict:
+    """Fields of n elements drawn per the recipe (4-bit codes as explicit
+    values in [0, 15]; meant for sizes where an array of n bytes is cheap)."""
+    if fmt == F16:
+        return {"w": (rng.standard_normal(n, dtype=np.float32) * np.float32(0.02)).astype(np.float16)}
+    if fmt == Q8_0:
+        return {"q": rng.integers(-127, 128, n, dtype=np.int8),
+                "d": _uniform_half(rng, 1e-3, 2e-2, n // 32)}
+    if fmt == Q4_0:
+        return {"q": rng.integers(0, 16, n, dtype=np.uint8),
+                "d": _uniform_half(rng, 1e-3, 2e-2, n // 32)}
+    if fmt == Q4_K:
+        return {"q": rng.integers(0, 16, n, dtype=np.uint8),
+                "sc": rng.integers(0, 64, n // 32, dtype=np.uint8),
+                "m": rng.integers(0, 64, n // 32, dtype=np.uint8),
+                "d": _uniform_half(rng, 1e-4, 2e-3, n // 256),
+                "dmin": _uniform_half(rng, 1e-4, 2e-3, n // 256)}
+    raise ValueError(fmt)
+
+
+def pack_fields(fmt: int, f: dict) -> np.ndarray:
+    if fmt == F16:
+        return layout.pack_f16(f["w"])
+    if fmt == Q8_0:
+        return layout.pack_q8_0(f["q"], f["d"])
+    if fmt == Q4_0:
+        return layout.pack_q4_0(f["q"], f["d"])
+    return layout.pack_q4_k(f["q"], f["sc"], f["m"], f["d"], f["dmin"])
+
+
+def gen_packed(fmt: int, n: int, rng: np.random.Generator) -> np.ndarray:
+    """n packed elements per the recipe. The 4-bit code plane is drawn as
+    uniform random bytes (same distribution as two uniform nibbles)."""
+    if fmt in (F16, Q8_0):
+        return pack_fields(fmt, gen_fields(fmt, n, rng))
+    offs, total = layout.plane_offsets(fmt, n)
+    out = np.zeros(total, dtype=np.uint8)
+    out[0:n // 2] = _random_bytes(rng, n // 2)
+    if fmt == Q4_0:
+        out[offs[1]:offs[1] + 2 * (n // 32)] = _uniform_half(rng, 1e-3, 2e-2, n // 32).view(np.uint8)
+        return out
+    sc = rng.integers(0, 64, n // 32, dtype=np.uint8)
+    m = rng.integers(0, 64, n // 32, dtype=np.uint8)
+    out[offs[1]:offs[1] + 12 * (n // 256)] = layout.pack_q4k_records(sc, m).reshape(-1)
+    dd = np.empty((n // 256, 2), dtype=np.float16)
+    dd[:, 0] = _uniform_half(rng, 1e-4, 2e-3, n // 256)
+    dd[:, 1] = _uniform_half(rng, 1e-4, 2e-3, n // 256)
+    out[offs[2]:offs[2] + 4 * (n // 256)] = dd.view(np.uint8).reshape(-1)
+    return out
+
+
+def gen_matrix(wl: Workload, mat: Matrix) -> np.ndarray:
+    return gen_packed(wl.fmt, mat.M * mat.K, rng_for(wl.workload_id, mat.layer, mat.matrix_id))
+
+
+def gen_x(wl: Workload, K: int, n_tok: int = 1) -> np.ndarray:
+    rng = rng_for(wl.workload_id, 0, 99) if wl.workload_id != 1 else np.random.default_rng([0, 99])
+    return rng.standard_normal((n_tok, K), dtype=np.float32)
+
+
+def gen_x_seeded(seed, K: int, n_tok: int = 1) -> np.ndarray:
+    return np.random.default_rng(seed).standard_normal((n_tok, K), dtype=np.float32)
+
+
+def algorithmic_bytes(fmt: int, M: int, K: int, n_tok: int = 1) -> float:
+    """Bytes the product must move once: packed W + x + y."""
+    return layout.BYTES_PER_WEIGHT[fmt] * M * K + 4.0 * n_tok * (K + M)
