@@ -1,0 +1,247 @@
+#!/usr/bin/env python3
+"""Benchmark of the fused dequantize x matrix-vector product on one MI355X.
+
+A step is one decode token's pass over every weight matrix of a workload: one
+lw_matvec per matrix, each matrix in its own HBM buffer (the 8B Q4_K-style set
+is 4.2 GB, far above the 256 MB Infinity Cache, so every step streams the
+weights from HBM). Inputs are synthetic and seeded (paper_2605_20706_amd.synth)
+and resident in HBM before the timed region starts.
+
+Printed (one JSON line): HBM GB/s from algorithmic bytes (packed W + x + y),
+its fraction of the 8 TB/s peak, the equivalent decode tokens/s, a roofline
+object for the GEMV kernel from per-launch HIP events, and the CPU oracle timed
+on a bounded sample of the same workload on this host.
+
+Usage: python bench.py [--workload q4_k_llama8b] [--steps K] [--warmup W]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+from concurrent.futures import ThreadPoolExecutor
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+from paper_2605_20706_amd import binding, layout, synth  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "dequant-GEMV HBM GB/s (% of peak) and equiv. decode tok/s, Llama-1B/8B shapes"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class Workset:
+    """All matrices of a workload on the GPU, their x and y buffers, and the
+    raw argument tuples of one lw_matvec per matrix."""
+
+    def __init__(self, wl, n_tok, keep_host=0):
+        import torch
+
+        self.wl, self.n_tok = wl, n_tok
+        self.lib = binding.library()
+        mats = list(wl.matrices)
+        t0 = time.time()
+        self.host = {}
+        self.W, self.y = [], []
+
+        def gen(i):
+            return i, synth.gen_matrix(wl, mats[i])
+
+        with ThreadPoolExecutor(8) as ex:
+            for i, Wh in ex.map(gen, range(len(mats))):
+                self.W.append(torch.from_numpy(Wh).to("cuda"))
+                if i < keep_host:
+                    self.host[i] = Wh
+        self.x = {K: torch.from_numpy(synth.gen_x(wl, K, n_tok)).to("cuda")
+                  for K in sorted({m.K for m in mats})}
+        self.xh = {K: v.cpu().numpy() for K, v in self.x.items()}
+        self.y = [torch.empty((n_tok, m.M), dtype=torch.float32, device="cuda") for m in mats]
+        torch.cuda.synchronize()
+        log("workload %s: %d matrices, %.3f GB packed, generated+uploaded in %.1fs"
+            % (wl.key, len(mats), sum(w.numel() for w in self.W) / 1e9, time.time() - t0))
+        self.mats = mats
+        self.args = [(wl.fmt, self.W[i].data_ptr(), self.x[m.K].data_ptr(), self.y[i].data_ptr(),
+                      m.M, m.K, n_tok) for i, m in enumerate(mats)]
+        self.alg_bytes = [synth.algorithmic_bytes(wl.fmt, m.M, m.K, n_tok) for m in mats]
+        self.flops = [2.0 * m.M * m.K * n_tok for m in mats]
+
+    def step(self, stream):
+        f = self.lib.lw_matvec
+        for a in self.args:
+            rc = f(*a, stream)
+            if rc != 0:
+                raise binding.LwError(rc, "lw_matvec")
+
+    def step_timed(self, stream, events):
+        f = self.lib.lw_matvec
+        for a, (e0, e1) in zip(self.args, events):
+            e0.record()
+            rc = f(*a, stream)
+            e1.record()
+            if rc != 0:
+                raise binding.LwError(rc, "lw_matvec")
+
+
+def run_gpu(ws, steps, warmup, mode):
+    import ctypes
+
+    import torch
+
+    # ---- whole-step throughput (timed region) ----
+    if mode == "graph":
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            ws.step(ctypes.c_void_p(side.cuda_stream))
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            ws.step(ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+        run = g.replay
+    else:
+        def run():
+            ws.step(ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+    for _ in range(warmup):
+        run()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        run()
+    end.record()
+    torch.cuda.synchronize()
+    ms_per_step = start.elapsed_time(end) / steps
+
+    # ---- per-launch kernel durations (eager launches bracketed by events on
+    # the launch stream; the stream is first held busy so that launches queue
+    # up back to back instead of waiting on the host) ----
+    stream = torch.cuda.current_stream()
+    n = len(ws.args)
+    reps = 3
+    durs = np.zeros((reps, n))
+    for r in range(reps):
+        events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+        torch.cuda._sleep(int(2.4e6 * 20))  # ~20 ms at 2.4 GHz
+        ws.step_timed(ctypes.c_void_p(stream.cuda_stream), events)
+        torch.cuda.synchronize()
+        durs[r] = [e0.elapsed_time(e1) for e0, e1 in events]
+    return ms_per_step, durs.mean(axis=0)
+
+
+def cpu_baseline(ws, budget_s):
+    import oracle
+
+    wl = ws.wl
+    # the host share of one GPU: OMP_NUM_THREADS when set, else at most 16 threads
+    n_threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or min(16, os.cpu_count() or 1)
+    t_used, nbytes, nweights, done = 0.0, 0, 0, []
+    threads = 0
+    for i, m in enumerate(ws.mats):
+        if i not in ws.host:
+            break
+        x = ws.xh[m.K]
+        t0 = time.perf_counter()
+        _, _, threads = oracle.matvec(wl.fmt, ws.host[i], x, m.M, m.K, n_threads=n_threads)
+        t_used += time.perf_counter() - t0
+        nbytes += synth.algorithmic_bytes(wl.fmt, m.M, m.K, ws.n_tok)
+        nweights += m.M * m.K
+        done.append("%s[%d]" % (m.name, m.layer))
+        if t_used >= budget_s:
+            break
+    gbs = nbytes / t_used / 1e9
+    tok_s = ws.n_tok * gbs * 1e9 / sum(ws.alg_bytes)
+    return {"value": round(gbs, 4), "unit": "GB/s", "cores": int(threads), "kind": "oracle",
+            "equiv_decode_tok_s": round(tok_s, 4), "seconds": round(t_used, 2),
+            "sample": "%d of %d matrices (%s), %.3g weights, same inputs; oracle = plain C, "
+                      "double accumulation, one thread per row block"
+                      % (len(done), len(ws.mats), ", ".join(done[:6]) + (" ..." if len(done) > 6 else ""),
+                         nweights)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="q4_k_llama8b", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--n-tok", type=int, default=1)
+    ap.add_argument("--mode", choices=["graph", "eager"], default="graph")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB 20 times (HBM counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (use --gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    binding.library()  # fails loudly if the HIP library is missing
+
+    if args.calibrate_copy:
+        n = args.calibrate_copy * (1 << 20)
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(20):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": n, "copies": 20}))
+        return
+
+    wl = synth.WORKLOADS[args.workload]
+    keep = 0 if args.no_cpu_baseline else len(wl.matrices)
+    ws = Workset(wl, args.n_tok, keep_host=keep)
+    ms_per_step, durs = run_gpu(ws, args.steps, args.warmup, args.mode)
+
+    step_bytes = sum(ws.alg_bytes)
+    gbs = step_bytes / (ms_per_step * 1e-3) / 1e9
+    tok_s = args.n_tok / (ms_per_step * 1e-3)
+    kern_s = durs.sum() * 1e-3
+    kern_gbs = step_bytes / kern_s / 1e9
+    fmt_name = layout.FORMAT_NAMES[wl.fmt]
+    roof = {"bound": "hbm", "achieved": round(kern_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(kern_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+            "kernel": "gemv_kernel<%s, n_tok=%d>" % (fmt_name, args.n_tok),
+            "launches_per_step": len(ws.args), "avg_launch_us": round(float(durs.mean()) * 1e3, 3),
+            "alg_bytes_per_launch": round(step_bytes / len(ws.args))}
+    per_shape = {}
+    for m, b, d in zip(ws.mats, ws.alg_bytes, durs):
+        k = "%s %dx%d" % (m.name, m.M, m.K)
+        s = per_shape.setdefault(k, [0.0, 0.0])
+        s[0] += b
+        s[1] += d * 1e-3
+    out = {
+        "metric": METRIC, "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded; shapes and value distributions of the workload)",
+        "config": {"workload": wl.key, "description": wl.description, "format": fmt_name,
+                   "matrices": len(ws.mats), "weights": wl.weights, "n_tok": args.n_tok,
+                   "bytes_per_step": round(step_bytes), "mode": args.mode},
+        "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
+        "equiv_decode_tok_s": round(tok_s, 1),
+        "roofline": roof,
+        "per_shape_kernel_gbs": {k: round(v[0] / v[1] / 1e9, 1) for k, v in per_shape.items()},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(ws, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,121 @@
+"""ctypes binding of the lw C ABI (``include/lw.h``): argument marshalling only.
+
+Every computation runs in the HIP kernels of ``liblw.so``. torch is used for
+device memory and streams: tensors pass their device pointers, and the
+current torch stream is passed to ``lw_matvec``. If the library is not built,
+or the tensors are not on a GPU, calls raise; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "liblw.so")
+
+LW_OK = 0
+EXPORTS = ("lw_matvec", "lw_dequant", "lw_weight_bytes", "lw_strerror")
+
+
+class LwError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__("%s: %s (%d)" % (where, _strerror(code), code))
+
+
+_lib = None
+
+
+def library() -> ctypes.CDLL:
+    """Load liblw.so (built in-tree by ``python -m paper_2605_20706_amd.build``)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("liblw.so is not built (%s); run python -m paper_2605_20706_amd.build"
+                               % LIB_PATH)
+        lib = ctypes.CDLL(LIB_PATH)
+        i64 = ctypes.c_int64
+        vp = ctypes.c_void_p
+        lib.lw_matvec.argtypes = [ctypes.c_int, vp, vp, vp, i64, i64, i64, vp]
+        lib.lw_matvec.restype = ctypes.c_int
+        lib.lw_dequant.argtypes = [ctypes.c_int, vp, vp, i64]
+        lib.lw_dequant.restype = ctypes.c_int
+        lib.lw_weight_bytes.argtypes = [ctypes.c_int, i64]
+        lib.lw_weight_bytes.restype = i64
+        lib.lw_strerror.argtypes = [ctypes.c_int]
+        lib.lw_strerror.restype = ctypes.c_char_p
+        _lib = lib
+    return _lib
+
+
+def raw():
+    """The ctypes functions themselves (pointers as ints), for ABI-level use."""
+    return library()
+
+
+def _strerror(code: int) -> str:
+    return library().lw_strerror(code).decode()
+
+
+def strerror(code: int) -> str:
+    return _strerror(code)
+
+
+def weight_bytes(fmt: int, n: int) -> int:
+    v = library().lw_weight_bytes(fmt, n)
+    if v < 0:
+        raise LwError(v, "lw_weight_bytes")
+    return v
+
+
+def _check_gpu(t, name):
+    if not t.is_cuda:
+        raise ValueError("%s must be a GPU tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+
+
+def matvec(fmt: int, W, x, M: int, K: int, y=None, stream=None):
+    """y[n_tok, M] = dequant(W)[M, K] @ x[n_tok, K]^T on the GPU.
+
+    W: uint8 GPU tensor with the packed weights (lw layout); x: float32 GPU
+    tensor [K] or [n_tok, K]; y: optional float32 output [n_tok, M].
+    stream: a torch.cuda.Stream (default: the current stream)."""
+    import torch
+
+    _check_gpu(W, "W")
+    _check_gpu(x, "x")
+    if x.dtype != torch.float32:
+        raise ValueError("x must be float32")
+    x2 = x.reshape(1, -1) if x.dim() == 1 else x
+    if x2.dim() != 2 or x2.shape[1] != K:
+        raise ValueError("x must be [n_tok, K] with K = %d" % K)
+    n_tok = x2.shape[0]
+    if y is None:
+        y = torch.empty((n_tok, M), dtype=torch.float32, device=x.device)
+    _check_gpu(y, "y")
+    if y.dtype != torch.float32 or y.numel() != n_tok * M:
+        raise ValueError("y must be float32 with n_tok*M elements")
+    if stream is None:
+        stream = torch.cuda.current_stream(x.device)
+    rc = library().lw_matvec(fmt, W.data_ptr(), x2.data_ptr(), y.data_ptr(), M, K, n_tok,
+                             ctypes.c_void_p(stream.cuda_stream))
+    if rc != LW_OK:
+        raise LwError(rc, "lw_matvec")
+    return y
+
+
+def dequant(fmt: int, W, n: int, out=None):
+    """float32[n] = dequant(W) on the GPU (null stream)."""
+    import torch
+
+    _check_gpu(W, "W")
+    if out is None:
+        out = torch.empty(n, dtype=torch.float32, device=W.device)
+    _check_gpu(out, "out")
+    if out.dtype != torch.float32 or out.numel() != n:
+        raise ValueError("out must be float32[n]")
+    rc = library().lw_dequant(fmt, W.data_ptr(), out.data_ptr(), n)
+    if rc != LW_OK:
+        raise LwError(rc, "lw_dequant")
+    return out

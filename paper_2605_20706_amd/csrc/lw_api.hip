@@ -1,0 +1,69 @@
+// C ABI of the lw library: argument validation and dispatch (see include/lw.h).
+//
+// Every check runs on the host before any HIP call, in the documented order
+// (format, values, shape, alignment); a call that fails a check launches
+// nothing. Dispatch picks the matrix-vector kernels for n_tok <= LW_GEMV_MAX_TOK
+// and the matrix-core prefill kernels above that.
+#include "lw_internal.hpp"
+
+namespace {
+
+bool known_fmt(int fmt) { return fmt == LW_F16 || fmt == LW_Q8_0 || fmt == LW_Q4_0 || fmt == LW_Q4_K; }
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+int64_t lw_weight_bytes(int fmt, int64_t n) {
+    if (!known_fmt(fmt)) return LW_EFMT;
+    if (n < 0 || n > LW_MAX_ELEMS) return LW_EINVAL;
+    if (n % 256) return LW_ESHAPE;
+    return lw::planes_of(fmt, n).total;
+}
+
+const char* lw_strerror(int code) {
+    switch (code) {
+    case LW_OK: return "success";
+    case LW_EINVAL: return "invalid argument: null pointer or size out of range";
+    case LW_EFMT: return "unknown weight format";
+    case LW_ESHAPE: return "shape error: K (or n) must be a multiple of 256";
+    case LW_EALIGN: return "alignment error: W must be 256-byte aligned, x/y/out 16-byte aligned";
+    case LW_EHIP: return "HIP kernel launch failed";
+    default: return "unknown error code";
+    }
+}
+
+int lw_matvec(int fmt, const void* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
+              void* stream) {
+    if (!known_fmt(fmt)) return LW_EFMT;
+    if (!W || !x || !y) return LW_EINVAL;
+    if (M < 1 || K < 1 || n_tok < 1 || M > LW_MAX_DIM || K > LW_MAX_DIM || n_tok > LW_MAX_DIM)
+        return LW_EINVAL;
+    if (M > LW_MAX_ELEMS / K || n_tok > LW_MAX_ELEMS / K || n_tok > LW_MAX_ELEMS / M) return LW_EINVAL;
+    if (K % 256) return LW_ESHAPE;
+    if (!aligned(W, 256) || !aligned(x, 16) || !aligned(y, 16)) return LW_EALIGN;
+    const lw::Planes p = lw::planes_of(fmt, M * K);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    hipError_t err;
+    if (n_tok <= LW_GEMV_MAX_TOK)
+        err = lw::launch_gemv(fmt, static_cast<const uint8_t*>(W), x, y, M, K, n_tok, p, s);
+    else
+        err = lw::launch_prefill(fmt, static_cast<const uint8_t*>(W), x, y, M, K, n_tok, p, s);
+    return err == hipSuccess ? LW_OK : LW_EHIP;
+}
+
+int lw_dequant(int fmt, const void* W, float* out, int64_t n) {
+    if (!known_fmt(fmt)) return LW_EFMT;
+    if (!W || !out) return LW_EINVAL;
+    if (n < 0 || n > LW_MAX_ELEMS) return LW_EINVAL;
+    if (n % 256) return LW_ESHAPE;
+    if (!aligned(W, 256) || !aligned(out, 16)) return LW_EALIGN;
+    if (n == 0) return LW_OK;
+    const lw::Planes p = lw::planes_of(fmt, n);
+    const hipError_t err = lw::launch_dequant(fmt, static_cast<const uint8_t*>(W), out, n, p, nullptr);
+    return err == hipSuccess ? LW_OK : LW_EHIP;
+}
+
+}  // extern "C"

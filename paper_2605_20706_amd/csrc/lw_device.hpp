@@ -1,0 +1,58 @@
+// Device-side helpers shared by the lw kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lw {
+
+constexpr int kWave = 64;
+
+// binary16 bit pattern -> float32. v_cvt_f32_f16 is exact for every pattern,
+// subnormals included (half denormals are not flushed).
+__device__ __forceinline__ float half_bits_to_float(uint32_t h16) {
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)h16);
+}
+
+// Hide the known-zero bits of a value from the optimiser. Without it, a mask
+// such as v & 0x0F0F0F0F followed by per-byte float conversion is rewritten
+// into bit-field extracts plus conversions (two operations per code); with it
+// each code is one v_cvt_f32_ubyteN.
+__device__ __forceinline__ uint32_t opaque(uint32_t v) {
+    asm("" : "+v"(v));
+    return v;
+}
+
+// Byte b (0..3) of v as float: one v_cvt_f32_ubyteN.
+template <int B>
+__device__ __forceinline__ float ubyte(uint32_t v) {
+    return (float)((v >> (8 * B)) & 0xFFu);
+}
+
+// Signed byte b of v as float.
+template <int B>
+__device__ __forceinline__ float sbyte(uint32_t v) {
+    return (float)(int32_t)(int8_t)(uint8_t)(v >> (8 * B));
+}
+
+template <int CTRL, int ROW_MASK = 0xF, int BANK_MASK = 0xF>
+__device__ __forceinline__ float dpp_move(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
+                                                                 ROW_MASK, BANK_MASK, false));
+}
+
+// Sum over the 64 lanes of a wave with DPP adds; the total lands in lane 63.
+// row_shr 1, 2, 4, 8 leaves each 16-lane row's sum in its lane 15;
+// row_bcast:15 adds row 0 into row 1 and row 2 into row 3; row_bcast:31 adds
+// the first half (lane 31) into rows 2 and 3.
+__device__ __forceinline__ float wave_sum_to_lane63(float v) {
+    v += dpp_move<0x111>(v);
+    v += dpp_move<0x112>(v);
+    v += dpp_move<0x114>(v);
+    v += dpp_move<0x118>(v);
+    v += dpp_move<0x142, 0xA>(v);
+    v += dpp_move<0x143, 0xC>(v);
+    return v;
+}
+
+}  // namespace lw

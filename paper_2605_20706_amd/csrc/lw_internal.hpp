@@ -1,0 +1,55 @@
+// Host-side declarations shared by the C-ABI layer and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "lw.h"
+
+namespace lw {
+
+// Byte offsets of planes 1 and 2 and the total size of n packed elements of
+// fmt (split-plane layout: later planes start at the end of the previous one
+// rounded up to 256 bytes). n must already be valid for fmt.
+struct Planes {
+    int64_t off1 = 0, off2 = 0, total = 0;
+};
+
+inline int64_t round_up_256(int64_t v) { return (v + 255) / 256 * 256; }
+
+inline Planes planes_of(int fmt, int64_t n) {
+    Planes p;
+    switch (fmt) {
+    case LW_F16:
+        p.total = 2 * n;
+        break;
+    case LW_Q8_0:
+        p.off1 = round_up_256(n);
+        p.total = p.off1 + 2 * (n / 32);
+        break;
+    case LW_Q4_0:
+        p.off1 = round_up_256(n / 2);
+        p.total = p.off1 + 2 * (n / 32);
+        break;
+    case LW_Q4_K:
+        p.off1 = round_up_256(n / 2);
+        p.off2 = round_up_256(p.off1 + 12 * (n / 256));
+        p.total = p.off2 + 4 * (n / 256);
+        break;
+    default:
+        break;
+    }
+    return p;
+}
+
+// Kernel launchers. Arguments are already validated; each returns the
+// hipError_t of its launch.
+hipError_t launch_dequant(int fmt, const uint8_t* W, float* out, int64_t n, const Planes& p,
+                          hipStream_t stream);
+hipError_t launch_gemv(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
+                       int64_t n_tok, const Planes& p, hipStream_t stream);
+// Matrix-core path for n_tok > LW_GEMV_MAX_TOK.
+hipError_t launch_prefill(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
+                          int64_t n_tok, const Planes& p, hipStream_t stream);
+
+}  // namespace lw

@@ -100,7 +100,9 @@ def _uniform_half(rng, lo, hi, size):
 
 
 def _random_bytes(rng, nbytes):
-    return np.frombuffer(rng.bytes(nbytes), dtype=np.uint8)
+    """Uniform random bytes: little-endian bytes of uniform 64-bit draws."""
+    words = (nbytes + 7) // 8
+    return rng.integers(0, 2 ** 64 - 1, words, dtype=np.uint64, endpoint=True).view(np.uint8)[:nbytes]
 
 
 def gen_fields(fmt: int, n: int, rng: np.random.Generator) -> dict:

@@ -1,0 +1,89 @@
+"""lw_matvec against the oracle on shapes spanning several 1 KiB chunks,
+ragged row and column tails and every token count of the matrix-vector path,
+plus token counts of the prefill path.
+
+Bar: the gate (scaled error and normwise error <= 2e-3); the matrix-vector
+path (float32 activations and accumulation) must also stay within 1e-4 of
+sum |w*x|, far below what any reduced-precision shortcut would give."""
+import numpy as np
+import pytest
+
+import gate
+from gpu_util import gpu_matvec, to_gpu
+from paper_2605_20706_amd import synth
+from paper_2605_20706_amd.layout import F16, Q4_0, Q4_K, Q8_0
+
+pytestmark = pytest.mark.gpu
+
+FMTS = [F16, Q8_0, Q4_0, Q4_K]
+# (M, K): single row; row tail below a workgroup's rows; K below one chunk;
+# K one chunk plus a ragged tail; several chunks; large K that needs x tiling.
+SHAPES = [(1, 256), (3, 768), (17, 2048), (67, 2304), (130, 4352), (33, 16640)]
+NTOKS = [1, 2, 3, 5, 8, 9, 16, 33]
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("M,K", SHAPES)
+def test_parity_small(oracle_mod, fmt, M, K):
+    W = synth.gen_packed(fmt, M * K, np.random.default_rng([fmt, M, K]))
+    x = synth.gen_x_seeded([7, fmt, M, K], K, max(NTOKS))
+    Wg = to_gpu(W)
+    y_ref, A, _ = oracle_mod.matvec(fmt, W, x, M, K)
+    for nt in NTOKS:
+        print("matvec fmt=%d M=%d K=%d n_tok=%d" % (fmt, M, K, nt), flush=True)
+        y = gpu_matvec(fmt, W, x[:nt], M, K, Wg=Wg)
+        bound = 1e-4 if nt <= 8 else None
+        gate.check(y, y_ref[:nt], A[:nt], f32_bound=bound, what=(fmt, M, K, nt))
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_one_hot_columns(oracle_mod, fmt):
+    """x = e_k returns column k of the dequantized matrix exactly (one product)."""
+    M, K = 70, 2304
+    W = synth.gen_packed(fmt, M * K, np.random.default_rng([3, fmt]))
+    Wd = oracle_mod.dequant(fmt, W, M * K).reshape(M, K)
+    ks = [0, 31, 32, 1000, 2047, 2048, 2303]
+    x = np.zeros((len(ks), K), np.float32)
+    for i, k in enumerate(ks):
+        x[i, k] = 1.0
+    y = gpu_matvec(fmt, W, x, M, K)
+    for i, k in enumerate(ks):
+        assert np.array_equal(y[i], Wd[:, k]), (fmt, k)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_zero_x_and_zero_weights(oracle_mod, fmt):
+    M, K = 20, 512
+    W = synth.gen_packed(fmt, M * K, np.random.default_rng([4, fmt]))
+    y = gpu_matvec(fmt, W, np.zeros((2, K), np.float32), M, K)
+    assert (y == 0).all()
+
+
+def test_y_is_overwritten(oracle_mod):
+    import torch
+    from paper_2605_20706_amd import binding
+    M, K = 40, 1024
+    W = synth.gen_packed(Q4_0, M * K, np.random.default_rng(5))
+    x = synth.gen_x_seeded(6, K, 2)
+    y = torch.full((2, M), float("nan"), device="cuda")
+    binding.matvec(Q4_0, to_gpu(W), to_gpu(x), M, K, y=y)
+    torch.cuda.synchronize()
+    y_ref, A, _ = oracle_mod.matvec(Q4_0, W, x, M, K)
+    gate.check(y.cpu().numpy(), y_ref, A)
+
+
+def test_stream_argument(oracle_mod):
+    """The call is enqueued on the given stream."""
+    import torch
+    from paper_2605_20706_amd import binding
+    M, K = 64, 2048
+    W = synth.gen_packed(Q4_K, M * K, np.random.default_rng(8))
+    x = synth.gen_x_seeded(9, K)
+    s = torch.cuda.Stream()
+    Wg, xg = to_gpu(W), to_gpu(x)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        y = binding.matvec(Q4_K, Wg, xg, M, K, stream=s)
+    s.synchronize()
+    y_ref, A, _ = oracle_mod.matvec(Q4_K, W, x, M, K)
+    gate.check(y.cpu().numpy(), y_ref, A)
