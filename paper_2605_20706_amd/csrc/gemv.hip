@@ -24,6 +24,8 @@
 //    with the per-group sums of x precomputed in LDS per tile.
 // Accumulation is float32 throughout; only the rounding order differs from
 // the plain definition.
+#include <atomic>
+
 #include "lw_device.hpp"
 #include "lw_internal.hpp"
 
@@ -45,6 +47,18 @@ struct Traits<LW_F16> {
     __device__ static Packet load(const uint8_t* W, int64_t e, int64_t, int64_t) {
         Packet p;
         p.c = *reinterpret_cast<const uint4*>(W + 2 * e);
+        return p;
+    }
+    // Byte offsets of row `row` in each plane, lane part included (32-bit:
+    // the kernel using them is chosen only for planes below 4 GiB), and the
+    // packet of chunk c (512 elements) at those offsets.
+    struct RowOff {
+        uint32_t c;
+    };
+    __device__ static RowOff row_off(uint32_t row, uint32_t K, int lane) { return {row * (2u * K) + 16u * lane}; }
+    __device__ static Packet load_chunk(const uint8_t* W, const uint8_t*, const uint8_t*, const RowOff& o, int c) {
+        Packet p;
+        p.c = stream_load16(W + (o.c + 1024u * c));
         return p;
     }
     __device__ static float dot(const Packet& p, const float4* xv, float, int) {
@@ -73,6 +87,19 @@ struct Traits<LW_Q8_0> {
         Packet p;
         p.c = *reinterpret_cast<const uint4*>(W + e);
         p.d = *reinterpret_cast<const uint16_t*>(W + off1 + 2 * (e >> 5));
+        return p;
+    }
+    struct RowOff {
+        uint32_t c, d;
+    };
+    __device__ static RowOff row_off(uint32_t row, uint32_t K, int lane) {
+        return {row * K + 16u * lane, row * (K / 16u) + 2u * (lane >> 1)};
+    }
+    __device__ static Packet load_chunk(const uint8_t* W, const uint8_t* P1, const uint8_t*, const RowOff& o,
+                                        int c) {  // chunk = 1024 elements
+        Packet p;
+        p.c = stream_load16(W + (o.c + 1024u * c));
+        p.d = *reinterpret_cast<const uint16_t*>(P1 + (o.d + 64u * c));
         return p;
     }
     __device__ static float dot(const Packet& p, const float4* xv, float, int) {
@@ -124,6 +151,19 @@ struct Traits<LW_Q4_0> {
         p.d = *reinterpret_cast<const uint16_t*>(W + off1 + 2 * (e >> 5));
         return p;
     }
+    struct RowOff {
+        uint32_t c, d;
+    };
+    __device__ static RowOff row_off(uint32_t row, uint32_t K, int lane) {
+        return {row * (K / 2u) + 16u * lane, row * (K / 16u) + 2u * lane};
+    }
+    __device__ static Packet load_chunk(const uint8_t* W, const uint8_t* P1, const uint8_t*, const RowOff& o,
+                                        int c) {  // chunk = 2048 elements
+        Packet p;
+        p.c = stream_load16(W + (o.c + 1024u * c));
+        p.d = *reinterpret_cast<const uint16_t*>(P1 + (o.d + 128u * c));
+        return p;
+    }
     // d * (sum q*x - 8 * sum x)
     __device__ static float dot(const Packet& p, const float4* xv, float sx, int) {
         return half_bits_to_float(p.d) * __builtin_fmaf(-8.0f, sx, nibble_dot(p.c, xv));
@@ -146,6 +186,24 @@ struct Traits<LW_Q4_K> {
         p.r1 = rec[1];
         p.r2 = rec[2];
         p.dd = *reinterpret_cast<const uint32_t*>(W + off2 + 4 * (e >> 8));
+        return p;
+    }
+    struct RowOff {
+        uint32_t c, rec, dd;
+    };
+    __device__ static RowOff row_off(uint32_t row, uint32_t K, int lane) {
+        return {row * (K / 2u) + 16u * lane, row * (12u * (K / 256u)) + 12u * (lane >> 3),
+                row * (4u * (K / 256u)) + 4u * (lane >> 3)};
+    }
+    __device__ static Packet load_chunk(const uint8_t* W, const uint8_t* P1, const uint8_t* P2, const RowOff& o,
+                                        int c) {  // chunk = 2048 elements = 8 super-blocks
+        Packet p;
+        p.c = stream_load16(W + (o.c + 1024u * c));
+        const uint32_t* rec = reinterpret_cast<const uint32_t*>(P1 + (o.rec + 96u * c));
+        p.r0 = rec[0];
+        p.r1 = rec[1];
+        p.r2 = rec[2];
+        p.dd = *reinterpret_cast<const uint32_t*>(P2 + (o.dd + 32u * c));
         return p;
     }
     // d*sc_j * sum q*x - dmin*m_j * sum x; j is the lane's sub-block (0..7).
@@ -249,6 +307,138 @@ __global__ void __launch_bounds__(NW * kWave)
         }
 }
 
+// Single-token kernel. The workgroup is persistent: it stages x once and then
+// walks row batches (R rows) with a stride of the whole grid. A batch is split
+// into steps of CH chunks; each wave keeps the packets of its next step in
+// flight while it computes the current one. To keep the start short, every
+// thread first issues its x loads, then the loads of its first step, and only
+// then waits for x (vector-memory results return in issue order), so the x
+// tile and its group sums are in LDS after one barrier while the weights are
+// still on their way.
+template <int FMT, int R, int CH, int NW>
+__global__ void __launch_bounds__(NW * kWave)
+    gemv1_kernel(const uint8_t* __restrict__ W, const float* __restrict__ x, float* __restrict__ y,
+                 int64_t M, int64_t K, int64_t off1, int64_t off2) {
+    using T = Traits<FMT>;
+    constexpr int EPL = T::EPL;
+    constexpr int J4 = EPL / 4;
+    constexpr int E = kWave * EPL;
+    extern __shared__ float4 smem[];
+
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int nc = (int)((K + E - 1) / E);  // chunks per row
+    const int ns = (nc + CH - 1) / CH;      // steps per row batch
+    float4* xs = smem;                                          // nc * E floats, lane-interleaved
+    float* sxs = reinterpret_cast<float*>(smem + nc * (E / 4));  // nc * 64 group sums (4-bit formats)
+    const int64_t nbatch = (M + R - 1) / R;
+    const int64_t bstride = (int64_t)gridDim.x * NW;
+    int64_t b = (int64_t)blockIdx.x * NW + wave;
+
+    // (1) x loads first: thread t owns lane-slices t, t + blockDim, ... (EPL floats each).
+    const int nsl = (int)(K / EPL);
+    const int t0 = threadIdx.x;
+    float4 xr[J4];
+    if (t0 < nsl) {
+#pragma unroll
+        for (int j4 = 0; j4 < J4; ++j4) xr[j4] = *reinterpret_cast<const float4*>(x + (int64_t)EPL * t0 + 4 * j4);
+    }
+
+    // (2) the first step of this wave's first batch. Row offsets (32-bit,
+    // plane bases uniform) are formed once per batch, not per step.
+    const uint32_t K32 = (uint32_t)K;
+    const uint8_t* P1 = W + off1;
+    const uint8_t* P2 = W + off2;
+    typename T::Packet cur[R][CH], nxt[R][CH];
+    typename T::RowOff ro[R];  // rows of the batch whose steps are being issued
+    auto row_offs = [&](int64_t bb) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int64_t rr = bb * R + r;
+            ro[r] = T::row_off((uint32_t)(rr < M ? rr : M - 1), K32, lane);
+        }
+    };
+    auto load_step = [&](typename T::Packet (*pk)[CH], int ss) {
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int cc = 0; cc < CH; ++cc) {
+                const int c = ss * CH + cc;
+                if ((uint32_t)(c * E + lane * EPL) < K32) pk[r][cc] = T::load_chunk(W, P1, P2, ro[r], c);
+            }
+    };
+    if (b < nbatch) {
+        row_offs(b);
+        load_step(cur, 0);
+    }
+
+    // (3) x into LDS (and the group sums), one barrier
+    auto put_slice = [&](int t, const float4* v) {
+        const int c = t / kWave, l = t - c * kWave;
+        float sum = 0.f;
+#pragma unroll
+        for (int j4 = 0; j4 < J4; ++j4) {
+            xs[(c * J4 + j4) * kWave + l] = v[j4];
+            sum += (v[j4].x + v[j4].y) + (v[j4].z + v[j4].w);
+        }
+        if (T::kGroupSums) sxs[t] = sum;
+    };
+    if (t0 < nsl) put_slice(t0, xr);
+    for (int t = t0 + NW * kWave; t < nsl; t += NW * kWave) {
+        float4 v[J4];
+#pragma unroll
+        for (int j4 = 0; j4 < J4; ++j4) v[j4] = *reinterpret_cast<const float4*>(x + (int64_t)EPL * t + 4 * j4);
+        put_slice(t, v);
+    }
+    __syncthreads();
+
+    // (4) stream the batches
+    const int j = lane & 7;
+    int s = 0;
+    float acc[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) acc[r] = 0.f;
+    while (b < nbatch) {
+        int64_t nb = b;
+        int nss = s + 1;
+        if (nss == ns) {
+            nss = 0;
+            nb += bstride;
+        }
+        if (nb < nbatch) {
+            // every step of batch b is already issued when the next batch starts
+            if (nss == 0) row_offs(nb);
+            load_step(nxt, nss);
+        }
+#pragma unroll
+        for (int cc = 0; cc < CH; ++cc) {
+            const int c = s * CH + cc;
+            if ((uint32_t)(c * E + lane * EPL) < K32) {
+                float4 xv[J4];
+#pragma unroll
+                for (int j4 = 0; j4 < J4; ++j4) xv[j4] = xs[(c * J4 + j4) * kWave + lane];
+                const float sx = T::kGroupSums ? sxs[c * kWave + lane] : 0.f;
+#pragma unroll
+                for (int r = 0; r < R; ++r) acc[r] += T::dot(cur[r][cc], xv, sx, j);
+            }
+        }
+        if (s == ns - 1) {
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const float v = wave_sum_to_lane63(acc[r]);
+                if (lane == kWave - 1 && b * R + r < M) y[b * R + r] = v;
+                acc[r] = 0.f;
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int cc = 0; cc < CH; ++cc) cur[r][cc] = nxt[r][cc];
+        b = nb;
+        s = nss;
+    }
+}
+
 struct Config {
     int R, NW;
 };
@@ -281,9 +471,47 @@ constexpr bool fits_one_chunk() {
            kLdsBytes;
 }
 
+// Compute units of the current device, looked up once per device.
+int cu_count() {
+    static std::atomic<int> cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    int v = cache[dev].load(std::memory_order_relaxed);
+    if (v <= 0) {
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
+        cache[dev].store(v, std::memory_order_relaxed);
+    }
+    return v;
+}
+
+// Single token: the persistent kernel when the whole x row fits the LDS
+// budget, else the K-tiled kernel.
+template <int FMT, int R, int CH>
+hipError_t launch_single(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
+                         const Planes& p, hipStream_t stream) {
+    constexpr int NW = 8;
+    constexpr int E = kWave * Traits<FMT>::EPL;
+    const int64_t nc = (K + E - 1) / E;
+    const int64_t lds = nc * E * 4 + (Traits<FMT>::kGroupSums ? nc * kWave * 4 : 0);
+    if (lds > kLdsBytes || p.total >= ((int64_t)1 << 32) || M >= ((int64_t)1 << 31))
+        return launch_nt<FMT, 1>(W, x, y, M, K, p, stream);
+    const int64_t nbatch = (M + R - 1) / R;
+    int64_t grid = (nbatch + NW - 1) / NW;
+    const int64_t cap = 2 * (int64_t)cu_count();  // two 8-wave workgroups per CU
+    if (grid > cap) grid = cap;
+    hipLaunchKernelGGL((gemv1_kernel<FMT, R, CH, NW>), dim3((unsigned)grid), dim3(NW * kWave), (size_t)lds,
+                       stream, W, x, y, M, K, p.off1, p.off2);
+    return hipGetLastError();
+}
+
 template <int FMT>
 hipError_t launch_fmt(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                       int64_t n_tok, const Planes& p, hipStream_t stream) {
+    if (n_tok == 1) {
+        if constexpr (FMT == LW_Q4_0) return launch_single<FMT, 4, 1>(W, x, y, M, K, p, stream);
+
+        return launch_single<FMT, 2, 1>(W, x, y, M, K, p, stream);
+    }
     if constexpr (!fits_one_chunk<FMT, 8>()) {
         // 8 tokens of a 4-bit chunk (64 KiB of x) plus group sums exceed the
         // budget: run them as two launches of 4 tokens.

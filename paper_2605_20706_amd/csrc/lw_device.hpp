@@ -14,6 +14,14 @@ __device__ __forceinline__ float half_bits_to_float(uint32_t h16) {
     return (float)__builtin_bit_cast(_Float16, (uint16_t)h16);
 }
 
+// 16-byte load of weight data that is read exactly once: a non-temporal hint
+// keeps the stream from displacing reused data (x, scales) in the caches.
+__device__ __forceinline__ uint4 stream_load16(const uint8_t* p) {
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // Hide the known-zero bits of a value from the optimiser. Without it, a mask
 // such as v & 0x0F0F0F0F followed by per-byte float conversion is rewritten
 // into bit-field extracts plus conversions (two operations per code); with it
