@@ -2,8 +2,10 @@
 //
 // Every check runs on the host before any HIP call, in the documented order
 // (format, values, shape, alignment); a call that fails a check launches
-// nothing. Dispatch picks the matrix-vector kernels for n_tok <= LW_GEMV_MAX_TOK
-// and the matrix-core prefill kernels above that.
+// nothing. Dispatch: up to LW_GEMV_MAX_TOK tokens -> the VALU matrix-vector
+// kernels; up to 16 tokens -> the matrix-core kernel that streams the weights
+// once; more tokens -> the tiled matrix-core (prefill) kernel. f16 weights use
+// the VALU kernel in token blocks of LW_GEMV_MAX_TOK for any token count.
 #include "lw_internal.hpp"
 
 namespace {
@@ -47,10 +49,13 @@ int lw_matvec(int fmt, const void* W, const float* x, float* y, int64_t M, int64
     const lw::Planes p = lw::planes_of(fmt, M * K);
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     hipError_t err;
+    const uint8_t* Wb = static_cast<const uint8_t*>(W);
     if (n_tok <= LW_GEMV_MAX_TOK)
-        err = lw::launch_gemv(fmt, static_cast<const uint8_t*>(W), x, y, M, K, n_tok, p, s);
+        err = lw::launch_gemv(fmt, Wb, x, y, M, K, n_tok, p, s);
+    else if (n_tok <= 16 && lw::skinny_supported(fmt))
+        err = lw::launch_skinny(fmt, Wb, x, y, M, K, n_tok, p, s);
     else
-        err = lw::launch_prefill(fmt, static_cast<const uint8_t*>(W), x, y, M, K, n_tok, p, s);
+        err = lw::launch_prefill(fmt, Wb, x, y, M, K, n_tok, p, s);
     return err == hipSuccess ? LW_OK : LW_EHIP;
 }
 

@@ -48,7 +48,11 @@ hipError_t launch_dequant(int fmt, const uint8_t* W, float* out, int64_t n, cons
                           hipStream_t stream);
 hipError_t launch_gemv(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                        int64_t n_tok, const Planes& p, hipStream_t stream);
-// Matrix-core path for n_tok > LW_GEMV_MAX_TOK.
+// Matrix-core path for 2 <= n_tok <= 16 with streamed weights (4-bit and 8-bit formats).
+bool skinny_supported(int fmt);
+hipError_t launch_skinny(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
+                         int64_t n_tok, const Planes& p, hipStream_t stream);
+// Matrix-core path for larger token counts (prefill).
 hipError_t launch_prefill(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                           int64_t n_tok, const Planes& p, hipStream_t stream);
 
