@@ -31,6 +31,8 @@ import numpy as np  # noqa: E402
 from paper_2605_20706_amd import binding, layout, synth  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFS = 2500.0  # dense bf16 matrix-core peak of MI355X
+CSRC = os.path.join(ROOT, "paper_2605_20706_amd", "csrc")
 METRIC = "dequant-GEMV HBM GB/s (% of peak) and equiv. decode tok/s, Llama-1B/8B shapes"
 
 
@@ -73,21 +75,19 @@ class Workset:
         self.alg_bytes = [synth.algorithmic_bytes(wl.fmt, m.M, m.K, n_tok) for m in mats]
         self.flops = [2.0 * m.M * m.K * n_tok for m in mats]
 
-    def step(self, stream):
+    def step(self, stream, idx=None):
         f = self.lib.lw_matvec
-        for a in self.args:
-            rc = f(*a, stream)
+        for i in range(len(self.args)) if idx is None else idx:
+            rc = f(*self.args[i], stream)
             if rc != 0:
                 raise binding.LwError(rc, "lw_matvec")
 
-    def step_timed(self, stream, events):
-        f = self.lib.lw_matvec
-        for a, (e0, e1) in zip(self.args, events):
-            e0.record()
-            rc = f(*a, stream)
-            e1.record()
-            if rc != 0:
-                raise binding.LwError(rc, "lw_matvec")
+    def shapes(self):
+        """Matrix indices grouped by 'name MxK', in first-seen order."""
+        groups = {}
+        for i, m in enumerate(self.mats):
+            groups.setdefault("%s %dx%d" % (m.name, m.M, m.K), []).append(i)
+        return groups
 
 
 def run_gpu(ws, steps, warmup, mode):
@@ -121,20 +121,89 @@ def run_gpu(ws, steps, warmup, mode):
     torch.cuda.synchronize()
     ms_per_step = start.elapsed_time(end) / steps
 
-    # ---- per-launch kernel durations (eager launches bracketed by events on
-    # the launch stream; the stream is first held busy so that launches queue
-    # up back to back instead of waiting on the host) ----
+    # ---- per-shape launch durations: 192 launches of one matrix shape back
+    # to back (cycling over that shape's matrices; one graph in graph mode),
+    # queued behind a short device-side sleep so that host launch latency stays
+    # out of the timed span; events on the launch stream ----
     stream = torch.cuda.current_stream()
-    n = len(ws.args)
-    reps = 3
-    durs = np.zeros((reps, n))
-    for r in range(reps):
-        events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
-        torch.cuda._sleep(int(2.4e6 * 20))  # ~20 ms at 2.4 GHz
-        ws.step_timed(ctypes.c_void_p(stream.cuda_stream), events)
+    per_shape = {}
+    n_seq = 192
+    for key, idx in ws.shapes().items():
+        seq = (idx * ((n_seq + len(idx) - 1) // len(idx)))[:max(n_seq, len(idx))]
+
+        def sub():
+            ws.step(ctypes.c_void_p(torch.cuda.current_stream().cuda_stream), seq)
+
+        if mode == "graph":
+            g2 = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g2):
+                sub()
+            sub_run = g2.replay
+        else:
+            sub_run = sub
+        sub_run()
         torch.cuda.synchronize()
-        durs[r] = [e0.elapsed_time(e1) for e0, e1 in events]
-    return ms_per_step, durs.mean(axis=0)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(int(2.4e6 * 5))  # ~5 ms at 2.4 GHz
+        e0.record(stream)
+        sub_run()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        per_shape[key] = (e0.elapsed_time(e1) / len(seq), idx)
+    return ms_per_step, per_shape
+
+
+def kernel_of(fmt, n_tok):
+    """Kernel lw_matvec runs for (fmt, n_tok) -- a label that follows the
+    dispatch in lw_api.hip --, whether it is a matrix-core kernel, and the
+    sources that define it."""
+    name = layout.FORMAT_NAMES[fmt]
+    if n_tok == 1:
+        return "gemv1_kernel<%s>" % name, False, ["gemv.hip"]
+    if n_tok <= 16 and fmt in (layout.Q4_0, layout.Q4_K):
+        return "multitok_kernel<%s, NTS=%d>" % (name, (n_tok + 3) // 4), True, ["multitok.hip"]
+    if n_tok <= 8 or fmt == layout.F16:
+        return "gemv_kernel<%s, NT=%d>" % (name, min(n_tok, 8)), False, ["gemv.hip"]
+    if n_tok <= 16:
+        return "skinny_kernel<%s>" % name, True, ["skinny.hip"]
+    return "mfma_kernel<%s>" % name, True, ["prefill.hip"]
+
+
+def source_hash(fmt, n_tok):
+    """sha256 over the sources of the kernel that (fmt, n_tok) runs, with the
+    shared device helpers and the C header: a stored HBM traffic figure is valid
+    only for the sources it was measured on."""
+    import hashlib
+
+    h = hashlib.sha256()
+    files = [os.path.join(CSRC, f) for f in kernel_of(fmt, n_tok)[2] + ["lw_device.hpp"]]
+    files.append(os.path.join(ROOT, "include", "lw.h"))
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def stored_traffic(workload, fmt, n_tok):
+    """HBM bytes per launch from the calibrated rocprofv3 FETCH_SIZE and
+    WRITE_SIZE summary in profiles/, or None when there is none for these
+    sources."""
+    path = os.path.join(ROOT, "profiles", "hbm_traffic_%s_nt%d.txt" % (workload, n_tok))
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as fh:
+        for line in fh:
+            if "=" in line and not line.startswith((" ", "#", "|")):
+                k, v = line.strip().split("=", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("source_sha256") != source_hash(fmt, n_tok):
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(ws, budget_s):
@@ -178,7 +247,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
-                    help="only run a plain device copy of MIB MiB 20 times (HBM counter calibration)")
+                    help="only run a plain copy kernel over MIB MiB 20 times (HBM counter calibration)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -194,11 +263,11 @@ def main():
 
     if args.calibrate_copy:
         n = args.calibrate_copy * (1 << 20)
-        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
         for _ in range(20):
-            dst.copy_(src)
+            torch.neg(src, out=dst)  # a plain elementwise kernel: reads n bytes, writes n bytes
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes": n, "copies": 20}))
         return
@@ -206,25 +275,35 @@ def main():
     wl = synth.WORKLOADS[args.workload]
     keep = 0 if args.no_cpu_baseline else len(wl.matrices)
     ws = Workset(wl, args.n_tok, keep_host=keep)
-    ms_per_step, durs = run_gpu(ws, args.steps, args.warmup, args.mode)
+    ms_per_step, per_shape = run_gpu(ws, args.steps, args.warmup, args.mode)
 
+    n_launch = len(ws.args)
     step_bytes = sum(ws.alg_bytes)
     gbs = step_bytes / (ms_per_step * 1e-3) / 1e9
     tok_s = args.n_tok / (ms_per_step * 1e-3)
-    kern_s = durs.sum() * 1e-3
-    kern_gbs = step_bytes / kern_s / 1e9
+    # every launch of a step runs the same kernel; its average launch duration
+    # is the timed region over the launches it holds
+    avg_launch_s = ms_per_step * 1e-3 / n_launch
     fmt_name = layout.FORMAT_NAMES[wl.fmt]
-    roof = {"bound": "hbm", "achieved": round(kern_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(kern_gbs / HBM_PEAK_GBS, 4), "traffic": None,
-            "kernel": "gemv_kernel<%s, n_tok=%d>" % (fmt_name, args.n_tok),
-            "launches_per_step": len(ws.args), "avg_launch_us": round(float(durs.mean()) * 1e3, 3),
-            "alg_bytes_per_launch": round(step_bytes / len(ws.args))}
-    per_shape = {}
-    for m, b, d in zip(ws.mats, ws.alg_bytes, durs):
-        k = "%s %dx%d" % (m.name, m.M, m.K)
-        s = per_shape.setdefault(k, [0.0, 0.0])
-        s[0] += b
-        s[1] += d * 1e-3
+    kname, mfma, _ = kernel_of(wl.fmt, args.n_tok)
+    if mfma:
+        kern_tfs = sum(ws.flops) / n_launch / avg_launch_s / 1e12
+        roof = {"bound": "mfma", "achieved": round(kern_tfs, 2), "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
+                "frac": round(kern_tfs / MFMA_BF16_PEAK_TFS, 4)}
+    else:
+        kern_gbs = step_bytes / n_launch / avg_launch_s / 1e9
+        roof = {"bound": "hbm", "achieved": round(kern_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(kern_gbs / HBM_PEAK_GBS, 4)}
+    roof.update({"traffic": stored_traffic(wl.key, wl.fmt, args.n_tok), "kernel": kname,
+                 "launches_per_step": n_launch, "avg_launch_us": round(avg_launch_s * 1e6, 3),
+                 "alg_bytes_per_launch": round(step_bytes / n_launch),
+                 "alg_flop_per_launch": round(sum(ws.flops) / n_launch)})
+    shape_out = {}
+    for k, (ms, idx) in per_shape.items():
+        b = ws.alg_bytes[idx[0]]
+        shape_out[k] = {"us": round(ms * 1e3, 2), "GB/s": round(b / (ms * 1e-3) / 1e9, 1)}
+        if mfma:
+            shape_out[k]["TFLOP/s"] = round(ws.flops[idx[0]] / (ms * 1e-3) / 1e12, 1)
     out = {
         "metric": METRIC, "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True,
@@ -236,7 +315,7 @@ def main():
         "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
         "equiv_decode_tok_s": round(tok_s, 1),
         "roofline": roof,
-        "per_shape_kernel_gbs": {k: round(v[0] / v[1] / 1e9, 1) for k, v in per_shape.items()},
+        "per_shape": shape_out,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(ws, args.cpu_seconds)

@@ -52,6 +52,11 @@ hipError_t launch_gemv(int fmt, const uint8_t* W, const float* x, float* y, int6
 bool skinny_supported(int fmt);
 hipError_t launch_skinny(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                          int64_t n_tok, const Planes& p, hipStream_t stream);
+// Matrix-core path for 2 <= n_tok <= 16 over the 4-bit formats (block-diagonal
+// activation operand; weights streamed once).
+bool multitok_supported(int fmt, int64_t n_tok);
+hipError_t launch_multitok(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
+                           int64_t n_tok, const Planes& p, hipStream_t stream);
 // Matrix-core path for larger token counts (prefill).
 hipError_t launch_prefill(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                           int64_t n_tok, const Planes& p, hipStream_t stream);
