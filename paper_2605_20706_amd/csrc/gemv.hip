@@ -49,16 +49,16 @@ struct Traits<LW_F16> {
         p.c = *reinterpret_cast<const uint4*>(W + 2 * e);
         return p;
     }
-    // Byte offsets of row `row` in each plane, lane part included (32-bit:
-    // the kernel using them is chosen only for planes below 4 GiB), and the
-    // packet of chunk c (512 elements) at those offsets.
-    struct RowOff {
+    // Byte offsets (wave-uniform, 32-bit: the kernel using them is chosen
+    // only for planes below 4 GiB) of chunk c (512 elements) of row `row` in
+    // each plane, and the packet of lane la at those offsets.
+    struct Base {
         uint32_t c;
     };
-    __device__ static RowOff row_off(uint32_t row, uint32_t K, int lane) { return {row * (2u * K) + 16u * lane}; }
-    __device__ static Packet load_chunk(const uint8_t* W, const uint8_t*, const uint8_t*, const RowOff& o, int c) {
+    __device__ static Base base(uint32_t row, uint32_t K, uint32_t c) { return {row * (2u * K) + 1024u * c}; }
+    __device__ static Packet load_at(const uint8_t* W, const uint8_t*, const uint8_t*, const Base& b, uint32_t la) {
         Packet p;
-        p.c = stream_load16(W + (o.c + 1024u * c));
+        p.c = stream_load16(W + b.c + 16u * la);
         return p;
     }
     __device__ static float dot(const Packet& p, const float4* xv, float, int) {
@@ -89,17 +89,17 @@ struct Traits<LW_Q8_0> {
         p.d = *reinterpret_cast<const uint16_t*>(W + off1 + 2 * (e >> 5));
         return p;
     }
-    struct RowOff {
+    struct Base {
         uint32_t c, d;
     };
-    __device__ static RowOff row_off(uint32_t row, uint32_t K, int lane) {
-        return {row * K + 16u * lane, row * (K / 16u) + 2u * (lane >> 1)};
+    __device__ static Base base(uint32_t row, uint32_t K, uint32_t c) {  // chunk = 1024 elements
+        return {row * K + 1024u * c, row * (K / 16u) + 64u * c};
     }
-    __device__ static Packet load_chunk(const uint8_t* W, const uint8_t* P1, const uint8_t*, const RowOff& o,
-                                        int c) {  // chunk = 1024 elements
+    __device__ static Packet load_at(const uint8_t* W, const uint8_t* P1, const uint8_t*, const Base& b,
+                                     uint32_t la) {
         Packet p;
-        p.c = stream_load16(W + (o.c + 1024u * c));
-        p.d = *reinterpret_cast<const uint16_t*>(P1 + (o.d + 64u * c));
+        p.c = stream_load16(W + b.c + 16u * la);
+        p.d = *reinterpret_cast<const uint16_t*>(P1 + b.d + 2u * (la >> 1));
         return p;
     }
     __device__ static float dot(const Packet& p, const float4* xv, float, int) {
@@ -116,25 +116,37 @@ struct Traits<LW_Q8_0> {
     }
 };
 
-// Sum over the lane's 32 elements of q * x for 4-bit codes: returns
-// sum_lo + sum_hi / 16, where the high nibbles are converted in place as 16*q.
+// Half h (0: bits 0..15, 1: bits 16..31) of v as a binary16 value, widened.
+template <int H>
+__device__ __forceinline__ float half_of(uint32_t v) {
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)(H ? (v >> 16) : (v & 0xFFFFu)));
+}
+
+// Sum over the lane's 32 elements of q * x for 4-bit codes. A 4-bit code
+// masked into the low bits of a 16-bit half is the binary16 subnormal
+// q * 2^-24 (exactly); a high nibble masked in place reads as 16q * 2^-24.
+// Each product then takes one v_fma_mix_f32 (binary16 x float32, fused, the
+// 16-bit operand picked from its half by op_sel) and needs no conversion
+// instruction; the powers of two are undone once at the end (exact).
 __device__ __forceinline__ float nibble_dot(const uint4& c, const float4* xv) {
     const uint32_t w[4] = {c.x, c.y, c.z, c.w};
     float lo_s = 0.f, hi_s = 0.f;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const uint32_t lo = opaque(w[i] & 0x0F0F0F0Fu);  // elements 4i .. 4i+3
-        const uint32_t hi = opaque(w[i] & 0xF0F0F0F0u);  // elements 16+4i .. 16+4i+3, times 16
-        lo_s = __builtin_fmaf(ubyte<0>(lo), xv[i].x, lo_s);
-        lo_s = __builtin_fmaf(ubyte<1>(lo), xv[i].y, lo_s);
-        lo_s = __builtin_fmaf(ubyte<2>(lo), xv[i].z, lo_s);
-        lo_s = __builtin_fmaf(ubyte<3>(lo), xv[i].w, lo_s);
-        hi_s = __builtin_fmaf(ubyte<0>(hi), xv[4 + i].x, hi_s);
-        hi_s = __builtin_fmaf(ubyte<1>(hi), xv[4 + i].y, hi_s);
-        hi_s = __builtin_fmaf(ubyte<2>(hi), xv[4 + i].z, hi_s);
-        hi_s = __builtin_fmaf(ubyte<3>(hi), xv[4 + i].w, hi_s);
+        const uint32_t l02 = opaque(w[i] & 0x000F000Fu);         // elements 4i, 4i+2
+        const uint32_t h02 = opaque(w[i] & 0x00F000F0u);         // 16+4i, 16+4i+2 (times 16)
+        const uint32_t l13 = opaque((w[i] >> 8) & 0x000F000Fu);  // 4i+1, 4i+3
+        const uint32_t h13 = opaque((w[i] >> 8) & 0x00F000F0u);  // 16+4i+1, 16+4i+3 (times 16)
+        lo_s = __builtin_fmaf(half_of<0>(l02), xv[i].x, lo_s);
+        lo_s = __builtin_fmaf(half_of<1>(l02), xv[i].z, lo_s);
+        lo_s = __builtin_fmaf(half_of<0>(l13), xv[i].y, lo_s);
+        lo_s = __builtin_fmaf(half_of<1>(l13), xv[i].w, lo_s);
+        hi_s = __builtin_fmaf(half_of<0>(h02), xv[4 + i].x, hi_s);
+        hi_s = __builtin_fmaf(half_of<1>(h02), xv[4 + i].z, hi_s);
+        hi_s = __builtin_fmaf(half_of<0>(h13), xv[4 + i].y, hi_s);
+        hi_s = __builtin_fmaf(half_of<1>(h13), xv[4 + i].w, hi_s);
     }
-    return __builtin_fmaf(hi_s, 0.0625f, lo_s);
+    return __builtin_fmaf(hi_s, 1048576.0f, lo_s * 16777216.0f);  // 2^20 = 2^24 / 16, 2^24
 }
 
 template <>
@@ -151,17 +163,17 @@ struct Traits<LW_Q4_0> {
         p.d = *reinterpret_cast<const uint16_t*>(W + off1 + 2 * (e >> 5));
         return p;
     }
-    struct RowOff {
+    struct Base {
         uint32_t c, d;
     };
-    __device__ static RowOff row_off(uint32_t row, uint32_t K, int lane) {
-        return {row * (K / 2u) + 16u * lane, row * (K / 16u) + 2u * lane};
+    __device__ static Base base(uint32_t row, uint32_t K, uint32_t c) {  // chunk = 2048 elements
+        return {row * (K / 2u) + 1024u * c, row * (K / 16u) + 128u * c};
     }
-    __device__ static Packet load_chunk(const uint8_t* W, const uint8_t* P1, const uint8_t*, const RowOff& o,
-                                        int c) {  // chunk = 2048 elements
+    __device__ static Packet load_at(const uint8_t* W, const uint8_t* P1, const uint8_t*, const Base& b,
+                                     uint32_t la) {
         Packet p;
-        p.c = stream_load16(W + (o.c + 1024u * c));
-        p.d = *reinterpret_cast<const uint16_t*>(P1 + (o.d + 128u * c));
+        p.c = stream_load16(W + b.c + 16u * la);
+        p.d = *reinterpret_cast<const uint16_t*>(P1 + b.d + 2u * la);
         return p;
     }
     // d * (sum q*x - 8 * sum x)
@@ -188,30 +200,35 @@ struct Traits<LW_Q4_K> {
         p.dd = *reinterpret_cast<const uint32_t*>(W + off2 + 4 * (e >> 8));
         return p;
     }
-    struct RowOff {
+    struct Base {
         uint32_t c, rec, dd;
     };
-    __device__ static RowOff row_off(uint32_t row, uint32_t K, int lane) {
-        return {row * (K / 2u) + 16u * lane, row * (12u * (K / 256u)) + 12u * (lane >> 3),
-                row * (4u * (K / 256u)) + 4u * (lane >> 3)};
+    __device__ static Base base(uint32_t row, uint32_t K, uint32_t c) {  // chunk = 2048 elements = 8 super-blocks
+        return {row * (K / 2u) + 1024u * c, row * (12u * (K / 256u)) + 96u * c, row * (4u * (K / 256u)) + 32u * c};
     }
-    __device__ static Packet load_chunk(const uint8_t* W, const uint8_t* P1, const uint8_t* P2, const RowOff& o,
-                                        int c) {  // chunk = 2048 elements = 8 super-blocks
+    __device__ static Packet load_at(const uint8_t* W, const uint8_t* P1, const uint8_t* P2, const Base& b,
+                                     uint32_t la) {
         Packet p;
-        p.c = stream_load16(W + (o.c + 1024u * c));
-        const uint32_t* rec = reinterpret_cast<const uint32_t*>(P1 + (o.rec + 96u * c));
+        p.c = stream_load16(W + b.c + 16u * la);
+        const uint32_t* rec = reinterpret_cast<const uint32_t*>(P1 + b.rec + 12u * (la >> 3));
         p.r0 = rec[0];
         p.r1 = rec[1];
         p.r2 = rec[2];
-        p.dd = *reinterpret_cast<const uint32_t*>(P2 + (o.dd + 32u * c));
+        p.dd = *reinterpret_cast<const uint32_t*>(P2 + b.dd + 4u * (la >> 3));
         return p;
     }
     // d*sc_j * sum q*x - dmin*m_j * sum x; j is the lane's sub-block (0..7).
+    // The 6-bit fields are cut out of the 96-bit record {r2:r1:r0} with 32-bit
+    // funnel shifts (v_alignbit_b32): no 64-bit register pairs, so the loaded
+    // words are used where they land.
     __device__ static float dot(const Packet& p, const float4* xv, float sx, int j) {
-        const uint64_t lo = (uint64_t)p.r0 | ((uint64_t)p.r1 << 32);  // record bits 0..63
-        const uint64_t hi = (uint64_t)p.r1 | ((uint64_t)p.r2 << 32);  // record bits 32..95
-        const float sc = (float)((uint32_t)(lo >> (6 * j)) & 63u);
-        const float m = (float)((uint32_t)(hi >> (16 + 6 * j)) & 63u);
+        const uint32_t ts = 6u * (uint32_t)j;         // sc_j at bit ts (0..42)
+        const uint32_t tm = 16u + 6u * (uint32_t)j;   // m_j at bit 32 + tm (tm 16..58)
+        const bool sl = ts < 32u, ml = tm < 32u;  // field starts in the lower word of the pair
+        const uint32_t sc_w = __builtin_amdgcn_alignbit(sl ? p.r1 : 0u, sl ? p.r0 : p.r1, ts & 31u);
+        const uint32_t m_w = __builtin_amdgcn_alignbit(ml ? p.r2 : 0u, ml ? p.r1 : p.r2, tm & 31u);
+        const float sc = (float)(sc_w & 63u);
+        const float m = (float)(m_w & 63u);
         const float ds = half_bits_to_float(p.dd & 0xFFFFu) * sc;
         const float dm = half_bits_to_float(p.dd >> 16) * m;
         return __builtin_fmaf(ds, nibble_dot(p.c, xv), -dm * sx);
@@ -308,32 +325,37 @@ __global__ void __launch_bounds__(NW * kWave)
 }
 
 // Single-token kernel. The workgroup is persistent: it stages x once and then
-// walks row batches (R rows) with a stride of the whole grid. A batch is split
-// into steps of CH chunks; each wave keeps the packets of its next step in
-// flight while it computes the current one. To keep the start short, every
-// thread first issues its x loads, then the loads of its first step, and only
-// then waits for x (vector-memory results return in issue order), so the x
-// tile and its group sums are in LDS after one barrier while the weights are
-// still on their way.
-template <int FMT, int R, int CH, int NW>
+// walks row batches (R rows) with a stride of the whole grid. A batch is one
+// chunk-sized step per chunk of the row; the wave's steps over all its batches
+// form one sequence, and the packets of the next D steps of that sequence are
+// always in flight (a ring of D packet sets, refilled as each is consumed), so
+// a wave keeps D * R * 1 KiB of weights outstanding across row boundaries. To
+// keep the start short, every thread first issues its x loads, then the loads
+// of its first D steps, and only then waits for x (vector-memory results
+// return in issue order), so the x tile and its group sums are in LDS after
+// one barrier while the weights are still on their way.
+template <int FMT, int R, int D, int NW>
 __global__ void __launch_bounds__(NW * kWave)
     gemv1_kernel(const uint8_t* __restrict__ W, const float* __restrict__ x, float* __restrict__ y,
                  int64_t M, int64_t K, int64_t off1, int64_t off2) {
     using T = Traits<FMT>;
+    using Packet = typename T::Packet;
     constexpr int EPL = T::EPL;
     constexpr int J4 = EPL / 4;
     constexpr int E = kWave * EPL;
     extern __shared__ float4 smem[];
 
     const int lane = threadIdx.x & (kWave - 1);
-    const int wave = threadIdx.x / kWave;
-    const int nc = (int)((K + E - 1) / E);  // chunks per row
-    const int ns = (nc + CH - 1) / CH;      // steps per row batch
+    // wave-uniform (the compiler cannot tell on its own): all row and plane
+    // offsets derived from it live in scalar registers
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int nc = (int)((K + E - 1) / E);  // chunks per row = steps per batch
     float4* xs = smem;                                          // nc * E floats, lane-interleaved
     float* sxs = reinterpret_cast<float*>(smem + nc * (E / 4));  // nc * 64 group sums (4-bit formats)
     const int64_t nbatch = (M + R - 1) / R;
     const int64_t bstride = (int64_t)gridDim.x * NW;
-    int64_t b = (int64_t)blockIdx.x * NW + wave;
+    const int64_t b0 = (int64_t)blockIdx.x * NW + wave;
+    const int nbw = b0 < nbatch ? (int)((nbatch - b0 + bstride - 1) / bstride) : 0;  // batches of this wave
 
     // (1) x loads first: thread t owns lane-slices t, t + blockDim, ... (EPL floats each).
     const int nsl = (int)(K / EPL);
@@ -344,33 +366,37 @@ __global__ void __launch_bounds__(NW * kWave)
         for (int j4 = 0; j4 < J4; ++j4) xr[j4] = *reinterpret_cast<const float4*>(x + (int64_t)EPL * t0 + 4 * j4);
     }
 
-    // (2) the first step of this wave's first batch. Row offsets (32-bit,
-    // plane bases uniform) are formed once per batch, not per step.
+    // (2) the first D steps. Every issue loads: a step past the wave's end
+    // reads chunk 0 of row 0 and its packet is never used; in a chunk that
+    // runs past K the lanes beyond it reload the last valid lane's bytes. So
+    // the loads are unconditional and the compiler can count them, keeping
+    // the next steps in flight while one is consumed.
     const uint32_t K32 = (uint32_t)K;
     const uint8_t* P1 = W + off1;
     const uint8_t* P2 = W + off2;
-    typename T::Packet cur[R][CH], nxt[R][CH];
-    typename T::RowOff ro[R];  // rows of the batch whose steps are being issued
-    auto row_offs = [&](int64_t bb) {
+    const int total = nbw * nc;  // steps of this wave
+    const uint32_t ulane = (uint32_t)lane;
+    Packet ring[D][R];
+    int ik = 0, ic = 0;  // next step to issue: batch ik of the wave, chunk ic
+    auto issue = [&](Packet* pk) {
+        const bool live = ik < nbw;
+        const int64_t bb = b0 + (int64_t)ik * bstride;
+        const uint32_t cc = live ? (uint32_t)ic : 0u;
+        const uint32_t lmax = (K32 - cc * E) / EPL - 1u;  // last lane inside K
+        const uint32_t la = ulane < lmax ? ulane : lmax;
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const int64_t rr = bb * R + r;
-            ro[r] = T::row_off((uint32_t)(rr < M ? rr : M - 1), K32, lane);
+            const uint32_t row = live ? (uint32_t)(rr < M ? rr : M - 1) : 0u;
+            pk[r] = T::load_at(W, P1, P2, T::base(row, K32, cc), la);
+        }
+        if (++ic == nc) {
+            ic = 0;
+            ++ik;
         }
     };
-    auto load_step = [&](typename T::Packet (*pk)[CH], int ss) {
 #pragma unroll
-        for (int r = 0; r < R; ++r)
-#pragma unroll
-            for (int cc = 0; cc < CH; ++cc) {
-                const int c = ss * CH + cc;
-                if ((uint32_t)(c * E + lane * EPL) < K32) pk[r][cc] = T::load_chunk(W, P1, P2, ro[r], c);
-            }
-    };
-    if (b < nbatch) {
-        row_offs(b);
-        load_step(cur, 0);
-    }
+    for (int d = 0; d < D; ++d) issue(ring[d]);
 
     // (3) x into LDS (and the group sums), one barrier
     auto put_slice = [&](int t, const float4* v) {
@@ -392,50 +418,64 @@ __global__ void __launch_bounds__(NW * kWave)
     }
     __syncthreads();
 
-    // (4) stream the batches
+    // (4) consume the steps in order, refilling each ring slot D steps ahead.
+    // Steady rounds (every refill is a real step) are straight-line code with
+    // unconditional loads; only the last two rounds test what to refill.
     const int j = lane & 7;
-    int s = 0;
+    int k = 0, c = 0;  // step being consumed: batch k of the wave, chunk c
     float acc[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) acc[r] = 0.f;
-    while (b < nbatch) {
-        int64_t nb = b;
-        int nss = s + 1;
-        if (nss == ns) {
-            nss = 0;
-            nb += bstride;
-        }
-        if (nb < nbatch) {
-            // every step of batch b is already issued when the next batch starts
-            if (nss == 0) row_offs(nb);
-            load_step(nxt, nss);
-        }
+    auto consume = [&](const Packet* pk, bool live) {
+        const bool ok = live && (uint32_t)(c * E + lane * EPL) < K32;
+        float4 xv[J4];
 #pragma unroll
-        for (int cc = 0; cc < CH; ++cc) {
-            const int c = s * CH + cc;
-            if ((uint32_t)(c * E + lane * EPL) < K32) {
-                float4 xv[J4];
+        for (int j4 = 0; j4 < J4; ++j4) xv[j4] = xs[(c * J4 + j4) * kWave + lane];
+        const float sx = T::kGroupSums ? sxs[c * kWave + lane] : 0.f;
 #pragma unroll
-                for (int j4 = 0; j4 < J4; ++j4) xv[j4] = xs[(c * J4 + j4) * kWave + lane];
-                const float sx = T::kGroupSums ? sxs[c * kWave + lane] : 0.f;
-#pragma unroll
-                for (int r = 0; r < R; ++r) acc[r] += T::dot(cur[r][cc], xv, sx, j);
-            }
+        for (int r = 0; r < R; ++r) {
+            const float v = T::dot(pk[r], xv, sx, j);
+            acc[r] += ok ? v : 0.f;
         }
-        if (s == ns - 1) {
+    };
+    auto finish_step = [&](bool live) {
+        if (live && c == nc - 1) {
+            const int64_t bb = b0 + (int64_t)k * bstride;
 #pragma unroll
             for (int r = 0; r < R; ++r) {
                 const float v = wave_sum_to_lane63(acc[r]);
-                if (lane == kWave - 1 && b * R + r < M) y[b * R + r] = v;
+                if (lane == kWave - 1 && bb * R + r < M) y[bb * R + r] = v;
                 acc[r] = 0.f;
             }
         }
+        if (++c == nc) {
+            c = 0;
+            ++k;
+        }
+    };
+    int s0 = 0;
+    for (; s0 + 2 * D <= total; s0 += D) {
 #pragma unroll
-        for (int r = 0; r < R; ++r)
+        for (int d = 0; d < D; ++d) {
+            consume(ring[d], true);
+            issue(ring[d]);
+            finish_step(true);
+        }
+    }
 #pragma unroll
-            for (int cc = 0; cc < CH; ++cc) cur[r][cc] = nxt[r][cc];
-        b = nb;
-        s = nss;
+    for (int d = 0; d < D; ++d) {
+        const bool live = s0 + d < total;
+        consume(ring[d], live);
+        if (s0 + d + D < total) issue(ring[d]);
+        finish_step(live);
+    }
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+        const bool live = s0 + D + d < total;
+        if (live) {
+            consume(ring[d], true);
+            finish_step(true);
+        }
     }
 }
 
@@ -486,7 +526,7 @@ int cu_count() {
 
 // Single token: the persistent kernel when the whole x row fits the LDS
 // budget, else the K-tiled kernel.
-template <int FMT, int R, int CH>
+template <int FMT, int R, int D>
 hipError_t launch_single(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                          const Planes& p, hipStream_t stream) {
     constexpr int NW = 8;
@@ -499,7 +539,7 @@ hipError_t launch_single(const uint8_t* W, const float* x, float* y, int64_t M, 
     int64_t grid = (nbatch + NW - 1) / NW;
     const int64_t cap = 2 * (int64_t)cu_count();  // two 8-wave workgroups per CU
     if (grid > cap) grid = cap;
-    hipLaunchKernelGGL((gemv1_kernel<FMT, R, CH, NW>), dim3((unsigned)grid), dim3(NW * kWave), (size_t)lds,
+    hipLaunchKernelGGL((gemv1_kernel<FMT, R, D, NW>), dim3((unsigned)grid), dim3(NW * kWave), (size_t)lds,
                        stream, W, x, y, M, K, p.off1, p.off2);
     return hipGetLastError();
 }
@@ -508,9 +548,9 @@ template <int FMT>
 hipError_t launch_fmt(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                       int64_t n_tok, const Planes& p, hipStream_t stream) {
     if (n_tok == 1) {
-        if constexpr (FMT == LW_Q4_0) return launch_single<FMT, 4, 1>(W, x, y, M, K, p, stream);
+        if constexpr (FMT == LW_Q4_0 || FMT == LW_Q4_K) return launch_single<FMT, 1, 2>(W, x, y, M, K, p, stream);
 
-        return launch_single<FMT, 2, 1>(W, x, y, M, K, p, stream);
+        return launch_single<FMT, 2, 2>(W, x, y, M, K, p, stream);
     }
     if constexpr (!fits_one_chunk<FMT, 8>()) {
         // 8 tokens of a 4-bit chunk (64 KiB of x) plus group sums exceed the
