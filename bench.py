@@ -166,7 +166,7 @@ def kernel_of(fmt, n_tok):
         return "gemv_kernel<%s, NT=%d>" % (name, min(n_tok, 8)), False, ["gemv.hip"]
     if n_tok <= 16:
         return "skinny_kernel<%s>" % name, True, ["skinny.hip"]
-    return "mfma_kernel<%s>" % name, True, ["prefill.hip"]
+    return "gemm_kernel<%s>" % name, True, ["prefill.hip"]
 
 
 def source_hash(fmt, n_tok):
