@@ -479,6 +479,155 @@ __global__ void __launch_bounds__(NW * kWave)
     }
 }
 
+// Group sum over aligned 8-lane groups: lane 8m+7 ends with the sum of
+// lanes 8m..8m+7 (row_shr 1, 2, 4 inside each 16-lane row).
+__device__ __forceinline__ float sum8_to_last(float v) {
+    v += dpp_move<0x111>(v);
+    v += dpp_move<0x112>(v);
+    v += dpp_move<0x114>(v);
+    return v;
+}
+
+// Single-token kernel for the 4-bit formats with the activation held in
+// registers. K is a whole number NC of chunks (2048 elements); a workgroup is
+// G row groups x WPR waves, and wave w of a row group owns chunks
+// [w*CPW, (w+1)*CPW) of every row of that group (NC = CPW*WPR), so lane l
+// keeps x[c*2048 + 32l : +32] and its group sum for those CPW chunks in VGPRs
+// for the whole kernel and never reads x again. The rows of row group
+// rg = blockIdx.x*G + g are rg, rg + gridDim.x*G, ...; each wave keeps the
+// packets of its next DR rows in flight (a ring refilled as each row is
+// consumed). With WPR == 1 a wave reduces its row over the 64 lanes with DPP
+// adds and stores it; with WPR > 1 each wave's per-row partial goes to LDS and
+// the WPR partials of a row are added in wave order after one barrier at the
+// end. x is staged once: coalesced 16-byte loads (issued before the first
+// rows' packets), group sums by DPP over the 8 lanes that hold one group, an
+// LDS tile in which float4 j4 of lane l of chunk c sits at row c*8 + j4,
+// column l ^ j4 (the 8 lanes that stage one group write 8 different bank
+// groups, and the 64 lanes reading one row read 64 different float4s), one
+// barrier, then one read per lane.
+template <int FMT, int CPW, int WPR, int G, int DR>
+__global__ void __launch_bounds__(G * WPR * kWave)
+    gemv1r_kernel(const uint8_t* __restrict__ W, const float* __restrict__ x, float* __restrict__ y,
+                  int M, int nr_max, int64_t off1, int64_t off2) {
+    using T = Traits<FMT>;
+    using Packet = typename T::Packet;
+    static_assert(T::EPL == 32 && T::kGroupSums, "4-bit formats only");
+    constexpr int J4 = 8;                    // float4s of x per lane per chunk
+    constexpr int E = kWave * 32;            // elements per chunk
+    constexpr int NC = CPW * WPR;            // chunks per row
+    constexpr uint32_t K = (uint32_t)NC * E;
+    constexpr int NT = G * WPR * kWave;      // threads per workgroup
+    constexpr int NQ = (int)(K / 4);         // float4s of x
+    constexpr int XPT = (NQ + NT - 1) / NT;  // x float4s per thread
+    static_assert(NT % kWave == 0 && NQ % 8 == 0, "group sums need whole 8-lane groups");
+    extern __shared__ float4 smem[];
+    float4* xs = smem;                                       // NQ float4s, lane-interleaved
+    float* sxs = reinterpret_cast<float*>(smem + NQ);        // NC * 64 group sums
+    float* red = sxs + NC * kWave;                           // [G][nr_max][WPR] row partials
+
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1);
+    const int wv = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const int g = wv / WPR, w = wv - g * WPR;
+    const int rg = blockIdx.x * G + g;
+    const int rgs = gridDim.x * G;
+    const int nr = rg < M ? (M - 1 - rg) / rgs + 1 : 0;  // rows of this row group
+
+    // (1) x loads (clamped index: every load is issued)
+    float4 xv[XPT];
+#pragma unroll
+    for (int i = 0; i < XPT; ++i) {
+        const int q = tid + i * NT;
+        xv[i] = *reinterpret_cast<const float4*>(x + 4 * (q < NQ ? q : NQ - 1));
+    }
+
+    // (2) packets of the first DR rows. A row index past the group's end loads
+    // row 0 and its packets are never used.
+    const uint8_t* P1 = W + off1;
+    const uint8_t* P2 = W + off2;
+    const uint32_t ulane = (uint32_t)lane;
+    Packet ring[DR][CPW];
+    int ik = 0;  // next row (of the group) to issue
+    auto issue = [&](Packet* pk) __attribute__((always_inline)) {
+        const uint32_t row = ik < nr ? (uint32_t)(rg + ik * rgs) : 0u;
+#pragma unroll
+        for (int cc = 0; cc < CPW; ++cc)
+            pk[cc] = T::load_at(W, P1, P2, T::base(row, K, (uint32_t)(w * CPW + cc)), ulane);
+        ++ik;
+    };
+#pragma unroll
+    for (int d = 0; d < DR; ++d) issue(ring[d]);
+
+    // (3) x into LDS with its group sums, one barrier, then this lane's slices
+#pragma unroll
+    for (int i = 0; i < XPT; ++i) {
+        const int q = tid + i * NT;
+        const int c = q / (E / 4), rem = q - c * (E / 4), l = rem / J4, j4 = rem - l * J4;
+        const float s = sum8_to_last((xv[i].x + xv[i].y) + (xv[i].z + xv[i].w));
+        if (q < NQ) {
+            xs[(c * J4 + j4) * kWave + (l ^ j4)] = xv[i];
+            if ((tid & 7) == 7) sxs[q / J4] = s;
+        }
+    }
+    __syncthreads();
+    float4 xr[CPW][J4];
+    float sx[CPW];
+#pragma unroll
+    for (int cc = 0; cc < CPW; ++cc) {
+        const int c = w * CPW + cc;
+#pragma unroll
+        for (int j4 = 0; j4 < J4; ++j4) xr[cc][j4] = xs[(c * J4 + j4) * kWave + (lane ^ j4)];
+        sx[cc] = sxs[c * kWave + lane];
+    }
+
+    // (4) consume rows in order, refilling each ring slot DR rows ahead.
+    // Steady rounds issue only real rows (unconditional loads); the last two
+    // rounds test what to consume and refill.
+    const int j = lane & 7;  // the lane's sub-block within a super-block
+    auto consume = [&](const Packet* pk, int kk) __attribute__((always_inline)) {
+        float acc = 0.f;
+#pragma unroll
+        for (int cc = 0; cc < CPW; ++cc) acc += T::dot(pk[cc], xr[cc], sx[cc], j);
+        const float v = wave_sum_to_lane63(acc);
+        if (lane == kWave - 1) {
+            if constexpr (WPR == 1)
+                y[rg + kk * rgs] = v;
+            else
+                red[(g * nr_max + kk) * WPR + w] = v;
+        }
+    };
+    int s0 = 0;
+    for (; s0 + 2 * DR <= nr; s0 += DR) {
+#pragma unroll
+        for (int d = 0; d < DR; ++d) {
+            consume(ring[d], s0 + d);
+            issue(ring[d]);
+        }
+    }
+#pragma unroll
+    for (int d = 0; d < DR; ++d) {
+        if (s0 + d < nr) consume(ring[d], s0 + d);
+        if (s0 + d + DR < nr) issue(ring[d]);
+    }
+#pragma unroll
+    for (int d = 0; d < DR; ++d)
+        if (s0 + DR + d < nr) consume(ring[d], s0 + DR + d);
+
+    if constexpr (WPR > 1) {
+        __syncthreads();
+        for (int idx = tid; idx < G * nr_max; idx += NT) {
+            const int gg = idx / nr_max, ii = idx - gg * nr_max;
+            const int64_t row = (int64_t)blockIdx.x * G + gg + (int64_t)ii * rgs;
+            if (row < M) {
+                float s = 0.f;
+#pragma unroll
+                for (int ww = 0; ww < WPR; ++ww) s += red[idx * WPR + ww];
+                y[row] = s;
+            }
+        }
+    }
+}
+
 struct Config {
     int R, NW;
 };
@@ -544,11 +693,54 @@ hipError_t launch_single(const uint8_t* W, const float* x, float* y, int64_t M, 
     return hipGetLastError();
 }
 
+// Register-resident-x kernel: G row groups x WPR waves per workgroup, at most
+// CAP workgroups per compute unit. Returns hipErrorNotSupported when the shape
+// does not fit it (the caller then uses the LDS kernel).
+template <int FMT, int CPW, int WPR, int G, int DR, int CAP>
+hipError_t launch_reg(const uint8_t* W, const float* x, float* y, int64_t M, const Planes& p,
+                      hipStream_t stream) {
+    constexpr int64_t NC = CPW * WPR;
+    constexpr int64_t K = NC * kWave * 32;
+    if (p.total >= ((int64_t)1 << 32) || M >= ((int64_t)1 << 31)) return hipErrorNotSupported;
+    int64_t grid = (M + G - 1) / G;
+    const int64_t cap = CAP * (int64_t)cu_count();
+    if (grid > cap) grid = cap;
+    const int64_t nr_max = (M + grid * G - 1) / (grid * G);
+    const int64_t lds = K * 4 + NC * kWave * 4 + (WPR > 1 ? G * nr_max * WPR * 4 : 0);
+    if (lds > kLdsBytes) return hipErrorNotSupported;
+    hipLaunchKernelGGL((gemv1r_kernel<FMT, CPW, WPR, G, DR>), dim3((unsigned)grid), dim3(G * WPR * kWave),
+                       (size_t)lds, stream, W, x, y, (int)M, (int)nr_max, p.off1, p.off2);
+    return hipGetLastError();
+}
+
+// Kernel selection for one token over the 4-bit formats, by the number of
+// 2048-element chunks per row (K / 2048) and the row count. The register
+// kernel needs a few rows per wave to pay for staging x whole; below that
+// (and for other K) the LDS kernel, which spreads single chunks over the
+// waves, is faster.
+template <int FMT>
+hipError_t launch_single_q4(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
+                            const Planes& p, hipStream_t stream) {
+    hipError_t err = hipErrorNotSupported;
+    if (K % 2048 == 0) {
+        switch (K / 2048) {
+        case 1: err = launch_reg<FMT, 1, 1, 8, 2, 2>(W, x, y, M, p, stream); break;
+        case 2:
+            if (M >= 10240) err = launch_reg<FMT, 2, 1, 8, 2, 2>(W, x, y, M, p, stream);
+            break;
+        case 7: err = launch_reg<FMT, 1, 7, 2, 2, 1>(W, x, y, M, p, stream); break;
+        default: break;
+        }
+    }
+    if (err != hipErrorNotSupported) return err;
+    return launch_single<FMT, 1, 2>(W, x, y, M, K, p, stream);
+}
+
 template <int FMT>
 hipError_t launch_fmt(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                       int64_t n_tok, const Planes& p, hipStream_t stream) {
     if (n_tok == 1) {
-        if constexpr (FMT == LW_Q4_0 || FMT == LW_Q4_K) return launch_single<FMT, 1, 2>(W, x, y, M, K, p, stream);
+        if constexpr (FMT == LW_Q4_0 || FMT == LW_Q4_K) return launch_single_q4<FMT>(W, x, y, M, K, p, stream);
 
         return launch_single<FMT, 2, 2>(W, x, y, M, K, p, stream);
     }
