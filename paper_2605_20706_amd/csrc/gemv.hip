@@ -235,6 +235,109 @@ struct Traits<LW_Q4_K> {
     }
 };
 
+// Scaled forms for the register kernel: the lane's 32 products are
+// accumulated in units of 2^-24 (the value of a nibble masked into the low
+// bits of a binary16 half), so no per-step rescaling is needed; the caller
+// multiplies the row total by 2^24 once, after the cross-lane sum (exact:
+// powers of two). sx24 is the lane's group sum of x times 2^-24.
+__device__ __forceinline__ float nibble_dot24(const uint4& c, const float4* xv) {
+    const uint32_t w[4] = {c.x, c.y, c.z, c.w};
+    float lo_s = 0.f, hi_s = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const uint32_t l02 = opaque(w[i] & 0x000F000Fu);
+        const uint32_t h02 = opaque(w[i] & 0x00F000F0u);
+        const uint32_t l13 = opaque((w[i] >> 8) & 0x000F000Fu);
+        const uint32_t h13 = opaque((w[i] >> 8) & 0x00F000F0u);
+        lo_s = __builtin_fmaf(half_of<0>(l02), xv[i].x, lo_s);
+        lo_s = __builtin_fmaf(half_of<1>(l02), xv[i].z, lo_s);
+        lo_s = __builtin_fmaf(half_of<0>(l13), xv[i].y, lo_s);
+        lo_s = __builtin_fmaf(half_of<1>(l13), xv[i].w, lo_s);
+        hi_s = __builtin_fmaf(half_of<0>(h02), xv[4 + i].x, hi_s);
+        hi_s = __builtin_fmaf(half_of<1>(h02), xv[4 + i].z, hi_s);
+        hi_s = __builtin_fmaf(half_of<0>(h13), xv[4 + i].y, hi_s);
+        hi_s = __builtin_fmaf(half_of<1>(h13), xv[4 + i].w, hi_s);
+    }
+    return __builtin_fmaf(hi_s, 0.0625f, lo_s);  // high nibbles read as 16q
+}
+
+// acc + (Q4_0 contribution of the lane) * 2^-24: d * (sum q*x - 8 * sum x)
+__device__ __forceinline__ float dot24(const Traits<LW_Q4_0>::Packet& p, const float4* xv, float sx24,
+                                       uint32_t, uint32_t, bool, bool, float acc) {
+    return __builtin_fmaf(half_bits_to_float(p.d), __builtin_fmaf(-8.0f, sx24, nibble_dot24(p.c, xv)), acc);
+}
+
+// acc + (Q4_K-style contribution) * 2^-24: d*sc_j * sum q*x - dmin*m_j * sum x.
+// sc_j sits at record bit ts = 6j and m_j at bit 32 + tm, tm = 16 + 6j. A
+// field inside one word is cut out of that word rotated (v_alignbit_b32 of
+// the word with itself); a field across two words out of the pair, so each
+// field takes one select of the low source word, fixed per lane.
+__device__ __forceinline__ float dot24(const Traits<LW_Q4_K>::Packet& p, const float4* xv, float sx24,
+                                       uint32_t ts, uint32_t tm, bool sl, bool ml, float acc) {
+    const uint32_t sc_w = __builtin_amdgcn_alignbit(p.r1, sl ? p.r0 : p.r1, ts & 31u);
+    const uint32_t m_w = __builtin_amdgcn_alignbit(p.r2, ml ? p.r1 : p.r2, tm & 31u);
+    const float ds = half_bits_to_float(p.dd & 0xFFFFu) * (float)(sc_w & 63u);
+    const float dm = half_bits_to_float(p.dd >> 16) * (float)(m_w & 63u);
+    return __builtin_fmaf(-dm, sx24, __builtin_fmaf(ds, nibble_dot24(p.c, xv), acc));
+}
+
+// Sums over the 64 lanes of DR row accumulators at once (v_permlane32_swap /
+// v_permlane16_swap fold the halves of several rows into one register, then
+// DPP adds finish inside 16-lane rows). DR = 1: the total is in lane 63.
+// DR = 2: row 0 in lane 31, row 1 in lane 63. DR = 4: rows 0, 2, 1, 3 in
+// lanes 15, 31, 47, 63. lane_of<DR>(d) gives the lane of row d.
+template <int DR>
+__device__ __forceinline__ int lane_of(int d) {
+    if constexpr (DR == 1) return 63;
+    else if constexpr (DR == 2) return 32 * d + 31;
+    else return 16 * (2 * (d & 1) + (d >> 1)) + 15;
+}
+
+__device__ __forceinline__ float fswap32(float a, float b, float& hi) {
+    const auto s = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, a), __builtin_bit_cast(uint32_t, b),
+                                                    false, false);
+    hi = __builtin_bit_cast(float, (uint32_t)s[1]);
+    return __builtin_bit_cast(float, (uint32_t)s[0]);
+}
+
+__device__ __forceinline__ float fswap16(float a, float b, float& odd) {
+    const auto s = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(uint32_t, a), __builtin_bit_cast(uint32_t, b),
+                                                    false, false);
+    odd = __builtin_bit_cast(float, (uint32_t)s[1]);
+    return __builtin_bit_cast(float, (uint32_t)s[0]);
+}
+
+template <int DR>
+__device__ __forceinline__ float rows_sum(const float* acc) {
+    if constexpr (DR == 1) {
+        return wave_sum_to_lane63(acc[0]);
+    } else if constexpr (DR == 2) {
+        float h;
+        const float l = fswap32(acc[0], acc[1], h);
+        float v = l + h;  // lanes 0-31: row 0 folded to 32 lanes; 32-63: row 1
+        v += dpp_move<0x111>(v);
+        v += dpp_move<0x112>(v);
+        v += dpp_move<0x114>(v);
+        v += dpp_move<0x118>(v);
+        v += dpp_move<0x142, 0xA>(v);  // row_bcast:15 into rows 1 and 3
+        return v;
+    } else {
+        static_assert(DR == 4, "1, 2 or 4 rows");
+        float h01, h23;
+        const float l01 = fswap32(acc[0], acc[1], h01);
+        const float l23 = fswap32(acc[2], acc[3], h23);
+        const float a = l01 + h01, b = l23 + h23;  // [row0 | row1] and [row2 | row3], 32 lanes each
+        float o;
+        const float e = fswap16(a, b, o);
+        float v = e + o;  // 16-lane rows: row 0, row 2, row 1, row 3
+        v += dpp_move<0x111>(v);
+        v += dpp_move<0x112>(v);
+        v += dpp_move<0x114>(v);
+        v += dpp_move<0x118>(v);
+        return v;
+    }
+}
+
 template <int FMT, int NT, int R, int NW>
 __global__ void __launch_bounds__(NW * kWave)
     gemv_kernel(const uint8_t* __restrict__ W, const float* __restrict__ x, float* __restrict__ y,
@@ -496,10 +599,10 @@ __device__ __forceinline__ float sum8_to_last(float v) {
 // for the whole kernel and never reads x again. The rows of row group
 // rg = blockIdx.x*G + g are rg, rg + gridDim.x*G, ...; each wave keeps the
 // packets of its next DR rows in flight (a ring refilled as each row is
-// consumed). With WPR == 1 a wave reduces its row over the 64 lanes with DPP
-// adds and stores it; with WPR > 1 each wave's per-row partial goes to LDS and
-// the WPR partials of a row are added in wave order after one barrier at the
-// end. x is staged once: coalesced 16-byte loads (issued before the first
+// consumed) and sums DR rows over its 64 lanes at once. With WPR == 1 the
+// wave stores the row totals; with WPR > 1 each wave's per-row partial goes
+// to LDS and the WPR partials of a row are added in wave order after one
+// barrier at the end. x is staged once: coalesced 16-byte loads (issued before the first
 // rows' packets), group sums by DPP over the 8 lanes that hold one group, an
 // LDS tile in which float4 j4 of lane l of chunk c sits at row c*8 + j4,
 // column l ^ j4 (the 8 lanes that stage one group write 8 different bank
@@ -580,16 +683,32 @@ __global__ void __launch_bounds__(G * WPR * kWave)
         sx[cc] = sxs[c * kWave + lane];
     }
 
-    // (4) consume rows in order, refilling each ring slot DR rows ahead.
-    // Steady rounds issue only real rows (unconditional loads); the last two
-    // rounds test what to consume and refill.
+    // (4) consume rows in order, DR at a time, refilling each ring slot DR
+    // rows ahead. Steady rounds refill only real rows, so their loads are
+    // unconditional; the last two rounds test what to consume and refill.
     const int j = lane & 7;  // the lane's sub-block within a super-block
-    auto consume = [&](const Packet* pk, int kk) __attribute__((always_inline)) {
-        float acc = 0.f;
+    const uint32_t ts = 6u * (uint32_t)j, tm = 16u + 6u * (uint32_t)j;
+    const bool sl = ts < 32u, ml = tm < 32u;
+    float sx24[CPW];
 #pragma unroll
-        for (int cc = 0; cc < CPW; ++cc) acc += T::dot(pk[cc], xr[cc], sx[cc], j);
-        const float v = wave_sum_to_lane63(acc);
-        if (lane == kWave - 1) {
+    for (int cc = 0; cc < CPW; ++cc) sx24[cc] = sx[cc] * 5.9604644775390625e-8f;  // 2^-24
+    const int my_d = lane == lane_of<DR>(0) ? 0 : lane == lane_of<DR>(1) ? 1 : lane == lane_of<DR>(2) ? 2
+                   : lane == lane_of<DR>(3) ? 3 : -1;  // the row whose total this lane receives
+    auto round = [&](int s0, bool steady) __attribute__((always_inline)) {
+        float acc[DR];
+#pragma unroll
+        for (int d = 0; d < DR; ++d) {
+            acc[d] = 0.f;
+            if (steady || s0 + d < nr) {
+#pragma unroll
+                for (int cc = 0; cc < CPW; ++cc)
+                    acc[d] = dot24(ring[d][cc], xr[cc], sx24[cc], ts, tm, sl, ml, acc[d]);
+            }
+            if (steady || s0 + d + DR < nr) issue(ring[d]);
+        }
+        const float v = rows_sum<DR>(acc) * 16777216.0f;  // 2^24
+        const int kk = s0 + my_d;
+        if (my_d >= 0 && my_d < DR && kk < nr) {
             if constexpr (WPR == 1)
                 y[rg + kk * rgs] = v;
             else
@@ -597,21 +716,9 @@ __global__ void __launch_bounds__(G * WPR * kWave)
         }
     };
     int s0 = 0;
-    for (; s0 + 2 * DR <= nr; s0 += DR) {
-#pragma unroll
-        for (int d = 0; d < DR; ++d) {
-            consume(ring[d], s0 + d);
-            issue(ring[d]);
-        }
-    }
-#pragma unroll
-    for (int d = 0; d < DR; ++d) {
-        if (s0 + d < nr) consume(ring[d], s0 + d);
-        if (s0 + d + DR < nr) issue(ring[d]);
-    }
-#pragma unroll
-    for (int d = 0; d < DR; ++d)
-        if (s0 + DR + d < nr) consume(ring[d], s0 + DR + d);
+    for (; s0 + 2 * DR <= nr; s0 += DR) round(s0, true);
+    round(s0, false);
+    round(s0 + DR, false);
 
     if constexpr (WPR > 1) {
         __syncthreads();
