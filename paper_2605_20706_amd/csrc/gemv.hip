@@ -32,7 +32,8 @@
 namespace lw {
 namespace {
 
-constexpr int64_t kLdsBytes = 64 * 1024;  // LDS budget of a workgroup (x tile + group sums)
+constexpr int64_t kLdsBytes = 64 * 1024;      // LDS budget of a workgroup (x tile + group sums)
+constexpr int64_t kRegLdsBytes = 128 * 1024;  // of a register-kernel workgroup (one per compute unit or two)
 
 template <int FMT>
 struct Traits;
@@ -240,45 +241,75 @@ struct Traits<LW_Q4_K> {
 // bits of a binary16 half), so no per-step rescaling is needed; the caller
 // multiplies the row total by 2^24 once, after the cross-lane sum (exact:
 // powers of two). sx24 is the lane's group sum of x times 2^-24.
-__device__ __forceinline__ float nibble_dot24(const uint4& c, const float4* xv) {
+//
+// For NTK tokens at once (the masks are shared): out[t] = sum over the lane's
+// 32 elements of q * x_t in units of 2^-24. xv[t] points at token t's 8 float4s.
+template <int NTK>
+__device__ __forceinline__ void nibble_dot24(const uint4& c, const float4* const* xv, float* out) {
     const uint32_t w[4] = {c.x, c.y, c.z, c.w};
-    float lo_s = 0.f, hi_s = 0.f;
+    float lo_s[NTK], hi_s[NTK];
+#pragma unroll
+    for (int t = 0; t < NTK; ++t) lo_s[t] = hi_s[t] = 0.f;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const uint32_t l02 = opaque(w[i] & 0x000F000Fu);
         const uint32_t h02 = opaque(w[i] & 0x00F000F0u);
         const uint32_t l13 = opaque((w[i] >> 8) & 0x000F000Fu);
         const uint32_t h13 = opaque((w[i] >> 8) & 0x00F000F0u);
-        lo_s = __builtin_fmaf(half_of<0>(l02), xv[i].x, lo_s);
-        lo_s = __builtin_fmaf(half_of<1>(l02), xv[i].z, lo_s);
-        lo_s = __builtin_fmaf(half_of<0>(l13), xv[i].y, lo_s);
-        lo_s = __builtin_fmaf(half_of<1>(l13), xv[i].w, lo_s);
-        hi_s = __builtin_fmaf(half_of<0>(h02), xv[4 + i].x, hi_s);
-        hi_s = __builtin_fmaf(half_of<1>(h02), xv[4 + i].z, hi_s);
-        hi_s = __builtin_fmaf(half_of<0>(h13), xv[4 + i].y, hi_s);
-        hi_s = __builtin_fmaf(half_of<1>(h13), xv[4 + i].w, hi_s);
+#pragma unroll
+        for (int t = 0; t < NTK; ++t) {
+            const float4* x4 = xv[t];
+            lo_s[t] = __builtin_fmaf(half_of<0>(l02), x4[i].x, lo_s[t]);
+            lo_s[t] = __builtin_fmaf(half_of<1>(l02), x4[i].z, lo_s[t]);
+            lo_s[t] = __builtin_fmaf(half_of<0>(l13), x4[i].y, lo_s[t]);
+            lo_s[t] = __builtin_fmaf(half_of<1>(l13), x4[i].w, lo_s[t]);
+            hi_s[t] = __builtin_fmaf(half_of<0>(h02), x4[4 + i].x, hi_s[t]);
+            hi_s[t] = __builtin_fmaf(half_of<1>(h02), x4[4 + i].z, hi_s[t]);
+            hi_s[t] = __builtin_fmaf(half_of<0>(h13), x4[4 + i].y, hi_s[t]);
+            hi_s[t] = __builtin_fmaf(half_of<1>(h13), x4[4 + i].w, hi_s[t]);
+        }
     }
-    return __builtin_fmaf(hi_s, 0.0625f, lo_s);  // high nibbles read as 16q
+#pragma unroll
+    for (int t = 0; t < NTK; ++t) out[t] = __builtin_fmaf(hi_s[t], 0.0625f, lo_s[t]);  // high nibbles read as 16q
 }
 
-// acc + (Q4_0 contribution of the lane) * 2^-24: d * (sum q*x - 8 * sum x)
-__device__ __forceinline__ float dot24(const Traits<LW_Q4_0>::Packet& p, const float4* xv, float sx24,
-                                       uint32_t, uint32_t, bool, bool, float acc) {
-    return __builtin_fmaf(half_bits_to_float(p.d), __builtin_fmaf(-8.0f, sx24, nibble_dot24(p.c, xv)), acc);
+// Per-lane constants of the Q4_K-style scale fields: sc_j sits at record bit
+// ts = 6j and m_j at bit 32 + tm, tm = 16 + 6j. A field inside one word is cut
+// out of that word rotated (v_alignbit_b32 of the word with itself), a field
+// across two words out of the pair, so each field takes one select of the low
+// source word, fixed per lane.
+struct SubBlock {
+    uint32_t ts, tm;
+    bool sl, ml;
+    __device__ explicit SubBlock(int j)
+        : ts(6u * (uint32_t)j), tm(16u + 6u * (uint32_t)j), sl(6 * j < 32), ml(16 + 6 * j < 32) {}
+};
+
+// acc[t] += (Q4_0 contribution of the lane for token t) * 2^-24:
+// d * (sum q*x_t - 8 * sum x_t).
+template <int NTK>
+__device__ __forceinline__ void dot24(const Traits<LW_Q4_0>::Packet& p, const float4* const* xv,
+                                      const float* sx24, const SubBlock&, float* acc) {
+    float qx[NTK];
+    nibble_dot24<NTK>(p.c, xv, qx);
+    const float d = half_bits_to_float(p.d);
+#pragma unroll
+    for (int t = 0; t < NTK; ++t) acc[t] = __builtin_fmaf(d, __builtin_fmaf(-8.0f, sx24[t], qx[t]), acc[t]);
 }
 
-// acc + (Q4_K-style contribution) * 2^-24: d*sc_j * sum q*x - dmin*m_j * sum x.
-// sc_j sits at record bit ts = 6j and m_j at bit 32 + tm, tm = 16 + 6j. A
-// field inside one word is cut out of that word rotated (v_alignbit_b32 of
-// the word with itself); a field across two words out of the pair, so each
-// field takes one select of the low source word, fixed per lane.
-__device__ __forceinline__ float dot24(const Traits<LW_Q4_K>::Packet& p, const float4* xv, float sx24,
-                                       uint32_t ts, uint32_t tm, bool sl, bool ml, float acc) {
-    const uint32_t sc_w = __builtin_amdgcn_alignbit(p.r1, sl ? p.r0 : p.r1, ts & 31u);
-    const uint32_t m_w = __builtin_amdgcn_alignbit(p.r2, ml ? p.r1 : p.r2, tm & 31u);
+// acc[t] += (Q4_K-style contribution for token t) * 2^-24:
+// d*sc_j * sum q*x_t - dmin*m_j * sum x_t.
+template <int NTK>
+__device__ __forceinline__ void dot24(const Traits<LW_Q4_K>::Packet& p, const float4* const* xv,
+                                      const float* sx24, const SubBlock& sb, float* acc) {
+    const uint32_t sc_w = __builtin_amdgcn_alignbit(p.r1, sb.sl ? p.r0 : p.r1, sb.ts & 31u);
+    const uint32_t m_w = __builtin_amdgcn_alignbit(p.r2, sb.ml ? p.r1 : p.r2, sb.tm & 31u);
     const float ds = half_bits_to_float(p.dd & 0xFFFFu) * (float)(sc_w & 63u);
     const float dm = half_bits_to_float(p.dd >> 16) * (float)(m_w & 63u);
-    return __builtin_fmaf(-dm, sx24, __builtin_fmaf(ds, nibble_dot24(p.c, xv), acc));
+    float qx[NTK];
+    nibble_dot24<NTK>(p.c, xv, qx);
+#pragma unroll
+    for (int t = 0; t < NTK; ++t) acc[t] = __builtin_fmaf(-dm, sx24[t], __builtin_fmaf(ds, qx[t], acc[t]));
 }
 
 // Sums over the 64 lanes of DR row accumulators at once (v_permlane32_swap /
@@ -591,42 +622,46 @@ __device__ __forceinline__ float sum8_to_last(float v) {
     return v;
 }
 
-// Single-token kernel for the 4-bit formats with the activation held in
-// registers. K is a whole number NC of chunks (2048 elements); a workgroup is
-// G row groups x WPR waves, and wave w of a row group owns chunks
+// Kernel for one to a few tokens over the 4-bit formats with the activation
+// held in registers. K is a whole number NC of chunks (2048 elements); a
+// workgroup is G row groups x WPR waves, and wave w of a row group owns chunks
 // [w*CPW, (w+1)*CPW) of every row of that group (NC = CPW*WPR), so lane l
-// keeps x[c*2048 + 32l : +32] and its group sum for those CPW chunks in VGPRs
-// for the whole kernel and never reads x again. The rows of row group
+// keeps x_t[c*2048 + 32l : +32] and its group sum, for each of the NTK tokens
+// and those CPW chunks, in VGPRs for the whole kernel and never reads x
+// again; the nibble masks of a packet serve all tokens. The rows of row group
 // rg = blockIdx.x*G + g are rg, rg + gridDim.x*G, ...; each wave keeps the
 // packets of its next DR rows in flight (a ring refilled as each row is
-// consumed) and sums DR rows over its 64 lanes at once. With WPR == 1 the
-// wave stores the row totals; with WPR > 1 each wave's per-row partial goes
-// to LDS and the WPR partials of a row are added in wave order after one
-// barrier at the end. x is staged once: coalesced 16-byte loads (issued before the first
-// rows' packets), group sums by DPP over the 8 lanes that hold one group, an
-// LDS tile in which float4 j4 of lane l of chunk c sits at row c*8 + j4,
-// column l ^ j4 (the 8 lanes that stage one group write 8 different bank
-// groups, and the 64 lanes reading one row read 64 different float4s), one
-// barrier, then one read per lane.
-template <int FMT, int CPW, int WPR, int G, int DR>
+// consumed) and sums its DR x NTK (row, token) accumulators over the 64 lanes
+// at once. With WPR == 1 the wave stores the totals; with WPR > 1 each wave's
+// per-row partials go to LDS and the WPR partials of an output are added in
+// wave order after one barrier at the end. x is staged once: coalesced
+// 16-byte loads (issued before the first rows' packets), group sums by DPP
+// over the 8 lanes that hold one group, an LDS tile in which float4 j4 of
+// lane l of chunk c of token t sits at row (t*NC + c)*8 + j4, column l ^ j4
+// (the 8 lanes that stage one group write 8 different bank groups, and the 64
+// lanes reading one row read 64 different float4s), one barrier, then one
+// read per lane.
+template <int FMT, int NTK, int CPW, int WPR, int G, int DR>
 __global__ void __launch_bounds__(G * WPR * kWave)
     gemv1r_kernel(const uint8_t* __restrict__ W, const float* __restrict__ x, float* __restrict__ y,
                   int M, int nr_max, int64_t off1, int64_t off2) {
     using T = Traits<FMT>;
     using Packet = typename T::Packet;
     static_assert(T::EPL == 32 && T::kGroupSums, "4-bit formats only");
-    constexpr int J4 = 8;                    // float4s of x per lane per chunk
-    constexpr int E = kWave * 32;            // elements per chunk
-    constexpr int NC = CPW * WPR;            // chunks per row
+    constexpr int J4 = 8;                      // float4s of x per lane per chunk
+    constexpr int E = kWave * 32;              // elements per chunk
+    constexpr int NC = CPW * WPR;              // chunks per row
     constexpr uint32_t K = (uint32_t)NC * E;
-    constexpr int NT = G * WPR * kWave;      // threads per workgroup
-    constexpr int NQ = (int)(K / 4);         // float4s of x
-    constexpr int XPT = (NQ + NT - 1) / NT;  // x float4s per thread
-    static_assert(NT % kWave == 0 && NQ % 8 == 0, "group sums need whole 8-lane groups");
+    constexpr int NTH = G * WPR * kWave;       // threads per workgroup
+    constexpr int NQ = NTK * (int)(K / 4);     // float4s of x (all tokens)
+    constexpr int XPT = (NQ + NTH - 1) / NTH;  // x float4s per thread
+    constexpr int NR = DR * NTK;               // (row, token) sums per round
+    static_assert(NTH % kWave == 0 && NQ % 8 == 0, "group sums need whole 8-lane groups");
+    static_assert(NR == 1 || NR == 2 || NR == 4, "1, 2 or 4 lane sums per round");
     extern __shared__ float4 smem[];
-    float4* xs = smem;                                       // NQ float4s, lane-interleaved
-    float* sxs = reinterpret_cast<float*>(smem + NQ);        // NC * 64 group sums
-    float* red = sxs + NC * kWave;                           // [G][nr_max][WPR] row partials
+    float4* xs = smem;                                 // NQ float4s
+    float* sxs = reinterpret_cast<float*>(smem + NQ);  // NTK * NC * 64 group sums
+    float* red = sxs + NTK * NC * kWave;               // [G][nr_max][NTK][WPR] partials
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
@@ -640,7 +675,7 @@ __global__ void __launch_bounds__(G * WPR * kWave)
     float4 xv[XPT];
 #pragma unroll
     for (int i = 0; i < XPT; ++i) {
-        const int q = tid + i * NT;
+        const int q = tid + i * NTH;
         xv[i] = *reinterpret_cast<const float4*>(x + 4 * (q < NQ ? q : NQ - 1));
     }
 
@@ -661,58 +696,68 @@ __global__ void __launch_bounds__(G * WPR * kWave)
 #pragma unroll
     for (int d = 0; d < DR; ++d) issue(ring[d]);
 
-    // (3) x into LDS with its group sums, one barrier, then this lane's slices
+    // (3) x into LDS with its group sums, one barrier, then this lane's slices.
+    // Float4 q of x is token q / (K/4), chunk (q mod K/4) / 512 of it.
 #pragma unroll
     for (int i = 0; i < XPT; ++i) {
-        const int q = tid + i * NT;
-        const int c = q / (E / 4), rem = q - c * (E / 4), l = rem / J4, j4 = rem - l * J4;
+        const int q = tid + i * NTH;
+        const int tc = q / (E / 4), rem = q - tc * (E / 4), l = rem / J4, j4 = rem - l * J4;
         const float s = sum8_to_last((xv[i].x + xv[i].y) + (xv[i].z + xv[i].w));
         if (q < NQ) {
-            xs[(c * J4 + j4) * kWave + (l ^ j4)] = xv[i];
+            xs[(tc * J4 + j4) * kWave + (l ^ j4)] = xv[i];
             if ((tid & 7) == 7) sxs[q / J4] = s;
         }
     }
     __syncthreads();
-    float4 xr[CPW][J4];
-    float sx[CPW];
+    float4 xr[NTK][CPW][J4];
+    float sx24[NTK][CPW];
 #pragma unroll
-    for (int cc = 0; cc < CPW; ++cc) {
-        const int c = w * CPW + cc;
+    for (int t = 0; t < NTK; ++t)
 #pragma unroll
-        for (int j4 = 0; j4 < J4; ++j4) xr[cc][j4] = xs[(c * J4 + j4) * kWave + (lane ^ j4)];
-        sx[cc] = sxs[c * kWave + lane];
-    }
+        for (int cc = 0; cc < CPW; ++cc) {
+            const int tc = t * NC + w * CPW + cc;
+#pragma unroll
+            for (int j4 = 0; j4 < J4; ++j4) xr[t][cc][j4] = xs[(tc * J4 + j4) * kWave + (lane ^ j4)];
+            sx24[t][cc] = sxs[tc * kWave + lane] * 5.9604644775390625e-8f;  // 2^-24
+        }
 
     // (4) consume rows in order, DR at a time, refilling each ring slot DR
     // rows ahead. Steady rounds refill only real rows, so their loads are
     // unconditional; the last two rounds test what to consume and refill.
-    const int j = lane & 7;  // the lane's sub-block within a super-block
-    const uint32_t ts = 6u * (uint32_t)j, tm = 16u + 6u * (uint32_t)j;
-    const bool sl = ts < 32u, ml = tm < 32u;
-    float sx24[CPW];
+    const SubBlock sb(lane & 7);  // the lane's sub-block within a super-block
+    int my_i = -1;  // the (row, token) sum this lane receives: i = d * NTK + t
 #pragma unroll
-    for (int cc = 0; cc < CPW; ++cc) sx24[cc] = sx[cc] * 5.9604644775390625e-8f;  // 2^-24
-    const int my_d = lane == lane_of<DR>(0) ? 0 : lane == lane_of<DR>(1) ? 1 : lane == lane_of<DR>(2) ? 2
-                   : lane == lane_of<DR>(3) ? 3 : -1;  // the row whose total this lane receives
+    for (int i = 0; i < NR; ++i)
+        if (lane == lane_of<NR>(i)) my_i = i;
+    const int my_d = my_i / NTK, my_t = my_i - my_d * NTK;
     auto round = [&](int s0, bool steady) __attribute__((always_inline)) {
-        float acc[DR];
+        float acc[NR];
 #pragma unroll
         for (int d = 0; d < DR; ++d) {
-            acc[d] = 0.f;
+#pragma unroll
+            for (int t = 0; t < NTK; ++t) acc[d * NTK + t] = 0.f;
             if (steady || s0 + d < nr) {
 #pragma unroll
-                for (int cc = 0; cc < CPW; ++cc)
-                    acc[d] = dot24(ring[d][cc], xr[cc], sx24[cc], ts, tm, sl, ml, acc[d]);
+                for (int cc = 0; cc < CPW; ++cc) {
+                    const float4* xp[NTK];
+                    float s24[NTK];
+#pragma unroll
+                    for (int t = 0; t < NTK; ++t) {
+                        xp[t] = xr[t][cc];
+                        s24[t] = sx24[t][cc];
+                    }
+                    dot24<NTK>(ring[d][cc], xp, s24, sb, acc + d * NTK);
+                }
             }
             if (steady || s0 + d + DR < nr) issue(ring[d]);
         }
-        const float v = rows_sum<DR>(acc) * 16777216.0f;  // 2^24
+        const float v = rows_sum<NR>(acc) * 16777216.0f;  // 2^24
         const int kk = s0 + my_d;
-        if (my_d >= 0 && my_d < DR && kk < nr) {
+        if (my_i >= 0 && kk < nr) {
             if constexpr (WPR == 1)
-                y[rg + kk * rgs] = v;
+                y[(int64_t)my_t * M + rg + kk * rgs] = v;
             else
-                red[(g * nr_max + kk) * WPR + w] = v;
+                red[((g * nr_max + kk) * NTK + my_t) * WPR + w] = v;
         }
     };
     int s0 = 0;
@@ -722,14 +767,15 @@ __global__ void __launch_bounds__(G * WPR * kWave)
 
     if constexpr (WPR > 1) {
         __syncthreads();
-        for (int idx = tid; idx < G * nr_max; idx += NT) {
-            const int gg = idx / nr_max, ii = idx - gg * nr_max;
+        for (int idx = tid; idx < G * nr_max * NTK; idx += NTH) {
+            const int t = idx % NTK, gi = idx / NTK;
+            const int gg = gi / nr_max, ii = gi - gg * nr_max;
             const int64_t row = (int64_t)blockIdx.x * G + gg + (int64_t)ii * rgs;
             if (row < M) {
                 float s = 0.f;
 #pragma unroll
                 for (int ww = 0; ww < WPR; ++ww) s += red[idx * WPR + ww];
-                y[row] = s;
+                y[(int64_t)t * M + row] = s;
             }
         }
     }
@@ -802,8 +848,8 @@ hipError_t launch_single(const uint8_t* W, const float* x, float* y, int64_t M, 
 
 // Register-resident-x kernel: G row groups x WPR waves per workgroup, at most
 // CAP workgroups per compute unit. Returns hipErrorNotSupported when the shape
-// does not fit it (the caller then uses the LDS kernel).
-template <int FMT, int CPW, int WPR, int G, int DR, int CAP>
+// does not fit it (the caller then uses another kernel).
+template <int FMT, int NTK, int CPW, int WPR, int G, int DR, int CAP>
 hipError_t launch_reg(const uint8_t* W, const float* x, float* y, int64_t M, const Planes& p,
                       hipStream_t stream) {
     constexpr int64_t NC = CPW * WPR;
@@ -813,41 +859,41 @@ hipError_t launch_reg(const uint8_t* W, const float* x, float* y, int64_t M, con
     const int64_t cap = CAP * (int64_t)cu_count();
     if (grid > cap) grid = cap;
     const int64_t nr_max = (M + grid * G - 1) / (grid * G);
-    const int64_t lds = K * 4 + NC * kWave * 4 + (WPR > 1 ? G * nr_max * WPR * 4 : 0);
-    if (lds > kLdsBytes) return hipErrorNotSupported;
-    hipLaunchKernelGGL((gemv1r_kernel<FMT, CPW, WPR, G, DR>), dim3((unsigned)grid), dim3(G * WPR * kWave),
-                       (size_t)lds, stream, W, x, y, (int)M, (int)nr_max, p.off1, p.off2);
+    const int64_t lds = NTK * (K * 4 + NC * kWave * 4) + (WPR > 1 ? G * nr_max * NTK * WPR * 4 : 0);
+    if (lds > kRegLdsBytes) return hipErrorNotSupported;
+    hipLaunchKernelGGL((gemv1r_kernel<FMT, NTK, CPW, WPR, G, DR>), dim3((unsigned)grid),
+                       dim3(G * WPR * kWave), (size_t)lds, stream, W, x, y, (int)M, (int)nr_max, p.off1, p.off2);
     return hipGetLastError();
 }
 
-// Kernel selection for one token over the 4-bit formats, by the number of
-// 2048-element chunks per row (K / 2048) and the row count. The register
-// kernel needs a few rows per wave to pay for staging x whole; below that
-// (and for other K) the LDS kernel, which spreads single chunks over the
-// waves, is faster.
+// Kernel selection for the register kernel over the 4-bit formats, by token
+// count, the number of 2048-element chunks per row (K / 2048) and the row
+// count. With one token the register kernel needs a few rows per wave to pay
+// for staging x whole; below that (and for other K) the LDS kernel, which
+// spreads single chunks over the waves, is faster.
 template <int FMT>
-hipError_t launch_single_q4(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
-                            const Planes& p, hipStream_t stream) {
-    hipError_t err = hipErrorNotSupported;
-    if (K % 2048 == 0) {
-        switch (K / 2048) {
-        case 1: err = launch_reg<FMT, 1, 1, 8, 2, 2>(W, x, y, M, p, stream); break;
-        case 2:
-            if (M >= 10240) err = launch_reg<FMT, 2, 1, 8, 2, 2>(W, x, y, M, p, stream);
-            break;
-        case 7: err = launch_reg<FMT, 1, 7, 2, 2, 1>(W, x, y, M, p, stream); break;
-        default: break;
-        }
+hipError_t launch_reg_fmt(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
+                          const Planes& p, hipStream_t stream) {
+    if (K % 2048) return hipErrorNotSupported;
+    const int64_t nc = K / 2048;
+    if (n_tok == 1) {
+        if (nc == 1) return launch_reg<FMT, 1, 1, 1, 8, 2, 2>(W, x, y, M, p, stream);
+        if (nc == 2 && M >= 10240) return launch_reg<FMT, 1, 2, 1, 8, 2, 2>(W, x, y, M, p, stream);
+        if (nc == 7) return launch_reg<FMT, 1, 1, 7, 2, 2, 1>(W, x, y, M, p, stream);
+    } else if (n_tok == 2) {
+        if (nc == 1) return launch_reg<FMT, 2, 1, 1, 8, 2, 2>(W, x, y, M, p, stream);
+        if (nc == 2) return launch_reg<FMT, 2, 1, 2, 4, 2, 2>(W, x, y, M, p, stream);
+        if (nc == 4) return launch_reg<FMT, 2, 1, 4, 2, 2, 1>(W, x, y, M, p, stream);
+        if (nc == 7) return launch_reg<FMT, 2, 1, 7, 2, 2, 1>(W, x, y, M, p, stream);
     }
-    if (err != hipErrorNotSupported) return err;
-    return launch_single<FMT, 1, 2>(W, x, y, M, K, p, stream);
+    return hipErrorNotSupported;
 }
 
 template <int FMT>
 hipError_t launch_fmt(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                       int64_t n_tok, const Planes& p, hipStream_t stream) {
     if (n_tok == 1) {
-        if constexpr (FMT == LW_Q4_0 || FMT == LW_Q4_K) return launch_single_q4<FMT>(W, x, y, M, K, p, stream);
+        if constexpr (FMT == LW_Q4_0 || FMT == LW_Q4_K) return launch_single<FMT, 1, 2>(W, x, y, M, K, p, stream);
 
         return launch_single<FMT, 2, 2>(W, x, y, M, K, p, stream);
     }
@@ -876,6 +922,15 @@ hipError_t launch_fmt(const uint8_t* W, const float* x, float* y, int64_t M, int
 }
 
 }  // namespace
+
+hipError_t launch_gemv_reg(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
+                           int64_t n_tok, const Planes& p, hipStream_t stream) {
+    switch (fmt) {
+    case LW_Q4_0: return launch_reg_fmt<LW_Q4_0>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q4_K: return launch_reg_fmt<LW_Q4_K>(W, x, y, M, K, n_tok, p, stream);
+    default: return hipErrorNotSupported;
+    }
+}
 
 hipError_t launch_gemv(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                        int64_t n_tok, const Planes& p, hipStream_t stream) {

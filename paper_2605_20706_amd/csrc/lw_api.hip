@@ -2,12 +2,15 @@
 //
 // Every check runs on the host before any HIP call, in the documented order
 // (format, values, shape, alignment); a call that fails a check launches
-// nothing. Dispatch: one token -> the VALU matrix-vector kernel; 2..16 tokens
-// over the 4-bit formats -> the matrix-core kernel with a block-diagonal
-// activation operand; Q8_0 with up to LW_GEMV_MAX_TOK tokens -> the VALU
-// kernels, up to 16 -> the matrix-core kernel with K split across waves; more
-// tokens -> the tiled matrix-core (prefill) kernel. f16 weights use the VALU
-// kernel in token blocks of LW_GEMV_MAX_TOK for any token count.
+// nothing. Dispatch: one or two tokens over the 4-bit formats with K a
+// multiple of 2048 -> the VALU matrix-vector kernel with the activation in
+// registers, where its table has an entry for the shape; else one token ->
+// the VALU matrix-vector kernel with the activation in LDS; 2..16 tokens over
+// the 4-bit formats -> the matrix-core kernel with a block-diagonal activation
+// operand; Q8_0 with up to LW_GEMV_MAX_TOK tokens -> the VALU kernels, up to
+// 16 -> the matrix-core kernel with K split across waves; more tokens -> the
+// tiled matrix-core (prefill) kernel. f16 weights use the VALU kernel in
+// token blocks of LW_GEMV_MAX_TOK for any token count.
 #include "lw_internal.hpp"
 
 namespace {
@@ -50,16 +53,19 @@ int lw_matvec(int fmt, const void* W, const float* x, float* y, int64_t M, int64
     if (!aligned(W, 256) || !aligned(x, 16) || !aligned(y, 16)) return LW_EALIGN;
     const lw::Planes p = lw::planes_of(fmt, M * K);
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    hipError_t err;
+    hipError_t err = hipErrorNotSupported;
     const uint8_t* Wb = static_cast<const uint8_t*>(W);
-    if (n_tok > 1 && lw::multitok_supported(fmt, n_tok))
-        err = lw::launch_multitok(fmt, Wb, x, y, M, K, n_tok, p, s);
-    else if (n_tok <= LW_GEMV_MAX_TOK)
-        err = lw::launch_gemv(fmt, Wb, x, y, M, K, n_tok, p, s);
-    else if (n_tok <= 16 && lw::skinny_supported(fmt))
-        err = lw::launch_skinny(fmt, Wb, x, y, M, K, n_tok, p, s);
-    else
-        err = lw::launch_prefill(fmt, Wb, x, y, M, K, n_tok, p, s);
+    if (n_tok <= 2) err = lw::launch_gemv_reg(fmt, Wb, x, y, M, K, n_tok, p, s);
+    if (err == hipErrorNotSupported) {
+        if (n_tok > 1 && lw::multitok_supported(fmt, n_tok))
+            err = lw::launch_multitok(fmt, Wb, x, y, M, K, n_tok, p, s);
+        else if (n_tok <= LW_GEMV_MAX_TOK)
+            err = lw::launch_gemv(fmt, Wb, x, y, M, K, n_tok, p, s);
+        else if (n_tok <= 16 && lw::skinny_supported(fmt))
+            err = lw::launch_skinny(fmt, Wb, x, y, M, K, n_tok, p, s);
+        else
+            err = lw::launch_prefill(fmt, Wb, x, y, M, K, n_tok, p, s);
+    }
     return err == hipSuccess ? LW_OK : LW_EHIP;
 }
 

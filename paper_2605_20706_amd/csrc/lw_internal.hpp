@@ -48,6 +48,11 @@ hipError_t launch_dequant(int fmt, const uint8_t* W, float* out, int64_t n, cons
                           hipStream_t stream);
 hipError_t launch_gemv(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                        int64_t n_tok, const Planes& p, hipStream_t stream);
+// Register-resident-activation kernel (4-bit formats, one or two tokens, K a
+// multiple of 2048 with a table entry); hipErrorNotSupported when the shape
+// is not one it takes.
+hipError_t launch_gemv_reg(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
+                           int64_t n_tok, const Planes& p, hipStream_t stream);
 // Matrix-core path for 2 <= n_tok <= 16 with streamed weights (4-bit and 8-bit formats).
 bool skinny_supported(int fmt);
 hipError_t launch_skinny(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,

@@ -52,23 +52,25 @@ def test_parity_many_rows(oracle_mod, fmt):
         gate.check(y, y_ref[:nt], A[:nt], f32_bound=1e-4, what=(fmt, M, K, nt))
 
 
-# One token over the 4-bit formats with K a whole number of 2048-element
-# chunks (1, 2, 4 or 7 chunks per row): row counts from a single row to
-# enough rows that every wave runs several full rounds of its row ring, with
-# ragged row groups at the end.
+# One and two tokens over the 4-bit formats with K a whole number of
+# 2048-element chunks (1, 2, 4 or 7 chunks per row): row counts from a single
+# row to enough rows that every wave runs several full rounds of its row
+# ring, with ragged row groups at the end.
 REG_SHAPES = [(1, 2048), (40000, 2048), (9, 4096), (16500, 4096), (5, 8192), (8300, 8192),
               (1, 14336), (3500, 14336)]
 
 
 @pytest.mark.parametrize("fmt", [Q4_0, Q4_K])
 @pytest.mark.parametrize("M,K", REG_SHAPES)
-def test_parity_one_token_whole_chunks(oracle_mod, fmt, M, K):
+def test_parity_whole_chunks(oracle_mod, fmt, M, K):
     W = synth.gen_packed(fmt, M * K, np.random.default_rng([fmt, M, K, 5]))
-    x = synth.gen_x_seeded([13, fmt, M, K], K, 1)
+    Wg = to_gpu(W)
+    x = synth.gen_x_seeded([13, fmt, M, K], K, 2)
     y_ref, A, _ = oracle_mod.matvec(fmt, W, x, M, K)
-    print("matvec fmt=%d M=%d K=%d n_tok=1" % (fmt, M, K), flush=True)
-    y = gpu_matvec(fmt, W, x, M, K)
-    gate.check(y, y_ref, A, f32_bound=1e-4, what=(fmt, M, K, 1))
+    for nt in (1, 2):
+        print("matvec fmt=%d M=%d K=%d n_tok=%d" % (fmt, M, K, nt), flush=True)
+        y = gpu_matvec(fmt, W, x[:nt], M, K, Wg=Wg)
+        gate.check(y, y_ref[:nt], A[:nt], f32_bound=1e-4, what=(fmt, M, K, nt))
 
 
 @pytest.mark.parametrize("fmt", FMTS)
