@@ -312,16 +312,26 @@ __device__ __forceinline__ void dot24(const Traits<LW_Q4_K>::Packet& p, const fl
     for (int t = 0; t < NTK; ++t) acc[t] = __builtin_fmaf(-dm, sx24[t], __builtin_fmaf(ds, qx[t], acc[t]));
 }
 
-// Sums over the 64 lanes of DR row accumulators at once (v_permlane32_swap /
-// v_permlane16_swap fold the halves of several rows into one register, then
-// DPP adds finish inside 16-lane rows). DR = 1: the total is in lane 63.
-// DR = 2: row 0 in lane 31, row 1 in lane 63. DR = 4: rows 0, 2, 1, 3 in
-// lanes 15, 31, 47, 63. lane_of<DR>(d) gives the lane of row d.
-template <int DR>
-__device__ __forceinline__ int lane_of(int d) {
-    if constexpr (DR == 1) return 63;
-    else if constexpr (DR == 2) return 32 * d + 31;
-    else return 16 * (2 * (d & 1) + (d >> 1)) + 15;
+// Sums over the 64 lanes of NR accumulators at once: v_permlane32_swap and
+// v_permlane16_swap fold the halves of different accumulators into one
+// register, then DPP adds finish inside 16-lane (or 8-lane) rows. NR is
+// padded with zeros to 1, 2, 4 or 8. The total of accumulator i lands in lane
+// lane_of<NR>(i) of the returned register: NR = 1: lane 63; NR = 2: lanes 31,
+// 63; NR = 4: lanes 15, 47, 31, 63; NR = 8: lanes 7, 39, 23, 55 (i < 4) and
+// 15, 47, 31, 63 (i >= 4).
+template <int NR>
+constexpr int padded_rows() {
+    return NR <= 1 ? 1 : NR <= 2 ? 2 : NR <= 4 ? 4 : 8;
+}
+
+template <int NR>
+__device__ __forceinline__ int lane_of(int i) {
+    constexpr int P = padded_rows<NR>();
+    const int r16 = 2 * (i & 1) + ((i >> 1) & 1);  // 16-lane row of accumulator i (P = 4, 8)
+    if constexpr (P == 1) return 63;
+    else if constexpr (P == 2) return 32 * i + 31;
+    else if constexpr (P == 4) return 16 * r16 + 15;
+    else return 16 * r16 + (i < 4 ? 7 : 15);
 }
 
 __device__ __forceinline__ float fswap32(float a, float b, float& hi) {
@@ -338,33 +348,52 @@ __device__ __forceinline__ float fswap16(float a, float b, float& odd) {
     return __builtin_bit_cast(float, (uint32_t)s[0]);
 }
 
-template <int DR>
+// Four accumulators -> one register whose 16-lane rows hold accumulators 0,
+// 2, 1, 3, each folded to 16 lanes.
+__device__ __forceinline__ float fold4(float a0, float a1, float a2, float a3) {
+    float h01, h23, o;
+    const float l01 = fswap32(a0, a1, h01);
+    const float l23 = fswap32(a2, a3, h23);
+    const float e = fswap16(l01 + h01, l23 + h23, o);
+    return e + o;
+}
+
+template <int NR>
 __device__ __forceinline__ float rows_sum(const float* acc) {
-    if constexpr (DR == 1) {
-        return wave_sum_to_lane63(acc[0]);
-    } else if constexpr (DR == 2) {
+    constexpr int P = padded_rows<NR>();
+    float a[P];
+#pragma unroll
+    for (int i = 0; i < P; ++i) a[i] = i < NR ? acc[i] : 0.f;
+    if constexpr (P == 1) {
+        return wave_sum_to_lane63(a[0]);
+    } else if constexpr (P == 2) {
         float h;
-        const float l = fswap32(acc[0], acc[1], h);
-        float v = l + h;  // lanes 0-31: row 0 folded to 32 lanes; 32-63: row 1
+        const float l = fswap32(a[0], a[1], h);
+        float v = l + h;  // lanes 0-31: accumulator 0 folded to 32 lanes; 32-63: accumulator 1
         v += dpp_move<0x111>(v);
         v += dpp_move<0x112>(v);
         v += dpp_move<0x114>(v);
         v += dpp_move<0x118>(v);
         v += dpp_move<0x142, 0xA>(v);  // row_bcast:15 into rows 1 and 3
         return v;
-    } else {
-        static_assert(DR == 4, "1, 2 or 4 rows");
-        float h01, h23;
-        const float l01 = fswap32(acc[0], acc[1], h01);
-        const float l23 = fswap32(acc[2], acc[3], h23);
-        const float a = l01 + h01, b = l23 + h23;  // [row0 | row1] and [row2 | row3], 32 lanes each
-        float o;
-        const float e = fswap16(a, b, o);
-        float v = e + o;  // 16-lane rows: row 0, row 2, row 1, row 3
+    } else if constexpr (P == 4) {
+        float v = fold4(a[0], a[1], a[2], a[3]);
         v += dpp_move<0x111>(v);
         v += dpp_move<0x112>(v);
         v += dpp_move<0x114>(v);
         v += dpp_move<0x118>(v);
+        return v;
+    } else {
+        const float r0 = fold4(a[0], a[1], a[2], a[3]);
+        const float r1 = fold4(a[4], a[5], a[6], a[7]);
+        // lanes 0-7 of each 16-lane row fold r0's row, lanes 8-15 fold r1's
+        // (row_ror:8 brings the other half of the row)
+        const bool upper = (__lane_id() & 8) != 0;
+        const float t = upper ? r1 : r0, u = upper ? r0 : r1;
+        float v = t + dpp_move<0x128>(u);
+        v += dpp_move<0x111>(v);
+        v += dpp_move<0x112>(v);
+        v += dpp_move<0x114>(v);
         return v;
     }
 }
@@ -657,7 +686,7 @@ __global__ void __launch_bounds__(G * WPR * kWave)
     constexpr int XPT = (NQ + NTH - 1) / NTH;  // x float4s per thread
     constexpr int NR = DR * NTK;               // (row, token) sums per round
     static_assert(NTH % kWave == 0 && NQ % 8 == 0, "group sums need whole 8-lane groups");
-    static_assert(NR == 1 || NR == 2 || NR == 4, "1, 2 or 4 lane sums per round");
+    static_assert(NR <= 8, "at most 8 lane sums per round");
     extern __shared__ float4 smem[];
     float4* xs = smem;                                 // NQ float4s
     float* sxs = reinterpret_cast<float*>(smem + NQ);  // NTK * NC * 64 group sums

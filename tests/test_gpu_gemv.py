@@ -52,7 +52,8 @@ def test_parity_many_rows(oracle_mod, fmt):
         gate.check(y, y_ref[:nt], A[:nt], f32_bound=1e-4, what=(fmt, M, K, nt))
 
 
-# One and two tokens over the 4-bit formats with K a whole number of
+# One to four tokens (the register kernel takes one or two, the matrix-core
+# kernel more) over the 4-bit formats with K a whole number of
 # 2048-element chunks (1, 2, 4 or 7 chunks per row): row counts from a single
 # row to enough rows that every wave runs several full rounds of its row
 # ring, with ragged row groups at the end.
@@ -65,9 +66,9 @@ REG_SHAPES = [(1, 2048), (40000, 2048), (9, 4096), (16500, 4096), (5, 8192), (83
 def test_parity_whole_chunks(oracle_mod, fmt, M, K):
     W = synth.gen_packed(fmt, M * K, np.random.default_rng([fmt, M, K, 5]))
     Wg = to_gpu(W)
-    x = synth.gen_x_seeded([13, fmt, M, K], K, 2)
+    x = synth.gen_x_seeded([13, fmt, M, K], K, 4)
     y_ref, A, _ = oracle_mod.matvec(fmt, W, x, M, K)
-    for nt in (1, 2):
+    for nt in (1, 2, 3, 4):
         print("matvec fmt=%d M=%d K=%d n_tok=%d" % (fmt, M, K, nt), flush=True)
         y = gpu_matvec(fmt, W, x[:nt], M, K, Wg=Wg)
         gate.check(y, y_ref[:nt], A[:nt], f32_bound=1e-4, what=(fmt, M, K, nt))
