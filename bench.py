@@ -9,8 +9,10 @@ and resident in HBM before the timed region starts.
 
 Printed (one JSON line): HBM GB/s from algorithmic bytes (packed W + x + y),
 its fraction of the 8 TB/s peak, the equivalent decode tokens/s, a roofline
-object for the GEMV kernel from per-launch HIP events, and the CPU oracle timed
-on a bounded sample of the same workload on this host.
+object for the kernel that takes most of a step (from HIP events around
+back-to-back launches of each matrix shape; lw_kernel_name says which kernel
+each shape runs), and the CPU oracle timed on a bounded sample of the same
+workload on this host.
 
 Usage: python bench.py [--workload q4_k_llama8b] [--steps K] [--warmup W]
 """
@@ -153,30 +155,17 @@ def run_gpu(ws, steps, warmup, mode):
     return ms_per_step, per_shape
 
 
-def kernel_of(fmt, n_tok):
-    """Kernel lw_matvec runs for (fmt, n_tok) -- a label that follows the
-    dispatch in lw_api.hip --, whether it is a matrix-core kernel, and the
-    sources that define it."""
-    name = layout.FORMAT_NAMES[fmt]
-    if n_tok == 1:
-        return "gemv1_kernel<%s>" % name, False, ["gemv.hip"]
-    if n_tok <= 16 and fmt in (layout.Q4_0, layout.Q4_K):
-        return "multitok_kernel<%s, NTS=%d>" % (name, (n_tok + 3) // 4), True, ["multitok.hip"]
-    if n_tok <= 8 or fmt == layout.F16:
-        return "gemv_kernel<%s, NT=%d>" % (name, min(n_tok, 8)), False, ["gemv.hip"]
-    if n_tok <= 16:
-        return "skinny_kernel<%s>" % name, True, ["skinny.hip"]
-    return "gemm_kernel<%s>" % name, True, ["prefill.hip"]
+MFMA_KERNELS = ("gemm_kernel", "multitok_kernel", "skinny_kernel")
 
 
-def source_hash(fmt, n_tok):
-    """sha256 over the sources of the kernel that (fmt, n_tok) runs, with the
-    shared device helpers and the C header: a stored HBM traffic figure is valid
-    only for the sources it was measured on."""
+def source_hash():
+    """sha256 over every kernel source, the device helpers and the C header: a
+    stored HBM traffic figure is valid only for the sources it was measured on."""
+    import glob
     import hashlib
 
     h = hashlib.sha256()
-    files = [os.path.join(CSRC, f) for f in kernel_of(fmt, n_tok)[2] + ["lw_device.hpp"]]
+    files = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.hpp")))
     files.append(os.path.join(ROOT, "include", "lw.h"))
     for f in files:
         h.update(os.path.basename(f).encode())
@@ -185,9 +174,9 @@ def source_hash(fmt, n_tok):
     return h.hexdigest()
 
 
-def stored_traffic(workload, fmt, n_tok):
-    """HBM bytes per launch from the calibrated rocprofv3 FETCH_SIZE and
-    WRITE_SIZE summary in profiles/, or None when there is none for these
+def stored_traffic(workload, n_tok, kernel):
+    """HBM bytes per launch of `kernel` from the calibrated rocprofv3 FETCH_SIZE
+    and WRITE_SIZE summary in profiles/, or None when there is none for these
     sources."""
     path = os.path.join(ROOT, "profiles", "hbm_traffic_%s_nt%d.txt" % (workload, n_tok))
     if not os.path.exists(path):
@@ -198,12 +187,27 @@ def stored_traffic(workload, fmt, n_tok):
             if "=" in line and not line.startswith((" ", "#", "|")):
                 k, v = line.strip().split("=", 1)
                 vals[k.strip()] = v.strip()
-    if vals.get("source_sha256") != source_hash(fmt, n_tok):
+    if vals.get("source_sha256") != source_hash():
         return None
     try:
-        return float(vals["hbm_bytes_per_launch"])
+        return float(vals["hbm_bytes_per_launch[%s]" % kernel])
     except (KeyError, ValueError):
         return None
+
+
+def kernel_groups(ws, per_shape):
+    """Launches of a step grouped by the kernel the library selects for them
+    (lw_kernel_name), with each group's time per step from the per-shape
+    launch durations: {kernel: {launches, us, bytes, flop}}."""
+    names = [binding.kernel_name(ws.wl.fmt, m.M, m.K, ws.n_tok) for m in ws.mats]
+    groups = {}
+    for _, (ms, idx) in per_shape.items():
+        g = groups.setdefault(names[idx[0]], {"launches": 0, "us": 0.0, "bytes": 0.0, "flop": 0.0})
+        g["launches"] += len(idx)
+        g["us"] += ms * 1e3 * len(idx)
+        g["bytes"] += sum(ws.alg_bytes[i] for i in idx)
+        g["flop"] += sum(ws.flops[i] for i in idx)
+    return names, groups
 
 
 def cpu_baseline(ws, budget_s):
@@ -281,27 +285,35 @@ def main():
     step_bytes = sum(ws.alg_bytes)
     gbs = step_bytes / (ms_per_step * 1e-3) / 1e9
     tok_s = args.n_tok / (ms_per_step * 1e-3)
-    # every launch of a step runs the same kernel; its average launch duration
-    # is the timed region over the launches it holds
-    avg_launch_s = ms_per_step * 1e-3 / n_launch
     fmt_name = layout.FORMAT_NAMES[wl.fmt]
-    kname, mfma, _ = kernel_of(wl.fmt, args.n_tok)
+    # the roofline of the kernel that takes most of a step: its algorithmic
+    # bytes (or flops) per launch over its average launch duration, both from
+    # the per-shape phase (HIP events around back-to-back launches of one
+    # shape on the launch stream)
+    names, groups = kernel_groups(ws, per_shape)
+    kname = max(groups, key=lambda k: groups[k]["us"])
+    g = groups[kname]
+    mfma = kname.startswith(MFMA_KERNELS)
+    avg_launch_s = g["us"] * 1e-6 / g["launches"]
     if mfma:
-        kern_tfs = sum(ws.flops) / n_launch / avg_launch_s / 1e12
+        kern_tfs = g["flop"] / (g["us"] * 1e-6) / 1e12
         roof = {"bound": "mfma", "achieved": round(kern_tfs, 2), "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
                 "frac": round(kern_tfs / MFMA_BF16_PEAK_TFS, 4)}
     else:
-        kern_gbs = step_bytes / n_launch / avg_launch_s / 1e9
+        kern_gbs = g["bytes"] / (g["us"] * 1e-6) / 1e9
         roof = {"bound": "hbm", "achieved": round(kern_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(kern_gbs / HBM_PEAK_GBS, 4)}
-    roof.update({"traffic": stored_traffic(wl.key, wl.fmt, args.n_tok), "kernel": kname,
-                 "launches_per_step": n_launch, "avg_launch_us": round(avg_launch_s * 1e6, 3),
-                 "alg_bytes_per_launch": round(step_bytes / n_launch),
-                 "alg_flop_per_launch": round(sum(ws.flops) / n_launch)})
+    roof.update({"traffic": stored_traffic(wl.key, args.n_tok, kname), "kernel": kname,
+                 "launches_per_step": g["launches"], "avg_launch_us": round(avg_launch_s * 1e6, 3),
+                 "alg_bytes_per_launch": round(g["bytes"] / g["launches"]),
+                 "alg_flop_per_launch": round(g["flop"] / g["launches"]),
+                 "share_of_step": round(g["us"] / sum(v["us"] for v in groups.values()), 4)})
+    kernels_out = {k: {"launches": v["launches"], "us_per_step": round(v["us"], 1),
+                       "GB/s": round(v["bytes"] / (v["us"] * 1e-6) / 1e9, 1)} for k, v in groups.items()}
     shape_out = {}
     for k, (ms, idx) in per_shape.items():
         b = ws.alg_bytes[idx[0]]
-        shape_out[k] = {"us": round(ms * 1e3, 2), "GB/s": round(b / (ms * 1e-3) / 1e9, 1)}
+        shape_out[k] = {"us": round(ms * 1e3, 2), "GB/s": round(b / (ms * 1e-3) / 1e9, 1), "kernel": names[idx[0]]}
         if mfma:
             shape_out[k]["TFLOP/s"] = round(ws.flops[idx[0]] / (ms * 1e-3) / 1e12, 1)
     out = {
@@ -315,6 +327,7 @@ def main():
         "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
         "equiv_decode_tok_s": round(tok_s, 1),
         "roofline": roof,
+        "kernels": kernels_out,
         "per_shape": shape_out,
     }
     if not args.no_cpu_baseline:

@@ -135,6 +135,23 @@ int64_t lw_weight_bytes(int fmt, int64_t n);
 /* lw_strerror — static, NUL-terminated description of a return code. */
 const char* lw_strerror(int code);
 
+/*
+ * lw_kernel_name — the kernel lw_matvec(fmt, W, x, y, M, K, n_tok, stream)
+ * would launch for these sizes (the first one, where the call launches
+ * several), as the template part of its name, e.g. "gemv1r_kernel<3, 1, 2, 1,
+ * 8, 2>": the static kernel-selection table of Sec. 3.3 (ahead-of-time
+ * instantiations chosen per shape) made visible to profilers and tests.
+ *
+ *   fmt, M, K, n_tok  as for lw_matvec.
+ *
+ * Returns NULL when these arguments would fail lw_matvec's checks on format,
+ * sizes or shape. The string is owned by the library and valid until the
+ * process ends. Host-only: launches nothing and touches no device memory;
+ * the selection may depend on the compute-unit count of the current device
+ * (256 when there is none).
+ */
+const char* lw_kernel_name(int fmt, int64_t M, int64_t K, int64_t n_tok);
+
 #ifdef __cplusplus
 }
 #endif

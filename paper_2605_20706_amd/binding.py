@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "liblw.so")
 
 LW_OK = 0
-EXPORTS = ("lw_matvec", "lw_dequant", "lw_weight_bytes", "lw_strerror")
+EXPORTS = ("lw_matvec", "lw_dequant", "lw_weight_bytes", "lw_strerror", "lw_kernel_name")
 
 
 class LwError(RuntimeError):
@@ -44,6 +44,8 @@ def library() -> ctypes.CDLL:
         lib.lw_weight_bytes.restype = i64
         lib.lw_strerror.argtypes = [ctypes.c_int]
         lib.lw_strerror.restype = ctypes.c_char_p
+        lib.lw_kernel_name.argtypes = [ctypes.c_int, i64, i64, i64]
+        lib.lw_kernel_name.restype = ctypes.c_char_p
         _lib = lib
     return _lib
 
@@ -66,6 +68,13 @@ def weight_bytes(fmt: int, n: int) -> int:
     if v < 0:
         raise LwError(v, "lw_weight_bytes")
     return v
+
+
+def kernel_name(fmt: int, M: int, K: int, n_tok: int):
+    """Name (template part) of the kernel lw_matvec launches for these sizes,
+    or None when lw_matvec would reject them. Host-only."""
+    v = library().lw_kernel_name(fmt, M, K, n_tok)
+    return None if v is None else v.decode()
 
 
 def _check_gpu(t, name):

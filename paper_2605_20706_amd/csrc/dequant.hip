@@ -16,6 +16,11 @@
 namespace lw {
 namespace {
 
+// names of the kernel templates, for lw_kernel_name
+struct Name_dequant_kernel {
+    static constexpr const char* base = "dequant_kernel";
+};
+
 template <int FMT>
 __global__ void __launch_bounds__(256) dequant_kernel(const uint8_t* __restrict__ W,
                                                       float4* __restrict__ out, int64_t n4,
@@ -79,6 +84,7 @@ hipError_t launch(const uint8_t* W, float* out, int64_t n, const Planes& p, hipS
     int64_t blocks = (n4 + threads - 1) / threads;
     const int64_t cap = 256 * 32;  // 32 workgroups per CU on 256 CUs; the rest is grid-stride
     if (blocks > cap) blocks = cap;
+    if (query_only(kernel_name<Name_dequant_kernel, FMT>())) return hipSuccess;
     hipLaunchKernelGGL(dequant_kernel<FMT>, dim3((unsigned)blocks), dim3(threads), 0, stream, W,
                        reinterpret_cast<float4*>(out), n4, p.off1, p.off2);
     return hipGetLastError();

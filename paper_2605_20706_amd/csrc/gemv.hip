@@ -32,6 +32,17 @@
 namespace lw {
 namespace {
 
+// names of the kernel templates, for lw_kernel_name
+struct Name_gemv_kernel {
+    static constexpr const char* base = "gemv_kernel";
+};
+struct Name_gemv1_kernel {
+    static constexpr const char* base = "gemv1_kernel";
+};
+struct Name_gemv1r_kernel {
+    static constexpr const char* base = "gemv1r_kernel";
+};
+
 constexpr int64_t kLdsBytes = 64 * 1024;      // LDS budget of a workgroup (x tile + group sums)
 constexpr int64_t kRegLdsBytes = 128 * 1024;  // of a register-kernel workgroup (one per compute unit or two)
 
@@ -830,6 +841,7 @@ hipError_t launch_nt(const uint8_t* W, const float* x, float* y, int64_t M, int6
     const int64_t KT = nch * E;
     const size_t lds = (size_t)(nch * chunk_bytes);
     const int64_t blocks = (M + (int64_t)NW * R - 1) / ((int64_t)NW * R);
+    if (query_only(kernel_name<Name_gemv_kernel, FMT, NT, R, NW>())) return hipSuccess;
     hipLaunchKernelGGL((gemv_kernel<FMT, NT, R, NW>), dim3((unsigned)blocks), dim3(NW * kWave), lds,
                        stream, W, x, y, M, K, (int)KT, p.off1, p.off2);
     return hipGetLastError();
@@ -870,6 +882,7 @@ hipError_t launch_single(const uint8_t* W, const float* x, float* y, int64_t M, 
     int64_t grid = (nbatch + NW - 1) / NW;
     const int64_t cap = 2 * (int64_t)cu_count();  // two 8-wave workgroups per CU
     if (grid > cap) grid = cap;
+    if (query_only(kernel_name<Name_gemv1_kernel, FMT, R, D, NW>())) return hipSuccess;
     hipLaunchKernelGGL((gemv1_kernel<FMT, R, D, NW>), dim3((unsigned)grid), dim3(NW * kWave), (size_t)lds,
                        stream, W, x, y, M, K, p.off1, p.off2);
     return hipGetLastError();
@@ -890,6 +903,7 @@ hipError_t launch_reg(const uint8_t* W, const float* x, float* y, int64_t M, con
     const int64_t nr_max = (M + grid * G - 1) / (grid * G);
     const int64_t lds = NTK * (K * 4 + NC * kWave * 4) + (WPR > 1 ? G * nr_max * NTK * WPR * 4 : 0);
     if (lds > kRegLdsBytes) return hipErrorNotSupported;
+    if (query_only(kernel_name<Name_gemv1r_kernel, FMT, NTK, CPW, WPR, G, DR>())) return hipSuccess;
     hipLaunchKernelGGL((gemv1r_kernel<FMT, NTK, CPW, WPR, G, DR>), dim3((unsigned)grid),
                        dim3(G * WPR * kWave), (size_t)lds, stream, W, x, y, (int)M, (int)nr_max, p.off1, p.off2);
     return hipGetLastError();

@@ -19,7 +19,44 @@ bool known_fmt(int fmt) { return fmt == LW_F16 || fmt == LW_Q8_0 || fmt == LW_Q4
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
+// The checks of lw_matvec that need no pointer, in the documented order.
+int check_shape(int fmt, int64_t M, int64_t K, int64_t n_tok) {
+    if (!known_fmt(fmt)) return LW_EFMT;
+    if (M < 1 || K < 1 || n_tok < 1 || M > LW_MAX_DIM || K > LW_MAX_DIM || n_tok > LW_MAX_DIM) return LW_EINVAL;
+    if (M > LW_MAX_ELEMS / K || n_tok > LW_MAX_ELEMS / K || n_tok > LW_MAX_ELEMS / M) return LW_EINVAL;
+    if (K % 256) return LW_ESHAPE;
+    return LW_OK;
+}
+
+// Kernel selection for a validated call.
+hipError_t dispatch(int fmt, const uint8_t* Wb, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
+                    hipStream_t s) {
+    const lw::Planes p = lw::planes_of(fmt, M * K);
+    hipError_t err = hipErrorNotSupported;
+    if (n_tok <= 2) err = lw::launch_gemv_reg(fmt, Wb, x, y, M, K, n_tok, p, s);
+    if (err == hipErrorNotSupported) {
+        if (n_tok > 1 && lw::multitok_supported(fmt, n_tok))
+            err = lw::launch_multitok(fmt, Wb, x, y, M, K, n_tok, p, s);
+        else if (n_tok <= LW_GEMV_MAX_TOK)
+            err = lw::launch_gemv(fmt, Wb, x, y, M, K, n_tok, p, s);
+        else if (n_tok <= 16 && lw::skinny_supported(fmt))
+            err = lw::launch_skinny(fmt, Wb, x, y, M, K, n_tok, p, s);
+        else
+            err = lw::launch_prefill(fmt, Wb, x, y, M, K, n_tok, p, s);
+    }
+    return err;
+}
+
 }  // namespace
+
+namespace lw {
+
+LaunchQuery& launch_query() {
+    static thread_local LaunchQuery q;
+    return q;
+}
+
+}  // namespace lw
 
 extern "C" {
 
@@ -46,27 +83,26 @@ int lw_matvec(int fmt, const void* W, const float* x, float* y, int64_t M, int64
               void* stream) {
     if (!known_fmt(fmt)) return LW_EFMT;
     if (!W || !x || !y) return LW_EINVAL;
-    if (M < 1 || K < 1 || n_tok < 1 || M > LW_MAX_DIM || K > LW_MAX_DIM || n_tok > LW_MAX_DIM)
-        return LW_EINVAL;
-    if (M > LW_MAX_ELEMS / K || n_tok > LW_MAX_ELEMS / K || n_tok > LW_MAX_ELEMS / M) return LW_EINVAL;
-    if (K % 256) return LW_ESHAPE;
+    const int rc = check_shape(fmt, M, K, n_tok);
+    if (rc != LW_OK) return rc;
     if (!aligned(W, 256) || !aligned(x, 16) || !aligned(y, 16)) return LW_EALIGN;
-    const lw::Planes p = lw::planes_of(fmt, M * K);
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    hipError_t err = hipErrorNotSupported;
-    const uint8_t* Wb = static_cast<const uint8_t*>(W);
-    if (n_tok <= 2) err = lw::launch_gemv_reg(fmt, Wb, x, y, M, K, n_tok, p, s);
-    if (err == hipErrorNotSupported) {
-        if (n_tok > 1 && lw::multitok_supported(fmt, n_tok))
-            err = lw::launch_multitok(fmt, Wb, x, y, M, K, n_tok, p, s);
-        else if (n_tok <= LW_GEMV_MAX_TOK)
-            err = lw::launch_gemv(fmt, Wb, x, y, M, K, n_tok, p, s);
-        else if (n_tok <= 16 && lw::skinny_supported(fmt))
-            err = lw::launch_skinny(fmt, Wb, x, y, M, K, n_tok, p, s);
-        else
-            err = lw::launch_prefill(fmt, Wb, x, y, M, K, n_tok, p, s);
-    }
+    const hipError_t err = dispatch(fmt, static_cast<const uint8_t*>(W), x, y, M, K, n_tok,
+                                    reinterpret_cast<hipStream_t>(stream));
     return err == hipSuccess ? LW_OK : LW_EHIP;
+}
+
+const char* lw_kernel_name(int fmt, int64_t M, int64_t K, int64_t n_tok) {
+    if (check_shape(fmt, M, K, n_tok) != LW_OK) return nullptr;
+    lw::LaunchQuery& q = lw::launch_query();
+    q.active = true;
+    q.name = nullptr;
+    // nothing is launched or dereferenced: the launchers stop at the launch
+    alignas(256) static const uint8_t stand_in[256] = {};
+    const hipError_t err = dispatch(fmt, stand_in, reinterpret_cast<const float*>(stand_in),
+                                    const_cast<float*>(reinterpret_cast<const float*>(stand_in)), M, K, n_tok,
+                                    nullptr);
+    q.active = false;
+    return err == hipSuccess ? q.name : nullptr;
 }
 
 int lw_dequant(int fmt, const void* W, float* out, int64_t n) {

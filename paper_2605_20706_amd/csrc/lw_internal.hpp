@@ -4,9 +4,44 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <string>
+
 #include "lw.h"
 
 namespace lw {
+
+// Kernel-name query (lw_kernel_name). While a query is active on the calling
+// thread the launchers launch nothing: at the point where they would launch,
+// they record the kernel's name (the first one, when a call launches several)
+// and return hipSuccess. So a query walks exactly the selection a real call
+// makes.
+struct LaunchQuery {
+    bool active = false;
+    const char* name = nullptr;
+};
+LaunchQuery& launch_query();
+
+// True when a query is active (the caller returns hipSuccess instead of
+// launching); records name if none is recorded yet.
+inline bool query_only(const char* name) {
+    LaunchQuery& q = launch_query();
+    if (!q.active) return false;
+    if (!q.name) q.name = name;
+    return true;
+}
+
+// "base<V0, V1, ...>": the template part of a kernel's demangled name, built
+// once per instantiation (Tag::base names the kernel template).
+template <class Tag, int... V>
+const char* kernel_name() {
+    static const std::string s = [] {
+        std::string r = std::string(Tag::base) + "<";
+        const int v[] = {V...};
+        for (size_t i = 0; i < sizeof...(V); ++i) r += (i ? ", " : "") + std::to_string(v[i]);
+        return r + ">";
+    }();
+    return s.c_str();
+}
 
 // Byte offsets of planes 1 and 2 and the total size of n packed elements of
 // fmt (split-plane layout: later planes start at the end of the previous one

@@ -44,6 +44,11 @@
 namespace lw {
 namespace {
 
+// names of the kernel templates, for lw_kernel_name
+struct Name_multitok_kernel {
+    static constexpr const char* base = "multitok_kernel";
+};
+
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -279,6 +284,7 @@ hipError_t launch3(const uint8_t* W, const float* x, float* y, int64_t M, int64_
     const int64_t grid = (M + 16 * RG - 1) / (16 * RG);
     if (grid > 0x7fffffff || nw < 1 || nw > kMaxWaves) return hipErrorInvalidConfiguration;
     const size_t lds = (size_t)nw * 128 * 16 + (size_t)nw * 4 * (4 * NTS) * (16 * RG) * 4;
+    if (query_only(kernel_name<Name_multitok_kernel, FMT, NTS, RG>())) return hipSuccess;
     hipLaunchKernelGGL((multitok_kernel<FMT, NTS, RG>), dim3((unsigned)grid), dim3(64 * nw), lds, stream, W, x, y, M,
                        K, (int)n_tok, p.off1, p.off2);
     return hipGetLastError();

@@ -31,6 +31,11 @@
 namespace lw {
 namespace {
 
+// names of the kernel templates, for lw_kernel_name
+struct Name_gemm_kernel {
+    static constexpr const char* base = "gemm_kernel";
+};
+
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -521,6 +526,7 @@ hipError_t launch_gemm(const uint8_t* W, const float* x, float* y, int64_t M, in
                        const Planes& p, hipStream_t stream) {
     const int64_t grid = ((M + kBM - 1) / kBM) * ((n_tok + kBN - 1) / kBN);
     if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
+    if (query_only(kernel_name<Name_gemm_kernel, FMT>())) return hipSuccess;
     hipLaunchKernelGGL((gemm_kernel<FMT>), dim3((unsigned)grid), dim3(kGT), GemmLds::kBytes, stream, W, x, y, M, K,
                        n_tok, p.off1, p.off2);
     return hipGetLastError();

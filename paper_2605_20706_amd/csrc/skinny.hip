@@ -25,6 +25,11 @@
 namespace lw {
 namespace {
 
+// names of the kernel templates, for lw_kernel_name
+struct Name_skinny_kernel {
+    static constexpr const char* base = "skinny_kernel";
+};
+
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -286,6 +291,7 @@ hipError_t launch_s(const uint8_t* W, const float* x, float* y, int64_t M, int64
     if (lds < (size_t)S * 256 * 4) lds = (size_t)S * 256 * 4;  // final split reduction
     const int64_t grid = (M + 15) / 16;
     if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
+    if (query_only(kernel_name<Name_skinny_kernel, FMT, S>())) return hipSuccess;
     hipLaunchKernelGGL((skinny_kernel<FMT, S>), dim3((unsigned)grid), dim3(64 * S), lds, stream, W, x, y, M, K,
                        (int)n_tok, (int)KT, p.off1, p.off2);
     return hipGetLastError();

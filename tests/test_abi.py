@@ -102,3 +102,42 @@ def test_binding_fails_loudly_without_gpu_tensors(lib):
         binding.matvec(Q4_0, W, x, 4, 256)
     with pytest.raises(ValueError):
         binding.dequant(Q4_0, W, 256)
+
+
+def test_kernel_name_rejects_what_matvec_rejects(lib):
+    assert binding.kernel_name(7, 4, 256, 1) is None           # format
+    assert binding.kernel_name(Q4_0, 0, 256, 1) is None        # sizes
+    assert binding.kernel_name(Q4_0, 4, 256, 0) is None
+    assert binding.kernel_name(Q4_0, 4, 300, 1) is None        # shape
+    assert binding.kernel_name(Q4_0, 4, 256, 1) is not None
+
+
+def test_kernel_selection_table(lib):
+    """The kernels the workloads' shapes select (no launch: a host-only query).
+    One token: the register-activation kernel when K is a whole number of
+    2048-element chunks and its table has the shape, else the LDS-activation
+    kernel; two tokens over the 4-bit formats: the register kernel; 3..16
+    tokens over the 4-bit formats: the block-diagonal matrix-core kernel;
+    more: the tiled matrix-core kernel."""
+    from paper_2605_20706_amd import synth
+
+    def kind(fmt, M, K, nt):
+        return binding.kernel_name(fmt, M, K, nt).split("<")[0]
+
+    for key, wl in synth.WORKLOADS.items():
+        for m in wl.matrices:
+            for nt in (1, 2, 4, 8, 12, 512):
+                name = binding.kernel_name(wl.fmt, m.M, m.K, nt)
+                assert name and re.fullmatch(r"\w+_kernel<\d+(, \d+)*>", name), (key, m, nt, name)
+                assert name.startswith(("gemv", "multitok", "skinny", "gemm")), name
+    assert kind(Q4_K, 14336, 4096, 1) == "gemv1r_kernel"      # 8B gate: 2 chunks, many rows
+    assert kind(Q4_K, 4096, 14336, 1) == "gemv1r_kernel"      # 8B down: 7 chunks split over 7 waves
+    assert kind(Q4_K, 6144, 4096, 1) == "gemv1_kernel"        # 8B qkv: too few rows per wave
+    assert kind(Q4_0, 100, 2304, 1) == "gemv1_kernel"         # K not whole chunks
+    assert kind(Q4_0, 14336, 4096, 2) == "gemv1r_kernel"
+    assert kind(Q4_0, 14336, 4096, 4) == "multitok_kernel"
+    assert kind(Q4_0, 14336, 4096, 512) == "gemm_kernel"
+    assert kind(F16, 2048, 2048, 1) == "gemv1_kernel"
+    assert kind(Q8_0, 2048, 2048, 12) == "skinny_kernel"
+    assert kind(F16, 2048, 2048, 20) == "gemv_kernel"
+    assert binding.kernel_name(Q4_K, 14336, 4096, 1) == "gemv1r_kernel<%d, 1, 2, 1, 8, 2>" % Q4_K
