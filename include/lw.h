@@ -82,9 +82,12 @@ enum {
 /* Largest accepted M and K, and largest accepted element count M*K or n. */
 #define LW_MAX_DIM ((int64_t)1 << 31)
 #define LW_MAX_ELEMS ((int64_t)1 << 40)
-/* Token counts up to this bound take the matrix-vector path (W is streamed
- * once, every token reuses each decoded weight in registers); larger token
- * counts take the matrix-core (MFMA) prefill path. */
+/* Token blocks of the VALU matrix-vector kernel: f16 and Q8_0 weights take
+ * it for up to this many tokens (W streamed once, every token reusing each
+ * decoded weight in registers). The 4-bit formats take a VALU kernel for one
+ * or two tokens and the matrix cores from three tokens on; Q8_0 takes the
+ * matrix cores above this bound; f16 stays on the VALU kernel, in blocks of
+ * this many tokens. lw_kernel_name names the kernel a call selects. */
 #define LW_GEMV_MAX_TOK 8
 
 /*
@@ -93,8 +96,8 @@ enum {
  *
  * Decode step of Sec. 2.1 with the dequantize-in-registers matrix-vector
  * kernel of Sec. 3.3; n_tok > 1 is the multi-token batch of the same product,
- * and n_tok > LW_GEMV_MAX_TOK the prefill matrix multiplication of Sec. 3.2
- * (dequantized weight tiles reused across tokens, Sec. 3.3).
+ * and n_tok > 16 the prefill matrix multiplication of Sec. 3.2 (dequantized
+ * weight tiles reused across tokens, Sec. 3.3).
  *
  *   fmt    one of lw_fmt.
  *   W      device; M*K elements packed in the layout above, 256-byte aligned.
@@ -107,10 +110,11 @@ enum {
  *   stream hipStream_t to enqueue on (NULL: the null stream).
  *
  * Arithmetic: products and sums in float32 with float32 accumulation (no
- * reduced-precision activations) on the matrix-vector path. The prefill path
- * multiplies exact integer codes by activations split into a bfloat16 high
- * part and a bfloat16 low part, accumulating in float32; its error relative to
- * sum_k |w * x| stays below 1e-4.
+ * reduced-precision activations) on the VALU paths. The matrix-core paths
+ * (4-bit formats from three tokens, Q8_0 above LW_GEMV_MAX_TOK tokens)
+ * multiply exact integer codes by activations split into a bfloat16 high
+ * part and a bfloat16 low part, accumulating in float32. Every path's error
+ * relative to sum_k |w * x| stays below 1e-4.
  */
 int lw_matvec(int fmt, const void* W, const float* x, float* y,
               int64_t M, int64_t K, int64_t n_tok, void* stream);
