@@ -3,41 +3,17 @@
 // Y[t][r] = sum_k value(W, r*K + k) * X[t][k]: the decode product of Sec. 2.1
 // for a small batch of tokens, with the weights streamed from HBM exactly once
 // and dequantized in registers (Sec. 3.3). The contraction runs on
-// v_mfma_f32_16x16x32_bf16 (D[16x16] += A[16x32] . B[32x16]).
+// v_mfma_f32_16x16x32_bf16 (D[16x16] += A[16x32] . B[32x16]) with one MFMA K
+// step per 32-element block, so each block's scale applies to its own partial
+// product: A = X (the token rows), B = the codes of 16 weight rows.
 //
-// Operand mapping. Lane l = 16*g + n (g = l/16, n = l%16) loads the 16 code
-// bytes of one whole 32-weight block: block 4s+g of weight row n, for step s
-// (4 blocks = 128 columns). Word j of those bytes holds elements 4j..4j+3 (low
-// nibbles) and 16+4j..16+4j+3 (high nibbles) of the block, which become the 8
-// bf16 B values of the lane in MFMA j (j = 0..3). So in MFMA j the 32 K indices
-// are quarter j of four different blocks (one per lane group g).
-//
-// To keep every block's scale separate, A is block-diagonal: A row i stands
-// for (block i/4, token i%4) and holds X only in the K indices of its own
-// block; all other entries are zero. Summed over j = 0..3, D[i][n] is then the
-// dot product of token i%4 with block i/4 of row n. In the MFMA output layout
-// lane l holds D[4g + v][n], v = 0..3: the four tokens of block 4s+g of row n,
-// i.e. exactly the block whose codes (and scale) the lane loaded -- each lane
-// applies its own block's scale with no data exchange, once per step.
-//
-// Precision (the same reading as the other matrix-core paths): B holds the
-// exact bf16 of the biased code 128 + q (bit pattern 0x4300 | q); X is split
-// into a bf16 high part and a bf16 low part (two MFMAs per K step); per block
-// y += c1 * P + c2 * S with S the block sum of the operand actually multiplied
-// (hi + lo), obtained from the same A operands against a B of ones:
-//   Q4_0:     w = d (q - 8)         -> c1 = d,    c2 = -136 d
-//   Q4_K:     w = d sc q - dmin m   -> c1 = d sc, c2 = -(128 d sc + dmin m)
-//
-// X staging: each wave converts the X columns of its own K range, one step
-// and one set of 4 tokens at a time, densely (every lane converts 8 values of
-// one (token, block, quarter)), writes hi/lo to its private LDS slice, and
-// reads them back in the block-diagonal arrangement (the 16 lanes with
-// n/4 == g; the other lanes keep zero operands). Codes are decoded once per
-// step for all token sets. Codes, scales and X are prefetched two steps ahead.
-//
-// Workgroup: NW waves on the same 16*RG rows, each on one contiguous range of
-// K steps; the partials (over the four lane groups and the NW waves) are
-// summed through LDS at the end.
+// Precision (the reading shared by the matrix-core paths): B holds the exact
+// bf16 of the biased code 128 + q (bit pattern 0x4300 | q); X is split into a
+// bf16 high part and a bf16 low part (two MFMAs per block); per block
+// y += c1 * (P + k * S) - dm * S, with S the block sum of the operand actually
+// multiplied (hi + lo), obtained from the same A operands against a B of ones:
+//   Q4_0:     w = d (q - 8)         -> c1 = d,    k = -136, dm = 0
+//   Q4_K:     w = d sc q - dmin m   -> c1 = d sc, k = -128, dm = dmin m
 #include "lw_device.hpp"
 #include "lw_internal.hpp"
 
@@ -72,70 +48,115 @@ __device__ __forceinline__ bf16x8 biased_codes(uint32_t w) {
     return __builtin_bit_cast(bf16x8, v);
 }
 
-// Scale data of the lane's block, and its two coefficients.
+int cu_count_mt() {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0)
+        return 256;
+    return v;
+}
+
+// 4 x 4 transpose across the four 16-lane groups: lane (g, i) holds words
+// w0..w3 of block g of its row; afterwards word j of the result is word g of
+// block j (v_permlane32_swap, v_permlane16_swap).
+__device__ __forceinline__ u32x4 quad_transpose(u32x4 w) {
+    const auto s02 = __builtin_amdgcn_permlane32_swap(w[0], w[2], false, false);
+    const auto s13 = __builtin_amdgcn_permlane32_swap(w[1], w[3], false, false);
+    const auto s01 = __builtin_amdgcn_permlane16_swap(s02[0], s13[0], false, false);
+    const auto s23 = __builtin_amdgcn_permlane16_swap(s02[1], s13[1], false, false);
+    return u32x4{s01[0], s01[1], s23[0], s23[1]};
+}
+
+// Scale data of a step (4 blocks of one weight row, inside one super-block).
 template <int FMT>
-struct Scale;
+struct StepScale;
 
 template <>
-struct Scale<LW_Q4_0> {
-    uint32_t h;  // binary16 d
-    __device__ void load(const uint8_t* W, int64_t off1, int64_t, uint64_t row, uint32_t K, uint32_t blk) {
-        h = *reinterpret_cast<const uint16_t*>(W + off1 + 2 * (row * (K / 32u) + blk));
+struct StepScale<LW_Q4_0> {
+    uint32_t a, b;  // binary16 d of the 4 blocks
+    __device__ void load(const uint8_t* P1, const uint8_t*, uint64_t row, uint32_t K, uint32_t s, int) {
+        const uint2 v = *reinterpret_cast<const uint2*>(P1 + 2 * (row * (K / 32u) + 4u * s));
+        a = v.x;
+        b = v.y;
     }
-    __device__ void coef(uint32_t, float* c1, float* c2) const {
-        const float d = half_bits_to_float(h);
-        *c1 = d;
-        *c2 = -136.0f * d;
+    // c1 of the step's blocks (d), and dm = 0
+    __device__ void coef(uint32_t, int, float* c1, float* dm) const {
+        c1[0] = half_bits_to_float(a & 0xFFFFu);
+        c1[1] = half_bits_to_float(a >> 16);
+        c1[2] = half_bits_to_float(b & 0xFFFFu);
+        c1[3] = half_bits_to_float(b >> 16);
+        dm[0] = dm[1] = dm[2] = dm[3] = 0.f;
     }
 };
 
 template <>
-struct Scale<LW_Q4_K> {
-    uint32_t a, b, c, dd;  // 96-bit scale record, {d, dmin}
-    __device__ void load(const uint8_t* W, int64_t off1, int64_t off2, uint64_t row, uint32_t K, uint32_t blk) {
-        const uint64_t sb = row * (K / 256u) + (blk >> 3);
-        const uint32_t* rec = reinterpret_cast<const uint32_t*>(W + off1 + 12 * sb);
-        a = rec[0];
-        b = rec[1];
-        c = rec[2];
-        dd = *reinterpret_cast<const uint32_t*>(W + off2 + 4 * sb);
+struct StepScale<LW_Q4_K> {
+    uint32_t r0, r1, r2, dd;  // the super-block's 96-bit record and {d, dmin}
+    __device__ void load(const uint8_t* P1, const uint8_t* P2, uint64_t row, uint32_t K, uint32_t s, int) {
+        const uint64_t sb = row * (K / 256u) + (s >> 1);
+        const uint32_t* rec = reinterpret_cast<const uint32_t*>(P1 + 12 * sb);
+        r0 = rec[0];
+        r1 = rec[1];
+        r2 = rec[2];
+        dd = *reinterpret_cast<const uint32_t*>(P2 + 4 * sb);
     }
-    __device__ void coef(uint32_t blk, float* c1, float* c2) const {
-        const uint32_t j = blk & 7u;
-        const uint64_t lo = (uint64_t)a | ((uint64_t)b << 32);
-        const uint64_t hi = (uint64_t)b | ((uint64_t)c << 32);
-        const float ds = half_bits_to_float(dd & 0xFFFFu) * (float)((uint32_t)(lo >> (6 * j)) & 63u);
-        const float dm = half_bits_to_float(dd >> 16) * (float)((uint32_t)(hi >> (16 + 6 * j)) & 63u);
-        *c1 = ds;
-        *c2 = -__builtin_fmaf(128.0f, ds, dm);
+    // c1 = d*sc_j and dm = dmin*m_j of the step's blocks, sub-blocks
+    // j = 4(s&1) + 0..3 of the super-block: sc_j at record bit 6j, m_j at
+    // bit 48 + 6j, cut out of one rotated word or one word pair each.
+    __device__ void coef(uint32_t s, int, float* c1, float* dm) const {
+        const float d = half_bits_to_float(dd & 0xFFFFu), dmin = half_bits_to_float(dd >> 16);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t j = 4u * (s & 1u) + (uint32_t)i;
+            const uint32_t ts = 6u * j, tm = 16u + 6u * j;
+            const uint32_t sc_w = __builtin_amdgcn_alignbit(r1, ts < 32u ? r0 : r1, ts & 31u);
+            const uint32_t m_w = __builtin_amdgcn_alignbit(r2, tm < 32u ? r1 : r2, tm & 31u);
+            c1[i] = d * (float)(sc_w & 63u);
+            dm[i] = dmin * (float)(m_w & 63u);
+        }
     }
 };
 
-template <int FMT, int NTS, int RG>
+template <int FMT, int NX, int RG>
 struct Stage {
     u32x4 codes[RG];
-    Scale<FMT> sc[RG];
-    float4 xa[NTS], xb[NTS];
+    StepScale<FMT> sc[RG];
+    float4 xv[NX];
 };
 
-template <int FMT, int NTS, int RG>
+// Few-token product with whole-block MFMAs: D = X . W^T per 32-element block,
+// A = X (16 token rows, tokens >= n_tok zero), B = the codes of 16 weight
+// rows. A step is 4 blocks (128 columns) of RG row tiles. Lane (g, i) loads
+// block 4s+g of row i of each tile (one 16-byte load, a whole block), and a
+// transpose across the lane groups gives it word g of each of the 4 blocks,
+// its B slice (elements 4g..4g+3 and 16+4g..16+4g+3) for the 4 MFMAs. D lands
+// as D[4g+v][i] = (token 4g+v, row i): one row per lane, so each lane applies
+// its row's block scale with no exchange.
+// X: every step, the wave converts its 4 blocks of the n_tok token rows
+// densely (lane -> token, block, float4; NX float4 per lane; the loads of one
+// block are 128 contiguous bytes), hi/lo bf16 halves into its private LDS
+// slice in the A layout, then reads its A operands back. The slice's rows of
+// tokens >= n_tok are zeroed once and never written. Waves split K; their
+// partials are summed through LDS at the end.
+template <int FMT, int NX, int RG>
 __global__ void __launch_bounds__(64 * kMaxWaves)
     multitok_kernel(const uint8_t* __restrict__ W, const float* __restrict__ x, float* __restrict__ y, int64_t M,
-                    int64_t K, int ntok, int64_t off1, int64_t off2) {
+                     int64_t K, int ntok, int64_t off1, int64_t off2) {
     extern __shared__ float4 smem4[];
     const int nw = blockDim.x >> 6;
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int n16 = lane & 15, g = lane >> 4;
     const uint32_t K32 = (uint32_t)K;
+    const uint8_t* P1 = W + off1;
+    const uint8_t* P2 = W + off2;
 
-    // this wave's steps
     const int nsteps = (int)(K / 128);
     const int spw = (nsteps + nw - 1) / nw;
     const int s0 = wave * spw;
     const int s1 = (s0 + spw) < nsteps ? (s0 + spw) : nsteps;
 
-    // rows of the lane in each row group (clamped; stores are masked)
     const int64_t row0 = (int64_t)blockIdx.x * 16 * RG;
     uint64_t row[RG];
     const uint8_t* cp[RG];
@@ -145,183 +166,192 @@ __global__ void __launch_bounds__(64 * kMaxWaves)
         row[q] = (uint64_t)(r < M ? r : M - 1);
         cp[q] = W + row[q] * (K32 / 2u) + 16u * g;
     }
-    // dense X conversion: lane -> (quarter jd, block bd, token td of a token set)
-    const int jd = lane >> 4, bd = (lane >> 2) & 3, td = lane & 3;
-    const float* xp[NTS];
-    bool xv[NTS];
+    // dense X items: item e of the lane is float4 m of block j of token t
+    int xm[NX], xj[NX], xt[NX];
+    bool xlive[NX];
+    const float* xp[NX];
 #pragma unroll
-    for (int ts = 0; ts < NTS; ++ts) {
-        const int T = 4 * ts + td;
-        xv[ts] = T < ntok;
-        xp[ts] = x + (int64_t)(xv[ts] ? T : 0) * K + 32 * bd + 4 * jd;
+    for (int e = 0; e < NX; ++e) {
+        const int idx = lane + 64 * e;
+        xm[e] = idx & 7;
+        xj[e] = (idx >> 3) & 3;
+        xt[e] = idx >> 5;
+        xlive[e] = xt[e] < ntok;
+        xp[e] = x + (int64_t)(xlive[e] ? xt[e] : ntok - 1) * K + 32 * xj[e] + 4 * xm[e];
     }
-    // LDS: per wave, hi then lo of one token set, 64 x 16 bytes each
-    float4* xs = smem4 + (size_t)wave * 128;
-    const bool active = (n16 >> 2) == g;
+    // the wave's A slice: [hi, lo][block j][64 slots] of 16 bytes, then a
+    // spare 16 bytes that absorb the writes of padding items. Lane (g, n)'s
+    // operand of block j sits in slot 16g + (n ^ (2g + (j & 1) + 8(j >> 1))):
+    // a permutation of each 64-slot row, so the reads stay conflict-free,
+    // which spreads the 8-byte writes of one instruction (items of fixed
+    // token, 4 blocks x 8 float4) over distinct banks.
+    auto xslot = [](int gg, int t, int j) { return 16 * gg + (t ^ (2 * gg + (j & 1) + 8 * (j >> 1))); };
+    constexpr int kSpare = 2 * 512;
+    uint2* xs = reinterpret_cast<uint2*>(smem4 + (size_t)wave * 513);
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            xs[2 * ((h * 4 + j) * 64 + lane)] = uint2{0u, 0u};
+            xs[2 * ((h * 4 + j) * 64 + lane) + 1] = uint2{0u, 0u};
+        }
 
-    auto load = [&](Stage<FMT, NTS, RG>& st, int s) {
+    auto load = [&](Stage<FMT, NX, RG>& st, int s) __attribute__((always_inline)) {
 #pragma unroll
         for (int q = 0; q < RG; ++q) {
             st.codes[q] = load_codes(cp[q] + 64u * (uint32_t)s);
-            st.sc[q].load(W, off1, off2, row[q], K32, 4u * (uint32_t)s + (uint32_t)g);
+            st.sc[q].load(P1, P2, row[q], K32, (uint32_t)s, g);
         }
 #pragma unroll
-        for (int ts = 0; ts < NTS; ++ts) {
-            st.xa[ts] = *reinterpret_cast<const float4*>(xp[ts] + 128 * s);
-            st.xb[ts] = *reinterpret_cast<const float4*>(xp[ts] + 128 * s + 16);
-        }
+        for (int e = 0; e < NX; ++e) st.xv[e] = *reinterpret_cast<const float4*>(xp[e] + 128 * s);
     };
 
     const bf16x8 ones = __builtin_bit_cast(bf16x8, u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u});
-    // block-diagonal A operands of one token set; the lanes outside the
-    // diagonal never write them, so they stay zero
-    bf16x8 ah[4], al[4];
+    const float bias_k = FMT == LW_Q4_0 ? -136.0f : -128.0f;  // bias (and the Q4_0 offset) per unit of S
+    f32x4 acc[RG];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        ah[j] = bf16x8{};
-        al[j] = bf16x8{};
-    }
-    f32x4 acc[NTS][RG];
-#pragma unroll
-    for (int ts = 0; ts < NTS; ++ts)
-#pragma unroll
-        for (int q = 0; q < RG; ++q) acc[ts][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int q = 0; q < RG; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    auto consume = [&](const Stage<FMT, NTS, RG>& st, int s) {
-        // codes of the step -> B operands, once for all token sets
-        bf16x8 bq[RG][4];
+    auto consume = [&](const Stage<FMT, NX, RG>& st, int s) __attribute__((always_inline)) {
+        // X of the step -> hi/lo halves in the A layout: item (t, j, m) is
+        // half m >> 2 of the 16 bytes of lane 16 (m & 3) + t in block j
+        __builtin_amdgcn_wave_barrier();
 #pragma unroll
-        for (int q = 0; q < RG; ++q)
+        for (int e = 0; e < NX; ++e) {
+            const float v[4] = {st.xv[e].x, st.xv[e].y, st.xv[e].z, st.xv[e].w};
+            typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+            typedef float f32x2 __attribute__((ext_vector_type(2)));
+            uint32_t hw[2], lw[2];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) bq[q][j] = biased_codes(st.codes[q][j]);
-        float c1[RG], c2[RG];
-        const uint32_t blk = 4u * (uint32_t)s + (uint32_t)g;
-#pragma unroll
-        for (int q = 0; q < RG; ++q) st.sc[q].coef(blk, &c1[q], &c2[q]);
-#pragma unroll
-        for (int ts = 0; ts < NTS; ++ts) {
-            // X of this step and token set: dense hi/lo conversion -> LDS ->
-            // block-diagonal operands
-            const float v[8] = {st.xa[ts].x, st.xa[ts].y, st.xa[ts].z, st.xa[ts].w,
-                                st.xb[ts].x, st.xb[ts].y, st.xb[ts].z, st.xb[ts].w};
-            bf16x8 h, l;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const float ve = xv[ts] ? v[e] : 0.f;
-                h[e] = (__bf16)ve;
-                l[e] = (__bf16)(ve - (float)h[e]);
+            for (int p2 = 0; p2 < 2; ++p2) {
+                const uint32_t hb = __builtin_bit_cast(
+                    uint32_t, __builtin_convertvector((f32x2{v[2 * p2], v[2 * p2 + 1]}), bf16x2));
+                const float h0 = __builtin_bit_cast(float, hb << 16), h1 = __builtin_bit_cast(float, hb & 0xFFFF0000u);
+                hw[p2] = hb;
+                lw[p2] = __builtin_bit_cast(
+                    uint32_t, __builtin_convertvector((f32x2{v[2 * p2] - h0, v[2 * p2 + 1] - h1}), bf16x2));
             }
-            __builtin_amdgcn_wave_barrier();
-            xs[lane] = __builtin_bit_cast(float4, h);
-            xs[64 + lane] = __builtin_bit_cast(float4, l);
-            __builtin_amdgcn_wave_barrier();
-            if (active) {
+            // an item of a token >= n_tok goes to the slice's spare slot
+            const int slot = xslot(xm[e] & 3, xt[e], xj[e]);
+            const int half = xm[e] >> 2;
+            const int ih = xlive[e] ? 2 * ((0 * 4 + xj[e]) * 64 + slot) + half : kSpare;
+            const int il = xlive[e] ? 2 * ((1 * 4 + xj[e]) * 64 + slot) + half : kSpare;
+            xs[ih] = uint2{hw[0], hw[1]};
+            xs[il] = uint2{lw[0], lw[1]};
+        }
+        __builtin_amdgcn_wave_barrier();
+        bf16x8 ah[4], al[4];
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    ah[j] = __builtin_bit_cast(bf16x8, xs[16 * j + n16]);
-                    al[j] = __builtin_bit_cast(bf16x8, xs[64 + 16 * j + n16]);
-                }
-            }
-            __builtin_amdgcn_wave_barrier();
-            // block sums of the multiplied operand (against ones), and the products
-            f32x4 S = {0.f, 0.f, 0.f, 0.f};
-            f32x4 P[RG];
+        for (int j = 0; j < 4; ++j) {
+            const int sl = xslot(g, n16, j);
+            ah[j] = __builtin_bit_cast(bf16x8, reinterpret_cast<const float4*>(xs)[(0 * 4 + j) * 64 + sl]);
+            al[j] = __builtin_bit_cast(bf16x8, reinterpret_cast<const float4*>(xs)[(1 * 4 + j) * 64 + sl]);
+        }
+        // block sums of the multiplied values, in the D layout (token 4g+v)
+        f32x4 S[4];
 #pragma unroll
-            for (int q = 0; q < RG; ++q) P[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < 4; ++j) {
+            S[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[j], ones, f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+            S[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[j], ones, S[j], 0, 0, 0);
+        }
+#pragma unroll
+        for (int q = 0; q < RG; ++q) {
+            const u32x4 wq = quad_transpose(st.codes[q]);
+            float c1[4], dm[4];
+            st.sc[q].coef((uint32_t)s, g, c1, dm);
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                S = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[j], ones, S, 0, 0, 0);
+                const bf16x8 bq = biased_codes(wq[j]);
+                f32x4 P = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[j], bq, f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                P = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[j], bq, P, 0, 0, 0);
 #pragma unroll
-                for (int q = 0; q < RG; ++q) P[q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[j], bq[q][j], P[q], 0, 0, 0);
-                S = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[j], ones, S, 0, 0, 0);
-#pragma unroll
-                for (int q = 0; q < RG; ++q) P[q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[j], bq[q][j], P[q], 0, 0, 0);
+                for (int v = 0; v < 4; ++v) {
+                    float o = __builtin_fmaf(c1[j], __builtin_fmaf(bias_k, S[j][v], P[v]), acc[q][v]);
+                    if constexpr (FMT == LW_Q4_K) o = __builtin_fmaf(-dm[j], S[j][v], o);
+                    acc[q][v] = o;
+                }
             }
-#pragma unroll
-            for (int q = 0; q < RG; ++q)
-#pragma unroll
-                for (int v4 = 0; v4 < 4; ++v4)
-                    acc[ts][q][v4] = __builtin_fmaf(c2[q], S[v4], __builtin_fmaf(c1[q], P[q][v4], acc[ts][q][v4]));
         }
     };
 
-    Stage<FMT, NTS, RG> sa, sb;
-    if (s0 < s1) load(sa, s0);
-    if (s0 + 1 < s1) load(sb, s0 + 1);
-    for (int s = s0; s < s1; s += 2) {
+    // Two stages in flight. Every load is issued unconditionally (a step
+    // index past the wave's range is clamped to its last step, an in-range
+    // reload never consumed), so the compiler's vmcnt waits stay exact and a
+    // consume never waits for the refill issued after it.
+    const int slast = s1 > s0 ? s1 - 1 : (s0 < nsteps ? s0 : nsteps - 1);
+    auto clampst = [&](int st) { return st < s1 ? st : slast; };
+    Stage<FMT, NX, RG> sa, sb;
+    load(sa, clampst(s0));
+    load(sb, clampst(s0 + 1));
+    int s = s0;
+    for (; s + 4 <= s1; s += 2) {
         consume(sa, s);
-        if (s + 2 < s1) load(sa, s + 2);
-        if (s + 1 < s1) {
-            consume(sb, s + 1);
-            if (s + 3 < s1) load(sb, s + 3);
-        }
+        __builtin_amdgcn_sched_barrier(0);
+        load(sa, s + 2);
+        __builtin_amdgcn_sched_barrier(0);
+        consume(sb, s + 1);
+        __builtin_amdgcn_sched_barrier(0);
+        load(sb, s + 3);
+        __builtin_amdgcn_sched_barrier(0);
     }
+    // the last 0..3 steps
+    if (s < s1) consume(sa, s);
+    load(sa, clampst(s + 2));
+    if (s + 1 < s1) consume(sb, s + 1);
+    if (s + 2 < s1) consume(sa, s + 2);
 
-    // sum the partials over the 4 lane groups and the waves
-    float* red = reinterpret_cast<float*>(smem4 + (size_t)nw * 128);  // [nw*4][NTS*4][16*RG]
-    constexpr int kRows = 16 * RG, kTok = 4 * NTS;
-#pragma unroll
-    for (int ts = 0; ts < NTS; ++ts)
-#pragma unroll
-        for (int q = 0; q < RG; ++q)
-#pragma unroll
-            for (int v = 0; v < 4; ++v)
-                red[((wave * 4 + g) * kTok + 4 * ts + v) * kRows + 16 * q + n16] = acc[ts][q][v];
+    // sum the partials of the waves: lane holds tokens 4g + v of row 16q + n16
     __syncthreads();
-    for (int it = tid; it < kTok * kRows; it += blockDim.x) {
+    constexpr int kRows = 16 * RG;
+    float* red = reinterpret_cast<float*>(smem4);  // [nw][16 tokens][kRows]
+#pragma unroll
+    for (int q = 0; q < RG; ++q)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) red[(wave * 16 + 4 * g + v) * kRows + 16 * q + n16] = acc[q][v];
+    __syncthreads();
+    for (int it = tid; it < 16 * kRows; it += blockDim.x) {
         const int t = it / kRows, r = it % kRows;
         if (t < ntok && row0 + r < M) {
             float o = 0.f;
-            for (int p = 0; p < nw * 4; ++p) o += red[(p * kTok + t) * kRows + r];
+            for (int p = 0; p < nw; ++p) o += red[(p * 16 + t) * kRows + r];
             y[(int64_t)t * M + row0 + r] = o;
         }
     }
 }
 
-template <int FMT, int NTS, int RG>
-hipError_t launch3(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok, const Planes& p,
-                   int nw, hipStream_t stream) {
+template <int FMT, int NX, int RG>
+hipError_t launch_mt(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
+                      const Planes& p, int nw, hipStream_t stream) {
     const int64_t grid = (M + 16 * RG - 1) / (16 * RG);
     if (grid > 0x7fffffff || nw < 1 || nw > kMaxWaves) return hipErrorInvalidConfiguration;
-    const size_t lds = (size_t)nw * 128 * 16 + (size_t)nw * 4 * (4 * NTS) * (16 * RG) * 4;
-    if (query_only(kernel_name<Name_multitok_kernel, FMT, NTS, RG>())) return hipSuccess;
-    hipLaunchKernelGGL((multitok_kernel<FMT, NTS, RG>), dim3((unsigned)grid), dim3(64 * nw), lds, stream, W, x, y, M,
-                       K, (int)n_tok, p.off1, p.off2);
+    size_t lds = (size_t)nw * 513 * 16;                       // A slices, 8 KiB + 16 B per wave
+    const size_t red = (size_t)nw * 16 * (16 * RG) * 4;       // final partial sums
+    if (lds < red) lds = red;
+    if (query_only(kernel_name<Name_multitok_kernel, FMT, NX, RG>())) return hipSuccess;
+    hipLaunchKernelGGL((multitok_kernel<FMT, NX, RG>), dim3((unsigned)grid), dim3(64 * nw), lds, stream, W, x, y,
+                       M, K, (int)n_tok, p.off1, p.off2);
     return hipGetLastError();
 }
 
-int cu_count_mt() {
-    int dev = 0, v = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0)
-        return 256;
-    return v;
-}
-
 template <int FMT>
-hipError_t launch_f(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok, const Planes& p,
-                    hipStream_t stream) {
+hipError_t launch_f(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
+                     const Planes& p, hipStream_t stream) {
     const int64_t cus = cu_count_mt();
-    // two row groups per workgroup when that still leaves two workgroups per CU
-    // (and registers allow: one row group for 13..16 tokens)
-    const bool rg2 = (M + 31) / 32 >= 2 * cus && n_tok <= 12;
+    const bool rg2 = (M + 31) / 32 >= cus;
     const int64_t wgs = rg2 ? (M + 31) / 32 : (M + 15) / 16;
     const int nw = wgs >= 2 * cus ? 4 : 8;
-    const int nts = (int)((n_tok + 3) / 4);
+    const int nx = n_tok <= 4 ? 2 : (n_tok <= 8 ? 4 : 8);  // 32 * n_tok floats over 64 lanes, in float4s
     if (rg2) {
-        switch (nts) {
-        case 1: return launch3<FMT, 1, 2>(W, x, y, M, K, n_tok, p, nw, stream);
-        case 2: return launch3<FMT, 2, 2>(W, x, y, M, K, n_tok, p, nw, stream);
-        case 3: return launch3<FMT, 3, 2>(W, x, y, M, K, n_tok, p, nw, stream);
-        default: return hipErrorInvalidValue;
+        switch (nx) {
+        case 2: return launch_mt<FMT, 2, 2>(W, x, y, M, K, n_tok, p, nw, stream);
+        case 4: return launch_mt<FMT, 4, 2>(W, x, y, M, K, n_tok, p, nw, stream);
+        default: return launch_mt<FMT, 8, 2>(W, x, y, M, K, n_tok, p, nw, stream);
         }
     }
-    switch (nts) {
-    case 1: return launch3<FMT, 1, 1>(W, x, y, M, K, n_tok, p, nw, stream);
-    case 2: return launch3<FMT, 2, 1>(W, x, y, M, K, n_tok, p, nw, stream);
-    case 3: return launch3<FMT, 3, 1>(W, x, y, M, K, n_tok, p, nw, stream);
-    case 4: return launch3<FMT, 4, 1>(W, x, y, M, K, n_tok, p, nw, stream);
-    default: return hipErrorInvalidValue;
+    switch (nx) {
+    case 2: return launch_mt<FMT, 2, 1>(W, x, y, M, K, n_tok, p, nw, stream);
+    case 4: return launch_mt<FMT, 4, 1>(W, x, y, M, K, n_tok, p, nw, stream);
+    default: return launch_mt<FMT, 8, 1>(W, x, y, M, K, n_tok, p, nw, stream);
     }
 }
 
