@@ -209,15 +209,21 @@ def run_gpu(ws, steps, warmup, mode):
     return ms_per_step, per_shape
 
 
-def source_hash():
-    """sha256 over every kernel source, the device helpers and the C header: a
-    stored HBM traffic figure is valid only for the sources it was measured on."""
-    import glob
+KERNEL_SOURCES = {"gemv_kernel": "gemv.hip", "gemv1_kernel": "gemv.hip", "gemv1r_kernel": "gemv.hip",
+                  "multitok_kernel": "multitok.hip", "skinny_kernel": "skinny.hip", "gemm_kernel": "prefill.hip",
+                  "dequant_kernel": "dequant.hip"}
+
+
+def source_hash(kernels):
+    """sha256 over the sources of the given kernels (names as lw_kernel_name
+    gives them), the shared device and host headers and the C header: a stored
+    HBM traffic figure is valid only for the sources it was measured on."""
     import hashlib
 
-    h = hashlib.sha256()
-    files = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.hpp")))
+    files = sorted({KERNEL_SOURCES[k.split("<")[0]] for k in kernels})
+    files = [os.path.join(CSRC, f) for f in files + ["lw_device.hpp", "lw_internal.hpp"]]
     files.append(os.path.join(ROOT, "include", "lw.h"))
+    h = hashlib.sha256()
     for f in files:
         h.update(os.path.basename(f).encode())
         with open(f, "rb") as fh:
@@ -228,7 +234,7 @@ def source_hash():
 def stored_traffic(workload, n_tok, kernel):
     """HBM bytes per launch of `kernel` from the calibrated rocprofv3 FETCH_SIZE
     and WRITE_SIZE summary in profiles/, or None when there is none for these
-    sources."""
+    sources (the hash covers the sources of every kernel the summary lists)."""
     path = os.path.join(ROOT, "profiles", "hbm_traffic_%s_nt%d.txt" % (workload, n_tok))
     if not os.path.exists(path):
         return None
@@ -238,7 +244,8 @@ def stored_traffic(workload, n_tok, kernel):
             if "=" in line and not line.startswith((" ", "#", "|")):
                 k, v = line.strip().split("=", 1)
                 vals[k.strip()] = v.strip()
-    if vals.get("source_sha256") != source_hash():
+    kernels = [k[len("hbm_bytes_per_launch["):-1] for k in vals if k.startswith("hbm_bytes_per_launch[")]
+    if not kernels or vals.get("source_sha256") != source_hash(kernels):
         return None
     try:
         return float(vals["hbm_bytes_per_launch[%s]" % kernel])

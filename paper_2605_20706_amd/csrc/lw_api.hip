@@ -6,9 +6,10 @@
 // multiple of 2048 -> the VALU matrix-vector kernel with the activation in
 // registers, where its table has an entry for the shape; else one token ->
 // the VALU matrix-vector kernel with the activation in LDS; 2..16 tokens over
-// the 4-bit formats -> the matrix-core kernel with a block-diagonal activation
-// operand; Q8_0 with up to LW_GEMV_MAX_TOK tokens -> the VALU kernels, up to
-// 16 -> the matrix-core kernel with K split across waves; more tokens -> the
+// the 4-bit formats -> the matrix-core kernel (token rows against 16 weight
+// rows, one MFMA K step per 32-element block); Q8_0 with up to
+// LW_GEMV_MAX_TOK tokens -> the VALU kernels, up to 16 -> the matrix-core
+// kernel with K split across waves; more tokens -> the
 // tiled matrix-core (prefill) kernel. f16 weights use the VALU kernel in
 // token blocks of LW_GEMV_MAX_TOK for any token count.
 #include "lw_internal.hpp"

@@ -92,8 +92,8 @@ hipError_t launch_gemv_reg(int fmt, const uint8_t* W, const float* x, float* y, 
 bool skinny_supported(int fmt);
 hipError_t launch_skinny(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                          int64_t n_tok, const Planes& p, hipStream_t stream);
-// Matrix-core path for 2 <= n_tok <= 16 over the 4-bit formats (block-diagonal
-// activation operand; weights streamed once).
+// Matrix-core path for 2 <= n_tok <= 16 over the 4-bit formats (token rows
+// against 16 weight rows per MFMA; weights streamed once).
 bool multitok_supported(int fmt, int64_t n_tok);
 hipError_t launch_multitok(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                            int64_t n_tok, const Planes& p, hipStream_t stream);

@@ -9,9 +9,10 @@
 //
 // Precision (the reading shared by the matrix-core paths): B holds the exact
 // bf16 of the biased code 128 + q (bit pattern 0x4300 | q); X is split into a
-// bf16 high part and a bf16 low part (two MFMAs per block); per block
+// bf16 high part and a bf16 low part, both multiplied; per block
 // y += c1 * (P + k * S) - dm * S, with S the block sum of the operand actually
-// multiplied (hi + lo), obtained from the same A operands against a B of ones:
+// multiplied (hi + lo). k * S comes from the same A operands against a B of
+// the constant k (exact in bf16) and is the accumulator P starts from:
 //   Q4_0:     w = d (q - 8)         -> c1 = d,    k = -136, dm = 0
 //   Q4_K:     w = d sc q - dmin m   -> c1 = d sc, k = -128, dm = dmin m
 #include "lw_device.hpp"
@@ -100,11 +101,11 @@ struct StepScale<LW_Q4_K> {
         r2 = rec[2];
         dd = *reinterpret_cast<const uint32_t*>(P2 + 4 * sb);
     }
-    // c1 = d*sc_j and dm = dmin*m_j of the step's blocks, sub-blocks
+    // c1 = d*sc_j and dm = dmin*m_j/128 of the step's blocks, sub-blocks
     // j = 4(s&1) + 0..3 of the super-block: sc_j at record bit 6j, m_j at
     // bit 48 + 6j, cut out of one rotated word or one word pair each.
     __device__ void coef(uint32_t s, int, float* c1, float* dm) const {
-        const float d = half_bits_to_float(dd & 0xFFFFu), dmin = half_bits_to_float(dd >> 16);
+        const float d = half_bits_to_float(dd & 0xFFFFu), dmin = half_bits_to_float(dd >> 16) * (1.0f / 128.0f);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const uint32_t j = 4u * (s & 1u) + (uint32_t)i;
@@ -125,24 +126,33 @@ struct Stage {
 };
 
 // Few-token product with whole-block MFMAs: D = X . W^T per 32-element block,
-// A = X (16 token rows, tokens >= n_tok zero), B = the codes of 16 weight
-// rows. A step is 4 blocks (128 columns) of RG row tiles. Lane (g, i) loads
-// block 4s+g of row i of each tile (one 16-byte load, a whole block), and a
-// transpose across the lane groups gives it word g of each of the 4 blocks,
-// its B slice (elements 4g..4g+3 and 16+4g..16+4g+3) for the 4 MFMAs. D lands
-// as D[4g+v][i] = (token 4g+v, row i): one row per lane, so each lane applies
-// its row's block scale with no exchange.
+// A = X (token rows), B = the codes of 16 weight rows. A step is 4 blocks
+// (128 columns) of RG row tiles. Lane (g, i) loads block 4s+g of row i of
+// each tile (one 16-byte load, a whole block), and a transpose across the
+// lane groups gives it word g of each of the 4 blocks, its B slice (elements
+// 4g..4g+3 and 16+4g..16+4g+3) for the 4 MFMAs. D lands as D[4g+v][i]: one
+// weight row per lane, so each lane applies its row's block scale with no
+// exchange.
+// A rows: with PK (n_tok <= 8) rows 0..7 hold the bf16 high parts of tokens
+// 0..7 and rows 8..15 their low parts, so one MFMA per block multiplies both
+// halves and the two D rows of a token are added at the end; without PK (up
+// to 16 tokens) the rows are tokens and the low parts take a second MFMA.
+// Rows of tokens >= n_tok are zero.
+// The bias correction k * S enters as the MFMA accumulator: C = A . B_k, with
+// B_k the constant bf16 k, per block, shared by the row tiles. Then
+// y += c1 * P per block (Q4_K: also + dmin m / 128 * C, C being -128 S).
 // X: every step, the wave converts its 4 blocks of the n_tok token rows
 // densely (lane -> token, block, float4; NX float4 per lane; the loads of one
 // block are 128 contiguous bytes), hi/lo bf16 halves into its private LDS
-// slice in the A layout, then reads its A operands back. The slice's rows of
-// tokens >= n_tok are zeroed once and never written. Waves split K; their
+// slice in the A layout, then reads its A operands back. Waves split K; their
 // partials are summed through LDS at the end.
-template <int FMT, int NX, int RG>
+template <int FMT, int NX, int RG, bool PK>
 __global__ void __launch_bounds__(64 * kMaxWaves)
     multitok_kernel(const uint8_t* __restrict__ W, const float* __restrict__ x, float* __restrict__ y, int64_t M,
                      int64_t K, int ntok, int64_t off1, int64_t off2) {
     extern __shared__ float4 smem4[];
+    constexpr int NH = PK ? 1 : 2;              // A planes: hi/lo packed in one, or hi and lo
+    constexpr int kSlice = NH * 4 * 64 + 1;     // the wave's LDS slice, in 16-byte slots
     const int nw = blockDim.x >> 6;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -179,22 +189,20 @@ __global__ void __launch_bounds__(64 * kMaxWaves)
         xlive[e] = xt[e] < ntok;
         xp[e] = x + (int64_t)(xlive[e] ? xt[e] : ntok - 1) * K + 32 * xj[e] + 4 * xm[e];
     }
-    // the wave's A slice: [hi, lo][block j][64 slots] of 16 bytes, then a
-    // spare 16 bytes that absorb the writes of padding items. Lane (g, n)'s
-    // operand of block j sits in slot 16g + (n ^ (2g + (j & 1) + 8(j >> 1))):
-    // a permutation of each 64-slot row, so the reads stay conflict-free,
-    // which spreads the 8-byte writes of one instruction (items of fixed
-    // token, 4 blocks x 8 float4) over distinct banks.
-    auto xslot = [](int gg, int t, int j) { return 16 * gg + (t ^ (2 * gg + (j & 1) + 8 * (j >> 1))); };
-    constexpr int kSpare = 2 * 512;
-    uint2* xs = reinterpret_cast<uint2*>(smem4 + (size_t)wave * 513);
+    // the wave's A slice: [plane][block j][64 slots] of 16 bytes, then a
+    // spare 16 bytes that absorb the writes of padding items. A row n of lane
+    // group gg in block j sits in slot 16gg + (n ^ (2gg + (j & 1) + 8(j >> 1))):
+    // a permutation of each 16-slot group, so the reads stay conflict-free,
+    // which spreads the 8-byte writes of one instruction (items of one token,
+    // 4 blocks x 8 float4) over distinct banks.
+    auto xslot = [](int gg, int n, int j) { return 16 * gg + (n ^ (2 * gg + (j & 1) + 8 * (j >> 1))); };
+    constexpr int kSpare = 2 * (kSlice - 1);
+    uint2* xs = reinterpret_cast<uint2*>(smem4 + (size_t)wave * kSlice);
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            xs[2 * ((h * 4 + j) * 64 + lane)] = uint2{0u, 0u};
-            xs[2 * ((h * 4 + j) * 64 + lane) + 1] = uint2{0u, 0u};
-        }
+    for (int h = 0; h < NH * 4; ++h) {
+        xs[2 * (h * 64 + lane)] = uint2{0u, 0u};
+        xs[2 * (h * 64 + lane) + 1] = uint2{0u, 0u};
+    }
 
     auto load = [&](Stage<FMT, NX, RG>& st, int s) __attribute__((always_inline)) {
 #pragma unroll
@@ -206,15 +214,18 @@ __global__ void __launch_bounds__(64 * kMaxWaves)
         for (int e = 0; e < NX; ++e) st.xv[e] = *reinterpret_cast<const float4*>(xp[e] + 128 * s);
     };
 
-    const bf16x8 ones = __builtin_bit_cast(bf16x8, u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u});
-    const float bias_k = FMT == LW_Q4_0 ? -136.0f : -128.0f;  // bias (and the Q4_0 offset) per unit of S
+    // bf16 k: -136 (Q4_0: code bias 128 plus the format's offset 8) or -128
+    const uint32_t kb = FMT == LW_Q4_0 ? 0xC308C308u : 0xC300C300u;
+    const bf16x8 bias_b = __builtin_bit_cast(bf16x8, u32x4{kb, kb, kb, kb});
     f32x4 acc[RG];
 #pragma unroll
     for (int q = 0; q < RG; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     auto consume = [&](const Stage<FMT, NX, RG>& st, int s) __attribute__((always_inline)) {
         // X of the step -> hi/lo halves in the A layout: item (t, j, m) is
-        // half m >> 2 of the 16 bytes of lane 16 (m & 3) + t in block j
+        // half m >> 2 of the 16 bytes of lane group m & 3 in block j, A row
+        // t (high part) and 8 + t (low part) when packed, else row t of
+        // plane 0 and of plane 1
         __builtin_amdgcn_wave_barrier();
 #pragma unroll
         for (int e = 0; e < NX; ++e) {
@@ -232,27 +243,28 @@ __global__ void __launch_bounds__(64 * kMaxWaves)
                     uint32_t, __builtin_convertvector((f32x2{v[2 * p2] - h0, v[2 * p2 + 1] - h1}), bf16x2));
             }
             // an item of a token >= n_tok goes to the slice's spare slot
-            const int slot = xslot(xm[e] & 3, xt[e], xj[e]);
-            const int half = xm[e] >> 2;
-            const int ih = xlive[e] ? 2 * ((0 * 4 + xj[e]) * 64 + slot) + half : kSpare;
-            const int il = xlive[e] ? 2 * ((1 * 4 + xj[e]) * 64 + slot) + half : kSpare;
+            const int gg = xm[e] & 3, half = xm[e] >> 2, j = xj[e], t = xt[e];
+            const int sh = PK ? j * 64 + xslot(gg, t, j) : j * 64 + xslot(gg, t, j);
+            const int sl = PK ? j * 64 + xslot(gg, 8 + t, j) : (4 + j) * 64 + xslot(gg, t, j);
+            const int ih = xlive[e] ? 2 * sh + half : kSpare;
+            const int il = xlive[e] ? 2 * sl + half : kSpare;
             xs[ih] = uint2{hw[0], hw[1]};
             xs[il] = uint2{lw[0], lw[1]};
         }
         __builtin_amdgcn_wave_barrier();
-        bf16x8 ah[4], al[4];
+        bf16x8 a[NH][4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int h = 0; h < NH; ++h)
+                a[h][j] = __builtin_bit_cast(bf16x8,
+                                             reinterpret_cast<const float4*>(xs)[(h * 4 + j) * 64 + xslot(g, n16, j)]);
+        // C = k * (block sums of the multiplied values), in the D layout
+        f32x4 C[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int sl = xslot(g, n16, j);
-            ah[j] = __builtin_bit_cast(bf16x8, reinterpret_cast<const float4*>(xs)[(0 * 4 + j) * 64 + sl]);
-            al[j] = __builtin_bit_cast(bf16x8, reinterpret_cast<const float4*>(xs)[(1 * 4 + j) * 64 + sl]);
-        }
-        // block sums of the multiplied values, in the D layout (token 4g+v)
-        f32x4 S[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            S[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[j], ones, f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-            S[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[j], ones, S[j], 0, 0, 0);
+            C[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[0][j], bias_b, f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+            if constexpr (!PK) C[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[1][j], bias_b, C[j], 0, 0, 0);
         }
 #pragma unroll
         for (int q = 0; q < RG; ++q) {
@@ -262,12 +274,12 @@ __global__ void __launch_bounds__(64 * kMaxWaves)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const bf16x8 bq = biased_codes(wq[j]);
-                f32x4 P = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[j], bq, f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-                P = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[j], bq, P, 0, 0, 0);
+                f32x4 P = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[0][j], bq, C[j], 0, 0, 0);
+                if constexpr (!PK) P = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[1][j], bq, P, 0, 0, 0);
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
-                    float o = __builtin_fmaf(c1[j], __builtin_fmaf(bias_k, S[j][v], P[v]), acc[q][v]);
-                    if constexpr (FMT == LW_Q4_K) o = __builtin_fmaf(-dm[j], S[j][v], o);
+                    float o = __builtin_fmaf(c1[j], P[v], acc[q][v]);
+                    if constexpr (FMT == LW_Q4_K) o = __builtin_fmaf(dm[j], C[j][v], o);
                     acc[q][v] = o;
                 }
             }
@@ -300,10 +312,11 @@ __global__ void __launch_bounds__(64 * kMaxWaves)
     if (s + 1 < s1) consume(sb, s + 1);
     if (s + 2 < s1) consume(sa, s + 2);
 
-    // sum the partials of the waves: lane holds tokens 4g + v of row 16q + n16
+    // sum the partials of the waves (and, packed, the high and low D rows of
+    // a token): lane holds D rows 4g + v of weight row 16q + n16
     __syncthreads();
     constexpr int kRows = 16 * RG;
-    float* red = reinterpret_cast<float*>(smem4);  // [nw][16 tokens][kRows]
+    float* red = reinterpret_cast<float*>(smem4);  // [nw][16 D rows][kRows]
 #pragma unroll
     for (int q = 0; q < RG; ++q)
 #pragma unroll
@@ -313,24 +326,37 @@ __global__ void __launch_bounds__(64 * kMaxWaves)
         const int t = it / kRows, r = it % kRows;
         if (t < ntok && row0 + r < M) {
             float o = 0.f;
-            for (int p = 0; p < nw; ++p) o += red[(p * 16 + t) * kRows + r];
+            for (int p = 0; p < nw; ++p) {
+                o += red[(p * 16 + t) * kRows + r];
+                if constexpr (PK) o += red[(p * 16 + 8 + t) * kRows + r];
+            }
             y[(int64_t)t * M + row0 + r] = o;
         }
     }
 }
 
-template <int FMT, int NX, int RG>
+template <int FMT, int NX, int RG, bool PK>
 hipError_t launch_mt(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
                       const Planes& p, int nw, hipStream_t stream) {
     const int64_t grid = (M + 16 * RG - 1) / (16 * RG);
     if (grid > 0x7fffffff || nw < 1 || nw > kMaxWaves) return hipErrorInvalidConfiguration;
-    size_t lds = (size_t)nw * 513 * 16;                       // A slices, 8 KiB + 16 B per wave
+    if (n_tok > (PK ? 8 : 16) || 32 * n_tok > 64 * NX) return hipErrorInvalidValue;
+    size_t lds = (size_t)nw * (PK ? 257 : 513) * 16;          // A slices, 4 or 8 KiB + 16 B per wave
     const size_t red = (size_t)nw * 16 * (16 * RG) * 4;       // final partial sums
     if (lds < red) lds = red;
-    if (query_only(kernel_name<Name_multitok_kernel, FMT, NX, RG>())) return hipSuccess;
-    hipLaunchKernelGGL((multitok_kernel<FMT, NX, RG>), dim3((unsigned)grid), dim3(64 * nw), lds, stream, W, x, y,
-                       M, K, (int)n_tok, p.off1, p.off2);
+    if (query_only(kernel_name<Name_multitok_kernel, FMT, NX, RG, PK>())) return hipSuccess;
+    hipLaunchKernelGGL((multitok_kernel<FMT, NX, RG, PK>), dim3((unsigned)grid), dim3(64 * nw), lds, stream, W, x,
+                       y, M, K, (int)n_tok, p.off1, p.off2);
     return hipGetLastError();
+}
+
+template <int FMT, int RG>
+hipError_t launch_rg(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
+                      const Planes& p, int nw, hipStream_t stream) {
+    // 32 n_tok floats per step over 64 lanes, in float4s
+    if (n_tok <= 4) return launch_mt<FMT, 2, RG, true>(W, x, y, M, K, n_tok, p, nw, stream);
+    if (n_tok <= 8) return launch_mt<FMT, 4, RG, true>(W, x, y, M, K, n_tok, p, nw, stream);
+    return launch_mt<FMT, 8, RG, false>(W, x, y, M, K, n_tok, p, nw, stream);
 }
 
 template <int FMT>
@@ -340,19 +366,8 @@ hipError_t launch_f(const uint8_t* W, const float* x, float* y, int64_t M, int64
     const bool rg2 = (M + 31) / 32 >= cus;
     const int64_t wgs = rg2 ? (M + 31) / 32 : (M + 15) / 16;
     const int nw = wgs >= 2 * cus ? 4 : 8;
-    const int nx = n_tok <= 4 ? 2 : (n_tok <= 8 ? 4 : 8);  // 32 * n_tok floats over 64 lanes, in float4s
-    if (rg2) {
-        switch (nx) {
-        case 2: return launch_mt<FMT, 2, 2>(W, x, y, M, K, n_tok, p, nw, stream);
-        case 4: return launch_mt<FMT, 4, 2>(W, x, y, M, K, n_tok, p, nw, stream);
-        default: return launch_mt<FMT, 8, 2>(W, x, y, M, K, n_tok, p, nw, stream);
-        }
-    }
-    switch (nx) {
-    case 2: return launch_mt<FMT, 2, 1>(W, x, y, M, K, n_tok, p, nw, stream);
-    case 4: return launch_mt<FMT, 4, 1>(W, x, y, M, K, n_tok, p, nw, stream);
-    default: return launch_mt<FMT, 8, 1>(W, x, y, M, K, n_tok, p, nw, stream);
-    }
+    return rg2 ? launch_rg<FMT, 2>(W, x, y, M, K, n_tok, p, nw, stream)
+               : launch_rg<FMT, 1>(W, x, y, M, K, n_tok, p, nw, stream);
 }
 
 }  // namespace

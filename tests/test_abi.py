@@ -117,7 +117,7 @@ def test_kernel_selection_table(lib):
     One token: the register-activation kernel when K is a whole number of
     2048-element chunks and its table has the shape, else the LDS-activation
     kernel; two tokens over the 4-bit formats: the register kernel; 3..16
-    tokens over the 4-bit formats: the block-diagonal matrix-core kernel;
+    tokens over the 4-bit formats: the few-token matrix-core kernel;
     more: the tiled matrix-core kernel."""
     from paper_2605_20706_amd import synth
 
