@@ -116,9 +116,10 @@ def test_kernel_selection_table(lib):
     """The kernels the workloads' shapes select (no launch: a host-only query).
     One token: the register-activation kernel when K is a whole number of
     2048-element chunks and its table has the shape, else the LDS-activation
-    kernel; two tokens over the 4-bit formats: the register kernel; 3..16
-    tokens over the 4-bit formats: the few-token matrix-core kernel;
-    more: the tiled matrix-core kernel."""
+    kernel; two tokens over the 4-bit formats: the register kernel; 3..8
+    tokens over the 4-bit formats: the pair-step matrix-core kernel, 9..16 the
+    few-token one with two MFMAs per block; more: the tiled matrix-core
+    kernel."""
     from paper_2605_20706_amd import synth
 
     def kind(fmt, M, K, nt):
@@ -135,7 +136,9 @@ def test_kernel_selection_table(lib):
     assert kind(Q4_K, 6144, 4096, 1) == "gemv1_kernel"        # 8B qkv: too few rows per wave
     assert kind(Q4_0, 100, 2304, 1) == "gemv1_kernel"         # K not whole chunks
     assert kind(Q4_0, 14336, 4096, 2) == "gemv1r_kernel"
-    assert kind(Q4_0, 14336, 4096, 4) == "multitok_kernel"
+    assert kind(Q4_0, 14336, 4096, 4) == "multitok_pk_kernel"
+    assert kind(Q4_K, 4096, 14336, 8) == "multitok_pk_kernel"
+    assert kind(Q4_K, 14336, 4096, 9) == "multitok_kernel"
     assert kind(Q4_0, 14336, 4096, 512) == "gemm_kernel"
     assert kind(F16, 2048, 2048, 1) == "gemv1_kernel"
     assert kind(Q8_0, 2048, 2048, 12) == "skinny_kernel"
