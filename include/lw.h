@@ -65,6 +65,15 @@
 extern "C" {
 #endif
 
+/* The entry points below are the library's only exported symbols (it is
+ * built with hidden visibility), so no symbol of a host program can take the
+ * place of one of its internal functions. */
+#if defined(__GNUC__) || defined(__clang__)
+#define LW_API __attribute__((visibility("default")))
+#else
+#define LW_API
+#endif
+
 /* Weight formats (Sec. 2.2: f16 storage, legacy symmetric blocks of 32,
  * K-quant super-blocks of 256 with double-quantized scales and mins). */
 typedef enum { LW_F16 = 0, LW_Q8_0 = 1, LW_Q4_0 = 2, LW_Q4_K = 3 } lw_fmt;
@@ -116,7 +125,7 @@ enum {
  * part and a bfloat16 low part, accumulating in float32. Every path's error
  * relative to sum_k |w * x| stays below 1e-4.
  */
-int lw_matvec(int fmt, const void* W, const float* x, float* y,
+LW_API int lw_matvec(int fmt, const void* W, const float* x, float* y,
               int64_t M, int64_t K, int64_t n_tok, void* stream);
 
 /*
@@ -127,17 +136,17 @@ int lw_matvec(int fmt, const void* W, const float* x, float* y,
  *   out  device; float32 [n], 16-byte aligned; must not overlap W.
  *   n    element count, 0 <= n <= LW_MAX_ELEMS, a multiple of 256.
  */
-int lw_dequant(int fmt, const void* W, float* out, int64_t n);
+LW_API int lw_dequant(int fmt, const void* W, float* out, int64_t n);
 
 /*
  * lw_weight_bytes — size in bytes of n packed elements (plane 0 through the
  * end of the last plane). Returns LW_EFMT, LW_EINVAL (n < 0 or too large) or
  * LW_ESHAPE (n not a multiple of 256) as a negative value. Host-only.
  */
-int64_t lw_weight_bytes(int fmt, int64_t n);
+LW_API int64_t lw_weight_bytes(int fmt, int64_t n);
 
 /* lw_strerror — static, NUL-terminated description of a return code. */
-const char* lw_strerror(int code);
+LW_API const char* lw_strerror(int code);
 
 /*
  * lw_kernel_name — the kernel lw_matvec(fmt, W, x, y, M, K, n_tok, stream)
@@ -154,7 +163,7 @@ const char* lw_strerror(int code);
  * the selection may depend on the compute-unit count of the current device
  * (256 when there is none).
  */
-const char* lw_kernel_name(int fmt, int64_t M, int64_t K, int64_t n_tok);
+LW_API const char* lw_kernel_name(int fmt, int64_t M, int64_t K, int64_t n_tok);
 
 #ifdef __cplusplus
 }

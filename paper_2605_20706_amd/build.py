@@ -21,6 +21,8 @@ FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
+    # export only the C ABI (LW_API in lw.h): internal symbols stay inside
+    "-fvisibility=hidden", "-fvisibility-inlines-hidden",
 ]
 
 

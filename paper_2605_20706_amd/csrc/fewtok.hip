@@ -1,0 +1,479 @@
+// Few-token product (2 <= n_tok <= 8) over the 4-bit formats on the matrix
+// cores, with the activations converted once per workgroup.
+//
+// Y[t][r] = sum_k value(W, r*K + k) * X[t][k]: the decode product of Sec. 2.1
+// for a small batch of tokens. The weights are read from HBM exactly once and
+// dequantized in registers (Sec. 3.3); the contraction runs on
+// v_mfma_f32_16x16x32_bf16, one MFMA K step per 32-element block, so each
+// block's scale applies to its own partial product.
+//
+// MFMA roles (layout in lw_mfma.hpp): A = the activations, 16 rows = the bf16
+// high parts of tokens 0..7 (rows 0..7) and the bf16 low parts (rows 8..15);
+// B = the biased codes 128 + q of 16 weight rows; D[4g+v][n] = token half
+// 4g+v of weight row n. Rows of tokens >= n_tok are zero.
+//
+// Work split: workgroup b owns the rows [b*rpw, min((b+1)*rpw, M)), about
+// M / #CU of them, so every compute unit streams the same number of weight
+// bytes. They form ntq tiles of 16 rows (a tile past the last row repeats
+// it). The nw waves are nw/P tile slots x P parts of K: wave w serves tiles
+// w/P, w/P + nw/P, ... and, of every window of ws super-blocks (256 columns
+// each), the (w mod P)-th of P equal parts. The unit of work is one
+// super-block of one tile: 16 rows x 128 code bytes (two 16-byte loads per
+// lane: lane (g, n) loads block 4h + g of row n, and a transpose across the
+// lane groups gives it word g of blocks 4h..4h+3) plus the super-block's
+// scales. Each wave keeps two units in flight; the loads of a unit are issued
+// two units ahead of its use, across window boundaries.
+//
+// Activations: per window, all threads convert X[t][window] into LDS in the
+// A layout (8 KiB per super-block): thread item (t, block, g) reads the two
+// float4 of its lane group's elements, splits them into bf16 high and low
+// parts and writes one 16-byte slot of row t and one of row 8 + t. The MFMA
+// reads one slot per lane per block. Barriers wait only for LDS, never for the
+// weight loads in flight.
+//
+// Precision (the reading shared by the matrix-core paths): the codes enter as
+// the exact bf16 of 128 + q; X = high + low to 16 significant bits; per block
+// y += c1 * (P + k * S) + dm * (k * S)-term, with S the block sum of the
+// multiplied operand, computed by the same MFMA against a B of the constant k
+// and used as P's accumulator:
+//   Q4_0:     w = d (q - 8)         -> c1 = d,    k = -136, dm = 0
+//   Q4_K:     w = d sc q - dmin m   -> c1 = d sc, k = -128, dm = dmin m / 128
+// Accumulation is f32 throughout.
+#include "lw_internal.hpp"
+#include "lw_mfma.hpp"
+
+namespace lw {
+namespace {
+
+struct Name_fewtok_kernel {
+    static constexpr const char* base = "fewtok_kernel";
+};
+
+constexpr int kFtMaxWaves = 16;  // waves per workgroup
+constexpr int kFtWinSB = 16;     // super-blocks per window: 16 x 8 blocks x 1 KiB of A = 128 KiB of LDS
+constexpr int kFtMaxTpw = 4;     // tiles per wave when the waves do not split K
+template <int FMT>
+constexpr int kFtRing = FMT == LW_Q4_K ? 2 : 3;  // units in flight per wave (Q4_K: fewer, its scales take more registers)
+
+// Scale data of one super-block (8 blocks, 256 columns) of one weight row.
+template <int FMT>
+struct SbScale;
+
+template <>
+struct SbScale<LW_Q4_0> {
+    u32x4 d;  // binary16 d of the 8 blocks
+    __device__ void load(const uint8_t* P1, const uint8_t*, uint64_t sbi) {
+        d = *reinterpret_cast<const u32x4*>(P1 + 16 * sbi);
+    }
+    // c1 of blocks 4h .. 4h+3 (d); dm is unused
+    __device__ void coef(int h, float* c1, float*) const {
+        const uint32_t a = h ? d[2] : d[0], b = h ? d[3] : d[1];
+        c1[0] = half_bits_to_float(a & 0xFFFFu);
+        c1[1] = half_bits_to_float(a >> 16);
+        c1[2] = half_bits_to_float(b & 0xFFFFu);
+        c1[3] = half_bits_to_float(b >> 16);
+    }
+};
+
+template <>
+struct SbScale<LW_Q4_K> {
+    uint32_t r0, r1, r2, dd;  // the 96-bit scale record and {d, dmin}
+    __device__ void load(const uint8_t* P1, const uint8_t* P2, uint64_t sbi) {
+        const uint32_t* rec = reinterpret_cast<const uint32_t*>(P1 + 12 * sbi);
+        r0 = rec[0];
+        r1 = rec[1];
+        r2 = rec[2];
+        dd = *reinterpret_cast<const uint32_t*>(P2 + 4 * sbi);
+    }
+    // c1 = d * sc_j and dm = dmin * m_j / 128 of sub-blocks j = 4h .. 4h+3:
+    // sc_j sits at record bit 6j, m_j at bit 48 + 6j (one funnel shift each;
+    // h is a compile-time constant at every use, so the word choice is too)
+    __device__ void coef(int h, float* c1, float* dm) const {
+        const float d = half_bits_to_float(dd & 0xFFFFu), dmin = half_bits_to_float(dd >> 16) * (1.0f / 128.0f);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t j = 4u * (uint32_t)h + (uint32_t)i;
+            const uint32_t ts = 6u * j, tm = 16u + 6u * j;
+            const uint32_t sc_w = __builtin_amdgcn_alignbit(r1, ts < 32u ? r0 : r1, ts & 31u);
+            const uint32_t m_w = __builtin_amdgcn_alignbit(r2, tm < 32u ? r1 : r2, tm & 31u);
+            c1[i] = d * (float)(sc_w & 63u);
+            dm[i] = dmin * (float)(m_w & 63u);
+        }
+    }
+};
+
+template <int FMT>
+struct Unit {
+    u32x4 c[2];  // code lines: block 8s + 4h + g of the lane's row, h = 0, 1
+    SbScale<FMT> sc;
+    int i, s;  // tile (of the wave), super-block
+};
+
+// LDS-only barrier: waits for this wave's LDS traffic, not for its global
+// loads (the weight units in flight stay in flight).
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+template <int FMT, int TPW>
+__global__ void __launch_bounds__(64 * kFtMaxWaves)
+    fewtok_kernel(const uint8_t* __restrict__ W, const float* __restrict__ x, float* __restrict__ y, int M, int K,
+                  int ntok, int64_t off1, int64_t off2, int rpw, int ntq, int P, int ws) {
+    extern __shared__ uint4 lds[];
+    const int nthr = blockDim.x;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 4, n = lane & 15;
+    const int nslots = (nthr >> 6) / P;
+    const int ts = wave / P, kp = wave - ts * P;
+    const int nsb = K >> 8;
+    const int nwin = (nsb + ws - 1) / ws;
+    const int64_t r0 = (int64_t)blockIdx.x * rpw;
+    const int64_t rl = (r0 + rpw < (int64_t)M ? r0 + rpw : (int64_t)M) - 1;  // last row of the workgroup
+    const uint8_t* P1 = W + off1;
+    const uint8_t* P2 = W + off2;
+    const uint64_t rowb = (uint64_t)K / 2u;  // code bytes per row
+
+    // the wave's tiles: the lane's row in each (past the workgroup's last row:
+    // that row again, whose lines are read anyway)
+    int ntl = 0;
+#pragma unroll
+    for (int i = 0; i < TPW; ++i)
+        if (ts + i * nslots < ntq) ntl = i + 1;
+    auto row_of = [&](int i) __attribute__((always_inline)) {
+        const int64_t rr = r0 + 16 * (int64_t)(ts + i * nslots) + n;
+        return (uint64_t)(rr <= rl ? rr : rl);
+    };
+
+    // The wave's units of window w: for each of its ntl tiles, the
+    // super-blocks [w*ws + kp*cnt/P, w*ws + (kp+1)*cnt/P), cnt = the
+    // window's super-blocks; unit u of the window is tile u / len,
+    // super-block a + u mod len. All wave-uniform scalar work.
+    auto part = [&](int win, int& a, int& len) __attribute__((always_inline)) {
+        const int w0 = win * ws;
+        const int cnt = (nsb - w0) < ws ? (nsb - w0) : ws;
+        a = w0 + (kp * cnt) / P;
+        len = w0 + ((kp + 1) * cnt) / P - a;
+    };
+    int wa = 0, wlen = 0, wn = 0;  // the current window's part and unit count
+    // Loads unit u of the current window into stage st; past the window's
+    // last unit (or with no unit at all) it loads that last unit (or the
+    // window's first super-block of the first tile) again, so every load is
+    // issued unconditionally.
+    auto load = [&](Unit<FMT>& st, int u) __attribute__((always_inline)) {
+        int i = 0, sb = wa < nsb ? wa : nsb - 1;
+        if (wn > 0) {
+            const int ue = u < wn ? u : wn - 1;
+            i = ue / wlen;
+            sb = wa + (ue - i * wlen);
+        }
+        const uint64_t r = row_of(i);
+        const uint8_t* cp = W + r * rowb + 128u * (uint32_t)sb + 16u * (uint32_t)g;
+        st.c[0] = *reinterpret_cast<const u32x4*>(cp);
+        st.c[1] = *reinterpret_cast<const u32x4*>(cp + 64);
+        st.sc.load(P1, P2, r * (uint64_t)nsb + (uint64_t)sb);
+        st.i = i;
+        st.s = sb;
+    };
+
+    // X window -> LDS in the A layout. Slot of (window block lb, lane group
+    // gg, A row a): lb*64 + gg*16 + ((a + 4*gg) & 15). The MFMA read of a
+    // block (lane (g, n) reads row n of lane group g) covers 64 distinct
+    // slots, and consecutive conversion items write distinct 16-byte bank
+    // groups. An item is (window block lb, token t < n_tok, lane group gg),
+    // item index = 4 (lb * n_tok + t) + gg: two float4 loads, a high/low split
+    // and two 16-byte writes (rows t and 8 + t). Rows of absent tokens are
+    // zeroed in the first window and stay zero. A batch issues the loads of
+    // kXb items per thread before it converts any. The division by n_tok
+    // (<= 8) is a multiplication by ceil(2^20 / n_tok), exact for the item
+    // counts here (below 2^13 per window).
+    constexpr int kXb = TPW >= 4 ? 2 : 4;
+    const uint32_t tmag = ((1u << 20) + (uint32_t)ntok - 1u) / (uint32_t)ntok;
+    auto win_items = [&](int win) __attribute__((always_inline)) {
+        const int w0 = win * ws;
+        return 32 * ntok * ((nsb - w0) < ws ? (nsb - w0) : ws);  // 4 items per block and token, 8 blocks per super-block
+    };
+    auto xload = [&](int win, int base, float4* v0, float4* v1) __attribute__((always_inline)) {
+        const int items = win_items(win);
+#pragma unroll
+        for (int k = 0; k < kXb; ++k) {
+            // clamped index: every load is issued
+            int it = base + tid + k * nthr;
+            it = it < items ? it : items - 1;
+            const uint32_t q = (uint32_t)it >> 2;
+            const int lb = (int)((q * tmag) >> 20);
+            const int t = (int)q - lb * ntok;
+            const float* xp = x + (int64_t)t * K + 32 * (int64_t)(8 * win * ws + lb) + 4 * (it & 3);
+            v0[k] = *reinterpret_cast<const float4*>(xp);
+            v1[k] = *reinterpret_cast<const float4*>(xp + 16);
+        }
+    };
+    auto xstore = [&](int win, int base, const float4* v0, const float4* v1) __attribute__((always_inline)) {
+        const int items = win_items(win);
+#pragma unroll
+        for (int k = 0; k < kXb; ++k) {
+            const int it = base + tid + k * nthr;
+            if (it < items) {
+                const int gg = it & 3;
+                const uint32_t q = (uint32_t)it >> 2;
+                const int lb = (int)((q * tmag) >> 20);
+                const int t = (int)q - lb * ntok;
+                uint4 hi, lo;
+                split_bf16x2(v0[k].x, v0[k].y, hi.x, lo.x);
+                split_bf16x2(v0[k].z, v0[k].w, hi.y, lo.y);
+                split_bf16x2(v1[k].x, v1[k].y, hi.z, lo.z);
+                split_bf16x2(v1[k].z, v1[k].w, hi.w, lo.w);
+                lds[lb * 64 + gg * 16 + ((t + 4 * gg) & 15)] = hi;
+                lds[lb * 64 + gg * 16 + ((t + 8 + 4 * gg) & 15)] = lo;
+            }
+        }
+    };
+    auto convert_rest = [&](int win, int first) __attribute__((always_inline)) {
+        const int items = win_items(win);
+        for (int base = first; base < items; base += kXb * nthr) {
+            float4 w0[kXb], w1[kXb];
+            xload(win, base, w0, w1);
+            xstore(win, base, w0, w1);
+        }
+    };
+    auto zero_rows = [&]() __attribute__((always_inline)) {
+        const int nz = 8 - ntok;
+        const int items = 32 * 8 * (nsb < ws ? nsb : ws);  // (block, row slot r < 8, lane group) of window 0
+        const uint4 z = {0u, 0u, 0u, 0u};
+        for (int it = tid; it < items; it += nthr) {
+            const int gg = it & 3;
+            const int q = it >> 2;
+            const int lb = q >> 3, r = q & 7;  // r < 8: row index among the 8 - ntok absent ones when r < nz
+            if (r < nz) {
+                const int t = ntok + r;
+                lds[lb * 64 + gg * 16 + ((t + 4 * gg) & 15)] = z;
+                lds[lb * 64 + gg * 16 + ((t + 8 + 4 * gg) & 15)] = z;
+            }
+        }
+    };
+
+    // bf16 k: -136 (Q4_0: code bias 128 plus the format's offset 8) or -128
+    const uint32_t kb = FMT == LW_Q4_0 ? 0xC308C308u : 0xC300C300u;
+    const bf16x8 bias_b = __builtin_bit_cast(bf16x8, u32x4{kb, kb, kb, kb});
+    // the lane's A slot within a block: g * 16 + ((n + 4g) & 15)
+    const int aoff = g * 16 + ((n + 4 * g) & 15);
+
+    f32x4 acc[TPW];
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    int cur = 0;  // the window in LDS
+    auto consume = [&](const Unit<FMT>& u) __attribute__((always_inline)) {
+        const int b0 = 8 * (u.s - cur * ws);  // window block of the super-block's first block
+        f32x4 t = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            // four blocks: A slices from LDS, the bias term k * S as an MFMA
+            // of A against the constant k, codes decoded, the products with
+            // the bias term as accumulator, then the scales
+            bf16x8 a[4];
+            f32x4 C[4], Pm[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) a[j] = __builtin_bit_cast(bf16x8, lds[(b0 + 4 * h + j) * 64 + aoff]);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                C[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[j], bias_b, f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+            const u32x4 wq = quad_transpose(u.c[h]);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) Pm[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[j], biased_codes(wq[j]), C[j], 0, 0, 0);
+            float c1[4], dm[4];
+            u.sc.coef(h, c1, dm);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    float o = __builtin_fmaf(c1[j], Pm[j][v], t[v]);
+                    if constexpr (FMT == LW_Q4_K) o = __builtin_fmaf(dm[j], C[j][v], o);
+                    t[v] = o;
+                }
+        }
+        // add to the unit's tile without a branch (a branch here costs the
+        // loop its exact load waits)
+        if constexpr (TPW == 1) {
+            acc[0] += t;
+        } else {
+#pragma unroll
+            for (int i = 0; i < TPW; ++i) {
+                const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+                acc[i] += u.i == i ? t : z;
+            }
+        }
+    };
+
+    // Per window: the first x batch's loads, then the window's first kFtRing
+    // units' weight loads (both issued while the previous window is still in
+    // use), then, once every wave is done with the previous window, the
+    // conversion; the weights stream in meanwhile. Within a window the units
+    // are consumed in groups of kFtRing, each stage refilled with the unit
+    // kFtRing ahead (unconditionally, past the window's end with its last
+    // unit again, so the waits stay exact); the last partial group only
+    // consumes.
+    constexpr int R = kFtRing<FMT>;
+    Unit<FMT> ring[R];
+    float4 v0[kXb], v1[kXb];
+    part(0, wa, wlen);
+    wn = ntl * wlen;
+    zero_rows();
+    xload(0, 0, v0, v1);
+#pragma unroll
+    for (int d = 0; d < R; ++d) load(ring[d], d);
+    for (;;) {
+        xstore(cur, 0, v0, v1);
+        convert_rest(cur, kXb * nthr);
+        lds_barrier();
+        // the first units are needed now anyway: waiting for every load here
+        // (vmcnt(0)) leaves the steady loop below a clean entry state, so its
+        // own waits are exact (one stage at a time)
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+        int k = 0;
+        for (; k + R <= wn; k += R) {
+#pragma unroll
+            for (int d = 0; d < R; ++d) {
+                consume(ring[d]);
+                __builtin_amdgcn_sched_barrier(0);
+                load(ring[d], k + d + R);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+#pragma unroll
+        for (int d = 0; d < R - 1; ++d)
+            if (k + d < wn) consume(ring[d]);
+        if (cur + 1 >= nwin) break;
+        ++cur;
+        part(cur, wa, wlen);
+        wn = ntl * wlen;
+        xload(cur, 0, v0, v1);
+#pragma unroll
+        for (int d = 0; d < R; ++d) load(ring[d], d);
+        lds_barrier();  // every wave is done with the previous window
+    }
+
+    if (P == 1) {
+        // whole tiles per wave: lanes 0..31 hold the high parts of tokens
+        // 4g + v, lanes 32..63 the low parts of the same tokens
+#pragma unroll
+        for (int i = 0; i < TPW; ++i) {
+            if (i < ntl) {
+                const int64_t rr = r0 + 16 * (int64_t)(ts + i * nslots) + n;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const float o = acc[i][v] + __shfl_xor(acc[i][v], 32);
+                    const int t = 4 * g + v;
+                    if (g < 2 && t < ntok && rr <= rl) y[(int64_t)t * M + rr] = o;
+                }
+            }
+        }
+    } else {
+        // K split over the P waves of a tile: partials through LDS
+        lds_barrier();
+        float4* red = reinterpret_cast<float4*>(lds);
+        red[wave * 64 + lane] = float4{acc[0][0], acc[0][1], acc[0][2], acc[0][3]};
+        lds_barrier();
+        const float* rf = reinterpret_cast<const float*>(lds);
+        for (int it = tid; it < ntq * 128; it += nthr) {
+            const int q = it >> 7, t = (it >> 4) & 7, nn = it & 15;
+            const int64_t rr = r0 + 16 * (int64_t)q + nn;
+            if (t < ntok && rr <= rl) {
+                float o = 0.f;
+                const float* hp = rf + (q * P * 64 + (t >> 2) * 16 + nn) * 4 + (t & 3);
+#pragma unroll 4
+                for (int p = 0; p < P; ++p) o += hp[p * 256] + hp[p * 256 + 128];
+                y[(int64_t)t * M + rr] = o;
+            }
+        }
+    }
+}
+
+template <int FMT, int TPW>
+hipError_t launch_tpw(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
+                      const Planes& p, int G, int nw, int rpw, int ntq, int P, int ws, size_t lds, hipStream_t stream) {
+    if (query_only(kernel_name<Name_fewtok_kernel, FMT, TPW>())) return hipSuccess;
+    hipLaunchKernelGGL((fewtok_kernel<FMT, TPW>), dim3((unsigned)G), dim3(64 * nw), lds, stream, W, x, y, (int)M,
+                       (int)K, (int)n_tok, p.off1, p.off2, rpw, ntq, P, ws);
+    return hipGetLastError();
+}
+
+int cu_count_ft() {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0)
+        return 256;
+    return v;
+}
+
+template <int FMT>
+hipError_t launch_f(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
+                    const Planes& p, hipStream_t stream) {
+    if (n_tok < 2 || n_tok > 8 || K % 256 || M >= ((int64_t)1 << 30) || K >= ((int64_t)1 << 30))
+        return hipErrorNotSupported;
+    const int nsb = (int)(K / 256);
+    const int64_t cus = cu_count_ft();
+    // rows per workgroup: about M / #CU, at least 8
+    int64_t G = (M + 7) / 8;
+    if (G > cus) G = cus;
+    int64_t rpw = (M + G - 1) / G;
+    int ntq = (int)((rpw + 15) / 16);
+    // Selection (MI355X sweeps against the few-token kernel of multitok.hip):
+    // this kernel pays a workgroup-wide conversion of X per window, which
+    // takes a few tiles per workgroup to amortize: it is taken from two tiles
+    // per workgroup with K >= 4096 (Q4_K-style: any K) and for very tall
+    // matrices (more tiles than waves); other shapes go to the other kernel.
+    const bool take = ntq > kFtMaxWaves || (ntq >= 2 && (K >= 4096 || FMT == LW_Q4_K));
+    if (!take) return hipErrorNotSupported;
+    int nw, P, tpw;
+    if (ntq > kFtMaxWaves) {
+        // more tiles than waves: each wave owns whole tiles
+        nw = kFtMaxWaves;
+        P = 1;
+        tpw = (ntq + nw - 1) / nw;
+        if (tpw > kFtMaxTpw) {
+            rpw = 16 * kFtMaxWaves * kFtMaxTpw;
+            ntq = kFtMaxWaves * kFtMaxTpw;
+            tpw = kFtMaxTpw;
+        }
+    } else {
+        // waves split K: P parts per tile, preferring a P that divides the
+        // super-blocks of a row
+        const int pmax = kFtMaxWaves / ntq;
+        P = pmax;
+        for (int c = pmax; c >= (pmax + 1) / 2; --c)
+            if (nsb % c == 0) {
+                P = c;
+                break;
+            }
+        nw = ntq * P;
+        tpw = 1;
+    }
+    G = (M + rpw - 1) / rpw;
+    int ws = P * (kFtWinSB / P);
+    if (ws > nsb) ws = nsb;
+    size_t lds = (size_t)ws * 8 * 1024;  // the A slices of a window
+    if (lds < (size_t)nw * 1024) lds = (size_t)nw * 1024;
+    const int tp = tpw <= 1 ? 1 : tpw <= 2 ? 2 : 4;
+    switch (tp) {
+    case 1: return launch_tpw<FMT, 1>(W, x, y, M, K, n_tok, p, (int)G, nw, (int)rpw, ntq, P, ws, lds, stream);
+    case 2: return launch_tpw<FMT, 2>(W, x, y, M, K, n_tok, p, (int)G, nw, (int)rpw, ntq, P, ws, lds, stream);
+    default: return launch_tpw<FMT, 4>(W, x, y, M, K, n_tok, p, (int)G, nw, (int)rpw, ntq, P, ws, lds, stream);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_fewtok(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
+                         const Planes& p, hipStream_t stream) {
+    switch (fmt) {
+    case LW_Q4_0: return launch_f<LW_Q4_0>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q4_K: return launch_f<LW_Q4_K>(W, x, y, M, K, n_tok, p, stream);
+    default: return hipErrorNotSupported;
+    }
+}
+
+}  // namespace lw

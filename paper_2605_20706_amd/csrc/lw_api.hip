@@ -35,6 +35,7 @@ hipError_t dispatch(int fmt, const uint8_t* Wb, const float* x, float* y, int64_
     const lw::Planes p = lw::planes_of(fmt, M * K);
     hipError_t err = hipErrorNotSupported;
     if (n_tok <= 2) err = lw::launch_gemv_reg(fmt, Wb, x, y, M, K, n_tok, p, s);
+    if (err == hipErrorNotSupported && n_tok >= 2 && n_tok <= 8) err = lw::launch_fewtok(fmt, Wb, x, y, M, K, n_tok, p, s);
     if (err == hipErrorNotSupported) {
         if (n_tok > 1 && lw::multitok_supported(fmt, n_tok))
             err = lw::launch_multitok(fmt, Wb, x, y, M, K, n_tok, p, s);

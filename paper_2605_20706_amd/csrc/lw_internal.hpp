@@ -97,6 +97,11 @@ hipError_t launch_skinny(int fmt, const uint8_t* W, const float* x, float* y, in
 bool multitok_supported(int fmt, int64_t n_tok);
 hipError_t launch_multitok(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                            int64_t n_tok, const Planes& p, hipStream_t stream);
+// Matrix-core path for 2 <= n_tok <= 8 over the 4-bit formats with the
+// activations converted once per workgroup into LDS; hipErrorNotSupported
+// when the call is not one it takes.
+hipError_t launch_fewtok(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
+                         int64_t n_tok, const Planes& p, hipStream_t stream);
 // Matrix-core path for larger token counts (prefill).
 hipError_t launch_prefill(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                           int64_t n_tok, const Planes& p, hipStream_t stream);

@@ -40,6 +40,22 @@ def test_exports_every_declared_symbol(lib):
         assert hasattr(lib, n), n
 
 
+def test_exports_only_the_c_abi(lib):
+    """Only the C ABI is exported (hidden visibility): no symbol of a host
+    program can stand in for one of the library's internal functions (such as
+    the kernel-name query flag the launchers consult)."""
+    import shutil
+    import subprocess
+    nm = shutil.which("nm")
+    if nm is None:
+        pytest.skip("nm not available")
+    out = subprocess.run([nm, "-D", "--defined-only", binding.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    names = {l.split()[-1] for l in out.splitlines() if l.strip() and l.split()[-2] in ("T", "W", "D", "B")}
+    names = {n for n in names if not n.startswith("__hip_cuid")}
+    assert names == set(binding.EXPORTS), sorted(names)
+
+
 def test_weight_bytes_matches_hand_sizes(lib):
     for name, n, _, _, total in golden_io.plane_sizes():
         assert lib.lw_weight_bytes(FMT[name], n) == total
@@ -117,9 +133,11 @@ def test_kernel_selection_table(lib):
     One token: the register-activation kernel when K is a whole number of
     2048-element chunks and its table has the shape, else the LDS-activation
     kernel; two tokens over the 4-bit formats: the register kernel; 3..8
-    tokens over the 4-bit formats: the pair-step matrix-core kernel, 9..16 the
-    few-token one with two MFMAs per block; more: the tiled matrix-core
-    kernel."""
+    tokens over the 4-bit formats: the matrix-core kernel with the
+    activations in LDS for matrices with at least two 16-row tiles per
+    workgroup (and K >= 4096 for Q4_0), else the pair-step matrix-core kernel;
+    9..16 the few-token one with two MFMAs per block; more: the tiled
+    matrix-core kernel."""
     from paper_2605_20706_amd import synth
 
     def kind(fmt, M, K, nt):
@@ -130,14 +148,19 @@ def test_kernel_selection_table(lib):
             for nt in (1, 2, 4, 8, 12, 512):
                 name = binding.kernel_name(wl.fmt, m.M, m.K, nt)
                 assert name and re.fullmatch(r"\w+_kernel<\d+(, \d+)*>", name), (key, m, nt, name)
-                assert name.startswith(("gemv", "multitok", "skinny", "gemm")), name
+                assert name.startswith(("gemv", "multitok", "fewtok", "skinny", "gemm")), name
     assert kind(Q4_K, 14336, 4096, 1) == "gemv1r_kernel"      # 8B gate: 2 chunks, many rows
     assert kind(Q4_K, 4096, 14336, 1) == "gemv1r_kernel"      # 8B down: 7 chunks split over 7 waves
     assert kind(Q4_K, 6144, 4096, 1) == "gemv1_kernel"        # 8B qkv: too few rows per wave
     assert kind(Q4_0, 100, 2304, 1) == "gemv1_kernel"         # K not whole chunks
     assert kind(Q4_0, 14336, 4096, 2) == "gemv1r_kernel"
-    assert kind(Q4_0, 14336, 4096, 4) == "multitok_pk_kernel"
+    assert kind(Q4_0, 14336, 4096, 4) == "fewtok_kernel"        # 8B gate: 56 rows per workgroup
+    assert kind(Q4_0, 14336, 4096, 2) == "gemv1r_kernel"
+    assert kind(Q4_0, 4096, 14336, 4) == "multitok_pk_kernel"   # 8B down: one tile per workgroup
     assert kind(Q4_K, 4096, 14336, 8) == "multitok_pk_kernel"
+    assert kind(Q4_K, 128256, 4096, 8) == "fewtok_kernel"       # lm_head: two tiles per wave
+    assert kind(Q4_0, 8192, 2048, 4) == "multitok_pk_kernel"    # 1B gate Q4_0: K below 4096
+    assert kind(Q4_K, 8192, 2048, 4) == "fewtok_kernel"
     assert kind(Q4_K, 14336, 4096, 9) == "multitok_kernel"
     assert kind(Q4_0, 14336, 4096, 512) == "gemm_kernel"
     assert kind(F16, 2048, 2048, 1) == "gemv1_kernel"

@@ -52,6 +52,23 @@ def test_parity_many_rows(oracle_mod, fmt):
         gate.check(y, y_ref[:nt], A[:nt], f32_bound=1e-4, what=(fmt, M, K, nt))
 
 
+@pytest.mark.parametrize("fmt", [Q4_0, Q4_K])
+@pytest.mark.parametrize("M,K", [(70000, 512), (300000, 256), (8200, 14336)])
+def test_parity_few_tokens_tiles(oracle_mod, fmt, M, K):
+    """Few-token matrix-core kernel with the activations in LDS: more 16-row
+    tiles per workgroup than waves (two and four tiles per wave, a ragged last
+    workgroup), and three tiles per workgroup with a long K that takes four
+    activation windows (the last one partial), each split over four waves."""
+    W = synth.gen_packed(fmt, M * K, np.random.default_rng([fmt, M, K, 21]))
+    Wg = to_gpu(W)
+    x = synth.gen_x_seeded([22, fmt, M, K], K, 8)
+    y_ref, A, _ = oracle_mod.matvec(fmt, W, x, M, K)
+    for nt in (2, 3, 6, 8):
+        print("matvec fmt=%d M=%d K=%d n_tok=%d" % (fmt, M, K, nt), flush=True)
+        y = gpu_matvec(fmt, W, x[:nt], M, K, Wg=Wg)
+        gate.check(y, y_ref[:nt], A[:nt], f32_bound=1e-4, what=(fmt, M, K, nt))
+
+
 # One to four tokens (the register kernel takes one or two, the matrix-core
 # kernel more) over the 4-bit formats with K a whole number of
 # 2048-element chunks (1, 2, 4 or 7 chunks per row): row counts from a single
