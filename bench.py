@@ -2,7 +2,9 @@
 """Benchmark of the fused dequantize x matrix-vector product on one MI355X.
 
 A step is one decode token's pass over every weight matrix of a workload: one
-lw_matvec per matrix, each matrix in its own HBM buffer (the 8B Q4_K-style set
+lw_matvec per matrix, except that a layer's gate and up projections (same
+input, independent outputs) share one lw_matvec_multi call, as a decode step
+issues them (--no-fuse: one call each). Each matrix has its own HBM buffer (the 8B Q4_K-style set
 is 4.2 GB, far above the 256 MB Infinity Cache, so every step streams the
 weights from HBM). Inputs are synthetic and seeded (paper_2605_20706_amd.synth)
 and resident in HBM before the timed region starts.
@@ -48,7 +50,7 @@ class Workset:
     op "dequant", one float32 output per matrix), and the raw argument tuples
     of one lw_matvec (lw_dequant) per matrix."""
 
-    def __init__(self, wl, n_tok, keep_host=0, op="matvec", rotate_bytes=2e9):
+    def __init__(self, wl, n_tok, keep_host=0, op="matvec", rotate_bytes=2e9, fuse=True):
         import torch
 
         self.wl, self.n_tok, self.op = wl, n_tok, op
@@ -95,40 +97,79 @@ class Workset:
                           m.M, m.K, n_tok) for r in range(self.reps) for i, m in enumerate(mats)]
             self.alg_bytes = [synth.algorithmic_bytes(wl.fmt, m.M, m.K, n_tok) for m in mats]
             self.flops = [2.0 * m.M * m.K * n_tok for m in mats]
+        # Calls of a step: one per matrix, except that a layer's gate and up
+        # projections (same input, independent outputs) are one
+        # lw_matvec_multi call when fuse is set (op "matvec" only).
+        self.groups = []
+        for i, m in enumerate(mats):
+            prev = self.groups[-1] if self.groups else None
+            if (fuse and op == "matvec" and m.name == "up" and prev and len(prev) == 1
+                    and mats[prev[0]].name == "gate" and mats[prev[0]].layer == m.layer and mats[prev[0]].K == m.K):
+                self.groups[-1] = (prev[0], i)
+            else:
+                self.groups.append((i,))
+        self._keep = []
+        self.calls = []  # (multi?, args) per weight copy and group
+        for r in range(self.reps):
+            for grp in self.groups:
+                if len(grp) == 1 or op != "matvec":
+                    self.calls.append((False, self.args[r * n + grp[0]]))
+                else:
+                    K = mats[grp[0]].K
+                    arr = binding.multi_args([self.W[r * n + i].data_ptr() for i in grp],
+                                             [self.y[i].data_ptr() for i in grp], [mats[i].M for i in grp])
+                    self._keep.append(arr)
+                    self.calls.append((True, (wl.fmt, len(grp)) + arr + (self.x[K].data_ptr(), K, n_tok)))
+        self.fuse_used = any(len(g) > 1 for g in self.groups)
+        self.call_bytes = [sum(self.alg_bytes[i] for i in grp) for grp in self.groups]
+        self.call_flops = [sum(self.flops[i] for i in grp) for grp in self.groups]
 
     def step(self, stream, idx=None, rep=0):
-        """One call per matrix of weight copy `rep`, or the calls `idx` (indices
-        over all copies). lw_dequant runs on the null stream: op "dequant" is
-        timed eagerly on it."""
-        n = len(self.mats)
-        calls = range(rep * n, rep * n + n) if idx is None else idx
+        """The calls of weight copy `rep`, or the calls `idx` (indices over all
+        copies). lw_dequant runs on the null stream: op "dequant" is timed
+        eagerly on it."""
+        ng = len(self.groups)
+        calls = range(rep * ng, rep * ng + ng) if idx is None else idx
         if self.op == "dequant":
             f = self.lib.lw_dequant
             for i in calls:
-                rc = f(*self.args[i])
+                rc = f(*self.calls[i][1])
                 if rc != 0:
                     raise binding.LwError(rc, "lw_dequant")
             return
-        f = self.lib.lw_matvec
+        f, fm = self.lib.lw_matvec, self.lib.lw_matvec_multi
         for i in calls:
-            rc = f(*self.args[i], stream)
+            multi, a = self.calls[i]
+            rc = fm(*a, stream) if multi else f(*a, stream)
             if rc != 0:
-                raise binding.LwError(rc, "lw_matvec")
+                raise binding.LwError(rc, "lw_matvec_multi" if multi else "lw_matvec")
 
     def kernel_names(self):
-        """The kernel each matrix's call launches (lw_kernel_name for lw_matvec)."""
+        """The kernel each call of a step launches (lw_kernel_name /
+        lw_kernel_name_multi for op matvec)."""
         if self.op == "dequant":
-            return ["dequant_kernel<%d>" % self.wl.fmt for _ in self.mats]
-        return [binding.kernel_name(self.wl.fmt, m.M, m.K, self.n_tok) for m in self.mats]
+            return ["dequant_kernel<%d>" % self.wl.fmt for _ in self.groups]
+        out = []
+        for grp in self.groups:
+            ms = [self.mats[i] for i in grp]
+            if len(grp) == 1:
+                out.append(binding.kernel_name(self.wl.fmt, ms[0].M, ms[0].K, self.n_tok))
+            else:
+                out.append(binding.kernel_name_multi(self.wl.fmt, [m.M for m in ms], ms[0].K, self.n_tok))
+        return out
+
+    def call_label(self, j):
+        ms = [self.mats[i] for i in self.groups[j]]
+        return "+".join(m.name for m in ms) + " " + "+".join("%dx%d" % (m.M, m.K) for m in ms)
 
     def shapes(self):
-        """Call indices (over all weight copies) grouped by 'name MxK', in
+        """Call indices (over all weight copies) grouped by 'names MxK', in
         first-seen order."""
         groups = {}
-        n = len(self.mats)
+        ng = len(self.groups)
         for r in range(self.reps):
-            for i, m in enumerate(self.mats):
-                groups.setdefault("%s %dx%d" % (m.name, m.M, m.K), []).append(r * n + i)
+            for j in range(ng):
+                groups.setdefault(self.call_label(j), []).append(r * ng + j)
         return groups
 
 
@@ -210,7 +251,8 @@ def run_gpu(ws, steps, warmup, mode):
 
 
 KERNEL_SOURCES = {"gemv_kernel": "gemv.hip", "gemv1_kernel": "gemv.hip", "gemv1r_kernel": "gemv.hip",
-                  "multitok_kernel": "multitok.hip", "skinny_kernel": "skinny.hip", "gemm_kernel": "prefill.hip",
+                  "multitok_kernel": "multitok.hip", "multitok_pk_kernel": "multitok.hip",
+                  "fewtok_kernel": "fewtok.hip", "skinny_kernel": "skinny.hip", "gemm_kernel": "prefill.hip",
                   "dequant_kernel": "dequant.hip"}
 
 
@@ -255,18 +297,18 @@ def stored_traffic(workload, n_tok, kernel):
 
 def kernel_groups(ws, per_shape):
     """Launches of a step grouped by the kernel the library selects for them
-    (lw_kernel_name), with each group's time per step from the per-shape
-    launch durations: {kernel: {launches, us, bytes, flop}}."""
+    (lw_kernel_name / lw_kernel_name_multi), with each group's time per step
+    from the per-shape launch durations: {kernel: {launches, us, bytes, flop}}."""
     names = ws.kernel_names()
-    n = len(ws.mats)
+    ng = len(ws.groups)
     groups = {}
     for _, (ms, idx) in per_shape.items():
-        one = [i for i in idx if i < n]  # this shape's matrices in one step
+        one = [i for i in idx if i < ng]  # this shape's calls in one step
         g = groups.setdefault(names[one[0]], {"launches": 0, "us": 0.0, "bytes": 0.0, "flop": 0.0})
         g["launches"] += len(one)
         g["us"] += ms * 1e3 * len(one)
-        g["bytes"] += sum(ws.alg_bytes[i] for i in one)
-        g["flop"] += sum(ws.flops[i] for i in one)
+        g["bytes"] += sum(ws.call_bytes[i] for i in one)
+        g["flop"] += sum(ws.call_flops[i] for i in one)
     return names, groups
 
 
@@ -314,6 +356,8 @@ def main():
     ap.add_argument("--op", choices=["matvec", "dequant"], default="matvec",
                     help="matvec: one lw_matvec per matrix (the decode step); dequant: one lw_dequant per "
                          "matrix into float32 (eager, on the null stream)")
+    ap.add_argument("--no-fuse", action="store_true",
+                    help="one lw_matvec per matrix (default: a layer's gate and up share one lw_matvec_multi call)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -346,10 +390,10 @@ def main():
     keep = 0 if args.no_cpu_baseline else len(wl.matrices)
     if args.op == "dequant":
         args.mode = "eager"  # lw_dequant is on the null stream, which a graph capture cannot record
-    ws = Workset(wl, args.n_tok, keep_host=keep, op=args.op)
+    ws = Workset(wl, args.n_tok, keep_host=keep, op=args.op, fuse=not args.no_fuse)
     ms_per_step, per_shape = run_gpu(ws, args.steps, args.warmup, args.mode)
 
-    n_launch = len(ws.mats)
+    n_launch = len(ws.groups)
     step_bytes = sum(ws.alg_bytes)
     gbs = step_bytes / (ms_per_step * 1e-3) / 1e9
     tok_s = args.n_tok / (ms_per_step * 1e-3)
@@ -382,18 +426,22 @@ def main():
     kernels_out = {k: {"launches": v["launches"], "us_per_step": round(v["us"], 1),
                        "GB/s": round(v["bytes"] / (v["us"] * 1e-6) / 1e9, 1)} for k, v in groups.items()}
     shape_out = {}
+    ng = len(ws.groups)
     for k, (ms, idx) in per_shape.items():
-        b = ws.alg_bytes[idx[0]]
-        shape_out[k] = {"us": round(ms * 1e3, 2), "GB/s": round(b / (ms * 1e-3) / 1e9, 1), "kernel": names[idx[0]]}
+        j = idx[0] % ng
+        b = ws.call_bytes[j]
+        shape_out[k] = {"us": round(ms * 1e3, 2), "GB/s": round(b / (ms * 1e-3) / 1e9, 1), "kernel": names[j]}
         if mfma:
-            shape_out[k]["TFLOP/s"] = round(ws.flops[idx[0]] / (ms * 1e-3) / 1e12, 1)
+            shape_out[k]["TFLOP/s"] = round(ws.call_flops[j] / (ms * 1e-3) / 1e12, 1)
     out = {
         "metric": METRIC if args.op == "matvec" else METRIC_DEQUANT, "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic (seeded; shapes and value distributions of the workload)",
         "config": {"workload": wl.key, "description": wl.description, "format": fmt_name,
-                   "matrices": len(ws.mats), "weights": wl.weights, "n_tok": args.n_tok,
+                   "matrices": len(ws.mats), "calls_per_step": n_launch,
+                   "fused": "a layer's gate and up in one lw_matvec_multi call" if ws.fuse_used else "none",
+                   "weights": wl.weights, "n_tok": args.n_tok,
                    "bytes_per_step": round(step_bytes), "mode": args.mode, "op": args.op,
                    "weight_copies": ws.reps},
         "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),

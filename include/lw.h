@@ -128,6 +128,35 @@ enum {
 LW_API int lw_matvec(int fmt, const void* W, const float* x, float* y,
               int64_t M, int64_t K, int64_t n_tok, void* stream);
 
+/* Most matrices one lw_matvec_multi call takes. */
+#define LW_MULTI_MAX 4
+
+/*
+ * lw_matvec_multi — y_i[t][r] = sum_k value(W_i, r*K + k) * x[t][k] for each
+ * i < n_mat: several matrices applied to the same activations, the
+ * independent projections of one decoder layer (q/k/v, gate/up) in the
+ * decode step of Sec. 2.1. Results equal n_mat lw_matvec calls, up to float32
+ * summation order. With one token the rows of all matrices form one row space
+ * and the call is a single kernel launch (the single-token kernels, selected
+ * as for lw_matvec with M = the sum of the M_i); otherwise, and where no
+ * single-token kernel takes the shapes, it enqueues one lw_matvec per matrix.
+ *
+ *   fmt      one of lw_fmt, shared by all matrices.
+ *   n_mat    1 <= n_mat <= LW_MULTI_MAX.
+ *   W        host array of n_mat device pointers, each as W of lw_matvec.
+ *   y        host array of n_mat device pointers, each float32 [n_tok][M[i]],
+ *            16-byte aligned, overwritten; no overlap with any W, x or
+ *            another y.
+ *   M        host array of n_mat row counts, each as M of lw_matvec.
+ *   x, K, n_tok, stream  as for lw_matvec, shared by all matrices.
+ *
+ * Checks as lw_matvec's, in the same order over all matrices (LW_EINVAL also
+ * for a null array or n_mat out of range); nothing is launched when one
+ * fails. The arrays are read during the call only.
+ */
+LW_API int lw_matvec_multi(int fmt, int n_mat, const void* const* W, float* const* y, const int64_t* M,
+                           const float* x, int64_t K, int64_t n_tok, void* stream);
+
 /*
  * lw_dequant — out[e] = value(W, e) for 0 <= e < n, bit-exact (see above).
  * Runs on the null stream. n == 0 is a no-op returning LW_OK.
@@ -164,6 +193,16 @@ LW_API const char* lw_strerror(int code);
  * (256 when there is none).
  */
 LW_API const char* lw_kernel_name(int fmt, int64_t M, int64_t K, int64_t n_tok);
+
+/*
+ * lw_kernel_name_multi — the kernel lw_matvec_multi(fmt, n_mat, ..., M, x, K,
+ * n_tok, stream) would launch: the fused launch's kernel where the call is one
+ * launch, else the kernel of its first matrix's lw_matvec. Same string
+ * conventions and checks as lw_kernel_name (NULL when the sizes would fail
+ * lw_matvec_multi's checks; M is a host array of n_mat row counts).
+ * Host-only: launches nothing.
+ */
+LW_API const char* lw_kernel_name_multi(int fmt, int n_mat, const int64_t* M, int64_t K, int64_t n_tok);
 
 #ifdef __cplusplus
 }

@@ -14,7 +14,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "liblw.so")
 
 LW_OK = 0
-EXPORTS = ("lw_matvec", "lw_dequant", "lw_weight_bytes", "lw_strerror", "lw_kernel_name")
+EXPORTS = ("lw_matvec", "lw_matvec_multi", "lw_dequant", "lw_weight_bytes", "lw_strerror", "lw_kernel_name",
+           "lw_kernel_name_multi")
+LW_MULTI_MAX = 4
 
 
 class LwError(RuntimeError):
@@ -38,6 +40,9 @@ def library() -> ctypes.CDLL:
         vp = ctypes.c_void_p
         lib.lw_matvec.argtypes = [ctypes.c_int, vp, vp, vp, i64, i64, i64, vp]
         lib.lw_matvec.restype = ctypes.c_int
+        lib.lw_matvec_multi.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.POINTER(vp), ctypes.POINTER(vp),
+                                        ctypes.POINTER(i64), vp, i64, i64, vp]
+        lib.lw_matvec_multi.restype = ctypes.c_int
         lib.lw_dequant.argtypes = [ctypes.c_int, vp, vp, i64]
         lib.lw_dequant.restype = ctypes.c_int
         lib.lw_weight_bytes.argtypes = [ctypes.c_int, i64]
@@ -46,6 +51,8 @@ def library() -> ctypes.CDLL:
         lib.lw_strerror.restype = ctypes.c_char_p
         lib.lw_kernel_name.argtypes = [ctypes.c_int, i64, i64, i64]
         lib.lw_kernel_name.restype = ctypes.c_char_p
+        lib.lw_kernel_name_multi.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.POINTER(i64), i64, i64]
+        lib.lw_kernel_name_multi.restype = ctypes.c_char_p
         _lib = lib
     return _lib
 
@@ -74,6 +81,14 @@ def kernel_name(fmt: int, M: int, K: int, n_tok: int):
     """Name (template part) of the kernel lw_matvec launches for these sizes,
     or None when lw_matvec would reject them. Host-only."""
     v = library().lw_kernel_name(fmt, M, K, n_tok)
+    return None if v is None else v.decode()
+
+
+def kernel_name_multi(fmt: int, Ms, K: int, n_tok: int):
+    """Name of the kernel lw_matvec_multi launches for matrices of Ms rows
+    sharing x (the fused launch's, else the first matrix's), or None."""
+    ma = (ctypes.c_int64 * len(Ms))(*Ms)
+    v = library().lw_kernel_name_multi(fmt, len(Ms), ma, K, n_tok)
     return None if v is None else v.decode()
 
 
@@ -112,6 +127,46 @@ def matvec(fmt: int, W, x, M: int, K: int, y=None, stream=None):
     if rc != LW_OK:
         raise LwError(rc, "lw_matvec")
     return y
+
+
+def multi_args(Ws, ys, Ms):
+    """ctypes arrays (W pointers, y pointers, row counts) for lw_matvec_multi
+    from integer device addresses."""
+    n = len(Ws)
+    vp = ctypes.c_void_p
+    return ((vp * n)(*[vp(w) for w in Ws]), (vp * n)(*[vp(v) for v in ys]),
+            (ctypes.c_int64 * n)(*Ms))
+
+
+def matvec_multi(fmt: int, Ws, x, Ms, K: int, ys=None, stream=None):
+    """[y_i[n_tok, M_i] = dequant(W_i) @ x^T for each i], as one lw_matvec_multi
+    call: matrices that share the activations x (float32 [K] or [n_tok, K]).
+    Ws: uint8 GPU tensors (lw layout); ys: optional float32 outputs."""
+    import torch
+
+    x2 = x.reshape(1, -1) if x.dim() == 1 else x
+    _check_gpu(x2, "x")
+    if x2.dtype != torch.float32 or x2.dim() != 2 or x2.shape[1] != K:
+        raise ValueError("x must be float32 [n_tok, K] with K = %d" % K)
+    n_tok = x2.shape[0]
+    if len(Ws) != len(Ms):
+        raise ValueError("one row count per matrix")
+    for i, W in enumerate(Ws):
+        _check_gpu(W, "W[%d]" % i)
+    if ys is None:
+        ys = [torch.empty((n_tok, m), dtype=torch.float32, device=x.device) for m in Ms]
+    for i, (v, m) in enumerate(zip(ys, Ms)):
+        _check_gpu(v, "y[%d]" % i)
+        if v.dtype != torch.float32 or v.numel() != n_tok * m:
+            raise ValueError("y[%d] must be float32 with n_tok*M elements" % i)
+    if stream is None:
+        stream = torch.cuda.current_stream(x.device)
+    wa, ya, ma = multi_args([W.data_ptr() for W in Ws], [v.data_ptr() for v in ys], list(Ms))
+    rc = library().lw_matvec_multi(fmt, len(Ws), wa, ya, ma, x2.data_ptr(), K, n_tok,
+                                   ctypes.c_void_p(stream.cuda_stream))
+    if rc != LW_OK:
+        raise LwError(rc, "lw_matvec_multi")
+    return ys
 
 
 def dequant(fmt: int, W, n: int, out=None):

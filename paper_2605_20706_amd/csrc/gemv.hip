@@ -46,6 +46,19 @@ struct Name_gemv1r_kernel {
 constexpr int64_t kLdsBytes = 64 * 1024;      // LDS budget of a workgroup (x tile + group sums)
 constexpr int64_t kRegLdsBytes = 128 * 1024;  // of a register-kernel workgroup (one per compute unit or two)
 
+// Device view of the rows of NS matrices that share the same activations as
+// one row space (lw_matvec_multi): segment i holds global rows [start[i],
+// start[i] + M[i]); its plane offsets, weights and output are its own.
+// Unused segments start past every row.
+template <int NS>
+__device__ __forceinline__ int seg_of(const RowSegs<NS>& sg, int64_t row) {
+    int i = 0;
+#pragma unroll
+    for (int k = 1; k < NS; ++k)
+        if (row >= sg.start[k]) i = k;
+    return i;
+}
+
 template <int FMT>
 struct Traits;
 
@@ -508,10 +521,9 @@ __global__ void __launch_bounds__(NW * kWave)
 // of its first D steps, and only then waits for x (vector-memory results
 // return in issue order), so the x tile and its group sums are in LDS after
 // one barrier while the weights are still on their way.
-template <int FMT, int R, int D, int NW>
+template <int FMT, int R, int D, int NW, int NS>
 __global__ void __launch_bounds__(NW * kWave)
-    gemv1_kernel(const uint8_t* __restrict__ W, const float* __restrict__ x, float* __restrict__ y,
-                 int64_t M, int64_t K, int64_t off1, int64_t off2) {
+    gemv1_kernel(const RowSegs<NS> sg, const float* __restrict__ x, int64_t M, int64_t K) {
     using T = Traits<FMT>;
     using Packet = typename T::Packet;
     constexpr int EPL = T::EPL;
@@ -546,8 +558,6 @@ __global__ void __launch_bounds__(NW * kWave)
     // the loads are unconditional and the compiler can count them, keeping
     // the next steps in flight while one is consumed.
     const uint32_t K32 = (uint32_t)K;
-    const uint8_t* P1 = W + off1;
-    const uint8_t* P2 = W + off2;
     const int total = nbw * nc;  // steps of this wave
     const uint32_t ulane = (uint32_t)lane;
     Packet ring[D][R];
@@ -561,8 +571,11 @@ __global__ void __launch_bounds__(NW * kWave)
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const int64_t rr = bb * R + r;
-            const uint32_t row = live ? (uint32_t)(rr < M ? rr : M - 1) : 0u;
-            pk[r] = T::load_at(W, P1, P2, T::base(row, K32, cc), la);
+            const int64_t row = live ? (rr < M ? rr : M - 1) : 0;
+            const int si = seg_of(sg, row);
+            const uint8_t* Ws = sg.W[si];
+            pk[r] = T::load_at(Ws, Ws + sg.off1[si], Ws + sg.off2[si],
+                               T::base((uint32_t)(row - sg.start[si]), K32, cc), la);
         }
         if (++ic == nc) {
             ic = 0;
@@ -618,7 +631,11 @@ __global__ void __launch_bounds__(NW * kWave)
 #pragma unroll
             for (int r = 0; r < R; ++r) {
                 const float v = wave_sum_to_lane63(acc[r]);
-                if (lane == kWave - 1 && bb * R + r < M) y[bb * R + r] = v;
+                const int64_t row = bb * R + r;
+                if (lane == kWave - 1 && row < M) {
+                    const int si = seg_of(sg, row);
+                    sg.y[si][row - sg.start[si]] = v;
+                }
                 acc[r] = 0.f;
             }
         }
@@ -681,10 +698,9 @@ __device__ __forceinline__ float sum8_to_last(float v) {
 // (the 8 lanes that stage one group write 8 different bank groups, and the 64
 // lanes reading one row read 64 different float4s), one barrier, then one
 // read per lane.
-template <int FMT, int NTK, int CPW, int WPR, int G, int DR>
+template <int FMT, int NTK, int CPW, int WPR, int G, int DR, int NS>
 __global__ void __launch_bounds__(G * WPR * kWave)
-    gemv1r_kernel(const uint8_t* __restrict__ W, const float* __restrict__ x, float* __restrict__ y,
-                  int M, int nr_max, int64_t off1, int64_t off2) {
+    gemv1r_kernel(const RowSegs<NS> sg, const float* __restrict__ x, int M, int nr_max) {
     using T = Traits<FMT>;
     using Packet = typename T::Packet;
     static_assert(T::EPL == 32 && T::kGroupSums, "4-bit formats only");
@@ -721,16 +737,19 @@ __global__ void __launch_bounds__(G * WPR * kWave)
 
     // (2) packets of the first DR rows. A row index past the group's end loads
     // row 0 and its packets are never used.
-    const uint8_t* P1 = W + off1;
-    const uint8_t* P2 = W + off2;
     const uint32_t ulane = (uint32_t)lane;
     Packet ring[DR][CPW];
     int ik = 0;  // next row (of the group) to issue
     auto issue = [&](Packet* pk) __attribute__((always_inline)) {
-        const uint32_t row = ik < nr ? (uint32_t)(rg + ik * rgs) : 0u;
+        const int row = ik < nr ? rg + ik * rgs : 0;
+        const int si = seg_of(sg, row);
+        const uint8_t* Ws = sg.W[si];
+        const uint8_t* P1 = Ws + sg.off1[si];
+        const uint8_t* P2 = Ws + sg.off2[si];
+        const uint32_t lr = (uint32_t)(row - (int)sg.start[si]);
 #pragma unroll
         for (int cc = 0; cc < CPW; ++cc)
-            pk[cc] = T::load_at(W, P1, P2, T::base(row, K, (uint32_t)(w * CPW + cc)), ulane);
+            pk[cc] = T::load_at(Ws, P1, P2, T::base(lr, K, (uint32_t)(w * CPW + cc)), ulane);
         ++ik;
     };
 #pragma unroll
@@ -794,9 +813,11 @@ __global__ void __launch_bounds__(G * WPR * kWave)
         const float v = rows_sum<NR>(acc) * 16777216.0f;  // 2^24
         const int kk = s0 + my_d;
         if (my_i >= 0 && kk < nr) {
-            if constexpr (WPR == 1)
-                y[(int64_t)my_t * M + rg + kk * rgs] = v;
-            else
+            if constexpr (WPR == 1) {
+                const int row = rg + kk * rgs;
+                const int si = seg_of(sg, row);
+                sg.y[si][(int64_t)my_t * sg.M[si] + (row - sg.start[si])] = v;
+            } else
                 red[((g * nr_max + kk) * NTK + my_t) * WPR + w] = v;
         }
     };
@@ -815,7 +836,8 @@ __global__ void __launch_bounds__(G * WPR * kWave)
                 float s = 0.f;
 #pragma unroll
                 for (int ww = 0; ww < WPR; ++ww) s += red[idx * WPR + ww];
-                y[(int64_t)t * M + row] = s;
+                const int si = seg_of(sg, row);
+                sg.y[si][(int64_t)t * sg.M[si] + (row - sg.start[si])] = s;
             }
         }
     }
@@ -867,45 +889,64 @@ int cu_count() {
     return v;
 }
 
+// Rows of one matrix as a one-segment row space.
+inline RowSegs<1> one_seg(const uint8_t* W, float* y, int64_t M, const Planes& p) {
+    RowSegs<1> sg;
+    sg.W[0] = W;
+    sg.y[0] = y;
+    sg.off1[0] = p.off1;
+    sg.off2[0] = p.off2;
+    sg.start[0] = 0;
+    sg.M[0] = M;
+    return sg;
+}
+
 // Single token: the persistent kernel when the whole x row fits the LDS
-// budget, else the K-tiled kernel.
-template <int FMT, int R, int D>
-hipError_t launch_single(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
-                         const Planes& p, hipStream_t stream) {
+// budget and every segment's planes stay below 4 GiB (32-bit offsets), else
+// hipErrorNotSupported (a single matrix then takes the K-tiled kernel).
+template <int FMT, int R, int D, int NS>
+hipError_t launch_single_segs(const RowSegs<NS>& sg, const float* x, int64_t M, int64_t K, int64_t max_total,
+                              hipStream_t stream) {
     constexpr int NW = 8;
     constexpr int E = kWave * Traits<FMT>::EPL;
     const int64_t nc = (K + E - 1) / E;
     const int64_t lds = nc * E * 4 + (Traits<FMT>::kGroupSums ? nc * kWave * 4 : 0);
-    if (lds > kLdsBytes || p.total >= ((int64_t)1 << 32) || M >= ((int64_t)1 << 31))
-        return launch_nt<FMT, 1>(W, x, y, M, K, p, stream);
+    if (lds > kLdsBytes || max_total >= ((int64_t)1 << 32) || M >= ((int64_t)1 << 31)) return hipErrorNotSupported;
     const int64_t nbatch = (M + R - 1) / R;
     int64_t grid = (nbatch + NW - 1) / NW;
     const int64_t cap = 2 * (int64_t)cu_count();  // two 8-wave workgroups per CU
     if (grid > cap) grid = cap;
-    if (query_only(kernel_name<Name_gemv1_kernel, FMT, R, D, NW>())) return hipSuccess;
-    hipLaunchKernelGGL((gemv1_kernel<FMT, R, D, NW>), dim3((unsigned)grid), dim3(NW * kWave), (size_t)lds,
-                       stream, W, x, y, M, K, p.off1, p.off2);
+    if (query_only(kernel_name<Name_gemv1_kernel, FMT, R, D, NW, NS>())) return hipSuccess;
+    hipLaunchKernelGGL((gemv1_kernel<FMT, R, D, NW, NS>), dim3((unsigned)grid), dim3(NW * kWave), (size_t)lds,
+                       stream, sg, x, M, K);
     return hipGetLastError();
+}
+
+template <int FMT, int R, int D>
+hipError_t launch_single(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
+                         const Planes& p, hipStream_t stream) {
+    const hipError_t err = launch_single_segs<FMT, R, D, 1>(one_seg(W, y, M, p), x, M, K, p.total, stream);
+    if (err == hipErrorNotSupported) return launch_nt<FMT, 1>(W, x, y, M, K, p, stream);
+    return err;
 }
 
 // Register-resident-x kernel: G row groups x WPR waves per workgroup, at most
 // CAP workgroups per compute unit. Returns hipErrorNotSupported when the shape
 // does not fit it (the caller then uses another kernel).
-template <int FMT, int NTK, int CPW, int WPR, int G, int DR, int CAP>
-hipError_t launch_reg(const uint8_t* W, const float* x, float* y, int64_t M, const Planes& p,
-                      hipStream_t stream) {
+template <int FMT, int NTK, int CPW, int WPR, int G, int DR, int CAP, int NS>
+hipError_t launch_reg(const RowSegs<NS>& sg, const float* x, int64_t M, int64_t max_total, hipStream_t stream) {
     constexpr int64_t NC = CPW * WPR;
     constexpr int64_t K = NC * kWave * 32;
-    if (p.total >= ((int64_t)1 << 32) || M >= ((int64_t)1 << 31)) return hipErrorNotSupported;
+    if (max_total >= ((int64_t)1 << 32) || M >= ((int64_t)1 << 31)) return hipErrorNotSupported;
     int64_t grid = (M + G - 1) / G;
     const int64_t cap = CAP * (int64_t)cu_count();
     if (grid > cap) grid = cap;
     const int64_t nr_max = (M + grid * G - 1) / (grid * G);
     const int64_t lds = NTK * (K * 4 + NC * kWave * 4) + (WPR > 1 ? G * nr_max * NTK * WPR * 4 : 0);
     if (lds > kRegLdsBytes) return hipErrorNotSupported;
-    if (query_only(kernel_name<Name_gemv1r_kernel, FMT, NTK, CPW, WPR, G, DR>())) return hipSuccess;
-    hipLaunchKernelGGL((gemv1r_kernel<FMT, NTK, CPW, WPR, G, DR>), dim3((unsigned)grid),
-                       dim3(G * WPR * kWave), (size_t)lds, stream, W, x, y, (int)M, (int)nr_max, p.off1, p.off2);
+    if (query_only(kernel_name<Name_gemv1r_kernel, FMT, NTK, CPW, WPR, G, DR, NS>())) return hipSuccess;
+    hipLaunchKernelGGL((gemv1r_kernel<FMT, NTK, CPW, WPR, G, DR, NS>), dim3((unsigned)grid),
+                       dim3(G * WPR * kWave), (size_t)lds, stream, sg, x, (int)M, (int)nr_max);
     return hipGetLastError();
 }
 
@@ -914,22 +955,66 @@ hipError_t launch_reg(const uint8_t* W, const float* x, float* y, int64_t M, con
 // count. With one token the register kernel needs a few rows per wave to pay
 // for staging x whole; below that (and for other K) the LDS kernel, which
 // spreads single chunks over the waves, is faster.
-template <int FMT>
-hipError_t launch_reg_fmt(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
-                          const Planes& p, hipStream_t stream) {
+template <int FMT, int NS>
+hipError_t launch_reg_segs(const RowSegs<NS>& sg, const float* x, int64_t M, int64_t K, int64_t n_tok,
+                           int64_t max_total, hipStream_t stream) {
     if (K % 2048) return hipErrorNotSupported;
     const int64_t nc = K / 2048;
     if (n_tok == 1) {
-        if (nc == 1) return launch_reg<FMT, 1, 1, 1, 8, 2, 2>(W, x, y, M, p, stream);
-        if (nc == 2 && M >= 10240) return launch_reg<FMT, 1, 2, 1, 8, 2, 2>(W, x, y, M, p, stream);
-        if (nc == 7) return launch_reg<FMT, 1, 1, 7, 2, 2, 1>(W, x, y, M, p, stream);
-    } else if (n_tok == 2) {
-        if (nc == 1) return launch_reg<FMT, 2, 1, 1, 8, 2, 2>(W, x, y, M, p, stream);
-        if (nc == 2) return launch_reg<FMT, 2, 1, 2, 4, 2, 2>(W, x, y, M, p, stream);
-        if (nc == 4) return launch_reg<FMT, 2, 1, 4, 2, 2, 1>(W, x, y, M, p, stream);
-        if (nc == 7) return launch_reg<FMT, 2, 1, 7, 2, 2, 1>(W, x, y, M, p, stream);
+        if (nc == 1) return launch_reg<FMT, 1, 1, 1, 8, 2, 2, NS>(sg, x, M, max_total, stream);
+        if (nc == 2 && M >= 10240) return launch_reg<FMT, 1, 2, 1, 8, 2, 2, NS>(sg, x, M, max_total, stream);
+        if (nc == 7) return launch_reg<FMT, 1, 1, 7, 2, 2, 1, NS>(sg, x, M, max_total, stream);
+    } else if (n_tok == 2 && NS == 1) {
+        if (nc == 1) return launch_reg<FMT, 2, 1, 1, 8, 2, 2, NS>(sg, x, M, max_total, stream);
+        if (nc == 2) return launch_reg<FMT, 2, 1, 2, 4, 2, 2, NS>(sg, x, M, max_total, stream);
+        if (nc == 4) return launch_reg<FMT, 2, 1, 4, 2, 2, 1, NS>(sg, x, M, max_total, stream);
+        if (nc == 7) return launch_reg<FMT, 2, 1, 7, 2, 2, 1, NS>(sg, x, M, max_total, stream);
     }
     return hipErrorNotSupported;
+}
+
+template <int FMT>
+hipError_t launch_reg_fmt(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
+                          const Planes& p, hipStream_t stream) {
+    return launch_reg_segs<FMT, 1>(one_seg(W, y, M, p), x, M, K, n_tok, p.total, stream);
+}
+
+// One launch over the rows of n matrices sharing x (one token): the register
+// kernel's table for the total row count, else the LDS single-token kernel.
+template <int FMT, int NS>
+hipError_t launch_multi_ns(int n, const uint8_t* const* W, float* const* y, const int64_t* M, const float* x,
+                           int64_t K, hipStream_t stream) {
+    RowSegs<NS> sg;
+    int64_t tot = 0, max_total = 0;
+    for (int i = 0; i < NS; ++i) {
+        const bool used = i < n;
+        const Planes p = planes_of(FMT, used ? M[i] * K : 0);
+        sg.W[i] = used ? W[i] : W[0];
+        sg.y[i] = used ? y[i] : y[0];
+        sg.off1[i] = p.off1;
+        sg.off2[i] = p.off2;
+        sg.start[i] = used ? tot : INT64_MAX;
+        sg.M[i] = used ? M[i] : 0;
+        if (used) {
+            tot += M[i];
+            if (p.total > max_total) max_total = p.total;
+        }
+    }
+    if constexpr (FMT == LW_Q4_0 || FMT == LW_Q4_K) {
+        const hipError_t err = launch_reg_segs<FMT, NS>(sg, x, tot, K, 1, max_total, stream);
+        if (err != hipErrorNotSupported) return err;
+        return launch_single_segs<FMT, 1, 2, NS>(sg, x, tot, K, max_total, stream);
+    }
+    return launch_single_segs<FMT, 2, 2, NS>(sg, x, tot, K, max_total, stream);
+}
+
+// Two matrices (a layer's gate and up) get a segment table of two, which
+// keeps the per-row segment choice to one compare.
+template <int FMT>
+hipError_t launch_multi_fmt(int n, const uint8_t* const* W, float* const* y, const int64_t* M, const float* x,
+                            int64_t K, hipStream_t stream) {
+    if (n <= 2) return launch_multi_ns<FMT, 2>(n, W, y, M, x, K, stream);
+    return launch_multi_ns<FMT, kMaxSegs>(n, W, y, M, x, K, stream);
 }
 
 template <int FMT>
@@ -965,6 +1050,17 @@ hipError_t launch_fmt(const uint8_t* W, const float* x, float* y, int64_t M, int
 }
 
 }  // namespace
+
+hipError_t launch_gemv_multi(int fmt, int n, const uint8_t* const* W, float* const* y, const int64_t* M,
+                             const float* x, int64_t K, hipStream_t stream) {
+    switch (fmt) {
+    case LW_F16: return launch_multi_fmt<LW_F16>(n, W, y, M, x, K, stream);
+    case LW_Q8_0: return launch_multi_fmt<LW_Q8_0>(n, W, y, M, x, K, stream);
+    case LW_Q4_0: return launch_multi_fmt<LW_Q4_0>(n, W, y, M, x, K, stream);
+    case LW_Q4_K: return launch_multi_fmt<LW_Q4_K>(n, W, y, M, x, K, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
 
 hipError_t launch_gemv_reg(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                            int64_t n_tok, const Planes& p, hipStream_t stream) {

@@ -93,6 +93,34 @@ int lw_matvec(int fmt, const void* W, const float* x, float* y, int64_t M, int64
     return err == hipSuccess ? LW_OK : LW_EHIP;
 }
 
+int lw_matvec_multi(int fmt, int n_mat, const void* const* W, float* const* y, const int64_t* M, const float* x,
+                    int64_t K, int64_t n_tok, void* stream) {
+    if (!known_fmt(fmt)) return LW_EFMT;
+    if (!W || !y || !M || !x || n_mat < 1 || n_mat > LW_MULTI_MAX) return LW_EINVAL;
+    for (int i = 0; i < n_mat; ++i)
+        if (!W[i] || !y[i]) return LW_EINVAL;
+    int worst = LW_OK;  // the first failing check in the documented order over all matrices
+    for (int i = 0; i < n_mat; ++i) {
+        const int rc = check_shape(fmt, M[i], K, n_tok);
+        if (rc == LW_EINVAL) return LW_EINVAL;
+        if (rc != LW_OK) worst = rc;
+    }
+    if (worst != LW_OK) return worst;
+    if (!aligned(x, 16)) return LW_EALIGN;
+    for (int i = 0; i < n_mat; ++i)
+        if (!aligned(W[i], 256) || !aligned(y[i], 16)) return LW_EALIGN;
+    const hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    hipError_t err = hipErrorNotSupported;
+    if (n_tok == 1 && n_mat > 1)
+        err = lw::launch_gemv_multi(fmt, n_mat, reinterpret_cast<const uint8_t* const*>(W), y, M, x, K, s);
+    if (err == hipErrorNotSupported) {
+        err = hipSuccess;
+        for (int i = 0; i < n_mat && err == hipSuccess; ++i)
+            err = dispatch(fmt, static_cast<const uint8_t*>(W[i]), x, y[i], M[i], K, n_tok, s);
+    }
+    return err == hipSuccess ? LW_OK : LW_EHIP;
+}
+
 const char* lw_kernel_name(int fmt, int64_t M, int64_t K, int64_t n_tok) {
     if (check_shape(fmt, M, K, n_tok) != LW_OK) return nullptr;
     lw::LaunchQuery& q = lw::launch_query();
@@ -105,6 +133,29 @@ const char* lw_kernel_name(int fmt, int64_t M, int64_t K, int64_t n_tok) {
                                     nullptr);
     q.active = false;
     return err == hipSuccess ? q.name : nullptr;
+}
+
+const char* lw_kernel_name_multi(int fmt, int n_mat, const int64_t* M, int64_t K, int64_t n_tok) {
+    if (!M || n_mat < 1 || n_mat > LW_MULTI_MAX) return nullptr;
+    for (int i = 0; i < n_mat; ++i)
+        if (check_shape(fmt, M[i], K, n_tok) != LW_OK) return nullptr;
+    if (n_tok != 1 || n_mat == 1) return lw_kernel_name(fmt, M[0], K, n_tok);
+    lw::LaunchQuery& q = lw::launch_query();
+    q.active = true;
+    q.name = nullptr;
+    // nothing is launched or dereferenced: the launchers stop at the launch
+    alignas(256) static const uint8_t stand_in[256] = {};
+    const uint8_t* Ws[LW_MULTI_MAX];
+    float* ys[LW_MULTI_MAX];
+    for (int i = 0; i < LW_MULTI_MAX; ++i) {
+        Ws[i] = stand_in;
+        ys[i] = const_cast<float*>(reinterpret_cast<const float*>(stand_in));
+    }
+    const hipError_t err =
+        lw::launch_gemv_multi(fmt, n_mat, Ws, ys, M, reinterpret_cast<const float*>(stand_in), K, nullptr);
+    q.active = false;
+    if (err == hipSuccess) return q.name;
+    return lw_kernel_name(fmt, M[0], K, n_tok);
 }
 
 int lw_dequant(int fmt, const void* W, float* out, int64_t n) {

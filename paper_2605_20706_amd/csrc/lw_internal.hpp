@@ -77,12 +77,29 @@ inline Planes planes_of(int fmt, int64_t n) {
     return p;
 }
 
+// Rows of up to kMaxSegs matrices that share the same activations, seen by a
+// kernel as one row space (lw_matvec_multi): segment i holds the global rows
+// [start[i], start[i] + M[i]) of weights W[i] (plane offsets off1[i],
+// off2[i]) and writes y[i]. Unused segments start past every row.
+constexpr int kMaxSegs = LW_MULTI_MAX;
+template <int NS>
+struct RowSegs {
+    const uint8_t* W[NS];
+    float* y[NS];
+    int64_t off1[NS], off2[NS], start[NS], M[NS];
+};
+
 // Kernel launchers. Arguments are already validated; each returns the
 // hipError_t of its launch.
 hipError_t launch_dequant(int fmt, const uint8_t* W, float* out, int64_t n, const Planes& p,
                           hipStream_t stream);
 hipError_t launch_gemv(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                        int64_t n_tok, const Planes& p, hipStream_t stream);
+// One launch of a single-token kernel over the rows of n matrices that share
+// x (one token, same format and K); hipErrorNotSupported when the shapes are
+// not ones the single-token kernels take as one row space.
+hipError_t launch_gemv_multi(int fmt, int n, const uint8_t* const* W, float* const* y, const int64_t* M,
+                             const float* x, int64_t K, hipStream_t stream);
 // Register-resident-activation kernel (4-bit formats, one or two tokens, K a
 // multiple of 2048 with a table entry); hipErrorNotSupported when the shape
 // is not one it takes.

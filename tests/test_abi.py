@@ -93,6 +93,45 @@ def test_matvec_error_order(lib):
     assert mv(lib, y=A16 + 8) == LW_EALIGN
 
 
+def mvm(lib, fmt=Q4_0, Ws=(A256, A256 + 4096), ys=(A16, A16 + 4096), Ms=(4, 8), x=A16, K=256, n_tok=1, n=None):
+    n = len(Ws) if n is None else n
+    wa, ya, ma = binding.multi_args(list(Ws), list(ys), list(Ms))
+    return lib.lw_matvec_multi(fmt, n, wa, ya, ma, x, K, n_tok, None)
+
+
+def test_matvec_multi_error_order(lib):
+    """lw_matvec_multi checks as lw_matvec does, over all matrices, in the same
+    order (no call here reaches a launch)."""
+    assert mvm(lib, fmt=5, x=None) == LW_EFMT
+    assert mvm(lib, x=None) == LW_EINVAL
+    assert mvm(lib, n=0) == LW_EINVAL
+    assert mvm(lib, n=binding.LW_MULTI_MAX + 1) == LW_EINVAL
+    assert lib.lw_matvec_multi(Q4_0, 2, None, None, None, A16, 256, 1, None) == LW_EINVAL
+    assert mvm(lib, Ws=(A256, 0)) == LW_EINVAL
+    assert mvm(lib, ys=(0, A16)) == LW_EINVAL
+    assert mvm(lib, Ms=(4, 0)) == LW_EINVAL
+    assert mvm(lib, Ms=(0, 4), K=300) == LW_EINVAL                      # sizes before shape
+    assert mvm(lib, K=300, Ws=(A256 + 1, A256)) == LW_ESHAPE            # shape before alignment
+    assert mvm(lib, Ws=(A256, A256 + 128)) == LW_EALIGN
+    assert mvm(lib, ys=(A16, A16 + 4)) == LW_EALIGN
+    assert mvm(lib, x=A16 + 8) == LW_EALIGN
+
+
+def test_kernel_name_multi(lib):
+    """One token: one fused launch of the single-token kernel over all rows
+    (last template parameter: a table of 2 or 4 segments); more tokens: the first matrix's
+    lw_matvec kernel; None where lw_matvec_multi would reject the sizes."""
+    assert binding.kernel_name_multi(Q4_K, [14336, 14336], 4096, 1) == "gemv1r_kernel<%d, 1, 2, 1, 8, 2, 2>" % Q4_K
+    assert binding.kernel_name_multi(F16, [8192, 8192], 2048, 1) == "gemv1_kernel<%d, 2, 2, 8, 2>" % F16
+    assert binding.kernel_name_multi(Q4_K, [3000, 3000, 2048], 4096, 1) == "gemv1_kernel<%d, 1, 2, 8, 4>" % Q4_K
+    assert binding.kernel_name_multi(Q4_K, [4096, 4096, 2048], 4096, 1) == "gemv1r_kernel<%d, 1, 2, 1, 8, 2, 4>" % Q4_K
+    assert binding.kernel_name_multi(Q4_0, [14336, 14336], 4096, 4) == binding.kernel_name(Q4_0, 14336, 4096, 4)
+    assert binding.kernel_name_multi(Q4_0, [100], 2304, 1) == binding.kernel_name(Q4_0, 100, 2304, 1)
+    assert binding.kernel_name_multi(Q4_0, [100, 0], 2304, 1) is None
+    assert binding.kernel_name_multi(Q4_0, [100, 4], 300, 1) is None
+    assert binding.kernel_name_multi(Q4_0, [1] * (binding.LW_MULTI_MAX + 1), 256, 1) is None
+
+
 def test_dequant_errors(lib):
     assert lib.lw_dequant(9, A256, A16, 256) == LW_EFMT
     assert lib.lw_dequant(Q4_K, None, A16, 256) == LW_EINVAL
@@ -166,4 +205,4 @@ def test_kernel_selection_table(lib):
     assert kind(F16, 2048, 2048, 1) == "gemv1_kernel"
     assert kind(Q8_0, 2048, 2048, 12) == "skinny_kernel"
     assert kind(F16, 2048, 2048, 20) == "gemv_kernel"
-    assert binding.kernel_name(Q4_K, 14336, 4096, 1) == "gemv1r_kernel<%d, 1, 2, 1, 8, 2>" % Q4_K
+    assert binding.kernel_name(Q4_K, 14336, 4096, 1) == "gemv1r_kernel<%d, 1, 2, 1, 8, 2, 1>" % Q4_K
