@@ -922,10 +922,25 @@ hipError_t launch_single_segs(const RowSegs<NS>& sg, const float* x, int64_t M, 
     return hipGetLastError();
 }
 
-template <int FMT, int R, int D>
+// Rows per wave step (R) and ring depth (D) of the LDS single-token kernel,
+// from MI355X sweeps: one row and two steps for the 4-bit formats and Q8_0;
+// f16 keeps four steps in flight (two rows each for 3072..8191 rows at
+// K <= 2048, e.g. the 1B q/k/v projection).
+template <int FMT, int NS>
+hipError_t launch_single_table(const RowSegs<NS>& sg, const float* x, int64_t M, int64_t K, int64_t max_total,
+                               hipStream_t stream) {
+    if constexpr (FMT == LW_F16) {
+        if (K <= 2048 && M >= 3072 && M < 8192) return launch_single_segs<FMT, 2, 4, NS>(sg, x, M, K, max_total, stream);
+        return launch_single_segs<FMT, 1, 4, NS>(sg, x, M, K, max_total, stream);
+    } else {
+        return launch_single_segs<FMT, 1, 2, NS>(sg, x, M, K, max_total, stream);
+    }
+}
+
+template <int FMT>
 hipError_t launch_single(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                          const Planes& p, hipStream_t stream) {
-    const hipError_t err = launch_single_segs<FMT, R, D, 1>(one_seg(W, y, M, p), x, M, K, p.total, stream);
+    const hipError_t err = launch_single_table<FMT, 1>(one_seg(W, y, M, p), x, M, K, p.total, stream);
     if (err == hipErrorNotSupported) return launch_nt<FMT, 1>(W, x, y, M, K, p, stream);
     return err;
 }
@@ -1003,9 +1018,8 @@ hipError_t launch_multi_ns(int n, const uint8_t* const* W, float* const* y, cons
     if constexpr (FMT == LW_Q4_0 || FMT == LW_Q4_K) {
         const hipError_t err = launch_reg_segs<FMT, NS>(sg, x, tot, K, 1, max_total, stream);
         if (err != hipErrorNotSupported) return err;
-        return launch_single_segs<FMT, 1, 2, NS>(sg, x, tot, K, max_total, stream);
     }
-    return launch_single_segs<FMT, 2, 2, NS>(sg, x, tot, K, max_total, stream);
+    return launch_single_table<FMT, NS>(sg, x, tot, K, max_total, stream);
 }
 
 // Two matrices (a layer's gate and up) get a segment table of two, which
@@ -1020,11 +1034,7 @@ hipError_t launch_multi_fmt(int n, const uint8_t* const* W, float* const* y, con
 template <int FMT>
 hipError_t launch_fmt(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                       int64_t n_tok, const Planes& p, hipStream_t stream) {
-    if (n_tok == 1) {
-        if constexpr (FMT == LW_Q4_0 || FMT == LW_Q4_K) return launch_single<FMT, 1, 2>(W, x, y, M, K, p, stream);
-
-        return launch_single<FMT, 2, 2>(W, x, y, M, K, p, stream);
-    }
+    if (n_tok == 1) return launch_single<FMT>(W, x, y, M, K, p, stream);
     if constexpr (!fits_one_chunk<FMT, 8>()) {
         // 8 tokens of a 4-bit chunk (64 KiB of x) plus group sums exceed the
         // budget: run them as two launches of 4 tokens.

@@ -122,7 +122,7 @@ def test_kernel_name_multi(lib):
     (last template parameter: a table of 2 or 4 segments); more tokens: the first matrix's
     lw_matvec kernel; None where lw_matvec_multi would reject the sizes."""
     assert binding.kernel_name_multi(Q4_K, [14336, 14336], 4096, 1) == "gemv1r_kernel<%d, 1, 2, 1, 8, 2, 2>" % Q4_K
-    assert binding.kernel_name_multi(F16, [8192, 8192], 2048, 1) == "gemv1_kernel<%d, 2, 2, 8, 2>" % F16
+    assert binding.kernel_name_multi(F16, [8192, 8192], 2048, 1) == "gemv1_kernel<%d, 1, 4, 8, 2>" % F16
     assert binding.kernel_name_multi(Q4_K, [3000, 3000, 2048], 4096, 1) == "gemv1_kernel<%d, 1, 2, 8, 4>" % Q4_K
     assert binding.kernel_name_multi(Q4_K, [4096, 4096, 2048], 4096, 1) == "gemv1r_kernel<%d, 1, 2, 1, 8, 2, 4>" % Q4_K
     assert binding.kernel_name_multi(Q4_0, [14336, 14336], 4096, 4) == binding.kernel_name(Q4_0, 14336, 4096, 4)
