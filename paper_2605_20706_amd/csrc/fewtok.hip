@@ -117,11 +117,21 @@ __device__ __forceinline__ void lds_barrier() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-template <int FMT, int TPW>
+template <int FMT, int TPW, int NS>
 __global__ void __launch_bounds__(64 * kFtMaxWaves)
-    fewtok_kernel(const uint8_t* __restrict__ W, const float* __restrict__ x, float* __restrict__ y, int M, int K,
-                  int ntok, int64_t off1, int64_t off2, int rpw, int ntq, int P, int ws) {
+    fewtok_kernel(const RowSegs<NS> sg, const float* __restrict__ x, int K, int ntok, int rpw, int ntq, int P,
+                  int ws) {
     extern __shared__ uint4 lds[];
+    // the workgroup's matrix (lw_matvec_multi: segment si holds workgroups
+    // wg0[si] ..; a workgroup never spans two matrices)
+    int si = 0;
+#pragma unroll
+    for (int k = 1; k < NS; ++k)
+        if ((int64_t)blockIdx.x >= sg.wg0[k]) si = k;
+    const uint8_t* const W = sg.W[si];
+    float* const y = sg.y[si];
+    const int M = (int)sg.M[si];
+    const int64_t wgi = (int64_t)blockIdx.x - sg.wg0[si];
     const int nthr = blockDim.x;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -131,10 +141,10 @@ __global__ void __launch_bounds__(64 * kFtMaxWaves)
     const int ts = wave / P, kp = wave - ts * P;
     const int nsb = K >> 8;
     const int nwin = (nsb + ws - 1) / ws;
-    const int64_t r0 = (int64_t)blockIdx.x * rpw;
+    const int64_t r0 = wgi * rpw;
     const int64_t rl = (r0 + rpw < (int64_t)M ? r0 + rpw : (int64_t)M) - 1;  // last row of the workgroup
-    const uint8_t* P1 = W + off1;
-    const uint8_t* P2 = W + off2;
+    const uint8_t* P1 = W + sg.off1[si];
+    const uint8_t* P2 = W + sg.off2[si];
     const uint64_t rowb = (uint64_t)K / 2u;  // code bytes per row
 
     // the wave's tiles: the lane's row in each (past the workgroup's last row:
@@ -392,12 +402,19 @@ __global__ void __launch_bounds__(64 * kFtMaxWaves)
     }
 }
 
-template <int FMT, int TPW>
-hipError_t launch_tpw(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
-                      const Planes& p, int G, int nw, int rpw, int ntq, int P, int ws, size_t lds, hipStream_t stream) {
-    if (query_only(kernel_name<Name_fewtok_kernel, FMT, TPW>())) return hipSuccess;
-    hipLaunchKernelGGL((fewtok_kernel<FMT, TPW>), dim3((unsigned)G), dim3(64 * nw), lds, stream, W, x, y, (int)M,
-                       (int)K, (int)n_tok, p.off1, p.off2, rpw, ntq, P, ws);
+template <int FMT, int TPW, int NS>
+hipError_t launch_tpw(RowSegs<NS> sg, const float* x, int64_t K, int64_t n_tok, int nw, int rpw, int ntq, int P,
+                      int ws, size_t lds, hipStream_t stream) {
+    // workgroups per matrix: its rows in groups of rpw
+    int64_t G = 0;
+    for (int i = 0; i < NS; ++i) {
+        sg.wg0[i] = sg.M[i] > 0 ? G : INT64_MAX;
+        G += (sg.M[i] + rpw - 1) / rpw;
+    }
+    if (G > 0x7fffffff) return hipErrorNotSupported;
+    if (query_only(kernel_name<Name_fewtok_kernel, FMT, TPW, NS>())) return hipSuccess;
+    hipLaunchKernelGGL((fewtok_kernel<FMT, TPW, NS>), dim3((unsigned)G), dim3(64 * nw), lds, stream, sg, x, (int)K,
+                       (int)n_tok, rpw, ntq, P, ws);
     return hipGetLastError();
 }
 
@@ -409,9 +426,9 @@ int cu_count_ft() {
     return v;
 }
 
-template <int FMT>
-hipError_t launch_f(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
-                    const Planes& p, hipStream_t stream) {
+// M: rows of the row space (all segments)
+template <int FMT, int NS>
+hipError_t launch_f(const RowSegs<NS>& sg, const float* x, int64_t M, int64_t K, int64_t n_tok, hipStream_t stream) {
     if (n_tok < 2 || n_tok > 8 || K % 256 || M >= ((int64_t)1 << 30) || K >= ((int64_t)1 << 30))
         return hipErrorNotSupported;
     const int nsb = (int)(K / 256);
@@ -452,17 +469,55 @@ hipError_t launch_f(const uint8_t* W, const float* x, float* y, int64_t M, int64
         nw = ntq * P;
         tpw = 1;
     }
-    G = (M + rpw - 1) / rpw;
     int ws = P * (kFtWinSB / P);
     if (ws > nsb) ws = nsb;
     size_t lds = (size_t)ws * 8 * 1024;  // the A slices of a window
     if (lds < (size_t)nw * 1024) lds = (size_t)nw * 1024;
     const int tp = tpw <= 1 ? 1 : tpw <= 2 ? 2 : 4;
     switch (tp) {
-    case 1: return launch_tpw<FMT, 1>(W, x, y, M, K, n_tok, p, (int)G, nw, (int)rpw, ntq, P, ws, lds, stream);
-    case 2: return launch_tpw<FMT, 2>(W, x, y, M, K, n_tok, p, (int)G, nw, (int)rpw, ntq, P, ws, lds, stream);
-    default: return launch_tpw<FMT, 4>(W, x, y, M, K, n_tok, p, (int)G, nw, (int)rpw, ntq, P, ws, lds, stream);
+    case 1: return launch_tpw<FMT, 1, NS>(sg, x, K, n_tok, nw, (int)rpw, ntq, P, ws, lds, stream);
+    case 2: return launch_tpw<FMT, 2, NS>(sg, x, K, n_tok, nw, (int)rpw, ntq, P, ws, lds, stream);
+    default: return launch_tpw<FMT, 4, NS>(sg, x, K, n_tok, nw, (int)rpw, ntq, P, ws, lds, stream);
     }
+}
+
+template <int FMT>
+hipError_t launch_one(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
+                      const Planes& p, hipStream_t stream) {
+    RowSegs<1> sg;
+    sg.W[0] = W;
+    sg.y[0] = y;
+    sg.off1[0] = p.off1;
+    sg.off2[0] = p.off2;
+    sg.start[0] = 0;
+    sg.M[0] = M;
+    return launch_f<FMT, 1>(sg, x, M, K, n_tok, stream);
+}
+
+template <int FMT, int NS>
+hipError_t launch_segs(int n, const uint8_t* const* W, float* const* y, const int64_t* M, const float* x, int64_t K,
+                       int64_t n_tok, hipStream_t stream) {
+    RowSegs<NS> sg;
+    int64_t tot = 0;
+    for (int i = 0; i < NS; ++i) {
+        const bool used = i < n;
+        const Planes p = planes_of(FMT, used ? M[i] * K : 0);
+        sg.W[i] = used ? W[i] : W[0];
+        sg.y[i] = used ? y[i] : y[0];
+        sg.off1[i] = p.off1;
+        sg.off2[i] = p.off2;
+        sg.start[i] = used ? tot : INT64_MAX;
+        sg.M[i] = used ? M[i] : 0;
+        if (used) tot += M[i];
+    }
+    return launch_f<FMT, NS>(sg, x, tot, K, n_tok, stream);
+}
+
+template <int FMT>
+hipError_t launch_multi_ft(int n, const uint8_t* const* W, float* const* y, const int64_t* M, const float* x,
+                           int64_t K, int64_t n_tok, hipStream_t stream) {
+    if (n <= 2) return launch_segs<FMT, 2>(n, W, y, M, x, K, n_tok, stream);
+    return launch_segs<FMT, kMaxSegs>(n, W, y, M, x, K, n_tok, stream);
 }
 
 }  // namespace
@@ -470,8 +525,17 @@ hipError_t launch_f(const uint8_t* W, const float* x, float* y, int64_t M, int64
 hipError_t launch_fewtok(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
                          const Planes& p, hipStream_t stream) {
     switch (fmt) {
-    case LW_Q4_0: return launch_f<LW_Q4_0>(W, x, y, M, K, n_tok, p, stream);
-    case LW_Q4_K: return launch_f<LW_Q4_K>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q4_0: return launch_one<LW_Q4_0>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q4_K: return launch_one<LW_Q4_K>(W, x, y, M, K, n_tok, p, stream);
+    default: return hipErrorNotSupported;
+    }
+}
+
+hipError_t launch_fewtok_multi(int fmt, int n, const uint8_t* const* W, float* const* y, const int64_t* M,
+                               const float* x, int64_t K, int64_t n_tok, hipStream_t stream) {
+    switch (fmt) {
+    case LW_Q4_0: return launch_multi_ft<LW_Q4_0>(n, W, y, M, x, K, n_tok, stream);
+    case LW_Q4_K: return launch_multi_ft<LW_Q4_K>(n, W, y, M, x, K, n_tok, stream);
     default: return hipErrorNotSupported;
     }
 }

@@ -111,8 +111,11 @@ int lw_matvec_multi(int fmt, int n_mat, const void* const* W, float* const* y, c
         if (!aligned(W[i], 256) || !aligned(y[i], 16)) return LW_EALIGN;
     const hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     hipError_t err = hipErrorNotSupported;
-    if (n_tok == 1 && n_mat > 1)
-        err = lw::launch_gemv_multi(fmt, n_mat, reinterpret_cast<const uint8_t* const*>(W), y, M, x, K, s);
+    const uint8_t* const* Wb = reinterpret_cast<const uint8_t* const*>(W);
+    if (n_tok == 1 && n_mat > 1) err = lw::launch_gemv_multi(fmt, n_mat, Wb, y, M, x, K, s);
+    // two tokens: the register kernel, one launch per matrix, is faster than
+    // the few-token kernel at every shape (and takes one matrix only)
+    if (n_tok >= 3 && n_tok <= 8 && n_mat > 1) err = lw::launch_fewtok_multi(fmt, n_mat, Wb, y, M, x, K, n_tok, s);
     if (err == hipErrorNotSupported) {
         err = hipSuccess;
         for (int i = 0; i < n_mat && err == hipSuccess; ++i)
@@ -139,7 +142,7 @@ const char* lw_kernel_name_multi(int fmt, int n_mat, const int64_t* M, int64_t K
     if (!M || n_mat < 1 || n_mat > LW_MULTI_MAX) return nullptr;
     for (int i = 0; i < n_mat; ++i)
         if (check_shape(fmt, M[i], K, n_tok) != LW_OK) return nullptr;
-    if (n_tok != 1 || n_mat == 1) return lw_kernel_name(fmt, M[0], K, n_tok);
+    if (n_mat == 1 || n_tok == 2 || n_tok > 8) return lw_kernel_name(fmt, M[0], K, n_tok);
     lw::LaunchQuery& q = lw::launch_query();
     q.active = true;
     q.name = nullptr;
@@ -151,8 +154,9 @@ const char* lw_kernel_name_multi(int fmt, int n_mat, const int64_t* M, int64_t K
         Ws[i] = stand_in;
         ys[i] = const_cast<float*>(reinterpret_cast<const float*>(stand_in));
     }
-    const hipError_t err =
-        lw::launch_gemv_multi(fmt, n_mat, Ws, ys, M, reinterpret_cast<const float*>(stand_in), K, nullptr);
+    const float* xs = reinterpret_cast<const float*>(stand_in);
+    const hipError_t err = n_tok == 1 ? lw::launch_gemv_multi(fmt, n_mat, Ws, ys, M, xs, K, nullptr)
+                                      : lw::launch_fewtok_multi(fmt, n_mat, Ws, ys, M, xs, K, n_tok, nullptr);
     q.active = false;
     if (err == hipSuccess) return q.name;
     return lw_kernel_name(fmt, M[0], K, n_tok);

@@ -80,13 +80,15 @@ inline Planes planes_of(int fmt, int64_t n) {
 // Rows of up to kMaxSegs matrices that share the same activations, seen by a
 // kernel as one row space (lw_matvec_multi): segment i holds the global rows
 // [start[i], start[i] + M[i]) of weights W[i] (plane offsets off1[i],
-// off2[i]) and writes y[i]. Unused segments start past every row.
+// off2[i]) and writes y[i]. Unused segments start past every row. Kernels
+// that give each workgroup rows of one matrix only use wg0[i], the first
+// workgroup of segment i, instead of start.
 constexpr int kMaxSegs = LW_MULTI_MAX;
 template <int NS>
 struct RowSegs {
     const uint8_t* W[NS];
     float* y[NS];
-    int64_t off1[NS], off2[NS], start[NS], M[NS];
+    int64_t off1[NS], off2[NS], start[NS], M[NS], wg0[NS];
 };
 
 // Kernel launchers. Arguments are already validated; each returns the
@@ -119,6 +121,9 @@ hipError_t launch_multitok(int fmt, const uint8_t* W, const float* x, float* y, 
 // when the call is not one it takes.
 hipError_t launch_fewtok(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                          int64_t n_tok, const Planes& p, hipStream_t stream);
+// The same over the rows of n matrices that share x (lw_matvec_multi).
+hipError_t launch_fewtok_multi(int fmt, int n, const uint8_t* const* W, float* const* y, const int64_t* M,
+                               const float* x, int64_t K, int64_t n_tok, hipStream_t stream);
 // Matrix-core path for larger token counts (prefill).
 hipError_t launch_prefill(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                           int64_t n_tok, const Planes& p, hipStream_t stream);

@@ -119,13 +119,19 @@ def test_matvec_multi_error_order(lib):
 
 def test_kernel_name_multi(lib):
     """One token: one fused launch of the single-token kernel over all rows
-    (last template parameter: a table of 2 or 4 segments); more tokens: the first matrix's
-    lw_matvec kernel; None where lw_matvec_multi would reject the sizes."""
+    (last template parameter: a table of 2 or 4 segments); 3 to 8 tokens of a
+    4-bit format: one few-token launch where that kernel takes the summed rows;
+    otherwise the first matrix's lw_matvec kernel; None where lw_matvec_multi
+    would reject the sizes."""
     assert binding.kernel_name_multi(Q4_K, [14336, 14336], 4096, 1) == "gemv1r_kernel<%d, 1, 2, 1, 8, 2, 2>" % Q4_K
     assert binding.kernel_name_multi(F16, [8192, 8192], 2048, 1) == "gemv1_kernel<%d, 1, 4, 8, 2>" % F16
     assert binding.kernel_name_multi(Q4_K, [3000, 3000, 2048], 4096, 1) == "gemv1_kernel<%d, 1, 2, 8, 4>" % Q4_K
     assert binding.kernel_name_multi(Q4_K, [4096, 4096, 2048], 4096, 1) == "gemv1r_kernel<%d, 1, 2, 1, 8, 2, 4>" % Q4_K
-    assert binding.kernel_name_multi(Q4_0, [14336, 14336], 4096, 4) == binding.kernel_name(Q4_0, 14336, 4096, 4)
+    assert binding.kernel_name_multi(Q4_0, [14336, 14336], 4096, 4) == "fewtok_kernel<%d, 1, 2>" % Q4_0
+    assert binding.kernel_name_multi(Q4_K, [3000, 3000, 2048], 4096, 8) == "fewtok_kernel<%d, 1, 4>" % Q4_K
+    for args in [(Q4_0, [14336, 14336], 4096, 2), (Q4_0, [14336, 14336], 4096, 9), (Q4_0, [8192, 8192], 2048, 4),
+                 (F16, [8192, 8192], 2048, 4), (Q8_0, [14336, 14336], 4096, 4)]:
+        assert binding.kernel_name_multi(*args) == binding.kernel_name(args[0], args[1][0], args[2], args[3]), args
     assert binding.kernel_name_multi(Q4_0, [100], 2304, 1) == binding.kernel_name(Q4_0, 100, 2304, 1)
     assert binding.kernel_name_multi(Q4_0, [100, 0], 2304, 1) is None
     assert binding.kernel_name_multi(Q4_0, [100, 4], 300, 1) is None

@@ -1,6 +1,7 @@
 """lw_matvec_multi against the oracle: several matrices sharing the same
 activations, as one launch (one token: the single-token kernels over the
-concatenated rows) or as one lw_matvec per matrix (more tokens). Every output
+concatenated rows; 3 to 8 tokens: the few-token matrix-core kernel, each
+workgroup on rows of one matrix) or as one lw_matvec per matrix. Every output
 meets the same bar as lw_matvec's, and each equals the separate lw_matvec
 result within the gate."""
 import numpy as np
@@ -44,9 +45,29 @@ def test_multi_small(oracle_mod, fmt, Ms, K):
 @pytest.mark.parametrize("Ms,K", [((14336, 14336), 4096), ((8192, 8192), 2048), ((2000, 3000, 9000), 14336)])
 def test_multi_register_kernel(oracle_mod, fmt, Ms, K):
     """The register-activation kernel over the rows of two or three matrices
-    (the 8B and 1B gate/up pairs; segments that end inside a row group and
-    inside a workgroup)."""
+    (the 8B and 1B gate/up pairs, as the benchmark's decode step calls them;
+    segments that end inside a row group and inside a workgroup)."""
     run_multi(oracle_mod, fmt, list(Ms), K, 1, 32)
+
+
+@pytest.mark.parametrize("fmt", [F16, Q8_0])
+def test_multi_lds_kernel_full_size(oracle_mod, fmt):
+    """The LDS single-token kernel over the 1B gate/up pair (8192 + 8192 rows,
+    K = 2048), the fused call of the benchmark's f16 decode step."""
+    run_multi(oracle_mod, fmt, [8192, 8192], 2048, 1, 33)
+
+
+@pytest.mark.parametrize("fmt", [Q4_0, Q4_K])
+@pytest.mark.parametrize("Ms,K", [((14336, 14336), 4096), ((3000, 3000, 2048), 4096), ((40000, 37, 40000), 256),
+                                  ((70000, 70000), 256)])
+def test_multi_fewtok_kernel(oracle_mod, fmt, Ms, K):
+    """The few-token kernel over two to four matrices in one launch: the 8B
+    gate/up pair, ragged segments whose last workgroup is short, a segment
+    smaller than one workgroup's rows, and two or three tiles per wave."""
+    for n_tok in (3, 8):
+        name = binding.kernel_name_multi(fmt, list(Ms), K, n_tok)
+        assert name.startswith("fewtok_kernel<%d, " % fmt), name
+        run_multi(oracle_mod, fmt, list(Ms), K, n_tok, 34)
 
 
 def test_multi_in_graph(oracle_mod):
