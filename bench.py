@@ -121,6 +121,18 @@ class Workset:
                     self._keep.append(arr)
                     self.calls.append((True, (wl.fmt, len(grp)) + arr + (self.x[K].data_ptr(), K, n_tok)))
         self.fuse_used = any(len(g) > 1 for g in self.groups)
+        # kernel launches per call: a multi call is one launch where the
+        # library fuses it (lw_kernel_name_multi then names another kernel
+        # than the first matrix's lw_matvec), else one launch per matrix
+        self.call_launches = []
+        for grp in self.groups:
+            fused = False
+            if len(grp) > 1:
+                Ms = [mats[i].M for i in grp]
+                K = mats[grp[0]].K
+                fused = (binding.kernel_name_multi(wl.fmt, Ms, K, n_tok)
+                         != binding.kernel_name(wl.fmt, Ms[0], K, n_tok))
+            self.call_launches.append(1 if fused or len(grp) == 1 else len(grp))
         self.call_bytes = [sum(self.alg_bytes[i] for i in grp) for grp in self.groups]
         self.call_flops = [sum(self.flops[i] for i in grp) for grp in self.groups]
 
@@ -305,7 +317,7 @@ def kernel_groups(ws, per_shape):
     for _, (ms, idx) in per_shape.items():
         one = [i for i in idx if i < ng]  # this shape's calls in one step
         g = groups.setdefault(names[one[0]], {"launches": 0, "us": 0.0, "bytes": 0.0, "flop": 0.0})
-        g["launches"] += len(one)
+        g["launches"] += sum(ws.call_launches[i] for i in one)
         g["us"] += ms * 1e3 * len(one)
         g["bytes"] += sum(ws.call_bytes[i] for i in one)
         g["flop"] += sum(ws.call_flops[i] for i in one)

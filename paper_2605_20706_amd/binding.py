@@ -35,6 +35,14 @@ def library() -> ctypes.CDLL:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError("liblw.so is not built (%s); run python -m paper_2605_20706_amd.build"
                                % LIB_PATH)
+        # torch ships its own HIP runtime under the same soname as the one
+        # liblw.so links; whichever is loaded first serves both. Loading
+        # torch first keeps torch on its own runtime (loaded second, it would
+        # bind to the system one and may find no device).
+        try:
+            import torch  # noqa: F401
+        except ImportError:
+            pass
         lib = ctypes.CDLL(LIB_PATH)
         i64 = ctypes.c_int64
         vp = ctypes.c_void_p

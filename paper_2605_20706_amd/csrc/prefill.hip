@@ -192,40 +192,50 @@ struct MF<LW_Q8_0> {
     }
 };
 
-// Tiled kernel: a workgroup computes kBM weight rows x kBN tokens with
-// 2 * kWM waves, wave (wm, wn) owning rows 64*wm .. +64 and tokens
-// kTT*16*wn .. as 4 x kTT tiles of 16 x 16. Roles in D = A . B: A is X (16
-// tokens x one 32-element block), B the decoded codes (one block x 16 weight
-// rows), so lane l holds D[4*(l/16) + v][l % 16] = (token 4*(l/16) + v, weight
-// row l % 16) and one coefficient per row tile and block serves its outputs.
+// Tiled kernel. A workgroup of WM waves computes BM = 64*WM weight rows x
+// BN = 16*TT tokens over the blocks of one K split; wave wm owns rows
+// 64*wm .. 64*wm+63 as four 16-row tiles rt and all BN tokens as TT tiles of
+// 16. Roles in D = A . B: A is X (16 tokens x one 32-element block), B the
+// decoded codes (one block x 16 weight rows), so lane l holds
+// D[4*(l/16) + v][l % 16] = (token 4*(l/16) + v, weight row l % 16) and one
+// coefficient per row tile and block serves all of a lane's outputs.
 //
-// The two parts of a block's contribution are accumulated separately:
-// c1 * P, one FMA per output and block right after the block's MFMAs, and
-// c2 * S, which is itself a product over blocks, sum_b S[t][b] * c2[r][b]:
-// block sums and c2 coefficients are gathered for windows of 16 blocks and
-// multiplied on the matrix cores once per window (one v_mfma_f32_16x16x16_bf16
-// K-step spans the window, with the same output layout), split three ways
-// into bf16 parts (exact to 24 bits each), six partial products accumulated
-// straight into the output tile. This halves the
-// per-block vector work, which bounds this kernel.
+// A block's contribution has two parts. c1 * P: one FMA per output and block
+// right after the block's MFMAs. c2 * S: a product over blocks,
+// sum_b S[t][b] * c2[r][b], done on the matrix cores once per window of 16
+// blocks (one v_mfma_f32_16x16x16_bf16 K-step spans the window), with S and
+// c2 split three ways into bf16 parts (exact to 24 bits each): six partial
+// products accumulated straight into the output tile.
 //
 // K advances in stages of kKB blocks. Per stage the workgroup converts the X
-// slab (kBN tokens x 32*kKB values) to hi/lo bf16 and the c1 coefficients of
-// its kBM rows into one of two LDS stage buffers (one barrier per stage), and
-// appends block sums and c2 to the window buffer (one barrier more per window). Each
-// wave loads the codes of its own 64 rows directly into registers, two stages
-// ahead. Consecutive workgroups take consecutive token tiles of the same rows,
-// so a weight tile is read from HBM once and reused from L2.
-constexpr int kWM = 2, kBM = 64 * kWM, kTT = 2, kBN = 32 * kTT, kKB = 2, kGT = 128 * kWM;
-constexpr int kWin = 16;       // blocks per window (coefficients; the c2 * S product: one 16x16x16 MFMA K-step)
-constexpr int kWp = kWin + 1;  // padded row of the S / c2 window buffers (bank-conflict free writes)
+// slab (BN tokens x 32*kKB values) to hi/lo bf16 into one of two LDS stage
+// buffers and appends the block sums S to the window buffer; the c1 and c2
+// coefficients of a window's BM rows are computed once per window, one row
+// per thread. Each wave loads the codes of its own 64 rows straight into
+// registers, a quad of four blocks ahead. The vector work that bounds this
+// kernel is the c1 FMAs, the code decode (amortized over the TT token tiles
+// of a wave) and the X conversion (amortized over the BM rows of a
+// workgroup); every address is a base computed once plus a stage offset.
+//
+// Work split: (row tile, token tile) pairs and, where those are too few to
+// occupy every compute unit, K splits on super-block boundaries whose
+// partial results are added to y atomically (y is zeroed first by a fill
+// kernel). Consecutive workgroup indices go to different XCDs, so the tile
+// order is permuted to give each XCD a contiguous run of tiles: the token
+// tiles of a row tile then share that XCD's L2 for the weight tile.
+constexpr int kKB = 2;    // blocks per stage
+constexpr int kWin = 16;  // blocks per coefficient window (the c2 * S product: one 16x16x16 K-step)
 
-struct GemmLds {
-    static constexpr int kX = kKB * 4 * kBN;                       // bf16x8 entries per half per stage
-    static constexpr size_t kStage = (size_t)2 * kX * 16;          // stage buffer: xh, xl [kKB][4][kBN]
-    static constexpr size_t kC1 = (size_t)kWin * kBM * 4;          // c1 of a window [kWin][kBM]
-    static constexpr size_t kWinB = (size_t)(kBN + kBM) * kWp * 4;  // S [kBN][kWp], c2 [kBM][kWp]
-    static constexpr size_t kBytes = 2 * kStage + 2 * kC1 + kWinB;
+template <int WM, int TT>
+struct GemmTile {
+    static constexpr int BM = 64 * WM, BN = 16 * TT, NT = 64 * WM;
+    static constexpr int XI = kKB * BN * 4 / NT;  // X items (8 values) per thread and stage
+    static_assert(XI >= 1 && XI * NT == kKB * BN * 4, "whole X items per thread");
+    static constexpr int kX = kKB * 4 * BN;                // bf16x8 entries per half per stage
+    static constexpr size_t kStage = (size_t)2 * kX * 16;  // xh, xl [kKB][4][BN]
+    static constexpr size_t kC = (size_t)kWin * BM * 4;    // c1 (or c2) of a window
+    static constexpr size_t kS = (size_t)kWin * BN * 4;    // block sums of a window
+    static constexpr size_t bytes(bool sums) { return 2 * kStage + 2 * kC + (sums ? kC + kS : 0); }
 };
 
 // v = h + m + l with h, m, l bfloat16 (round to nearest even at each step):
@@ -265,183 +275,230 @@ __device__ __forceinline__ u32x4v transpose_quad(u32x4v w) {
     return u32x4v{s01[0], s01[1], s23[0], s23[1]};
 }
 
-template <int FMT>
-__global__ void __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+// Work split of one launch: nrt x ntt tiles, ks K splits of sbp super-blocks
+// (the last one possibly shorter).
+struct GemmSplit {
+    int64_t nrt, ntt;
+    int ks, sbp;
+};
+
+template <int FMT, int WM, int TT>
+__global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2, 2)))
     gemm_kernel(const uint8_t* __restrict__ W, const float* __restrict__ x, float* __restrict__ y, int64_t M,
-                int64_t K, int64_t N, int64_t off1, int64_t off2) {
+                int64_t K, int64_t N, int64_t off1, int64_t off2, GemmSplit sp) {
     using T = MF<FMT>;
+    using TL = GemmTile<WM, TT>;
+    constexpr int BM = TL::BM, BN = TL::BN, NT = TL::NT, XI = TL::XI;
     constexpr bool kQ4 = FMT != LW_Q8_0;
+    constexpr bool kSums = T::kSums;
     extern __shared__ bf16x8 smem[];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave % kWM, wn = wave / kWM;
+    const int wm = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int i16 = lane & 15, s4 = lane >> 4;
-    const int64_t ntt = (N + kBN - 1) / kBN;
-    const int64_t row0 = (int64_t)(blockIdx.x / ntt) * kBM;
-    const int64_t tok0 = (int64_t)(blockIdx.x % ntt) * kBN;
+
+    // tile of this workgroup: XCD x (= index mod 8) takes the contiguous run
+    // of tiles [x * G/8, (x+1) * G/8) when G is a multiple of 8
+    const int64_t G = (int64_t)gridDim.x;
+    const int64_t bi = (int64_t)blockIdx.x;
+    const int64_t L = (G & 7) == 0 ? (bi & 7) * (G >> 3) + (bi >> 3) : bi;
+    const int64_t tt_i = L % sp.ntt;
+    const int64_t rest = L / sp.ntt;
+    const int split = (int)(rest % sp.ks);
+    const int64_t rti = rest / sp.ks;
+    const int64_t row0 = rti * BM;
+    const int64_t tok0 = tt_i * BN;
     const uint32_t K32 = (uint32_t)K;
-    const int nblk = (int)(K / 32);
-    const int nst = nblk / kKB;  // K is a multiple of 256: a multiple of 4 stages
-    const int nwin = (nblk + kWin - 1) / kWin;
+    const int nsb = (int)(K / 256);
+    const int sb0 = split * sp.sbp;
+    const int sb1 = sb0 + sp.sbp < nsb ? sb0 + sp.sbp : nsb;
+    const int kb0 = 8 * sb0;            // first block of the split
+    const int nb = 8 * (sb1 - sb0);     // blocks of the split (a multiple of 8)
+    const int nst = nb / kKB;           // stages (a multiple of 4)
+    const int nwin = (nb + kWin - 1) / kWin;
 
     char* lds = reinterpret_cast<char*>(smem);
-    auto st_xh = [&](int bf) __attribute__((always_inline)) { return reinterpret_cast<bf16x8*>(lds + bf * GemmLds::kStage); };
-    auto st_xl = [&](int bf) __attribute__((always_inline)) { return st_xh(bf) + GemmLds::kX; };
+    auto st_xh = [&](int bf) __attribute__((always_inline)) { return reinterpret_cast<bf16x8*>(lds + bf * TL::kStage); };
+    auto st_xl = [&](int bf) __attribute__((always_inline)) { return st_xh(bf) + TL::kX; };
     auto win_c1 = [&](int w) __attribute__((always_inline)) {
-        return reinterpret_cast<float*>(lds + 2 * GemmLds::kStage + (w & 1) * GemmLds::kC1);
+        return reinterpret_cast<float*>(lds + 2 * TL::kStage + (w & 1) * TL::kC);
     };
-    float* win_s = reinterpret_cast<float*>(lds + 2 * GemmLds::kStage + 2 * GemmLds::kC1);  // [kBN][kWp]
-    float* win_c2 = win_s + kBN * kWp;                                                      // [kBM][kWp]
+    // c2 [row tile][g][row in tile][4]: lane (g, n) of a row tile reads the
+    // c2 of blocks 4g..4g+3 of row n as one float4 (the 16x16x16 B operand);
+    // S [token tile][g][token in tile][4] likewise (the A operand)
+    float* win_c2 = reinterpret_cast<float*>(lds + 2 * TL::kStage + 2 * TL::kC);
+    float* win_s = win_c2 + kWin * BM;
 
     // ---- codes of this lane's rows (B operand columns), clamped; stores are masked ----
-    uint64_t wrow[4];
+    const uint8_t* wp[4];
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt) {
         const int64_t r = row0 + 64 * wm + 16 * rt + i16;
-        wrow[rt] = (uint64_t)(r < M ? r : M - 1);
+        const uint64_t rr = (uint64_t)(r < M ? r : M - 1);
+        if constexpr (kQ4)
+            wp[rt] = W + rr * (K32 / 2u) + 16u * (uint32_t)(kb0 + s4);
+        else
+            wp[rt] = W + rr * K32 + 32u * (uint32_t)kb0 + 8u * (uint32_t)s4;
     }
     // 4-bit formats: a quad = 4 blocks = 2 stages; lane (s4, i16) loads block
     // 4q + s4 of its row (16 bytes) and a register transpose hands it word s4
     // of each of the 4 blocks. Q8_0: per stage, word s4 of each block.
     u32x4v qraw[4], qcur[4];
-    using Word8 = uint64_t;
-    Word8 cwA[4][kKB], cwB[4][kKB];
+    uint64_t cwA[4][kKB], cwB[4][kKB];
     auto load_quad = [&](int q) __attribute__((always_inline)) {
 #pragma unroll
-        for (int rt = 0; rt < 4; ++rt)
-            qraw[rt] = *reinterpret_cast<const u32x4v*>(W + wrow[rt] * (K32 / 2u) + 16u * (uint32_t)(4 * q + s4));
+        for (int rt = 0; rt < 4; ++rt) qraw[rt] = *reinterpret_cast<const u32x4v*>(wp[rt] + 64u * (uint32_t)q);
     };
-    auto load_codes8 = [&](Word8 (*cw)[kKB], int st) __attribute__((always_inline)) {
+    auto load_codes8 = [&](uint64_t (*cw)[kKB], int st) __attribute__((always_inline)) {
 #pragma unroll
         for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
             for (int b = 0; b < kKB; ++b)
-                cw[rt][b] = *reinterpret_cast<const uint64_t*>(W + wrow[rt] * K32 + 32u * (uint32_t)(st * kKB + b) + 8u * s4);
+                cw[rt][b] = *reinterpret_cast<const uint64_t*>(wp[rt] + 32u * (uint32_t)(st * kKB + b));
     };
 
-    // ---- window coefficients: thread (row cr, half ch) handles blocks 8ch..8ch+7 of a window ----
-    static_assert(kGT == 2 * kBM && kWin == 16, "one 8-block scale item per thread");
-    const int cr = tid % kBM, ch = tid / kBM;
-    const int64_t crow = row0 + cr < M ? row0 + cr : M - 1;
-    uint32_t sraw[4];
+    // ---- window coefficients: thread tid handles row tid, all 16 blocks ----
+    const int64_t crow = row0 + tid < M ? row0 + tid : M - 1;
+    const int c_at = (tid >> 6) * 64 + (tid & 15) * 4 + ((tid >> 4) & 3);   // c1 slot (wave, row, rt) of this row
+    float* const c2_row = win_c2 + (tid >> 4) * 256 + (tid & 15) * 4;       // + g * 64 + j
+    uint32_t sraw[2][4];
     auto load_win_scales = [&](int w) __attribute__((always_inline)) {
-        int blk0 = w * kWin + 8 * ch;
-        blk0 = blk0 < nblk ? blk0 : nblk - 8;  // past the end: a valid copy, never used
-        T::load_scale8(W, off1, off2, (uint64_t)crow, K32, blk0, sraw);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            int blk0 = kb0 + w * kWin + 8 * h;
+            blk0 = blk0 < kb0 + nb ? blk0 : kb0 + nb - 8;  // past the split: a valid copy, never used
+            T::load_scale8(W, off1, off2, (uint64_t)crow, K32, blk0, sraw[h]);
+        }
     };
     auto put_win_scales = [&](int w) __attribute__((always_inline)) {
         float* c1w = win_c1(w);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            float c1, c2;
-            T::coef8(sraw, e, &c1, &c2);
-            c1w[(8 * ch + e) * kBM + cr] = c1;
-            if constexpr (T::kSums) win_c2[cr * kWp + 8 * ch + e] = c2;
-        }
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int b16 = 8 * h + e;
+                float c1, c2;
+                T::coef8(sraw[h], e, &c1, &c2);
+                c1w[b16 * BM + c_at] = c1;
+                if constexpr (kSums) c2_row[(b16 >> 2) * 64 + (b16 & 3)] = c2;
+            }
     };
 
-    // ---- X stage producer: items (block, token, slice) ----
-    constexpr int kXI = kKB * kBN * 4 / kGT;
-    float4 xa[kXI], xb[kXI];
+    // ---- X stage producer: items (block b, token t, slice sl), fixed per thread ----
+    const float* xp[XI];
+    int xo[XI], so[XI], xb_[XI];
+#pragma unroll
+    for (int i = 0; i < XI; ++i) {
+        const int it = tid + i * NT;
+        const int sl = it & 3, t = (it >> 2) % BN, b = (it >> 2) / BN;
+        // tokens past N read the last token: their outputs are never stored
+        const int64_t tk = tok0 + t < N ? tok0 + t : N - 1;
+        xp[i] = x + tk * K + 32 * (int64_t)(kb0 + b) + T::x_first(sl, 0);
+        // token slots are XOR-swizzled by the slice so that the four slices
+        // written by a lane quad fall into different LDS banks
+        xo[i] = (b * 4 + sl) * BN + (t ^ (sl << 2));
+        so[i] = ((t >> 4) * 4) * 64 + (t & 15) * 4;  // S slot of (t, block 0); + (b16 >> 2) * 64 + (b16 & 3)
+        xb_[i] = b;
+    }
+    constexpr int kHalf2 = kQ4 ? 16 : 4;  // offset of the slice's second 4 values
+    float4 xa[XI], xb[XI];
     auto fetch = [&](int st) __attribute__((always_inline)) {
 #pragma unroll
-        for (int i = 0; i < kXI; ++i) {
-            const int it = tid + i * kGT;
-            const int sl = it & 3, t = (it >> 2) % kBN, b = (it >> 2) / kBN;
-            // tokens past N read the last token: their outputs are never stored
-            const int64_t tt = tok0 + t < N ? tok0 + t : N - 1;
-            const float* xp = x + tt * K + 32 * (int64_t)(st * kKB + b);
-            xa[i] = *reinterpret_cast<const float4*>(xp + T::x_first(sl, 0));
-            xb[i] = *reinterpret_cast<const float4*>(xp + T::x_first(sl, 1));
+        for (int i = 0; i < XI; ++i) {
+            const float* p = xp[i] + 32 * kKB * st;
+            xa[i] = *reinterpret_cast<const float4*>(p);
+            xb[i] = *reinterpret_cast<const float4*>(p + kHalf2);
         }
     };
     auto commit = [&](int bf, int st) __attribute__((always_inline)) {
         bf16x8* xh = st_xh(bf);
         bf16x8* xl = st_xl(bf);
 #pragma unroll
-        for (int i = 0; i < kXI; ++i) {
-            const int it = tid + i * kGT;
-            const int sl = it & 3, t = (it >> 2) % kBN, b = (it >> 2) / kBN;
+        for (int i = 0; i < XI; ++i) {
             const float v[8] = {xa[i].x, xa[i].y, xa[i].z, xa[i].w, xb[i].x, xb[i].y, xb[i].z, xb[i].w};
             bf16x8 h, l;
             float sum = split_bf16x8(v, &h, &l);
-            // token slots are XOR-swizzled by the slice so that the four
-            // slices written by a lane quad fall into different LDS banks
-            xh[(b * 4 + sl) * kBN + (t ^ (sl << 2))] = h;
-            xl[(b * 4 + sl) * kBN + (t ^ (sl << 2))] = l;
-            if constexpr (T::kSums) {
-                const int blk = st * kKB + b;
+            xh[xo[i]] = h;
+            xl[xo[i]] = l;
+            if constexpr (kSums) {
+                const int b16 = (st * kKB + xb_[i]) % kWin;
                 sum += dpp_move<0xB1>(sum);  // the 4 slices of (block, token) are one lane quad
                 sum += dpp_move<0x4E>(sum);
-                if (sl == 0) win_s[t * kWp + blk % kWin] = sum;
+                if ((tid & 3) == 0) win_s[so[i] + (b16 >> 2) * 64 + (b16 & 3)] = sum;
             }
         }
     };
 
-    f32x4 acc[4][kTT];
+    f32x4 acc[4][TT];
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
-        for (int tt = 0; tt < kTT; ++tt) acc[rt][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int tt = 0; tt < TT; ++tt) acc[rt][tt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+    // A operand slot of token tile tt for this lane (block 0 of a stage)
+    const int a_at = s4 * BN + (i16 ^ (s4 << 2));
     // stage st from LDS buffer bf; the codes of its block b: word j0 + b of
     // qcur (4-bit) or cw[.][b] (Q8_0)
-    auto compute = [&](int bf, int st, int j0, Word8 (*cw)[kKB]) __attribute__((always_inline)) {
+    auto compute = [&](int bf, int st, int j0, uint64_t (*cw)[kKB]) __attribute__((always_inline)) {
         const bf16x8* xh = st_xh(bf);
         const bf16x8* xl = st_xl(bf);
+        const float4* c1w = reinterpret_cast<const float4*>(win_c1(st * kKB / kWin));
 #pragma unroll
         for (int b = 0; b < kKB; ++b) {
-            const int blk = st * kKB + b;
-            const float* c1s = win_c1(blk / kWin) + (blk % kWin) * kBM;
-            bf16x8 ah[kTT], al[kTT];
-#pragma unroll
-            for (int tt = 0; tt < kTT; ++tt) {
-                const int t = (16 * kTT * wn + 16 * tt + i16) ^ (s4 << 2);
-                ah[tt] = xh[(b * 4 + s4) * kBN + t];
-                al[tt] = xl[(b * 4 + s4) * kBN + t];
-            }
+            const int b16 = (st * kKB + b) % kWin;
+            const float4 c1v = c1w[(b16 * BM + 64 * wm) / 4 + i16];
+            const float c1[4] = {c1v.x, c1v.y, c1v.z, c1v.w};
+            // the block's codes of the four row tiles, decoded once for all
+            // token tiles; the token tiles' A operands one at a time
+            bf16x8 bw[4];
 #pragma unroll
             for (int rt = 0; rt < 4; ++rt) {
-                bf16x8 bw;
                 if constexpr (kQ4)
-                    bw = T::decode(qcur[rt][j0 + b]);
+                    bw[rt] = T::decode(qcur[rt][j0 + b]);
                 else
-                    bw = T::decode(cw[rt][b]);
-                const float c1 = c1s[64 * wm + 16 * rt + i16];
+                    bw[rt] = T::decode(cw[rt][b]);
+            }
 #pragma unroll
-                for (int tt = 0; tt < kTT; ++tt) {
-                    f32x4 p = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[tt], bw, f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-                    p = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[tt], bw, p, 0, 0, 0);
+            for (int tt = 0; tt < TT; ++tt) {
+                const bf16x8 ah = xh[b * 4 * BN + a_at + 16 * tt];
+                const bf16x8 al = xl[b * 4 * BN + a_at + 16 * tt];
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) acc[rt][tt][v] = __builtin_fmaf(c1, p[v], acc[rt][tt][v]);
+                for (int rt = 0; rt < 4; ++rt) {
+                    f32x4 p = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bw[rt], f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                    p = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bw[rt], p, 0, 0, 0);
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) acc[rt][tt][v] = __builtin_fmaf(c1[rt], p[v], acc[rt][tt][v]);
                 }
             }
         }
+        // the FMAs complete here: sunk past the window's branch they would
+        // keep every partial product of the stage live across it
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+            for (int tt = 0; tt < TT; ++tt) asm volatile("" : "+v"(acc[rt][tt]));
     };
-    // acc += S(window) . c2(window)^T for window w (nv valid blocks; the rest masked)
+    // acc += S(window) . c2(window)^T for window w (nv valid blocks; S of the
+    // others is masked to zero)
     auto bias = [&](int w) __attribute__((always_inline)) {
-        const int nv = nblk - w * kWin < kWin ? nblk - w * kWin : kWin;
-        bf16x4 sh[kTT], sm[kTT], sl[kTT];
+        const int nv = nb - w * kWin < kWin ? nb - w * kWin : kWin;
+        bf16x4 sh[TT], sm[TT], sl[TT];
 #pragma unroll
-        for (int tt = 0; tt < kTT; ++tt) {
-            const float* sp = win_s + (16 * kTT * wn + 16 * tt + i16) * kWp + 4 * s4;
-            float v[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = 4 * s4 + e < nv ? sp[e] : 0.f;
+        for (int tt = 0; tt < TT; ++tt) {
+            const float4 s = reinterpret_cast<const float4*>(win_s)[(tt * 4 + s4) * 16 + i16];
+            const float v[4] = {4 * s4 + 0 < nv ? s.x : 0.f, 4 * s4 + 1 < nv ? s.y : 0.f,
+                                4 * s4 + 2 < nv ? s.z : 0.f, 4 * s4 + 3 < nv ? s.w : 0.f};
             split3_bf16x4(v, &sh[tt], &sm[tt], &sl[tt]);
         }
 #pragma unroll
         for (int rt = 0; rt < 4; ++rt) {
-            const float* cp = win_c2 + (64 * wm + 16 * rt + i16) * kWp + 4 * s4;
-            float v[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = 4 * s4 + e < nv ? cp[e] : 0.f;
+            const float4 c = reinterpret_cast<const float4*>(win_c2)[((wm * 4 + rt) * 4 + s4) * 16 + i16];
+            const float v[4] = {c.x, c.y, c.z, c.w};
             bf16x4 chh, chm, chl;
             split3_bf16x4(v, &chh, &chm, &chl);
 #pragma unroll
-            for (int tt = 0; tt < kTT; ++tt) {
+            for (int tt = 0; tt < TT; ++tt) {
                 f32x4 a = acc[rt][tt];
                 a = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(sh[tt], chh, a, 0, 0, 0);
                 a = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(sh[tt], chm, a, 0, 0, 0);
@@ -459,7 +516,7 @@ __global__ void __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2, 2))
     auto window_end = [&](int st) __attribute__((always_inline)) {
         if (((st + 1) * kKB) % kWin == 0 || st == nst - 1) {
             const int w = st * kKB / kWin;
-            if constexpr (T::kSums) bias(w);
+            if constexpr (kSums) bias(w);
             __syncthreads();
             if (w + 1 < nwin) put_win_scales(w + 1);
             load_win_scales(w + 2 < nwin ? w + 2 : nwin - 1);
@@ -506,30 +563,89 @@ __global__ void __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2, 2))
         __syncthreads();
     }
 
-    // store: lane holds tokens 16*kTT*wn + 16*tt + 4*s4 + v of weight row 64*wm + 16*rt + i16
+    // store: lane holds tokens 16*tt + 4*s4 + v of weight row 64*wm + 16*rt + i16
+    // (K splits: added to the zeroed y)
+    const bool split_k = sp.ks > 1;
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt) {
         const int64_t r = row0 + 64 * wm + 16 * rt + i16;
-        if (r >= M) continue;
 #pragma unroll
-        for (int tt = 0; tt < kTT; ++tt)
+        for (int tt = 0; tt < TT; ++tt)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                const int64_t t = tok0 + 16 * kTT * wn + 16 * tt + 4 * s4 + v;
-                if (t < N) y[t * M + r] = acc[rt][tt][v];
+                const int64_t t = tok0 + 16 * tt + 4 * s4 + v;
+                if (r < M && t < N) {
+                    float* const o = y + t * M + r;
+                    if (split_k)
+                        unsafeAtomicAdd(o, acc[rt][tt][v]);
+                    else
+                        *o = acc[rt][tt][v];
+                }
             }
     }
+}
+
+__global__ void zero_kernel(float* __restrict__ y, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        y[i] = 0.f;
+}
+
+int cu_count_pf() {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0)
+        return 256;
+    return v;
+}
+
+template <int FMT, int WM, int TT>
+hipError_t launch_tile(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
+                       const Planes& p, hipStream_t stream) {
+    using TL = GemmTile<WM, TT>;
+    GemmSplit sp;
+    sp.nrt = (M + TL::BM - 1) / TL::BM;
+    sp.ntt = (n_tok + TL::BN - 1) / TL::BN;
+    const int nsb = (int)(K / 256);
+    // K splits: the fewest that keep the compute units (one workgroup each)
+    // at least 85 % busy over the launch's rounds, else the best of them;
+    // every split keeps at least four super-blocks
+    const int64_t tiles = sp.nrt * sp.ntt;
+    const int64_t cus = cu_count_pf();
+    const int kmax = nsb / 4 > 1 ? nsb / 4 : 1;
+    int best = 1;
+    double best_eff = 0.0;
+    for (int ks = 1; ks <= kmax && ks <= 64; ++ks) {
+        const int64_t g = tiles * ks;
+        const double eff = (double)g / (double)(((g + cus - 1) / cus) * cus);
+        if (eff > best_eff + 1e-9) {
+            best = ks;
+            best_eff = eff;
+        }
+        if (eff >= 0.85) break;
+    }
+    sp.sbp = (nsb + best - 1) / best;
+    sp.ks = (nsb + sp.sbp - 1) / sp.sbp;
+    const int64_t grid = tiles * sp.ks;
+    if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
+    if (query_only(kernel_name<Name_gemm_kernel, FMT, WM, TT>())) return hipSuccess;
+    if (sp.ks > 1) {
+        const int64_t n = n_tok * M;
+        const int64_t zb = (n + 255) / 256 < 2048 ? (n + 255) / 256 : 2048;
+        hipLaunchKernelGGL(zero_kernel, dim3((unsigned)zb), dim3(256), 0, stream, y, n);
+    }
+    hipLaunchKernelGGL((gemm_kernel<FMT, WM, TT>), dim3((unsigned)grid), dim3(TL::NT),
+                       TL::bytes(MF<FMT>::kSums), stream, W, x, y, M, K, n_tok, p.off1, p.off2, sp);
+    return hipGetLastError();
 }
 
 template <int FMT>
 hipError_t launch_gemm(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
                        const Planes& p, hipStream_t stream) {
-    const int64_t grid = ((M + kBM - 1) / kBM) * ((n_tok + kBN - 1) / kBN);
-    if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
-    if (query_only(kernel_name<Name_gemm_kernel, FMT>())) return hipSuccess;
-    hipLaunchKernelGGL((gemm_kernel<FMT>), dim3((unsigned)grid), dim3(kGT), GemmLds::kBytes, stream, W, x, y, M, K,
-                       n_tok, p.off1, p.off2);
-    return hipGetLastError();
+    // Q8_0: two code words per block and lane in flight, so half the token tiles
+    if constexpr (FMT == LW_Q8_0)
+        return launch_tile<FMT, 4, 2>(W, x, y, M, K, n_tok, p, stream);
+    else
+        return launch_tile<FMT, 8, 4>(W, x, y, M, K, n_tok, p, stream);
 }
 
 }  // namespace

@@ -1,0 +1,56 @@
+"""Prefill (more than 16 tokens, the 4-bit formats and Q8_0) on the matrix
+cores against the oracle: several row and token tiles with ragged tails, the
+K-split launch (partial products added into a zeroed y) with an uneven last
+split and a half coefficient window, and the unsplit launch.
+
+Bar: the gate, and within 1e-4 of sum |w*x| (the activations enter the
+matrix cores as a bf16 high/low pair, exact to 2^-17)."""
+import numpy as np
+import pytest
+
+import gate
+from gpu_util import gpu_matvec, to_gpu
+from paper_2605_20706_amd import binding, synth
+from paper_2605_20706_amd.layout import Q4_0, Q4_K, Q8_0
+
+pytestmark = pytest.mark.gpu
+
+
+def run(oracle_mod, fmt, M, K, n_tok, seed):
+    W = synth.gen_packed(fmt, M * K, np.random.default_rng([seed, fmt, M, K]))
+    x = synth.gen_x_seeded([seed + 1, fmt, K], K, n_tok)
+    print("prefill fmt=%d M=%d K=%d n_tok=%d kernel=%s" % (fmt, M, K, n_tok, binding.kernel_name(fmt, M, K, n_tok)),
+          flush=True)
+    y = gpu_matvec(fmt, W, x, M, K, Wg=to_gpu(W))
+    y_ref, A, _ = oracle_mod.matvec(fmt, W, x, M, K)
+    gate.check(y, y_ref, A, f32_bound=1e-4, what=(fmt, M, K, n_tok))
+
+
+@pytest.mark.parametrize("fmt", [Q4_0, Q4_K, Q8_0])
+@pytest.mark.parametrize("M,K,n_tok", [
+    (1100, 4352, 100),  # 3 x 2 tiles (ragged rows and tokens); K split 5 + 5 + 5 + 2 super-blocks
+    (300, 1024, 17),    # one tile, 17 tokens (one past the few-token paths); unsplit (4 super-blocks)
+    (8192, 512, 240),   # 16 x 4 tiles of the 4-bit tile, unsplit (two super-blocks)
+    (40, 2048, 65),     # 40 rows (most of the row tile masked); two K splits
+])
+def test_prefill_tiles(oracle_mod, fmt, M, K, n_tok):
+    run(oracle_mod, fmt, M, K, n_tok, 50)
+
+
+@pytest.mark.parametrize("fmt", [Q4_0, Q4_K])
+def test_prefill_repeat_equal(oracle_mod, fmt):
+    """The unsplit launch writes y with plain stores: two calls give the same
+    bits. The split launch adds partials in any order: two calls agree to the
+    float32 rounding of those additions."""
+    import torch
+    for M, K, n_tok, exact in [(8192, 512, 240, True), (1100, 4352, 100, False)]:
+        W = to_gpu(synth.gen_packed(fmt, M * K, np.random.default_rng([60, fmt, M])))
+        x = to_gpu(synth.gen_x_seeded([61, fmt], K, n_tok))
+        a = binding.matvec(fmt, W, x, M, K)
+        b = binding.matvec(fmt, W, x, M, K)
+        torch.cuda.synchronize()
+        if exact:
+            assert torch.equal(a, b), (M, K, n_tok)
+        else:
+            d = (a - b).abs().max().item()
+            assert d <= 1e-5 * a.abs().max().item(), (M, K, n_tok, d)
