@@ -235,7 +235,7 @@ struct GemmTile {
     static constexpr size_t kStage = (size_t)2 * kX * 16;  // xh, xl [kKB][4][BN]
     static constexpr size_t kC = (size_t)kWin * BM * 4;    // c1 (or c2) of a window
     static constexpr size_t kS = (size_t)kWin * BN * 4;    // block sums of a window
-    static constexpr size_t bytes(bool sums) { return 2 * kStage + 2 * kC + (sums ? kC + kS : 0); }
+    static constexpr size_t bytes(bool sums) { return 2 * kStage + 2 * kC + (sums ? kC + 2 * kS : 0); }
 };
 
 // v = h + m + l with h, m, l bfloat16 (round to nearest even at each step):
@@ -326,9 +326,11 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
     };
     // c2 [row tile][g][row in tile][4]: lane (g, n) of a row tile reads the
     // c2 of blocks 4g..4g+3 of row n as one float4 (the 16x16x16 B operand);
-    // S [token tile][g][token in tile][4] likewise (the A operand)
+    // S [token tile][g][token in tile][4] likewise (the A operand), one
+    // buffer per window parity: the next window's sums are written while the
+    // current window's product still reads its own
     float* win_c2 = reinterpret_cast<float*>(lds + 2 * TL::kStage + 2 * TL::kC);
-    float* win_s = win_c2 + kWin * BM;
+    auto win_s = [&](int w) __attribute__((always_inline)) { return win_c2 + kWin * BM + (w & 1) * kWin * BN; };
 
     // ---- codes of this lane's rows (B operand columns), clamped; stores are masked ----
     const uint8_t* wp[4];
@@ -423,9 +425,12 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
             xl[xo[i]] = l;
             if constexpr (kSums) {
                 const int b16 = (st * kKB + xb_[i]) % kWin;
-                sum += dpp_move<0xB1>(sum);  // the 4 slices of (block, token) are one lane quad
+                // the 4 slices of (block, token) are one lane quad: after two
+                // exchanges every lane of it holds the block sum, and all four
+                // store it (one address, one value; no branch in the stage)
+                sum += dpp_move<0xB1>(sum);
                 sum += dpp_move<0x4E>(sum);
-                if ((tid & 3) == 0) win_s[so[i] + (b16 >> 2) * 64 + (b16 & 3)] = sum;
+                win_s(st * kKB / kWin)[so[i] + (b16 >> 2) * 64 + (b16 & 3)] = sum;
             }
         }
     };
@@ -472,12 +477,6 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
                 }
             }
         }
-        // the FMAs complete here: sunk past the window's branch they would
-        // keep every partial product of the stage live across it
-#pragma unroll
-        for (int rt = 0; rt < 4; ++rt)
-#pragma unroll
-            for (int tt = 0; tt < TT; ++tt) asm volatile("" : "+v"(acc[rt][tt]));
     };
     // acc += S(window) . c2(window)^T for window w (nv valid blocks; S of the
     // others is masked to zero)
@@ -486,7 +485,7 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
         bf16x4 sh[TT], sm[TT], sl[TT];
 #pragma unroll
         for (int tt = 0; tt < TT; ++tt) {
-            const float4 s = reinterpret_cast<const float4*>(win_s)[(tt * 4 + s4) * 16 + i16];
+            const float4 s = reinterpret_cast<const float4*>(win_s(w))[(tt * 4 + s4) * 16 + i16];
             const float v[4] = {4 * s4 + 0 < nv ? s.x : 0.f, 4 * s4 + 1 < nv ? s.y : 0.f,
                                 4 * s4 + 2 < nv ? s.z : 0.f, 4 * s4 + 3 < nv ? s.w : 0.f};
             split3_bf16x4(v, &sh[tt], &sm[tt], &sl[tt]);
@@ -509,6 +508,14 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
                 acc[rt][tt] = a;
             }
         }
+    };
+    // the FMAs of the stage complete before the window's branch: sunk past
+    // it they would keep every partial product of the stage live across it
+    auto pin = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+            for (int tt = 0; tt < TT; ++tt) asm volatile("" : "+v"(acc[rt][tt]));
     };
     // after stage st: when it ends a window, the window's c2 * S product is
     // added, and (after a barrier: the window buffers are reused) the next
@@ -549,17 +556,21 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
             for (int rt = 0; rt < 4; ++rt) qcur[rt] = transpose_quad(qraw[rt]);
             load_quad(s2 / 2);
         }
+        // the next stage's X conversion shares a basic block with this
+        // stage's MFMAs, so its vector work can issue while they run
         compute(0, st, 0, cwA);
-        window_end(st);
         if constexpr (!kQ4) load_codes8(cwA, s2);
         commit(1, st + 1);
         fetch(s2);
+        pin();
+        window_end(st);
         __syncthreads();
         compute(1, st + 1, 2, cwB);
-        window_end(st + 1);
         if constexpr (!kQ4) load_codes8(cwB, s3);
         commit(0, s2);  // past the end: a copy of the last stage, never read
         fetch(s3);
+        pin();
+        window_end(st + 1);
         __syncthreads();
     }
 
