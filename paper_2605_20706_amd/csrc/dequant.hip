@@ -6,10 +6,13 @@
 // value d*sc*q - dmin*m is one fused multiply-add of the exact d*sc and the
 // exact dmin*m. No half-precision arithmetic is used.
 //
-// Work split: one thread writes one float4 (4 consecutive elements) per
-// grid-stride step; consecutive lanes write consecutive 16-byte chunks, so a
-// wave's store is one contiguous 1 KiB. The op is bound by the float32 writes
-// (4 bytes out per 0.56-2 bytes in).
+// Work split: per grid-stride step a thread writes four float4 (4 consecutive
+// elements each), 256 float4 apart, so each store instruction of a wave is
+// one contiguous 1 KiB; all four values are computed before any is stored,
+// which keeps four loads of each kind in flight. The op is bound by the
+// float32 writes (4 bytes out per 0.56-2 bytes in). They are non-temporal:
+// the output is written once and is far larger than the caches (15-20 %
+// faster than plain stores on MI355X).
 #include "lw_device.hpp"
 #include "lw_internal.hpp"
 
@@ -21,59 +24,78 @@ struct Name_dequant_kernel {
     static constexpr const char* base = "dequant_kernel";
 };
 
+// the 4 elements e .. e+3 (e a multiple of 4)
+template <int FMT>
+__device__ __forceinline__ float4 value4(const uint8_t* __restrict__ W, int64_t off1, int64_t off2, int64_t e) {
+    float4 v;
+    if constexpr (FMT == LW_F16) {
+        const uint2 h = *reinterpret_cast<const uint2*>(W + 2 * e);
+        v.x = half_bits_to_float(h.x & 0xFFFFu);
+        v.y = half_bits_to_float(h.x >> 16);
+        v.z = half_bits_to_float(h.y & 0xFFFFu);
+        v.w = half_bits_to_float(h.y >> 16);
+    } else if constexpr (FMT == LW_Q8_0) {
+        const uint32_t q = *reinterpret_cast<const uint32_t*>(W + e);
+        const float d = half_bits_to_float(*reinterpret_cast<const uint16_t*>(W + off1 + 2 * (e >> 5)));
+        v.x = sbyte<0>(q) * d;
+        v.y = sbyte<1>(q) * d;
+        v.z = sbyte<2>(q) * d;
+        v.w = sbyte<3>(q) * d;
+    } else {
+        // Q4 code plane: group g = e/32 owns bytes [16g, 16g+16); byte i
+        // holds element 32g+i (low nibble) and 32g+i+16 (high nibble).
+        const int64_t g = e >> 5;
+        const int i0 = (int)(e & 31);  // multiple of 4
+        uint32_t b = *reinterpret_cast<const uint32_t*>(W + 16 * g + (i0 & 15));
+        b = (i0 < 16) ? (b & 0x0F0F0F0Fu) : ((b >> 4) & 0x0F0F0F0Fu);
+        b = opaque(b);
+        if constexpr (FMT == LW_Q4_0) {
+            const float d = half_bits_to_float(*reinterpret_cast<const uint16_t*>(W + off1 + 2 * g));
+            v.x = (ubyte<0>(b) - 8.0f) * d;
+            v.y = (ubyte<1>(b) - 8.0f) * d;
+            v.z = (ubyte<2>(b) - 8.0f) * d;
+            v.w = (ubyte<3>(b) - 8.0f) * d;
+        } else {
+            const int64_t S = e >> 8;
+            const int j = (int)(g & 7);
+            const uint32_t* rec = reinterpret_cast<const uint32_t*>(W + off1 + 12 * S);
+            const uint64_t lo = (uint64_t)rec[0] | ((uint64_t)rec[1] << 32);  // bits 0..63
+            const uint64_t hi = (uint64_t)rec[1] | ((uint64_t)rec[2] << 32);  // bits 32..95
+            const uint32_t sc = (uint32_t)(lo >> (6 * j)) & 63u;
+            const uint32_t m = (uint32_t)(hi >> (16 + 6 * j)) & 63u;
+            const uint32_t dd = *reinterpret_cast<const uint32_t*>(W + off2 + 4 * S);
+            const float ds = half_bits_to_float(dd & 0xFFFFu) * (float)sc;  // exact
+            const float dm = half_bits_to_float(dd >> 16) * (float)m;       // exact
+            v.x = __builtin_fmaf(ds, ubyte<0>(b), -dm);                    // one rounding
+            v.y = __builtin_fmaf(ds, ubyte<1>(b), -dm);
+            v.z = __builtin_fmaf(ds, ubyte<2>(b), -dm);
+            v.w = __builtin_fmaf(ds, ubyte<3>(b), -dm);
+        }
+    }
+    return v;
+}
+
+constexpr int kDqU = 4;  // float4 per thread and grid-stride step
+
 template <int FMT>
 __global__ void __launch_bounds__(256) dequant_kernel(const uint8_t* __restrict__ W,
                                                       float4* __restrict__ out, int64_t n4,
                                                       int64_t off1, int64_t off2) {
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
-        const int64_t e = 4 * i;  // first of the 4 elements
-        float4 v;
-        if constexpr (FMT == LW_F16) {
-            const uint2 h = *reinterpret_cast<const uint2*>(W + 2 * e);
-            v.x = half_bits_to_float(h.x & 0xFFFFu);
-            v.y = half_bits_to_float(h.x >> 16);
-            v.z = half_bits_to_float(h.y & 0xFFFFu);
-            v.w = half_bits_to_float(h.y >> 16);
-        } else if constexpr (FMT == LW_Q8_0) {
-            const uint32_t q = *reinterpret_cast<const uint32_t*>(W + e);
-            const float d = half_bits_to_float(*reinterpret_cast<const uint16_t*>(W + off1 + 2 * (e >> 5)));
-            v.x = sbyte<0>(q) * d;
-            v.y = sbyte<1>(q) * d;
-            v.z = sbyte<2>(q) * d;
-            v.w = sbyte<3>(q) * d;
-        } else {
-            // Q4 code plane: group g = e/32 owns bytes [16g, 16g+16); byte i
-            // holds element 32g+i (low nibble) and 32g+i+16 (high nibble).
-            const int64_t g = e >> 5;
-            const int i0 = (int)(e & 31);  // multiple of 4
-            uint32_t b = *reinterpret_cast<const uint32_t*>(W + 16 * g + (i0 & 15));
-            b = (i0 < 16) ? (b & 0x0F0F0F0Fu) : ((b >> 4) & 0x0F0F0F0Fu);
-            b = opaque(b);
-            if constexpr (FMT == LW_Q4_0) {
-                const float d = half_bits_to_float(*reinterpret_cast<const uint16_t*>(W + off1 + 2 * g));
-                v.x = (ubyte<0>(b) - 8.0f) * d;
-                v.y = (ubyte<1>(b) - 8.0f) * d;
-                v.z = (ubyte<2>(b) - 8.0f) * d;
-                v.w = (ubyte<3>(b) - 8.0f) * d;
-            } else {
-                const int64_t S = e >> 8;
-                const int j = (int)(g & 7);
-                const uint32_t* rec = reinterpret_cast<const uint32_t*>(W + off1 + 12 * S);
-                const uint64_t lo = (uint64_t)rec[0] | ((uint64_t)rec[1] << 32);  // bits 0..63
-                const uint64_t hi = (uint64_t)rec[1] | ((uint64_t)rec[2] << 32);  // bits 32..95
-                const uint32_t sc = (uint32_t)(lo >> (6 * j)) & 63u;
-                const uint32_t m = (uint32_t)(hi >> (16 + 6 * j)) & 63u;
-                const uint32_t dd = *reinterpret_cast<const uint32_t*>(W + off2 + 4 * S);
-                const float ds = half_bits_to_float(dd & 0xFFFFu) * (float)sc;   // exact
-                const float dm = half_bits_to_float(dd >> 16) * (float)m;        // exact
-                v.x = __builtin_fmaf(ds, ubyte<0>(b), -dm);                     // one rounding
-                v.y = __builtin_fmaf(ds, ubyte<1>(b), -dm);
-                v.z = __builtin_fmaf(ds, ubyte<2>(b), -dm);
-                v.w = __builtin_fmaf(ds, ubyte<3>(b), -dm);
-            }
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x * kDqU;
+    for (int64_t base = (int64_t)blockIdx.x * blockDim.x * kDqU + threadIdx.x; base < n4; base += stride) {
+        float4 v[kDqU];
+#pragma unroll
+        for (int u = 0; u < kDqU; ++u) {
+            const int64_t i = base + (int64_t)u * blockDim.x;
+            v[u] = value4<FMT>(W, off1, off2, 4 * (i < n4 ? i : n4 - 1));  // past the end: a copy, not stored
         }
-        out[i] = v;
+#pragma unroll
+        for (int u = 0; u < kDqU; ++u) {
+            const int64_t i = base + (int64_t)u * blockDim.x;
+            if (i < n4)
+                __builtin_nontemporal_store(f32x4{v[u].x, v[u].y, v[u].z, v[u].w}, reinterpret_cast<f32x4*>(out + i));
+        }
     }
 }
 
@@ -81,7 +103,7 @@ template <int FMT>
 hipError_t launch(const uint8_t* W, float* out, int64_t n, const Planes& p, hipStream_t stream) {
     const int64_t n4 = n / 4;
     const int threads = 256;
-    int64_t blocks = (n4 + threads - 1) / threads;
+    int64_t blocks = (n4 + threads * kDqU - 1) / (threads * kDqU);
     const int64_t cap = 256 * 32;  // 32 workgroups per CU on 256 CUs; the rest is grid-stride
     if (blocks > cap) blocks = cap;
     if (query_only(kernel_name<Name_dequant_kernel, FMT>())) return hipSuccess;
