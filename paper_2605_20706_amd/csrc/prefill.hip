@@ -596,9 +596,13 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
     }
 }
 
+// y[0 .. n) = 0 (y 16-byte aligned): float4 stores, then the n % 4 tail
 __global__ void zero_kernel(float* __restrict__ y, int64_t n) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
-        y[i] = 0.f;
+    const int64_t n4 = n / 4;
+    const int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    for (int64_t i = i0; i < n4; i += (int64_t)gridDim.x * blockDim.x)
+        reinterpret_cast<float4*>(y)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (i0 < n - 4 * n4) y[4 * n4 + i0] = 0.f;
 }
 
 int cu_count_pf() {
@@ -641,7 +645,7 @@ hipError_t launch_tile(const uint8_t* W, const float* x, float* y, int64_t M, in
     if (query_only(kernel_name<Name_gemm_kernel, FMT, WM, TT>())) return hipSuccess;
     if (sp.ks > 1) {
         const int64_t n = n_tok * M;
-        const int64_t zb = (n + 255) / 256 < 2048 ? (n + 255) / 256 : 2048;
+        const int64_t zb = (n / 4 + 255) / 256 < 16384 ? (n / 4 + 255) / 256 + 1 : 16384;
         hipLaunchKernelGGL(zero_kernel, dim3((unsigned)zb), dim3(256), 0, stream, y, n);
     }
     hipLaunchKernelGGL((gemm_kernel<FMT, WM, TT>), dim3((unsigned)grid), dim3(TL::NT),

@@ -31,7 +31,7 @@ def run(oracle_mod, fmt, M, K, n_tok, seed):
     (1100, 4352, 100),  # 3 x 2 tiles (ragged rows and tokens); K split 5 + 5 + 5 + 2 super-blocks
     (300, 1024, 17),    # one tile, 17 tokens (one past the few-token paths); unsplit (4 super-blocks)
     (8192, 512, 240),   # 16 x 4 tiles of the 4-bit tile, unsplit (two super-blocks)
-    (40, 2048, 65),     # 40 rows (most of the row tile masked); two K splits
+    (41, 2048, 67),     # 41 rows (most of the row tile masked); two K splits; y of 2747 floats (a fill tail)
 ])
 def test_prefill_tiles(oracle_mod, fmt, M, K, n_tok):
     run(oracle_mod, fmt, M, K, n_tok, 50)
