@@ -449,13 +449,16 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
         const bf16x8* xh = st_xh(bf);
         const bf16x8* xl = st_xl(bf);
         const float4* c1w = reinterpret_cast<const float4*>(win_c1(st * kKB / kWin));
+        // A operands one token tile ahead (across the block boundary too):
+        // the LDS reads of tile tt+1 are in flight during tile tt's MFMAs
+        bf16x8 ahn = xh[a_at], aln = xl[a_at];
 #pragma unroll
         for (int b = 0; b < kKB; ++b) {
             const int b16 = (st * kKB + b) % kWin;
             const float4 c1v = c1w[(b16 * BM + 64 * wm) / 4 + i16];
             const float c1[4] = {c1v.x, c1v.y, c1v.z, c1v.w};
             // the block's codes of the four row tiles, decoded once for all
-            // token tiles; the token tiles' A operands one at a time
+            // token tiles
             bf16x8 bw[4];
 #pragma unroll
             for (int rt = 0; rt < 4; ++rt) {
@@ -466,8 +469,14 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
             }
 #pragma unroll
             for (int tt = 0; tt < TT; ++tt) {
-                const bf16x8 ah = xh[b * 4 * BN + a_at + 16 * tt];
-                const bf16x8 al = xl[b * 4 * BN + a_at + 16 * tt];
+                const bf16x8 ah = ahn, al = aln;
+                if (tt + 1 < TT) {
+                    ahn = xh[b * 4 * BN + a_at + 16 * (tt + 1)];
+                    aln = xl[b * 4 * BN + a_at + 16 * (tt + 1)];
+                } else if (b + 1 < kKB) {
+                    ahn = xh[(b + 1) * 4 * BN + a_at];
+                    aln = xl[(b + 1) * 4 * BN + a_at];
+                }
 #pragma unroll
                 for (int rt = 0; rt < 4; ++rt) {
                     f32x4 p = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bw[rt], f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
