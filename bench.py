@@ -307,6 +307,57 @@ def stored_traffic(workload, n_tok, kernel):
         return None
 
 
+def ceilings(write, launch_bytes, mode):
+    """Streaming ceilings from libceiling.so in this process: GB/s of a plain
+    128-bit read (write: non-temporal write, the dequantization's store form)
+    over a 1 GiB buffer (one launch), and at `launch_bytes` per launch timed as
+    the per-shape launches are (192 back to back at rotating offsets of that
+    buffer, so no launch finds the previous one's bytes in the 256 MB Infinity
+    Cache; one graph in graph mode; behind a device-side sleep; HIP events on
+    the launch stream)."""
+    import ctypes
+    import torch
+
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2605_20706_amd", "libceiling.so"))
+    lib.lw_ceiling_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
+    lib.lw_ceiling_write.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+    total = 1 << 30
+    buf = torch.empty(total, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+
+    def launches(offs, nbytes):
+        s = torch.cuda.current_stream().cuda_stream
+        for off in offs:
+            ptr = buf.data_ptr() + off
+            rc = lib.lw_ceiling_write(ptr, nbytes, s) if write else lib.lw_ceiling_read(ptr, nbytes, sink.data_ptr(), s)
+            if rc != 0:
+                raise RuntimeError("libceiling: code %d" % rc)
+
+    def rate(nbytes, n, graph):
+        step = (nbytes + 255) // 256 * 256
+        offs = [(i * step) % (total - step + 1) // 256 * 256 for i in range(n)]
+        run = lambda: launches(offs, nbytes)  # noqa: E731
+        if graph:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                run()
+            run = g.replay
+        run()
+        torch.cuda.synchronize()
+        stream = torch.cuda.current_stream()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(int(2.4e6 * 5))  # ~5 ms at 2.4 GHz
+        e0.record(stream)
+        run()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return nbytes * n / (e0.elapsed_time(e1) * 1e-3) / 1e9
+
+    lb = max(16, min(int(launch_bytes), total) // 16 * 16)
+    return {"kind": "write" if write else "read", "GB/s_1GiB": round(rate(total, 3, False), 1),
+            "launch_bytes": lb, "GB/s_at_launch_bytes": round(rate(lb, 192, mode == "graph"), 1)}
+
+
 def kernel_groups(ws, per_shape):
     """Launches of a step grouped by the kernel the library selects for them
     (lw_kernel_name / lw_kernel_name_multi), with each group's time per step
@@ -462,6 +513,14 @@ def main():
         "kernels": kernels_out,
         "per_shape": shape_out,
     }
+    # the value against a plain streaming kernel's rate in the same process
+    # (read, or write for the dequantization), and the dominant kernel against
+    # that kernel at the dominant kernel's bytes per launch
+    ceil = ceilings(args.op == "dequant", roof["alg_bytes_per_launch"], args.mode)
+    ceil["value_over_1GiB_ceiling"] = round(gbs / ceil["GB/s_1GiB"], 4)
+    if roof["bound"] == "hbm":
+        ceil["dominant_kernel_over_launch_ceiling"] = round(roof["achieved"] / ceil["GB/s_at_launch_bytes"], 4)
+    out["stream_ceiling"] = ceil
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(ws, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -1,6 +1,8 @@
-"""Build the HIP library ``liblw.so`` for gfx950 with hipcc (in-tree).
+"""Build the HIP libraries for gfx950 with hipcc (in-tree).
 
-Run ``python -m paper_2605_20706_amd.build``. Every HIP source in ``csrc/`` is
+Run ``python -m paper_2605_20706_amd.build``. ``liblw.so`` (the product) is
+every HIP source in ``csrc/``; ``libceiling.so`` (the streaming-ceiling
+kernels the benchmark times beside it) is ``ceiling/ceiling.hip``. Both are
 compiled for ``--offload-arch=gfx950`` only, with packed-FP32 instruction
 selection disabled.
 """
@@ -15,6 +17,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "liblw.so")
+CEILING_LIB = os.path.join(HERE, "libceiling.so")
+CEILING_SRC = os.path.join(HERE, "ceiling", "ceiling.hip")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -30,9 +34,9 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [HIPCC] + FLAGS + ["-I", os.path.join(ROOT, "include"), "-I", CSRC] + sources() + ["-o", tmp]
+def _hipcc(srcs, out, verbose):
+    tmp = out + ".tmp%d" % os.getpid()
+    cmd = [HIPCC] + FLAGS + ["-I", os.path.join(ROOT, "include"), "-I", CSRC] + srcs + ["-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -44,8 +48,14 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError("hipcc failed:\n" + err)
     if verbose and err.strip():
         print(err, file=sys.stderr)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
+
+
+def build(verbose: bool = False) -> str:
+    """Builds liblw.so and libceiling.so; returns the path of liblw.so."""
+    _hipcc([CEILING_SRC], CEILING_LIB, verbose)
+    return _hipcc(sources(), LIB, verbose)
 
 
 if __name__ == "__main__":

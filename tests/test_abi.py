@@ -212,3 +212,24 @@ def test_kernel_selection_table(lib):
     assert kind(Q8_0, 2048, 2048, 12) == "skinny_kernel"
     assert kind(F16, 2048, 2048, 20) == "gemv_kernel"
     assert binding.kernel_name(Q4_K, 14336, 4096, 1) == "gemv1r_kernel<%d, 1, 2, 1, 8, 2, 1>" % Q4_K
+
+
+def test_ceiling_library_exports_and_checks():
+    """libceiling.so (the benchmark's streaming-ceiling kernels) exports what
+    include/lw_ceiling.h declares and rejects bad arguments before any HIP
+    call."""
+    path = os.path.join(ROOT, "paper_2605_20706_amd", "libceiling.so")
+    if not os.path.exists(path):
+        pytest.skip("libceiling.so not built")
+    src = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "lw_ceiling.h")).read(), flags=re.S)
+    names = sorted(set(re.findall(r"\b(lw_[a-z_]+)\s*\(", src)))
+    assert names == ["lw_ceiling_read", "lw_ceiling_write"]
+    lib = ctypes.CDLL(path)
+    lib.lw_ceiling_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
+    lib.lw_ceiling_write.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+    assert lib.lw_ceiling_read(None, 16, A16, None) == -1
+    assert lib.lw_ceiling_read(A256, 16, None, None) == -1
+    assert lib.lw_ceiling_read(A256, 24, A16, None) == -1
+    assert lib.lw_ceiling_read(A256 + 8, 16, A16, None) == -1
+    assert lib.lw_ceiling_write(A256, 0, None) == -1
+    assert lib.lw_ceiling_write(A256 + 4, 16, None) == -1

@@ -36,8 +36,9 @@ def run_multi(oracle_mod, fmt, Ms, K, n_tok, seed):
 @pytest.mark.parametrize("Ms,K", [((67, 130, 1), 2304), ((17, 5), 256), ((33, 40, 64, 3), 4352)])
 def test_multi_small(oracle_mod, fmt, Ms, K):
     """Ragged row counts (one launch over the LDS single-token kernel), up to
-    the four-matrix limit; two tokens go matrix by matrix."""
-    for n_tok in (1, 2):
+    the four-matrix limit; 2, 12 and 33 tokens (register, many-token and
+    prefill kernels) go matrix by matrix."""
+    for n_tok in (1, 2, 12, 33):
         run_multi(oracle_mod, fmt, list(Ms), K, n_tok, 31)
 
 
