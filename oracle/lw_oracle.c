@@ -21,6 +21,9 @@
  *   - Sec. 2.2, legacy formats: blocks of 32 weights; q8_0 and q4_0 are
  *     symmetric (no offset): value = d * q for q8_0, d * (q - 8) for the
  *     unsigned 4-bit codes of q4_0.
+ *   - Sec. 2.2, legacy formats with an offset (q4_1 among them): Eq. (1) with
+ *     both terms per block of 32, scale d and offset (min) m stored as
+ *     binary16: value = d * q + m for the unsigned 4-bit codes.
  *   - Sec. 2.2, K-quants: super-blocks of 256 = 8 sub-blocks of 32, each with
  *     its own scale, the scales quantized against a super-block scale; the
  *     K-quant style used here also carries a per-sub-block min quantized
@@ -34,7 +37,8 @@
  * four bits and element 32g+i+16 in its high four bits. Q4_K plane 1 holds one
  * 12-byte record per super-block, read as a 96-bit little-endian integer R:
  * sc_j = bits [6j, 6j+6), m_j = bits [48+6j, 48+6j+6). Q4_K plane 2 holds
- * {binary16 d, binary16 dmin} per super-block.
+ * {binary16 d, binary16 dmin} per super-block. Q4_1 plane 0 is as Q4_0's;
+ * plane 1 holds {binary16 d, binary16 m} per group of 32.
  *
  * Build: gcc -O2 -ffp-contract=off -fPIC -shared -pthread (no fast-math, no
  * vector intrinsics). Results do not depend on the thread count: each output
@@ -47,7 +51,7 @@
 #include <string.h>
 #include <unistd.h>
 
-enum { OR_F16 = 0, OR_Q8_0 = 1, OR_Q4_0 = 2, OR_Q4_K = 3 };
+enum { OR_F16 = 0, OR_Q8_0 = 1, OR_Q4_0 = 2, OR_Q4_K = 3, OR_Q4_1 = 4 };
 
 /* ---- plane arithmetic ---------------------------------------------------- */
 
@@ -72,6 +76,11 @@ static int planes(int fmt, int64_t n, int64_t off[3], int64_t* total) {
         if (n % 32) return -1;
         off[1] = round_up_256(n / 2);           /* two codes per byte */
         *total = off[1] + 2 * (n / 32);
+        return 0;
+    case OR_Q4_1:
+        if (n % 32) return -1;
+        off[1] = round_up_256(n / 2);
+        *total = off[1] + 4 * (n / 32);         /* n/32 {binary16 d, binary16 m} */
         return 0;
     case OR_Q4_K:
         if (n % 256) return -1;
@@ -146,6 +155,14 @@ static double exact_value(int fmt, const uint8_t* W, const int64_t off[3], int64
         int q = (int)q4_code(W, e);
         double d = half_value(read_u16(W + off[1] + 2 * (e / 32)));
         return (double)(q - 8) * d; /* exact */
+    }
+    case OR_Q4_1: {
+        int q = (int)q4_code(W, e);
+        double d = half_value(read_u16(W + off[1] + 4 * (e / 32)));
+        double m = half_value(read_u16(W + off[1] + 4 * (e / 32) + 2));
+        /* d*q has <= 15 significant bits; d*q and m are integer multiples of
+         * 2^-24 below 2^20 in magnitude, so their double sum is exact */
+        return (double)q * d + m;
     }
     case OR_Q4_K: {
         int64_t S = e / 256;

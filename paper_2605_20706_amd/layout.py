@@ -16,16 +16,17 @@ the previous one rounded up to 256 bytes):
 * q4_k  plane 0: as q4_0;  plane 1: n/256 x 12-byte record, a 96-bit
         little-endian integer with sc_j at bits [6j, 6j+6) and m_j at bits
         [48+6j, 48+6j+6);  plane 2: n/256 x {binary16 d, binary16 dmin}
+* q4_1  plane 0: as q4_0;  plane 1: n/32 x {binary16 d, binary16 m}
 """
 from __future__ import annotations
 
 import numpy as np
 
-F16, Q8_0, Q4_0, Q4_K = 0, 1, 2, 3
-FORMATS = {"f16": F16, "q8_0": Q8_0, "q4_0": Q4_0, "q4_k": Q4_K}
+F16, Q8_0, Q4_0, Q4_K, Q4_1 = 0, 1, 2, 3, 4
+FORMATS = {"f16": F16, "q8_0": Q8_0, "q4_0": Q4_0, "q4_k": Q4_K, "q4_1": Q4_1}
 FORMAT_NAMES = {v: k for k, v in FORMATS.items()}
 # Packed bytes per weight (codes and scales, ignoring plane padding).
-BYTES_PER_WEIGHT = {F16: 2.0, Q8_0: 34.0 / 32.0, Q4_0: 18.0 / 32.0, Q4_K: 144.0 / 256.0}
+BYTES_PER_WEIGHT = {F16: 2.0, Q8_0: 34.0 / 32.0, Q4_0: 18.0 / 32.0, Q4_K: 144.0 / 256.0, Q4_1: 20.0 / 32.0}
 
 ALIGN = 256
 
@@ -45,6 +46,11 @@ def plane_offsets(fmt: int, n: int):
             raise ValueError("n must be a multiple of 32")
         o1 = _up(n if fmt == Q8_0 else n // 2)
         return (0, o1, 0), o1 + 2 * (n // 32)
+    if fmt == Q4_1:
+        if n % 32:
+            raise ValueError("n must be a multiple of 32")
+        o1 = _up(n // 2)
+        return (0, o1, 0), o1 + 4 * (n // 32)
     if fmt == Q4_K:
         if n % 256:
             raise ValueError("n must be a multiple of 256")
@@ -135,3 +141,15 @@ def pack_q4_k(q, sc, m, d, dmin) -> np.ndarray:
     dd[:, 0] = d
     dd[:, 1] = dmin
     return assemble(Q4_K, n, pack_nibbles(q), pack_q4k_records(sc, m), dd)
+
+
+def pack_q4_1(q, d, m) -> np.ndarray:
+    q = np.asarray(q).reshape(-1)
+    d = _half_bits(d)
+    m = _half_bits(m)
+    if d.size * 32 != q.size or m.size * 32 != q.size:
+        raise ValueError("need one scale and one min per 32 codes")
+    dm = np.empty((q.size // 32, 2), dtype="<u2")
+    dm[:, 0] = d
+    dm[:, 1] = m
+    return assemble(Q4_1, q.size, pack_nibbles(q), dm)

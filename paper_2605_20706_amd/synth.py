@@ -15,6 +15,9 @@ Q8_0 matrix uses the literal seed 0):
         independent uniform nibbles per byte); d uniform in [1e-3, 2e-2];
 * q4_k  codes as q4_0; sc and m uniform in [0, 63]; d and dmin uniform in
         [1e-4, 2e-3] -> binary16;
+* q4_1  codes as q4_0; d uniform in [1e-3, 2e-2] and m uniform in [-0.2, 0]
+        -> binary16 (a block's values span [m, m + 15 d], as for weights
+        quantized against their block minimum);
 * x     float32 N(0, 1), shape [n_tok, K], from the generator of the workload
         (matrix_id 99).
 """
@@ -25,7 +28,7 @@ from dataclasses import dataclass
 import numpy as np
 
 from . import layout
-from .layout import F16, Q4_0, Q4_K, Q8_0
+from .layout import F16, Q4_0, Q4_1, Q4_K, Q8_0
 
 
 @dataclass(frozen=True)
@@ -116,6 +119,10 @@ def gen_fields(fmt: int, n: int, rng: np.random.Generator) -> dict:
     if fmt == Q4_0:
         return {"q": rng.integers(0, 16, n, dtype=np.uint8),
                 "d": _uniform_half(rng, 1e-3, 2e-2, n // 32)}
+    if fmt == Q4_1:
+        return {"q": rng.integers(0, 16, n, dtype=np.uint8),
+                "d": _uniform_half(rng, 1e-3, 2e-2, n // 32),
+                "m": _uniform_half(rng, -0.2, 0.0, n // 32)}
     if fmt == Q4_K:
         return {"q": rng.integers(0, 16, n, dtype=np.uint8),
                 "sc": rng.integers(0, 64, n // 32, dtype=np.uint8),
@@ -132,6 +139,8 @@ def pack_fields(fmt: int, f: dict) -> np.ndarray:
         return layout.pack_q8_0(f["q"], f["d"])
     if fmt == Q4_0:
         return layout.pack_q4_0(f["q"], f["d"])
+    if fmt == Q4_1:
+        return layout.pack_q4_1(f["q"], f["d"], f["m"])
     return layout.pack_q4_k(f["q"], f["sc"], f["m"], f["d"], f["dmin"])
 
 
@@ -145,6 +154,12 @@ def gen_packed(fmt: int, n: int, rng: np.random.Generator) -> np.ndarray:
     out[0:n // 2] = _random_bytes(rng, n // 2)
     if fmt == Q4_0:
         out[offs[1]:offs[1] + 2 * (n // 32)] = _uniform_half(rng, 1e-3, 2e-2, n // 32).view(np.uint8)
+        return out
+    if fmt == Q4_1:
+        dm = np.empty((n // 32, 2), dtype=np.float16)
+        dm[:, 0] = _uniform_half(rng, 1e-3, 2e-2, n // 32)
+        dm[:, 1] = _uniform_half(rng, -0.2, 0.0, n // 32)
+        out[offs[1]:offs[1] + 4 * (n // 32)] = dm.view(np.uint8).reshape(-1)
         return out
     sc = rng.integers(0, 64, n // 32, dtype=np.uint8)
     m = rng.integers(0, 64, n // 32, dtype=np.uint8)

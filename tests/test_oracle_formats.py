@@ -12,9 +12,9 @@ import pytest
 
 import golden_io
 from paper_2605_20706_amd import layout
-from paper_2605_20706_amd.layout import F16, Q4_0, Q4_K, Q8_0
+from paper_2605_20706_amd.layout import F16, Q4_0, Q4_1, Q4_K, Q8_0
 
-FMT = {"f16": F16, "q8_0": Q8_0, "q4_0": Q4_0, "q4_k": Q4_K}
+FMT = {"f16": F16, "q8_0": Q8_0, "q4_0": Q4_0, "q4_k": Q4_K, "q4_1": Q4_1}
 
 
 def bits(a):
@@ -77,6 +77,33 @@ def test_q4_0_exhaustive(oracle_mod):
     assert same_bits_or_both_zero(got, ref).all()
 
 
+def test_q4_1_every_scale(oracle_mod):
+    """All 16 codes x every finite binary16 scale, each block with a random
+    finite binary16 min, against q*d + m in double rounded once (q*d and m are
+    multiples of 2^-24 below 2^20, so the double sum is exact)."""
+    d = finite_halves()
+    m = np.random.default_rng(21).choice(finite_halves(), d.size)
+    q = np.tile(np.concatenate([np.arange(16), np.arange(16)]).astype(np.uint8), d.size)
+    got = oracle_mod.dequant(Q4_1, layout.pack_q4_1(q, d, m), q.size)
+    ref = (q.astype(np.float64) * np.repeat(d.view(np.float16).astype(np.float64), 32)
+           + np.repeat(m.view(np.float16).astype(np.float64), 32)).astype(np.float32)
+    ok = same_bits_or_both_zero(got, ref) | (np.isinf(got) & (got == ref))
+    assert ok.all(), np.flatnonzero(~ok)[:5]
+
+
+def test_q4_1_nibble_order_and_pair_plane(oracle_mod):
+    """Plane 1 holds {d, m} per group: with d = 1 and m = -8 a group decodes
+    like Q4_0 with d = 1, and with d = 0 every element is its group's min."""
+    codes = bytes(((i & 15) | ((15 - i) << 4)) for i in range(16))
+    plane0 = np.frombuffer(codes * 8, np.uint8)
+    dm = np.array([0x3C00, 0xC800] * 4 + [0x0000, 0x4500] * 4, np.uint16)  # (1, -8) x 4, (0, 5) x 4
+    W = layout.assemble(Q4_1, 256, plane0, dm)
+    got = oracle_mod.dequant(Q4_1, W, 256)
+    assert list(got[0:16]) == [i - 8 for i in range(16)]
+    assert list(got[16:32]) == [(15 - i) - 8 for i in range(16)]
+    assert (got[128:256] == 5.0).all()
+
+
 # --------------------------------------------------------------------------- hand values
 
 def _block_for(name, f):
@@ -90,6 +117,10 @@ def _block_for(name, f):
         q = np.zeros(256, np.uint8)
         q[0] = f["q"]
         return layout.pack_q4_0(q, np.repeat(h(f["d"]), 8)), 0
+    if name == "q4_1":
+        q = np.zeros(256, np.uint8)
+        q[0] = f["q"]
+        return layout.pack_q4_1(q, np.repeat(h(f["d"]), 8), np.repeat(h(f["m"]), 8)), 0
     q = np.zeros(256, np.uint8)
     q[0] = f["q"]
     sc = np.zeros(8, np.uint8)
@@ -225,6 +256,27 @@ def test_roundtrip_q8_0_q4_0_eq1(oracle_mod):
     in4 = (raw >= 0) & (raw <= 15)
     assert (np.abs(w - got4)[in4] <= s4[in4] / 2 * (1 + 1e-6)).all()
     assert in4.mean() > 0.95
+
+
+def test_roundtrip_q4_1_eq1(oracle_mod):
+    """Eq. (1) with an offset per block: m = the block minimum, d = the block
+    range / 15 (both rounded to binary16), q = round((w - m) / d) in [0, 15];
+    the oracle's d*q + m is within d/2 of w (plus one float32 rounding)."""
+    rng = np.random.default_rng(13)
+    n = 32 * 2048
+    w = rng.standard_normal(n) * 0.02
+    blocks = w.reshape(-1, 32)
+    m16 = blocks.min(axis=1).astype(np.float16)
+    d16 = ((blocks.max(axis=1) - m16.astype(np.float64)) / 15).astype(np.float16)
+    s = np.repeat(d16.astype(np.float64), 32)
+    mu = np.repeat(m16.astype(np.float64), 32)
+    raw = _round_half_away((w - mu) / s)
+    q = np.clip(raw, 0, 15)
+    got = oracle_mod.dequant(Q4_1, layout.pack_q4_1(q.astype(np.uint8), d16, m16), n).astype(np.float64)
+    inr = (raw >= 0) & (raw <= 15)
+    tol = s / 2 + np.abs(got) * 2.0 ** -24
+    assert (np.abs(w - got)[inr] <= tol[inr] * (1 + 1e-9)).all()
+    assert inr.mean() > 0.95
 
 
 def test_roundtrip_q4_k_eq1(oracle_mod):
