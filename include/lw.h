@@ -49,11 +49,15 @@
  *                    m_j = (R >> (48 + 6j)) & 63, j = 0..7.
  *           plane 2: n/256 x { binary16 d, binary16 dmin } (4 bytes each).
  *                                    value = d[S] * sc_j * q[e] - dmin[S] * m_j
+ *   LW_Q4_1 plane 0: as LW_Q4_0 plane 0.
+ *           plane 1: n/32 x { binary16 d, binary16 m } (4 bytes each).
+ *                                    value = q[e] * d[g] + m[g]
  *
  * The dequantized value of an element is the exact real value of its closed
  * form rounded once to binary32 with round-to-nearest-even. For LW_F16,
  * LW_Q8_0 and LW_Q4_0 the closed form is exactly representable in binary32;
- * for LW_Q4_K the two products are exact and the difference is rounded once.
+ * for LW_Q4_K the two products are exact and the difference is rounded once;
+ * for LW_Q4_1 the product is exact and the sum with the min is rounded once.
  * ------------------------------------------------------------------------
  */
 #ifndef LW_H
@@ -74,9 +78,10 @@ extern "C" {
 #define LW_API
 #endif
 
-/* Weight formats (Sec. 2.2: f16 storage, legacy symmetric blocks of 32,
- * K-quant super-blocks of 256 with double-quantized scales and mins). */
-typedef enum { LW_F16 = 0, LW_Q8_0 = 1, LW_Q4_0 = 2, LW_Q4_K = 3 } lw_fmt;
+/* Weight formats (Sec. 2.2: f16 storage, legacy blocks of 32 without (Q8_0,
+ * Q4_0) and with (Q4_1) an offset, K-quant super-blocks of 256 with
+ * double-quantized scales and mins). */
+typedef enum { LW_F16 = 0, LW_Q8_0 = 1, LW_Q4_0 = 2, LW_Q4_K = 3, LW_Q4_1 = 4 } lw_fmt;
 
 /* Return codes. */
 enum {

@@ -4,7 +4,8 @@
 // block structures of Sec. 2.2) is evaluated with exact float32 products and at
 // most one rounding: q*d and (q-8)*d are exact products; the K-quant style
 // value d*sc*q - dmin*m is one fused multiply-add of the exact d*sc and the
-// exact dmin*m. No half-precision arithmetic is used.
+// exact dmin*m, and Q4_1's q*d + m one fused multiply-add of the exact q*d
+// and m. No half-precision arithmetic is used.
 //
 // Work split: per grid-stride step a thread writes four float4 (4 consecutive
 // elements each), 256 float4 apart, so each store instruction of a wave is
@@ -55,6 +56,13 @@ __device__ __forceinline__ float4 value4(const uint8_t* __restrict__ W, int64_t 
             v.y = (ubyte<1>(b) - 8.0f) * d;
             v.z = (ubyte<2>(b) - 8.0f) * d;
             v.w = (ubyte<3>(b) - 8.0f) * d;
+        } else if constexpr (FMT == LW_Q4_1) {
+            const uint32_t dm = *reinterpret_cast<const uint32_t*>(W + off1 + 4 * g);
+            const float d = half_bits_to_float(dm & 0xFFFFu), m = half_bits_to_float(dm >> 16);
+            v.x = __builtin_fmaf(ubyte<0>(b), d, m);  // exact product, one rounding
+            v.y = __builtin_fmaf(ubyte<1>(b), d, m);
+            v.z = __builtin_fmaf(ubyte<2>(b), d, m);
+            v.w = __builtin_fmaf(ubyte<3>(b), d, m);
         } else {
             const int64_t S = e >> 8;
             const int j = (int)(g & 7);
@@ -121,6 +129,7 @@ hipError_t launch_dequant(int fmt, const uint8_t* W, float* out, int64_t n, cons
     case LW_Q8_0: return launch<LW_Q8_0>(W, out, n, p, stream);
     case LW_Q4_0: return launch<LW_Q4_0>(W, out, n, p, stream);
     case LW_Q4_K: return launch<LW_Q4_K>(W, out, n, p, stream);
+    case LW_Q4_1: return launch<LW_Q4_1>(W, out, n, p, stream);
     default: return hipErrorInvalidValue;
     }
 }

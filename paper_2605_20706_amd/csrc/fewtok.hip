@@ -38,6 +38,7 @@
 // and used as P's accumulator:
 //   Q4_0:     w = d (q - 8)         -> c1 = d,    k = -136, dm = 0
 //   Q4_K:     w = d sc q - dmin m   -> c1 = d sc, k = -128, dm = dmin m / 128
+//   Q4_1:     w = d q + m           -> c1 = d,    k = -128, dm = -m / 128
 // Accumulation is f32 throughout.
 #include "lw_internal.hpp"
 #include "lw_mfma.hpp"
@@ -53,7 +54,7 @@ constexpr int kFtMaxWaves = 16;  // waves per workgroup
 constexpr int kFtWinSB = 16;     // super-blocks per window: 16 x 8 blocks x 1 KiB of A = 128 KiB of LDS
 constexpr int kFtMaxTpw = 4;     // tiles per wave when the waves do not split K
 template <int FMT>
-constexpr int kFtRing = FMT == LW_Q4_K ? 2 : 3;  // units in flight per wave (Q4_K: fewer, its scales take more registers)
+constexpr int kFtRing = FMT == LW_Q4_0 ? 3 : 2;  // units in flight per wave (fewer where the scales take more registers)
 
 // Scale data of one super-block (8 blocks, 256 columns) of one weight row.
 template <int FMT>
@@ -72,6 +73,24 @@ struct SbScale<LW_Q4_0> {
         c1[1] = half_bits_to_float(a >> 16);
         c1[2] = half_bits_to_float(b & 0xFFFFu);
         c1[3] = half_bits_to_float(b >> 16);
+    }
+};
+
+template <>
+struct SbScale<LW_Q4_1> {
+    u32x4 dm[2];  // {binary16 d, binary16 m} of the 8 blocks
+    __device__ void load(const uint8_t* P1, const uint8_t*, uint64_t sbi) {
+        dm[0] = *reinterpret_cast<const u32x4*>(P1 + 32 * sbi);
+        dm[1] = *reinterpret_cast<const u32x4*>(P1 + 32 * sbi + 16);
+    }
+    // c1 = d and dm = -m / 128 of blocks 4h .. 4h+3
+    __device__ void coef(int h, float* c1, float* dmo) const {
+        const u32x4 v = h ? dm[1] : dm[0];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            c1[i] = half_bits_to_float(v[i] & 0xFFFFu);
+            dmo[i] = half_bits_to_float(v[i] >> 16) * (-1.0f / 128.0f);
+        }
     }
 };
 
@@ -301,7 +320,7 @@ __global__ void __launch_bounds__(64 * kFtMaxWaves)
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
                     float o = __builtin_fmaf(c1[j], Pm[j][v], t[v]);
-                    if constexpr (FMT == LW_Q4_K) o = __builtin_fmaf(dm[j], C[j][v], o);
+                    if constexpr (FMT != LW_Q4_0) o = __builtin_fmaf(dm[j], C[j][v], o);
                     t[v] = o;
                 }
         }
@@ -527,6 +546,7 @@ hipError_t launch_fewtok(int fmt, const uint8_t* W, const float* x, float* y, in
     switch (fmt) {
     case LW_Q4_0: return launch_one<LW_Q4_0>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q4_K: return launch_one<LW_Q4_K>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q4_1: return launch_one<LW_Q4_1>(W, x, y, M, K, n_tok, p, stream);
     default: return hipErrorNotSupported;
     }
 }
@@ -536,6 +556,7 @@ hipError_t launch_fewtok_multi(int fmt, int n, const uint8_t* const* W, float* c
     switch (fmt) {
     case LW_Q4_0: return launch_multi_ft<LW_Q4_0>(n, W, y, M, x, K, n_tok, stream);
     case LW_Q4_K: return launch_multi_ft<LW_Q4_K>(n, W, y, M, x, K, n_tok, stream);
+    case LW_Q4_1: return launch_multi_ft<LW_Q4_1>(n, W, y, M, x, K, n_tok, stream);
     default: return hipErrorNotSupported;
     }
 }

@@ -20,7 +20,8 @@
 //  * Codes become floats with one v_cvt_f32_ubyteN each (4-bit: the low and
 //    high nibbles are masked in place, the high-nibble sum is scaled by 1/16
 //    at the end); block scales are applied once per 32 elements in factored
-//    form: Q4_0 d*(sum q*x - 8*sum x), Q4_K-style d*sc*sum q*x - dmin*m*sum x,
+//    form: Q4_0 d*(sum q*x - 8*sum x), Q4_1 d*sum q*x + m*sum x, Q4_K-style
+//    d*sc*sum q*x - dmin*m*sum x,
 //    with the per-group sums of x precomputed in LDS per tile.
 // Accumulation is float32 throughout; only the rounding order differs from
 // the plain definition.
@@ -207,6 +208,41 @@ struct Traits<LW_Q4_0> {
     }
 };
 
+// Q4_1: Q4_0's codes with a {binary16 d, binary16 m} pair per group.
+template <>
+struct Traits<LW_Q4_1> {
+    static constexpr int EPL = 32;
+    static constexpr bool kGroupSums = true;
+    struct Packet {
+        uint4 c;
+        uint32_t dm;  // d in bits 0..15, m in bits 16..31
+    };
+    __device__ static Packet load(const uint8_t* W, int64_t e, int64_t off1, int64_t) {
+        Packet p;
+        p.c = *reinterpret_cast<const uint4*>(W + (e >> 1));
+        p.dm = *reinterpret_cast<const uint32_t*>(W + off1 + 4 * (e >> 5));
+        return p;
+    }
+    struct Base {
+        uint32_t c, dm;
+    };
+    __device__ static Base base(uint32_t row, uint32_t K, uint32_t c) {  // chunk = 2048 elements
+        return {row * (K / 2u) + 1024u * c, row * (K / 8u) + 256u * c};
+    }
+    __device__ static Packet load_at(const uint8_t* W, const uint8_t* P1, const uint8_t*, const Base& b,
+                                     uint32_t la) {
+        Packet p;
+        p.c = stream_load16(W + b.c + 16u * la);
+        p.dm = *reinterpret_cast<const uint32_t*>(P1 + b.dm + 4u * la);
+        return p;
+    }
+    // d * sum q*x + m * sum x
+    __device__ static float dot(const Packet& p, const float4* xv, float sx, int) {
+        return __builtin_fmaf(half_bits_to_float(p.dm >> 16), sx,
+                              half_bits_to_float(p.dm & 0xFFFFu) * nibble_dot(p.c, xv));
+    }
+};
+
 template <>
 struct Traits<LW_Q4_K> {
     static constexpr int EPL = 32;
@@ -319,6 +355,18 @@ __device__ __forceinline__ void dot24(const Traits<LW_Q4_0>::Packet& p, const fl
     const float d = half_bits_to_float(p.d);
 #pragma unroll
     for (int t = 0; t < NTK; ++t) acc[t] = __builtin_fmaf(d, __builtin_fmaf(-8.0f, sx24[t], qx[t]), acc[t]);
+}
+
+// acc[t] += (Q4_1 contribution of the lane for token t) * 2^-24:
+// d * sum q*x_t + m * sum x_t.
+template <int NTK>
+__device__ __forceinline__ void dot24(const Traits<LW_Q4_1>::Packet& p, const float4* const* xv,
+                                      const float* sx24, const SubBlock&, float* acc) {
+    float qx[NTK];
+    nibble_dot24<NTK>(p.c, xv, qx);
+    const float d = half_bits_to_float(p.dm & 0xFFFFu), m = half_bits_to_float(p.dm >> 16);
+#pragma unroll
+    for (int t = 0; t < NTK; ++t) acc[t] = __builtin_fmaf(m, sx24[t], __builtin_fmaf(d, qx[t], acc[t]));
 }
 
 // acc[t] += (Q4_K-style contribution for token t) * 2^-24:
@@ -1015,7 +1063,7 @@ hipError_t launch_multi_ns(int n, const uint8_t* const* W, float* const* y, cons
             if (p.total > max_total) max_total = p.total;
         }
     }
-    if constexpr (FMT == LW_Q4_0 || FMT == LW_Q4_K) {
+    if constexpr (FMT == LW_Q4_0 || FMT == LW_Q4_K || FMT == LW_Q4_1) {
         const hipError_t err = launch_reg_segs<FMT, NS>(sg, x, tot, K, 1, max_total, stream);
         if (err != hipErrorNotSupported) return err;
     }
@@ -1068,6 +1116,7 @@ hipError_t launch_gemv_multi(int fmt, int n, const uint8_t* const* W, float* con
     case LW_Q8_0: return launch_multi_fmt<LW_Q8_0>(n, W, y, M, x, K, stream);
     case LW_Q4_0: return launch_multi_fmt<LW_Q4_0>(n, W, y, M, x, K, stream);
     case LW_Q4_K: return launch_multi_fmt<LW_Q4_K>(n, W, y, M, x, K, stream);
+    case LW_Q4_1: return launch_multi_fmt<LW_Q4_1>(n, W, y, M, x, K, stream);
     default: return hipErrorInvalidValue;
     }
 }
@@ -1077,6 +1126,7 @@ hipError_t launch_gemv_reg(int fmt, const uint8_t* W, const float* x, float* y, 
     switch (fmt) {
     case LW_Q4_0: return launch_reg_fmt<LW_Q4_0>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q4_K: return launch_reg_fmt<LW_Q4_K>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q4_1: return launch_reg_fmt<LW_Q4_1>(W, x, y, M, K, n_tok, p, stream);
     default: return hipErrorNotSupported;
     }
 }
@@ -1088,6 +1138,7 @@ hipError_t launch_gemv(int fmt, const uint8_t* W, const float* x, float* y, int6
     case LW_Q8_0: return launch_fmt<LW_Q8_0>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q4_0: return launch_fmt<LW_Q4_0>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q4_K: return launch_fmt<LW_Q4_K>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q4_1: return launch_fmt<LW_Q4_1>(W, x, y, M, K, n_tok, p, stream);
     default: return hipErrorInvalidValue;
     }
 }

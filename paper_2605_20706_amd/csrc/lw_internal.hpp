@@ -66,6 +66,10 @@ inline Planes planes_of(int fmt, int64_t n) {
         p.off1 = round_up_256(n / 2);
         p.total = p.off1 + 2 * (n / 32);
         break;
+    case LW_Q4_1:
+        p.off1 = round_up_256(n / 2);
+        p.total = p.off1 + 4 * (n / 32);
+        break;
     case LW_Q4_K:
         p.off1 = round_up_256(n / 2);
         p.off2 = round_up_256(p.off1 + 12 * (n / 256));

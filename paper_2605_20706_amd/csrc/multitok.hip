@@ -19,6 +19,7 @@
 // the constant k (exact in bf16) and is the accumulator P starts from:
 //   Q4_0:     w = d (q - 8)         -> c1 = d,    k = -136, dm = 0
 //   Q4_K:     w = d sc q - dmin m   -> c1 = d sc, k = -128, dm = dmin m
+//   Q4_1:     w = d q + m           -> c1 = d,    k = -128, dm = -m
 #include "lw_device.hpp"
 #include "lw_internal.hpp"
 
@@ -91,6 +92,22 @@ struct StepScale<LW_Q4_0> {
         c1[2] = half_bits_to_float(b & 0xFFFFu);
         c1[3] = half_bits_to_float(b >> 16);
         dm[0] = dm[1] = dm[2] = dm[3] = 0.f;
+    }
+};
+
+template <>
+struct StepScale<LW_Q4_1> {
+    u32x4 v;  // {binary16 d, binary16 m} of the 4 blocks
+    __device__ void load(const uint8_t* P1, const uint8_t*, uint64_t row, uint32_t K, uint32_t s, int) {
+        v = *reinterpret_cast<const u32x4*>(P1 + 4 * (row * (K / 32u) + 4u * s));
+    }
+    // c1 = d and dm = -m / 128 of the step's blocks
+    __device__ void coef(uint32_t, int, float* c1, float* dm) const {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            c1[i] = half_bits_to_float(v[i] & 0xFFFFu);
+            dm[i] = half_bits_to_float(v[i] >> 16) * (-1.0f / 128.0f);
+        }
     }
 };
 
@@ -279,7 +296,7 @@ __global__ void __launch_bounds__(64 * kMaxWaves)
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
                     float o = __builtin_fmaf(c1[j], P[v], acc[q][v]);
-                    if constexpr (FMT == LW_Q4_K) o = __builtin_fmaf(dm[j], C[j][v], o);
+                    if constexpr (FMT != LW_Q4_0) o = __builtin_fmaf(dm[j], C[j][v], o);
                     acc[q][v] = o;
                 }
             }
@@ -350,6 +367,25 @@ struct PairScale<LW_Q4_0> {
         c1[1] = half_bits_to_float(a >> 16);
         c1[2] = half_bits_to_float(b & 0xFFFFu);
         c1[3] = half_bits_to_float(b >> 16);
+    }
+};
+
+template <>
+struct PairScale<LW_Q4_1> {
+    u32x4 v[2];  // {binary16 d, binary16 m} of the 8 blocks
+    __device__ void load(const uint8_t* P1, const uint8_t*, uint64_t row, uint32_t K, uint32_t ps) {
+        const uint8_t* p = P1 + 4 * (row * (K / 32u) + 8u * ps);
+        v[0] = *reinterpret_cast<const u32x4*>(p);
+        v[1] = *reinterpret_cast<const u32x4*>(p + 16);
+    }
+    // c1 = d and dm = -m / 128 of blocks 4h..4h+3
+    __device__ void coef(int h, float* c1, float* dm) const {
+        const u32x4 w = h ? v[1] : v[0];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            c1[i] = half_bits_to_float(w[i] & 0xFFFFu);
+            dm[i] = half_bits_to_float(w[i] >> 16) * (-1.0f / 128.0f);
+        }
     }
 };
 
@@ -537,7 +573,7 @@ __global__ void __launch_bounds__(64 * kMaxWaves)
 #pragma unroll
                     for (int v = 0; v < 4; ++v) {
                         float o = __builtin_fmaf(c1[j], P[j][v], acc[q][v]);
-                        if constexpr (FMT == LW_Q4_K) o = __builtin_fmaf(dm[j], C[j][v], o);
+                        if constexpr (FMT != LW_Q4_0) o = __builtin_fmaf(dm[j], C[j][v], o);
                         acc[q][v] = o;
                     }
             }
@@ -648,7 +684,7 @@ hipError_t launch_f(const uint8_t* W, const float* x, float* y, int64_t M, int64
     const bool rg2 = (M + 31) / 32 >= cus;
     const int64_t wgs = rg2 ? (M + 31) / 32 : (M + 15) / 16;
     const int nw = wgs >= 2 * cus ? 4 : 8;
-    if (n_tok <= 8 && FMT == LW_Q4_K) return launch_rg<FMT, 1>(W, x, y, M, K, n_tok, p, nw, stream);
+    if (n_tok <= 8 && FMT != LW_Q4_0) return launch_rg<FMT, 1>(W, x, y, M, K, n_tok, p, nw, stream);
     return rg2 ? launch_rg<FMT, 2>(W, x, y, M, K, n_tok, p, nw, stream)
                : launch_rg<FMT, 1>(W, x, y, M, K, n_tok, p, nw, stream);
 }
@@ -656,7 +692,7 @@ hipError_t launch_f(const uint8_t* W, const float* x, float* y, int64_t M, int64
 }  // namespace
 
 bool multitok_supported(int fmt, int64_t n_tok) {
-    return (fmt == LW_Q4_0 || fmt == LW_Q4_K) && n_tok >= 2 && n_tok <= 16;
+    return (fmt == LW_Q4_0 || fmt == LW_Q4_K || fmt == LW_Q4_1) && n_tok >= 2 && n_tok <= 16;
 }
 
 hipError_t launch_multitok(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
@@ -664,6 +700,7 @@ hipError_t launch_multitok(int fmt, const uint8_t* W, const float* x, float* y, 
     switch (fmt) {
     case LW_Q4_0: return launch_f<LW_Q4_0>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q4_K: return launch_f<LW_Q4_K>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q4_1: return launch_f<LW_Q4_1>(W, x, y, M, K, n_tok, p, stream);
     default: return hipErrorInvalidValue;
     }
 }

@@ -15,6 +15,7 @@
 // bias are applied to its float32 partial P:
 //   Q4_0:   y += d * P - 136 * d * S     (128 + q = (q - 8) + 136)
 //   Q4_K:   y += d*sc * P - (128*d*sc + dmin*m) * S
+//   Q4_1:   y += d * P + (m - 128*d) * S
 //   Q8_0:   y += d * P
 // where S = sum over the block of (hi + lo), the very values fed to the
 // matrix core, so the bias cancels to float32 rounding. The error relative
@@ -71,6 +72,7 @@ struct MF;
 template <int FMT>
 struct MF4 {
     static constexpr bool kSums = true;
+    static constexpr int kRaw = FMT == LW_Q4_1 ? 8 : 4;  // raw scale words of 8 blocks
     __device__ static uint32_t code_word(const uint8_t* W, uint64_t row, uint32_t K, int blk, int s) {
         return *reinterpret_cast<const uint32_t*>(W + row * (K / 2u) + 16u * (uint32_t)blk + 4u * s);
     }
@@ -94,6 +96,8 @@ struct MF4 {
                                       int blk, uint32_t* r) {
         if constexpr (FMT == LW_Q4_0) {
             r[0] = *reinterpret_cast<const uint16_t*>(W + off1 + 2 * (row * (K / 32u) + (uint32_t)blk));
+        } else if constexpr (FMT == LW_Q4_1) {
+            r[0] = *reinterpret_cast<const uint32_t*>(W + off1 + 4 * (row * (K / 32u) + (uint32_t)blk));
         } else {
             const uint64_t sb = row * (K / 256u) + (uint32_t)(blk >> 3);
             const uint32_t* rec = reinterpret_cast<const uint32_t*>(W + off1 + 12 * sb);
@@ -114,6 +118,17 @@ struct MF4 {
             r[1] = v.y;
             r[2] = v.z;
             r[3] = v.w;
+        } else if constexpr (FMT == LW_Q4_1) {
+            const uint4* p = reinterpret_cast<const uint4*>(W + off1 + 4 * (row * (K / 32u) + (uint32_t)blk0));
+            const uint4 v = p[0], u = p[1];
+            r[0] = v.x;
+            r[1] = v.y;
+            r[2] = v.z;
+            r[3] = v.w;
+            r[4] = u.x;
+            r[5] = u.y;
+            r[6] = u.z;
+            r[7] = u.w;
         } else {
             load_scale(W, off1, off2, row, K, blk0, r);
         }
@@ -123,6 +138,8 @@ struct MF4 {
             const float d = half_bits_to_float((r[e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
             *c1 = d;
             *c2 = -136.0f * d;
+        } else if constexpr (FMT == LW_Q4_1) {
+            coef_raw(r + e, e, c1, c2);
         } else {
             coef_raw(r, e, c1, c2);
         }
@@ -132,6 +149,10 @@ struct MF4 {
             const float d = half_bits_to_float(r[0]);
             *c1 = d;
             *c2 = -136.0f * d;
+        } else if constexpr (FMT == LW_Q4_1) {
+            const float d = half_bits_to_float(r[0] & 0xFFFFu);
+            *c1 = d;
+            *c2 = __builtin_fmaf(-128.0f, d, half_bits_to_float(r[0] >> 16));  // m - 128 d
         } else {
             const uint32_t ts = 6u * (uint32_t)(blk & 7), tm = ts + 16u;
             const bool sl = ts < 32u, ml = tm < 32u;
@@ -148,10 +169,13 @@ template <>
 struct MF<LW_Q4_0> : MF4<LW_Q4_0> {};
 template <>
 struct MF<LW_Q4_K> : MF4<LW_Q4_K> {};
+template <>
+struct MF<LW_Q4_1> : MF4<LW_Q4_1> {};
 
 template <>
 struct MF<LW_Q8_0> {
     static constexpr bool kSums = false;
+    static constexpr int kRaw = 4;  // raw scale words of 8 blocks
     // two words: elements 8s .. 8s+7; returned packed in one 64-bit value
     __device__ static uint64_t code_word(const uint8_t* W, uint64_t row, uint32_t K, int blk, int s) {
         return *reinterpret_cast<const uint64_t*>(W + row * K + 32u * (uint32_t)blk + 8u * s);
@@ -364,7 +388,7 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
     const int64_t crow = row0 + tid < M ? row0 + tid : M - 1;
     const int c_at = (tid >> 6) * 64 + (tid & 15) * 4 + ((tid >> 4) & 3);   // c1 slot (wave, row, rt) of this row
     float* const c2_row = win_c2 + (tid >> 4) * 256 + (tid & 15) * 4;       // + g * 64 + j
-    uint32_t sraw[2][4];
+    uint32_t sraw[2][T::kRaw];
     auto load_win_scales = [&](int w) __attribute__((always_inline)) {
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
@@ -679,6 +703,7 @@ hipError_t launch_prefill(int fmt, const uint8_t* W, const float* x, float* y, i
     switch (fmt) {
     case LW_Q4_0: return launch_gemm<LW_Q4_0>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q4_K: return launch_gemm<LW_Q4_K>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q4_1: return launch_gemm<LW_Q4_1>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q8_0: return launch_gemm<LW_Q8_0>(W, x, y, M, K, n_tok, p, stream);
     default:
         // f16 weights: token blocks of the matrix-vector kernel (float32 throughout)

@@ -10,7 +10,7 @@
 // its own row's block scale without any exchange.
 //
 // Precision: as on the prefill path -- B holds the exact bf16 of the biased
-// 4-bit code 128 + q (Q4_0, Q4_K-style) or of the int8 code (Q8_0); X is split
+// 4-bit code 128 + q (Q4_0, Q4_K-style, Q4_1) or of the int8 code (Q8_0); X is split
 // into bf16 high and low parts; per block, y += c1 * P + c2 * S with S the sum
 // of the block's hi + lo values, so the bias cancels to float32 rounding.
 //
@@ -70,6 +70,12 @@ struct SK4 {
             r.a = v.x;
             r.b = v.y;
             r.c = r.d = 0;
+        } else if constexpr (FMT == LW_Q4_1) {
+            const uint4 v = *reinterpret_cast<const uint4*>(W + off1 + 4 * (row * (K / 32u) + (uint32_t)blk));
+            r.a = v.x;  // {d, m} of the step's 4 blocks
+            r.b = v.y;
+            r.c = v.z;
+            r.d = v.w;
         } else {
             const uint64_t Sb = row * (K / 256u) + (uint32_t)(blk >> 3);
             const uint32_t* rec = reinterpret_cast<const uint32_t*>(W + off1 + 12 * Sb);
@@ -88,6 +94,12 @@ struct SK4 {
             const float d = half_bits_to_float(h & 0xFFFFu);
             *c1 = d;
             *c2 = -136.0f * d;
+        } else if constexpr (FMT == LW_Q4_1) {
+            const int i = blk & 3;
+            const uint32_t dm = i == 0 ? r.a : i == 1 ? r.b : i == 2 ? r.c : r.d;
+            const float d = half_bits_to_float(dm & 0xFFFFu);
+            *c1 = d;
+            *c2 = __builtin_fmaf(-128.0f, d, half_bits_to_float(dm >> 16));  // m - 128 d
         } else {
             const int j = blk & 7;
             const uint64_t lo = (uint64_t)r.a | ((uint64_t)r.b << 32);
@@ -103,6 +115,8 @@ template <>
 struct SK<LW_Q4_0> : SK4<LW_Q4_0> {};
 template <>
 struct SK<LW_Q4_K> : SK4<LW_Q4_K> {};
+template <>
+struct SK<LW_Q4_1> : SK4<LW_Q4_1> {};
 
 template <>
 struct SK<LW_Q8_0> {
@@ -299,13 +313,14 @@ hipError_t launch_s(const uint8_t* W, const float* x, float* y, int64_t M, int64
 
 }  // namespace
 
-bool skinny_supported(int fmt) { return fmt == LW_Q4_0 || fmt == LW_Q4_K || fmt == LW_Q8_0; }
+bool skinny_supported(int fmt) { return fmt == LW_Q4_0 || fmt == LW_Q4_K || fmt == LW_Q4_1 || fmt == LW_Q8_0; }
 
 hipError_t launch_skinny(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
                          const Planes& p, hipStream_t stream) {
     switch (fmt) {
     case LW_Q4_0: return launch_s<LW_Q4_0, 4>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q4_K: return launch_s<LW_Q4_K, 4>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q4_1: return launch_s<LW_Q4_1, 4>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q8_0: return launch_s<LW_Q8_0, 4>(W, x, y, M, K, n_tok, p, stream);
     default: return hipErrorInvalidValue;
     }

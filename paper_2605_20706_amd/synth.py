@@ -89,6 +89,12 @@ WORKLOADS = {
                                  n_toks=(1, 2, 4, 8, 512),
                                  description="multi-token Q4_0 on Llama-3-8B gate/up/down, "
                                              "n_tok in {1,2,4,8} and prefill 512"),
+    "q4_1_llama8b_ffn": Workload("q4_1_llama8b_ffn", 6, Q4_1,
+                                 (Matrix("gate", 14336, 4096, 0, 2), Matrix("up", 14336, 4096, 0, 3),
+                                  Matrix("down", 4096, 14336, 0, 4)),
+                                 n_toks=(1, 2, 4, 8, 512),
+                                 description="Q4_1 (blocks with a min) on Llama-3-8B gate/up/down, "
+                                             "n_tok in {1,2,4,8} and prefill 512"),
 }
 
 

@@ -39,7 +39,8 @@ def test_q8_0_2048_full(oracle_mod):
 
 # one matrix of every distinct shape of each workload (layer 0, and the lm_head)
 CASES = [("f16_llama1b", i) for i in range(5)] + [("q4_0_llama1b", i) for i in (0, 1, 2, 4, 80)] + \
-        [("q4_k_llama8b", i) for i in (0, 1, 2, 4, 160)] + [("q4_0_llama8b_ffn", i) for i in range(3)]
+        [("q4_k_llama8b", i) for i in (0, 1, 2, 4, 160)] + [("q4_0_llama8b_ffn", i) for i in range(3)] + \
+        [("q4_1_llama8b_ffn", i) for i in range(3)]
 
 
 @pytest.mark.parametrize("key,idx", CASES)
@@ -53,12 +54,13 @@ def test_workload_matrix_sampled(oracle_mod, key, idx):
     gate.check(y[0, rows], y_ref, A, f32_bound=1e-4, what=(key, idx))
 
 
+@pytest.mark.parametrize("key", ["q4_0_llama8b_ffn", "q4_1_llama8b_ffn"])
 @pytest.mark.parametrize("idx", range(3))
-def test_multi_token_ffn(oracle_mod, idx):
+def test_multi_token_ffn(oracle_mod, key, idx):
     """n_tok in {1, 2, 4, 8} and 512 on the 8B gate/up/down matrices; every
     token column of a batched call also agrees with its own n_tok = 1 call."""
     import torch
-    wl = synth.WORKLOADS["q4_0_llama8b_ffn"]
+    wl = synth.WORKLOADS[key]
     mat = wl.matrices[idx]
     W = synth.gen_matrix(wl, mat)
     Wg = to_gpu(W)

@@ -5,7 +5,7 @@ import pytest
 
 from gpu_util import gpu_dequant, same_bits_or_both_zero
 from paper_2605_20706_amd import layout, synth
-from paper_2605_20706_amd.layout import F16, Q4_0, Q4_K, Q8_0
+from paper_2605_20706_amd.layout import F16, Q4_0, Q4_1, Q4_K, Q8_0
 
 pytestmark = pytest.mark.gpu
 
@@ -60,8 +60,25 @@ def test_q4_k_tie_and_hand_values(oracle_mod):
     assert (got.view(np.uint32) == 0x45974ECA).all()
 
 
+def test_q4_1_every_scale(oracle_mod):
+    """All 16 codes x every finite binary16 d, random finite binary16 mins."""
+    d = finite_halves()
+    d = np.concatenate([d, d[: (-d.size) % 8]])  # whole super-block multiples of groups
+    m = np.random.default_rng(98).choice(finite_halves(), d.size)
+    q = np.tile(np.concatenate([np.arange(16), np.arange(16)]).astype(np.uint8), d.size)
+    check(oracle_mod, Q4_1, layout.pack_q4_1(q, d, m), q.size)
+
+
+def test_q4_1_tie_hand_value():
+    # the round-to-nearest-even tie of the golden file: q=13 d=0x5A4E m=0x2678
+    q = np.full(256, 13, np.uint8)
+    W = layout.pack_q4_1(q, np.full(8, 0x5A4E, np.uint16), np.full(8, 0x2678, np.uint16))
+    got = gpu_dequant(Q4_1, W, 256)
+    assert (got.view(np.uint32) == 0x4523EC68).all()
+
+
 @pytest.mark.parametrize("n", [256, 512 + 256, 4096 * 3 + 256])
-@pytest.mark.parametrize("fmt", [F16, Q8_0, Q4_0, Q4_K])
+@pytest.mark.parametrize("fmt", [F16, Q8_0, Q4_0, Q4_K, Q4_1])
 def test_small_and_ragged(oracle_mod, fmt, n):
     check(oracle_mod, fmt, synth.gen_packed(fmt, n, np.random.default_rng(n + fmt)), n)
 

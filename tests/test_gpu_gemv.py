@@ -12,11 +12,11 @@ import pytest
 import gate
 from gpu_util import gpu_matvec, to_gpu
 from paper_2605_20706_amd import synth
-from paper_2605_20706_amd.layout import F16, Q4_0, Q4_K, Q8_0
+from paper_2605_20706_amd.layout import F16, Q4_0, Q4_1, Q4_K, Q8_0
 
 pytestmark = pytest.mark.gpu
 
-FMTS = [F16, Q8_0, Q4_0, Q4_K]
+FMTS = [F16, Q8_0, Q4_0, Q4_K, Q4_1]
 # (M, K): single row; row tail below a workgroup's rows; K below one chunk;
 # K one chunk plus a ragged tail; several chunks; large K that needs x tiling.
 SHAPES = [(1, 256), (3, 768), (17, 2048), (67, 2304), (130, 4352), (33, 16640)]
@@ -36,7 +36,7 @@ def test_parity_small(oracle_mod, fmt, M, K):
         gate.check(y, y_ref[:nt], A[:nt], f32_bound=1e-4, what=(fmt, M, K, nt))
 
 
-@pytest.mark.parametrize("fmt", [Q4_0, Q4_K])
+@pytest.mark.parametrize("fmt", [Q4_0, Q4_K, Q4_1])
 def test_parity_many_rows(oracle_mod, fmt):
     """Enough rows for the matrix-core few-token kernel to take two row groups
     per workgroup and four waves (a ragged last workgroup of one row group,
@@ -52,7 +52,7 @@ def test_parity_many_rows(oracle_mod, fmt):
         gate.check(y, y_ref[:nt], A[:nt], f32_bound=1e-4, what=(fmt, M, K, nt))
 
 
-@pytest.mark.parametrize("fmt", [Q4_0, Q4_K])
+@pytest.mark.parametrize("fmt", [Q4_0, Q4_K, Q4_1])
 @pytest.mark.parametrize("M,K", [(70000, 512), (300000, 256), (8200, 14336)])
 def test_parity_few_tokens_tiles(oracle_mod, fmt, M, K):
     """Few-token matrix-core kernel with the activations in LDS: more 16-row
@@ -78,7 +78,7 @@ REG_SHAPES = [(1, 2048), (40000, 2048), (9, 4096), (16500, 4096), (5, 8192), (83
               (1, 14336), (3500, 14336)]
 
 
-@pytest.mark.parametrize("fmt", [Q4_0, Q4_K])
+@pytest.mark.parametrize("fmt", [Q4_0, Q4_K, Q4_1])
 @pytest.mark.parametrize("M,K", REG_SHAPES)
 def test_parity_whole_chunks(oracle_mod, fmt, M, K):
     W = synth.gen_packed(fmt, M * K, np.random.default_rng([fmt, M, K, 5]))

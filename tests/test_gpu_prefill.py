@@ -11,7 +11,7 @@ import pytest
 import gate
 from gpu_util import gpu_matvec, to_gpu
 from paper_2605_20706_amd import binding, synth
-from paper_2605_20706_amd.layout import Q4_0, Q4_K, Q8_0
+from paper_2605_20706_amd.layout import Q4_0, Q4_1, Q4_K, Q8_0
 
 pytestmark = pytest.mark.gpu
 
@@ -26,7 +26,7 @@ def run(oracle_mod, fmt, M, K, n_tok, seed):
     gate.check(y, y_ref, A, f32_bound=1e-4, what=(fmt, M, K, n_tok))
 
 
-@pytest.mark.parametrize("fmt", [Q4_0, Q4_K, Q8_0])
+@pytest.mark.parametrize("fmt", [Q4_0, Q4_K, Q4_1, Q8_0])
 @pytest.mark.parametrize("M,K,n_tok", [
     (1100, 4352, 100),  # 3 x 2 tiles (ragged rows and tokens); K split 5 + 5 + 5 + 2 super-blocks
     (300, 1024, 17),    # one tile, 17 tokens (one past the few-token paths); unsplit (4 super-blocks)
