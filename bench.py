@@ -265,6 +265,7 @@ def run_gpu(ws, steps, warmup, mode):
 KERNEL_SOURCES = {"gemv_kernel": "gemv.hip", "gemv1_kernel": "gemv.hip", "gemv1r_kernel": "gemv.hip",
                   "multitok_kernel": "multitok.hip", "multitok_pk_kernel": "multitok.hip",
                   "fewtok_kernel": "fewtok.hip", "skinny_kernel": "skinny.hip", "gemm_kernel": "prefill.hip",
+                  "gemm32_kernel": "prefill.hip",
                   "dequant_kernel": "dequant.hip"}
 
 

@@ -36,6 +36,9 @@ namespace {
 struct Name_gemm_kernel {
     static constexpr const char* base = "gemm_kernel";
 };
+struct Name_gemm32_kernel {
+    static constexpr const char* base = "gemm32_kernel";
+};
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -629,6 +632,387 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
     }
 }
 
+// ---------------------------------------------------------------------------
+// The 4-bit formats on 32 x 32 output tiles (v_mfma_f32_32x32x16_bf16, which
+// runs at about twice the rate of the 16 x 16 x 32 form on MI355X: 2.2-2.4
+// against 0.9-1.4 dense bf16 PFLOP/s in a throughput probe). Operand layout
+// (verified on the GPU): lane l supplies A[l % 32][8 (l / 32) + v] and
+// B[8 (l / 32) + v][l % 32], v = 0..7, and receives D[i][l % 32] for
+// i = 8 (v / 4) + 4 (l / 32) + v % 4, v = 0..15. A is X (32 tokens x 16 k),
+// B the biased codes (16 k x 32 weight rows): a lane holds 16 tokens of one
+// weight row, so one c1 per lane and tile scales all of its outputs.
+//
+// A 32-element block is two K-steps: lane (h, n) feeds elements 8h .. 8h+7
+// (K-step 0) and 16 + 8h .. 16 + 8h + 7 (K-step 1) of the block, which are the
+// low and the high nibbles of the block's bytes 8h .. 8h+7. Per block and
+// tile: four MFMAs (two K-steps, X high and low parts), then the 16 c1 FMAs.
+// A workgroup of WM waves covers 64 WM rows x 64 tokens; each wave owns 64
+// rows x 64 tokens as 2 x 2 tiles. The rest (stages, windows of 16 blocks
+// for the c2 * S product, now on v_mfma_f32_32x32x8_bf16, K splits and the
+// XCD-grouped tile order) is as in gemm_kernel.
+template <int WM>
+struct Tile32 {
+    static constexpr int BM = 64 * WM, BN = 64, NT = 64 * WM;
+    static constexpr int XI = kKB * BN * 4 / NT;  // X items (8 values) per thread and stage
+    static_assert(XI >= 1 && XI * NT == kKB * BN * 4, "whole X items per thread");
+    static constexpr int kX = kKB * 4 * BN;                // bf16x8 entries per half per stage: [b][2s+h][t]
+    static constexpr size_t kStage = (size_t)2 * kX * 16;  // xh, xl
+    static constexpr size_t kC = (size_t)kWin * BM * 4;    // c1 (or c2) of a window
+    static constexpr size_t kS = (size_t)kWin * BN * 4;    // block sums of a window
+    static constexpr size_t bytes() { return 2 * kStage + 2 * kC + kC + 2 * kS; }
+};
+
+// Biased bf16 codes (bits 0x4300 | q) of bytes 8h .. 8h+7 of a block, given as
+// two words: the low nibbles feed K-step 0, the high nibbles K-step 1.
+__device__ __forceinline__ void decode8(uint32_t w0, uint32_t w1, bf16x8* s0, bf16x8* s1) {
+    const uint32_t k43 = 0x43434343u;
+    const uint32_t l0 = opaque(w0 & 0x0F0F0F0Fu), l1 = opaque(w1 & 0x0F0F0F0Fu);
+    const uint32_t h0 = opaque((w0 >> 4) & 0x0F0F0F0Fu), h1 = opaque((w1 >> 4) & 0x0F0F0F0Fu);
+    const u32x4v a = {__builtin_amdgcn_perm(k43, l0, 0x04010400u), __builtin_amdgcn_perm(k43, l0, 0x04030402u),
+                      __builtin_amdgcn_perm(k43, l1, 0x04010400u), __builtin_amdgcn_perm(k43, l1, 0x04030402u)};
+    const u32x4v b = {__builtin_amdgcn_perm(k43, h0, 0x04010400u), __builtin_amdgcn_perm(k43, h0, 0x04030402u),
+                      __builtin_amdgcn_perm(k43, h1, 0x04010400u), __builtin_amdgcn_perm(k43, h1, 0x04030402u)};
+    *s0 = __builtin_bit_cast(bf16x8, a);
+    *s1 = __builtin_bit_cast(bf16x8, b);
+}
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+template <int FMT, int WM>
+__global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2, 2)))
+    gemm32_kernel(const uint8_t* __restrict__ W, const float* __restrict__ x, float* __restrict__ y, int64_t M,
+                  int64_t K, int64_t N, int64_t off1, int64_t off2, GemmSplit sp) {
+    using T = MF<FMT>;
+    using TL = Tile32<WM>;
+    constexpr int BM = TL::BM, BN = TL::BN, NT = TL::NT, XI = TL::XI;
+    static_assert(FMT != LW_Q8_0 && T::kSums, "the 4-bit formats");
+    extern __shared__ bf16x8 smem[];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wm = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int n32 = lane & 31, h = lane >> 5;
+
+    // tile of this workgroup (XCD-grouped order, as in gemm_kernel)
+    const int64_t G = (int64_t)gridDim.x;
+    const int64_t bi = (int64_t)blockIdx.x;
+    const int64_t L = (G & 7) == 0 ? (bi & 7) * (G >> 3) + (bi >> 3) : bi;
+    const int64_t tt_i = L % sp.ntt;
+    const int64_t rest = L / sp.ntt;
+    const int split = (int)(rest % sp.ks);
+    const int64_t rti = rest / sp.ks;
+    const int64_t row0 = rti * BM;
+    const int64_t tok0 = tt_i * BN;
+    const uint32_t K32 = (uint32_t)K;
+    const int nsb = (int)(K / 256);
+    const int sb0 = split * sp.sbp;
+    const int sb1 = sb0 + sp.sbp < nsb ? sb0 + sp.sbp : nsb;
+    const int kb0 = 8 * sb0;
+    const int nb = 8 * (sb1 - sb0);
+    const int nst = nb / kKB;
+    const int nwin = (nb + kWin - 1) / kWin;
+
+    char* lds = reinterpret_cast<char*>(smem);
+    auto st_xh = [&](int bf) __attribute__((always_inline)) { return reinterpret_cast<bf16x8*>(lds + bf * TL::kStage); };
+    auto st_xl = [&](int bf) __attribute__((always_inline)) { return st_xh(bf) + TL::kX; };
+    auto win_c1 = [&](int w) __attribute__((always_inline)) {
+        return reinterpret_cast<float*>(lds + 2 * TL::kStage + (w & 1) * TL::kC);
+    };
+    // c2 [row tile of 32][k-group g = block / 4][row in tile][4] and S
+    // [k-group][token][4] (one buffer per window parity): the operands of
+    // v_mfma_f32_32x32x8_bf16, lane (h, n) reading one float4 of each
+    float* win_c2 = reinterpret_cast<float*>(lds + 2 * TL::kStage + 2 * TL::kC);
+    auto win_s = [&](int w) __attribute__((always_inline)) { return win_c2 + kWin * BM + (w & 1) * kWin * BN; };
+
+    // ---- codes: lane (h, n) of row tile rt reads row 64 wm + 32 rt + n, bytes
+    // [32h, 32h + 32) of each quad's 64 (blocks 2h, 2h + 1) ----
+    const uint8_t* wp[2];
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+        const int64_t r = row0 + 64 * wm + 32 * rt + n32;
+        const uint64_t rr = (uint64_t)(r < M ? r : M - 1);
+        wp[rt] = W + rr * (K32 / 2u) + 16u * (uint32_t)kb0 + 32u * (uint32_t)h;
+    }
+    u32x4v qraw[2][2], qcur[2][2];
+    auto load_quad = [&](int q) __attribute__((always_inline)) {
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt) {
+            qraw[rt][0] = *reinterpret_cast<const u32x4v*>(wp[rt] + 64u * (uint32_t)q);
+            qraw[rt][1] = *reinterpret_cast<const u32x4v*>(wp[rt] + 64u * (uint32_t)q + 16u);
+        }
+    };
+    // lanes 0-31 hold blocks 0, 1 of the quad and lanes 32-63 blocks 2, 3 (four
+    // words each); swapping words 2, 3 of each low block with words 0, 1 of
+    // each high block leaves every lane the two words it feeds of every block:
+    // block 0 in words (0, 1) of qcur[0], block 1 in (0, 1) of qcur[1],
+    // block 2 in (2, 3) of qcur[0], block 3 in (2, 3) of qcur[1]
+    auto swap_quad = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+            for (int hv = 0; hv < 2; ++hv) {
+                const u32x4v v = qraw[rt][hv];
+                const auto s02 = __builtin_amdgcn_permlane32_swap(v[0], v[2], false, false);
+                const auto s13 = __builtin_amdgcn_permlane32_swap(v[1], v[3], false, false);
+                qcur[rt][hv] = u32x4v{s02[0], s13[0], s02[1], s13[1]};
+            }
+    };
+
+    // ---- window coefficients: thread tid handles row tid, all 16 blocks ----
+    const int64_t crow = row0 + tid < M ? row0 + tid : M - 1;
+    const int c_at = (tid >> 6) * 64 + (tid & 31) * 2 + ((tid >> 5) & 1);  // c1 slot of this row
+    float* const c2_row = win_c2 + (tid >> 5) * 512 + (tid & 31) * 4;      // + g * 128 + j
+    uint32_t sraw[2][T::kRaw];
+    auto load_win_scales = [&](int w) __attribute__((always_inline)) {
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+            int blk0 = kb0 + w * kWin + 8 * hh;
+            blk0 = blk0 < kb0 + nb ? blk0 : kb0 + nb - 8;  // past the split: a valid copy, never used
+            T::load_scale8(W, off1, off2, (uint64_t)crow, K32, blk0, sraw[hh]);
+        }
+    };
+    auto put_win_scales = [&](int w) __attribute__((always_inline)) {
+        float* c1w = win_c1(w);
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int b16 = 8 * hh + e;
+                float c1, c2;
+                T::coef8(sraw[hh], e, &c1, &c2);
+                c1w[b16 * BM + c_at] = c1;
+                c2_row[(b16 >> 2) * 128 + (b16 & 3)] = c2;
+            }
+    };
+
+    // ---- X stage producer: item (block b, token t, quarter q = 2s + hx):
+    // elements 16s + 8hx .. +7 of the block for token t ----
+    const float* xp[XI];
+    int xo[XI], so[XI], xb_[XI];
+#pragma unroll
+    for (int i = 0; i < XI; ++i) {
+        const int it = tid + i * NT;
+        const int q = it & 3, t = (it >> 2) % BN, b = (it >> 2) / BN;
+        const int64_t tk = tok0 + t < N ? tok0 + t : N - 1;  // past N: the last token, never stored
+        xp[i] = x + tk * K + 32 * (int64_t)(kb0 + b) + 8 * q;
+        xo[i] = (b * 4 + q) * BN + (t ^ (q << 2));  // the four quarters of a token in four bank groups
+        so[i] = t * 4;                               // S slot of (t, block 0); + (b16 >> 2) * 4 BN + (b16 & 3)
+        xb_[i] = b;
+    }
+    float4 xa[XI], xb[XI];
+    auto fetch = [&](int st) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < XI; ++i) {
+            const float* p = xp[i] + 32 * kKB * st;
+            xa[i] = *reinterpret_cast<const float4*>(p);
+            xb[i] = *reinterpret_cast<const float4*>(p + 4);
+        }
+    };
+    auto commit = [&](int bf, int st) __attribute__((always_inline)) {
+        bf16x8* xh = st_xh(bf);
+        bf16x8* xl = st_xl(bf);
+#pragma unroll
+        for (int i = 0; i < XI; ++i) {
+            const float v[8] = {xa[i].x, xa[i].y, xa[i].z, xa[i].w, xb[i].x, xb[i].y, xb[i].z, xb[i].w};
+            bf16x8 hv, lv;
+            float sum = split_bf16x8(v, &hv, &lv);
+            xh[xo[i]] = hv;
+            xl[xo[i]] = lv;
+            // the 4 quarters of (block, token) are one lane quad: after two
+            // exchanges every lane holds the block sum; all four store it
+            const int b16 = (st * kKB + xb_[i]) % kWin;
+            sum += dpp_move<0xB1>(sum);
+            sum += dpp_move<0x4E>(sum);
+            win_s(st * kKB / kWin)[so[i] + (b16 >> 2) * 4 * BN + (b16 & 3)] = sum;
+        }
+    };
+
+    f32x16 acc[2][2];  // [row tile][token tile]
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[rt][tt][v] = 0.f;
+
+    // A operand slot of K-step s (block 0 of a stage, token tile 0)
+    int a_at[2];
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) a_at[s2] = (2 * s2 + h) * BN + (n32 ^ ((2 * s2 + h) << 2));
+    // the words this lane feeds of quad block jb of row tile rt
+    auto pair_of = [&](int rt, int jb, uint32_t* w0, uint32_t* w1) __attribute__((always_inline)) {
+        const u32x4v v = qcur[rt][jb & 1];
+        *w0 = jb < 2 ? v[0] : v[2];
+        *w1 = jb < 2 ? v[1] : v[3];
+    };
+    auto compute = [&](int bf, int st, int j0) __attribute__((always_inline)) {
+        const bf16x8* xh = st_xh(bf);
+        const bf16x8* xl = st_xl(bf);
+        const float2* c1w = reinterpret_cast<const float2*>(win_c1(st * kKB / kWin));
+        // A operands one token tile ahead (across the block boundary too)
+        bf16x8 an[2][2];  // [s][hi, lo]
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) {
+            an[s2][0] = xh[a_at[s2]];
+            an[s2][1] = xl[a_at[s2]];
+        }
+#pragma unroll
+        for (int b = 0; b < kKB; ++b) {
+            const int b16 = (st * kKB + b) % kWin;
+            const float2 c1v = c1w[(b16 * BM + 64 * wm) / 2 + n32];
+            const float c1[2] = {c1v.x, c1v.y};
+            bf16x8 bw[2][2];  // [rt][s]
+#pragma unroll
+            for (int rt = 0; rt < 2; ++rt) {
+                uint32_t w0, w1;
+                pair_of(rt, j0 + b, &w0, &w1);
+                decode8(w0, w1, &bw[rt][0], &bw[rt][1]);
+            }
+#pragma unroll
+            for (int tt = 0; tt < 2; ++tt) {
+                bf16x8 a[2][2];
+#pragma unroll
+                for (int s2 = 0; s2 < 2; ++s2) {
+                    a[s2][0] = an[s2][0];
+                    a[s2][1] = an[s2][1];
+                }
+                if (tt == 0) {
+#pragma unroll
+                    for (int s2 = 0; s2 < 2; ++s2) {
+                        an[s2][0] = xh[b * 4 * BN + a_at[s2] + 32];
+                        an[s2][1] = xl[b * 4 * BN + a_at[s2] + 32];
+                    }
+                } else if (b + 1 < kKB) {
+#pragma unroll
+                    for (int s2 = 0; s2 < 2; ++s2) {
+                        an[s2][0] = xh[(b + 1) * 4 * BN + a_at[s2]];
+                        an[s2][1] = xl[(b + 1) * 4 * BN + a_at[s2]];
+                    }
+                }
+#pragma unroll
+                for (int rt = 0; rt < 2; ++rt) {
+                    f32x16 pz;
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) pz[v] = 0.f;
+                    f32x16 p = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0][0], bw[rt][0], pz, 0, 0, 0);
+                    p = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0][1], bw[rt][0], p, 0, 0, 0);
+                    p = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[1][0], bw[rt][1], p, 0, 0, 0);
+                    p = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[1][1], bw[rt][1], p, 0, 0, 0);
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) acc[rt][tt][v] = __builtin_fmaf(c1[rt], p[v], acc[rt][tt][v]);
+                }
+            }
+        }
+    };
+    // acc += S(window) . c2(window)^T for window w: two K-steps of 8 blocks on
+    // v_mfma_f32_32x32x8_bf16, S and c2 split three ways into bf16 parts
+    // (blocks past the split's end: S masked to zero)
+    auto bias = [&](int w) __attribute__((always_inline)) {
+        const int nv = nb - w * kWin < kWin ? nb - w * kWin : kWin;
+        const float4* sw = reinterpret_cast<const float4*>(win_s(w));
+        const float4* cw = reinterpret_cast<const float4*>(win_c2);
+#pragma unroll
+        for (int s8 = 0; s8 < 2; ++s8) {
+            const int g = 2 * s8 + h;  // k-group of this lane: blocks 4g .. 4g+3
+            bf16x4 sh[2], sm[2], sl[2];
+#pragma unroll
+            for (int tt = 0; tt < 2; ++tt) {
+                const float4 sv = sw[g * BN + 32 * tt + n32];
+                const float v[4] = {4 * g + 0 < nv ? sv.x : 0.f, 4 * g + 1 < nv ? sv.y : 0.f,
+                                    4 * g + 2 < nv ? sv.z : 0.f, 4 * g + 3 < nv ? sv.w : 0.f};
+                split3_bf16x4(v, &sh[tt], &sm[tt], &sl[tt]);
+            }
+#pragma unroll
+            for (int rt = 0; rt < 2; ++rt) {
+                const float4 cv = cw[((wm * 2 + rt) * 4 + g) * 32 + n32];
+                const float v[4] = {cv.x, cv.y, cv.z, cv.w};
+                bf16x4 chh, chm, chl;
+                split3_bf16x4(v, &chh, &chm, &chl);
+#pragma unroll
+                for (int tt = 0; tt < 2; ++tt) {
+                    f32x16 a = acc[rt][tt];
+                    a = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(sh[tt], chh, a, 0, 0, 0);
+                    a = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(sh[tt], chm, a, 0, 0, 0);
+                    a = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(sm[tt], chh, a, 0, 0, 0);
+                    a = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(sh[tt], chl, a, 0, 0, 0);
+                    a = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(sm[tt], chm, a, 0, 0, 0);
+                    a = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(sl[tt], chh, a, 0, 0, 0);
+                    acc[rt][tt] = a;
+                }
+            }
+        }
+    };
+    auto pin = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+            for (int tt = 0; tt < 2; ++tt) asm volatile("" : "+v"(acc[rt][tt]));
+    };
+    auto window_end = [&](int st) __attribute__((always_inline)) {
+        if (((st + 1) * kKB) % kWin == 0 || st == nst - 1) {
+            const int w = st * kKB / kWin;
+            bias(w);
+            __syncthreads();
+            if (w + 1 < nwin) put_win_scales(w + 1);
+            load_win_scales(w + 2 < nwin ? w + 2 : nwin - 1);
+        }
+    };
+
+    // ---- prologue ----
+    load_quad(0);
+    load_win_scales(0);
+    fetch(0);
+    put_win_scales(0);
+    load_win_scales(nwin > 1 ? 1 : 0);
+    commit(0, 0);
+    fetch(1);
+    __syncthreads();
+
+    // ---- main loop: stages in pairs (one quad of blocks); all global loads
+    // unconditional (indices past the end clamped; those copies never used) ----
+    for (int st = 0; st < nst; st += 2) {
+        const int s2 = st + 2 < nst ? st + 2 : nst - 1;
+        const int s3 = st + 3 < nst ? st + 3 : nst - 1;
+        swap_quad();
+        load_quad(s2 / 2);
+        // the next stage's X conversion shares a basic block with this
+        // stage's MFMAs; the FMAs complete before the window's branch
+        compute(0, st, 0);
+        commit(1, st + 1);
+        fetch(s2);
+        pin();
+        window_end(st);
+        __syncthreads();
+        compute(1, st + 1, 2);
+        commit(0, s2);  // past the end: a copy of the last stage, never read
+        fetch(s3);
+        pin();
+        window_end(st + 1);
+        __syncthreads();
+    }
+
+    // store: lane (h, n) holds tokens 32 tt + 8 (v / 4) + 4 h + v % 4 of weight
+    // row 64 wm + 32 rt + n (K splits: added to the zeroed y)
+    const bool split_k = sp.ks > 1;
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+        const int64_t r = row0 + 64 * wm + 32 * rt + n32;
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int64_t t = tok0 + 32 * tt + 8 * (v >> 2) + 4 * h + (v & 3);
+                if (r < M && t < N) {
+                    float* const o = y + t * M + r;
+                    if (split_k)
+                        unsafeAtomicAdd(o, acc[rt][tt][v]);
+                    else
+                        *o = acc[rt][tt][v];
+                }
+            }
+    }
+}
+
 // y[0 .. n) = 0 (y 16-byte aligned): float4 stores, then the n % 4 tail
 __global__ void zero_kernel(float* __restrict__ y, int64_t n) {
     const int64_t n4 = n / 4;
@@ -646,18 +1030,16 @@ int cu_count_pf() {
     return v;
 }
 
-template <int FMT, int WM, int TT>
-hipError_t launch_tile(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
-                       const Planes& p, hipStream_t stream) {
-    using TL = GemmTile<WM, TT>;
+// Work split of a launch over `tiles` (row tile, token tile) pairs: K splits
+// on super-block boundaries, the fewest that keep the compute units (one
+// workgroup each) at least 85 % busy over the launch's rounds, else the best
+// of them; every split keeps at least four super-blocks.
+GemmSplit plan_split(int64_t nrt, int64_t ntt, int64_t K) {
     GemmSplit sp;
-    sp.nrt = (M + TL::BM - 1) / TL::BM;
-    sp.ntt = (n_tok + TL::BN - 1) / TL::BN;
+    sp.nrt = nrt;
+    sp.ntt = ntt;
     const int nsb = (int)(K / 256);
-    // K splits: the fewest that keep the compute units (one workgroup each)
-    // at least 85 % busy over the launch's rounds, else the best of them;
-    // every split keeps at least four super-blocks
-    const int64_t tiles = sp.nrt * sp.ntt;
+    const int64_t tiles = nrt * ntt;
     const int64_t cus = cu_count_pf();
     const int kmax = nsb / 4 > 1 ? nsb / 4 : 1;
     int best = 1;
@@ -673,27 +1055,52 @@ hipError_t launch_tile(const uint8_t* W, const float* x, float* y, int64_t M, in
     }
     sp.sbp = (nsb + best - 1) / best;
     sp.ks = (nsb + sp.sbp - 1) / sp.sbp;
-    const int64_t grid = tiles * sp.ks;
+    return sp;
+}
+
+// y = 0 ahead of a K-split launch (its partial results are added atomically)
+void zero_fill(float* y, int64_t n, hipStream_t stream) {
+    const int64_t zb = (n / 4 + 255) / 256 < 16384 ? (n / 4 + 255) / 256 + 1 : 16384;
+    hipLaunchKernelGGL(zero_kernel, dim3((unsigned)zb), dim3(256), 0, stream, y, n);
+}
+
+template <int FMT, int WM, int TT>
+hipError_t launch_tile(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
+                       const Planes& p, hipStream_t stream) {
+    using TL = GemmTile<WM, TT>;
+    const GemmSplit sp = plan_split((M + TL::BM - 1) / TL::BM, (n_tok + TL::BN - 1) / TL::BN, K);
+    const int64_t grid = sp.nrt * sp.ntt * sp.ks;
     if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
     if (query_only(kernel_name<Name_gemm_kernel, FMT, WM, TT>())) return hipSuccess;
-    if (sp.ks > 1) {
-        const int64_t n = n_tok * M;
-        const int64_t zb = (n / 4 + 255) / 256 < 16384 ? (n / 4 + 255) / 256 + 1 : 16384;
-        hipLaunchKernelGGL(zero_kernel, dim3((unsigned)zb), dim3(256), 0, stream, y, n);
-    }
+    if (sp.ks > 1) zero_fill(y, n_tok * M, stream);
     hipLaunchKernelGGL((gemm_kernel<FMT, WM, TT>), dim3((unsigned)grid), dim3(TL::NT),
                        TL::bytes(MF<FMT>::kSums), stream, W, x, y, M, K, n_tok, p.off1, p.off2, sp);
+    return hipGetLastError();
+}
+
+template <int FMT, int WM>
+hipError_t launch_tile32(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
+                         const Planes& p, hipStream_t stream) {
+    using TL = Tile32<WM>;
+    const GemmSplit sp = plan_split((M + TL::BM - 1) / TL::BM, (n_tok + TL::BN - 1) / TL::BN, K);
+    const int64_t grid = sp.nrt * sp.ntt * sp.ks;
+    if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
+    if (query_only(kernel_name<Name_gemm32_kernel, FMT, WM>())) return hipSuccess;
+    if (sp.ks > 1) zero_fill(y, n_tok * M, stream);
+    hipLaunchKernelGGL((gemm32_kernel<FMT, WM>), dim3((unsigned)grid), dim3(TL::NT), TL::bytes(), stream, W, x, y,
+                       M, K, n_tok, p.off1, p.off2, sp);
     return hipGetLastError();
 }
 
 template <int FMT>
 hipError_t launch_gemm(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
                        const Planes& p, hipStream_t stream) {
-    // Q8_0: two code words per block and lane in flight, so half the token tiles
+    // Q8_0: 16 x 16 tiles (two code words per block and lane in flight), half
+    // the token tiles; the 4-bit formats: 32 x 32 tiles
     if constexpr (FMT == LW_Q8_0)
         return launch_tile<FMT, 4, 2>(W, x, y, M, K, n_tok, p, stream);
     else
-        return launch_tile<FMT, 8, 4>(W, x, y, M, K, n_tok, p, stream);
+        return launch_tile32<FMT, 8>(W, x, y, M, K, n_tok, p, stream);
 }
 
 }  // namespace

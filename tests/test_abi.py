@@ -207,7 +207,8 @@ def test_kernel_selection_table(lib):
     assert kind(Q4_0, 8192, 2048, 4) == "multitok_pk_kernel"    # 1B gate Q4_0: K below 4096
     assert kind(Q4_K, 8192, 2048, 4) == "fewtok_kernel"
     assert kind(Q4_K, 14336, 4096, 9) == "multitok_kernel"
-    assert kind(Q4_0, 14336, 4096, 512) == "gemm_kernel"
+    assert kind(Q4_0, 14336, 4096, 512) == "gemm32_kernel"
+    assert kind(Q8_0, 14336, 4096, 512) == "gemm_kernel"
     assert kind(F16, 2048, 2048, 1) == "gemv1_kernel"
     assert kind(Q8_0, 2048, 2048, 12) == "skinny_kernel"
     assert kind(F16, 2048, 2048, 20) == "gemv_kernel"
