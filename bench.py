@@ -308,14 +308,15 @@ def stored_traffic(workload, n_tok, kernel):
         return None
 
 
-def ceilings(write, launch_bytes, mode):
+def ceilings(write, launch_bytes, mode, extra_bytes=()):
     """Streaming ceilings from libceiling.so in this process: GB/s of a plain
     128-bit read (write: non-temporal write, the dequantization's store form)
     over a 1 GiB buffer (one launch), and at `launch_bytes` per launch timed as
     the per-shape launches are (192 back to back at rotating offsets of that
     buffer, so no launch finds the previous one's bytes in the 256 MB Infinity
     Cache; one graph in graph mode; behind a device-side sleep; HIP events on
-    the launch stream)."""
+    the launch stream). Also returns {b: GB/s} at each size in `extra_bytes`,
+    timed the same way."""
     import ctypes
     import torch
 
@@ -354,9 +355,18 @@ def ceilings(write, launch_bytes, mode):
         torch.cuda.synchronize()
         return nbytes * n / (e0.elapsed_time(e1) * 1e-3) / 1e9
 
-    lb = max(16, min(int(launch_bytes), total) // 16 * 16)
-    return {"kind": "write" if write else "read", "GB/s_1GiB": round(rate(total, 3, False), 1),
-            "launch_bytes": lb, "GB/s_at_launch_bytes": round(rate(lb, 192, mode == "graph"), 1)}
+    def clamp(b):
+        return max(16, min(int(b), total) // 16 * 16)
+
+    lb = clamp(launch_bytes)
+    out = {"kind": "write" if write else "read", "GB/s_1GiB": round(rate(total, 3, False), 1),
+           "launch_bytes": lb, "GB/s_at_launch_bytes": round(rate(lb, 192, mode == "graph"), 1)}
+    at = {}
+    for b in extra_bytes:
+        cb = clamp(b)
+        if cb not in at:
+            at[cb] = out["GB/s_at_launch_bytes"] if cb == lb else rate(cb, 192, mode == "graph")
+    return out, {b: at[clamp(b)] for b in extra_bytes}
 
 
 def kernel_groups(ws, per_shape):
@@ -517,10 +527,24 @@ def main():
     # the value against a plain streaming kernel's rate in the same process
     # (read, or write for the dequantization), and the dominant kernel against
     # that kernel at the dominant kernel's bytes per launch
-    ceil = ceilings(args.op == "dequant", roof["alg_bytes_per_launch"], args.mode)
+    # Per call shape (memory-bound paths): the streaming kernel at the call's
+    # bytes per launch; and the step as a whole if every call ran at that
+    # rate (the launch sequence's own ceiling, launch gaps and ramp included).
+    shape_b = {k: ws.call_bytes[idx[0] % ng] for k, (_, idx) in per_shape.items()}
+    ceil, at = ceilings(args.op == "dequant", roof["alg_bytes_per_launch"], args.mode,
+                        () if mfma else tuple(shape_b.values()))
     ceil["value_over_1GiB_ceiling"] = round(gbs / ceil["GB/s_1GiB"], 4)
     if roof["bound"] == "hbm":
         ceil["dominant_kernel_over_launch_ceiling"] = round(roof["achieved"] / ceil["GB/s_at_launch_bytes"], 4)
+    if at:
+        step_s = 0.0
+        for k, (_, idx) in per_shape.items():
+            c = at[shape_b[k]]
+            shape_out[k]["ceiling_GB/s"] = round(c, 1)
+            shape_out[k]["over_ceiling"] = round(shape_out[k]["GB/s"] / c, 4)
+            step_s += sum(1 for i in idx if i < ng) * shape_b[k] / (c * 1e9)
+        ceil["step_GB/s_at_shape_ceilings"] = round(step_bytes / step_s / 1e9, 1)
+        ceil["value_over_step_ceiling"] = round(gbs * 1e9 * step_s / step_bytes, 4)
     out["stream_ceiling"] = ceil
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(ws, args.cpu_seconds)
