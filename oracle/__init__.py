@@ -27,7 +27,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "lw_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
-F16, Q8_0, Q4_0, Q4_K, Q4_1 = 0, 1, 2, 3, 4
+F16, Q8_0, Q4_0, Q4_K, Q4_1, Q1_0 = 0, 1, 2, 3, 4, 5
 
 _lib = None
 

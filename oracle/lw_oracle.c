@@ -29,6 +29,10 @@
  *     K-quant style used here also carries a per-sub-block min quantized
  *     against a super-block dmin (Eq. (1)'s offset mu = -dmin * m):
  *     value = d * sc_j * q - dmin * m_j.
+ *   - Sec. 2.2, q1_0: symmetric quantization with one scale per block of 128
+ *     weights and one bit per weight; with Eq. (1)'s offset zero the bit b
+ *     selects one of the two symmetric levels, q = 2b - 1, so value = +-d
+ *     with the binary16 scale d of the block.
  *   - Sec. 2.1: decode is a matrix-vector product.
  *
  * Byte layout (the library's split-plane layout): plane 0 at offset 0; each
@@ -38,7 +42,9 @@
  * 12-byte record per super-block, read as a 96-bit little-endian integer R:
  * sc_j = bits [6j, 6j+6), m_j = bits [48+6j, 48+6j+6). Q4_K plane 2 holds
  * {binary16 d, binary16 dmin} per super-block. Q4_1 plane 0 is as Q4_0's;
- * plane 1 holds {binary16 d, binary16 m} per group of 32.
+ * plane 1 holds {binary16 d, binary16 m} per group of 32. Q1_0 plane 0 holds
+ * one bit per element, element e at bit (e mod 8) of byte e/8; plane 1 holds
+ * one binary16 d per block of 128.
  *
  * Build: gcc -O2 -ffp-contract=off -fPIC -shared -pthread (no fast-math, no
  * vector intrinsics). Results do not depend on the thread count: each output
@@ -51,7 +57,17 @@
 #include <string.h>
 #include <unistd.h>
 
-enum { OR_F16 = 0, OR_Q8_0 = 1, OR_Q4_0 = 2, OR_Q4_K = 3, OR_Q4_1 = 4 };
+enum { OR_F16 = 0, OR_Q8_0 = 1, OR_Q4_0 = 2, OR_Q4_K = 3, OR_Q4_1 = 4, OR_Q1_0 = 5 };
+
+/* Elements per block: a row of K elements starts a block when K is a multiple. */
+static int64_t block_elems(int fmt) {
+    switch (fmt) {
+    case OR_F16: return 1;
+    case OR_Q4_K: return 256;
+    case OR_Q1_0: return 128;
+    default: return 32;
+    }
+}
 
 /* ---- plane arithmetic ---------------------------------------------------- */
 
@@ -81,6 +97,11 @@ static int planes(int fmt, int64_t n, int64_t off[3], int64_t* total) {
         if (n % 32) return -1;
         off[1] = round_up_256(n / 2);
         *total = off[1] + 4 * (n / 32);         /* n/32 {binary16 d, binary16 m} */
+        return 0;
+    case OR_Q1_0:
+        if (n % 128) return -1;
+        off[1] = round_up_256(n / 8);           /* one bit per element */
+        *total = off[1] + 2 * (n / 128);        /* n/128 binary16 scales */
         return 0;
     case OR_Q4_K:
         if (n % 256) return -1;
@@ -164,6 +185,12 @@ static double exact_value(int fmt, const uint8_t* W, const int64_t off[3], int64
          * 2^-24 below 2^20 in magnitude, so their double sum is exact */
         return (double)q * d + m;
     }
+    case OR_Q1_0: {
+        /* symmetric, two levels: code bit b stands for q = 2b - 1 */
+        int b = (W[e / 8] >> (e % 8)) & 1;
+        double d = half_value(read_u16(W + off[1] + 2 * (e / 128)));
+        return (double)(2 * b - 1) * d; /* +-d: exact */
+    }
     case OR_Q4_K: {
         int64_t S = e / 256;
         int j = (int)((e / 32) % 8);
@@ -244,7 +271,7 @@ int oracle_matvec(int fmt, const uint8_t* W, const float* x, int64_t M, int64_t 
                   int64_t n_tok, double* y, double* A, int n_threads) {
     int64_t off[3], total;
     if (M < 1 || K < 1 || n_tok < 1 || !W || !x || !y) return -1;
-    if (planes(fmt, M * K, off, &total) || (fmt != OR_F16 && K % 32)) return -1;
+    if (planes(fmt, M * K, off, &total) || K % block_elems(fmt)) return -1;
     int T = n_threads_or_default(n_threads);
     if (T > M) T = (int)M;
     pthread_t* th = (pthread_t*)calloc((size_t)T, sizeof(pthread_t));
@@ -281,7 +308,7 @@ int oracle_matvec_sampled(int fmt, const uint8_t* W, const float* x, int64_t M, 
                           const int64_t* toks, double* y, double* A) {
     int64_t off[3], total;
     if (M < 1 || K < 1 || n_tok < 1 || !W || !x || !y || n_samples < 0) return -1;
-    if (planes(fmt, M * K, off, &total) || (fmt != OR_F16 && K % 32)) return -1;
+    if (planes(fmt, M * K, off, &total) || K % block_elems(fmt)) return -1;
     for (int64_t s = 0; s < n_samples; ++s) {
         int64_t r = rows[s], t = toks[s];
         if (r < 0 || r >= M || t < 0 || t >= n_tok) return -1;

@@ -17,16 +17,19 @@ the previous one rounded up to 256 bytes):
         little-endian integer with sc_j at bits [6j, 6j+6) and m_j at bits
         [48+6j, 48+6j+6);  plane 2: n/256 x {binary16 d, binary16 dmin}
 * q4_1  plane 0: as q4_0;  plane 1: n/32 x {binary16 d, binary16 m}
+* q1_0  plane 0: n/8 bytes, element e at bit (e mod 8) of byte e/8;
+        plane 1: n/128 x binary16 d
 """
 from __future__ import annotations
 
 import numpy as np
 
-F16, Q8_0, Q4_0, Q4_K, Q4_1 = 0, 1, 2, 3, 4
-FORMATS = {"f16": F16, "q8_0": Q8_0, "q4_0": Q4_0, "q4_k": Q4_K, "q4_1": Q4_1}
+F16, Q8_0, Q4_0, Q4_K, Q4_1, Q1_0 = 0, 1, 2, 3, 4, 5
+FORMATS = {"f16": F16, "q8_0": Q8_0, "q4_0": Q4_0, "q4_k": Q4_K, "q4_1": Q4_1, "q1_0": Q1_0}
 FORMAT_NAMES = {v: k for k, v in FORMATS.items()}
 # Packed bytes per weight (codes and scales, ignoring plane padding).
-BYTES_PER_WEIGHT = {F16: 2.0, Q8_0: 34.0 / 32.0, Q4_0: 18.0 / 32.0, Q4_K: 144.0 / 256.0, Q4_1: 20.0 / 32.0}
+BYTES_PER_WEIGHT = {F16: 2.0, Q8_0: 34.0 / 32.0, Q4_0: 18.0 / 32.0, Q4_K: 144.0 / 256.0, Q4_1: 20.0 / 32.0,
+                    Q1_0: 18.0 / 128.0}
 
 ALIGN = 256
 
@@ -51,6 +54,11 @@ def plane_offsets(fmt: int, n: int):
             raise ValueError("n must be a multiple of 32")
         o1 = _up(n // 2)
         return (0, o1, 0), o1 + 4 * (n // 32)
+    if fmt == Q1_0:
+        if n % 128:
+            raise ValueError("n must be a multiple of 128")
+        o1 = _up(n // 8)
+        return (0, o1, 0), o1 + 2 * (n // 128)
     if fmt == Q4_K:
         if n % 256:
             raise ValueError("n must be a multiple of 256")
@@ -153,3 +161,19 @@ def pack_q4_1(q, d, m) -> np.ndarray:
     dm[:, 0] = d
     dm[:, 1] = m
     return assemble(Q4_1, q.size, pack_nibbles(q), dm)
+
+
+def pack_bits(b) -> np.ndarray:
+    """1-bit codes (n,) in {0, 1} -> n/8 bytes, element e at bit (e mod 8) of byte e/8."""
+    b = np.asarray(b, dtype=np.uint8).reshape(-1)
+    if b.size and int(b.max()) > 1:
+        raise ValueError("1-bit codes must lie in {0, 1}")
+    return np.packbits(b, bitorder="little")
+
+
+def pack_q1_0(b, d) -> np.ndarray:
+    b = np.asarray(b).reshape(-1)
+    d = _half_bits(d).astype("<u2")
+    if d.size * 128 != b.size:
+        raise ValueError("need one scale per 128 codes")
+    return assemble(Q1_0, b.size, pack_bits(b), d)

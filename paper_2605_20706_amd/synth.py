@@ -18,6 +18,8 @@ Q8_0 matrix uses the literal seed 0):
 * q4_1  codes as q4_0; d uniform in [1e-3, 2e-2] and m uniform in [-0.2, 0]
         -> binary16 (a block's values span [m, m + 15 d], as for weights
         quantized against their block minimum);
+* q1_0  bits uniform in {0, 1} (uniform random bytes); d uniform in
+        [1e-3, 2e-2] -> binary16 (one per 128 weights);
 * x     float32 N(0, 1), shape [n_tok, K], from the generator of the workload
         (matrix_id 99).
 """
@@ -28,7 +30,7 @@ from dataclasses import dataclass
 import numpy as np
 
 from . import layout
-from .layout import F16, Q4_0, Q4_1, Q4_K, Q8_0
+from .layout import F16, Q1_0, Q4_0, Q4_1, Q4_K, Q8_0
 
 
 @dataclass(frozen=True)
@@ -68,6 +70,11 @@ _L1B = dict(n_layers=16, hidden=2048, qkv=3072, ffn=8192)
 # Llama-3-8B: hidden 4096, kv width 1024 -> QKV 6144, FFN 14336, 32 layers.
 _L8B = dict(n_layers=32, hidden=4096, qkv=6144, ffn=14336)
 _VOCAB = 128256
+# A 1.7B-parameter decoder for the 1-bit format: hidden 2048, 16 q-heads / 8
+# kv-heads of 128 -> QKV 4096, FFN 6144, 28 layers, vocabulary 151936
+# (1.72e9 weights; at 1.125 bits per weight 0.24 GB).
+_L1B7 = dict(n_layers=28, hidden=2048, qkv=4096, ffn=6144)
+_VOCAB_1B7 = 151936
 
 WORKLOADS = {
     "q8_0_2048": Workload("q8_0_2048", 1, Q8_0, (Matrix("w", 2048, 2048, 0, 0),),
@@ -95,6 +102,10 @@ WORKLOADS = {
                                  n_toks=(1, 2, 4, 8, 512),
                                  description="Q4_1 (blocks with a min) on Llama-3-8B gate/up/down, "
                                              "n_tok in {1,2,4,8} and prefill 512"),
+    "q1_0_1b7": Workload("q1_0_1b7", 7, Q1_0,
+                         tuple(_llama_layers(**_L1B7)) + (Matrix("lm_head", _VOCAB_1B7, 2048, 28, 5),),
+                         description="q1_0 (1 bit, one scale per 128) decode-step weight set of a "
+                                     "1.7B-parameter decoder (28 layers) + lm_head, 1 token"),
 }
 
 
@@ -129,6 +140,9 @@ def gen_fields(fmt: int, n: int, rng: np.random.Generator) -> dict:
         return {"q": rng.integers(0, 16, n, dtype=np.uint8),
                 "d": _uniform_half(rng, 1e-3, 2e-2, n // 32),
                 "m": _uniform_half(rng, -0.2, 0.0, n // 32)}
+    if fmt == Q1_0:
+        return {"b": rng.integers(0, 2, n, dtype=np.uint8),
+                "d": _uniform_half(rng, 1e-3, 2e-2, n // 128)}
     if fmt == Q4_K:
         return {"q": rng.integers(0, 16, n, dtype=np.uint8),
                 "sc": rng.integers(0, 64, n // 32, dtype=np.uint8),
@@ -147,6 +161,8 @@ def pack_fields(fmt: int, f: dict) -> np.ndarray:
         return layout.pack_q4_0(f["q"], f["d"])
     if fmt == Q4_1:
         return layout.pack_q4_1(f["q"], f["d"], f["m"])
+    if fmt == Q1_0:
+        return layout.pack_q1_0(f["b"], f["d"])
     return layout.pack_q4_k(f["q"], f["sc"], f["m"], f["d"], f["dmin"])
 
 
@@ -157,6 +173,10 @@ def gen_packed(fmt: int, n: int, rng: np.random.Generator) -> np.ndarray:
         return pack_fields(fmt, gen_fields(fmt, n, rng))
     offs, total = layout.plane_offsets(fmt, n)
     out = np.zeros(total, dtype=np.uint8)
+    if fmt == Q1_0:
+        out[0:n // 8] = _random_bytes(rng, n // 8)
+        out[offs[1]:offs[1] + 2 * (n // 128)] = _uniform_half(rng, 1e-3, 2e-2, n // 128).view(np.uint8)
+        return out
     out[0:n // 2] = _random_bytes(rng, n // 2)
     if fmt == Q4_0:
         out[offs[1]:offs[1] + 2 * (n // 32)] = _uniform_half(rng, 1e-3, 2e-2, n // 32).view(np.uint8)

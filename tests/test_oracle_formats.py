@@ -12,9 +12,9 @@ import pytest
 
 import golden_io
 from paper_2605_20706_amd import layout
-from paper_2605_20706_amd.layout import F16, Q4_0, Q4_1, Q4_K, Q8_0
+from paper_2605_20706_amd.layout import F16, Q1_0, Q4_0, Q4_1, Q4_K, Q8_0
 
-FMT = {"f16": F16, "q8_0": Q8_0, "q4_0": Q4_0, "q4_k": Q4_K, "q4_1": Q4_1}
+FMT = {"f16": F16, "q8_0": Q8_0, "q4_0": Q4_0, "q4_k": Q4_K, "q4_1": Q4_1, "q1_0": Q1_0}
 
 
 def bits(a):
@@ -104,6 +104,45 @@ def test_q4_1_nibble_order_and_pair_plane(oracle_mod):
     assert (got[128:256] == 5.0).all()
 
 
+def test_q1_0_every_scale(oracle_mod):
+    """Both codes x every finite binary16 scale (one scale per block of 128):
+    the bit b stands for 2b - 1, so the element is +d or -d, compared with
+    numpy's binary16 -> float32 conversion (negated for b = 0)."""
+    d = finite_halves()
+    rng = np.random.default_rng(31)
+    b = rng.integers(0, 2, 128 * d.size).astype(np.uint8)
+    b[0::128], b[1::128] = 0, 1  # both codes in every block
+    got = oracle_mod.dequant(Q1_0, layout.pack_q1_0(b, d), b.size)
+    dv = np.repeat(d.view(np.float16).astype(np.float32), 128)
+    ref = np.where(b == 1, dv, -dv)
+    assert (bits(got) == bits(ref)).all()  # signed zeros included: (-1) * (+0) = -0
+
+
+def test_q1_0_bit_order_hand_bytes(oracle_mod):
+    """Element e is bit (e mod 8) of byte e/8 (least significant first), and
+    the scale changes every 128 elements."""
+    plane0 = np.zeros(32, np.uint8)
+    plane0[0], plane0[1], plane0[16] = 0x01, 0x80, 0xFF
+    d = np.array([0x3C00, 0x4000], np.uint16)  # 1.0, 2.0
+    got = oracle_mod.dequant(Q1_0, layout.assemble(Q1_0, 256, plane0, d), 256)
+    want = -np.ones(256, np.float32)
+    want[[0, 15]] = 1.0
+    want[128:] = -2.0
+    want[128:136] = 2.0
+    assert np.array_equal(got, want)
+
+
+def test_q1_0_sign_quantizer_roundtrip(oracle_mod):
+    """Eq. (1) with two symmetric levels: quantizing by sign with d = the
+    block's mean |x| (as binary16) decodes to sign(x) * d exactly."""
+    rng = np.random.default_rng(32)
+    x = rng.standard_normal(128 * 64) * 0.02
+    d16 = np.abs(x).reshape(-1, 128).mean(axis=1).astype(np.float16)
+    b = (x >= 0).astype(np.uint8)
+    got = oracle_mod.dequant(Q1_0, layout.pack_q1_0(b, d16), x.size)
+    assert np.array_equal(got, np.sign(x) * np.repeat(d16.astype(np.float32), 128))
+
+
 # --------------------------------------------------------------------------- hand values
 
 def _block_for(name, f):
@@ -117,6 +156,10 @@ def _block_for(name, f):
         q = np.zeros(256, np.uint8)
         q[0] = f["q"]
         return layout.pack_q4_0(q, np.repeat(h(f["d"]), 8)), 0
+    if name == "q1_0":
+        b = np.zeros(256, np.uint8)
+        b[0] = f["b"]
+        return layout.pack_q1_0(b, np.repeat(h(f["d"]), 2)), 0
     if name == "q4_1":
         q = np.zeros(256, np.uint8)
         q[0] = f["q"]

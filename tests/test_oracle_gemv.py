@@ -11,9 +11,9 @@ import numpy as np
 import pytest
 
 from paper_2605_20706_amd import layout, synth
-from paper_2605_20706_amd.layout import F16, Q4_0, Q4_1, Q4_K, Q8_0
+from paper_2605_20706_amd.layout import F16, Q1_0, Q4_0, Q4_1, Q4_K, Q8_0
 
-ALL = [F16, Q8_0, Q4_0, Q4_K, Q4_1]
+ALL = [F16, Q8_0, Q4_0, Q4_K, Q4_1, Q1_0]
 
 
 def make(fmt, M, K, seed):
@@ -74,7 +74,7 @@ def test_linearity_and_token_independence(oracle_mod, fmt):
     assert np.allclose(yc[0], 2 * ya[0] + yb[0], rtol=0, atol=1e-6 * (2 * Aa[0] + Ab[0]).max())
 
 
-@pytest.mark.parametrize("fmt", [Q8_0, Q4_0, Q4_K, Q4_1])
+@pytest.mark.parametrize("fmt", [Q8_0, Q4_0, Q4_K, Q4_1, Q1_0])
 def test_power_of_two_scale(oracle_mod, fmt):
     """Doubling every binary16 scale and min (exponent + 1, no overflow)
     doubles y exactly."""
