@@ -52,12 +52,17 @@
  *   LW_Q4_1 plane 0: as LW_Q4_0 plane 0.
  *           plane 1: n/32 x { binary16 d, binary16 m } (4 bytes each).
  *                                    value = q[e] * d[g] + m[g]
+ *   LW_Q1_0 plane 0: n/8 bytes; element e is bit (e mod 8) of byte e/8
+ *                    (code b in {0, 1}, standing for the level 2b - 1).
+ *           plane 1: n/128 x binary16 d (block B = e / 128).
+ *                                    value = (2b[e] - 1) * d[B] = +-d[B]
  *
  * The dequantized value of an element is the exact real value of its closed
  * form rounded once to binary32 with round-to-nearest-even. For LW_F16,
  * LW_Q8_0 and LW_Q4_0 the closed form is exactly representable in binary32;
  * for LW_Q4_K the two products are exact and the difference is rounded once;
- * for LW_Q4_1 the product is exact and the sum with the min is rounded once.
+ * for LW_Q4_1 the product is exact and the sum with the min is rounded once;
+ * LW_Q1_0's value is +-d, exact.
  * ------------------------------------------------------------------------
  */
 #ifndef LW_H
@@ -80,8 +85,9 @@ extern "C" {
 
 /* Weight formats (Sec. 2.2: f16 storage, legacy blocks of 32 without (Q8_0,
  * Q4_0) and with (Q4_1) an offset, K-quant super-blocks of 256 with
- * double-quantized scales and mins). */
-typedef enum { LW_F16 = 0, LW_Q8_0 = 1, LW_Q4_0 = 2, LW_Q4_K = 3, LW_Q4_1 = 4 } lw_fmt;
+ * double-quantized scales and mins, and the 1-bit symmetric q1_0 with one
+ * scale per 128 weights). */
+typedef enum { LW_F16 = 0, LW_Q8_0 = 1, LW_Q4_0 = 2, LW_Q4_K = 3, LW_Q4_1 = 4, LW_Q1_0 = 5 } lw_fmt;
 
 /* Return codes. */
 enum {

@@ -42,6 +42,14 @@ __device__ __forceinline__ float4 value4(const uint8_t* __restrict__ W, int64_t 
         v.y = sbyte<1>(q) * d;
         v.z = sbyte<2>(q) * d;
         v.w = sbyte<3>(q) * d;
+    } else if constexpr (FMT == LW_Q1_0) {
+        // bit (e mod 8) of byte e/8; the 4 bits of e..e+3 share one byte
+        const uint32_t b = (uint32_t)W[e >> 3] >> (e & 4);
+        const float d = half_bits_to_float(*reinterpret_cast<const uint16_t*>(W + off1 + 2 * (e >> 7)));
+        v.x = (b & 1u) ? d : -d;
+        v.y = (b & 2u) ? d : -d;
+        v.z = (b & 4u) ? d : -d;
+        v.w = (b & 8u) ? d : -d;
     } else {
         // Q4 code plane: group g = e/32 owns bytes [16g, 16g+16); byte i
         // holds element 32g+i (low nibble) and 32g+i+16 (high nibble).
@@ -130,6 +138,7 @@ hipError_t launch_dequant(int fmt, const uint8_t* W, float* out, int64_t n, cons
     case LW_Q4_0: return launch<LW_Q4_0>(W, out, n, p, stream);
     case LW_Q4_K: return launch<LW_Q4_K>(W, out, n, p, stream);
     case LW_Q4_1: return launch<LW_Q4_1>(W, out, n, p, stream);
+    case LW_Q1_0: return launch<LW_Q1_0>(W, out, n, p, stream);
     default: return hipErrorInvalidValue;
     }
 }

@@ -243,6 +243,61 @@ struct Traits<LW_Q4_1> {
     }
 };
 
+// Sum over the lane's 32 elements of b * x for 1-bit codes b. A bit masked
+// into bit 0 of a 16-bit half is the binary16 subnormal b * 2^-24 (exact), so
+// as for the 4-bit codes each product is one v_fma_mix_f32 with no
+// conversion; bit i and bit 16 + i (elements i and 16 + i) come out of the
+// word with one shift and one mask.
+__device__ __forceinline__ float bit_dot(uint32_t w, const float4* xv) {
+    float lo_s = 0.f, hi_s = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+        const uint32_t m = opaque((w >> i) & 0x00010001u);
+        const float4& xl = xv[i >> 2];
+        const float4& xh = xv[4 + (i >> 2)];
+        const int c = i & 3;
+        lo_s = __builtin_fmaf(half_of<0>(m), c == 0 ? xl.x : c == 1 ? xl.y : c == 2 ? xl.z : xl.w, lo_s);
+        hi_s = __builtin_fmaf(half_of<1>(m), c == 0 ? xh.x : c == 1 ? xh.y : c == 2 ? xh.z : xh.w, hi_s);
+    }
+    return (lo_s + hi_s) * 16777216.0f;  // 2^24
+}
+
+// q1_0 (Sec. 2.2: one bit per weight, one binary16 scale per 128): a lane
+// holds 32 consecutive bits (one 32-bit word; a wave-wide load is 256
+// contiguous bytes) and its block's scale, shared by four lanes.
+template <>
+struct Traits<LW_Q1_0> {
+    static constexpr int EPL = 32;
+    static constexpr bool kGroupSums = true;
+    struct Packet {
+        uint32_t b;
+        uint32_t d;
+    };
+    __device__ static Packet load(const uint8_t* W, int64_t e, int64_t off1, int64_t) {
+        Packet p;
+        p.b = *reinterpret_cast<const uint32_t*>(W + (e >> 3));
+        p.d = *reinterpret_cast<const uint16_t*>(W + off1 + 2 * (e >> 7));
+        return p;
+    }
+    struct Base {
+        uint32_t c, d;
+    };
+    __device__ static Base base(uint32_t row, uint32_t K, uint32_t c) {  // chunk = 2048 elements
+        return {row * (K / 8u) + 256u * c, row * (K / 64u) + 32u * c};
+    }
+    __device__ static Packet load_at(const uint8_t* W, const uint8_t* P1, const uint8_t*, const Base& b,
+                                     uint32_t la) {
+        Packet p;
+        p.b = *reinterpret_cast<const uint32_t*>(W + b.c + 4u * la);
+        p.d = *reinterpret_cast<const uint16_t*>(P1 + b.d + 2u * (la >> 2));
+        return p;
+    }
+    // sum (2b - 1) * d * x = d * (2 * sum b*x - sum x)
+    __device__ static float dot(const Packet& p, const float4* xv, float sx, int) {
+        return half_bits_to_float(p.d) * __builtin_fmaf(2.0f, bit_dot(p.b, xv), -sx);
+    }
+};
+
 template <>
 struct Traits<LW_Q4_K> {
     static constexpr int EPL = 32;
@@ -480,6 +535,9 @@ __global__ void __launch_bounds__(NW * kWave)
     constexpr int E = kWave * EPL;
     extern __shared__ float4 smem[];
 
+    // token block blockIdx.y: tokens [NT * blockIdx.y, NT * blockIdx.y + NT)
+    x += (int64_t)blockIdx.y * NT * K;
+    y += (int64_t)blockIdx.y * NT * M;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     const int64_t row_base = ((int64_t)blockIdx.x * NW + wave) * R;
@@ -895,9 +953,11 @@ struct Config {
     int R, NW;
 };
 
+// ntb token blocks of NT tokens each (x and y advance by NT rows per block),
+// one launch: grid.y is the token block.
 template <int FMT, int NT>
 hipError_t launch_nt(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
-                     const Planes& p, hipStream_t stream) {
+                     const Planes& p, hipStream_t stream, int64_t ntb = 1) {
     constexpr int E = kWave * Traits<FMT>::EPL;
     constexpr int R = NT == 1 ? 4 : (NT <= 4 ? 2 : 1);
     constexpr int NW = 4;
@@ -912,7 +972,7 @@ hipError_t launch_nt(const uint8_t* W, const float* x, float* y, int64_t M, int6
     const size_t lds = (size_t)(nch * chunk_bytes);
     const int64_t blocks = (M + (int64_t)NW * R - 1) / ((int64_t)NW * R);
     if (query_only(kernel_name<Name_gemv_kernel, FMT, NT, R, NW>())) return hipSuccess;
-    hipLaunchKernelGGL((gemv_kernel<FMT, NT, R, NW>), dim3((unsigned)blocks), dim3(NW * kWave), lds,
+    hipLaunchKernelGGL((gemv_kernel<FMT, NT, R, NW>), dim3((unsigned)blocks, (unsigned)ntb), dim3(NW * kWave), lds,
                        stream, W, x, y, M, K, (int)KT, p.off1, p.off2);
     return hipGetLastError();
 }
@@ -971,7 +1031,8 @@ hipError_t launch_single_segs(const RowSegs<NS>& sg, const float* x, int64_t M, 
 }
 
 // Rows per wave step (R) and ring depth (D) of the LDS single-token kernel,
-// from MI355X sweeps: one row and two steps for the 4-bit formats and Q8_0;
+// from MI355X sweeps: one row and two steps for the 4-bit formats and Q8_0
+// (eight steps for q1_0, whose steps are a quarter of the bytes);
 // f16 keeps four steps in flight (two rows each for 3072..8191 rows at
 // K <= 2048, e.g. the 1B q/k/v projection).
 template <int FMT, int NS>
@@ -980,6 +1041,11 @@ hipError_t launch_single_table(const RowSegs<NS>& sg, const float* x, int64_t M,
     if constexpr (FMT == LW_F16) {
         if (K <= 2048 && M >= 3072 && M < 8192) return launch_single_segs<FMT, 2, 4, NS>(sg, x, M, K, max_total, stream);
         return launch_single_segs<FMT, 1, 4, NS>(sg, x, M, K, max_total, stream);
+    } else if constexpr (FMT == LW_Q1_0) {
+        // a step is 256 bytes of bits per wave: keep eight of them in flight
+        // (four rows per step, sharing each x read, leave too few waves with
+        // work on 2048-row matrices and measured slower)
+        return launch_single_segs<FMT, 1, 8, NS>(sg, x, M, K, max_total, stream);
     } else {
         return launch_single_segs<FMT, 1, 2, NS>(sg, x, M, K, max_total, stream);
     }
@@ -1117,6 +1183,7 @@ hipError_t launch_gemv_multi(int fmt, int n, const uint8_t* const* W, float* con
     case LW_Q4_0: return launch_multi_fmt<LW_Q4_0>(n, W, y, M, x, K, stream);
     case LW_Q4_K: return launch_multi_fmt<LW_Q4_K>(n, W, y, M, x, K, stream);
     case LW_Q4_1: return launch_multi_fmt<LW_Q4_1>(n, W, y, M, x, K, stream);
+    case LW_Q1_0: return launch_multi_fmt<LW_Q1_0>(n, W, y, M, x, K, stream);
     default: return hipErrorInvalidValue;
     }
 }
@@ -1131,6 +1198,38 @@ hipError_t launch_gemv_reg(int fmt, const uint8_t* W, const float* x, float* y, 
     }
 }
 
+// Any token count on the matrix-vector kernels: whole blocks of NT tokens
+// (8, or 4 where 8 tokens of a chunk exceed the LDS budget) in one launch per
+// 65535 blocks, the remaining tokens in one more.
+template <int FMT>
+hipError_t launch_blocks_fmt(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
+                             const Planes& p, hipStream_t stream) {
+    constexpr int NT = fits_one_chunk<FMT, 8>() ? 8 : 4;
+    constexpr int64_t kMaxGridY = 65535;
+    const int64_t nb = n_tok / NT;
+    for (int64_t b0 = 0; b0 < nb; b0 += kMaxGridY) {
+        const int64_t cnt = (nb - b0) < kMaxGridY ? (nb - b0) : kMaxGridY;
+        const hipError_t err = launch_nt<FMT, NT>(W, x + b0 * NT * K, y + b0 * NT * M, M, K, p, stream, cnt);
+        if (err != hipSuccess) return err;
+    }
+    const int64_t rem = n_tok - nb * NT;
+    if (rem == 0) return hipSuccess;
+    return launch_fmt<FMT>(W, x + nb * NT * K, y + nb * NT * M, M, K, rem, p, stream);
+}
+
+hipError_t launch_gemv_blocks(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
+                              int64_t n_tok, const Planes& p, hipStream_t stream) {
+    switch (fmt) {
+    case LW_F16: return launch_blocks_fmt<LW_F16>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q8_0: return launch_blocks_fmt<LW_Q8_0>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q4_0: return launch_blocks_fmt<LW_Q4_0>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q4_K: return launch_blocks_fmt<LW_Q4_K>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q4_1: return launch_blocks_fmt<LW_Q4_1>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q1_0: return launch_blocks_fmt<LW_Q1_0>(W, x, y, M, K, n_tok, p, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
 hipError_t launch_gemv(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                        int64_t n_tok, const Planes& p, hipStream_t stream) {
     switch (fmt) {
@@ -1139,6 +1238,7 @@ hipError_t launch_gemv(int fmt, const uint8_t* W, const float* x, float* y, int6
     case LW_Q4_0: return launch_fmt<LW_Q4_0>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q4_K: return launch_fmt<LW_Q4_K>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q4_1: return launch_fmt<LW_Q4_1>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q1_0: return launch_fmt<LW_Q1_0>(W, x, y, M, K, n_tok, p, stream);
     default: return hipErrorInvalidValue;
     }
 }

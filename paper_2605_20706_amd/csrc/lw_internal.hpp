@@ -70,6 +70,10 @@ inline Planes planes_of(int fmt, int64_t n) {
         p.off1 = round_up_256(n / 2);
         p.total = p.off1 + 4 * (n / 32);
         break;
+    case LW_Q1_0:
+        p.off1 = round_up_256(n / 8);
+        p.total = p.off1 + 2 * (n / 128);
+        break;
     case LW_Q4_K:
         p.off1 = round_up_256(n / 2);
         p.off2 = round_up_256(p.off1 + 12 * (n / 256));
@@ -101,6 +105,10 @@ hipError_t launch_dequant(int fmt, const uint8_t* W, float* out, int64_t n, cons
                           hipStream_t stream);
 hipError_t launch_gemv(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                        int64_t n_tok, const Planes& p, hipStream_t stream);
+// Any n_tok >= 1 on the matrix-vector kernels: whole token blocks in one
+// launch (grid.y = block), the remaining tokens in one more.
+hipError_t launch_gemv_blocks(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
+                              int64_t n_tok, const Planes& p, hipStream_t stream);
 // One launch of a single-token kernel over the rows of n matrices that share
 // x (one token, same format and K); hipErrorNotSupported when the shapes are
 // not ones the single-token kernels take as one row space.

@@ -1113,13 +1113,9 @@ hipError_t launch_prefill(int fmt, const uint8_t* W, const float* x, float* y, i
     case LW_Q4_1: return launch_gemm<LW_Q4_1>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q8_0: return launch_gemm<LW_Q8_0>(W, x, y, M, K, n_tok, p, stream);
     default:
-        // f16 weights: token blocks of the matrix-vector kernel (float32 throughout)
-        for (int64_t t0 = 0; t0 < n_tok; t0 += LW_GEMV_MAX_TOK) {
-            const int64_t nt = (n_tok - t0) < LW_GEMV_MAX_TOK ? (n_tok - t0) : LW_GEMV_MAX_TOK;
-            const hipError_t err = launch_gemv(fmt, W, x + t0 * K, y + t0 * M, M, K, nt, p, stream);
-            if (err != hipSuccess) return err;
-        }
-        return hipSuccess;
+        // f16 and q1_0 weights: token blocks of the matrix-vector kernel
+        // (float32 throughout), all whole blocks in one launch
+        return launch_gemv_blocks(fmt, W, x, y, M, K, n_tok, p, stream);
     }
 }
 

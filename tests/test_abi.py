@@ -9,11 +9,11 @@ import pytest
 
 import golden_io
 from paper_2605_20706_amd import binding
-from paper_2605_20706_amd.layout import F16, Q4_0, Q4_1, Q4_K, Q8_0
+from paper_2605_20706_amd.layout import F16, Q1_0, Q4_0, Q4_1, Q4_K, Q8_0
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 LW_OK, LW_EINVAL, LW_EFMT, LW_ESHAPE, LW_EALIGN = 0, -1, -2, -3, -4
-FMT = {"f16": F16, "q8_0": Q8_0, "q4_0": Q4_0, "q4_k": Q4_K, "q4_1": Q4_1}
+FMT = {"f16": F16, "q8_0": Q8_0, "q4_0": Q4_0, "q4_k": Q4_K, "q4_1": Q4_1, "q1_0": Q1_0}
 
 # Fake, never dereferenced addresses: every call below fails validation first.
 A256 = 0x7F0000000000
@@ -74,7 +74,7 @@ def mv(lib, fmt=Q4_0, W=A256, x=A16, y=A16, M=4, K=256, n_tok=1):
 
 
 def test_matvec_error_order(lib):
-    assert mv(lib, fmt=5, W=None) == LW_EFMT          # format first
+    assert mv(lib, fmt=6, W=None) == LW_EFMT          # format first
     assert mv(lib, fmt=-1) == LW_EFMT
     assert mv(lib, W=None) == LW_EINVAL
     assert mv(lib, x=None) == LW_EINVAL
@@ -102,7 +102,7 @@ def mvm(lib, fmt=Q4_0, Ws=(A256, A256 + 4096), ys=(A16, A16 + 4096), Ms=(4, 8), 
 def test_matvec_multi_error_order(lib):
     """lw_matvec_multi checks as lw_matvec does, over all matrices, in the same
     order (no call here reaches a launch)."""
-    assert mvm(lib, fmt=5, x=None) == LW_EFMT
+    assert mvm(lib, fmt=6, x=None) == LW_EFMT
     assert mvm(lib, x=None) == LW_EINVAL
     assert mvm(lib, n=0) == LW_EINVAL
     assert mvm(lib, n=binding.LW_MULTI_MAX + 1) == LW_EINVAL

@@ -40,7 +40,7 @@ def test_q8_0_2048_full(oracle_mod):
 # one matrix of every distinct shape of each workload (layer 0, and the lm_head)
 CASES = [("f16_llama1b", i) for i in range(5)] + [("q4_0_llama1b", i) for i in (0, 1, 2, 4, 80)] + \
         [("q4_k_llama8b", i) for i in (0, 1, 2, 4, 160)] + [("q4_0_llama8b_ffn", i) for i in range(3)] + \
-        [("q4_1_llama8b_ffn", i) for i in range(3)]
+        [("q4_1_llama8b_ffn", i) for i in range(3)] + [("q1_0_1b7", i) for i in (0, 1, 2, 4, 140)]
 
 
 @pytest.mark.parametrize("key,idx", CASES)

@@ -5,7 +5,7 @@ import pytest
 
 from gpu_util import gpu_dequant, same_bits_or_both_zero
 from paper_2605_20706_amd import layout, synth
-from paper_2605_20706_amd.layout import F16, Q4_0, Q4_1, Q4_K, Q8_0
+from paper_2605_20706_amd.layout import F16, Q1_0, Q4_0, Q4_1, Q4_K, Q8_0
 
 pytestmark = pytest.mark.gpu
 
@@ -77,8 +77,21 @@ def test_q4_1_tie_hand_value():
     assert (got.view(np.uint32) == 0x4523EC68).all()
 
 
+def test_q1_0_every_scale_and_signed_zero(oracle_mod):
+    """Both codes x every finite binary16 d (one scale per 128 elements):
+    +d or -d, bit for bit; a zero scale with code 0 gives -0."""
+    d = finite_halves()
+    d = np.concatenate([d, d[: (-d.size) % 2]])  # whole multiples of 256 elements
+    b = np.random.default_rng(97).integers(0, 2, 128 * d.size).astype(np.uint8)
+    b[0::128], b[1::128] = 0, 1
+    W = layout.pack_q1_0(b, d)
+    check(oracle_mod, Q1_0, W, b.size)
+    got = gpu_dequant(Q1_0, layout.pack_q1_0(np.zeros(256, np.uint8), np.zeros(2, np.uint16)), 256)
+    assert (got.view(np.uint32) == 0x80000000).all()
+
+
 @pytest.mark.parametrize("n", [256, 512 + 256, 4096 * 3 + 256])
-@pytest.mark.parametrize("fmt", [F16, Q8_0, Q4_0, Q4_K, Q4_1])
+@pytest.mark.parametrize("fmt", [F16, Q8_0, Q4_0, Q4_K, Q4_1, Q1_0])
 def test_small_and_ragged(oracle_mod, fmt, n):
     check(oracle_mod, fmt, synth.gen_packed(fmt, n, np.random.default_rng(n + fmt)), n)
 

@@ -10,7 +10,7 @@ import pytest
 import gate
 from gpu_util import to_gpu
 from paper_2605_20706_amd import binding, synth
-from paper_2605_20706_amd.layout import F16, Q4_0, Q4_1, Q4_K, Q8_0
+from paper_2605_20706_amd.layout import F16, Q1_0, Q4_0, Q4_1, Q4_K, Q8_0
 
 pytestmark = pytest.mark.gpu
 
@@ -32,7 +32,7 @@ def run_multi(oracle_mod, fmt, Ms, K, n_tok, seed):
         gate.check(y, singles[i].cpu().numpy().astype(np.float64), A, f32_bound=1e-4, what=("vs single", i))
 
 
-@pytest.mark.parametrize("fmt", [F16, Q8_0, Q4_0, Q4_K, Q4_1])
+@pytest.mark.parametrize("fmt", [F16, Q8_0, Q4_0, Q4_K, Q4_1, Q1_0])
 @pytest.mark.parametrize("Ms,K", [((67, 130, 1), 2304), ((17, 5), 256), ((33, 40, 64, 3), 4352)])
 def test_multi_small(oracle_mod, fmt, Ms, K):
     """Ragged row counts (one launch over the LDS single-token kernel), up to
@@ -51,7 +51,7 @@ def test_multi_register_kernel(oracle_mod, fmt, Ms, K):
     run_multi(oracle_mod, fmt, list(Ms), K, 1, 32)
 
 
-@pytest.mark.parametrize("fmt", [F16, Q8_0])
+@pytest.mark.parametrize("fmt", [F16, Q8_0, Q1_0])
 def test_multi_lds_kernel_full_size(oracle_mod, fmt):
     """The LDS single-token kernel over the 1B gate/up pair (8192 + 8192 rows,
     K = 2048), the fused call of the benchmark's f16 decode step."""

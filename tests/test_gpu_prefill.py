@@ -11,7 +11,7 @@ import pytest
 import gate
 from gpu_util import gpu_matvec, to_gpu
 from paper_2605_20706_amd import binding, synth
-from paper_2605_20706_amd.layout import Q4_0, Q4_1, Q4_K, Q8_0
+from paper_2605_20706_amd.layout import F16, Q1_0, Q4_0, Q4_1, Q4_K, Q8_0
 
 pytestmark = pytest.mark.gpu
 
@@ -35,6 +35,16 @@ def run(oracle_mod, fmt, M, K, n_tok, seed):
 ])
 def test_prefill_tiles(oracle_mod, fmt, M, K, n_tok):
     run(oracle_mod, fmt, M, K, n_tok, 50)
+
+
+@pytest.mark.parametrize("fmt", [F16, Q1_0])
+@pytest.mark.parametrize("M,K,n_tok", [(300, 2304, 517), (1, 256, 64)])
+def test_token_blocks_one_launch(oracle_mod, fmt, M, K, n_tok):
+    """f16 and q1_0 run many tokens as blocks of the matrix-vector kernel, all
+    whole blocks in one launch (grid.y = block) and the remaining tokens in
+    one more: 517 tokens are 64 blocks of 8 plus 5 (f16) or 129 blocks of 4
+    plus 1 (q1_0); 64 tokens leave no remainder."""
+    run(oracle_mod, fmt, M, K, n_tok, 70)
 
 
 @pytest.mark.parametrize("fmt", [Q4_0, Q4_K])
