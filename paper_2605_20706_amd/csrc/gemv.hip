@@ -412,6 +412,32 @@ __device__ __forceinline__ void dot24(const Traits<LW_Q4_0>::Packet& p, const fl
     for (int t = 0; t < NTK; ++t) acc[t] = __builtin_fmaf(d, __builtin_fmaf(-8.0f, sx24[t], qx[t]), acc[t]);
 }
 
+// acc[t] += (q1_0 contribution of the lane for token t) * 2^-24:
+// d * (2 * sum b*x_t - sum x_t); the masks of the 16 bit pairs serve every
+// token (a bit masked into bit 0 of a half is b * 2^-24, as in bit_dot).
+template <int NTK>
+__device__ __forceinline__ void dot24(const Traits<LW_Q1_0>::Packet& p, const float4* const* xv,
+                                      const float* sx24, const SubBlock&, float* acc) {
+    float lo_s[NTK], hi_s[NTK];
+#pragma unroll
+    for (int t = 0; t < NTK; ++t) lo_s[t] = hi_s[t] = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+        const uint32_t m = opaque((p.b >> i) & 0x00010001u);
+        const int c = i & 3;
+#pragma unroll
+        for (int t = 0; t < NTK; ++t) {
+            const float4& xl = xv[t][i >> 2];
+            const float4& xh = xv[t][4 + (i >> 2)];
+            lo_s[t] = __builtin_fmaf(half_of<0>(m), c == 0 ? xl.x : c == 1 ? xl.y : c == 2 ? xl.z : xl.w, lo_s[t]);
+            hi_s[t] = __builtin_fmaf(half_of<1>(m), c == 0 ? xh.x : c == 1 ? xh.y : c == 2 ? xh.z : xh.w, hi_s[t]);
+        }
+    }
+    const float d = half_bits_to_float(p.d);
+#pragma unroll
+    for (int t = 0; t < NTK; ++t) acc[t] = __builtin_fmaf(d, __builtin_fmaf(2.0f, lo_s[t] + hi_s[t], -sx24[t]), acc[t]);
+}
+
 // acc[t] += (Q4_1 contribution of the lane for token t) * 2^-24:
 // d * sum q*x_t + m * sum x_t.
 template <int NTK>
@@ -1089,6 +1115,13 @@ hipError_t launch_reg_segs(const RowSegs<NS>& sg, const float* x, int64_t M, int
                            int64_t max_total, hipStream_t stream) {
     if (K % 2048) return hipErrorNotSupported;
     const int64_t nc = K / 2048;
+    if constexpr (FMT == LW_Q1_0) {
+        // one-chunk rows (K = 2048) only: a row is 256 bytes of bits per
+        // wave, so each wave keeps four rows in flight
+        if (nc == 1 && n_tok == 1) return launch_reg<FMT, 1, 1, 1, 8, 4, 2, NS>(sg, x, M, max_total, stream);
+        if (nc == 1 && n_tok == 2 && NS == 1) return launch_reg<FMT, 2, 1, 1, 8, 4, 2, NS>(sg, x, M, max_total, stream);
+        return hipErrorNotSupported;
+    }
     if (n_tok == 1) {
         if (nc == 1) return launch_reg<FMT, 1, 1, 1, 8, 2, 2, NS>(sg, x, M, max_total, stream);
         if (nc == 2 && M >= 10240) return launch_reg<FMT, 1, 2, 1, 8, 2, 2, NS>(sg, x, M, max_total, stream);
@@ -1129,7 +1162,7 @@ hipError_t launch_multi_ns(int n, const uint8_t* const* W, float* const* y, cons
             if (p.total > max_total) max_total = p.total;
         }
     }
-    if constexpr (FMT == LW_Q4_0 || FMT == LW_Q4_K || FMT == LW_Q4_1) {
+    if constexpr (FMT == LW_Q4_0 || FMT == LW_Q4_K || FMT == LW_Q4_1 || FMT == LW_Q1_0) {
         const hipError_t err = launch_reg_segs<FMT, NS>(sg, x, tot, K, 1, max_total, stream);
         if (err != hipErrorNotSupported) return err;
     }
@@ -1194,6 +1227,7 @@ hipError_t launch_gemv_reg(int fmt, const uint8_t* W, const float* x, float* y, 
     case LW_Q4_0: return launch_reg_fmt<LW_Q4_0>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q4_K: return launch_reg_fmt<LW_Q4_K>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q4_1: return launch_reg_fmt<LW_Q4_1>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q1_0: return launch_reg_fmt<LW_Q1_0>(W, x, y, M, K, n_tok, p, stream);
     default: return hipErrorNotSupported;
     }
 }

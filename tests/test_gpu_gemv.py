@@ -78,7 +78,7 @@ REG_SHAPES = [(1, 2048), (40000, 2048), (9, 4096), (16500, 4096), (5, 8192), (83
               (1, 14336), (3500, 14336)]
 
 
-@pytest.mark.parametrize("fmt", [Q4_0, Q4_K, Q4_1])
+@pytest.mark.parametrize("fmt", [Q4_0, Q4_K, Q4_1, Q1_0])
 @pytest.mark.parametrize("M,K", REG_SHAPES)
 def test_parity_whole_chunks(oracle_mod, fmt, M, K):
     W = synth.gen_packed(fmt, M * K, np.random.default_rng([fmt, M, K, 5]))

@@ -42,7 +42,7 @@ def test_multi_small(oracle_mod, fmt, Ms, K):
         run_multi(oracle_mod, fmt, list(Ms), K, n_tok, 31)
 
 
-@pytest.mark.parametrize("fmt", [Q4_0, Q4_K, Q4_1])
+@pytest.mark.parametrize("fmt", [Q4_0, Q4_K, Q4_1, Q1_0])
 @pytest.mark.parametrize("Ms,K", [((14336, 14336), 4096), ((8192, 8192), 2048), ((2000, 3000, 9000), 14336)])
 def test_multi_register_kernel(oracle_mod, fmt, Ms, K):
     """The register-activation kernel over the rows of two or three matrices
