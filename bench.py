@@ -37,6 +37,19 @@ from paper_2605_20706_amd import binding, layout, synth  # noqa: E402
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFS = 2500.0  # dense bf16 matrix-core peak of MI355X
 CSRC = os.path.join(ROOT, "paper_2605_20706_amd", "csrc")
+# Kernel nodes one captured HIP graph may hold. A 1-bit benchmark process
+# once ended in a segmentation fault while its graphs held 90 k and 180 k
+# kernel nodes (512 tokens at 128 launches per call); the cause was not
+# isolated, so captures stay far below that: the timed steps are split over
+# several graphs (replayed back to back inside the timed region), and a step
+# that alone exceeds the budget runs eagerly.
+MAX_GRAPH_NODES = 16384
+# Rounding bound of the factored evaluations (see lw.h): 2^-17 per unit of
+# the term mass F on top of 1e-4 per unit of A.
+C_FACTORED = 2.0 ** -17
+F32_BOUND = 1e-4
+MFMA_KERNELS = ("fewtok_kernel", "multitok_kernel", "multitok_pk_kernel", "skinny_kernel", "gemm_kernel",
+                "gemm32_kernel")
 METRIC = "dequant-GEMV HBM GB/s (% of peak) and equiv. decode tok/s, Llama-1B/8B shapes"
 METRIC_DEQUANT = "standalone dequant HBM GB/s (packed read + float32 write), Llama-1B/8B shapes"
 
@@ -133,6 +146,17 @@ class Workset:
                 fused = (binding.kernel_name_multi(wl.fmt, Ms, K, n_tok)
                          != binding.kernel_name(wl.fmt, Ms[0], K, n_tok))
             self.call_launches.append(1 if fused or len(grp) == 1 else len(grp))
+        # kernel launches (graph nodes) per call, from the library's own count
+        self.call_nodes = []
+        for grp in self.groups:
+            ms = [mats[i] for i in grp]
+            if op == "dequant":
+                self.call_nodes.append(1)
+            elif len(grp) == 1:
+                self.call_nodes.append(binding.launch_count(wl.fmt, ms[0].M, ms[0].K, n_tok))
+            else:
+                self.call_nodes.append(binding.launch_count_multi(wl.fmt, [m.M for m in ms], ms[0].K, n_tok))
+        self.step_nodes = sum(self.call_nodes)
         self.call_bytes = [sum(self.alg_bytes[i] for i in grp) for grp in self.groups]
         self.call_flops = [sum(self.flops[i] for i in grp) for grp in self.groups]
 
@@ -185,6 +209,18 @@ class Workset:
         return groups
 
 
+def graph_chunks(first, count, nodes_per_step, budget=MAX_GRAPH_NODES):
+    """Steps [first, first + count) as consecutive (first, count) pieces of
+    at most `budget` kernel nodes each, or None when one step alone exceeds
+    the budget (then the steps run eagerly)."""
+    if count <= 0:
+        return []
+    if nodes_per_step > budget:
+        return None
+    per = max(1, budget // max(1, nodes_per_step))
+    return [(f, min(per, first + count - f)) for f in range(first, first + count, per)]
+
+
 def run_gpu(ws, steps, warmup, mode):
     import ctypes
 
@@ -198,6 +234,10 @@ def run_gpu(ws, steps, warmup, mode):
         for i in range(first, first + count):
             ws.step(ctypes.c_void_p(stream), rep=i % ws.reps)
 
+    if mode == "graph" and (graph_chunks(0, 1, ws.step_nodes) is None):
+        log("a step of %d kernel launches exceeds the graph budget of %d nodes: eager mode"
+            % (ws.step_nodes, MAX_GRAPH_NODES))
+        mode = "eager"
     if mode == "graph":
         side = torch.cuda.Stream()
         side.wait_stream(torch.cuda.current_stream())
@@ -205,15 +245,20 @@ def run_gpu(ws, steps, warmup, mode):
             ws.step(ctypes.c_void_p(side.cuda_stream))
         torch.cuda.current_stream().wait_stream(side)
         torch.cuda.synchronize()
-        graphs = []
+        runs = []
         for first, count in ((0, warmup), (warmup, steps)):
-            g = None
-            if count:
+            gs = []
+            for f, c in graph_chunks(first, count, ws.step_nodes):
                 g = torch.cuda.CUDAGraph()
                 with torch.cuda.graph(g):
-                    steps_on(torch.cuda.current_stream().cuda_stream, first, count)
-            graphs.append(g)
-        warm, timed = (g.replay if g else (lambda: None) for g in graphs)
+                    steps_on(torch.cuda.current_stream().cuda_stream, f, c)
+                gs.append(g)
+
+            def replay(gs=gs):
+                for g in gs:
+                    g.replay()
+            runs.append(replay)
+        warm, timed = runs
     else:
         def warm():
             steps_on(torch.cuda.current_stream().cuda_stream, 0, warmup)
@@ -229,6 +274,8 @@ def run_gpu(ws, steps, warmup, mode):
     end.record()
     torch.cuda.synchronize()
     ms_per_step = start.elapsed_time(end) / steps
+    # the outputs of the last timed step, for the parity check against the oracle
+    y_timed = [v.cpu().numpy() for v in ws.y] if ws.op == "matvec" else None
 
     # ---- per-shape launch durations: 192 launches of one matrix shape back
     # to back (cycling over that shape's matrices; one graph in graph mode),
@@ -236,8 +283,9 @@ def run_gpu(ws, steps, warmup, mode):
     # out of the timed span; events on the launch stream ----
     stream = torch.cuda.current_stream()
     per_shape = {}
-    n_seq = 192
     for key, idx in ws.shapes().items():
+        # 192 launches of the shape, fewer where its calls launch several kernels
+        n_seq = max(1, min(192, MAX_GRAPH_NODES // ws.call_nodes[idx[0] % len(ws.groups)]))
         seq = (idx * ((n_seq + len(idx) - 1) // len(idx)))[:max(n_seq, len(idx))]
 
         def sub():
@@ -259,7 +307,7 @@ def run_gpu(ws, steps, warmup, mode):
         e1.record(stream)
         torch.cuda.synchronize()
         per_shape[key] = (e0.elapsed_time(e1) / len(seq), idx)
-    return ms_per_step, per_shape
+    return ms_per_step, per_shape, y_timed, mode
 
 
 KERNEL_SOURCES = {"gemv_kernel": "gemv.hip", "gemv1_kernel": "gemv.hip", "gemv1r_kernel": "gemv.hip",
@@ -306,6 +354,20 @@ def stored_traffic(workload, n_tok, kernel):
         return float(vals["hbm_bytes_per_launch[%s]" % kernel])
     except (KeyError, ValueError):
         return None
+
+
+def traffic_method(workload, n_tok):
+    """How the stored traffic figure was taken: the counters and the
+    calibration factors (from one plain 1 GiB elementwise copy)."""
+    path = os.path.join(ROOT, "profiles", "hbm_traffic_%s_nt%d.txt" % (workload, n_tok))
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        for line in fh:
+            if "bytes = FETCH_SIZE" in line:
+                return ("rocprofv3 --pmc, one counter per run; " + line.strip("# \n")
+                        + "; factors from one 1 GiB elementwise copy (%s)" % os.path.relpath(path, ROOT))
+    return None
 
 
 def ceilings(write, launch_bytes, mode, extra_bytes=()):
@@ -386,14 +448,20 @@ def kernel_groups(ws, per_shape):
     return names, groups
 
 
-def cpu_baseline(ws, budget_s):
+def cpu_baseline(ws, budget_s, y_timed=None):
+    """The oracle on the host's cores over the first matrices of the workload
+    until budget_s is used (timed: its y and A), and, for op matvec, the
+    outputs of the last timed GPU step compared with the oracle on those
+    matrices (untimed: y, A and the term mass F of the kernel's form)."""
     import oracle
 
     wl = ws.wl
+    host_cpus = os.cpu_count() or 1
     # the host share of one GPU: OMP_NUM_THREADS when set, else at most 16 threads
-    n_threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or min(16, os.cpu_count() or 1)
+    n_threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or min(16, host_cpus)
     t_used, nbytes, nweights, done = 0.0, 0, 0, []
     threads = 0
+    refs = {}
     for i, m in enumerate(ws.mats):
         if i not in ws.host:
             break
@@ -402,7 +470,8 @@ def cpu_baseline(ws, budget_s):
             oracle.dequant(wl.fmt, ws.host[i], m.M * m.K)  # one thread
             threads = 1
         else:
-            _, _, threads = oracle.matvec(wl.fmt, ws.host[i], ws.xh[m.K], m.M, m.K, n_threads=n_threads)
+            refs[i] = oracle.matvec(wl.fmt, ws.host[i], ws.xh[m.K], m.M, m.K, n_threads=n_threads)
+            threads = refs[i][2]
         t_used += time.perf_counter() - t0
         nbytes += ws.alg_bytes[i]
         nweights += m.M * m.K
@@ -411,12 +480,61 @@ def cpu_baseline(ws, budget_s):
             break
     gbs = nbytes / t_used / 1e9
     tok_s = ws.n_tok * gbs * 1e9 / sum(ws.alg_bytes)
-    return {"value": round(gbs, 4), "unit": "GB/s", "cores": int(threads), "kind": "oracle",
-            "equiv_decode_tok_s": round(tok_s, 4), "seconds": round(t_used, 2),
-            "sample": "%d of %d matrices (%s), %.3g weights, same inputs; oracle = plain C, "
-                      "double accumulation, one thread per row block"
-                      % (len(done), len(ws.mats), ", ".join(done[:6]) + (" ..." if len(done) > 6 else ""),
-                         nweights)}
+    out = {"value": round(gbs, 4), "unit": "GB/s", "cores": int(threads), "host_cpus": int(host_cpus),
+           "kind": "oracle", "equiv_decode_tok_s": round(tok_s, 4), "seconds": round(t_used, 2),
+           "sample": "%d of %d matrices (%s), %.3g weights, same inputs; oracle = plain C, "
+                     "double accumulation, one thread per row block; %d threads of %d host CPUs"
+                     % (len(done), len(ws.mats), ", ".join(done[:6]) + (" ..." if len(done) > 6 else ""),
+                        nweights, threads, host_cpus)}
+    parity = None
+    if y_timed is not None and refs:
+        parity = timed_parity(ws, refs, y_timed, n_threads)
+    return out, parity
+
+
+def timed_parity(ws, refs, y_timed, n_threads):
+    """Every output of the last timed step, for the matrices the CPU baseline
+    covered, against the oracle: the float32 bound |dy| <= 1e-4 A + 2^-17 F
+    per output (F the term mass of the form the call's kernel evaluates; f16
+    and Q8_0 are plain sums, F = 0), the 2e-3 gate, the normwise error and
+    the NMSE."""
+    import oracle
+
+    wl = ws.wl
+    names = ws.kernel_names()
+    kern_of = {}
+    for j, grp in enumerate(ws.groups):
+        for i in grp:
+            kern_of[i] = names[j]
+    worst = {"scaled": 0.0, "normwise": 0.0, "nmse": 0.0, "f32_bound_ratio": 0.0}
+    n_out, ok = 0, True
+    for i, (y_ref, A, _) in refs.items():
+        m = ws.mats[i]
+        y = y_timed[i].astype(np.float64).reshape(y_ref.shape)
+        if wl.fmt in (layout.F16, layout.Q8_0):
+            F = np.zeros_like(A)
+        else:
+            beta = 128 if kern_of[i].split("<")[0] in MFMA_KERNELS else 0
+            _, _, F, _ = oracle.matvec_f(wl.fmt, ws.host[i], ws.xh[m.K], m.M, m.K, beta, n_threads=n_threads)
+        d = np.abs(y - y_ref)
+        bound = F32_BOUND * A + C_FACTORED * F
+        with np.errstate(divide="ignore", invalid="ignore"):
+            r = np.where(bound > 0, d / bound, np.where(d > 0, np.inf, 0.0))
+            sc = np.where(A > 0, d / A, 0.0)
+        den = np.abs(y_ref).max(axis=1)
+        den[den == 0] = 1.0
+        worst["scaled"] = max(worst["scaled"], float(sc.max()))
+        worst["normwise"] = max(worst["normwise"], float((d.max(axis=1) / den).max()))
+        worst["nmse"] = max(worst["nmse"], float((d ** 2).sum() / max((y_ref ** 2).sum(), 1e-300)))
+        worst["f32_bound_ratio"] = max(worst["f32_bound_ratio"], float(r.max()))
+        ok = ok and bool(np.isfinite(y).all()) and float(r.max()) <= 1.0 and float((d.max(axis=1) / den).max()) <= 2e-3
+        n_out += d.size
+    return {"outputs_checked": int(n_out), "matrices": len(refs), "of_matrices": len(ws.mats),
+            "what": "the last timed step's outputs vs the oracle",
+            "bound": "|dy| <= 1e-4*A + 2^-17*F per output; normwise <= 2e-3",
+            "scaled_max": float("%.4g" % worst["scaled"]), "normwise_max": float("%.4g" % worst["normwise"]),
+            "nmse_max": float("%.4g" % worst["nmse"]), "f32_bound_ratio_max": float("%.4g" % worst["f32_bound_ratio"]),
+            "pass": ok}
 
 
 def main():
@@ -465,7 +583,7 @@ def main():
     if args.op == "dequant":
         args.mode = "eager"  # lw_dequant is on the null stream, which a graph capture cannot record
     ws = Workset(wl, args.n_tok, keep_host=keep, op=args.op, fuse=not args.no_fuse)
-    ms_per_step, per_shape = run_gpu(ws, args.steps, args.warmup, args.mode)
+    ms_per_step, per_shape, y_timed, mode_used = run_gpu(ws, args.steps, args.warmup, args.mode)
 
     n_launch = len(ws.groups)
     step_bytes = sum(ws.alg_bytes)
@@ -492,7 +610,8 @@ def main():
         kern_gbs = g["bytes"] / (g["us"] * 1e-6) / 1e9
         roof = {"bound": "hbm", "achieved": round(kern_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(kern_gbs / HBM_PEAK_GBS, 4)}
-    roof.update({"traffic": stored_traffic(wl.key, args.n_tok, kname), "kernel": kname,
+    roof.update({"traffic": stored_traffic(wl.key, args.n_tok, kname),
+                 "traffic_method": traffic_method(wl.key, args.n_tok), "kernel": kname,
                  "launches_per_step": g["launches"], "avg_launch_us": round(avg_launch_s * 1e6, 3),
                  "alg_bytes_per_launch": round(g["bytes"] / g["launches"]),
                  "alg_flop_per_launch": round(g["flop"] / g["launches"]),
@@ -516,7 +635,8 @@ def main():
                    "matrices": len(ws.mats), "calls_per_step": n_launch,
                    "fused": "a layer's gate and up in one lw_matvec_multi call" if ws.fuse_used else "none",
                    "weights": wl.weights, "n_tok": args.n_tok,
-                   "bytes_per_step": round(step_bytes), "mode": args.mode, "op": args.op,
+                   "bytes_per_step": round(step_bytes), "mode": mode_used, "op": args.op,
+                   "launches_per_step": ws.step_nodes,
                    "weight_copies": ws.reps},
         "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
         "equiv_decode_tok_s": round(tok_s, 1) if args.op == "matvec" else None,
@@ -547,7 +667,9 @@ def main():
         ceil["value_over_step_ceiling"] = round(gbs * 1e9 * step_s / step_bytes, 4)
     out["stream_ceiling"] = ceil
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(ws, args.cpu_seconds)
+        out["cpu_baseline"], parity = cpu_baseline(ws, args.cpu_seconds, y_timed)
+        if parity is not None:
+            out["parity"] = parity
     print(json.dumps(out), flush=True)
 
 

@@ -217,6 +217,25 @@ LW_API const char* lw_kernel_name(int fmt, int64_t M, int64_t K, int64_t n_tok);
  */
 LW_API const char* lw_kernel_name_multi(int fmt, int n_mat, const int64_t* M, int64_t K, int64_t n_tok);
 
+/*
+ * lw_launch_count — the number of kernel launches lw_matvec(fmt, W, x, y, M,
+ * K, n_tok, stream) makes for these sizes (1 for most calls; 2 where a fill
+ * kernel zeroes y before a K-split prefill launch, or where tokens run as
+ * two batches). A caller that captures calls into a HIP graph can budget
+ * the graph's nodes with it. Returns the count (>= 1), or the error lw_matvec
+ * would return on format, sizes or shape (LW_EFMT, LW_EINVAL, LW_ESHAPE).
+ * Host-only: launches nothing.
+ */
+LW_API int64_t lw_launch_count(int fmt, int64_t M, int64_t K, int64_t n_tok);
+
+/*
+ * lw_launch_count_multi — the same for lw_matvec_multi(fmt, n_mat, ..., M, x,
+ * K, n_tok, stream) (M a host array of n_mat row counts); errors as
+ * lw_matvec_multi's size checks (LW_EINVAL also for a null array or n_mat out
+ * of range). Host-only.
+ */
+LW_API int64_t lw_launch_count_multi(int fmt, int n_mat, const int64_t* M, int64_t K, int64_t n_tok);
+
 #ifdef __cplusplus
 }
 #endif

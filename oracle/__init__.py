@@ -13,6 +13,11 @@ builds it with gcc and marshals numpy arrays through ctypes.
   structures of Sec. 2.2).
 * ``matvec(fmt, W_bytes, x, M, K)`` -> (y, A) in float64: y = dequant(W) . x
   (Sec. 2.1: decode is a matrix-vector product) and A = sum_k |w * x|.
+* ``matvec_f(fmt, W_bytes, x, M, K, beta)`` -> (y, A, F): also the term mass
+  F of Eq. (1)'s two terms with the unsigned code shifted by beta,
+  F = sum_k (|s|*(q + beta) + |mu - beta*s|) * |x| (F = A for f16 and q8_0),
+  the quantity that scales the rounding error of a kernel that sums the two
+  terms separately.
 * ``matvec_sampled(...)`` the same for a list of (token, row) outputs.
 """
 from __future__ import annotations
@@ -30,6 +35,9 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 F16, Q8_0, Q4_0, Q4_K, Q4_1, Q1_0 = 0, 1, 2, 3, 4, 5
 
 _lib = None
+# A test may point this module at another build of the oracle (a copy with a
+# planted mistake) through the environment; the default is liboracle.so here.
+_LIB_OVERRIDE = os.environ.get("LW_ORACLE_LIB")
 
 
 def build(force: bool = True) -> str:
@@ -46,9 +54,12 @@ def build(force: bool = True) -> str:
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-            build()
-        lib = ctypes.CDLL(_LIB)
+        if _LIB_OVERRIDE:
+            lib = ctypes.CDLL(_LIB_OVERRIDE)
+        else:
+            if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+                build()
+            lib = ctypes.CDLL(_LIB)
         u8p = ctypes.POINTER(ctypes.c_uint8)
         f32p = ctypes.POINTER(ctypes.c_float)
         f64p = ctypes.POINTER(ctypes.c_double)
@@ -60,6 +71,9 @@ def _load():
         lib.oracle_dequant.restype = ctypes.c_int
         lib.oracle_matvec.argtypes = [ctypes.c_int, u8p, f32p, i64, i64, i64, f64p, f64p, ctypes.c_int]
         lib.oracle_matvec.restype = ctypes.c_int
+        lib.oracle_matvec_f.argtypes = [ctypes.c_int, u8p, f32p, i64, i64, i64, f64p, f64p, f64p, ctypes.c_int,
+                                        ctypes.c_int]
+        lib.oracle_matvec_f.restype = ctypes.c_int
         lib.oracle_matvec_sampled.argtypes = [ctypes.c_int, u8p, f32p, i64, i64, i64, i64,
                                               i64p, i64p, f64p, f64p]
         lib.oracle_matvec_sampled.restype = ctypes.c_int
@@ -113,6 +127,30 @@ def matvec(fmt: int, W, x: np.ndarray, M: int, K: int, n_threads: int = 0):
     if T < 0:
         raise ValueError("oracle.matvec failed")
     return y, A, T
+
+
+def matvec_f(fmt: int, W, x: np.ndarray, M: int, K: int, beta: int = 0, n_threads: int = 0):
+    """Returns (y, A, F, threads): y and A as matvec's, F the term mass with
+    code shift beta (0 <= beta <= 1024), all float64 [n_tok, M]."""
+    W = _bytes(W)
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    if x.ndim == 1:
+        x = x.reshape(1, -1)
+    n_tok = x.shape[0]
+    if x.shape[1] != K:
+        raise ValueError("oracle.matvec_f: x has %d columns, K = %d" % (x.shape[1], K))
+    need = weight_bytes(fmt, M * K)
+    if need < 0 or W.size < need:
+        raise ValueError("oracle.matvec_f: bad format/size")
+    y = np.empty((n_tok, M), dtype=np.float64)
+    A = np.empty((n_tok, M), dtype=np.float64)
+    F = np.empty((n_tok, M), dtype=np.float64)
+    T = _load().oracle_matvec_f(fmt, _ptr(W, ctypes.c_uint8), _ptr(x, ctypes.c_float), M, K, n_tok,
+                                _ptr(y, ctypes.c_double), _ptr(A, ctypes.c_double), _ptr(F, ctypes.c_double),
+                                int(beta), n_threads)
+    if T < 0:
+        raise ValueError("oracle.matvec_f failed")
+    return y, A, F, T
 
 
 def matvec_sampled(fmt: int, W, x: np.ndarray, M: int, K: int, rows, toks):

@@ -14,7 +14,16 @@
  *   - the matrix-vector product y[t][r] = sum_k w[r][k] * x[t][k] with
  *     w = the float dequantized weight, every product taken in double (exact:
  *     24 + 24 bits) and summed in double in the order k = 0, 1, ..., K-1;
- *     alongside it the condition sum A[t][r] = sum_k |w[r][k] * x[t][k]|.
+ *     alongside it the condition sum A[t][r] = sum_k |w[r][k] * x[t][k]|;
+ *   - optionally the term mass F[t][r] of the same product written with
+ *     Eq. (1)'s two terms, value = s*q + mu for the stored unsigned code q,
+ *     and the code shifted by a constant beta:
+ *       value = s*(q + beta) + (mu - beta*s),
+ *       F[t][r] = sum_k (|s_k|*(q_k + beta) + |mu_k - beta*s_k|) * |x[t][k]|.
+ *     A kernel that sums the two terms separately (a factored form) rounds
+ *     sums of these magnitudes, so F scales its rounding error the way A
+ *     scales a plain sum's. Formats without an unsigned code and an offset
+ *     (f16, q8_0) have F = A.
  *
  * Passages followed:
  *   - Eq. (1), Sec. 2.2: x_hat = s * q + mu (scale s, optional offset mu).
@@ -212,6 +221,49 @@ static double exact_value(int fmt, const uint8_t* W, const int64_t off[3], int64
     }
 }
 
+/* |s|*(q + beta) + |mu - beta*s| of element e, exact in double: Eq. (1)'s
+ * scale s and offset mu of the element with its stored unsigned code q
+ * (q4_0: s = d, mu = -8d; q4_1: s = d, mu = m; q4_K-style: s = d*sc_j,
+ * mu = -dmin*m_j; q1_0: value = (2b - 1)*d, so s = 2d, q = b, mu = -d).
+ * f16 and q8_0 have no offset term: the magnitude of the value itself. */
+static double term_mass(int fmt, const uint8_t* W, const int64_t off[3], int64_t e, int beta) {
+    double s, mu, q;
+    switch (fmt) {
+    case OR_Q4_0:
+        s = half_value(read_u16(W + off[1] + 2 * (e / 32)));
+        mu = -8.0 * s;
+        q = (double)q4_code(W, e);
+        break;
+    case OR_Q4_1:
+        s = half_value(read_u16(W + off[1] + 4 * (e / 32)));
+        mu = half_value(read_u16(W + off[1] + 4 * (e / 32) + 2));
+        q = (double)q4_code(W, e);
+        break;
+    case OR_Q1_0: {
+        double d = half_value(read_u16(W + off[1] + 2 * (e / 128)));
+        s = 2.0 * d;
+        mu = -d;
+        q = (double)((W[e / 8] >> (e % 8)) & 1);
+        break;
+    }
+    case OR_Q4_K: {
+        int64_t S = e / 256;
+        int j = (int)((e / 32) % 8);
+        const uint8_t* rec = W + off[1] + 12 * S;
+        s = half_value(read_u16(W + off[2] + 4 * S)) * (double)bit_field(rec, 6 * j, 6);
+        mu = -half_value(read_u16(W + off[2] + 4 * S + 2)) * (double)bit_field(rec, 48 + 6 * j, 6);
+        q = (double)q4_code(W, e);
+        break;
+    }
+    default:
+        return fabs((double)(float)exact_value(fmt, W, off, e));
+    }
+    /* s has <= 17 significant bits and q + beta <= 2^10: the products and
+     * the difference below are exact in double for the scales of every
+     * finite binary16 */
+    return fabs(s) * (q + (double)beta) + fabs(mu - (double)beta * s);
+}
+
 /* out[e] = float(value(e)) for e in [0, n). Returns 0, or -1 on a bad
  * format or n. Single-threaded. */
 int oracle_dequant(int fmt, const uint8_t* W, int64_t n, float* out) {
@@ -231,17 +283,26 @@ typedef struct {
     int64_t M, K, n_tok;
     double* y;
     double* A;
+    double* F;
+    int beta;
     int64_t r_begin, r_end;
 } mv_job;
 
 static void* mv_rows(void* arg) {
     mv_job* jb = (mv_job*)arg;
     float* w = (float*)malloc(sizeof(float) * (size_t)jb->K);
-    if (!w) return (void*)1;
+    double* tm = jb->F ? (double*)malloc(sizeof(double) * (size_t)jb->K) : NULL;
+    if (!w || (jb->F && !tm)) {
+        free(w);
+        free(tm);
+        return (void*)1;
+    }
     for (int64_t r = jb->r_begin; r < jb->r_end; ++r) {
         /* the row of dequantized weights, each rounded once to float */
         for (int64_t k = 0; k < jb->K; ++k)
             w[k] = (float)exact_value(jb->fmt, jb->W, jb->off, r * jb->K + k);
+        if (tm)
+            for (int64_t k = 0; k < jb->K; ++k) tm[k] = term_mass(jb->fmt, jb->W, jb->off, r * jb->K + k, jb->beta);
         for (int64_t t = 0; t < jb->n_tok; ++t) {
             const float* xt = jb->x + t * jb->K;
             double s = 0.0, a = 0.0;
@@ -252,9 +313,15 @@ static void* mv_rows(void* arg) {
             }
             jb->y[t * jb->M + r] = s;
             if (jb->A) jb->A[t * jb->M + r] = a;
+            if (tm) {
+                double f = 0.0;
+                for (int64_t k = 0; k < jb->K; ++k) f += tm[k] * fabs((double)xt[k]);
+                jb->F[t * jb->M + r] = f;
+            }
         }
     }
     free(w);
+    free(tm);
     return NULL;
 }
 
@@ -264,13 +331,14 @@ static int n_threads_or_default(int n_threads) {
     return c > 0 ? (int)c : 1;
 }
 
-/* y[t*M + r] and A[t*M + r] (A may be NULL) for all t < n_tok, r < M.
- * x is float [n_tok][K]. n_threads <= 0 uses every online CPU. Returns the
- * number of threads used, or -1 on a bad argument / allocation failure. */
-int oracle_matvec(int fmt, const uint8_t* W, const float* x, int64_t M, int64_t K,
-                  int64_t n_tok, double* y, double* A, int n_threads) {
+/* y[t*M + r], A[t*M + r] and F[t*M + r] (A, F may be NULL; F with code
+ * shift beta, 0 <= beta <= 1024) for all t < n_tok, r < M. x is float
+ * [n_tok][K]. n_threads <= 0 uses every online CPU. Returns the number of
+ * threads used, or -1 on a bad argument / allocation failure. */
+int oracle_matvec_f(int fmt, const uint8_t* W, const float* x, int64_t M, int64_t K,
+                    int64_t n_tok, double* y, double* A, double* F, int beta, int n_threads) {
     int64_t off[3], total;
-    if (M < 1 || K < 1 || n_tok < 1 || !W || !x || !y) return -1;
+    if (M < 1 || K < 1 || n_tok < 1 || !W || !x || !y || beta < 0 || beta > 1024) return -1;
     if (planes(fmt, M * K, off, &total) || K % block_elems(fmt)) return -1;
     int T = n_threads_or_default(n_threads);
     if (T > M) T = (int)M;
@@ -283,7 +351,7 @@ int oracle_matvec(int fmt, const uint8_t* W, const float* x, int64_t M, int64_t 
     }
     int failed = 0;
     for (int i = 0; i < T; ++i) {
-        mv_job jb = {fmt, W, off, x, M, K, n_tok, y, A, M * i / T, M * (i + 1) / T};
+        mv_job jb = {fmt, W, off, x, M, K, n_tok, y, A, F, beta, M * i / T, M * (i + 1) / T};
         jobs[i] = jb;
         if (pthread_create(&th[i], NULL, mv_rows, &jobs[i])) {
             mv_rows(&jobs[i]); /* could not start a thread: do its rows here */
@@ -298,6 +366,12 @@ int oracle_matvec(int fmt, const uint8_t* W, const float* x, int64_t M, int64_t 
     free(th);
     free(jobs);
     return failed ? -1 : T;
+}
+
+/* oracle_matvec_f without the term mass. */
+int oracle_matvec(int fmt, const uint8_t* W, const float* x, int64_t M, int64_t K,
+                  int64_t n_tok, double* y, double* A, int n_threads) {
+    return oracle_matvec_f(fmt, W, x, M, K, n_tok, y, A, NULL, 0, n_threads);
 }
 
 /* The same product for a list of single outputs: for s < n_samples,

@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(HERE, "liblw.so")
 
 LW_OK = 0
 EXPORTS = ("lw_matvec", "lw_matvec_multi", "lw_dequant", "lw_weight_bytes", "lw_strerror", "lw_kernel_name",
-           "lw_kernel_name_multi")
+           "lw_kernel_name_multi", "lw_launch_count", "lw_launch_count_multi")
 LW_MULTI_MAX = 4
 
 
@@ -61,6 +61,10 @@ def library() -> ctypes.CDLL:
         lib.lw_kernel_name.restype = ctypes.c_char_p
         lib.lw_kernel_name_multi.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.POINTER(i64), i64, i64]
         lib.lw_kernel_name_multi.restype = ctypes.c_char_p
+        lib.lw_launch_count.argtypes = [ctypes.c_int, i64, i64, i64]
+        lib.lw_launch_count.restype = i64
+        lib.lw_launch_count_multi.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.POINTER(i64), i64, i64]
+        lib.lw_launch_count_multi.restype = i64
         _lib = lib
     return _lib
 
@@ -98,6 +102,23 @@ def kernel_name_multi(fmt: int, Ms, K: int, n_tok: int):
     ma = (ctypes.c_int64 * len(Ms))(*Ms)
     v = library().lw_kernel_name_multi(fmt, len(Ms), ma, K, n_tok)
     return None if v is None else v.decode()
+
+
+def launch_count(fmt: int, M: int, K: int, n_tok: int) -> int:
+    """Kernel launches lw_matvec makes for these sizes (host-only)."""
+    v = library().lw_launch_count(fmt, M, K, n_tok)
+    if v < 0:
+        raise LwError(v, "lw_launch_count")
+    return v
+
+
+def launch_count_multi(fmt: int, Ms, K: int, n_tok: int) -> int:
+    """Kernel launches lw_matvec_multi makes for matrices of Ms rows (host-only)."""
+    ma = (ctypes.c_int64 * len(Ms))(*Ms)
+    v = library().lw_launch_count_multi(fmt, len(Ms), ma, K, n_tok)
+    if v < 0:
+        raise LwError(v, "lw_launch_count_multi")
+    return v
 
 
 def _check_gpu(t, name):

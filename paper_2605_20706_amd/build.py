@@ -12,6 +12,7 @@ import glob
 import os
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
@@ -21,8 +22,9 @@ CEILING_LIB = os.path.join(HERE, "libceiling.so")
 CEILING_SRC = os.path.join(HERE, "ceiling", "ceiling.hip")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
+OBJ_DIR = os.path.join(ROOT, "_build")
 FLAGS = [
-    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
     # export only the C ABI (LW_API in lw.h): internal symbols stay inside
@@ -34,9 +36,7 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
-def _hipcc(srcs, out, verbose):
-    tmp = out + ".tmp%d" % os.getpid()
-    cmd = [HIPCC] + FLAGS + ["-I", os.path.join(ROOT, "include"), "-I", CSRC] + srcs + ["-o", tmp]
+def _run(cmd, verbose, tmp):
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -48,6 +48,25 @@ def _hipcc(srcs, out, verbose):
         raise RuntimeError("hipcc failed:\n" + err)
     if verbose and err.strip():
         print(err, file=sys.stderr)
+
+
+def _hipcc(srcs, out, verbose):
+    """Each source compiled to an object (in parallel), then one shared link."""
+    os.makedirs(OBJ_DIR, exist_ok=True)
+    inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC]
+
+    def obj(src):
+        o = os.path.join(OBJ_DIR, os.path.basename(out) + "." + os.path.basename(src) + ".o")
+        tmp = o + ".tmp%d" % os.getpid()
+        _run([HIPCC] + FLAGS + inc + ["-c", src, "-o", tmp], verbose, tmp)
+        os.replace(tmp, o)
+        return o
+
+    jobs = max(1, min(len(srcs), int(os.environ.get("MAX_JOBS", "0")) or (os.cpu_count() or 1), 16))
+    with ThreadPoolExecutor(jobs) as ex:
+        objs = list(ex.map(obj, srcs))
+    tmp = out + ".tmp%d" % os.getpid()
+    _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC"] + objs + ["-o", tmp], verbose, tmp)
     os.replace(tmp, out)
     return out
 

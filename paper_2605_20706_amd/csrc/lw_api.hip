@@ -126,42 +126,88 @@ int lw_matvec_multi(int fmt, int n_mat, const void* const* W, float* const* y, c
     return err == hipSuccess ? LW_OK : LW_EHIP;
 }
 
-const char* lw_kernel_name(int fmt, int64_t M, int64_t K, int64_t n_tok) {
-    if (check_shape(fmt, M, K, n_tok) != LW_OK) return nullptr;
+}  // extern "C"
+
+namespace {
+
+// Runs the selection of lw_matvec (n_mat == 0) or lw_matvec_multi with a
+// launch query active: nothing is launched or dereferenced, the launchers
+// stop at the launch. Returns false when the sizes fail the call's checks or
+// the selection fails.
+bool run_query(int fmt, int n_mat, const int64_t* Ms, int64_t M, int64_t K, int64_t n_tok, lw::LaunchQuery& out) {
+    if (n_mat == 0) {
+        if (check_shape(fmt, M, K, n_tok) != LW_OK) return false;
+    } else {
+        if (!Ms || n_mat < 1 || n_mat > LW_MULTI_MAX) return false;
+        for (int i = 0; i < n_mat; ++i)
+            if (check_shape(fmt, Ms[i], K, n_tok) != LW_OK) return false;
+    }
     lw::LaunchQuery& q = lw::launch_query();
     q.active = true;
     q.name = nullptr;
-    // nothing is launched or dereferenced: the launchers stop at the launch
+    q.count = 0;
     alignas(256) static const uint8_t stand_in[256] = {};
-    const hipError_t err = dispatch(fmt, stand_in, reinterpret_cast<const float*>(stand_in),
-                                    const_cast<float*>(reinterpret_cast<const float*>(stand_in)), M, K, n_tok,
-                                    nullptr);
+    const float* xs = reinterpret_cast<const float*>(stand_in);
+    float* ys0 = const_cast<float*>(xs);
+    hipError_t err;
+    if (n_mat == 0) {
+        err = dispatch(fmt, stand_in, xs, ys0, M, K, n_tok, nullptr);
+    } else {
+        // the same routing as lw_matvec_multi
+        const uint8_t* Ws[LW_MULTI_MAX];
+        float* ys[LW_MULTI_MAX];
+        for (int i = 0; i < LW_MULTI_MAX; ++i) {
+            Ws[i] = stand_in;
+            ys[i] = ys0;
+        }
+        err = hipErrorNotSupported;
+        if (n_tok == 1 && n_mat > 1) err = lw::launch_gemv_multi(fmt, n_mat, Ws, ys, Ms, xs, K, nullptr);
+        if (n_tok >= 3 && n_tok <= 8 && n_mat > 1)
+            err = lw::launch_fewtok_multi(fmt, n_mat, Ws, ys, Ms, xs, K, n_tok, nullptr);
+        if (err == hipErrorNotSupported) {
+            err = hipSuccess;
+            for (int i = 0; i < n_mat && err == hipSuccess; ++i)
+                err = dispatch(fmt, stand_in, xs, ys0, Ms[i], K, n_tok, nullptr);
+        }
+    }
+    out = q;
     q.active = false;
-    return err == hipSuccess ? q.name : nullptr;
+    return err == hipSuccess;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* lw_kernel_name(int fmt, int64_t M, int64_t K, int64_t n_tok) {
+    lw::LaunchQuery r;
+    return run_query(fmt, 0, nullptr, M, K, n_tok, r) ? r.name : nullptr;
 }
 
 const char* lw_kernel_name_multi(int fmt, int n_mat, const int64_t* M, int64_t K, int64_t n_tok) {
-    if (!M || n_mat < 1 || n_mat > LW_MULTI_MAX) return nullptr;
-    for (int i = 0; i < n_mat; ++i)
-        if (check_shape(fmt, M[i], K, n_tok) != LW_OK) return nullptr;
-    if (n_mat == 1 || n_tok == 2 || n_tok > 8) return lw_kernel_name(fmt, M[0], K, n_tok);
-    lw::LaunchQuery& q = lw::launch_query();
-    q.active = true;
-    q.name = nullptr;
-    // nothing is launched or dereferenced: the launchers stop at the launch
-    alignas(256) static const uint8_t stand_in[256] = {};
-    const uint8_t* Ws[LW_MULTI_MAX];
-    float* ys[LW_MULTI_MAX];
-    for (int i = 0; i < LW_MULTI_MAX; ++i) {
-        Ws[i] = stand_in;
-        ys[i] = const_cast<float*>(reinterpret_cast<const float*>(stand_in));
+    lw::LaunchQuery r;
+    return run_query(fmt, n_mat, M, 0, K, n_tok, r) ? r.name : nullptr;
+}
+
+int64_t lw_launch_count(int fmt, int64_t M, int64_t K, int64_t n_tok) {
+    const int rc = check_shape(fmt, M, K, n_tok);
+    if (rc != LW_OK) return rc;
+    lw::LaunchQuery r;
+    return run_query(fmt, 0, nullptr, M, K, n_tok, r) ? r.count : LW_EHIP;
+}
+
+int64_t lw_launch_count_multi(int fmt, int n_mat, const int64_t* M, int64_t K, int64_t n_tok) {
+    if (!known_fmt(fmt)) return LW_EFMT;
+    if (!M || n_mat < 1 || n_mat > LW_MULTI_MAX) return LW_EINVAL;
+    int worst = LW_OK;
+    for (int i = 0; i < n_mat; ++i) {
+        const int rc = check_shape(fmt, M[i], K, n_tok);
+        if (rc == LW_EINVAL) return LW_EINVAL;
+        if (rc != LW_OK) worst = rc;
     }
-    const float* xs = reinterpret_cast<const float*>(stand_in);
-    const hipError_t err = n_tok == 1 ? lw::launch_gemv_multi(fmt, n_mat, Ws, ys, M, xs, K, nullptr)
-                                      : lw::launch_fewtok_multi(fmt, n_mat, Ws, ys, M, xs, K, n_tok, nullptr);
-    q.active = false;
-    if (err == hipSuccess) return q.name;
-    return lw_kernel_name(fmt, M[0], K, n_tok);
+    if (worst != LW_OK) return worst;
+    lw::LaunchQuery r;
+    return run_query(fmt, n_mat, M, 0, K, n_tok, r) ? r.count : LW_EHIP;
 }
 
 int lw_dequant(int fmt, const void* W, float* out, int64_t n) {

@@ -10,23 +10,27 @@
 
 namespace lw {
 
-// Kernel-name query (lw_kernel_name). While a query is active on the calling
-// thread the launchers launch nothing: at the point where they would launch,
-// they record the kernel's name (the first one, when a call launches several)
-// and return hipSuccess. So a query walks exactly the selection a real call
+// Kernel-name query (lw_kernel_name, lw_launch_count). While a query is
+// active on the calling thread the launchers launch nothing: at the point
+// where they would launch, they record the kernel's name (the first one, when
+// a call launches several), add the launches they would make to the count and
+// return hipSuccess. So a query walks exactly the selection a real call
 // makes.
 struct LaunchQuery {
     bool active = false;
     const char* name = nullptr;
+    int64_t count = 0;
 };
 LaunchQuery& launch_query();
 
 // True when a query is active (the caller returns hipSuccess instead of
-// launching); records name if none is recorded yet.
-inline bool query_only(const char* name) {
+// launching); records name if none is recorded yet and counts `launches`
+// kernel launches (a launcher that would also launch a fill kernel passes 2).
+inline bool query_only(const char* name, int launches = 1) {
     LaunchQuery& q = launch_query();
     if (!q.active) return false;
     if (!q.name) q.name = name;
+    q.count += launches;
     return true;
 }
 

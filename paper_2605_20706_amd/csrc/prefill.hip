@@ -1071,7 +1071,7 @@ hipError_t launch_tile(const uint8_t* W, const float* x, float* y, int64_t M, in
     const GemmSplit sp = plan_split((M + TL::BM - 1) / TL::BM, (n_tok + TL::BN - 1) / TL::BN, K);
     const int64_t grid = sp.nrt * sp.ntt * sp.ks;
     if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
-    if (query_only(kernel_name<Name_gemm_kernel, FMT, WM, TT>())) return hipSuccess;
+    if (query_only(kernel_name<Name_gemm_kernel, FMT, WM, TT>(), sp.ks > 1 ? 2 : 1)) return hipSuccess;
     if (sp.ks > 1) zero_fill(y, n_tok * M, stream);
     hipLaunchKernelGGL((gemm_kernel<FMT, WM, TT>), dim3((unsigned)grid), dim3(TL::NT),
                        TL::bytes(MF<FMT>::kSums), stream, W, x, y, M, K, n_tok, p.off1, p.off2, sp);
@@ -1085,7 +1085,7 @@ hipError_t launch_tile32(const uint8_t* W, const float* x, float* y, int64_t M, 
     const GemmSplit sp = plan_split((M + TL::BM - 1) / TL::BM, (n_tok + TL::BN - 1) / TL::BN, K);
     const int64_t grid = sp.nrt * sp.ntt * sp.ks;
     if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
-    if (query_only(kernel_name<Name_gemm32_kernel, FMT, WM>())) return hipSuccess;
+    if (query_only(kernel_name<Name_gemm32_kernel, FMT, WM>(), sp.ks > 1 ? 2 : 1)) return hipSuccess;
     if (sp.ks > 1) zero_fill(y, n_tok * M, stream);
     hipLaunchKernelGGL((gemm32_kernel<FMT, WM>), dim3((unsigned)grid), dim3(TL::NT), TL::bytes(), stream, W, x, y,
                        M, K, n_tok, p.off1, p.off2, sp);

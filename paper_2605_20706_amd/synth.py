@@ -213,3 +213,122 @@ def gen_x_seeded(seed, K: int, n_tok: int = 1) -> np.ndarray:
 def algorithmic_bytes(fmt: int, M: int, K: int, n_tok: int = 1) -> float:
     """Bytes the product must move once: packed W + x + y."""
     return layout.BYTES_PER_WEIGHT[fmt] * M * K + 4.0 * n_tok * (K + M)
+
+
+# ---------------------------------------------------------------------------
+# Edge-case inputs for the parity tests. These draw and encode fields only;
+# they compute no dequantized value and no product.
+
+def _round_half_away(v):
+    return np.sign(v) * np.floor(np.abs(v) + 0.5)
+
+
+def gen_fields_eq1(fmt: int, n: int, rng: np.random.Generator, sigma: float = 0.02) -> dict:
+    """Fields of n weights w ~ N(0, sigma^2) encoded by a test-only Eq. (1)
+    quantizer (round half away from zero): the codes then peak at the code of
+    zero, as for real weights, instead of being uniform.
+
+    q8_0  d = fp16(amax / 127), q = clamp(round(w / d), -127, 127)
+    q4_0  d = fp16(amax / 7), q = clamp(round(w / d) + 8, 0, 15)
+    q4_1  m = fp16(min), d = fp16((max - m) / 15), q = clamp(round((w - m) / d), 0, 15)
+    q4_k  per sub-block of 32: scale (max - min') / 15 and offset -min' with
+          min' = min(min, 0); super-block d, dmin = fp16(largest / 63);
+          sc, m = clamp(round(. / d), 0, 63); q = clamp(round((w + dmin m) / (d sc)), 0, 15)
+    q1_0  d = fp16(mean |w|) per 128, b = (w >= 0)
+    f16   w rounded to binary16
+    """
+    w = rng.standard_normal(n) * sigma
+    if fmt == F16:
+        return {"w": w.astype(np.float16)}
+    if fmt == Q1_0:
+        blk = w.reshape(-1, 128)
+        return {"b": (w >= 0).astype(np.uint8), "d": np.abs(blk).mean(axis=1).astype(np.float16)}
+    blk = w.reshape(-1, 32)
+    if fmt in (Q8_0, Q4_0):
+        lim = 127 if fmt == Q8_0 else 7
+        d = (np.abs(blk).max(axis=1) / lim).astype(np.float16)
+        s = np.repeat(d.astype(np.float64), 32)
+        with np.errstate(divide="ignore", invalid="ignore"):
+            r = np.where(s > 0, _round_half_away(w / s), 0.0)
+        if fmt == Q8_0:
+            return {"q": np.clip(r, -127, 127).astype(np.int8), "d": d}
+        return {"q": np.clip(r + 8, 0, 15).astype(np.uint8), "d": d}
+    if fmt == Q4_1:
+        m = blk.min(axis=1).astype(np.float16)
+        d = ((blk.max(axis=1) - m.astype(np.float64)) / 15).astype(np.float16)
+        s = np.repeat(d.astype(np.float64), 32)
+        mu = np.repeat(m.astype(np.float64), 32)
+        with np.errstate(divide="ignore", invalid="ignore"):
+            r = np.where(s > 0, _round_half_away((w - mu) / s), 0.0)
+        return {"q": np.clip(r, 0, 15).astype(np.uint8), "d": d, "m": m}
+    if fmt == Q4_K:
+        mn = np.minimum(blk.min(axis=1), 0.0)
+        scale = (blk.max(axis=1) - mn) / 15
+        off = -mn
+        sup_s = scale.reshape(-1, 8).max(axis=1)
+        sup_o = off.reshape(-1, 8).max(axis=1)
+        d = (sup_s / 63).astype(np.float16)
+        dmin = (sup_o / 63).astype(np.float16)
+        dd = np.repeat(d.astype(np.float64), 8)
+        dm = np.repeat(dmin.astype(np.float64), 8)
+        with np.errstate(divide="ignore", invalid="ignore"):
+            sc = np.clip(np.where(dd > 0, _round_half_away(scale / dd), 0), 0, 63)
+            mm = np.clip(np.where(dm > 0, _round_half_away(off / dm), 0), 0, 63)
+        s = np.repeat(dd * sc, 32)
+        mu = np.repeat(dm * mm, 32)
+        with np.errstate(divide="ignore", invalid="ignore"):
+            r = np.where(s > 0, _round_half_away((w + mu) / s), 0.0)
+        return {"q": np.clip(r, 0, 15).astype(np.uint8), "sc": sc.astype(np.uint8), "m": mm.astype(np.uint8),
+                "d": d, "dmin": dmin}
+    raise ValueError(fmt)
+
+
+def zero_rows(fmt: int, f: dict, rows, K: int) -> dict:
+    """A copy of the fields in which every weight of the given rows (of a
+    row-major matrix with K columns) is exactly zero while the rows' scales
+    stay nonzero, chosen so that each row's codes and scales are those of the
+    format's other blocks:
+    q4_0  codes 8; q4_1  codes 4 and m = -4 d (exact in binary16);
+    q4_k  codes 3, dmin = d and m_j = 3 sc_j (sc_j in [1, 21]);
+    q8_0  codes 0; f16  +0; q1_0 has no zero level: its scales are set to 0."""
+    f = {k: v.copy() for k, v in f.items()}
+    rows = np.asarray(rows, np.int64)
+    el = (rows[:, None] * K + np.arange(K)[None, :]).reshape(-1)
+    grp = np.unique(el // 32)
+    if fmt == F16:
+        f["w"][el] = np.float16(0)
+    elif fmt == Q8_0:
+        f["q"][el] = 0
+    elif fmt == Q4_0:
+        f["q"][el] = 8
+    elif fmt == Q4_1:
+        f["q"][el] = 4
+        f["m"][grp] = (-4.0 * f["d"][grp].astype(np.float64)).astype(np.float16)
+    elif fmt == Q4_K:
+        f["q"][el] = 3
+        sup = np.unique(el // 256)
+        f["dmin"][sup] = f["d"][sup]
+        sc = (np.arange(grp.size) % 21 + 1).astype(np.uint8)
+        f["sc"][grp] = sc
+        f["m"][grp] = 3 * sc
+    elif fmt == Q1_0:
+        f["d"][np.unique(el // 128)] = np.float16(0)
+    else:
+        raise ValueError(fmt)
+    return f
+
+
+def zero_scales(fmt: int, f: dict, rng: np.random.Generator, frac: float = 0.25) -> dict:
+    """A copy of the fields with a random fraction of the blocks' scales set
+    to zero (q4_1: d = 0, the min kept; q4_k: d = 0 on some super-blocks, d
+    and dmin = 0 on others). f16 is returned unchanged."""
+    f = {k: v.copy() for k, v in f.items()}
+    if fmt == F16:
+        return f
+    d = f["d"]
+    pick = rng.random(d.size) < frac
+    d[pick] = np.float16(0)
+    if fmt == Q4_K:
+        both = pick & (rng.random(d.size) < 0.5)
+        f["dmin"][both] = np.float16(0)
+    return f

@@ -1,27 +1,68 @@
-"""Error measures for the GPU product against the oracle (float64 y, A).
+"""Error measures for the GPU product against the oracle (float64 y, A, F).
 
 The gate for the matrix-vector product is tolerance-based: several float32
 results are correct (any summation order), and a literal elementwise relative
-error cannot serve where y cancels to near zero. Two measures, both <= 2e-3:
-  (i)  max over outputs of |y - y_ref| / A, with A = sum_k |w_k * x_k|;
-  (ii) per token column, max |y - y_ref| / max |y_ref|.
-Also reported: NMSE = sum (y - y_ref)^2 / sum y_ref^2 (the paper's validation
-measure, Sec. 3.2), and the largest elementwise relative error.
+error cannot serve where y cancels to near zero.
+
+Plain sums. A float32 sum of the products w_k * x_k in any order is within
+gamma_n * A of the exact value, A = sum_k |w_k * x_k| (n = its depth).
+
+Factored sums. The kernels evaluate each block of 32 weights as
+s * sum (q + beta) * x + (mu - beta * s) * sum x (Eq. (1)'s two terms; beta = 0
+on the VALU kernels, beta = 128 on the matrix cores, whose code operand is the
+bfloat16 of 128 + q), so their rounding error scales with the term mass
+F = sum_k (|s| (q + beta) + |mu - beta s|) |x_k| (oracle.matvec_f), not with
+A. A row whose dequantized weights are all zero while the scales are not has
+A = 0 but F > 0: no factored evaluation returns exactly 0 there.
+
+Bound (derived before any run, from the form itself): a block's two terms
+are each formed by chains of at most 128 rounded float32 operations on the
+block's terms (at most 2 x 32 products plus the group sum, its scaling and
+the combination on the VALU kernels; at most 2 x 64 products of high and low
+activation parts on the matrix cores, each MFMA adding its products with an
+error no larger than a recursive float32 sum of them), so a block's value is
+within 128 * 2^-24 * F_block of the exact one; summing the block values
+(at most K/32 + a few additions deep) adds gamma_(K/32 + 16) * A, below
+1e-4 * A for K <= 32768. Hence every output must satisfy
+
+    |y - y_ref| <= 1e-4 * A + 2^-17 * F                          (f32 bound)
+
+and, as the target's 2e-3 reading:
+  (i)  |y - y_ref| <= 2e-3 * A + 2^-17 * F for every output;
+  (ii) per token column, max |y - y_ref| / max |y_ref| <= 2e-3.
+For plain sums (f16, Q8_0: no offset term; F not given) the bound is
+gamma_n * A alone and the F term is dropped.
+Also reported: the plain scaled error max |y - y_ref| / A over outputs with
+A > 0, NMSE = sum (y - y_ref)^2 / sum y_ref^2 (the paper's validation
+measure, Sec. 3.2), the largest elementwise relative error, and the largest
+ratio of the error to the f32 bound (<= 1 passes).
 """
 import numpy as np
 
 TOL = 2e-3
+F32_BOUND = 1e-4
+C_FACTORED = 2.0 ** -17
 
 
-def measures(y, y_ref, A):
+def _bounds(A, F, tol):
+    """tol * A + 2^-17 * F (F None: tol * A)."""
+    return tol * A + (0.0 if F is None else C_FACTORED * F)
+
+
+def _ratio(d, den):
+    with np.errstate(divide="ignore", invalid="ignore"):
+        return np.where(den > 0, d / den, np.where(d > 0, np.inf, 0.0))
+
+
+def measures(y, y_ref, A, F=None):
     y = np.asarray(y, np.float64).reshape(y_ref.shape)
     y_ref = np.asarray(y_ref, np.float64)
     A = np.asarray(A, np.float64).reshape(y_ref.shape)
+    if F is not None:
+        F = np.asarray(F, np.float64).reshape(y_ref.shape)
     d = np.abs(y - y_ref)
-    zeroA = A == 0
-    if zeroA.any():
-        assert (y[zeroA] == 0).all(), "an output whose terms are all zero must be exactly 0"
-    scaled = float((d[~zeroA] / A[~zeroA]).max()) if (~zeroA).any() else 0.0
+    pos = A > 0
+    scaled = float((d[pos] / A[pos]).max()) if pos.any() else 0.0
     if y_ref.ndim == 2:
         den = np.abs(y_ref).max(axis=1)
         den[den == 0] = 1.0
@@ -32,13 +73,30 @@ def measures(y, y_ref, A):
     with np.errstate(divide="ignore", invalid="ignore"):
         elem = np.where(y_ref != 0, d / np.abs(y_ref), 0.0)
     return {"scaled": scaled, "normwise": normwise, "nmse": nmse, "elem_max": float(elem.max()),
-            "n_over": int((elem > TOL).sum())}
+            "n_over": int((elem > TOL).sum()),
+            "f32_ratio": float(_ratio(d, _bounds(A, F, F32_BOUND)).max()),
+            "gate_ratio": float(_ratio(d, _bounds(A, F, TOL)).max()),
+            "zero_rows": int((~pos).sum()), "n": int(d.size)}
 
 
-def check(y, y_ref, A, tol=TOL, f32_bound=None, what=""):
-    m = measures(y, y_ref, A)
-    assert m["scaled"] <= tol, (what, m)
-    assert m["normwise"] <= tol, (what, m)
+def check(y, y_ref, A, F=None, tol=TOL, f32_bound=None, what="", normwise=True):
+    """Asserts gate (i) and (ii) at tol and, when f32_bound is set, the
+    float32 bound |y - y_ref| <= f32_bound * A + 2^-17 * F for every output.
+    F: the oracle's term mass for the evaluated form (None: a plain sum).
+    normwise=False skips (ii), for inputs built to cancel (all-zero rows)
+    where max |y_ref| says nothing about the kernel."""
+    y_ref = np.asarray(y_ref, np.float64)
+    yy = np.asarray(y, np.float64).reshape(y_ref.shape)
+    Aa = np.asarray(A, np.float64).reshape(y_ref.shape)
+    Fa = None if F is None else np.asarray(F, np.float64).reshape(y_ref.shape)
+    m = measures(yy, y_ref, Aa, Fa)
+    assert np.isfinite(yy).all(), (what, "non-finite output")
+    d = np.abs(yy - y_ref)
+    bad = d > _bounds(Aa, Fa, tol)
+    assert not bad.any(), (what, "gate (i)", int(bad.sum()), m)
+    if normwise:
+        assert m["normwise"] <= tol, (what, "gate (ii)", m)
     if f32_bound is not None:
-        assert m["scaled"] <= f32_bound, (what, "exceeds float32-accumulation bound", m)
+        bad = d > _bounds(Aa, Fa, f32_bound)
+        assert not bad.any(), (what, "exceeds float32-accumulation bound", int(bad.sum()), m)
     return m

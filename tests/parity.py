@@ -1,0 +1,59 @@
+"""Oracle references for the GPU parity tests: y and A, and the term mass F
+of the form the selected kernel evaluates (gate.py derives the bound).
+
+The VALU kernels evaluate the 4-bit and 1-bit formats as s * sum q x +
+mu * sum x (beta = 0); the matrix-core kernels multiply the bfloat16 of
+128 + q (beta = 128). f16 and Q8_0 are plain sums of products: F is None.
+lw_kernel_name / lw_kernel_name_multi say which kernel a call launches."""
+import numpy as np
+
+from paper_2605_20706_amd import binding
+from paper_2605_20706_amd.layout import F16, Q8_0
+
+MFMA_KERNELS = frozenset({"fewtok_kernel", "multitok_kernel", "multitok_pk_kernel", "skinny_kernel",
+                          "gemm_kernel", "gemm32_kernel"})
+
+
+def beta_of(kernel):
+    return 128 if kernel.split("<")[0] in MFMA_KERNELS else 0
+
+
+def plain(fmt):
+    return fmt in (F16, Q8_0)
+
+
+def kernel_of(fmt, M, K, n_tok, Ms=None):
+    """The kernel that computes the M-row matrix's outputs: the fused
+    launch's kernel where lw_matvec_multi over Ms is one launch, else the
+    kernel of the matrix's own lw_matvec."""
+    if Ms is not None and len(Ms) > 1 and binding.launch_count_multi(fmt, list(Ms), K, n_tok) == 1:
+        return binding.kernel_name_multi(fmt, list(Ms), K, n_tok)
+    return binding.kernel_name(fmt, M, K, n_tok)
+
+
+class Ref:
+    """The oracle's y, A and both term masses (beta 0 and 128) of one matrix
+    for a batch of tokens; F(kernel, nt) picks the one the kernel needs."""
+
+    def __init__(self, oracle_mod, fmt, W, x, M, K, betas=(0, 128), n_threads=0):
+        x = np.atleast_2d(x)
+        self.fmt = fmt
+        self.Fs = {}
+        if plain(fmt):
+            self.y, self.A, _ = oracle_mod.matvec(fmt, W, x, M, K, n_threads=n_threads)
+            return
+        for b in betas:
+            y, A, F, _ = oracle_mod.matvec_f(fmt, W, x, M, K, b, n_threads=n_threads)
+            self.y, self.A, self.Fs[b] = y, A, F
+
+    def F(self, kernel, nt=None):
+        if plain(self.fmt):
+            return None
+        F = self.Fs[beta_of(kernel)]
+        return F if nt is None else F[:nt]
+
+
+def reference(oracle_mod, fmt, W, x, M, K, kernel, n_threads=0):
+    """(y, A, F) for one call whose first kernel is `kernel`."""
+    r = Ref(oracle_mod, fmt, W, x, M, K, betas=(beta_of(kernel),), n_threads=n_threads)
+    return r.y, r.A, r.F(kernel)

@@ -234,3 +234,45 @@ def test_ceiling_library_exports_and_checks():
     assert lib.lw_ceiling_read(A256 + 8, 16, A16, None) == -1
     assert lib.lw_ceiling_write(A256, 0, None) == -1
     assert lib.lw_ceiling_write(A256 + 4, 16, None) == -1
+
+
+def test_edge_cases_cover_every_kernel_family(lib):
+    """The GPU edge-case table (zero rows, zero scales, Eq. (1)-encoded
+    weights, activations scaled by 2^+-60) reaches every kernel family the
+    library selects."""
+    import test_gpu_edges as e
+    seen = set()
+    for fmt in e.FMTS:
+        for M, K, nt in e.EDGE_SHAPES:
+            seen.add(binding.kernel_name(fmt, M, K, nt).split("<")[0])
+        for Ms, K, nt in e.EDGE_MULTI:
+            seen.add(binding.kernel_name_multi(fmt, list(Ms), K, nt).split("<")[0])
+    families = {"gemv_kernel", "gemv1_kernel", "gemv1r_kernel", "fewtok_kernel", "multitok_kernel",
+                "multitok_pk_kernel", "skinny_kernel", "gemm_kernel", "gemm32_kernel"}
+    assert families <= seen, families - seen
+
+
+def test_launch_count(lib):
+    """lw_launch_count / lw_launch_count_multi: the kernel launches a call
+    makes (a prefill K split adds the fill kernel; f16 token blocks plus a
+    remainder are two launches), and the size errors of the calls they
+    describe."""
+    assert binding.launch_count(Q4_K, 14336, 4096, 1) == 1
+    assert binding.launch_count(Q4_0, 4096, 14336, 512) == 2      # 8B down: K split over a zeroed y
+    assert binding.launch_count(Q4_0, 14336, 4096, 512) == 1
+    assert binding.launch_count(F16, 2048, 2048, 17) == 2         # two blocks of 8, then one token
+    assert binding.launch_count(F16, 2048, 2048, 16) == 1
+    assert binding.launch_count(Q1_0, 2048, 2048, 512) == 1       # 128 blocks of 4 in one launch
+    assert binding.launch_count_multi(Q4_K, [14336, 14336], 4096, 1) == 1   # fused gate + up
+    assert binding.launch_count_multi(Q4_K, [14336, 14336], 4096, 2) == 2   # one per matrix
+    assert binding.launch_count_multi(Q4_0, [14336, 14336], 4096, 4) == 1
+    f = lib.lw_launch_count
+    assert f(9, 4, 256, 1) == LW_EFMT
+    assert f(Q4_0, 0, 256, 1) == LW_EINVAL
+    assert f(Q4_0, 4, 300, 1) == LW_ESHAPE
+    g = lib.lw_launch_count_multi
+    Ms = (ctypes.c_int64 * 2)(4, 8)
+    assert g(Q4_0, 0, Ms, 256, 1) == LW_EINVAL
+    assert g(Q4_0, 2, None, 256, 1) == LW_EINVAL
+    assert g(9, 2, Ms, 256, 1) == LW_EFMT
+    assert g(Q4_0, 2, Ms, 300, 1) == LW_ESHAPE
