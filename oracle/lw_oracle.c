@@ -42,6 +42,15 @@
  *     weights and one bit per weight; with Eq. (1)'s offset zero the bit b
  *     selects one of the two symmetric levels, q = 2b - 1, so value = +-d
  *     with the binary16 scale d of the block.
+ *   - Sec. 2.2, 5-bit legacy formats (q5_0 symmetric, q5_1 with a min):
+ *     blocks of 32, value = d * (q - 16) and d * q + m for 5-bit codes.
+ *   - Sec. 2.2, further K-quants over super-blocks of 256 (Sec. 7 studies
+ *     q2_k; Appendix B lists q2_k .. q6_k): q5_K-style as q4_K with 5-bit
+ *     codes; q6_K-style with 16 sub-blocks of 16, a signed 8-bit scale each
+ *     and one binary16 d, value = d * sc_j * (q - 32) for 6-bit codes;
+ *     q2_K-style with 16 sub-blocks of 16, a 4-bit scale and a 4-bit min
+ *     each against binary16 d and dmin, value = d * sc_j * q - dmin * m_j
+ *     for 2-bit codes.
  *   - Sec. 2.1: decode is a matrix-vector product.
  *
  * Byte layout (the library's split-plane layout): plane 0 at offset 0; each
@@ -54,6 +63,15 @@
  * plane 1 holds {binary16 d, binary16 m} per group of 32. Q1_0 plane 0 holds
  * one bit per element, element e at bit (e mod 8) of byte e/8; plane 1 holds
  * one binary16 d per block of 128.
+ * The 5-bit formats keep the Q4 nibble plane for the low four bits of each
+ * code and add a plane of fifth bits, element e at bit (e mod 8) of byte
+ * e/8; then q5_0: binary16 d per 32; q5_1: {d, m} per 32; q5_K: the q4_K
+ * record plane, then {d, dmin}. q6_K: the nibble plane for the low four
+ * bits, a plane of the high two bits (element e at bits 2(e mod 4) of byte
+ * e/4), one int8 scale per 16 elements, one binary16 d per 256. q2_K: the
+ * 2-bit codes (element e at bits 2(e mod 4) of byte e/4), one byte per 16
+ * elements with the scale in bits 0-3 and the min in bits 4-7, then
+ * {d, dmin} per 256.
  *
  * Build: gcc -O2 -ffp-contract=off -fPIC -shared -pthread (no fast-math, no
  * vector intrinsics). Results do not depend on the thread count: each output
@@ -66,13 +84,19 @@
 #include <string.h>
 #include <unistd.h>
 
-enum { OR_F16 = 0, OR_Q8_0 = 1, OR_Q4_0 = 2, OR_Q4_K = 3, OR_Q4_1 = 4, OR_Q1_0 = 5 };
+enum {
+    OR_F16 = 0, OR_Q8_0 = 1, OR_Q4_0 = 2, OR_Q4_K = 3, OR_Q4_1 = 4, OR_Q1_0 = 5,
+    OR_Q5_0 = 6, OR_Q5_1 = 7, OR_Q5_K = 8, OR_Q6_K = 9, OR_Q2_K = 10
+};
 
 /* Elements per block: a row of K elements starts a block when K is a multiple. */
 static int64_t block_elems(int fmt) {
     switch (fmt) {
     case OR_F16: return 1;
-    case OR_Q4_K: return 256;
+    case OR_Q4_K:
+    case OR_Q5_K:
+    case OR_Q6_K:
+    case OR_Q2_K: return 256;
     case OR_Q1_0: return 128;
     default: return 32;
     }
@@ -85,9 +109,9 @@ static int64_t round_up_256(int64_t v) { return (v + 255) / 256 * 256; }
 /* Byte offset of each plane and the total size, for n elements of fmt.
  * Returns 0 on success, -1 for an unknown format or an n the format cannot
  * hold (negative, or not a multiple of the format's block). */
-static int planes(int fmt, int64_t n, int64_t off[3], int64_t* total) {
+static int planes(int fmt, int64_t n, int64_t off[4], int64_t* total) {
     if (n < 0) return -1;
-    off[0] = off[1] = off[2] = 0;
+    off[0] = off[1] = off[2] = off[3] = 0;
     switch (fmt) {
     case OR_F16:
         *total = 2 * n;
@@ -118,13 +142,40 @@ static int planes(int fmt, int64_t n, int64_t off[3], int64_t* total) {
         off[2] = round_up_256(off[1] + 12 * (n / 256));
         *total = off[2] + 4 * (n / 256);
         return 0;
+    case OR_Q5_0:
+    case OR_Q5_1:
+        if (n % 32) return -1;
+        off[1] = round_up_256(n / 2);            /* low four bits, two codes per byte */
+        off[2] = round_up_256(off[1] + n / 8);   /* fifth bits, eight per byte */
+        *total = off[2] + (fmt == OR_Q5_0 ? 2 : 4) * (n / 32);
+        return 0;
+    case OR_Q5_K:
+        if (n % 256) return -1;
+        off[1] = round_up_256(n / 2);
+        off[2] = round_up_256(off[1] + n / 8);
+        off[3] = round_up_256(off[2] + 12 * (n / 256));
+        *total = off[3] + 4 * (n / 256);
+        return 0;
+    case OR_Q6_K:
+        if (n % 256) return -1;
+        off[1] = round_up_256(n / 2);            /* low four bits */
+        off[2] = round_up_256(off[1] + n / 4);   /* high two bits, four codes per byte */
+        off[3] = round_up_256(off[2] + n / 16);  /* int8 scale per 16 */
+        *total = off[3] + 2 * (n / 256);         /* binary16 d per 256 */
+        return 0;
+    case OR_Q2_K:
+        if (n % 256) return -1;
+        off[1] = round_up_256(n / 4);            /* 2-bit codes, four per byte */
+        off[2] = round_up_256(off[1] + n / 16);  /* {scale, min} nibbles per 16 */
+        *total = off[2] + 4 * (n / 256);         /* {d, dmin} per 256 */
+        return 0;
     default:
         return -1;
     }
 }
 
 int64_t oracle_weight_bytes(int fmt, int64_t n) {
-    int64_t off[3], total;
+    int64_t off[4], total;
     if (planes(fmt, n, off, &total)) return -1;
     return total;
 }
@@ -169,10 +220,29 @@ static unsigned q4_code(const uint8_t* codes, int64_t e) {
     return i < 16 ? (byte & 15u) : (byte >> 4);
 }
 
+/* 5-bit code of element e: the Q4 nibble (low four bits) plus the fifth bit
+ * from its plane (element e at bit e mod 8 of byte e/8). */
+static unsigned q5_code(const uint8_t* W, const int64_t off[4], int64_t e) {
+    unsigned hi = bit_field(W + off[1] + e / 8, (int)(e % 8), 1);
+    return q4_code(W, e) | (hi << 4);
+}
+
+/* 2-bit field of element e in a plane of four codes per byte (element e at
+ * bits 2(e mod 4) of byte e/4). */
+static unsigned two_bits(const uint8_t* plane, int64_t e) {
+    return bit_field(plane + e / 4, 2 * (int)(e % 4), 2);
+}
+
+/* 6-bit code of element e of a q6_K-style tensor: the Q4 nibble plus the high
+ * two bits from plane 1. */
+static unsigned q6_code(const uint8_t* W, const int64_t off[4], int64_t e) {
+    return q4_code(W, e) | (two_bits(W + off[1], e) << 4);
+}
+
 /* ---- dequantization: exact closed form, one rounding ---------------------- */
 
 /* The exact real value of element e (before the final rounding). */
-static double exact_value(int fmt, const uint8_t* W, const int64_t off[3], int64_t e) {
+static double exact_value(int fmt, const uint8_t* W, const int64_t off[4], int64_t e) {
     switch (fmt) {
     case OR_F16:
         return half_value(read_u16(W + 2 * e));
@@ -216,6 +286,49 @@ static double exact_value(int fmt, const uint8_t* W, const int64_t off[3], int64
         double b = dmin * (double)m;
         return a - b;
     }
+    case OR_Q5_0: {
+        int q = (int)q5_code(W, off, e);
+        double d = half_value(read_u16(W + off[2] + 2 * (e / 32)));
+        return (double)(q - 16) * d; /* <= 5 + 11 significant bits: exact */
+    }
+    case OR_Q5_1: {
+        int q = (int)q5_code(W, off, e);
+        double d = half_value(read_u16(W + off[2] + 4 * (e / 32)));
+        double m = half_value(read_u16(W + off[2] + 4 * (e / 32) + 2));
+        return (double)q * d + m; /* both multiples of 2^-24 below 2^21: exact */
+    }
+    case OR_Q5_K: {
+        int64_t S = e / 256;
+        int j = (int)((e / 32) % 8);
+        const uint8_t* rec = W + off[2] + 12 * S;
+        unsigned sc = bit_field(rec, 6 * j, 6);
+        unsigned m = bit_field(rec, 48 + 6 * j, 6);
+        double d = half_value(read_u16(W + off[3] + 4 * S));
+        double dmin = half_value(read_u16(W + off[3] + 4 * S + 2));
+        unsigned q = q5_code(W, off, e);
+        double a = d * (double)sc * (double)q; /* <= 22 significant bits */
+        double b = dmin * (double)m;
+        return a - b;
+    }
+    case OR_Q6_K: {
+        int q = (int)q6_code(W, off, e);
+        int sc = (int)(int8_t)W[off[2] + e / 16];
+        double d = half_value(read_u16(W + off[3] + 2 * (e / 256)));
+        /* |sc| <= 2^7 and |q - 32| <= 2^5: <= 23 significant bits, exact in
+         * float as well */
+        return d * (double)sc * (double)(q - 32);
+    }
+    case OR_Q2_K: {
+        int64_t S = e / 256;
+        unsigned q = two_bits(W, e);
+        unsigned scm = W[off[1] + e / 16];
+        unsigned sc = scm & 15u, m = scm >> 4;
+        double d = half_value(read_u16(W + off[2] + 4 * S));
+        double dmin = half_value(read_u16(W + off[2] + 4 * S + 2));
+        double a = d * (double)sc * (double)q; /* <= 17 significant bits */
+        double b = dmin * (double)m;
+        return a - b;
+    }
     default:
         return NAN;
     }
@@ -224,9 +337,11 @@ static double exact_value(int fmt, const uint8_t* W, const int64_t off[3], int64
 /* |s|*(q + beta) + |mu - beta*s| of element e, exact in double: Eq. (1)'s
  * scale s and offset mu of the element with its stored unsigned code q
  * (q4_0: s = d, mu = -8d; q4_1: s = d, mu = m; q4_K-style: s = d*sc_j,
- * mu = -dmin*m_j; q1_0: value = (2b - 1)*d, so s = 2d, q = b, mu = -d).
+ * mu = -dmin*m_j; q1_0: value = (2b - 1)*d, so s = 2d, q = b, mu = -d;
+ * q5_0: s = d, mu = -16d; q5_1: s = d, mu = m; q5_K-style as q4_K;
+ * q6_K-style: s = d*sc_j, mu = -32 s; q2_K-style: s = d*sc_j, mu = -dmin*m_j).
  * f16 and q8_0 have no offset term: the magnitude of the value itself. */
-static double term_mass(int fmt, const uint8_t* W, const int64_t off[3], int64_t e, int beta) {
+static double term_mass(int fmt, const uint8_t* W, const int64_t off[4], int64_t e, int beta) {
     double s, mu, q;
     switch (fmt) {
     case OR_Q4_0:
@@ -255,10 +370,42 @@ static double term_mass(int fmt, const uint8_t* W, const int64_t off[3], int64_t
         q = (double)q4_code(W, e);
         break;
     }
+    case OR_Q5_0:
+        s = half_value(read_u16(W + off[2] + 2 * (e / 32)));
+        mu = -16.0 * s;
+        q = (double)q5_code(W, off, e);
+        break;
+    case OR_Q5_1:
+        s = half_value(read_u16(W + off[2] + 4 * (e / 32)));
+        mu = half_value(read_u16(W + off[2] + 4 * (e / 32) + 2));
+        q = (double)q5_code(W, off, e);
+        break;
+    case OR_Q5_K: {
+        int64_t S = e / 256;
+        int j = (int)((e / 32) % 8);
+        const uint8_t* rec = W + off[2] + 12 * S;
+        s = half_value(read_u16(W + off[3] + 4 * S)) * (double)bit_field(rec, 6 * j, 6);
+        mu = -half_value(read_u16(W + off[3] + 4 * S + 2)) * (double)bit_field(rec, 48 + 6 * j, 6);
+        q = (double)q5_code(W, off, e);
+        break;
+    }
+    case OR_Q6_K:
+        s = half_value(read_u16(W + off[3] + 2 * (e / 256))) * (double)(int8_t)W[off[2] + e / 16];
+        mu = -32.0 * s;
+        q = (double)q6_code(W, off, e);
+        break;
+    case OR_Q2_K: {
+        int64_t S = e / 256;
+        unsigned scm = W[off[1] + e / 16];
+        s = half_value(read_u16(W + off[2] + 4 * S)) * (double)(scm & 15u);
+        mu = -half_value(read_u16(W + off[2] + 4 * S + 2)) * (double)(scm >> 4);
+        q = (double)two_bits(W, e);
+        break;
+    }
     default:
         return fabs((double)(float)exact_value(fmt, W, off, e));
     }
-    /* s has <= 17 significant bits and q + beta <= 2^10: the products and
+    /* s has <= 19 significant bits and q + beta <= 2^11: the products and
      * the difference below are exact in double for the scales of every
      * finite binary16 */
     return fabs(s) * (q + (double)beta) + fabs(mu - (double)beta * s);
@@ -267,7 +414,7 @@ static double term_mass(int fmt, const uint8_t* W, const int64_t off[3], int64_t
 /* out[e] = float(value(e)) for e in [0, n). Returns 0, or -1 on a bad
  * format or n. Single-threaded. */
 int oracle_dequant(int fmt, const uint8_t* W, int64_t n, float* out) {
-    int64_t off[3], total;
+    int64_t off[4], total;
     if (planes(fmt, n, off, &total)) return -1;
     for (int64_t e = 0; e < n; ++e) out[e] = (float)exact_value(fmt, W, off, e);
     return 0;
@@ -337,7 +484,7 @@ static int n_threads_or_default(int n_threads) {
  * threads used, or -1 on a bad argument / allocation failure. */
 int oracle_matvec_f(int fmt, const uint8_t* W, const float* x, int64_t M, int64_t K,
                     int64_t n_tok, double* y, double* A, double* F, int beta, int n_threads) {
-    int64_t off[3], total;
+    int64_t off[4], total;
     if (M < 1 || K < 1 || n_tok < 1 || !W || !x || !y || beta < 0 || beta > 1024) return -1;
     if (planes(fmt, M * K, off, &total) || K % block_elems(fmt)) return -1;
     int T = n_threads_or_default(n_threads);
@@ -380,7 +527,7 @@ int oracle_matvec(int fmt, const uint8_t* W, const float* x, int64_t M, int64_t 
 int oracle_matvec_sampled(int fmt, const uint8_t* W, const float* x, int64_t M, int64_t K,
                           int64_t n_tok, int64_t n_samples, const int64_t* rows,
                           const int64_t* toks, double* y, double* A) {
-    int64_t off[3], total;
+    int64_t off[4], total;
     if (M < 1 || K < 1 || n_tok < 1 || !W || !x || !y || n_samples < 0) return -1;
     if (planes(fmt, M * K, off, &total) || K % block_elems(fmt)) return -1;
     for (int64_t s = 0; s < n_samples; ++s) {

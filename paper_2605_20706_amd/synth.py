@@ -20,6 +20,12 @@ Q8_0 matrix uses the literal seed 0):
         quantized against their block minimum);
 * q1_0  bits uniform in {0, 1} (uniform random bytes); d uniform in
         [1e-3, 2e-2] -> binary16 (one per 128 weights);
+* q5_0  codes uniform in [0, 31]; d as q4_0;   q5_1  codes as q5_0, d and m as q4_1;
+* q5_k  codes as q5_0; sc, m, d, dmin as q4_k;
+* q6_k  codes uniform in [0, 63]; int8 scales uniform in [-128, 127]; d uniform in
+        [1e-5, 2e-4] -> binary16 (the lower part binary16 subnormals);
+* q2_k  codes uniform in [0, 3]; 4-bit scales and mins uniform in [0, 15]; d and
+        dmin as q4_k;
 * x     float32 N(0, 1), shape [n_tok, K], from the generator of the workload
         (matrix_id 99).
 """
@@ -30,7 +36,7 @@ from dataclasses import dataclass
 import numpy as np
 
 from . import layout
-from .layout import F16, Q1_0, Q4_0, Q4_1, Q4_K, Q8_0
+from .layout import F16, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
 
 
 @dataclass(frozen=True)
@@ -102,6 +108,17 @@ WORKLOADS = {
                                  n_toks=(1, 2, 4, 8, 512),
                                  description="Q4_1 (blocks with a min) on Llama-3-8B gate/up/down, "
                                              "n_tok in {1,2,4,8} and prefill 512"),
+    **{"%s_llama8b_ffn" % name: Workload("%s_llama8b_ffn" % name, wid, fmt,
+                                        (Matrix("gate", 14336, 4096, 0, 2), Matrix("up", 14336, 4096, 0, 3),
+                                         Matrix("down", 4096, 14336, 0, 4)),
+                                        n_toks=(1, 2, 4, 8, 512),
+                                        description="%s on Llama-3-8B gate/up/down, n_tok in {1,2,4,8} and "
+                                                    "prefill 512" % desc)
+       for name, wid, fmt, desc in (("q5_0", 8, Q5_0, "Q5_0 (5-bit legacy blocks)"),
+                                    ("q5_1", 9, Q5_1, "Q5_1 (5-bit legacy blocks with a min)"),
+                                    ("q5_k", 10, Q5_K, "Q5_K-style (5-bit K-quant)"),
+                                    ("q6_k", 11, Q6_K, "Q6_K-style (6-bit K-quant, 16-element sub-blocks)"),
+                                    ("q2_k", 12, Q2_K, "Q2_K-style (2-bit K-quant, 16-element sub-blocks)"))},
     "q1_0_1b7": Workload("q1_0_1b7", 7, Q1_0,
                          tuple(_llama_layers(**_L1B7)) + (Matrix("lm_head", _VOCAB_1B7, 2048, 28, 5),),
                          description="q1_0 (1 bit, one scale per 128) decode-step weight set of a "
@@ -143,10 +160,27 @@ def gen_fields(fmt: int, n: int, rng: np.random.Generator) -> dict:
     if fmt == Q1_0:
         return {"b": rng.integers(0, 2, n, dtype=np.uint8),
                 "d": _uniform_half(rng, 1e-3, 2e-2, n // 128)}
-    if fmt == Q4_K:
-        return {"q": rng.integers(0, 16, n, dtype=np.uint8),
+    if fmt in (Q4_K, Q5_K):
+        return {"q": rng.integers(0, 16 if fmt == Q4_K else 32, n, dtype=np.uint8),
                 "sc": rng.integers(0, 64, n // 32, dtype=np.uint8),
                 "m": rng.integers(0, 64, n // 32, dtype=np.uint8),
+                "d": _uniform_half(rng, 1e-4, 2e-3, n // 256),
+                "dmin": _uniform_half(rng, 1e-4, 2e-3, n // 256)}
+    if fmt == Q5_0:
+        return {"q": rng.integers(0, 32, n, dtype=np.uint8),
+                "d": _uniform_half(rng, 1e-3, 2e-2, n // 32)}
+    if fmt == Q5_1:
+        return {"q": rng.integers(0, 32, n, dtype=np.uint8),
+                "d": _uniform_half(rng, 1e-3, 2e-2, n // 32),
+                "m": _uniform_half(rng, -0.2, 0.0, n // 32)}
+    if fmt == Q6_K:
+        return {"q": rng.integers(0, 64, n, dtype=np.uint8),
+                "sc": rng.integers(-128, 128, n // 16, dtype=np.int8),
+                "d": _uniform_half(rng, 1e-5, 2e-4, n // 256)}
+    if fmt == Q2_K:
+        return {"q": rng.integers(0, 4, n, dtype=np.uint8),
+                "sc": rng.integers(0, 16, n // 16, dtype=np.uint8),
+                "m": rng.integers(0, 16, n // 16, dtype=np.uint8),
                 "d": _uniform_half(rng, 1e-4, 2e-3, n // 256),
                 "dmin": _uniform_half(rng, 1e-4, 2e-3, n // 256)}
     raise ValueError(fmt)
@@ -163,13 +197,23 @@ def pack_fields(fmt: int, f: dict) -> np.ndarray:
         return layout.pack_q4_1(f["q"], f["d"], f["m"])
     if fmt == Q1_0:
         return layout.pack_q1_0(f["b"], f["d"])
+    if fmt == Q5_0:
+        return layout.pack_q5_0(f["q"], f["d"])
+    if fmt == Q5_1:
+        return layout.pack_q5_1(f["q"], f["d"], f["m"])
+    if fmt == Q5_K:
+        return layout.pack_q5_k(f["q"], f["sc"], f["m"], f["d"], f["dmin"])
+    if fmt == Q6_K:
+        return layout.pack_q6_k(f["q"], f["sc"], f["d"])
+    if fmt == Q2_K:
+        return layout.pack_q2_k(f["q"], f["sc"], f["m"], f["d"], f["dmin"])
     return layout.pack_q4_k(f["q"], f["sc"], f["m"], f["d"], f["dmin"])
 
 
 def gen_packed(fmt: int, n: int, rng: np.random.Generator) -> np.ndarray:
     """n packed elements per the recipe. The 4-bit code plane is drawn as
     uniform random bytes (same distribution as two uniform nibbles)."""
-    if fmt in (F16, Q8_0):
+    if fmt in (F16, Q8_0, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K):
         return pack_fields(fmt, gen_fields(fmt, n, rng))
     offs, total = layout.plane_offsets(fmt, n)
     out = np.zeros(total, dtype=np.uint8)
@@ -261,9 +305,53 @@ def gen_fields_eq1(fmt: int, n: int, rng: np.random.Generator, sigma: float = 0.
         with np.errstate(divide="ignore", invalid="ignore"):
             r = np.where(s > 0, _round_half_away((w - mu) / s), 0.0)
         return {"q": np.clip(r, 0, 15).astype(np.uint8), "d": d, "m": m}
-    if fmt == Q4_K:
+    if fmt == Q5_0:
+        d = (np.abs(blk).max(axis=1) / 15).astype(np.float16)
+        s = np.repeat(d.astype(np.float64), 32)
+        with np.errstate(divide="ignore", invalid="ignore"):
+            r = np.where(s > 0, _round_half_away(w / s), 0.0)
+        return {"q": np.clip(r + 16, 0, 31).astype(np.uint8), "d": d}
+    if fmt == Q5_1:
+        m = blk.min(axis=1).astype(np.float16)
+        d = ((blk.max(axis=1) - m.astype(np.float64)) / 31).astype(np.float16)
+        s = np.repeat(d.astype(np.float64), 32)
+        mu = np.repeat(m.astype(np.float64), 32)
+        with np.errstate(divide="ignore", invalid="ignore"):
+            r = np.where(s > 0, _round_half_away((w - mu) / s), 0.0)
+        return {"q": np.clip(r, 0, 31).astype(np.uint8), "d": d, "m": m}
+    if fmt == Q6_K:
+        b16 = w.reshape(-1, 16)
+        scale = np.abs(b16).max(axis=1) / 31
+        d = (scale.reshape(-1, 16).max(axis=1) / 127).astype(np.float16)
+        dd = np.repeat(d.astype(np.float64), 16)
+        with np.errstate(divide="ignore", invalid="ignore"):
+            sc = np.clip(np.where(dd > 0, _round_half_away(scale / dd), 0), -128, 127)
+        s = np.repeat(dd * sc, 16)
+        with np.errstate(divide="ignore", invalid="ignore"):
+            r = np.where(s > 0, _round_half_away(w / s), 0.0)
+        return {"q": np.clip(r + 32, 0, 63).astype(np.uint8), "sc": sc.astype(np.int8), "d": d}
+    if fmt == Q2_K:
+        b16 = w.reshape(-1, 16)
+        mn = np.minimum(b16.min(axis=1), 0.0)
+        scale = (b16.max(axis=1) - mn) / 3
+        off = -mn
+        d = (scale.reshape(-1, 16).max(axis=1) / 15).astype(np.float16)
+        dmin = (off.reshape(-1, 16).max(axis=1) / 15).astype(np.float16)
+        dd = np.repeat(d.astype(np.float64), 16)
+        dm = np.repeat(dmin.astype(np.float64), 16)
+        with np.errstate(divide="ignore", invalid="ignore"):
+            sc = np.clip(np.where(dd > 0, _round_half_away(scale / dd), 0), 0, 15)
+            mm = np.clip(np.where(dm > 0, _round_half_away(off / dm), 0), 0, 15)
+        s = np.repeat(dd * sc, 16)
+        mu = np.repeat(dm * mm, 16)
+        with np.errstate(divide="ignore", invalid="ignore"):
+            r = np.where(s > 0, _round_half_away((w + mu) / s), 0.0)
+        return {"q": np.clip(r, 0, 3).astype(np.uint8), "sc": sc.astype(np.uint8), "m": mm.astype(np.uint8),
+                "d": d, "dmin": dmin}
+    if fmt in (Q4_K, Q5_K):
+        top = 15 if fmt == Q4_K else 31
         mn = np.minimum(blk.min(axis=1), 0.0)
-        scale = (blk.max(axis=1) - mn) / 15
+        scale = (blk.max(axis=1) - mn) / top
         off = -mn
         sup_s = scale.reshape(-1, 8).max(axis=1)
         sup_o = off.reshape(-1, 8).max(axis=1)
@@ -278,7 +366,7 @@ def gen_fields_eq1(fmt: int, n: int, rng: np.random.Generator, sigma: float = 0.
         mu = np.repeat(dm * mm, 32)
         with np.errstate(divide="ignore", invalid="ignore"):
             r = np.where(s > 0, _round_half_away((w + mu) / s), 0.0)
-        return {"q": np.clip(r, 0, 15).astype(np.uint8), "sc": sc.astype(np.uint8), "m": mm.astype(np.uint8),
+        return {"q": np.clip(r, 0, top).astype(np.uint8), "sc": sc.astype(np.uint8), "m": mm.astype(np.uint8),
                 "d": d, "dmin": dmin}
     raise ValueError(fmt)
 
@@ -290,7 +378,9 @@ def zero_rows(fmt: int, f: dict, rows, K: int) -> dict:
     format's other blocks:
     q4_0  codes 8; q4_1  codes 4 and m = -4 d (exact in binary16);
     q4_k  codes 3, dmin = d and m_j = 3 sc_j (sc_j in [1, 21]);
-    q8_0  codes 0; f16  +0; q1_0 has no zero level: its scales are set to 0."""
+    q8_0  codes 0; f16  +0; q1_0 has no zero level: its scales are set to 0;
+    q5_0  codes 16; q5_1  codes 4 and m = -4 d; q5_k  as q4_k; q6_k  codes 32;
+    q2_k  codes 3 with dmin = d and m_j = 3 sc_j (sc_j in [1, 5])."""
     f = {k: v.copy() for k, v in f.items()}
     rows = np.asarray(rows, np.int64)
     el = (rows[:, None] * K + np.arange(K)[None, :]).reshape(-1)
@@ -313,6 +403,28 @@ def zero_rows(fmt: int, f: dict, rows, K: int) -> dict:
         f["m"][grp] = 3 * sc
     elif fmt == Q1_0:
         f["d"][np.unique(el // 128)] = np.float16(0)
+    elif fmt == Q5_0:
+        f["q"][el] = 16
+    elif fmt == Q5_1:
+        f["q"][el] = 4
+        f["m"][grp] = (-4.0 * f["d"][grp].astype(np.float64)).astype(np.float16)
+    elif fmt == Q5_K:
+        f["q"][el] = 3
+        sup = np.unique(el // 256)
+        f["dmin"][sup] = f["d"][sup]
+        sc = (np.arange(grp.size) % 21 + 1).astype(np.uint8)
+        f["sc"][grp] = sc
+        f["m"][grp] = 3 * sc
+    elif fmt == Q6_K:
+        f["q"][el] = 32
+    elif fmt == Q2_K:
+        f["q"][el] = 3
+        sup = np.unique(el // 256)
+        f["dmin"][sup] = f["d"][sup]
+        g16 = np.unique(el // 16)
+        sc = (np.arange(g16.size) % 5 + 1).astype(np.uint8)
+        f["sc"][g16] = sc
+        f["m"][g16] = 3 * sc
     else:
         raise ValueError(fmt)
     return f
@@ -320,15 +432,16 @@ def zero_rows(fmt: int, f: dict, rows, K: int) -> dict:
 
 def zero_scales(fmt: int, f: dict, rng: np.random.Generator, frac: float = 0.25) -> dict:
     """A copy of the fields with a random fraction of the blocks' scales set
-    to zero (q4_1: d = 0, the min kept; q4_k: d = 0 on some super-blocks, d
-    and dmin = 0 on others). f16 is returned unchanged."""
+    to zero (q4_1, q5_1: d = 0, the min kept; the K-quants with a min: d = 0
+    on some super-blocks, d and dmin = 0 on others). f16 is returned
+    unchanged."""
     f = {k: v.copy() for k, v in f.items()}
     if fmt == F16:
         return f
     d = f["d"]
     pick = rng.random(d.size) < frac
     d[pick] = np.float16(0)
-    if fmt == Q4_K:
+    if fmt in (Q4_K, Q5_K, Q2_K):
         both = pick & (rng.random(d.size) < 0.5)
         f["dmin"][both] = np.float16(0)
     return f

@@ -31,3 +31,7 @@ def scale_record():
 
 def plane_sizes():
     return [(t[0], int(t[1]), int(t[2]), int(t[3]), int(t[4])) for t in _lines("plane_sizes.txt")]
+
+
+def plane_sizes4():
+    return [(t[0], int(t[1]), int(t[2]), int(t[3]), int(t[4]), int(t[5])) for t in _lines("plane_sizes4.txt")]

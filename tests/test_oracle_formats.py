@@ -12,9 +12,10 @@ import pytest
 
 import golden_io
 from paper_2605_20706_amd import layout
-from paper_2605_20706_amd.layout import F16, Q1_0, Q4_0, Q4_1, Q4_K, Q8_0
+from paper_2605_20706_amd.layout import F16, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
 
-FMT = {"f16": F16, "q8_0": Q8_0, "q4_0": Q4_0, "q4_k": Q4_K, "q4_1": Q4_1, "q1_0": Q1_0}
+FMT = {"f16": F16, "q8_0": Q8_0, "q4_0": Q4_0, "q4_k": Q4_K, "q4_1": Q4_1, "q1_0": Q1_0,
+       "q5_0": Q5_0, "q5_1": Q5_1, "q5_k": Q5_K, "q6_k": Q6_K, "q2_k": Q2_K}
 
 
 def bits(a):
@@ -164,17 +165,39 @@ def _block_for(name, f):
         q = np.zeros(256, np.uint8)
         q[0] = f["q"]
         return layout.pack_q4_1(q, np.repeat(h(f["d"]), 8), np.repeat(h(f["m"]), 8)), 0
+    if name in ("q5_0", "q5_1"):
+        q = np.zeros(256, np.uint8)
+        q[0] = f["q"]
+        if name == "q5_0":
+            return layout.pack_q5_0(q, np.repeat(h(f["d"]), 8)), 0
+        return layout.pack_q5_1(q, np.repeat(h(f["d"]), 8), np.repeat(h(f["m"]), 8)), 0
+    if name == "q6_k":
+        q = np.zeros(256, np.uint8)
+        q[0] = f["q"]
+        sc = np.zeros(16, np.int8)
+        sc[0] = f["sc"]
+        return layout.pack_q6_k(q, sc, h(f["d"])), 0
+    if name == "q2_k":
+        q = np.zeros(256, np.uint8)
+        q[0] = f["q"]
+        sc = np.zeros(16, np.uint8)
+        m = np.zeros(16, np.uint8)
+        sc[0], m[0] = f["sc"], f["m"]
+        return layout.pack_q2_k(q, sc, m, h(f["d"]), h(f["dmin"])), 0
     q = np.zeros(256, np.uint8)
     q[0] = f["q"]
     sc = np.zeros(8, np.uint8)
     m = np.zeros(8, np.uint8)
     sc[0], m[0] = f["sc"], f["m"]
+    if name == "q5_k":
+        return layout.pack_q5_k(q, sc, m, h(f["d"]), h(f["dmin"])), 0
     return layout.pack_q4_k(q, sc, m, h(f["d"]), h(f["dmin"])), 0
 
 
 def test_hand_values(oracle_mod):
     rows = golden_io.hand_values()
-    assert len(rows) >= 10
+    assert len(rows) >= 30
+    assert {r[0] for r in rows} >= set(FMT) - {"f16"}
     for name, f, want_bits, want in rows:
         W, e = _block_for(name, f)
         got = oracle_mod.dequant(FMT[name], W, 256)[e]
@@ -339,3 +362,149 @@ def test_roundtrip_q4_k_eq1(oracle_mod):
     # one float32 rounding of the result on top of the s/2 bound
     tol = s / 2 + np.abs(got) * 2.0 ** -24
     assert (np.abs(w - got)[ok] <= tol[ok] * (1 + 1e-9)).all()
+
+
+# --------------------------------------------------------------------------- 5-bit, 6-bit, 2-bit formats
+
+def test_plane_sizes4_golden(oracle_mod):
+    for name, n, o1, o2, o3, total in golden_io.plane_sizes4():
+        assert oracle_mod.weight_bytes(FMT[name], n) == total, name
+        offs, tot = layout.plane_offsets4(FMT[name], n)
+        assert (offs[1], offs[2], offs[3], tot) == (o1, o2, o3, total), name
+
+
+def test_q5_0_exhaustive(oracle_mod):
+    """32 codes x every finite binary16 d against the exact products (q - 16) * d."""
+    d = finite_halves()
+    for q in range(32):
+        codes = np.full(d.size * 32, q, np.uint8)
+        W = layout.pack_q5_0(codes, d)
+        got = oracle_mod.dequant(Q5_0, W, codes.size)[::32]
+        ref = (np.float64(q - 16) * d.view(np.float16).astype(np.float64)).astype(np.float32)
+        assert same_bits_or_both_zero(got, ref).all(), q
+
+
+def test_q5_1_every_scale(oracle_mod):
+    """Every finite d with random finite mins: q*d + m rounded once (the
+    double sum is exact), against numpy's cast of the double sum."""
+    d = finite_halves()
+    rng = np.random.default_rng(31)
+    m = rng.choice(finite_halves(), d.size)
+    q = rng.integers(0, 32, d.size).astype(np.uint8)
+    codes = np.zeros(d.size * 32, np.uint8)
+    codes[::32] = q
+    got = oracle_mod.dequant(Q5_1, layout.pack_q5_1(codes, d, m), codes.size)[::32]
+    ref = (q.astype(np.float64) * d.view(np.float16).astype(np.float64)
+           + m.view(np.float16).astype(np.float64)).astype(np.float32)
+    ok = np.isfinite(ref)
+    assert same_bits_or_both_zero(got[ok], ref[ok]).all()
+
+
+@pytest.mark.parametrize("fmt", [Q5_K, Q2_K])
+def test_k_quant_fuzz_exact(oracle_mod, fmt):
+    """Random d, dmin (any finite binary16), scales, mins and codes: the exact
+    d*sc*q - dmin*m (fractions) rounded once."""
+    from fractions import Fraction
+    rng = np.random.default_rng(32 + fmt)
+    n = 256 * 64
+    hq = 32 if fmt == Q5_K else 4
+    hs = 64 if fmt == Q5_K else 16
+    per = 32 if fmt == Q5_K else 16
+    q = rng.integers(0, hq, n).astype(np.uint8)
+    sc = rng.integers(0, hs, n // per).astype(np.uint8)
+    m = rng.integers(0, hs, n // per).astype(np.uint8)
+    d = rng.choice(finite_halves(), n // 256)
+    dmin = rng.choice(finite_halves(), n // 256)
+    W = (layout.pack_q5_k(q, sc, m, d, dmin) if fmt == Q5_K else layout.pack_q2_k(q, sc, m, d, dmin))
+    got = oracle_mod.dequant(fmt, W, n)
+    dd = d.view(np.float16).astype(np.float64)
+    dm = dmin.view(np.float16).astype(np.float64)
+    for e in rng.integers(0, n, 3000):
+        S, j = e // 256, e // per
+        v = Fraction(dd[S]) * int(sc[j]) * int(q[e]) - Fraction(dm[S]) * int(m[j])
+        assert got[e] == np.float32(float(v)) or (got[e] == 0 and v == 0), (e, float(v), got[e])
+        # the nearest float of the exact value: within half an ulp
+        assert abs(Fraction(float(got[e])) - v) <= Fraction(float(np.spacing(np.float32(abs(float(v)))))) / 2
+
+
+def test_q6_k_codes_and_scales_exhaustive(oracle_mod):
+    """Every 6-bit code x every int8 scale for three binary16 d (one a
+    subnormal), and every finite d for one code and scale: d*sc*(q - 32) is
+    exact in float32 (<= 23 significant bits)."""
+    for dbits in (0x3C00, 0x2E66, 0x0003):
+        q = np.tile(np.arange(64, dtype=np.uint8), 256 * 16)           # element e: code e mod 64
+        sc = np.repeat(np.arange(-128, 128, dtype=np.int16), 4).astype(np.int8)  # 16 elements per scale
+        n = q.size
+        sc = np.resize(sc, n // 16)
+        W = layout.pack_q6_k(q, sc, np.full(n // 256, dbits, np.uint16))
+        got = oracle_mod.dequant(Q6_K, W, n)
+        dv = np.array([dbits], np.uint16).view(np.float16).astype(np.float64)[0]
+        ref = (dv * np.repeat(sc.astype(np.float64), 16) * (q.astype(np.float64) - 32)).astype(np.float32)
+        assert same_bits_or_both_zero(got, ref).all(), dbits
+    d = finite_halves()
+    q = np.zeros(d.size * 256, np.uint8)
+    q[::256] = 63
+    sc = np.zeros(d.size * 16, np.int8)
+    sc[::16] = -77
+    got = oracle_mod.dequant(Q6_K, layout.pack_q6_k(q, sc, d), q.size)[::256]
+    ref = (d.view(np.float16).astype(np.float64) * -77 * 31).astype(np.float32)
+    ok = np.isfinite(ref)
+    assert same_bits_or_both_zero(got[ok], ref[ok]).all()
+
+
+def test_high_bit_planes_hand_bytes(oracle_mod):
+    """Fifth bits (q5): element e at bit e mod 8 of byte e/8 of plane 1;
+    high two bits (q6_k) and 2-bit codes (q2_k): element e at bits 2(e mod 4)
+    of byte e/4; q2_k scale in bits 0-3, min in bits 4-7 of a sub-block's byte."""
+    n = 256
+    # q5_0: low nibbles all 0, fifth bits 0b00000101 in byte 0 -> elements 0 and 2 have q = 16
+    plane0 = np.zeros(n // 2, np.uint8)
+    plane1 = np.zeros(n // 8, np.uint8)
+    plane1[0] = 0x05
+    W = layout.assemble(Q5_0, n, plane0, plane1, np.full(n // 32, 0x3C00, np.uint16))
+    got = oracle_mod.dequant(Q5_0, W, n)
+    assert list(got[:4]) == [0.0, -16.0, 0.0, -16.0]
+    # q6_k: nibbles 0, high-bit byte 0 = 0b11100100 -> elements 0..3 have high bits 0, 1, 2, 3
+    p0 = np.zeros(n // 2, np.uint8)
+    p1 = np.zeros(n // 4, np.uint8)
+    p1[0] = 0b11100100
+    p2 = np.ones(n // 16, np.int8)
+    W = layout.assemble(Q6_K, n, p0, p1, p2, np.array([0x3C00], np.uint16))
+    got = oracle_mod.dequant(Q6_K, W, n)
+    assert list(got[:5]) == [-32.0, -16.0, 0.0, 16.0, -32.0]
+    # q2_k: code byte 0 = 0b00011011 -> elements 0..3 codes 3, 2, 1, 0; sub-block 0's byte = 0x21
+    #   (scale 1, min 2); d = 1, dmin = 0.5 -> values q - 1
+    c = np.zeros(n // 4, np.uint8)
+    c[0] = 0b00011011
+    scm = np.zeros(n // 16, np.uint8)
+    scm[0] = 0x21
+    dd = np.array([0x3C00, 0x3800], np.uint16)
+    W = layout.assemble(Q2_K, n, c, scm, dd)
+    got = oracle_mod.dequant(Q2_K, W, n)
+    assert list(got[:5]) == [2.0, 1.0, 0.0, -1.0, -1.0]
+    assert list(got[16:18]) == [0.0, 0.0]   # sub-block 1: scale 0, min 0
+
+
+@pytest.mark.parametrize("fmt", [Q5_0, Q5_1, Q5_K, Q6_K, Q2_K])
+def test_roundtrip_eq1_new_formats(oracle_mod, fmt):
+    """Weights from N(0, 0.02^2) encoded by the Eq. (1) test quantizer:
+    every element whose code was not clamped is within s/2 of the original
+    (s the element's effective scale), plus one float32 rounding."""
+    from paper_2605_20706_amd import synth
+    rng = np.random.default_rng(40 + fmt)
+    n = 256 * 256
+    f = synth.gen_fields_eq1(fmt, n, np.random.default_rng(40 + fmt))
+    w = np.random.default_rng(40 + fmt).standard_normal(n) * 0.02   # the same draw
+    got = oracle_mod.dequant(fmt, synth.pack_fields(fmt, f), n).astype(np.float64)
+    if fmt in (Q5_0, Q5_1):
+        s = np.repeat(f["d"].astype(np.float64), 32)
+    elif fmt == Q5_K:
+        s = np.repeat(f["d"].astype(np.float64), 256) * np.repeat(f["sc"].astype(np.float64), 32)
+    else:
+        s = np.abs(np.repeat(f["d"].astype(np.float64), 256) * np.repeat(f["sc"].astype(np.float64), 16))
+    top = {Q5_0: 31, Q5_1: 31, Q5_K: 31, Q6_K: 63, Q2_K: 3}[fmt]
+    inner = (f["q"] > 0) & (f["q"] < top) & (s > 0)
+    tol = s / 2 + np.abs(got) * 2.0 ** -24
+    assert (np.abs(w - got)[inner] <= tol[inner] * (1 + 1e-9)).all()
+    assert inner.mean() > 0.5
+    del rng

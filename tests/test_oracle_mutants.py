@@ -48,6 +48,17 @@ MUTANTS = [
     ("scale plane not aligned", "off[1] = round_up_256(n / 2);", "off[1] = n / 2;"),
     ("legacy scale of the even group used for the odd one", "W + off[1] + 2 * (e / 32)",
      "W + off[1] + 2 * ((e / 32) / 2 * 2)"),
+    ("q5 fifth bit ignored", "return q4_code(W, e) | (hi << 4);", "return q4_code(W, e);"),
+    ("q5_0 offset -15", "return (double)(q - 16) * d;", "return (double)(q - 15) * d;"),
+    ("q6_k high bits at the wrong place", "return q4_code(W, e) | (two_bits(W + off[1], e) << 4);",
+     "return q4_code(W, e) | (two_bits(W + off[1], e) << 3);"),
+    ("q6_k scales read unsigned", "int sc = (int)(int8_t)W[off[2] + e / 16];", "int sc = (int)W[off[2] + e / 16];"),
+    ("q6_k scale per 32 instead of 16", "int sc = (int)(int8_t)W[off[2] + e / 16];",
+     "int sc = (int)(int8_t)W[off[2] + e / 32];"),
+    ("q2_k scale and min nibbles swapped", "unsigned sc = scm & 15u, m = scm >> 4;",
+     "unsigned sc = scm >> 4, m = scm & 15u;"),
+    ("2-bit fields read most-significant first", "return bit_field(plane + e / 4, 2 * (int)(e % 4), 2);",
+     "return bit_field(plane + e / 4, 6 - 2 * (int)(e % 4), 2);"),
     ("term mass without the code shift", "return fabs(s) * (q + (double)beta) + fabs(mu - (double)beta * s);",
      "return fabs(s) * q + fabs(mu - (double)beta * s);"),
     ("term mass offset taken with its sign", "fabs(mu - (double)beta * s);", "(mu - (double)beta * s);"),

@@ -12,7 +12,7 @@ import numpy as np
 import pytest
 
 from paper_2605_20706_amd import synth
-from paper_2605_20706_amd.layout import F16, Q1_0, Q4_0, Q4_1, Q4_K, Q8_0
+from paper_2605_20706_amd.layout import F16, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
 
 M, K = 9, 512
 
@@ -39,7 +39,7 @@ def test_no_offset_formats_have_F_equal_A(oracle_mod, fmt, beta):
     assert np.array_equal(F_of(oracle_mod, fmt, f, x, beta), A_of(oracle_mod, fmt, f, x))
 
 
-@pytest.mark.parametrize("fmt", [Q4_0, Q4_K, Q4_1, Q1_0])
+@pytest.mark.parametrize("fmt", [Q4_0, Q4_K, Q4_1, Q1_0, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K])
 @pytest.mark.parametrize("beta", [0, 1, 128])
 def test_F_at_least_A(oracle_mod, fmt, beta):
     f = fields(fmt, 3)
@@ -111,3 +111,68 @@ def test_q1_0_against_condition_sums(oracle_mod):
         xr = (x[0] * b[r]).astype(np.float32)[None, :]
         _, Ar, _ = oracle_mod.matvec(Q1_0, W, xr, M, K)
         assert np.isclose(F[0, r], 2 * Ar[0, r] + A[0, r], rtol=1e-12, atol=0), r
+
+
+def test_q5_0_against_condition_sums(oracle_mod):
+    """F_beta = sum |d| (q + 16 + 2 beta) |x| = A(codes q, as q5_1 with m = 0)
+    + (16 + 2 beta) * A(codes 17, i.e. values d)."""
+    f = fields(Q5_0, 15)
+    x = synth.gen_x_seeded(16, K, 2)
+    a_q = A_of(oracle_mod, Q5_1, {"q": f["q"], "d": f["d"], "m": np.zeros_like(f["d"])}, x)
+    a_1 = A_of(oracle_mod, Q5_0, {"q": np.full_like(f["q"], 17), "d": f["d"]}, x)
+    for beta in (0, 128):
+        F = F_of(oracle_mod, Q5_0, f, x, beta)
+        assert np.allclose(F, a_q + (16 + 2 * beta) * a_1, rtol=1e-12, atol=0), beta
+
+
+def test_q6_k_against_condition_sums(oracle_mod):
+    """mu = -32 s: F_beta = sum |s| (q + 32 + 2 beta) |x| = A(codes q + 32
+    would overflow 6 bits, so): A(codes 33: values d sc) * (32 + 2 beta)
+    + sum |s| q |x|, the last from the one-hot rows of x (F at x = e_k is the
+    element's own |s| (q + 32 + 2 beta))."""
+    f = fields(Q6_K, 17)
+    x = synth.gen_x_seeded(18, K, 2)
+    a_1 = A_of(oracle_mod, Q6_K, {"q": np.full_like(f["q"], 33), "sc": f["sc"], "d": f["d"]}, x)
+    F0 = F_of(oracle_mod, Q6_K, f, x, 0)
+    F128 = F_of(oracle_mod, Q6_K, f, x, 128)
+    assert np.allclose(F128 - F0, 256 * a_1, rtol=1e-9, atol=0)
+    # one-hot: element (r, k) alone; A there is |s| |q - 32|, F_0 is |s| (q + 32)
+    W = synth.pack_fields(Q6_K, f)
+    q = f["q"].reshape(M, K).astype(np.float64)
+    for k in (0, 15, 16, 300, 511):
+        e = np.zeros((1, K), np.float32)
+        e[0, k] = 1.0
+        _, A, F, _ = oracle_mod.matvec_f(Q6_K, W, e, M, K, 0)
+        ok = q[:, k] != 32
+        s = np.zeros(M)
+        s[ok] = A[0][ok] / np.abs(q[ok, k] - 32)
+        assert np.allclose(F[0][ok], s[ok] * (q[ok, k] + 32), rtol=1e-12, atol=0), k
+
+
+@pytest.mark.parametrize("fmt", [Q5_K, Q2_K])
+def test_k_quants_with_min_against_condition_sums(oracle_mod, fmt):
+    """d, dmin >= 0: F_beta = A(codes q, m = 0) + A(codes 0: values -dmin m)
+    + 2 beta A(codes 1, m = 0)."""
+    f = fields(fmt, 19)
+    x = synth.gen_x_seeded(20, K, 2)
+    z = np.zeros_like(f["m"])
+    base = {"sc": f["sc"], "d": f["d"], "dmin": f["dmin"]}
+    a_q = A_of(oracle_mod, fmt, dict(base, q=f["q"], m=z), x)
+    a_m = A_of(oracle_mod, fmt, dict(base, q=np.zeros_like(f["q"]), m=f["m"]), x)
+    a_1 = A_of(oracle_mod, fmt, dict(base, q=np.ones_like(f["q"]), m=z), x)
+    for beta in (0, 128):
+        F = F_of(oracle_mod, fmt, f, x, beta)
+        assert np.allclose(F, a_q + a_m + 2 * beta * a_1, rtol=1e-12, atol=0), beta
+
+
+def test_q5_1_against_condition_sums(oracle_mod):
+    f = fields(Q5_1, 21)
+    assert (f["m"].astype(np.float64) <= 0).all()
+    x = synth.gen_x_seeded(22, K, 2)
+    z = np.zeros_like(f["m"])
+    a_q = A_of(oracle_mod, Q5_1, {"q": f["q"], "d": f["d"], "m": z}, x)
+    a_m = A_of(oracle_mod, Q5_1, {"q": np.zeros_like(f["q"]), "d": f["d"], "m": f["m"]}, x)
+    a_1 = A_of(oracle_mod, Q5_1, {"q": np.ones_like(f["q"]), "d": f["d"], "m": z}, x)
+    for beta in (0, 128):
+        F = F_of(oracle_mod, Q5_1, f, x, beta)
+        assert np.allclose(F, a_q + a_m + 2 * beta * a_1, rtol=1e-12, atol=0), beta
