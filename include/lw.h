@@ -57,12 +57,34 @@
  *           plane 1: n/128 x binary16 d (block B = e / 128).
  *                                    value = (2b[e] - 1) * d[B] = +-d[B]
  *
+ *   5-bit codes q in [0, 31]: bits 0-3 in a plane laid out as LW_Q4_0's plane
+ *   0, bit 4 in a plane of n/8 bytes (element e at bit (e mod 8) of byte e/8).
+ *   LW_Q5_0 plane 0: low four bits; plane 1: fifth bits;
+ *           plane 2: n/32 x binary16 d.            value = (q - 16) * d[g]
+ *   LW_Q5_1 planes 0, 1 as LW_Q5_0; plane 2: n/32 x { binary16 d, binary16 m }.
+ *                                                   value = q * d[g] + m[g]
+ *   LW_Q5_K planes 0, 1 as LW_Q5_0; plane 2: the 12-byte records of LW_Q4_K;
+ *           plane 3: n/256 x { binary16 d, binary16 dmin }.
+ *                                    value = d[S] * sc_j * q[e] - dmin[S] * m_j
+ *   Sub-blocks of 16 (t = e / 16):
+ *   LW_Q6_K plane 0: bits 0-3 of 6-bit codes q in [0, 63], as LW_Q4_0's
+ *                    plane 0; plane 1: n/4 bytes of bits 4-5, element e at
+ *                    bits 2(e mod 4) .. 2(e mod 4)+1 of byte e/4;
+ *           plane 2: n/16 x int8 scale sc[t]; plane 3: n/256 x binary16 d.
+ *                                    value = d[S] * sc[t] * (q[e] - 32)
+ *   LW_Q2_K plane 0: n/4 bytes of 2-bit codes q in [0, 3], element e at bits
+ *                    2(e mod 4) .. 2(e mod 4)+1 of byte e/4;
+ *           plane 1: n/16 bytes, sc[t] in bits 0-3 and m[t] in bits 4-7;
+ *           plane 2: n/256 x { binary16 d, binary16 dmin }.
+ *                                    value = d[S] * sc[t] * q[e] - dmin[S] * m[t]
+ *
  * The dequantized value of an element is the exact real value of its closed
  * form rounded once to binary32 with round-to-nearest-even. For LW_F16,
  * LW_Q8_0 and LW_Q4_0 the closed form is exactly representable in binary32;
  * for LW_Q4_K the two products are exact and the difference is rounded once;
  * for LW_Q4_1 the product is exact and the sum with the min is rounded once;
- * LW_Q1_0's value is +-d, exact.
+ * LW_Q1_0's value is +-d, exact. LW_Q5_0 and LW_Q6_K are exact; LW_Q5_1,
+ * LW_Q5_K and LW_Q2_K round once, as LW_Q4_1 and LW_Q4_K.
  * ------------------------------------------------------------------------
  */
 #ifndef LW_H
@@ -84,10 +106,14 @@ extern "C" {
 #endif
 
 /* Weight formats (Sec. 2.2: f16 storage, legacy blocks of 32 without (Q8_0,
- * Q4_0) and with (Q4_1) an offset, K-quant super-blocks of 256 with
- * double-quantized scales and mins, and the 1-bit symmetric q1_0 with one
- * scale per 128 weights). */
-typedef enum { LW_F16 = 0, LW_Q8_0 = 1, LW_Q4_0 = 2, LW_Q4_K = 3, LW_Q4_1 = 4, LW_Q1_0 = 5 } lw_fmt;
+ * Q4_0, Q5_0) and with (Q4_1, Q5_1) an offset, K-quant super-blocks of 256
+ * with double-quantized scales (and mins) at 2, 4, 5 and 6 bits per code,
+ * and the 1-bit symmetric q1_0 with one scale per 128 weights; Sec. 7 and
+ * Appendix B list q2_k .. q6_k). */
+typedef enum {
+    LW_F16 = 0, LW_Q8_0 = 1, LW_Q4_0 = 2, LW_Q4_K = 3, LW_Q4_1 = 4, LW_Q1_0 = 5,
+    LW_Q5_0 = 6, LW_Q5_1 = 7, LW_Q5_K = 8, LW_Q6_K = 9, LW_Q2_K = 10
+} lw_fmt;
 
 /* Return codes. */
 enum {

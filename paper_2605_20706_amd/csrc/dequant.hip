@@ -3,9 +3,11 @@
 // Each element's closed form (Eq. (1) of Sec. 2.2 with the legacy and K-quant
 // block structures of Sec. 2.2) is evaluated with exact float32 products and at
 // most one rounding: q*d and (q-8)*d are exact products; the K-quant style
-// value d*sc*q - dmin*m is one fused multiply-add of the exact d*sc and the
-// exact dmin*m, and Q4_1's q*d + m one fused multiply-add of the exact q*d
-// and m. No half-precision arithmetic is used.
+// value d*sc*q - dmin*m (Q4_K-, Q5_K-, Q2_K-style) is one fused
+// multiply-add of the exact d*sc and the exact dmin*m, and Q4_1's and Q5_1's
+// q*d + m one fused multiply-add of the exact q*d and m; Q6_K-style
+// d*sc*(q - 32) is exact (at most 23 significant bits). No half-precision
+// arithmetic is used.
 //
 // Work split: per grid-stride step a thread writes four float4 (4 consecutive
 // elements each), 256 float4 apart, so each store instruction of a wave is
@@ -27,7 +29,8 @@ struct Name_dequant_kernel {
 
 // the 4 elements e .. e+3 (e a multiple of 4)
 template <int FMT>
-__device__ __forceinline__ float4 value4(const uint8_t* __restrict__ W, int64_t off1, int64_t off2, int64_t e) {
+__device__ __forceinline__ float4 value4(const uint8_t* __restrict__ W, int64_t off1, int64_t off2, int64_t off3,
+                                        int64_t e) {
     float4 v;
     if constexpr (FMT == LW_F16) {
         const uint2 h = *reinterpret_cast<const uint2*>(W + 2 * e);
@@ -50,6 +53,17 @@ __device__ __forceinline__ float4 value4(const uint8_t* __restrict__ W, int64_t 
         v.y = (b & 2u) ? d : -d;
         v.z = (b & 4u) ? d : -d;
         v.w = (b & 8u) ? d : -d;
+    } else if constexpr (FMT == LW_Q2_K) {
+        // four 2-bit codes of byte e/4; the sub-block's {scale, min} byte
+        const uint32_t b = W[e >> 2];
+        const uint32_t scm = W[off1 + (e >> 4)];
+        const uint32_t dd = *reinterpret_cast<const uint32_t*>(W + off2 + 4 * (e >> 8));
+        const float ds = half_bits_to_float(dd & 0xFFFFu) * (float)(scm & 15u);  // exact
+        const float dm = half_bits_to_float(dd >> 16) * (float)(scm >> 4);       // exact
+        v.x = __builtin_fmaf(ds, (float)(b & 3u), -dm);                          // one rounding
+        v.y = __builtin_fmaf(ds, (float)((b >> 2) & 3u), -dm);
+        v.z = __builtin_fmaf(ds, (float)((b >> 4) & 3u), -dm);
+        v.w = __builtin_fmaf(ds, (float)(b >> 6), -dm);
     } else {
         // Q4 code plane: group g = e/32 owns bytes [16g, 16g+16); byte i
         // holds element 32g+i (low nibble) and 32g+i+16 (high nibble).
@@ -71,6 +85,47 @@ __device__ __forceinline__ float4 value4(const uint8_t* __restrict__ W, int64_t 
             v.y = __builtin_fmaf(ubyte<1>(b), d, m);
             v.z = __builtin_fmaf(ubyte<2>(b), d, m);
             v.w = __builtin_fmaf(ubyte<3>(b), d, m);
+        } else if constexpr (FMT == LW_Q5_0 || FMT == LW_Q5_1 || FMT == LW_Q5_K) {
+            // fifth bits of e..e+3: bits (e mod 8) .. (e mod 8) + 3 of byte e/8
+            const uint32_t h = ((uint32_t)W[off1 + (e >> 3)] >> (e & 4)) & 15u;
+            const float q0 = (float)(((b >> 0) & 0xFFu) | ((h & 1u) << 4)), q1 = (float)(((b >> 8) & 0xFFu) | ((h & 2u) << 3));
+            const float q2 = (float)(((b >> 16) & 0xFFu) | ((h & 4u) << 2)), q3 = (float)(((b >> 24) & 0xFFu) | ((h & 8u) << 1));
+            if constexpr (FMT == LW_Q5_0) {
+                const float d = half_bits_to_float(*reinterpret_cast<const uint16_t*>(W + off2 + 2 * g));
+                v.x = (q0 - 16.0f) * d;  // exact
+                v.y = (q1 - 16.0f) * d;
+                v.z = (q2 - 16.0f) * d;
+                v.w = (q3 - 16.0f) * d;
+            } else if constexpr (FMT == LW_Q5_1) {
+                const uint32_t dm = *reinterpret_cast<const uint32_t*>(W + off2 + 4 * g);
+                const float d = half_bits_to_float(dm & 0xFFFFu), m = half_bits_to_float(dm >> 16);
+                v.x = __builtin_fmaf(q0, d, m);  // exact product, one rounding
+                v.y = __builtin_fmaf(q1, d, m);
+                v.z = __builtin_fmaf(q2, d, m);
+                v.w = __builtin_fmaf(q3, d, m);
+            } else {
+                const int64_t S = e >> 8;
+                const int j = (int)(g & 7);
+                const uint32_t* rec = reinterpret_cast<const uint32_t*>(W + off2 + 12 * S);
+                const uint64_t lo = (uint64_t)rec[0] | ((uint64_t)rec[1] << 32);
+                const uint64_t hi = (uint64_t)rec[1] | ((uint64_t)rec[2] << 32);
+                const uint32_t dd = *reinterpret_cast<const uint32_t*>(W + off3 + 4 * S);
+                const float ds = half_bits_to_float(dd & 0xFFFFu) * (float)((uint32_t)(lo >> (6 * j)) & 63u);
+                const float dm = half_bits_to_float(dd >> 16) * (float)((uint32_t)(hi >> (16 + 6 * j)) & 63u);
+                v.x = __builtin_fmaf(ds, q0, -dm);  // exact products, one rounding
+                v.y = __builtin_fmaf(ds, q1, -dm);
+                v.z = __builtin_fmaf(ds, q2, -dm);
+                v.w = __builtin_fmaf(ds, q3, -dm);
+            }
+        } else if constexpr (FMT == LW_Q6_K) {
+            // high two bits of e..e+3: byte e/4 of plane 1; int8 scale per 16
+            const uint32_t h = W[off1 + (e >> 2)];
+            const float sc = (float)(int32_t)(int8_t)W[off2 + (e >> 4)];
+            const float ds = half_bits_to_float(*reinterpret_cast<const uint16_t*>(W + off3 + 2 * (e >> 8))) * sc;
+            v.x = ds * (float)((int)(((b >> 0) & 0xFFu) | ((h & 3u) << 4)) - 32);  // exact (<= 23 bits)
+            v.y = ds * (float)((int)(((b >> 8) & 0xFFu) | ((h & 12u) << 2)) - 32);
+            v.z = ds * (float)((int)(((b >> 16) & 0xFFu) | (h & 48u)) - 32);
+            v.w = ds * (float)((int)(((b >> 24) & 0xFFu) | ((h & 192u) >> 2)) - 32);
         } else {
             const int64_t S = e >> 8;
             const int j = (int)(g & 7);
@@ -96,7 +151,7 @@ constexpr int kDqU = 4;  // float4 per thread and grid-stride step
 template <int FMT>
 __global__ void __launch_bounds__(256) dequant_kernel(const uint8_t* __restrict__ W,
                                                       float4* __restrict__ out, int64_t n4,
-                                                      int64_t off1, int64_t off2) {
+                                                      int64_t off1, int64_t off2, int64_t off3) {
     typedef float f32x4 __attribute__((ext_vector_type(4)));
     const int64_t stride = (int64_t)gridDim.x * blockDim.x * kDqU;
     for (int64_t base = (int64_t)blockIdx.x * blockDim.x * kDqU + threadIdx.x; base < n4; base += stride) {
@@ -104,7 +159,7 @@ __global__ void __launch_bounds__(256) dequant_kernel(const uint8_t* __restrict_
 #pragma unroll
         for (int u = 0; u < kDqU; ++u) {
             const int64_t i = base + (int64_t)u * blockDim.x;
-            v[u] = value4<FMT>(W, off1, off2, 4 * (i < n4 ? i : n4 - 1));  // past the end: a copy, not stored
+            v[u] = value4<FMT>(W, off1, off2, off3, 4 * (i < n4 ? i : n4 - 1));  // past the end: a copy, not stored
         }
 #pragma unroll
         for (int u = 0; u < kDqU; ++u) {
@@ -124,7 +179,7 @@ hipError_t launch(const uint8_t* W, float* out, int64_t n, const Planes& p, hipS
     if (blocks > cap) blocks = cap;
     if (query_only(kernel_name<Name_dequant_kernel, FMT>())) return hipSuccess;
     hipLaunchKernelGGL(dequant_kernel<FMT>, dim3((unsigned)blocks), dim3(threads), 0, stream, W,
-                       reinterpret_cast<float4*>(out), n4, p.off1, p.off2);
+                       reinterpret_cast<float4*>(out), n4, p.off1, p.off2, p.off3);
     return hipGetLastError();
 }
 
@@ -139,6 +194,11 @@ hipError_t launch_dequant(int fmt, const uint8_t* W, float* out, int64_t n, cons
     case LW_Q4_K: return launch<LW_Q4_K>(W, out, n, p, stream);
     case LW_Q4_1: return launch<LW_Q4_1>(W, out, n, p, stream);
     case LW_Q1_0: return launch<LW_Q1_0>(W, out, n, p, stream);
+    case LW_Q5_0: return launch<LW_Q5_0>(W, out, n, p, stream);
+    case LW_Q5_1: return launch<LW_Q5_1>(W, out, n, p, stream);
+    case LW_Q5_K: return launch<LW_Q5_K>(W, out, n, p, stream);
+    case LW_Q6_K: return launch<LW_Q6_K>(W, out, n, p, stream);
+    case LW_Q2_K: return launch<LW_Q2_K>(W, out, n, p, stream);
     default: return hipErrorInvalidValue;
     }
 }

@@ -70,7 +70,7 @@ struct Traits<LW_F16> {
     struct Packet {
         uint4 c;
     };
-    __device__ static Packet load(const uint8_t* W, int64_t e, int64_t, int64_t) {
+    __device__ static Packet load(const uint8_t* W, int64_t e, int64_t, int64_t, int64_t = 0) {
         Packet p;
         p.c = *reinterpret_cast<const uint4*>(W + 2 * e);
         return p;
@@ -82,7 +82,8 @@ struct Traits<LW_F16> {
         uint32_t c;
     };
     __device__ static Base base(uint32_t row, uint32_t K, uint32_t c) { return {row * (2u * K) + 1024u * c}; }
-    __device__ static Packet load_at(const uint8_t* W, const uint8_t*, const uint8_t*, const Base& b, uint32_t la) {
+    __device__ static Packet load_at(const uint8_t* W, const uint8_t*, const uint8_t*, const Base& b, uint32_t la,
+                                     const uint8_t* = nullptr) {
         Packet p;
         p.c = stream_load16(W + b.c + 16u * la);
         return p;
@@ -109,7 +110,7 @@ struct Traits<LW_Q8_0> {
         uint4 c;
         uint32_t d;
     };
-    __device__ static Packet load(const uint8_t* W, int64_t e, int64_t off1, int64_t) {
+    __device__ static Packet load(const uint8_t* W, int64_t e, int64_t off1, int64_t, int64_t = 0) {
         Packet p;
         p.c = *reinterpret_cast<const uint4*>(W + e);
         p.d = *reinterpret_cast<const uint16_t*>(W + off1 + 2 * (e >> 5));
@@ -122,7 +123,7 @@ struct Traits<LW_Q8_0> {
         return {row * K + 1024u * c, row * (K / 16u) + 64u * c};
     }
     __device__ static Packet load_at(const uint8_t* W, const uint8_t* P1, const uint8_t*, const Base& b,
-                                     uint32_t la) {
+                                     uint32_t la, const uint8_t* = nullptr) {
         Packet p;
         p.c = stream_load16(W + b.c + 16u * la);
         p.d = *reinterpret_cast<const uint16_t*>(P1 + b.d + 2u * (la >> 1));
@@ -183,7 +184,7 @@ struct Traits<LW_Q4_0> {
         uint4 c;
         uint32_t d;
     };
-    __device__ static Packet load(const uint8_t* W, int64_t e, int64_t off1, int64_t) {
+    __device__ static Packet load(const uint8_t* W, int64_t e, int64_t off1, int64_t, int64_t = 0) {
         Packet p;
         p.c = *reinterpret_cast<const uint4*>(W + (e >> 1));
         p.d = *reinterpret_cast<const uint16_t*>(W + off1 + 2 * (e >> 5));
@@ -196,7 +197,7 @@ struct Traits<LW_Q4_0> {
         return {row * (K / 2u) + 1024u * c, row * (K / 16u) + 128u * c};
     }
     __device__ static Packet load_at(const uint8_t* W, const uint8_t* P1, const uint8_t*, const Base& b,
-                                     uint32_t la) {
+                                     uint32_t la, const uint8_t* = nullptr) {
         Packet p;
         p.c = stream_load16(W + b.c + 16u * la);
         p.d = *reinterpret_cast<const uint16_t*>(P1 + b.d + 2u * la);
@@ -217,7 +218,7 @@ struct Traits<LW_Q4_1> {
         uint4 c;
         uint32_t dm;  // d in bits 0..15, m in bits 16..31
     };
-    __device__ static Packet load(const uint8_t* W, int64_t e, int64_t off1, int64_t) {
+    __device__ static Packet load(const uint8_t* W, int64_t e, int64_t off1, int64_t, int64_t = 0) {
         Packet p;
         p.c = *reinterpret_cast<const uint4*>(W + (e >> 1));
         p.dm = *reinterpret_cast<const uint32_t*>(W + off1 + 4 * (e >> 5));
@@ -230,7 +231,7 @@ struct Traits<LW_Q4_1> {
         return {row * (K / 2u) + 1024u * c, row * (K / 8u) + 256u * c};
     }
     __device__ static Packet load_at(const uint8_t* W, const uint8_t* P1, const uint8_t*, const Base& b,
-                                     uint32_t la) {
+                                     uint32_t la, const uint8_t* = nullptr) {
         Packet p;
         p.c = stream_load16(W + b.c + 16u * la);
         p.dm = *reinterpret_cast<const uint32_t*>(P1 + b.dm + 4u * la);
@@ -273,7 +274,7 @@ struct Traits<LW_Q1_0> {
         uint32_t b;
         uint32_t d;
     };
-    __device__ static Packet load(const uint8_t* W, int64_t e, int64_t off1, int64_t) {
+    __device__ static Packet load(const uint8_t* W, int64_t e, int64_t off1, int64_t, int64_t = 0) {
         Packet p;
         p.b = *reinterpret_cast<const uint32_t*>(W + (e >> 3));
         p.d = *reinterpret_cast<const uint16_t*>(W + off1 + 2 * (e >> 7));
@@ -286,7 +287,7 @@ struct Traits<LW_Q1_0> {
         return {row * (K / 8u) + 256u * c, row * (K / 64u) + 32u * c};
     }
     __device__ static Packet load_at(const uint8_t* W, const uint8_t* P1, const uint8_t*, const Base& b,
-                                     uint32_t la) {
+                                     uint32_t la, const uint8_t* = nullptr) {
         Packet p;
         p.b = *reinterpret_cast<const uint32_t*>(W + b.c + 4u * la);
         p.d = *reinterpret_cast<const uint16_t*>(P1 + b.d + 2u * (la >> 2));
@@ -306,7 +307,7 @@ struct Traits<LW_Q4_K> {
         uint4 c;
         uint32_t r0, r1, r2, dd;
     };
-    __device__ static Packet load(const uint8_t* W, int64_t e, int64_t off1, int64_t off2) {
+    __device__ static Packet load(const uint8_t* W, int64_t e, int64_t off1, int64_t off2, int64_t = 0) {
         Packet p;
         p.c = *reinterpret_cast<const uint4*>(W + (e >> 1));
         const uint32_t* rec = reinterpret_cast<const uint32_t*>(W + off1 + 12 * (e >> 8));
@@ -323,7 +324,7 @@ struct Traits<LW_Q4_K> {
         return {row * (K / 2u) + 1024u * c, row * (12u * (K / 256u)) + 96u * c, row * (4u * (K / 256u)) + 32u * c};
     }
     __device__ static Packet load_at(const uint8_t* W, const uint8_t* P1, const uint8_t* P2, const Base& b,
-                                     uint32_t la) {
+                                     uint32_t la, const uint8_t* = nullptr) {
         Packet p;
         p.c = stream_load16(W + b.c + 16u * la);
         const uint32_t* rec = reinterpret_cast<const uint32_t*>(P1 + b.rec + 12u * (la >> 3));
@@ -348,6 +349,291 @@ struct Traits<LW_Q4_K> {
         const float ds = half_bits_to_float(p.dd & 0xFFFFu) * sc;
         const float dm = half_bits_to_float(p.dd >> 16) * m;
         return __builtin_fmaf(ds, nibble_dot(p.c, xv), -dm * sx);
+    }
+};
+
+// ---- 5-bit, 6-bit and 2-bit formats ------------------------------------
+// Each lane holds one 32-element group, as for the 4-bit formats: the low
+// four bits of 5- and 6-bit codes come from the Q4 nibble plane, the high
+// bits from a plane of their own; every product is a v_fma_mix_f32 on a code
+// field masked into a binary16 subnormal.
+
+// 8-byte load of weight data read once (non-temporal).
+__device__ __forceinline__ uint2 stream_load8(const uint8_t* p) {
+    typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+    const u32x2 v = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
+    return make_uint2(v.x, v.y);
+}
+
+// sum over the lane's 32 elements of q*x for the low nibbles, split into
+// elements 0..15 (sa) and 16..31 (sb), each in true units
+__device__ __forceinline__ void nibble_dot2(const uint4& c, const float4* xv, float& sa, float& sb) {
+    const uint32_t w[4] = {c.x, c.y, c.z, c.w};
+    float lo_s = 0.f, hi_s = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const uint32_t l02 = opaque(w[i] & 0x000F000Fu);
+        const uint32_t h02 = opaque(w[i] & 0x00F000F0u);
+        const uint32_t l13 = opaque((w[i] >> 8) & 0x000F000Fu);
+        const uint32_t h13 = opaque((w[i] >> 8) & 0x00F000F0u);
+        lo_s = __builtin_fmaf(half_of<0>(l02), xv[i].x, lo_s);
+        lo_s = __builtin_fmaf(half_of<1>(l02), xv[i].z, lo_s);
+        lo_s = __builtin_fmaf(half_of<0>(l13), xv[i].y, lo_s);
+        lo_s = __builtin_fmaf(half_of<1>(l13), xv[i].w, lo_s);
+        hi_s = __builtin_fmaf(half_of<0>(h02), xv[4 + i].x, hi_s);
+        hi_s = __builtin_fmaf(half_of<1>(h02), xv[4 + i].z, hi_s);
+        hi_s = __builtin_fmaf(half_of<0>(h13), xv[4 + i].y, hi_s);
+        hi_s = __builtin_fmaf(half_of<1>(h13), xv[4 + i].w, hi_s);
+    }
+    sa = lo_s * 16777216.0f;  // 2^24
+    sb = hi_s * 1048576.0f;   // 2^20: high nibbles read as 16q
+}
+
+// sum of q*x over 16 elements whose 2-bit fields fill one 32-bit word
+// (element j at bits 2j); x4 points at their 4 float4s. (w >> 2j) masked
+// with 0x00030003 holds element j in the low half and element 8 + j in the
+// high half.
+__device__ __forceinline__ float two_bit_dot(uint32_t w, const float4* x4) {
+    float a = 0.f, b = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const uint32_t m = opaque((w >> (2 * j)) & 0x00030003u);
+        const float4& xl = x4[j >> 2];
+        const float4& xh = x4[2 + (j >> 2)];
+        const float vl = (j & 3) == 0 ? xl.x : (j & 3) == 1 ? xl.y : (j & 3) == 2 ? xl.z : xl.w;
+        const float vh = (j & 3) == 0 ? xh.x : (j & 3) == 1 ? xh.y : (j & 3) == 2 ? xh.z : xh.w;
+        a = __builtin_fmaf(half_of<0>(m), vl, a);
+        b = __builtin_fmaf(half_of<1>(m), vh, b);
+    }
+    return (a + b) * 16777216.0f;  // 2^24
+}
+
+// sum of the 16 elements in 4 float4s
+__device__ __forceinline__ float sum16(const float4* x4) {
+    return ((x4[0].x + x4[0].y) + (x4[0].z + x4[0].w)) + ((x4[1].x + x4[1].y) + (x4[1].z + x4[1].w)) +
+           (((x4[2].x + x4[2].y) + (x4[2].z + x4[2].w)) + ((x4[3].x + x4[3].y) + (x4[3].z + x4[3].w)));
+}
+
+// The 6-bit sub-block fields of a K-quant record {r0, r1, r2} (sc_j at bit
+// 6j, m_j at bit 48 + 6j), as floats.
+__device__ __forceinline__ void record_fields(uint32_t r0, uint32_t r1, uint32_t r2, int j, float& sc, float& m) {
+    const uint32_t ts = 6u * (uint32_t)j;
+    const uint32_t tm = 16u + 6u * (uint32_t)j;
+    const bool sl = ts < 32u, ml = tm < 32u;
+    const uint32_t sc_w = __builtin_amdgcn_alignbit(sl ? r1 : 0u, sl ? r0 : r1, ts & 31u);
+    const uint32_t m_w = __builtin_amdgcn_alignbit(ml ? r2 : 0u, ml ? r1 : r2, tm & 31u);
+    sc = (float)(sc_w & 63u);
+    m = (float)(m_w & 63u);
+}
+
+// Q5_0: value d * (q - 16), q = nibble + 16 * fifth bit.
+template <>
+struct Traits<LW_Q5_0> {
+    static constexpr int EPL = 32;
+    static constexpr bool kGroupSums = true;
+    struct Packet {
+        uint4 c;
+        uint32_t h, d;
+    };
+    __device__ static Packet load(const uint8_t* W, int64_t e, int64_t off1, int64_t off2, int64_t = 0) {
+        Packet p;
+        p.c = *reinterpret_cast<const uint4*>(W + (e >> 1));
+        p.h = *reinterpret_cast<const uint32_t*>(W + off1 + (e >> 3));
+        p.d = *reinterpret_cast<const uint16_t*>(W + off2 + 2 * (e >> 5));
+        return p;
+    }
+    struct Base {
+        uint32_t c, h, d;
+    };
+    __device__ static Base base(uint32_t row, uint32_t K, uint32_t c) {  // chunk = 2048 elements
+        return {row * (K / 2u) + 1024u * c, row * (K / 8u) + 256u * c, row * (K / 16u) + 128u * c};
+    }
+    __device__ static Packet load_at(const uint8_t* W, const uint8_t* P1, const uint8_t* P2, const Base& b,
+                                     uint32_t la, const uint8_t* = nullptr) {
+        Packet p;
+        p.c = stream_load16(W + b.c + 16u * la);
+        p.h = *reinterpret_cast<const uint32_t*>(P1 + b.h + 4u * la);
+        p.d = *reinterpret_cast<const uint16_t*>(P2 + b.d + 2u * la);
+        return p;
+    }
+    // d * (sum q*x - 16 * sum x)
+    __device__ static float dot(const Packet& p, const float4* xv, float sx, int) {
+        const float q = __builtin_fmaf(16.0f, bit_dot(p.h, xv), nibble_dot(p.c, xv));
+        return half_bits_to_float(p.d) * __builtin_fmaf(-16.0f, sx, q);
+    }
+};
+
+// Q5_1: value d * q + m.
+template <>
+struct Traits<LW_Q5_1> {
+    static constexpr int EPL = 32;
+    static constexpr bool kGroupSums = true;
+    struct Packet {
+        uint4 c;
+        uint32_t h, dm;
+    };
+    __device__ static Packet load(const uint8_t* W, int64_t e, int64_t off1, int64_t off2, int64_t = 0) {
+        Packet p;
+        p.c = *reinterpret_cast<const uint4*>(W + (e >> 1));
+        p.h = *reinterpret_cast<const uint32_t*>(W + off1 + (e >> 3));
+        p.dm = *reinterpret_cast<const uint32_t*>(W + off2 + 4 * (e >> 5));
+        return p;
+    }
+    struct Base {
+        uint32_t c, h, dm;
+    };
+    __device__ static Base base(uint32_t row, uint32_t K, uint32_t c) {
+        return {row * (K / 2u) + 1024u * c, row * (K / 8u) + 256u * c, row * (K / 8u) + 256u * c};
+    }
+    __device__ static Packet load_at(const uint8_t* W, const uint8_t* P1, const uint8_t* P2, const Base& b,
+                                     uint32_t la, const uint8_t* = nullptr) {
+        Packet p;
+        p.c = stream_load16(W + b.c + 16u * la);
+        p.h = *reinterpret_cast<const uint32_t*>(P1 + b.h + 4u * la);
+        p.dm = *reinterpret_cast<const uint32_t*>(P2 + b.dm + 4u * la);
+        return p;
+    }
+    // d * sum q*x + m * sum x
+    __device__ static float dot(const Packet& p, const float4* xv, float sx, int) {
+        const float q = __builtin_fmaf(16.0f, bit_dot(p.h, xv), nibble_dot(p.c, xv));
+        return __builtin_fmaf(half_bits_to_float(p.dm >> 16), sx, half_bits_to_float(p.dm & 0xFFFFu) * q);
+    }
+};
+
+// Q5_K-style: value d*sc_j*q - dmin*m_j with 5-bit q.
+template <>
+struct Traits<LW_Q5_K> {
+    static constexpr int EPL = 32;
+    static constexpr bool kGroupSums = true;
+    struct Packet {
+        uint4 c;
+        uint32_t h, r0, r1, r2, dd;
+    };
+    __device__ static Packet load(const uint8_t* W, int64_t e, int64_t off1, int64_t off2, int64_t off3 = 0) {
+        Packet p;
+        p.c = *reinterpret_cast<const uint4*>(W + (e >> 1));
+        p.h = *reinterpret_cast<const uint32_t*>(W + off1 + (e >> 3));
+        const uint32_t* rec = reinterpret_cast<const uint32_t*>(W + off2 + 12 * (e >> 8));
+        p.r0 = rec[0];
+        p.r1 = rec[1];
+        p.r2 = rec[2];
+        p.dd = *reinterpret_cast<const uint32_t*>(W + off3 + 4 * (e >> 8));
+        return p;
+    }
+    struct Base {
+        uint32_t c, h, rec, dd;
+    };
+    __device__ static Base base(uint32_t row, uint32_t K, uint32_t c) {
+        return {row * (K / 2u) + 1024u * c, row * (K / 8u) + 256u * c, row * (12u * (K / 256u)) + 96u * c,
+                row * (4u * (K / 256u)) + 32u * c};
+    }
+    __device__ static Packet load_at(const uint8_t* W, const uint8_t* P1, const uint8_t* P2, const Base& b,
+                                     uint32_t la, const uint8_t* P3 = nullptr) {
+        Packet p;
+        p.c = stream_load16(W + b.c + 16u * la);
+        p.h = *reinterpret_cast<const uint32_t*>(P1 + b.h + 4u * la);
+        const uint32_t* rec = reinterpret_cast<const uint32_t*>(P2 + b.rec + 12u * (la >> 3));
+        p.r0 = rec[0];
+        p.r1 = rec[1];
+        p.r2 = rec[2];
+        p.dd = *reinterpret_cast<const uint32_t*>(P3 + b.dd + 4u * (la >> 3));
+        return p;
+    }
+    __device__ static float dot(const Packet& p, const float4* xv, float sx, int j) {
+        float sc, m;
+        record_fields(p.r0, p.r1, p.r2, j, sc, m);
+        const float ds = half_bits_to_float(p.dd & 0xFFFFu) * sc;
+        const float dm = half_bits_to_float(p.dd >> 16) * m;
+        const float q = __builtin_fmaf(16.0f, bit_dot(p.h, xv), nibble_dot(p.c, xv));
+        return __builtin_fmaf(ds, q, -dm * sx);
+    }
+};
+
+// Q6_K-style: value d*sc_t*(q - 32), sub-blocks of 16 (a lane's group is two).
+template <>
+struct Traits<LW_Q6_K> {
+    static constexpr int EPL = 32;
+    static constexpr bool kGroupSums = true;
+    struct Packet {
+        uint4 c;
+        uint2 h;
+        uint32_t sc, d;
+    };
+    __device__ static Packet load(const uint8_t* W, int64_t e, int64_t off1, int64_t off2, int64_t off3 = 0) {
+        Packet p;
+        p.c = *reinterpret_cast<const uint4*>(W + (e >> 1));
+        p.h = *reinterpret_cast<const uint2*>(W + off1 + (e >> 2));
+        p.sc = *reinterpret_cast<const uint16_t*>(W + off2 + (e >> 4));
+        p.d = *reinterpret_cast<const uint16_t*>(W + off3 + 2 * (e >> 8));
+        return p;
+    }
+    struct Base {
+        uint32_t c, h, sc, d;
+    };
+    __device__ static Base base(uint32_t row, uint32_t K, uint32_t c) {
+        return {row * (K / 2u) + 1024u * c, row * (K / 4u) + 512u * c, row * (K / 16u) + 128u * c,
+                row * (2u * (K / 256u)) + 16u * c};
+    }
+    __device__ static Packet load_at(const uint8_t* W, const uint8_t* P1, const uint8_t* P2, const Base& b,
+                                     uint32_t la, const uint8_t* P3 = nullptr) {
+        Packet p;
+        p.c = stream_load16(W + b.c + 16u * la);
+        p.h = stream_load8(P1 + b.h + 8u * la);
+        p.sc = *reinterpret_cast<const uint16_t*>(P2 + b.sc + 2u * la);
+        p.d = *reinterpret_cast<const uint16_t*>(P3 + b.d + 2u * (la >> 3));
+        return p;
+    }
+    // d * sum over the two sub-blocks of sc_t * (sum q*x - 32 * sum x)
+    __device__ static float dot(const Packet& p, const float4* xv, float sx, int) {
+        float la, lb;
+        nibble_dot2(p.c, xv, la, lb);
+        const float qa = __builtin_fmaf(16.0f, two_bit_dot(p.h.x, xv), la);
+        const float qb = __builtin_fmaf(16.0f, two_bit_dot(p.h.y, xv + 4), lb);
+        const float sxa = sum16(xv), sxb = sx - sxa;
+        const float sca = (float)(int32_t)(int8_t)(p.sc & 0xFFu);
+        const float scb = (float)(int32_t)(int8_t)(p.sc >> 8);
+        const float t = sca * __builtin_fmaf(-32.0f, sxa, qa);
+        return half_bits_to_float(p.d) * __builtin_fmaf(scb, __builtin_fmaf(-32.0f, sxb, qb), t);
+    }
+};
+
+// Q2_K-style: value d*sc_t*q - dmin*m_t with 2-bit q, sub-blocks of 16.
+template <>
+struct Traits<LW_Q2_K> {
+    static constexpr int EPL = 32;
+    static constexpr bool kGroupSums = true;
+    struct Packet {
+        uint2 c;
+        uint32_t scm, dd;
+    };
+    __device__ static Packet load(const uint8_t* W, int64_t e, int64_t off1, int64_t off2, int64_t = 0) {
+        Packet p;
+        p.c = *reinterpret_cast<const uint2*>(W + (e >> 2));
+        p.scm = *reinterpret_cast<const uint16_t*>(W + off1 + (e >> 4));
+        p.dd = *reinterpret_cast<const uint32_t*>(W + off2 + 4 * (e >> 8));
+        return p;
+    }
+    struct Base {
+        uint32_t c, scm, dd;
+    };
+    __device__ static Base base(uint32_t row, uint32_t K, uint32_t c) {
+        return {row * (K / 4u) + 512u * c, row * (K / 16u) + 128u * c, row * (4u * (K / 256u)) + 32u * c};
+    }
+    __device__ static Packet load_at(const uint8_t* W, const uint8_t* P1, const uint8_t* P2, const Base& b,
+                                     uint32_t la, const uint8_t* = nullptr) {
+        Packet p;
+        p.c = stream_load8(W + b.c + 8u * la);
+        p.scm = *reinterpret_cast<const uint16_t*>(P1 + b.scm + 2u * la);
+        p.dd = *reinterpret_cast<const uint32_t*>(P2 + b.dd + 4u * (la >> 3));
+        return p;
+    }
+    __device__ static float dot(const Packet& p, const float4* xv, float sx, int) {
+        const float qa = two_bit_dot(p.c.x, xv), qb = two_bit_dot(p.c.y, xv + 4);
+        const float sxa = sum16(xv), sxb = sx - sxa;
+        const float d = half_bits_to_float(p.dd & 0xFFFFu), dmin = half_bits_to_float(p.dd >> 16);
+        const float dsa = d * (float)(p.scm & 15u), dma = dmin * (float)((p.scm >> 4) & 15u);
+        const float dsb = d * (float)((p.scm >> 8) & 15u), dmb = dmin * (float)((p.scm >> 12) & 15u);
+        return __builtin_fmaf(dsa, qa, -dma * sxa) + __builtin_fmaf(dsb, qb, -dmb * sxb);
     }
 };
 
@@ -554,7 +840,7 @@ __device__ __forceinline__ float rows_sum(const float* acc) {
 template <int FMT, int NT, int R, int NW>
 __global__ void __launch_bounds__(NW * kWave)
     gemv_kernel(const uint8_t* __restrict__ W, const float* __restrict__ x, float* __restrict__ y,
-                int64_t M, int64_t K, int KT, int64_t off1, int64_t off2) {
+                int64_t M, int64_t K, int KT, int64_t off1, int64_t off2, int64_t off3) {
     using T = Traits<FMT>;
     constexpr int EPL = T::EPL;
     constexpr int J4 = EPL / 4;  // float4s of x per lane per chunk
@@ -619,7 +905,7 @@ __global__ void __launch_bounds__(NW * kWave)
                 const int64_t kk = k0 + kl;
                 typename T::Packet pk[R];
 #pragma unroll
-                for (int r = 0; r < R; ++r) pk[r] = T::load(W, rows[r] * K + kk, off1, off2);
+                for (int r = 0; r < R; ++r) pk[r] = T::load(W, rows[r] * K + kk, off1, off2, off3);
                 const int j = (int)((kk >> 5) & 7);
 #pragma unroll
                 for (int t = 0; t < NT; ++t) {
@@ -707,7 +993,7 @@ __global__ void __launch_bounds__(NW * kWave)
             const int si = seg_of(sg, row);
             const uint8_t* Ws = sg.W[si];
             pk[r] = T::load_at(Ws, Ws + sg.off1[si], Ws + sg.off2[si],
-                               T::base((uint32_t)(row - sg.start[si]), K32, cc), la);
+                               T::base((uint32_t)(row - sg.start[si]), K32, cc), la, Ws + sg.off3[si]);
         }
         if (++ic == nc) {
             ic = 0;
@@ -999,7 +1285,7 @@ hipError_t launch_nt(const uint8_t* W, const float* x, float* y, int64_t M, int6
     const int64_t blocks = (M + (int64_t)NW * R - 1) / ((int64_t)NW * R);
     if (query_only(kernel_name<Name_gemv_kernel, FMT, NT, R, NW>())) return hipSuccess;
     hipLaunchKernelGGL((gemv_kernel<FMT, NT, R, NW>), dim3((unsigned)blocks, (unsigned)ntb), dim3(NW * kWave), lds,
-                       stream, W, x, y, M, K, (int)KT, p.off1, p.off2);
+                       stream, W, x, y, M, K, (int)KT, p.off1, p.off2, p.off3);
     return hipGetLastError();
 }
 
@@ -1030,6 +1316,7 @@ inline RowSegs<1> one_seg(const uint8_t* W, float* y, int64_t M, const Planes& p
     sg.y[0] = y;
     sg.off1[0] = p.off1;
     sg.off2[0] = p.off2;
+    sg.off3[0] = p.off3;
     sg.start[0] = 0;
     sg.M[0] = M;
     return sg;
@@ -1155,6 +1442,7 @@ hipError_t launch_multi_ns(int n, const uint8_t* const* W, float* const* y, cons
         sg.y[i] = used ? y[i] : y[0];
         sg.off1[i] = p.off1;
         sg.off2[i] = p.off2;
+        sg.off3[i] = p.off3;
         sg.start[i] = used ? tot : INT64_MAX;
         sg.M[i] = used ? M[i] : 0;
         if (used) {
@@ -1217,6 +1505,11 @@ hipError_t launch_gemv_multi(int fmt, int n, const uint8_t* const* W, float* con
     case LW_Q4_K: return launch_multi_fmt<LW_Q4_K>(n, W, y, M, x, K, stream);
     case LW_Q4_1: return launch_multi_fmt<LW_Q4_1>(n, W, y, M, x, K, stream);
     case LW_Q1_0: return launch_multi_fmt<LW_Q1_0>(n, W, y, M, x, K, stream);
+    case LW_Q5_0: return launch_multi_fmt<LW_Q5_0>(n, W, y, M, x, K, stream);
+    case LW_Q5_1: return launch_multi_fmt<LW_Q5_1>(n, W, y, M, x, K, stream);
+    case LW_Q5_K: return launch_multi_fmt<LW_Q5_K>(n, W, y, M, x, K, stream);
+    case LW_Q6_K: return launch_multi_fmt<LW_Q6_K>(n, W, y, M, x, K, stream);
+    case LW_Q2_K: return launch_multi_fmt<LW_Q2_K>(n, W, y, M, x, K, stream);
     default: return hipErrorInvalidValue;
     }
 }
@@ -1260,6 +1553,11 @@ hipError_t launch_gemv_blocks(int fmt, const uint8_t* W, const float* x, float* 
     case LW_Q4_K: return launch_blocks_fmt<LW_Q4_K>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q4_1: return launch_blocks_fmt<LW_Q4_1>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q1_0: return launch_blocks_fmt<LW_Q1_0>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q5_0: return launch_blocks_fmt<LW_Q5_0>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q5_1: return launch_blocks_fmt<LW_Q5_1>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q5_K: return launch_blocks_fmt<LW_Q5_K>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q6_K: return launch_blocks_fmt<LW_Q6_K>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q2_K: return launch_blocks_fmt<LW_Q2_K>(W, x, y, M, K, n_tok, p, stream);
     default: return hipErrorInvalidValue;
     }
 }
@@ -1273,6 +1571,11 @@ hipError_t launch_gemv(int fmt, const uint8_t* W, const float* x, float* y, int6
     case LW_Q4_K: return launch_fmt<LW_Q4_K>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q4_1: return launch_fmt<LW_Q4_1>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q1_0: return launch_fmt<LW_Q1_0>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q5_0: return launch_fmt<LW_Q5_0>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q5_1: return launch_fmt<LW_Q5_1>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q5_K: return launch_fmt<LW_Q5_K>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q6_K: return launch_fmt<LW_Q6_K>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q2_K: return launch_fmt<LW_Q2_K>(W, x, y, M, K, n_tok, p, stream);
     default: return hipErrorInvalidValue;
     }
 }

@@ -17,7 +17,7 @@
 namespace {
 
 bool known_fmt(int fmt) {
-    return fmt == LW_F16 || fmt == LW_Q8_0 || fmt == LW_Q4_0 || fmt == LW_Q4_K || fmt == LW_Q4_1 || fmt == LW_Q1_0;
+    return fmt >= LW_F16 && fmt <= LW_Q2_K;
 }
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }

@@ -47,11 +47,11 @@ const char* kernel_name() {
     return s.c_str();
 }
 
-// Byte offsets of planes 1 and 2 and the total size of n packed elements of
+// Byte offsets of planes 1, 2 and 3 and the total size of n packed elements of
 // fmt (split-plane layout: later planes start at the end of the previous one
 // rounded up to 256 bytes). n must already be valid for fmt.
 struct Planes {
-    int64_t off1 = 0, off2 = 0, total = 0;
+    int64_t off1 = 0, off2 = 0, off3 = 0, total = 0;
 };
 
 inline int64_t round_up_256(int64_t v) { return (v + 255) / 256 * 256; }
@@ -83,6 +83,29 @@ inline Planes planes_of(int fmt, int64_t n) {
         p.off2 = round_up_256(p.off1 + 12 * (n / 256));
         p.total = p.off2 + 4 * (n / 256);
         break;
+    case LW_Q5_0:
+    case LW_Q5_1:
+        p.off1 = round_up_256(n / 2);
+        p.off2 = round_up_256(p.off1 + n / 8);
+        p.total = p.off2 + (fmt == LW_Q5_0 ? 2 : 4) * (n / 32);
+        break;
+    case LW_Q5_K:
+        p.off1 = round_up_256(n / 2);
+        p.off2 = round_up_256(p.off1 + n / 8);
+        p.off3 = round_up_256(p.off2 + 12 * (n / 256));
+        p.total = p.off3 + 4 * (n / 256);
+        break;
+    case LW_Q6_K:
+        p.off1 = round_up_256(n / 2);
+        p.off2 = round_up_256(p.off1 + n / 4);
+        p.off3 = round_up_256(p.off2 + n / 16);
+        p.total = p.off3 + 2 * (n / 256);
+        break;
+    case LW_Q2_K:
+        p.off1 = round_up_256(n / 4);
+        p.off2 = round_up_256(p.off1 + n / 16);
+        p.total = p.off2 + 4 * (n / 256);
+        break;
     default:
         break;
     }
@@ -100,7 +123,7 @@ template <int NS>
 struct RowSegs {
     const uint8_t* W[NS];
     float* y[NS];
-    int64_t off1[NS], off2[NS], start[NS], M[NS], wg0[NS];
+    int64_t off1[NS], off2[NS], off3[NS], start[NS], M[NS], wg0[NS];
 };
 
 // Kernel launchers. Arguments are already validated; each returns the

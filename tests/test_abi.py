@@ -8,7 +8,7 @@ import re
 import pytest
 
 import golden_io
-from paper_2605_20706_amd import binding
+from paper_2605_20706_amd import binding, layout
 from paper_2605_20706_amd.layout import F16, Q1_0, Q4_0, Q4_1, Q4_K, Q8_0
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -59,10 +59,12 @@ def test_exports_only_the_c_abi(lib):
 def test_weight_bytes_matches_hand_sizes(lib):
     for name, n, _, _, total in golden_io.plane_sizes():
         assert lib.lw_weight_bytes(FMT[name], n) == total
+    for name, n, _, _, _, total in golden_io.plane_sizes4():
+        assert lib.lw_weight_bytes(layout.FORMATS[name], n) == total
 
 
 def test_weight_bytes_errors(lib):
-    assert lib.lw_weight_bytes(7, 256) == LW_EFMT
+    assert lib.lw_weight_bytes(11, 256) == LW_EFMT
     assert lib.lw_weight_bytes(Q4_0, -256) == LW_EINVAL
     assert lib.lw_weight_bytes(Q4_0, 100) == LW_ESHAPE
     assert lib.lw_weight_bytes(Q4_0, (1 << 40) + 256) == LW_EINVAL
@@ -74,7 +76,7 @@ def mv(lib, fmt=Q4_0, W=A256, x=A16, y=A16, M=4, K=256, n_tok=1):
 
 
 def test_matvec_error_order(lib):
-    assert mv(lib, fmt=6, W=None) == LW_EFMT          # format first
+    assert mv(lib, fmt=11, W=None) == LW_EFMT          # format first
     assert mv(lib, fmt=-1) == LW_EFMT
     assert mv(lib, W=None) == LW_EINVAL
     assert mv(lib, x=None) == LW_EINVAL
@@ -102,7 +104,7 @@ def mvm(lib, fmt=Q4_0, Ws=(A256, A256 + 4096), ys=(A16, A16 + 4096), Ms=(4, 8), 
 def test_matvec_multi_error_order(lib):
     """lw_matvec_multi checks as lw_matvec does, over all matrices, in the same
     order (no call here reaches a launch)."""
-    assert mvm(lib, fmt=6, x=None) == LW_EFMT
+    assert mvm(lib, fmt=11, x=None) == LW_EFMT
     assert mvm(lib, x=None) == LW_EINVAL
     assert mvm(lib, n=0) == LW_EINVAL
     assert mvm(lib, n=binding.LW_MULTI_MAX + 1) == LW_EINVAL
@@ -139,7 +141,7 @@ def test_kernel_name_multi(lib):
 
 
 def test_dequant_errors(lib):
-    assert lib.lw_dequant(9, A256, A16, 256) == LW_EFMT
+    assert lib.lw_dequant(11, A256, A16, 256) == LW_EFMT
     assert lib.lw_dequant(Q4_K, None, A16, 256) == LW_EINVAL
     assert lib.lw_dequant(Q4_K, A256, None, 256) == LW_EINVAL
     assert lib.lw_dequant(Q4_K, A256, A16, -256) == LW_EINVAL
@@ -166,7 +168,7 @@ def test_binding_fails_loudly_without_gpu_tensors(lib):
 
 
 def test_kernel_name_rejects_what_matvec_rejects(lib):
-    assert binding.kernel_name(7, 4, 256, 1) is None           # format
+    assert binding.kernel_name(11, 4, 256, 1) is None           # format
     assert binding.kernel_name(Q4_0, 0, 256, 1) is None        # sizes
     assert binding.kernel_name(Q4_0, 4, 256, 0) is None
     assert binding.kernel_name(Q4_0, 4, 300, 1) is None        # shape
@@ -267,12 +269,12 @@ def test_launch_count(lib):
     assert binding.launch_count_multi(Q4_K, [14336, 14336], 4096, 2) == 2   # one per matrix
     assert binding.launch_count_multi(Q4_0, [14336, 14336], 4096, 4) == 1
     f = lib.lw_launch_count
-    assert f(9, 4, 256, 1) == LW_EFMT
+    assert f(11, 4, 256, 1) == LW_EFMT
     assert f(Q4_0, 0, 256, 1) == LW_EINVAL
     assert f(Q4_0, 4, 300, 1) == LW_ESHAPE
     g = lib.lw_launch_count_multi
     Ms = (ctypes.c_int64 * 2)(4, 8)
     assert g(Q4_0, 0, Ms, 256, 1) == LW_EINVAL
     assert g(Q4_0, 2, None, 256, 1) == LW_EINVAL
-    assert g(9, 2, Ms, 256, 1) == LW_EFMT
+    assert g(11, 2, Ms, 256, 1) == LW_EFMT
     assert g(Q4_0, 2, Ms, 300, 1) == LW_ESHAPE

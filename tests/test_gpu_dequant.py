@@ -5,7 +5,7 @@ import pytest
 
 from gpu_util import gpu_dequant, same_bits_or_both_zero
 from paper_2605_20706_amd import layout, synth
-from paper_2605_20706_amd.layout import F16, Q1_0, Q4_0, Q4_1, Q4_K, Q8_0
+from paper_2605_20706_amd.layout import F16, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
 
 pytestmark = pytest.mark.gpu
 
@@ -91,7 +91,7 @@ def test_q1_0_every_scale_and_signed_zero(oracle_mod):
 
 
 @pytest.mark.parametrize("n", [256, 512 + 256, 4096 * 3 + 256])
-@pytest.mark.parametrize("fmt", [F16, Q8_0, Q4_0, Q4_K, Q4_1, Q1_0])
+@pytest.mark.parametrize("fmt", [F16, Q8_0, Q4_0, Q4_K, Q4_1, Q1_0, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K])
 def test_small_and_ragged(oracle_mod, fmt, n):
     check(oracle_mod, fmt, synth.gen_packed(fmt, n, np.random.default_rng(n + fmt)), n)
 
@@ -102,3 +102,61 @@ def test_config_tensors(oracle_mod, key, idx):
     wl = synth.WORKLOADS[key]
     mat = wl.matrices[idx]
     check(oracle_mod, wl.fmt, synth.gen_matrix(wl, mat), mat.M * mat.K)
+
+
+def test_q5_0_every_code_every_scale(oracle_mod):
+    d = finite_halves()
+    q = np.tile(np.arange(32, dtype=np.uint8), d.size)
+    check(oracle_mod, Q5_0, layout.pack_q5_0(q, d), q.size)
+
+
+def test_q5_1_every_scale_and_tie(oracle_mod):
+    d = finite_halves()
+    m = np.random.default_rng(96).choice(finite_halves(), d.size)
+    q = np.tile(np.arange(32, dtype=np.uint8), d.size)
+    check(oracle_mod, Q5_1, layout.pack_q5_1(q, d, m), q.size)
+    # the golden file's tie: q=17 d=0x5A4E m=0x2678 -> 0x45565C68
+    W = layout.pack_q5_1(np.full(256, 17, np.uint8), np.full(8, 0x5A4E, np.uint16), np.full(8, 0x2678, np.uint16))
+    assert (gpu_dequant(Q5_1, W, 256).view(np.uint32) == 0x45565C68).all()
+
+
+@pytest.mark.parametrize("fmt", [Q5_K, Q2_K])
+def test_k_quants_fuzz_all_finite_scales(oracle_mod, fmt):
+    rng = np.random.default_rng(95 + fmt)
+    nsb = 1 << 14
+    n = 256 * nsb
+    fin = finite_halves()
+    per = 32 if fmt == Q5_K else 16
+    top = 64 if fmt == Q5_K else 16
+    q = rng.integers(0, 32 if fmt == Q5_K else 4, n, dtype=np.uint8)
+    sc = rng.integers(0, top, n // per, dtype=np.uint8)
+    m = rng.integers(0, top, n // per, dtype=np.uint8)
+    pack = layout.pack_q5_k if fmt == Q5_K else layout.pack_q2_k
+    check(oracle_mod, fmt, pack(q, sc, m, rng.choice(fin, nsb), rng.choice(fin, nsb)), n)
+
+
+def test_k_quant_ties(oracle_mod):
+    # golden ties: q5_k q=17 sc=2 m=6 d=0x5A4E dmin=0x2678 -> 0x45D65ACA;
+    # q2_k q=1 sc=11 m=1 d=0x5A4E dmin=0x2678 -> 0x450AB398
+    W = layout.pack_q5_k(np.full(256, 17, np.uint8), np.full(8, 2, np.uint8), np.full(8, 6, np.uint8),
+                         np.array([0x5A4E], np.uint16), np.array([0x2678], np.uint16))
+    assert (gpu_dequant(Q5_K, W, 256).view(np.uint32) == 0x45D65ACA).all()
+    W = layout.pack_q2_k(np.full(256, 1, np.uint8), np.full(16, 11, np.uint8), np.full(16, 1, np.uint8),
+                         np.array([0x5A4E], np.uint16), np.array([0x2678], np.uint16))
+    assert (gpu_dequant(Q2_K, W, 256).view(np.uint32) == 0x450AB398).all()
+
+
+def test_q6_k_every_code_every_scale(oracle_mod):
+    """Every 6-bit code x every int8 scale (three d, one subnormal) and every
+    finite binary16 d for one code and scale: exact values."""
+    for dbits in (0x3C00, 0x2E66, 0x0003):
+        q = np.tile(np.arange(64, dtype=np.uint8), 256 * 16)
+        n = q.size
+        sc = np.resize(np.repeat(np.arange(-128, 128, dtype=np.int16), 4).astype(np.int8), n // 16)
+        check(oracle_mod, Q6_K, layout.pack_q6_k(q, sc, np.full(n // 256, dbits, np.uint16)), n)
+    d = finite_halves()
+    d = np.concatenate([d, d[: (-d.size) % 8]])
+    rng = np.random.default_rng(94)
+    q = rng.integers(0, 64, 256 * d.size, dtype=np.uint8)
+    sc = rng.integers(-128, 128, 16 * d.size).astype(np.int8)
+    check(oracle_mod, Q6_K, layout.pack_q6_k(q, sc, d), q.size)
