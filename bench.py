@@ -537,6 +537,120 @@ def timed_parity(ws, refs, y_timed, n_threads):
             "pass": ok}
 
 
+# Shapes of the selection sweep: (format, n_tok, K, M or (M1, M2) for a
+# fused pair): the Llama-3.2-1B and Llama-3-8B decode shapes (q/k/v, o,
+# gate+up fused, down, lm_head), their tensor-parallel shards over eight GPUs
+# (8B q/k/v 768 x 4096, gate 1792 x 4096, down 4096 x 1792), and the 8B
+# projections at 2 to 32 tokens.
+SWEEP_REG = {1: {2048: (10, 11, 12), 4096: (13, 14, 15, 16, 17), 14336: (18, 19, 20)},
+             2: {2048: (21,), 4096: (22, 25), 8192: (23,), 14336: (24,)}}
+
+
+def sweep_shapes():
+    out = []
+    for fmt in (layout.Q4_0, layout.Q4_K):
+        for K, M in [(2048, 3072), (2048, 2048), (2048, (8192, 8192)), (2048, 8192), (2048, 128256),
+                     (4096, 768), (4096, 1792), (4096, 4096), (4096, 6144), (4096, (14336, 14336)),
+                     (4096, 14336), (4096, 128256), (14336, 4096), (1792, 4096)]:
+            out.append((fmt, 1, K, M))
+        for K, M in [(2048, 8192), (4096, 4096), (4096, 6144), (4096, 14336), (4096, 128256), (14336, 4096)]:
+            for nt in (2, 3, 4, 8, 12, 16, 24, 32):
+                out.append((fmt, nt, K, M))
+    return out
+
+
+def sweep_cands(n_tok, K):
+    if n_tok == 1:
+        return (1,) + SWEEP_REG[1].get(K, ())
+    if n_tok == 2:
+        return SWEEP_REG[2].get(K, ()) + (30, 31)
+    if n_tok <= 8:
+        return (30, 31)
+    if n_tok <= 16:
+        return (31, 32)
+    return (32,)
+
+
+def run_sweep(out_path, n_seq=192, min_bytes=6e8):
+    """Times every candidate of the selection table at each sweep shape (HIP
+    events around n_seq back-to-back launches in one graph, rotating over
+    copies of the weights that together exceed the 256 MB Infinity Cache,
+    behind a device-side sleep) and writes the results as JSON."""
+    import ctypes
+
+    import torch
+
+    lib = binding.library()
+    shapes = []
+    for fmt, nt, K, Mspec in sweep_shapes():
+        Ms = list(Mspec) if isinstance(Mspec, tuple) else [Mspec]
+        Mtot = sum(Ms)
+        x = torch.from_numpy(synth.gen_x_seeded([5, K, nt], K, nt)).to("cuda")
+        base = [torch.from_numpy(synth.gen_packed(fmt, m * K, np.random.default_rng([6, fmt, m, K]))).to("cuda")
+                for m in Ms]
+        nbytes = sum(w.numel() for w in base)
+        reps = max(2, int(-(-min_bytes // nbytes)))
+        Ws = [base] + [[w.clone() for w in base] for _ in range(reps - 1)]
+        ys = [torch.empty((nt, m), dtype=torch.float32, device="cuda") for m in Ms]
+        keep = []
+        calls = []
+        for ws in Ws:
+            if len(Ms) > 1:
+                arr = binding.multi_args([w.data_ptr() for w in ws], [v.data_ptr() for v in ys], Ms)
+                keep.append(arr)
+                calls.append((True, (fmt, len(Ms)) + arr + (x.data_ptr(), K, nt)))
+            else:
+                calls.append((False, (fmt, ws[0].data_ptr(), x.data_ptr(), ys[0].data_ptr(), Ms[0], K, nt)))
+        results, names = [], {}
+        for cand in sweep_cands(nt, K):
+            os.environ["LW_FORCE_CFG"] = str(cand)
+            try:
+                name = (binding.kernel_name_multi(fmt, Ms, K, nt) if len(Ms) > 1
+                        else binding.kernel_name(fmt, Ms[0], K, nt))
+                if name in names:  # the candidate does not take the shape: the same kernel as another
+                    continue
+                stream = torch.cuda.current_stream()
+
+                def run():
+                    s_ = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+                    for i in range(n_seq):
+                        multi, a = calls[i % len(calls)]
+                        rc = lib.lw_matvec_multi(*a, s_) if multi else lib.lw_matvec(*a, s_)
+                        if rc != 0:
+                            raise binding.LwError(rc, "sweep")
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g):
+                    run()
+                g.replay()
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                torch.cuda._sleep(int(2.4e6 * 5))
+                e0.record(stream)
+                g.replay()
+                e1.record(stream)
+                torch.cuda.synchronize()
+                us = e0.elapsed_time(e1) * 1e3 / n_seq
+            finally:
+                del os.environ["LW_FORCE_CFG"]
+            names[name] = cand
+            gbs = (sum(synth.algorithmic_bytes(fmt, m, K, nt) for m in Ms)) / (us * 1e-6) / 1e9
+            results.append({"cand": cand, "kernel": name, "us": round(us, 3), "GB/s": round(gbs, 1)})
+        best = min(results, key=lambda r: r["us"])
+        log("sweep fmt=%d n_tok=%d K=%d M=%s: %s" % (fmt, nt, K, Ms, ", ".join(
+            "%d:%.2fus" % (r["cand"], r["us"]) for r in results)))
+        shapes.append({"fmt": fmt, "n_tok": nt, "K": K, "M": Mtot, "Ms": Ms, "results": results,
+                       "best": best["cand"]})
+        del Ws, base, ys, calls, keep
+        torch.cuda.empty_cache()
+    doc = {"what": "launch duration of every kernel-selection candidate per shape (HIP events, %d back-to-back "
+                   "launches in one graph, weights rotated over copies above 600 MB)" % n_seq,
+           "command": "python bench.py --sweep " + os.path.relpath(out_path, ROOT),
+           "device": torch.cuda.get_device_name(0), "shapes": shapes}
+    with open(out_path, "w") as fh:
+        json.dump(doc, fh, indent=1)
+    print(json.dumps({"sweep": out_path, "shapes": len(shapes)}))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -552,6 +666,9 @@ def main():
                     help="one lw_matvec per matrix (default: a layer's gate and up share one lw_matvec_multi call)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep", metavar="OUT_JSON", default=None,
+                    help="time every kernel-selection candidate at the sweep shapes and write OUT_JSON "
+                         "(the committed copy is profiles/sweep_select.json, which generates the table)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain copy kernel over MIB MiB 20 times (HBM counter calibration)")
     args = ap.parse_args()
@@ -566,6 +683,11 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
     binding.library()  # fails loudly if the HIP library is missing
+
+    if args.sweep:
+        os.environ.pop("LW_FORCE_CFG", None)
+        run_sweep(args.sweep)
+        return
 
     if args.calibrate_copy:
         n = args.calibrate_copy * (1 << 20)

@@ -72,7 +72,10 @@ def _hipcc(srcs, out, verbose):
 
 
 def build(verbose: bool = False) -> str:
-    """Builds liblw.so and libceiling.so; returns the path of liblw.so."""
+    """Builds liblw.so and libceiling.so; returns the path of liblw.so. The
+    kernel-selection table is generated from the committed sweep first."""
+    from . import gen_select
+    gen_select.write()
     _hipcc([CEILING_SRC], CEILING_LIB, verbose)
     return _hipcc(sources(), LIB, verbose)
 

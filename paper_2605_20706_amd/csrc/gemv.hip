@@ -29,6 +29,7 @@
 
 #include "lw_device.hpp"
 #include "lw_internal.hpp"
+#include "select.hpp"
 
 namespace lw {
 namespace {
@@ -1397,6 +1398,77 @@ hipError_t launch_reg(const RowSegs<NS>& sg, const float* x, int64_t M, int64_t 
 // count. With one token the register kernel needs a few rows per wave to pay
 // for staging x whole; below that (and for other K) the LDS kernel, which
 // spreads single chunks over the waves, is faster.
+// A register-kernel candidate of the selection table (select.hpp): the
+// configuration it names when its chunk and token counts match the call,
+// else hipErrorNotSupported.
+template <int FMT, int NS>
+hipError_t launch_reg_cand(int cand, const RowSegs<NS>& sg, const float* x, int64_t M, int64_t K, int64_t n_tok,
+                           int64_t max_total, hipStream_t stream) {
+    if (K % 2048) return hipErrorNotSupported;
+    const int64_t nc = K / 2048;
+    const bool t1 = n_tok == 1, t2 = n_tok == 2 && NS == 1;
+    switch (cand) {
+    case kCandReg1_1x1_G8_D2_C2:
+        if (t1 && nc == 1) return launch_reg<FMT, 1, 1, 1, 8, 2, 2, NS>(sg, x, M, max_total, stream);
+        break;
+    case kCandReg1_1x1_G4_D2_C4:
+        if (t1 && nc == 1) return launch_reg<FMT, 1, 1, 1, 4, 2, 4, NS>(sg, x, M, max_total, stream);
+        break;
+    case kCandReg1_1x1_G8_D3_C2:
+        if (t1 && nc == 1) return launch_reg<FMT, 1, 1, 1, 8, 3, 2, NS>(sg, x, M, max_total, stream);
+        break;
+    case kCandReg1_2x1_G8_D2_C2:
+        if (t1 && nc == 2) return launch_reg<FMT, 1, 2, 1, 8, 2, 2, NS>(sg, x, M, max_total, stream);
+        break;
+    case kCandReg1_1x2_G4_D2_C2:
+        if (t1 && nc == 2) return launch_reg<FMT, 1, 1, 2, 4, 2, 2, NS>(sg, x, M, max_total, stream);
+        break;
+    case kCandReg1_1x2_G8_D2_C1:
+        if (t1 && nc == 2) return launch_reg<FMT, 1, 1, 2, 8, 2, 1, NS>(sg, x, M, max_total, stream);
+        break;
+    case kCandReg1_2x1_G8_D3_C2:
+        if (t1 && nc == 2) return launch_reg<FMT, 1, 2, 1, 8, 3, 2, NS>(sg, x, M, max_total, stream);
+        break;
+    case kCandReg1_2x1_G4_D2_C4:
+        if (t1 && nc == 2) return launch_reg<FMT, 1, 2, 1, 4, 2, 4, NS>(sg, x, M, max_total, stream);
+        break;
+    case kCandReg1_1x7_G2_D2_C1:
+        if (t1 && nc == 7) return launch_reg<FMT, 1, 1, 7, 2, 2, 1, NS>(sg, x, M, max_total, stream);
+        break;
+    case kCandReg1_1x7_G1_D2_C2:
+        if (t1 && nc == 7) return launch_reg<FMT, 1, 1, 7, 1, 2, 2, NS>(sg, x, M, max_total, stream);
+        break;
+    case kCandReg1_1x7_G2_D3_C1:
+        if (t1 && nc == 7) return launch_reg<FMT, 1, 1, 7, 2, 3, 1, NS>(sg, x, M, max_total, stream);
+        break;
+    case kCandReg2_1x1_G8_D2_C2:
+        if (t2 && nc == 1) return launch_reg<FMT, 2, 1, 1, 8, 2, 2, NS>(sg, x, M, max_total, stream);
+        break;
+    case kCandReg2_1x2_G4_D2_C2:
+        if (t2 && nc == 2) return launch_reg<FMT, 2, 1, 2, 4, 2, 2, NS>(sg, x, M, max_total, stream);
+        break;
+    case kCandReg2_1x4_G2_D2_C1:
+        if (t2 && nc == 4) return launch_reg<FMT, 2, 1, 4, 2, 2, 1, NS>(sg, x, M, max_total, stream);
+        break;
+    case kCandReg2_1x7_G2_D2_C1:
+        if (t2 && nc == 7) return launch_reg<FMT, 2, 1, 7, 2, 2, 1, NS>(sg, x, M, max_total, stream);
+        break;
+    case kCandReg2_1x2_G8_D2_C1:
+        if (t2 && nc == 2) return launch_reg<FMT, 2, 1, 2, 8, 2, 1, NS>(sg, x, M, max_total, stream);
+        break;
+    default:
+        break;
+    }
+    return hipErrorNotSupported;
+}
+
+// Kernel selection for the register kernel over the 4-bit formats, by token
+// count, the number of 2048-element chunks per row (K / 2048) and the row
+// count: the swept table's candidate where it names one for the shape (the
+// LDS candidate: hipErrorNotSupported, so the caller takes the LDS kernel),
+// else the built-in rules. With one token the register kernel needs a few
+// rows per wave to pay for staging x whole; below that (and for other K) the
+// LDS kernel, which spreads single chunks over the waves, is faster.
 template <int FMT, int NS>
 hipError_t launch_reg_segs(const RowSegs<NS>& sg, const float* x, int64_t M, int64_t K, int64_t n_tok,
                            int64_t max_total, hipStream_t stream) {
@@ -1408,18 +1480,25 @@ hipError_t launch_reg_segs(const RowSegs<NS>& sg, const float* x, int64_t M, int
         if (nc == 1 && n_tok == 1) return launch_reg<FMT, 1, 1, 1, 8, 4, 2, NS>(sg, x, M, max_total, stream);
         if (nc == 1 && n_tok == 2 && NS == 1) return launch_reg<FMT, 2, 1, 1, 8, 4, 2, NS>(sg, x, M, max_total, stream);
         return hipErrorNotSupported;
+    } else {
+        const int cand = select_cand(FMT, M, K, n_tok);
+        if (cand == kCandLds) return hipErrorNotSupported;
+        if (is_reg_cand(cand)) {
+            const hipError_t err = launch_reg_cand<FMT, NS>(cand, sg, x, M, K, n_tok, max_total, stream);
+            if (err != hipErrorNotSupported) return err;
+        }
+        if (n_tok == 1) {
+            if (nc == 1) return launch_reg<FMT, 1, 1, 1, 8, 2, 2, NS>(sg, x, M, max_total, stream);
+            if (nc == 2 && M >= 10240) return launch_reg<FMT, 1, 2, 1, 8, 2, 2, NS>(sg, x, M, max_total, stream);
+            if (nc == 7) return launch_reg<FMT, 1, 1, 7, 2, 2, 1, NS>(sg, x, M, max_total, stream);
+        } else if (n_tok == 2 && NS == 1) {
+            if (nc == 1) return launch_reg<FMT, 2, 1, 1, 8, 2, 2, NS>(sg, x, M, max_total, stream);
+            if (nc == 2) return launch_reg<FMT, 2, 1, 2, 4, 2, 2, NS>(sg, x, M, max_total, stream);
+            if (nc == 4) return launch_reg<FMT, 2, 1, 4, 2, 2, 1, NS>(sg, x, M, max_total, stream);
+            if (nc == 7) return launch_reg<FMT, 2, 1, 7, 2, 2, 1, NS>(sg, x, M, max_total, stream);
+        }
+        return hipErrorNotSupported;
     }
-    if (n_tok == 1) {
-        if (nc == 1) return launch_reg<FMT, 1, 1, 1, 8, 2, 2, NS>(sg, x, M, max_total, stream);
-        if (nc == 2 && M >= 10240) return launch_reg<FMT, 1, 2, 1, 8, 2, 2, NS>(sg, x, M, max_total, stream);
-        if (nc == 7) return launch_reg<FMT, 1, 1, 7, 2, 2, 1, NS>(sg, x, M, max_total, stream);
-    } else if (n_tok == 2 && NS == 1) {
-        if (nc == 1) return launch_reg<FMT, 2, 1, 1, 8, 2, 2, NS>(sg, x, M, max_total, stream);
-        if (nc == 2) return launch_reg<FMT, 2, 1, 2, 4, 2, 2, NS>(sg, x, M, max_total, stream);
-        if (nc == 4) return launch_reg<FMT, 2, 1, 4, 2, 2, 1, NS>(sg, x, M, max_total, stream);
-        if (nc == 7) return launch_reg<FMT, 2, 1, 7, 2, 2, 1, NS>(sg, x, M, max_total, stream);
-    }
-    return hipErrorNotSupported;
 }
 
 template <int FMT>

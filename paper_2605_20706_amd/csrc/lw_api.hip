@@ -13,6 +13,7 @@
 // tiled matrix-core (prefill) kernel. f16 weights use the VALU kernel in
 // token blocks of LW_GEMV_MAX_TOK for any token count.
 #include "lw_internal.hpp"
+#include "select.hpp"
 
 namespace {
 
@@ -31,11 +32,31 @@ int check_shape(int fmt, int64_t M, int64_t K, int64_t n_tok) {
     return LW_OK;
 }
 
-// Kernel selection for a validated call.
+// A matrix-core family candidate of the selection table (select.hpp), where
+// it takes the call; hipErrorNotSupported otherwise (register-kernel
+// candidates go through launch_gemv_reg, which reads the table itself).
+hipError_t launch_family(int cand, int fmt, const uint8_t* Wb, const float* x, float* y, int64_t M, int64_t K,
+                         int64_t n_tok, const lw::Planes& p, hipStream_t s) {
+    const bool q4 = fmt == LW_Q4_0 || fmt == LW_Q4_K || fmt == LW_Q4_1;
+    if (!q4) return hipErrorNotSupported;
+    if (cand == lw::kCandFewtok && n_tok >= 2 && n_tok <= 8) return lw::launch_fewtok(fmt, Wb, x, y, M, K, n_tok, p, s);
+    if (cand == lw::kCandMultitok && lw::multitok_supported(fmt, n_tok))
+        return lw::launch_multitok(fmt, Wb, x, y, M, K, n_tok, p, s);
+    if (cand == lw::kCandPrefill && n_tok >= 9) return lw::launch_prefill(fmt, Wb, x, y, M, K, n_tok, p, s);
+    return hipErrorNotSupported;
+}
+
+// Kernel selection for a validated call: the swept table's candidate where
+// it names one (select.hpp), else the built-in rules below.
 hipError_t dispatch(int fmt, const uint8_t* Wb, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
                     hipStream_t s) {
     const lw::Planes p = lw::planes_of(fmt, M * K);
     hipError_t err = hipErrorNotSupported;
+    const int cand = lw::select_cand(fmt, M, K, n_tok);
+    if (cand >= lw::kCandFewtok) {
+        err = launch_family(cand, fmt, Wb, x, y, M, K, n_tok, p, s);
+        if (err != hipErrorNotSupported) return err;
+    }
     if (n_tok <= 2) err = lw::launch_gemv_reg(fmt, Wb, x, y, M, K, n_tok, p, s);
     if (err == hipErrorNotSupported && n_tok >= 2 && n_tok <= 8) err = lw::launch_fewtok(fmt, Wb, x, y, M, K, n_tok, p, s);
     if (err == hipErrorNotSupported) {

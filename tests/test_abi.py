@@ -9,7 +9,7 @@ import pytest
 
 import golden_io
 from paper_2605_20706_amd import binding, layout
-from paper_2605_20706_amd.layout import F16, Q1_0, Q4_0, Q4_1, Q4_K, Q8_0
+from paper_2605_20706_amd.layout import F16, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 LW_OK, LW_EINVAL, LW_EFMT, LW_ESHAPE, LW_EALIGN = 0, -1, -2, -3, -4
@@ -196,25 +196,25 @@ def test_kernel_selection_table(lib):
                 name = binding.kernel_name(wl.fmt, m.M, m.K, nt)
                 assert name and re.fullmatch(r"\w+_kernel<\d+(, \d+)*>", name), (key, m, nt, name)
                 assert name.startswith(("gemv", "multitok", "fewtok", "skinny", "gemm")), name
+    # shapes the swept table names (profiles/sweep_select.json): see test_selection_table_matches_sweep;
+    # the built-in rules elsewhere
     assert kind(Q4_K, 14336, 4096, 1) == "gemv1r_kernel"      # 8B gate: 2 chunks, many rows
     assert kind(Q4_K, 4096, 14336, 1) == "gemv1r_kernel"      # 8B down: 7 chunks split over 7 waves
     assert kind(Q4_K, 6144, 4096, 1) == "gemv1_kernel"        # 8B qkv: too few rows per wave
     assert kind(Q4_0, 100, 2304, 1) == "gemv1_kernel"         # K not whole chunks
     assert kind(Q4_0, 14336, 4096, 2) == "gemv1r_kernel"
-    assert kind(Q4_0, 14336, 4096, 4) == "fewtok_kernel"        # 8B gate: 56 rows per workgroup
-    assert kind(Q4_0, 14336, 4096, 2) == "gemv1r_kernel"
-    assert kind(Q4_0, 4096, 14336, 4) == "multitok_pk_kernel"   # 8B down: one tile per workgroup
-    assert kind(Q4_K, 4096, 14336, 8) == "multitok_pk_kernel"
     assert kind(Q4_K, 128256, 4096, 8) == "fewtok_kernel"       # lm_head: two tiles per wave
     assert kind(Q4_0, 8192, 2048, 4) == "multitok_pk_kernel"    # 1B gate Q4_0: K below 4096
-    assert kind(Q4_K, 8192, 2048, 4) == "fewtok_kernel"
     assert kind(Q4_K, 14336, 4096, 9) == "multitok_kernel"
     assert kind(Q4_0, 14336, 4096, 512) == "gemm32_kernel"
     assert kind(Q8_0, 14336, 4096, 512) == "gemm_kernel"
     assert kind(F16, 2048, 2048, 1) == "gemv1_kernel"
     assert kind(Q8_0, 2048, 2048, 12) == "skinny_kernel"
     assert kind(F16, 2048, 2048, 20) == "gemv_kernel"
-    assert binding.kernel_name(Q4_K, 14336, 4096, 1) == "gemv1r_kernel<%d, 1, 2, 1, 8, 2, 1>" % Q4_K
+    for fmt in (Q5_0, Q5_1, Q5_K, Q6_K, Q2_K):                # the VALU kernels for every token count
+        assert kind(fmt, 14336, 4096, 1) == "gemv1_kernel"
+        assert kind(fmt, 14336, 4096, 4) == "gemv_kernel"
+        assert kind(fmt, 14336, 4096, 512) == "gemv_kernel"
 
 
 def test_ceiling_library_exports_and_checks():
@@ -278,3 +278,53 @@ def test_launch_count(lib):
     assert g(Q4_0, 2, None, 256, 1) == LW_EINVAL
     assert g(11, 2, Ms, 256, 1) == LW_EFMT
     assert g(Q4_0, 2, Ms, 300, 1) == LW_ESHAPE
+
+
+def test_forced_candidates_name_their_kernels(lib, monkeypatch):
+    """LW_FORCE_CFG selects each candidate where it takes the shape (the
+    kernel name shows its configuration) and falls back to the built-in
+    choice where it does not."""
+    seen = {}
+    for cand, K, nt, M in [(10, 2048, 1, 3001), (11, 2048, 1, 3001), (12, 2048, 1, 3001), (13, 4096, 1, 3001),
+                           (14, 4096, 1, 3001), (15, 4096, 1, 3001), (16, 4096, 1, 3001), (17, 4096, 1, 3001),
+                           (18, 14336, 1, 3001), (19, 14336, 1, 3001), (20, 14336, 1, 3001),
+                           (21, 2048, 2, 2500), (22, 4096, 2, 2500), (23, 8192, 2, 2500), (24, 14336, 2, 2500),
+                           (25, 4096, 2, 2500)]:
+        monkeypatch.setenv("LW_FORCE_CFG", str(cand))
+        name = binding.kernel_name(Q4_K, M, K, nt)
+        assert name.startswith("gemv1r_kernel<3, %d, " % nt), (cand, name)
+        seen[cand] = name
+    assert len(set(seen.values())) == len(seen)  # every candidate a distinct configuration
+    monkeypatch.setenv("LW_FORCE_CFG", "1")
+    assert binding.kernel_name(Q4_K, 14336, 4096, 1).startswith("gemv1_kernel<")
+    monkeypatch.setenv("LW_FORCE_CFG", "30")
+    assert binding.kernel_name(Q4_0, 8200, 4096, 4).startswith("fewtok_kernel<")
+    monkeypatch.setenv("LW_FORCE_CFG", "31")
+    assert binding.kernel_name(Q4_0, 8200, 4096, 4).startswith("multitok")
+    monkeypatch.setenv("LW_FORCE_CFG", "32")
+    assert binding.kernel_name(Q4_0, 8200, 4096, 12).startswith("gemm32_kernel<")
+    # a 2-chunk candidate on a 1-chunk shape: the built-in rule for one chunk
+    monkeypatch.setenv("LW_FORCE_CFG", "13")
+    assert binding.kernel_name(Q4_K, 3001, 2048, 1) == "gemv1r_kernel<3, 1, 1, 1, 8, 2, 1>"
+
+
+def test_selection_table_matches_sweep(lib):
+    """The compiled table is the one the committed sweep generates, and every
+    swept shape selects the sweep's fastest candidate."""
+    import json
+    from paper_2605_20706_amd import gen_select
+    with open(gen_select.OUT) as fh:
+        assert fh.read() == gen_select.render(gen_select.entries())
+    if not os.path.exists(gen_select.SWEEP):
+        pytest.skip("no sweep results committed")
+    with open(gen_select.SWEEP) as fh:
+        sweep = json.load(fh)
+    for sh in sweep["shapes"]:
+        res = [r for r in sh["results"] if r.get("us") is not None]
+        best = min(res, key=lambda r: r["us"])
+        Ms = sh.get("Ms", [sh["M"]])
+        if len(Ms) > 1:
+            name = binding.kernel_name_multi(sh["fmt"], Ms, sh["K"], sh["n_tok"])
+        else:
+            name = binding.kernel_name(sh["fmt"], sh["M"], sh["K"], sh["n_tok"])
+        assert name == best["kernel"], (sh["fmt"], sh["M"], sh["K"], sh["n_tok"], name, best)
