@@ -19,6 +19,11 @@ builds it with gcc and marshals numpy arrays through ctypes.
   the quantity that scales the rounding error of a kernel that sums the two
   terms separately.
 * ``matvec_sampled(...)`` the same for a list of (token, row) outputs.
+* ``attn_decode(fmt, q, K, V, n_heads, n_kv_heads, head_dim, kv_len, scale)``
+  -> (out, A, T): one query token's attention over a KV cache stored in a
+  weight format (Sec. 3.2 attention over quantized K/V, Sec. 3.3 the
+  dequantization reused for the KV cache), with A = sum_j p_j |v_j| per
+  output and T = the largest scale * sum |q k| per head.
 """
 from __future__ import annotations
 
@@ -77,6 +82,9 @@ def _load():
         lib.oracle_matvec_sampled.argtypes = [ctypes.c_int, u8p, f32p, i64, i64, i64, i64,
                                               i64p, i64p, f64p, f64p]
         lib.oracle_matvec_sampled.restype = ctypes.c_int
+        lib.oracle_attn_decode.argtypes = [ctypes.c_int, f32p, u8p, u8p, i64, i64, i64, i64, ctypes.c_double,
+                                           f64p, f64p, f64p]
+        lib.oracle_attn_decode.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -176,3 +184,23 @@ def matvec_sampled(fmt: int, W, x: np.ndarray, M: int, K: int, rows, toks):
     if rc != 0:
         raise ValueError("oracle.matvec_sampled failed")
     return y, A
+
+
+def attn_decode(fmt: int, q, Kc, Vc, n_heads: int, n_kv_heads: int, head_dim: int, kv_len: int, scale: float):
+    """Returns (out [n_heads, head_dim], A [n_heads, head_dim], T [n_heads]) in float64."""
+    q = np.ascontiguousarray(q, dtype=np.float32).reshape(-1)
+    if q.size != n_heads * head_dim:
+        raise ValueError("oracle.attn_decode: q must hold n_heads * head_dim floats")
+    Kc, Vc = _bytes(Kc), _bytes(Vc)
+    need = weight_bytes(fmt, n_kv_heads * kv_len * head_dim)
+    if need < 0 or Kc.size < need or Vc.size < need:
+        raise ValueError("oracle.attn_decode: bad format/size")
+    out = np.empty((n_heads, head_dim), np.float64)
+    A = np.empty((n_heads, head_dim), np.float64)
+    T = np.empty(n_heads, np.float64)
+    rc = _load().oracle_attn_decode(fmt, _ptr(q, ctypes.c_float), _ptr(Kc, ctypes.c_uint8), _ptr(Vc, ctypes.c_uint8),
+                                    n_heads, n_kv_heads, head_dim, kv_len, float(scale), _ptr(out, ctypes.c_double),
+                                    _ptr(A, ctypes.c_double), _ptr(T, ctypes.c_double))
+    if rc != 0:
+        raise ValueError("oracle.attn_decode failed")
+    return out, A, T

@@ -545,3 +545,70 @@ int oracle_matvec_sampled(int fmt, const uint8_t* W, const float* x, int64_t M, 
     }
     return 0;
 }
+
+/* ---- decode attention over a quantized KV cache ---------------------------
+ *
+ * Sec. 3.2 (attention kernels read quantized K and V and dequantize them on
+ * load) and Sec. 3.3 (the dequantization routines serve the KV cache too).
+ * One query token: for query head h and its key/value head g = h / (n_heads /
+ * n_kv_heads), over the kv_len cached positions j,
+ *   s_j = scale * sum_d q[h][d] * k[g][j][d]
+ *   p_j = exp(s_j - max_j s_j) / sum_j exp(s_j - max_j s_j)
+ *   out[h][d] = sum_j p_j * v[g][j][d]
+ * with k and v the dequantized cache elements (each rounded once to float,
+ * as oracle_dequant gives them), everything else in double. The caches are
+ * packed tensors of n_kv_heads * kv_len * head_dim elements, element
+ * (g * kv_len + j) * head_dim + d. Also returned per output: A[h][d] =
+ * sum_j p_j * |v[g][j][d]|, and per head T[h] = max_j scale * sum_d |q k|. */
+int oracle_attn_decode(int fmt, const float* q, const uint8_t* Kc, const uint8_t* Vc, int64_t n_heads,
+                       int64_t n_kv_heads, int64_t head_dim, int64_t kv_len, double scale, double* out,
+                       double* A, double* T) {
+    int64_t offk[4], offv[4], total;
+    if (n_heads < 1 || n_kv_heads < 1 || head_dim < 1 || kv_len < 1 || n_heads % n_kv_heads) return -1;
+    int64_t n = n_kv_heads * kv_len * head_dim;
+    if (planes(fmt, n, offk, &total) || planes(fmt, n, offv, &total) || head_dim % block_elems(fmt)) return -1;
+    double* s = (double*)malloc(sizeof(double) * (size_t)kv_len);
+    double* t = (double*)malloc(sizeof(double) * (size_t)kv_len);
+    if (!s || !t) {
+        free(s);
+        free(t);
+        return -1;
+    }
+    int64_t group = n_heads / n_kv_heads;
+    for (int64_t h = 0; h < n_heads; ++h) {
+        int64_t g = h / group;
+        const float* qh = q + h * head_dim;
+        double smax = -INFINITY, tmax = 0.0;
+        for (int64_t j = 0; j < kv_len; ++j) {
+            double acc = 0.0, mag = 0.0;
+            for (int64_t d = 0; d < head_dim; ++d) {
+                double k = (double)(float)exact_value(fmt, Kc, offk, (g * kv_len + j) * head_dim + d);
+                acc += (double)qh[d] * k;
+                mag += fabs((double)qh[d] * k);
+            }
+            s[j] = scale * acc;
+            t[j] = fabs(scale) * mag;
+            if (s[j] > smax) smax = s[j];
+            if (t[j] > tmax) tmax = t[j];
+        }
+        double denom = 0.0;
+        for (int64_t j = 0; j < kv_len; ++j) {
+            s[j] = exp(s[j] - smax);
+            denom += s[j];
+        }
+        for (int64_t d = 0; d < head_dim; ++d) {
+            double o = 0.0, a = 0.0;
+            for (int64_t j = 0; j < kv_len; ++j) {
+                double v = (double)(float)exact_value(fmt, Vc, offv, (g * kv_len + j) * head_dim + d);
+                o += s[j] * v;
+                a += s[j] * fabs(v);
+            }
+            out[h * head_dim + d] = o / denom;
+            if (A) A[h * head_dim + d] = a / denom;
+        }
+        if (T) T[h] = tmax;
+    }
+    free(s);
+    free(t);
+    return 0;
+}

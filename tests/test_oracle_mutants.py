@@ -17,7 +17,8 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "lw_oracle.c")
-PINS = ["tests/test_oracle_formats.py", "tests/test_oracle_gemv.py", "tests/test_oracle_termmass.py"]
+PINS = ["tests/test_oracle_formats.py", "tests/test_oracle_gemv.py", "tests/test_oracle_termmass.py",
+        "tests/test_oracle_attn.py"]
 
 # (name, text in the oracle, replacement); every occurrence is replaced.
 MUTANTS = [
@@ -59,6 +60,13 @@ MUTANTS = [
      "unsigned sc = scm >> 4, m = scm & 15u;"),
     ("2-bit fields read most-significant first", "return bit_field(plane + e / 4, 2 * (int)(e % 4), 2);",
      "return bit_field(plane + e / 4, 6 - 2 * (int)(e % 4), 2);"),
+    ("attention: key/value head of a query head taken modulo", "int64_t g = h / group;", "int64_t g = h % n_kv_heads;"),
+    ("attention: scale dropped", "s[j] = scale * acc;", "s[j] = acc;"),
+    ("attention: values read from the key cache",
+     "double v = (double)(float)exact_value(fmt, Vc, offv, (g * kv_len + j) * head_dim + d);",
+     "double v = (double)(float)exact_value(fmt, Kc, offv, (g * kv_len + j) * head_dim + d);"),
+    ("attention: last position skipped in the normalisation", "        for (int64_t j = 0; j < kv_len; ++j) {\n            s[j] = exp(s[j] - smax);",
+     "        for (int64_t j = 0; j + 1 < kv_len; ++j) {\n            s[j] = exp(s[j] - smax);"),
     ("term mass without the code shift", "return fabs(s) * (q + (double)beta) + fabs(mu - (double)beta * s);",
      "return fabs(s) * q + fabs(mu - (double)beta * s);"),
     ("term mass offset taken with its sign", "fabs(mu - (double)beta * s);", "(mu - (double)beta * s);"),
