@@ -244,6 +244,54 @@ LW_API const char* lw_kernel_name(int fmt, int64_t M, int64_t K, int64_t n_tok);
 LW_API const char* lw_kernel_name_multi(int fmt, int n_mat, const int64_t* M, int64_t K, int64_t n_tok);
 
 /*
+ * lw_attn_decode — one query token's attention over a KV cache stored in a
+ * weight format, dequantized as it is loaded (Sec. 3.2: attention kernels
+ * read quantized K and V; Sec. 3.3: the dequantization routines serve the KV
+ * cache as well as the weights). For query head h, its key/value head
+ * g = h / (n_heads / n_kv_heads), and the kv_len cached positions j:
+ *   s_j = scale * sum_d q[h][d] * k[g][j][d],  p = softmax over j of s,
+ *   out[h][d] = sum_j p_j * v[g][j][d].
+ *
+ *   fmt        LW_F16, LW_Q8_0, LW_Q4_0, LW_Q4_1, LW_Q5_0 or LW_Q5_1 (formats
+ *              whose blocks fit a head's row); both caches share it.
+ *   q          device; float32 [n_heads][head_dim], 16-byte aligned.
+ *   K, V       device; each n_kv_heads * kv_len * head_dim elements in the
+ *              packed layout above, element (g * kv_len + j) * head_dim + d
+ *              (head-major: a head's positions are consecutive rows),
+ *              256-byte aligned.
+ *   out        device; float32 [n_heads][head_dim], 16-byte aligned,
+ *              overwritten; must not overlap the inputs or the workspace.
+ *   n_heads, n_kv_heads  n_heads / n_kv_heads in {1, 2, 4, 8}, n_heads <= 4096.
+ *   head_dim   64 or 128.   kv_len  1 <= kv_len < 2^31.
+ *   scale      finite (usually 1 / sqrt(head_dim)).
+ *   workspace  device, 16-byte aligned, at least lw_attn_workspace_bytes(...)
+ *              bytes, owned by the caller; holds partial results between the
+ *              call's two kernels (its contents need no initialisation and are
+ *              undefined afterwards). Calls that overlap in time must not
+ *              share a workspace.
+ *   stream     hipStream_t (NULL: the null stream).
+ *
+ * Errors in the usual order: LW_EFMT (fmt not one of the above), LW_EINVAL
+ * (null pointer, sizes out of range, a head ratio or head_dim not listed,
+ * scale not finite, workspace too small), LW_ESHAPE (n_kv_heads * kv_len *
+ * head_dim not a multiple of 256), LW_EALIGN, LW_EHIP. Two kernel launches.
+ * Arithmetic in float32: each output is within 2^-12 * (1 + T) * sum_j p_j
+ * |v[g][j][d]| of the exact value, T the largest scale * sum_d |q k| of the
+ * head (the score error enters the weights through exp).
+ */
+LW_API int lw_attn_decode(int fmt, const float* q, const void* K, const void* V, float* out, int64_t n_heads,
+                          int64_t n_kv_heads, int64_t head_dim, int64_t kv_len, float scale, void* workspace,
+                          int64_t workspace_bytes, void* stream);
+
+/*
+ * lw_attn_workspace_bytes — the workspace lw_attn_decode needs for these
+ * sizes (n_heads * splits * (head_dim + 2) * 4 bytes for the library's split
+ * of the positions), or the size error of the call (negative). Host-only.
+ */
+LW_API int64_t lw_attn_workspace_bytes(int fmt, int64_t n_heads, int64_t n_kv_heads, int64_t head_dim,
+                                       int64_t kv_len);
+
+/*
  * lw_launch_count — the number of kernel launches lw_matvec(fmt, W, x, y, M,
  * K, n_tok, stream) makes for these sizes (1 for most calls; 2 where a fill
  * kernel zeroes y before a K-split prefill launch, or where tokens run as

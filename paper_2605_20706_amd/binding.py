@@ -15,7 +15,8 @@ LIB_PATH = os.path.join(HERE, "liblw.so")
 
 LW_OK = 0
 EXPORTS = ("lw_matvec", "lw_matvec_multi", "lw_dequant", "lw_weight_bytes", "lw_strerror", "lw_kernel_name",
-           "lw_kernel_name_multi", "lw_launch_count", "lw_launch_count_multi")
+           "lw_kernel_name_multi", "lw_launch_count", "lw_launch_count_multi", "lw_attn_decode",
+           "lw_attn_workspace_bytes")
 LW_MULTI_MAX = 4
 
 
@@ -65,6 +66,10 @@ def library() -> ctypes.CDLL:
         lib.lw_launch_count.restype = i64
         lib.lw_launch_count_multi.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.POINTER(i64), i64, i64]
         lib.lw_launch_count_multi.restype = i64
+        lib.lw_attn_decode.argtypes = [ctypes.c_int, vp, vp, vp, vp, i64, i64, i64, i64, ctypes.c_float, vp, i64, vp]
+        lib.lw_attn_decode.restype = ctypes.c_int
+        lib.lw_attn_workspace_bytes.argtypes = [ctypes.c_int, i64, i64, i64, i64]
+        lib.lw_attn_workspace_bytes.restype = i64
         _lib = lib
     return _lib
 
@@ -211,4 +216,40 @@ def dequant(fmt: int, W, n: int, out=None):
     rc = library().lw_dequant(fmt, W.data_ptr(), out.data_ptr(), n)
     if rc != LW_OK:
         raise LwError(rc, "lw_dequant")
+    return out
+
+
+def attn_workspace_bytes(fmt: int, n_heads: int, n_kv_heads: int, head_dim: int, kv_len: int) -> int:
+    v = library().lw_attn_workspace_bytes(fmt, n_heads, n_kv_heads, head_dim, kv_len)
+    if v < 0:
+        raise LwError(v, "lw_attn_workspace_bytes")
+    return v
+
+
+def attn_decode(fmt: int, q, K, V, n_heads: int, n_kv_heads: int, head_dim: int, kv_len: int, scale: float,
+                out=None, workspace=None, stream=None):
+    """out[n_heads, head_dim] = attention of one query token over the KV cache
+    (K, V: uint8 GPU tensors in the packed layout, head-major). The
+    workspace (a uint8 GPU tensor) is allocated here when not given."""
+    import torch
+
+    _check_gpu(q, "q")
+    _check_gpu(K, "K")
+    _check_gpu(V, "V")
+    if q.dtype != torch.float32 or q.numel() != n_heads * head_dim:
+        raise ValueError("q must be float32 [n_heads, head_dim]")
+    if out is None:
+        out = torch.empty((n_heads, head_dim), dtype=torch.float32, device=q.device)
+    _check_gpu(out, "out")
+    nb = attn_workspace_bytes(fmt, n_heads, n_kv_heads, head_dim, kv_len)
+    if workspace is None:
+        workspace = torch.empty(max(nb, 16), dtype=torch.uint8, device=q.device)
+    _check_gpu(workspace, "workspace")
+    if stream is None:
+        stream = torch.cuda.current_stream(q.device)
+    rc = library().lw_attn_decode(fmt, q.data_ptr(), K.data_ptr(), V.data_ptr(), out.data_ptr(), n_heads, n_kv_heads,
+                                  head_dim, kv_len, float(scale), workspace.data_ptr(), workspace.numel(),
+                                  ctypes.c_void_p(stream.cuda_stream))
+    if rc != LW_OK:
+        raise LwError(rc, "lw_attn_decode")
     return out

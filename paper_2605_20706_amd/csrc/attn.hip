@@ -1,0 +1,261 @@
+// Decode attention over a KV cache stored in a weight format.
+//
+// One query token (the decode step of Sec. 2.1) attends over kv_len cached
+// positions; K and V are dequantized as they are loaded, with the same
+// per-format routine as the weights (Sec. 3.2: attention reads quantized K
+// and V; Sec. 3.3: the dequantization routines serve the KV cache). For
+// query head h and its key/value head g = h / G (G = n_heads / n_kv_heads):
+//   s_j = scale * q_h . k_{g,j},  p = softmax(s),  out_h = sum_j p_j v_{g,j}.
+//
+// Split over the positions (flash decoding): workgroup (g, s) takes the G
+// query heads of key/value head g over positions [s*rps, (s+1)*rps) and
+// writes per head the running maximum m, the sum l of exp(s_j - m) and the
+// unnormalised output sum_j exp(s_j - m) v_j to the workspace; a second
+// kernel rescales the splits to their common maximum and divides. Inside a
+// workgroup each wave takes batches of RPW positions: lane (r, c) holds DPL
+// consecutive dimensions c*DPL .. of position r, its query slices for the G
+// heads in registers; scores are lane sums over the LPR = head_dim / DPL
+// lanes of a position, and the online softmax rescales the lane's G x DPL
+// output partials by exp(m_old - m_new) per batch. The wave's partials are
+// then summed over positions (lane shuffles) and the four waves combined
+// through LDS. Everything is float32; every exp argument is <= 0.
+#include <cmath>
+
+#include "lw_device.hpp"
+#include "lw_formats.hpp"
+#include "lw_internal.hpp"
+
+namespace lw {
+namespace {
+
+struct Name_attn_split_kernel {
+    static constexpr const char* base = "attn_split_kernel";
+};
+
+constexpr int kAttnWaves = 4;
+constexpr int kAttnThreads = kAttnWaves * kWave;
+
+template <int G>
+constexpr int dims_per_lane() {
+    return G <= 4 ? 16 : 8;
+}
+
+__device__ __forceinline__ float xor_sum(float v, int mask) { return v + __shfl_xor(v, mask, kWave); }
+__device__ __forceinline__ float xor_max(float v, int mask) { return fmaxf(v, __shfl_xor(v, mask, kWave)); }
+
+template <int FMT, int D, int G>
+__global__ void __launch_bounds__(kAttnThreads)
+    attn_split_kernel(const float* __restrict__ q, const uint8_t* __restrict__ Kc, const uint8_t* __restrict__ Vc,
+                      int64_t off1, int64_t off2, int64_t off3, int kv_len, int n_heads, float scale, int rps,
+                      float* __restrict__ ws) {
+    constexpr int DPL = dims_per_lane<G>();
+    constexpr int LPR = D / DPL;       // lanes per position
+    constexpr int RPW = kWave / LPR;   // positions per wave and batch
+    __shared__ float red[kAttnWaves][G][D + 2];
+
+    const int g = blockIdx.x, split = blockIdx.y;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int r = lane / LPR, c = lane - r * LPR;
+    const int j0 = split * rps;
+    const int j1 = min(kv_len, j0 + rps);
+
+    float qv[G][DPL];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        const float4* qp = reinterpret_cast<const float4*>(q + (int64_t)(g * G + h) * D + c * DPL);
+#pragma unroll
+        for (int i = 0; i < DPL / 4; ++i) {
+            const float4 t = qp[i];
+            qv[h][4 * i] = t.x;
+            qv[h][4 * i + 1] = t.y;
+            qv[h][4 * i + 2] = t.z;
+            qv[h][4 * i + 3] = t.w;
+        }
+    }
+    float m[G], l[G], acc[G][DPL];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        m[h] = -INFINITY;
+        l[h] = 0.f;
+#pragma unroll
+        for (int i = 0; i < DPL; ++i) acc[h][i] = 0.f;
+    }
+
+    const int64_t head_base = (int64_t)g * kv_len;
+    for (int b = j0 + wave * RPW; b < j1; b += kAttnWaves * RPW) {
+        const int row = b + r;
+        const bool valid = row < j1;
+        const int64_t e = (head_base + (valid ? row : j1 - 1)) * D + c * DPL;
+        float kk[DPL];
+#pragma unroll
+        for (int i = 0; i < DPL / 4; ++i) {
+            const float4 t = value4<FMT>(Kc, off1, off2, off3, e + 4 * i);
+            kk[4 * i] = t.x;
+            kk[4 * i + 1] = t.y;
+            kk[4 * i + 2] = t.z;
+            kk[4 * i + 3] = t.w;
+        }
+        float s[G];
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+            float d = 0.f;
+#pragma unroll
+            for (int i = 0; i < DPL; ++i) d = __builtin_fmaf(qv[h][i], kk[i], d);
+#pragma unroll
+            for (int o = 1; o < LPR; o <<= 1) d = xor_sum(d, o);
+            s[h] = valid ? d * scale : -INFINITY;
+        }
+        float vv[DPL];
+#pragma unroll
+        for (int i = 0; i < DPL / 4; ++i) {
+            const float4 t = value4<FMT>(Vc, off1, off2, off3, e + 4 * i);
+            vv[4 * i] = t.x;
+            vv[4 * i + 1] = t.y;
+            vv[4 * i + 2] = t.z;
+            vv[4 * i + 3] = t.w;
+        }
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+            float mb = s[h];
+#pragma unroll
+            for (int o = LPR; o < kWave; o <<= 1) mb = xor_max(mb, o);
+            const float mn = fmaxf(m[h], mb);  // finite: the batch has a valid position
+            const float alpha = expf(m[h] - mn);  // m = -inf: 0
+            const float p = valid ? expf(s[h] - mn) : 0.f;
+            m[h] = mn;
+            l[h] = __builtin_fmaf(l[h], alpha, c == 0 ? p : 0.f);
+#pragma unroll
+            for (int i = 0; i < DPL; ++i) acc[h][i] = __builtin_fmaf(p, vv[i], acc[h][i] * alpha);
+        }
+    }
+
+    // the wave's totals: l over all lanes, the outputs over the positions
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        float lt = l[h];
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) lt = xor_sum(lt, o);
+#pragma unroll
+        for (int i = 0; i < DPL; ++i) {
+            float a = acc[h][i];
+#pragma unroll
+            for (int o = LPR; o < kWave; o <<= 1) a = xor_sum(a, o);
+            if (r == 0) red[wave][h][c * DPL + i] = a;
+        }
+        if (lane == 0) {
+            red[wave][h][D] = m[h];
+            red[wave][h][D + 1] = lt;
+        }
+    }
+    __syncthreads();
+    // combine the waves (a wave without positions has m = -inf, l = 0, sums 0)
+    float* out = ws + ((int64_t)split * n_heads + (int64_t)g * G) * (D + 2);
+    for (int idx = threadIdx.x; idx < G * (D + 2); idx += kAttnThreads) {
+        const int h = idx / (D + 2), d = idx - h * (D + 2);
+        float M = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < kAttnWaves; ++w) M = fmaxf(M, red[w][h][D]);
+        float v = 0.f;
+        if (d == D) {
+            v = M;
+        } else {
+#pragma unroll
+            for (int w = 0; w < kAttnWaves; ++w) {
+                const float mw = red[w][h][D];
+                const float wgt = mw == -INFINITY ? 0.f : expf(mw - M);
+                v = __builtin_fmaf(wgt, red[w][h][d], v);
+            }
+        }
+        out[(int64_t)h * (D + 2) + d] = v;
+    }
+}
+
+// out[h][d] = sum_s exp(m_s - M) acc_s[d] / sum_s exp(m_s - M) l_s
+template <int D>
+__global__ void __launch_bounds__(D) attn_combine_kernel(const float* __restrict__ ws, float* __restrict__ out,
+                                                         int n_heads, int splits) {
+    const int h = blockIdx.x, d = threadIdx.x;
+    const float* base = ws + (int64_t)h * (D + 2);
+    const int64_t stride = (int64_t)n_heads * (D + 2);
+    float M = -INFINITY;
+    for (int s = 0; s < splits; ++s) M = fmaxf(M, base[s * stride + D]);
+    float L = 0.f, o = 0.f;
+    for (int s = 0; s < splits; ++s) {
+        const float ms = base[s * stride + D];
+        const float wgt = ms == -INFINITY ? 0.f : expf(ms - M);
+        L = __builtin_fmaf(wgt, base[s * stride + D + 1], L);
+        o = __builtin_fmaf(wgt, base[s * stride + d], o);
+    }
+    out[(int64_t)h * D + d] = o / L;
+}
+
+template <int FMT, int D, int G>
+hipError_t launch_g(const float* q, const uint8_t* K, const uint8_t* V, float* out, int64_t n_heads, int64_t n_kv,
+                    int64_t kv_len, float scale, const AttnPlan& pl, float* ws, hipStream_t stream) {
+    const Planes p = planes_of(FMT, n_kv * kv_len * D);
+    if (query_only(kernel_name<Name_attn_split_kernel, FMT, D, G>(), 2)) return hipSuccess;
+    hipLaunchKernelGGL((attn_split_kernel<FMT, D, G>), dim3((unsigned)n_kv, (unsigned)pl.splits), dim3(kAttnThreads),
+                       0, stream, q, K, V, p.off1, p.off2, p.off3, (int)kv_len, (int)n_heads, scale, (int)pl.rps, ws);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL((attn_combine_kernel<D>), dim3((unsigned)n_heads), dim3(D), 0, stream, ws, out, (int)n_heads,
+                       (int)pl.splits);
+    return hipGetLastError();
+}
+
+template <int FMT, int D>
+hipError_t launch_d(const float* q, const uint8_t* K, const uint8_t* V, float* out, int64_t n_heads, int64_t n_kv,
+                    int64_t kv_len, float scale, const AttnPlan& pl, float* ws, hipStream_t stream) {
+    switch (n_heads / n_kv) {
+    case 1: return launch_g<FMT, D, 1>(q, K, V, out, n_heads, n_kv, kv_len, scale, pl, ws, stream);
+    case 2: return launch_g<FMT, D, 2>(q, K, V, out, n_heads, n_kv, kv_len, scale, pl, ws, stream);
+    case 4: return launch_g<FMT, D, 4>(q, K, V, out, n_heads, n_kv, kv_len, scale, pl, ws, stream);
+    case 8: return launch_g<FMT, D, 8>(q, K, V, out, n_heads, n_kv, kv_len, scale, pl, ws, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+template <int FMT>
+hipError_t launch_f(const float* q, const uint8_t* K, const uint8_t* V, float* out, int64_t n_heads, int64_t n_kv,
+                    int64_t head_dim, int64_t kv_len, float scale, const AttnPlan& pl, float* ws,
+                    hipStream_t stream) {
+    if (head_dim == 64) return launch_d<FMT, 64>(q, K, V, out, n_heads, n_kv, kv_len, scale, pl, ws, stream);
+    if (head_dim == 128) return launch_d<FMT, 128>(q, K, V, out, n_heads, n_kv, kv_len, scale, pl, ws, stream);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+AttnPlan attn_plan(int64_t n_kv, int64_t head_dim, int64_t kv_len, int64_t n_heads) {
+    AttnPlan pl;
+    // about two workgroups per compute unit, at least 32 positions each
+    const int64_t by_len = (kv_len + 31) / 32;
+    const int64_t by_chip = (512 + n_kv - 1) / n_kv;
+    int64_t splits = by_len < by_chip ? by_len : by_chip;
+    if (splits < 1) splits = 1;
+    pl.rps = (kv_len + splits - 1) / splits;
+    pl.splits = (kv_len + pl.rps - 1) / pl.rps;  // no empty split
+    pl.ws_bytes = pl.splits * n_heads * (head_dim + 2) * 4;
+    return pl;
+}
+
+bool attn_fmt_supported(int fmt) {
+    return fmt == LW_F16 || fmt == LW_Q8_0 || fmt == LW_Q4_0 || fmt == LW_Q4_1 || fmt == LW_Q5_0 || fmt == LW_Q5_1;
+}
+
+hipError_t launch_attn(int fmt, const float* q, const uint8_t* K, const uint8_t* V, float* out, int64_t n_heads,
+                       int64_t n_kv, int64_t head_dim, int64_t kv_len, float scale, const AttnPlan& pl, float* ws,
+                       hipStream_t stream) {
+    switch (fmt) {
+    case LW_F16: return launch_f<LW_F16>(q, K, V, out, n_heads, n_kv, head_dim, kv_len, scale, pl, ws, stream);
+    case LW_Q8_0: return launch_f<LW_Q8_0>(q, K, V, out, n_heads, n_kv, head_dim, kv_len, scale, pl, ws, stream);
+    case LW_Q4_0: return launch_f<LW_Q4_0>(q, K, V, out, n_heads, n_kv, head_dim, kv_len, scale, pl, ws, stream);
+    case LW_Q4_1: return launch_f<LW_Q4_1>(q, K, V, out, n_heads, n_kv, head_dim, kv_len, scale, pl, ws, stream);
+    case LW_Q5_0: return launch_f<LW_Q5_0>(q, K, V, out, n_heads, n_kv, head_dim, kv_len, scale, pl, ws, stream);
+    case LW_Q5_1: return launch_f<LW_Q5_1>(q, K, V, out, n_heads, n_kv, head_dim, kv_len, scale, pl, ws, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace lw

@@ -12,6 +12,8 @@
 // kernel with K split across waves; more tokens -> the
 // tiled matrix-core (prefill) kernel. f16 weights use the VALU kernel in
 // token blocks of LW_GEMV_MAX_TOK for any token count.
+#include <cmath>
+
 #include "lw_internal.hpp"
 #include "select.hpp"
 
@@ -229,6 +231,52 @@ int64_t lw_launch_count_multi(int fmt, int n_mat, const int64_t* M, int64_t K, i
     if (worst != LW_OK) return worst;
     lw::LaunchQuery r;
     return run_query(fmt, n_mat, M, 0, K, n_tok, r) ? r.count : LW_EHIP;
+}
+
+}  // extern "C"
+
+namespace {
+
+// The checks of lw_attn_decode that need no pointer, in the documented order.
+int check_attn(int fmt, int64_t n_heads, int64_t n_kv, int64_t head_dim, int64_t kv_len, float scale) {
+    if (!known_fmt(fmt) || !lw::attn_fmt_supported(fmt)) return LW_EFMT;
+    if (n_heads < 1 || n_kv < 1 || kv_len < 1 || n_heads > 4096 || kv_len >= ((int64_t)1 << 31) ||
+        n_kv * kv_len > LW_MAX_ELEMS / 128)
+        return LW_EINVAL;
+    if (n_heads % n_kv) return LW_EINVAL;
+    const int64_t grp = n_heads / n_kv;
+    if (grp != 1 && grp != 2 && grp != 4 && grp != 8) return LW_EINVAL;
+    if (head_dim != 64 && head_dim != 128) return LW_EINVAL;
+    if (!std::isfinite(scale)) return LW_EINVAL;
+    if ((n_kv * kv_len * head_dim) % 256) return LW_ESHAPE;
+    return LW_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t lw_attn_workspace_bytes(int fmt, int64_t n_heads, int64_t n_kv_heads, int64_t head_dim, int64_t kv_len) {
+    const int rc = check_attn(fmt, n_heads, n_kv_heads, head_dim, kv_len, 1.0f);
+    if (rc != LW_OK) return rc;
+    return lw::attn_plan(n_kv_heads, head_dim, kv_len, n_heads).ws_bytes;
+}
+
+int lw_attn_decode(int fmt, const float* q, const void* K, const void* V, float* out, int64_t n_heads,
+                   int64_t n_kv_heads, int64_t head_dim, int64_t kv_len, float scale, void* workspace,
+                   int64_t workspace_bytes, void* stream) {
+    if (!known_fmt(fmt) || !lw::attn_fmt_supported(fmt)) return LW_EFMT;
+    if (!q || !K || !V || !out || !workspace) return LW_EINVAL;
+    const int rc = check_attn(fmt, n_heads, n_kv_heads, head_dim, kv_len, scale);
+    if (rc != LW_OK) return rc;
+    const lw::AttnPlan pl = lw::attn_plan(n_kv_heads, head_dim, kv_len, n_heads);
+    if (workspace_bytes < pl.ws_bytes) return LW_EINVAL;
+    if (!aligned(K, 256) || !aligned(V, 256) || !aligned(q, 16) || !aligned(out, 16) || !aligned(workspace, 16))
+        return LW_EALIGN;
+    const hipError_t err = lw::launch_attn(fmt, q, static_cast<const uint8_t*>(K), static_cast<const uint8_t*>(V), out,
+                                           n_heads, n_kv_heads, head_dim, kv_len, scale, pl,
+                                           static_cast<float*>(workspace), reinterpret_cast<hipStream_t>(stream));
+    return err == hipSuccess ? LW_OK : LW_EHIP;
 }
 
 int lw_dequant(int fmt, const void* W, float* out, int64_t n) {

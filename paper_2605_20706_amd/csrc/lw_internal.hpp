@@ -163,6 +163,17 @@ hipError_t launch_fewtok(int fmt, const uint8_t* W, const float* x, float* y, in
 // The same over the rows of n matrices that share x (lw_matvec_multi).
 hipError_t launch_fewtok_multi(int fmt, int n, const uint8_t* const* W, float* const* y, const int64_t* M,
                                const float* x, int64_t K, int64_t n_tok, hipStream_t stream);
+// Decode attention over a KV cache in a weight format (attn.hip): the split
+// of the kv_len positions over workgroups (rps positions per split) and the
+// workspace it needs, the formats it takes, and the two launches.
+struct AttnPlan {
+    int64_t splits = 0, rps = 0, ws_bytes = 0;
+};
+AttnPlan attn_plan(int64_t n_kv, int64_t head_dim, int64_t kv_len, int64_t n_heads);
+bool attn_fmt_supported(int fmt);
+hipError_t launch_attn(int fmt, const float* q, const uint8_t* K, const uint8_t* V, float* out, int64_t n_heads,
+                       int64_t n_kv, int64_t head_dim, int64_t kv_len, float scale, const AttnPlan& pl, float* ws,
+                       hipStream_t stream);
 // Matrix-core path for larger token counts (prefill).
 hipError_t launch_prefill(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                           int64_t n_tok, const Planes& p, hipStream_t stream);

@@ -328,3 +328,29 @@ def test_selection_table_matches_sweep(lib):
         else:
             name = binding.kernel_name(sh["fmt"], sh["M"], sh["K"], sh["n_tok"])
         assert name == best["kernel"], (sh["fmt"], sh["M"], sh["K"], sh["n_tok"], name, best)
+
+
+def test_attn_errors_and_workspace(lib):
+    """lw_attn_decode's checks in the documented order, and the workspace
+    size (heads x splits x (head_dim + 2) floats)."""
+    f = lib.lw_attn_decode
+
+    def call(fmt=Q8_0, q=A16, K=A256, V=A256, out=A16, H=32, kv=8, D=128, L=2048, scale=0.088, ws=A16, wsb=1 << 30):
+        return f(fmt, q, K, V, out, H, kv, D, L, scale, ws, wsb, None)
+    assert call(fmt=Q4_K) == LW_EFMT                      # a super-block format: rows of 128 hold no block
+    assert call(fmt=11, q=None) == LW_EFMT
+    assert call(q=None) == LW_EINVAL
+    assert call(ws=None) == LW_EINVAL
+    assert call(H=12) == LW_EINVAL                         # 12 heads over 8
+    assert call(H=96, kv=8) == LW_EINVAL                   # group of 12
+    assert call(D=96) == LW_EINVAL
+    assert call(L=0) == LW_EINVAL
+    assert call(scale=float("inf")) == LW_EINVAL
+    assert call(wsb=16) == LW_EINVAL                       # workspace too small
+    assert call(kv=1, H=1, D=64, L=3) == LW_ESHAPE         # 192 elements
+    assert call(K=A256 + 16) == LW_EALIGN
+    assert call(out=A16 + 4) == LW_EALIGN
+    wb = binding.attn_workspace_bytes(Q8_0, 32, 8, 128, 2048)
+    assert wb > 0 and wb % (32 * 130 * 4) == 0
+    assert binding.attn_workspace_bytes(Q8_0, 32, 8, 128, 1) == 32 * 130 * 4   # one split
+    assert lib.lw_attn_workspace_bytes(Q4_K, 32, 8, 128, 16) == LW_EFMT
