@@ -292,6 +292,21 @@ LW_API int64_t lw_attn_workspace_bytes(int fmt, int64_t n_heads, int64_t n_kv_he
                                        int64_t kv_len);
 
 /*
+ * lw_attn_decode_noalloc — lw_attn_decode without a workspace argument, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation). It allocates
+ * nothing: the partial results go to a fixed 4 MiB array of the library's
+ * own on each GPU (held until the process ends), so calls whose
+ * lw_attn_workspace_bytes exceeds 4 MiB return LW_EINVAL (32 heads over 8
+ * key/value heads of 128 need about 1 MiB at any length). Every call on a
+ * GPU shares that GPU's array: calls that overlap in time on one GPU race.
+ * Arguments, checks and results otherwise as lw_attn_decode's.
+ */
+LW_API int lw_attn_decode_noalloc(int fmt, const float* q, const void* K, const void* V, float* out,
+                                  int64_t n_heads, int64_t n_kv_heads, int64_t head_dim, int64_t kv_len,
+                                  float scale, void* stream);
+
+/*
  * lw_launch_count — the number of kernel launches lw_matvec(fmt, W, x, y, M,
  * K, n_tok, stream) makes for these sizes (1 for most calls; 2 where a fill
  * kernel zeroes y before a K-split prefill launch, or where tokens run as

@@ -16,7 +16,7 @@ LIB_PATH = os.path.join(HERE, "liblw.so")
 LW_OK = 0
 EXPORTS = ("lw_matvec", "lw_matvec_multi", "lw_dequant", "lw_weight_bytes", "lw_strerror", "lw_kernel_name",
            "lw_kernel_name_multi", "lw_launch_count", "lw_launch_count_multi", "lw_attn_decode",
-           "lw_attn_workspace_bytes")
+           "lw_attn_workspace_bytes", "lw_attn_decode_noalloc")
 LW_MULTI_MAX = 4
 
 
@@ -70,6 +70,8 @@ def library() -> ctypes.CDLL:
         lib.lw_attn_decode.restype = ctypes.c_int
         lib.lw_attn_workspace_bytes.argtypes = [ctypes.c_int, i64, i64, i64, i64]
         lib.lw_attn_workspace_bytes.restype = i64
+        lib.lw_attn_decode_noalloc.argtypes = [ctypes.c_int, vp, vp, vp, vp, i64, i64, i64, i64, ctypes.c_float, vp]
+        lib.lw_attn_decode_noalloc.restype = ctypes.c_int
         _lib = lib
     return _lib
 

@@ -237,9 +237,13 @@ int64_t lw_launch_count_multi(int fmt, int n_mat, const int64_t* M, int64_t K, i
 
 namespace {
 
+}  // namespace
+
+namespace lw {
+
 // The checks of lw_attn_decode that need no pointer, in the documented order.
 int check_attn(int fmt, int64_t n_heads, int64_t n_kv, int64_t head_dim, int64_t kv_len, float scale) {
-    if (!known_fmt(fmt) || !lw::attn_fmt_supported(fmt)) return LW_EFMT;
+    if (fmt < LW_F16 || fmt > LW_Q2_K || !lw::attn_fmt_supported(fmt)) return LW_EFMT;
     if (n_heads < 1 || n_kv < 1 || kv_len < 1 || n_heads > 4096 || kv_len >= ((int64_t)1 << 31) ||
         n_kv * kv_len > LW_MAX_ELEMS / 128)
         return LW_EINVAL;
@@ -252,12 +256,12 @@ int check_attn(int fmt, int64_t n_heads, int64_t n_kv, int64_t head_dim, int64_t
     return LW_OK;
 }
 
-}  // namespace
+}  // namespace lw
 
 extern "C" {
 
 int64_t lw_attn_workspace_bytes(int fmt, int64_t n_heads, int64_t n_kv_heads, int64_t head_dim, int64_t kv_len) {
-    const int rc = check_attn(fmt, n_heads, n_kv_heads, head_dim, kv_len, 1.0f);
+    const int rc = lw::check_attn(fmt, n_heads, n_kv_heads, head_dim, kv_len, 1.0f);
     if (rc != LW_OK) return rc;
     return lw::attn_plan(n_kv_heads, head_dim, kv_len, n_heads).ws_bytes;
 }
@@ -267,7 +271,7 @@ int lw_attn_decode(int fmt, const float* q, const void* K, const void* V, float*
                    int64_t workspace_bytes, void* stream) {
     if (!known_fmt(fmt) || !lw::attn_fmt_supported(fmt)) return LW_EFMT;
     if (!q || !K || !V || !out || !workspace) return LW_EINVAL;
-    const int rc = check_attn(fmt, n_heads, n_kv_heads, head_dim, kv_len, scale);
+    const int rc = lw::check_attn(fmt, n_heads, n_kv_heads, head_dim, kv_len, scale);
     if (rc != LW_OK) return rc;
     const lw::AttnPlan pl = lw::attn_plan(n_kv_heads, head_dim, kv_len, n_heads);
     if (workspace_bytes < pl.ws_bytes) return LW_EINVAL;

@@ -171,6 +171,9 @@ struct AttnPlan {
 };
 AttnPlan attn_plan(int64_t n_kv, int64_t head_dim, int64_t kv_len, int64_t n_heads);
 bool attn_fmt_supported(int fmt);
+// lw_attn_decode's checks that need no pointer, in the documented order
+// (LW_EFMT, LW_EINVAL, LW_ESHAPE); LW_OK when they pass.
+int check_attn(int fmt, int64_t n_heads, int64_t n_kv, int64_t head_dim, int64_t kv_len, float scale);
 hipError_t launch_attn(int fmt, const float* q, const uint8_t* K, const uint8_t* V, float* out, int64_t n_heads,
                        int64_t n_kv, int64_t head_dim, int64_t kv_len, float scale, const AttnPlan& pl, float* ws,
                        hipStream_t stream);
