@@ -51,6 +51,11 @@
  *     q2_K-style with 16 sub-blocks of 16, a 4-bit scale and a 4-bit min
  *     each against binary16 d and dmin, value = d * sc_j * q - dmin * m_j
  *     for 2-bit codes.
+ *   - Sec. 2.2 and Appendix B, mxfp4 (the microscaling 4-bit float format
+ *     the paper emulates for gpt-oss): blocks of 32 elements, each a 4-bit
+ *     float e2m1 (sign, 2-bit exponent with bias 1, 1-bit mantissa: the
+ *     magnitudes 0, 0.5, 1, 1.5, 2, 3, 4, 6), sharing an 8-bit power-of-two
+ *     scale E (e8m0): value = e2m1(code) * 2^(E - 127); E = 255 encodes NaN.
  *   - Sec. 2.1: decode is a matrix-vector product.
  *
  * Byte layout (the library's split-plane layout): plane 0 at offset 0; each
@@ -71,7 +76,8 @@
  * e/4), one int8 scale per 16 elements, one binary16 d per 256. q2_K: the
  * 2-bit codes (element e at bits 2(e mod 4) of byte e/4), one byte per 16
  * elements with the scale in bits 0-3 and the min in bits 4-7, then
- * {d, dmin} per 256.
+ * {d, dmin} per 256. mxfp4: the Q4 nibble plane of 4-bit codes, then one
+ * e8m0 byte per 32 elements.
  *
  * Build: gcc -O2 -ffp-contract=off -fPIC -shared -pthread (no fast-math, no
  * vector intrinsics). Results do not depend on the thread count: each output
@@ -86,7 +92,7 @@
 
 enum {
     OR_F16 = 0, OR_Q8_0 = 1, OR_Q4_0 = 2, OR_Q4_K = 3, OR_Q4_1 = 4, OR_Q1_0 = 5,
-    OR_Q5_0 = 6, OR_Q5_1 = 7, OR_Q5_K = 8, OR_Q6_K = 9, OR_Q2_K = 10
+    OR_Q5_0 = 6, OR_Q5_1 = 7, OR_Q5_K = 8, OR_Q6_K = 9, OR_Q2_K = 10, OR_MXFP4 = 11
 };
 
 /* Elements per block: a row of K elements starts a block when K is a multiple. */
@@ -163,6 +169,11 @@ static int planes(int fmt, int64_t n, int64_t off[4], int64_t* total) {
         off[3] = round_up_256(off[2] + n / 16);  /* int8 scale per 16 */
         *total = off[3] + 2 * (n / 256);         /* binary16 d per 256 */
         return 0;
+    case OR_MXFP4:
+        if (n % 32) return -1;
+        off[1] = round_up_256(n / 2);            /* 4-bit codes, two per byte */
+        *total = off[1] + n / 32;                /* one e8m0 exponent per 32 */
+        return 0;
     case OR_Q2_K:
         if (n % 256) return -1;
         off[1] = round_up_256(n / 4);            /* 2-bit codes, four per byte */
@@ -237,6 +248,15 @@ static unsigned two_bits(const uint8_t* plane, int64_t e) {
  * two bits from plane 1. */
 static unsigned q6_code(const uint8_t* W, const int64_t off[4], int64_t e) {
     return q4_code(W, e) | (two_bits(W + off[1], e) << 4);
+}
+
+/* Magnitude of a 4-bit e2m1 float (bits 0-2 of the code; bit 3 is the sign):
+ * exponent field e (bits 1-2, bias 1), mantissa bit m (bit 0); e = 0 is the
+ * subnormal m * 2^-1, otherwise 2^(e - 1) * (1 + m/2). */
+static double e2m1_magnitude(unsigned code) {
+    unsigned e = (code >> 1) & 3u, m = code & 1u;
+    if (e == 0) return 0.5 * (double)m;
+    return ldexp(1.0 + 0.5 * (double)m, (int)e - 1);
 }
 
 /* ---- dequantization: exact closed form, one rounding ---------------------- */
@@ -317,6 +337,13 @@ static double exact_value(int fmt, const uint8_t* W, const int64_t off[4], int64
         /* |sc| <= 2^7 and |q - 32| <= 2^5: <= 23 significant bits, exact in
          * float as well */
         return d * (double)sc * (double)(q - 32);
+    }
+    case OR_MXFP4: {
+        unsigned c = q4_code(W, e);
+        unsigned E = W[off[1] + e / 32];
+        if (E == 255) return NAN;
+        double v = e2m1_magnitude(c) * ldexp(1.0, (int)E - 127); /* exact in double */
+        return (c & 8u) ? -v : v;
     }
     case OR_Q2_K: {
         int64_t S = e / 256;

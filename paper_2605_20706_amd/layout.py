@@ -27,6 +27,8 @@ the previous one rounded up to 256 bytes):
 * q6_k  plane 0: the low four bits of each 6-bit code, as q4_0's plane 0;
         plane 1: n/4 bytes of high two bits, element e at bits 2(e mod 4) of byte e/4;
         plane 2: n/16 x int8 scale (sub-block of 16);  plane 3: n/256 x binary16 d
+* mxfp4 plane 0: 4-bit e2m1 codes (sign in bit 3), as q4_0's plane 0;
+        plane 1: n/32 e8m0 exponent bytes E (value = e2m1 * 2^(E - 127))
 * q2_k  plane 0: n/4 bytes of 2-bit codes, element e at bits 2(e mod 4) of byte e/4;
         plane 1: n/16 bytes, sub-block scale in bits 0-3 and min in bits 4-7;
         plane 2: n/256 x {binary16 d, binary16 dmin}
@@ -36,14 +38,14 @@ from __future__ import annotations
 import numpy as np
 
 F16, Q8_0, Q4_0, Q4_K, Q4_1, Q1_0 = 0, 1, 2, 3, 4, 5
-Q5_0, Q5_1, Q5_K, Q6_K, Q2_K = 6, 7, 8, 9, 10
+Q5_0, Q5_1, Q5_K, Q6_K, Q2_K, MXFP4 = 6, 7, 8, 9, 10, 11
 FORMATS = {"f16": F16, "q8_0": Q8_0, "q4_0": Q4_0, "q4_k": Q4_K, "q4_1": Q4_1, "q1_0": Q1_0,
-           "q5_0": Q5_0, "q5_1": Q5_1, "q5_k": Q5_K, "q6_k": Q6_K, "q2_k": Q2_K}
+           "q5_0": Q5_0, "q5_1": Q5_1, "q5_k": Q5_K, "q6_k": Q6_K, "q2_k": Q2_K, "mxfp4": MXFP4}
 FORMAT_NAMES = {v: k for k, v in FORMATS.items()}
 # Packed bytes per weight (codes and scales, ignoring plane padding).
 BYTES_PER_WEIGHT = {F16: 2.0, Q8_0: 34.0 / 32.0, Q4_0: 18.0 / 32.0, Q4_K: 144.0 / 256.0, Q4_1: 20.0 / 32.0,
                     Q1_0: 18.0 / 128.0, Q5_0: 22.0 / 32.0, Q5_1: 24.0 / 32.0, Q5_K: 176.0 / 256.0,
-                    Q6_K: 210.0 / 256.0, Q2_K: 84.0 / 256.0}
+                    Q6_K: 210.0 / 256.0, Q2_K: 84.0 / 256.0, MXFP4: 17.0 / 32.0}
 
 ALIGN = 256
 
@@ -109,6 +111,11 @@ def _plane_offsets3(fmt: int, n: int):
             raise ValueError("n must be a multiple of 128")
         o1 = _up(n // 8)
         return (0, o1, 0), o1 + 2 * (n // 128)
+    if fmt == MXFP4:
+        if n % 32:
+            raise ValueError("n must be a multiple of 32")
+        o1 = _up(n // 2)
+        return (0, o1, 0), o1 + n // 32
     if fmt == Q4_K:
         if n % 256:
             raise ValueError("n must be a multiple of 256")
@@ -310,3 +317,13 @@ def pack_q2_k(q, sc, m, d, dmin) -> np.ndarray:
     dd[:, 0] = d
     dd[:, 1] = dmin
     return assemble(Q2_K, n, pack_2bit(q), (sc | (m << 4)).astype(np.uint8), dd)
+
+
+def pack_mxfp4(codes, E) -> np.ndarray:
+    """4-bit e2m1 codes (n,) in [0, 15] (bit 3 the sign) and e8m0 exponents
+    (n/32,) in [0, 255] -> the mxfp4 layout."""
+    codes = np.asarray(codes).reshape(-1)
+    E = np.asarray(E, dtype=np.uint8).reshape(-1)
+    if E.size * 32 != codes.size:
+        raise ValueError("need one exponent per 32 codes")
+    return assemble(MXFP4, codes.size, pack_nibbles(codes), E)

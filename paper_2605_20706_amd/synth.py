@@ -26,6 +26,8 @@ Q8_0 matrix uses the literal seed 0):
         [1e-5, 2e-4] -> binary16 (the lower part binary16 subnormals);
 * q2_k  codes uniform in [0, 3]; 4-bit scales and mins uniform in [0, 15]; d and
         dmin as q4_k;
+* mxfp4 e2m1 codes uniform in [0, 15]; e8m0 exponents uniform in [118, 124]
+        (block scales 2^-9 .. 2^-3, weights up to 6 * 2^-3);
 * x     float32 N(0, 1), shape [n_tok, K], from the generator of the workload
         (matrix_id 99).
 """
@@ -36,7 +38,7 @@ from dataclasses import dataclass
 import numpy as np
 
 from . import layout
-from .layout import F16, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
+from .layout import F16, MXFP4, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
 
 
 @dataclass(frozen=True)
@@ -177,6 +179,9 @@ def gen_fields(fmt: int, n: int, rng: np.random.Generator) -> dict:
         return {"q": rng.integers(0, 64, n, dtype=np.uint8),
                 "sc": rng.integers(-128, 128, n // 16, dtype=np.int8),
                 "d": _uniform_half(rng, 1e-5, 2e-4, n // 256)}
+    if fmt == MXFP4:
+        return {"q": rng.integers(0, 16, n, dtype=np.uint8),
+                "E": rng.integers(118, 125, n // 32, dtype=np.uint8)}
     if fmt == Q2_K:
         return {"q": rng.integers(0, 4, n, dtype=np.uint8),
                 "sc": rng.integers(0, 16, n // 16, dtype=np.uint8),
@@ -207,13 +212,15 @@ def pack_fields(fmt: int, f: dict) -> np.ndarray:
         return layout.pack_q6_k(f["q"], f["sc"], f["d"])
     if fmt == Q2_K:
         return layout.pack_q2_k(f["q"], f["sc"], f["m"], f["d"], f["dmin"])
+    if fmt == MXFP4:
+        return layout.pack_mxfp4(f["q"], f["E"])
     return layout.pack_q4_k(f["q"], f["sc"], f["m"], f["d"], f["dmin"])
 
 
 def gen_packed(fmt: int, n: int, rng: np.random.Generator) -> np.ndarray:
     """n packed elements per the recipe. The 4-bit code plane is drawn as
     uniform random bytes (same distribution as two uniform nibbles)."""
-    if fmt in (F16, Q8_0, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K):
+    if fmt in (F16, Q8_0, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K, MXFP4):
         return pack_fields(fmt, gen_fields(fmt, n, rng))
     offs, total = layout.plane_offsets(fmt, n)
     out = np.zeros(total, dtype=np.uint8)
@@ -319,6 +326,17 @@ def gen_fields_eq1(fmt: int, n: int, rng: np.random.Generator, sigma: float = 0.
         with np.errstate(divide="ignore", invalid="ignore"):
             r = np.where(s > 0, _round_half_away((w - mu) / s), 0.0)
         return {"q": np.clip(r, 0, 31).astype(np.uint8), "d": d, "m": m}
+    if fmt == MXFP4:
+        # the block exponent puts the largest magnitude at or below 6 * 2^(E - 127)
+        # (E = ceil(log2(amax / 6)) + 127), each weight the nearest e2m1 magnitude
+        amax = np.abs(blk).max(axis=1)
+        with np.errstate(divide="ignore"):
+            E = np.clip(np.ceil(np.log2(np.where(amax > 0, amax, 1.0) / 6.0)) + 127, 0, 254).astype(np.int64)
+        s = np.repeat(np.ldexp(1.0, E - 127), 32)
+        mags = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])
+        a = np.abs(w) / s
+        idx = np.abs(a[:, None] - mags[None, :]).argmin(axis=1)
+        return {"q": (idx + 8 * (w < 0)).astype(np.uint8), "E": E.astype(np.uint8)}
     if fmt == Q6_K:
         b16 = w.reshape(-1, 16)
         scale = np.abs(b16).max(axis=1) / 31
@@ -417,6 +435,8 @@ def zero_rows(fmt: int, f: dict, rows, K: int) -> dict:
         f["m"][grp] = 3 * sc
     elif fmt == Q6_K:
         f["q"][el] = 32
+    elif fmt == MXFP4:
+        f["q"][el] = np.where(np.arange(el.size) % 2 == 0, 0, 8)  # +0 and -0
     elif fmt == Q2_K:
         f["q"][el] = 3
         sup = np.unique(el // 256)
@@ -437,6 +457,10 @@ def zero_scales(fmt: int, f: dict, rng: np.random.Generator, frac: float = 0.25)
     unchanged."""
     f = {k: v.copy() for k, v in f.items()}
     if fmt == F16:
+        return f
+    if fmt == MXFP4:
+        # the smallest exponent: a block scale of 2^-127 (binary32 subnormal products)
+        f["E"][rng.random(f["E"].size) < frac] = 0
         return f
     d = f["d"]
     pick = rng.random(d.size) < frac

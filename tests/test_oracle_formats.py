@@ -12,10 +12,10 @@ import pytest
 
 import golden_io
 from paper_2605_20706_amd import layout
-from paper_2605_20706_amd.layout import F16, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
+from paper_2605_20706_amd.layout import F16, MXFP4, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
 
 FMT = {"f16": F16, "q8_0": Q8_0, "q4_0": Q4_0, "q4_k": Q4_K, "q4_1": Q4_1, "q1_0": Q1_0,
-       "q5_0": Q5_0, "q5_1": Q5_1, "q5_k": Q5_K, "q6_k": Q6_K, "q2_k": Q2_K}
+       "q5_0": Q5_0, "q5_1": Q5_1, "q5_k": Q5_K, "q6_k": Q6_K, "q2_k": Q2_K, "mxfp4": MXFP4}
 
 
 def bits(a):
@@ -171,6 +171,10 @@ def _block_for(name, f):
         if name == "q5_0":
             return layout.pack_q5_0(q, np.repeat(h(f["d"]), 8)), 0
         return layout.pack_q5_1(q, np.repeat(h(f["d"]), 8), np.repeat(h(f["m"]), 8)), 0
+    if name == "mxfp4":
+        q = np.zeros(256, np.uint8)
+        q[0] = f["q"]
+        return layout.pack_mxfp4(q, np.full(8, f["E"], np.uint8)), 0
     if name == "q6_k":
         q = np.zeros(256, np.uint8)
         q[0] = f["q"]
@@ -202,7 +206,7 @@ def test_hand_values(oracle_mod):
         W, e = _block_for(name, f)
         got = oracle_mod.dequant(FMT[name], W, 256)[e]
         assert bits(got) == np.uint32(want_bits), (name, f, hex(int(bits(got))), hex(want_bits))
-        assert got == np.float32(want)
+        assert got == np.float32(want) or (np.isinf(want) and got == np.float32(want))
 
 
 def test_q4_0_nibble_order_hand_bytes(oracle_mod):
@@ -508,3 +512,40 @@ def test_roundtrip_eq1_new_formats(oracle_mod, fmt):
     assert (np.abs(w - got)[inner] <= tol[inner] * (1 + 1e-9)).all()
     assert inner.mean() > 0.5
     del rng
+
+
+# --------------------------------------------------------------------------- mxfp4
+
+E2M1 = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])
+
+
+def test_mxfp4_every_code_every_exponent(oracle_mod):
+    """16 codes x all 256 e8m0 exponents against numpy: the e2m1 magnitude
+    table (from its definition, by hand) times 2^(E - 127) with numpy's
+    ldexp, cast to float32 (overflow to +-inf); E = 255 is NaN."""
+    E = np.repeat(np.arange(256), 1).astype(np.uint8)
+    codes = np.tile(np.concatenate([np.arange(16), np.arange(16)]).astype(np.uint8), E.size)
+    got = oracle_mod.dequant(MXFP4, layout.pack_mxfp4(codes, E), codes.size).reshape(256, 32)
+    mag = E2M1[np.arange(16) & 7] * np.where(np.arange(16) >= 8, -1.0, 1.0)
+    with np.errstate(over="ignore"):
+        ref = (np.ldexp(np.tile(mag, 2)[None, :], (np.arange(256) - 127)[:, None])).astype(np.float32)
+    nan = np.arange(256) == 255
+    assert np.isnan(got[nan]).all()
+    assert same_bits_or_both_zero(got[~nan], ref[~nan]).all()
+    assert np.array_equal(np.signbit(got[~nan]), np.signbit(ref[~nan]))  # -0 for code 8
+
+
+def test_mxfp4_roundtrip_eq1(oracle_mod):
+    """Gaussian weights encoded with the largest magnitude at or below
+    6 * 2^(E - 127) and each weight at its nearest e2m1 level: the error is
+    at most half the local level spacing (0.25, 0.5 or 1 times the scale)."""
+    from paper_2605_20706_amd import synth
+    n = 32 * 4096
+    f = synth.gen_fields_eq1(MXFP4, n, np.random.default_rng(44))
+    w = np.random.default_rng(44).standard_normal(n) * 0.02
+    got = oracle_mod.dequant(MXFP4, synth.pack_fields(MXFP4, f), n).astype(np.float64)
+    s = np.repeat(np.ldexp(1.0, f["E"].astype(np.int64) - 127), 32)
+    a = np.abs(w) / s
+    half_gap = np.where(a <= 2, 0.25, np.where(a <= 4, 0.5, 1.0))
+    assert (np.abs(w - got) <= half_gap * s * (1 + 1e-12)).all()
+    assert (np.abs(w) <= 6 * s).all()

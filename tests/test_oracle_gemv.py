@@ -11,9 +11,9 @@ import numpy as np
 import pytest
 
 from paper_2605_20706_amd import layout, synth
-from paper_2605_20706_amd.layout import F16, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
+from paper_2605_20706_amd.layout import F16, MXFP4, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
 
-ALL = [F16, Q8_0, Q4_0, Q4_K, Q4_1, Q1_0, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K]
+ALL = [F16, Q8_0, Q4_0, Q4_K, Q4_1, Q1_0, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K, MXFP4]
 
 
 def make(fmt, M, K, seed):
@@ -74,7 +74,7 @@ def test_linearity_and_token_independence(oracle_mod, fmt):
     assert np.allclose(yc[0], 2 * ya[0] + yb[0], rtol=0, atol=1e-6 * (2 * Aa[0] + Ab[0]).max())
 
 
-@pytest.mark.parametrize("fmt", [Q8_0, Q4_0, Q4_K, Q4_1, Q1_0, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K])
+@pytest.mark.parametrize("fmt", [Q8_0, Q4_0, Q4_K, Q4_1, Q1_0, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K, MXFP4])
 def test_power_of_two_scale(oracle_mod, fmt):
     """Doubling every binary16 scale and min (exponent + 1, no overflow)
     doubles y exactly."""
@@ -86,6 +86,8 @@ def test_power_of_two_scale(oracle_mod, fmt):
     for key in (("d", "m") if fmt in (Q4_1, Q5_1) else ("d", "dmin")):
         if key in f2:
             f2[key] = (f2[key].astype(np.float64) * 2).astype(np.float16)
+    if fmt == MXFP4:
+        f2["E"] = (f2["E"] + 1).astype(np.uint8)  # e8m0 exponent + 1: the block scale doubles
     W2 = synth.pack_fields(fmt, f2)
     x = synth.gen_x_seeded(9, K, 2)
     y, _, _ = oracle_mod.matvec(fmt, W, x, M, K)

@@ -67,6 +67,11 @@ MUTANTS = [
      "double v = (double)(float)exact_value(fmt, Kc, offv, (g * kv_len + j) * head_dim + d);"),
     ("attention: last position skipped in the normalisation", "        for (int64_t j = 0; j < kv_len; ++j) {\n            s[j] = exp(s[j] - smax);",
      "        for (int64_t j = 0; j + 1 < kv_len; ++j) {\n            s[j] = exp(s[j] - smax);"),
+    ("e2m1 exponent bias 0", "return ldexp(1.0 + 0.5 * (double)m, (int)e - 1);",
+     "return ldexp(1.0 + 0.5 * (double)m, (int)e);"),
+    ("e2m1 sign ignored", "return (c & 8u) ? -v : v;", "return v;"),
+    ("e8m0 bias 126", "double v = e2m1_magnitude(c) * ldexp(1.0, (int)E - 127);",
+     "double v = e2m1_magnitude(c) * ldexp(1.0, (int)E - 126);"),
     ("term mass without the code shift", "return fabs(s) * (q + (double)beta) + fabs(mu - (double)beta * s);",
      "return fabs(s) * q + fabs(mu - (double)beta * s);"),
     ("term mass offset taken with its sign", "fabs(mu - (double)beta * s);", "(mu - (double)beta * s);"),

@@ -12,7 +12,7 @@ import numpy as np
 import pytest
 
 from paper_2605_20706_amd import synth
-from paper_2605_20706_amd.layout import F16, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
+from paper_2605_20706_amd.layout import F16, MXFP4, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
 
 M, K = 9, 512
 
@@ -31,7 +31,7 @@ def F_of(oracle_mod, fmt, f, x, beta):
     return F
 
 
-@pytest.mark.parametrize("fmt", [F16, Q8_0])
+@pytest.mark.parametrize("fmt", [F16, Q8_0, MXFP4])
 @pytest.mark.parametrize("beta", [0, 128])
 def test_no_offset_formats_have_F_equal_A(oracle_mod, fmt, beta):
     f = fields(fmt, 1)
