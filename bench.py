@@ -511,7 +511,7 @@ def timed_parity(ws, refs, y_timed, n_threads):
     for i, (y_ref, A, _) in refs.items():
         m = ws.mats[i]
         y = y_timed[i].astype(np.float64).reshape(y_ref.shape)
-        if wl.fmt in (layout.F16, layout.Q8_0):
+        if wl.fmt in (layout.F16, layout.Q8_0, layout.MXFP4):
             F = np.zeros_like(A)
         else:
             beta = 128 if kern_of[i].split("<")[0] in MFMA_KERNELS else 0

@@ -77,6 +77,13 @@
  *           plane 1: n/16 bytes, sc[t] in bits 0-3 and m[t] in bits 4-7;
  *           plane 2: n/256 x { binary16 d, binary16 dmin }.
  *                                    value = d[S] * sc[t] * q[e] - dmin[S] * m[t]
+ *   LW_MXFP4 plane 0: 4-bit e2m1 codes as LW_Q4_0's plane 0 (bit 3 the sign,
+ *                    bits 1-2 an exponent e with bias 1, bit 0 a mantissa m:
+ *                    e2m1 = m/2 for e = 0, else 2^(e-1) * (1 + m/2));
+ *           plane 1: n/32 bytes, an e8m0 exponent E per group.
+ *                                    value = e2m1(q[e]) * 2^(E[g] - 127)
+ *                    (E = 255 is NaN; 2^(E-127) below 2^-126 and products
+ *                    beyond binary32's range round as binary32 does)
  *
  * The dequantized value of an element is the exact real value of its closed
  * form rounded once to binary32 with round-to-nearest-even. For LW_F16,
@@ -84,7 +91,8 @@
  * for LW_Q4_K the two products are exact and the difference is rounded once;
  * for LW_Q4_1 the product is exact and the sum with the min is rounded once;
  * LW_Q1_0's value is +-d, exact. LW_Q5_0 and LW_Q6_K are exact; LW_Q5_1,
- * LW_Q5_K and LW_Q2_K round once, as LW_Q4_1 and LW_Q4_K.
+ * LW_Q5_K and LW_Q2_K round once, as LW_Q4_1 and LW_Q4_K. LW_MXFP4 is exact
+ * except for overflow to infinity.
  * ------------------------------------------------------------------------
  */
 #ifndef LW_H
@@ -109,10 +117,12 @@ extern "C" {
  * Q4_0, Q5_0) and with (Q4_1, Q5_1) an offset, K-quant super-blocks of 256
  * with double-quantized scales (and mins) at 2, 4, 5 and 6 bits per code,
  * and the 1-bit symmetric q1_0 with one scale per 128 weights; Sec. 7 and
- * Appendix B list q2_k .. q6_k). */
+ * Appendix B list q2_k .. q6_k; mxfp4, 4-bit floats with a shared
+ * power-of-two scale, which the paper emulates for gpt-oss and MI355X's
+ * matrix cores take natively). */
 typedef enum {
     LW_F16 = 0, LW_Q8_0 = 1, LW_Q4_0 = 2, LW_Q4_K = 3, LW_Q4_1 = 4, LW_Q1_0 = 5,
-    LW_Q5_0 = 6, LW_Q5_1 = 7, LW_Q5_K = 8, LW_Q6_K = 9, LW_Q2_K = 10
+    LW_Q5_0 = 6, LW_Q5_1 = 7, LW_Q5_K = 8, LW_Q6_K = 9, LW_Q2_K = 10, LW_MXFP4 = 11
 } lw_fmt;
 
 /* Return codes. */
@@ -252,8 +262,8 @@ LW_API const char* lw_kernel_name_multi(int fmt, int n_mat, const int64_t* M, in
  *   s_j = scale * sum_d q[h][d] * k[g][j][d],  p = softmax over j of s,
  *   out[h][d] = sum_j p_j * v[g][j][d].
  *
- *   fmt        LW_F16, LW_Q8_0, LW_Q4_0, LW_Q4_1, LW_Q5_0 or LW_Q5_1 (formats
- *              whose blocks fit a head's row); both caches share it.
+ *   fmt        LW_F16, LW_Q8_0, LW_Q4_0, LW_Q4_1, LW_Q5_0, LW_Q5_1 or LW_MXFP4
+ *              (formats whose blocks fit a head's row); both caches share it.
  *   q          device; float32 [n_heads][head_dim], 16-byte aligned.
  *   K, V       device; each n_kv_heads * kv_len * head_dim elements in the
  *              packed layout above, element (g * kv_len + j) * head_dim + d

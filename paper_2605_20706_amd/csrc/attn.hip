@@ -241,7 +241,8 @@ AttnPlan attn_plan(int64_t n_kv, int64_t head_dim, int64_t kv_len, int64_t n_hea
 }
 
 bool attn_fmt_supported(int fmt) {
-    return fmt == LW_F16 || fmt == LW_Q8_0 || fmt == LW_Q4_0 || fmt == LW_Q4_1 || fmt == LW_Q5_0 || fmt == LW_Q5_1;
+    return fmt == LW_F16 || fmt == LW_Q8_0 || fmt == LW_Q4_0 || fmt == LW_Q4_1 || fmt == LW_Q5_0 || fmt == LW_Q5_1 ||
+           fmt == LW_MXFP4;
 }
 
 hipError_t launch_attn(int fmt, const float* q, const uint8_t* K, const uint8_t* V, float* out, int64_t n_heads,
@@ -254,6 +255,7 @@ hipError_t launch_attn(int fmt, const float* q, const uint8_t* K, const uint8_t*
     case LW_Q4_1: return launch_f<LW_Q4_1>(q, K, V, out, n_heads, n_kv, head_dim, kv_len, scale, pl, ws, stream);
     case LW_Q5_0: return launch_f<LW_Q5_0>(q, K, V, out, n_heads, n_kv, head_dim, kv_len, scale, pl, ws, stream);
     case LW_Q5_1: return launch_f<LW_Q5_1>(q, K, V, out, n_heads, n_kv, head_dim, kv_len, scale, pl, ws, stream);
+    case LW_MXFP4: return launch_f<LW_MXFP4>(q, K, V, out, n_heads, n_kv, head_dim, kv_len, scale, pl, ws, stream);
     default: return hipErrorInvalidValue;
     }
 }

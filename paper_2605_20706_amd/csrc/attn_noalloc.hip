@@ -48,7 +48,7 @@ extern "C" {
 LW_API int lw_attn_decode_noalloc(int fmt, const float* q, const void* K, const void* V, float* out,
                                   int64_t n_heads, int64_t n_kv_heads, int64_t head_dim, int64_t kv_len,
                                   float scale, void* stream) {
-    if (fmt < LW_F16 || fmt > LW_Q2_K || !lw::attn_fmt_supported(fmt)) return LW_EFMT;
+    if (fmt < LW_F16 || fmt > LW_MXFP4 || !lw::attn_fmt_supported(fmt)) return LW_EFMT;
     if (!q || !K || !V || !out) return LW_EINVAL;
     const int rc = lw::check_attn(fmt, n_heads, n_kv_heads, head_dim, kv_len, scale);
     if (rc != LW_OK) return rc;

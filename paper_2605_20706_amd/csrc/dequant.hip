@@ -81,6 +81,7 @@ hipError_t launch_dequant(int fmt, const uint8_t* W, float* out, int64_t n, cons
     case LW_Q5_K: return launch<LW_Q5_K>(W, out, n, p, stream);
     case LW_Q6_K: return launch<LW_Q6_K>(W, out, n, p, stream);
     case LW_Q2_K: return launch<LW_Q2_K>(W, out, n, p, stream);
+    case LW_MXFP4: return launch<LW_MXFP4>(W, out, n, p, stream);
     default: return hipErrorInvalidValue;
     }
 }

@@ -638,6 +638,64 @@ struct Traits<LW_Q2_K> {
     }
 };
 
+// mxfp4: e2m1 codes in the Q4 nibble order and one e8m0 exponent per group.
+// Each code becomes the binary16 e2m1 * 2^-14 (its magnitude bits moved to
+// bits 9-11, its sign to bit 15), so every product is one v_fma_mix_f32 in
+// units of 2^-14; the lane's sum is scaled by 2^14 and the block's 2^(E-127).
+__device__ __forceinline__ float e2m1_dot(const uint4& c, const float4* xv) {
+    const uint32_t w[4] = {c.x, c.y, c.z, c.w};
+    float lo_s = 0.f, hi_s = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const uint32_t v = w[i];
+        const uint32_t l02 = opaque(((v & 0x00070007u) << 9) | ((v & 0x00080008u) << 12));  // elements 4i, 4i+2
+        const uint32_t h02 = opaque(((v & 0x00700070u) << 5) | ((v & 0x00800080u) << 8));   // 16+4i, 16+4i+2
+        const uint32_t l13 = opaque(((v & 0x07000700u) << 1) | ((v & 0x08000800u) << 4));   // 4i+1, 4i+3
+        const uint32_t h13 = opaque(((v & 0x70007000u) >> 3) | (v & 0x80008000u));         // 16+4i+1, 16+4i+3
+        lo_s = __builtin_fmaf(half_of<0>(l02), xv[i].x, lo_s);
+        lo_s = __builtin_fmaf(half_of<1>(l02), xv[i].z, lo_s);
+        lo_s = __builtin_fmaf(half_of<0>(l13), xv[i].y, lo_s);
+        lo_s = __builtin_fmaf(half_of<1>(l13), xv[i].w, lo_s);
+        hi_s = __builtin_fmaf(half_of<0>(h02), xv[4 + i].x, hi_s);
+        hi_s = __builtin_fmaf(half_of<1>(h02), xv[4 + i].z, hi_s);
+        hi_s = __builtin_fmaf(half_of<0>(h13), xv[4 + i].y, hi_s);
+        hi_s = __builtin_fmaf(half_of<1>(h13), xv[4 + i].w, hi_s);
+    }
+    return (lo_s + hi_s) * 16384.0f;  // 2^14
+}
+
+template <>
+struct Traits<LW_MXFP4> {
+    static constexpr int EPL = 32;
+    static constexpr bool kGroupSums = false;
+    struct Packet {
+        uint4 c;
+        uint32_t E;
+    };
+    __device__ static Packet load(const uint8_t* W, int64_t e, int64_t off1, int64_t, int64_t = 0) {
+        Packet p;
+        p.c = *reinterpret_cast<const uint4*>(W + (e >> 1));
+        p.E = W[off1 + (e >> 5)];
+        return p;
+    }
+    struct Base {
+        uint32_t c, E;
+    };
+    __device__ static Base base(uint32_t row, uint32_t K, uint32_t c) {  // chunk = 2048 elements
+        return {row * (K / 2u) + 1024u * c, row * (K / 32u) + 64u * c};
+    }
+    __device__ static Packet load_at(const uint8_t* W, const uint8_t* P1, const uint8_t*, const Base& b, uint32_t la,
+                                     const uint8_t* = nullptr) {
+        Packet p;
+        p.c = stream_load16(W + b.c + 16u * la);
+        p.E = P1[b.E + la];
+        return p;
+    }
+    __device__ static float dot(const Packet& p, const float4* xv, float, int) {
+        return e2m1_dot(p.c, xv) * e8m0_to_float(p.E);
+    }
+};
+
 // Scaled forms for the register kernel: the lane's 32 products are
 // accumulated in units of 2^-24 (the value of a nibble masked into the low
 // bits of a binary16 half), so no per-step rescaling is needed; the caller
@@ -1589,6 +1647,7 @@ hipError_t launch_gemv_multi(int fmt, int n, const uint8_t* const* W, float* con
     case LW_Q5_K: return launch_multi_fmt<LW_Q5_K>(n, W, y, M, x, K, stream);
     case LW_Q6_K: return launch_multi_fmt<LW_Q6_K>(n, W, y, M, x, K, stream);
     case LW_Q2_K: return launch_multi_fmt<LW_Q2_K>(n, W, y, M, x, K, stream);
+    case LW_MXFP4: return launch_multi_fmt<LW_MXFP4>(n, W, y, M, x, K, stream);
     default: return hipErrorInvalidValue;
     }
 }
@@ -1637,6 +1696,7 @@ hipError_t launch_gemv_blocks(int fmt, const uint8_t* W, const float* x, float* 
     case LW_Q5_K: return launch_blocks_fmt<LW_Q5_K>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q6_K: return launch_blocks_fmt<LW_Q6_K>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q2_K: return launch_blocks_fmt<LW_Q2_K>(W, x, y, M, K, n_tok, p, stream);
+    case LW_MXFP4: return launch_blocks_fmt<LW_MXFP4>(W, x, y, M, K, n_tok, p, stream);
     default: return hipErrorInvalidValue;
     }
 }
@@ -1655,6 +1715,7 @@ hipError_t launch_gemv(int fmt, const uint8_t* W, const float* x, float* y, int6
     case LW_Q5_K: return launch_fmt<LW_Q5_K>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q6_K: return launch_fmt<LW_Q6_K>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q2_K: return launch_fmt<LW_Q2_K>(W, x, y, M, K, n_tok, p, stream);
+    case LW_MXFP4: return launch_fmt<LW_MXFP4>(W, x, y, M, K, n_tok, p, stream);
     default: return hipErrorInvalidValue;
     }
 }

@@ -20,7 +20,7 @@
 namespace {
 
 bool known_fmt(int fmt) {
-    return fmt >= LW_F16 && fmt <= LW_Q2_K;
+    return fmt >= LW_F16 && fmt <= LW_MXFP4;
 }
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
@@ -243,7 +243,7 @@ namespace lw {
 
 // The checks of lw_attn_decode that need no pointer, in the documented order.
 int check_attn(int fmt, int64_t n_heads, int64_t n_kv, int64_t head_dim, int64_t kv_len, float scale) {
-    if (fmt < LW_F16 || fmt > LW_Q2_K || !lw::attn_fmt_supported(fmt)) return LW_EFMT;
+    if (fmt < LW_F16 || fmt > LW_MXFP4 || !lw::attn_fmt_supported(fmt)) return LW_EFMT;
     if (n_heads < 1 || n_kv < 1 || kv_len < 1 || n_heads > 4096 || kv_len >= ((int64_t)1 << 31) ||
         n_kv * kv_len > LW_MAX_ELEMS / 128)
         return LW_EINVAL;

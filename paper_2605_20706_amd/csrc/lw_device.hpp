@@ -63,4 +63,17 @@ __device__ __forceinline__ float wave_sum_to_lane63(float v) {
     return v;
 }
 
+// 2^(E - 127) for an e8m0 exponent byte E, as float32: E = 0 is the
+// subnormal 2^-127, E = 255 NaN.
+__device__ __forceinline__ float e8m0_to_float(uint32_t E) {
+    const uint32_t b = E == 0 ? 0x00400000u : (E == 255 ? 0x7FC00000u : (E << 23));
+    return __builtin_bit_cast(float, b);
+}
+
+// A 4-bit e2m1 code in bits 0-3 of a 16-bit half made the binary16 of
+// e2m1 * 2^-14: its magnitude bits to bits 9-11 (exponent bits 10-11 and the
+// top mantissa bit), its sign to bit 15 (exact for every code; e = 0 lands
+// in the binary16 subnormals).
+__device__ __forceinline__ uint32_t e2m1_half_bits(uint32_t c) { return ((c & 7u) << 9) | ((c & 8u) << 12); }
+
 }  // namespace lw

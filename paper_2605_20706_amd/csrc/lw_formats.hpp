@@ -38,6 +38,19 @@ __device__ __forceinline__ float4 value4(const uint8_t* __restrict__ W, int64_t 
         v.y = (b & 2u) ? d : -d;
         v.z = (b & 4u) ? d : -d;
         v.w = (b & 8u) ? d : -d;
+    } else if constexpr (FMT == LW_MXFP4) {
+        // e2m1 codes in the Q4 nibble order; one e8m0 exponent per group
+        const int64_t g = e >> 5;
+        const int i0 = (int)(e & 31);
+        uint32_t b = *reinterpret_cast<const uint32_t*>(W + 16 * g + (i0 & 15));
+        b = (i0 < 16) ? (b & 0x0F0F0F0Fu) : ((b >> 4) & 0x0F0F0F0Fu);
+        const float s = e8m0_to_float(W[off1 + g]);
+        // binary16 e2m1 * 2^-14, times 2^14 (exact), times the scale (exact
+        // unless the product leaves binary32's range)
+        v.x = half_bits_to_float(e2m1_half_bits(b & 15u)) * 16384.0f * s;
+        v.y = half_bits_to_float(e2m1_half_bits((b >> 8) & 15u)) * 16384.0f * s;
+        v.z = half_bits_to_float(e2m1_half_bits((b >> 16) & 15u)) * 16384.0f * s;
+        v.w = half_bits_to_float(e2m1_half_bits(b >> 24)) * 16384.0f * s;
     } else if constexpr (FMT == LW_Q2_K) {
         // four 2-bit codes of byte e/4; the sub-block's {scale, min} byte
         const uint32_t b = W[e >> 2];

@@ -101,6 +101,10 @@ inline Planes planes_of(int fmt, int64_t n) {
         p.off3 = round_up_256(p.off2 + n / 16);
         p.total = p.off3 + 2 * (n / 256);
         break;
+    case LW_MXFP4:
+        p.off1 = round_up_256(n / 2);
+        p.total = p.off1 + n / 32;
+        break;
     case LW_Q2_K:
         p.off1 = round_up_256(n / 4);
         p.off2 = round_up_256(p.off1 + n / 16);

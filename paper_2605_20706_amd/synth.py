@@ -120,7 +120,8 @@ WORKLOADS = {
                                     ("q5_1", 9, Q5_1, "Q5_1 (5-bit legacy blocks with a min)"),
                                     ("q5_k", 10, Q5_K, "Q5_K-style (5-bit K-quant)"),
                                     ("q6_k", 11, Q6_K, "Q6_K-style (6-bit K-quant, 16-element sub-blocks)"),
-                                    ("q2_k", 12, Q2_K, "Q2_K-style (2-bit K-quant, 16-element sub-blocks)"))},
+                                    ("q2_k", 12, Q2_K, "Q2_K-style (2-bit K-quant, 16-element sub-blocks)"),
+                                    ("mxfp4", 13, MXFP4, "mxfp4 (e2m1 with an e8m0 scale per 32)"))},
     "q1_0_1b7": Workload("q1_0_1b7", 7, Q1_0,
                          tuple(_llama_layers(**_L1B7)) + (Matrix("lm_head", _VOCAB_1B7, 2048, 28, 5),),
                          description="q1_0 (1 bit, one scale per 128) decode-step weight set of a "

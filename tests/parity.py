@@ -1,14 +1,15 @@
 """Oracle references for the GPU parity tests: y and A, and the term mass F
 of the form the selected kernel evaluates (gate.py derives the bound).
 
-The VALU kernels evaluate the 4-bit and 1-bit formats as s * sum q x +
+The VALU kernels evaluate the formats with an offset as s * sum q x +
 mu * sum x (beta = 0); the matrix-core kernels multiply the bfloat16 of
-128 + q (beta = 128). f16 and Q8_0 are plain sums of products: F is None.
+128 + q (beta = 128). f16, Q8_0 and mxfp4 are plain sums of products (mxfp4
+scaled by powers of two only): F is None.
 lw_kernel_name / lw_kernel_name_multi say which kernel a call launches."""
 import numpy as np
 
 from paper_2605_20706_amd import binding
-from paper_2605_20706_amd.layout import F16, Q8_0
+from paper_2605_20706_amd.layout import F16, MXFP4, Q8_0
 
 MFMA_KERNELS = frozenset({"fewtok_kernel", "multitok_kernel", "multitok_pk_kernel", "skinny_kernel",
                           "gemm_kernel", "gemm32_kernel"})
@@ -19,7 +20,7 @@ def beta_of(kernel):
 
 
 def plain(fmt):
-    return fmt in (F16, Q8_0)
+    return fmt in (F16, Q8_0, MXFP4)
 
 
 def kernel_of(fmt, M, K, n_tok, Ms=None):

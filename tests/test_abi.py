@@ -64,7 +64,7 @@ def test_weight_bytes_matches_hand_sizes(lib):
 
 
 def test_weight_bytes_errors(lib):
-    assert lib.lw_weight_bytes(11, 256) == LW_EFMT
+    assert lib.lw_weight_bytes(12, 256) == LW_EFMT
     assert lib.lw_weight_bytes(Q4_0, -256) == LW_EINVAL
     assert lib.lw_weight_bytes(Q4_0, 100) == LW_ESHAPE
     assert lib.lw_weight_bytes(Q4_0, (1 << 40) + 256) == LW_EINVAL
@@ -76,7 +76,7 @@ def mv(lib, fmt=Q4_0, W=A256, x=A16, y=A16, M=4, K=256, n_tok=1):
 
 
 def test_matvec_error_order(lib):
-    assert mv(lib, fmt=11, W=None) == LW_EFMT          # format first
+    assert mv(lib, fmt=12, W=None) == LW_EFMT          # format first
     assert mv(lib, fmt=-1) == LW_EFMT
     assert mv(lib, W=None) == LW_EINVAL
     assert mv(lib, x=None) == LW_EINVAL
@@ -104,7 +104,7 @@ def mvm(lib, fmt=Q4_0, Ws=(A256, A256 + 4096), ys=(A16, A16 + 4096), Ms=(4, 8), 
 def test_matvec_multi_error_order(lib):
     """lw_matvec_multi checks as lw_matvec does, over all matrices, in the same
     order (no call here reaches a launch)."""
-    assert mvm(lib, fmt=11, x=None) == LW_EFMT
+    assert mvm(lib, fmt=12, x=None) == LW_EFMT
     assert mvm(lib, x=None) == LW_EINVAL
     assert mvm(lib, n=0) == LW_EINVAL
     assert mvm(lib, n=binding.LW_MULTI_MAX + 1) == LW_EINVAL
@@ -141,7 +141,7 @@ def test_kernel_name_multi(lib):
 
 
 def test_dequant_errors(lib):
-    assert lib.lw_dequant(11, A256, A16, 256) == LW_EFMT
+    assert lib.lw_dequant(12, A256, A16, 256) == LW_EFMT
     assert lib.lw_dequant(Q4_K, None, A16, 256) == LW_EINVAL
     assert lib.lw_dequant(Q4_K, A256, None, 256) == LW_EINVAL
     assert lib.lw_dequant(Q4_K, A256, A16, -256) == LW_EINVAL
@@ -168,7 +168,7 @@ def test_binding_fails_loudly_without_gpu_tensors(lib):
 
 
 def test_kernel_name_rejects_what_matvec_rejects(lib):
-    assert binding.kernel_name(11, 4, 256, 1) is None           # format
+    assert binding.kernel_name(12, 4, 256, 1) is None           # format
     assert binding.kernel_name(Q4_0, 0, 256, 1) is None        # sizes
     assert binding.kernel_name(Q4_0, 4, 256, 0) is None
     assert binding.kernel_name(Q4_0, 4, 300, 1) is None        # shape
@@ -211,7 +211,7 @@ def test_kernel_selection_table(lib):
     assert kind(F16, 2048, 2048, 1) == "gemv1_kernel"
     assert kind(Q8_0, 2048, 2048, 12) == "skinny_kernel"
     assert kind(F16, 2048, 2048, 20) == "gemv_kernel"
-    for fmt in (Q5_0, Q5_1, Q5_K, Q6_K, Q2_K):                # the VALU kernels for every token count
+    for fmt in (Q5_0, Q5_1, Q5_K, Q6_K, Q2_K, 11):            # the VALU kernels for every token count
         assert kind(fmt, 14336, 4096, 1) == "gemv1_kernel"
         assert kind(fmt, 14336, 4096, 4) == "gemv_kernel"
         assert kind(fmt, 14336, 4096, 512) == "gemv_kernel"
@@ -269,14 +269,14 @@ def test_launch_count(lib):
     assert binding.launch_count_multi(Q4_K, [14336, 14336], 4096, 2) == 2   # one per matrix
     assert binding.launch_count_multi(Q4_0, [14336, 14336], 4096, 4) == 1
     f = lib.lw_launch_count
-    assert f(11, 4, 256, 1) == LW_EFMT
+    assert f(12, 4, 256, 1) == LW_EFMT
     assert f(Q4_0, 0, 256, 1) == LW_EINVAL
     assert f(Q4_0, 4, 300, 1) == LW_ESHAPE
     g = lib.lw_launch_count_multi
     Ms = (ctypes.c_int64 * 2)(4, 8)
     assert g(Q4_0, 0, Ms, 256, 1) == LW_EINVAL
     assert g(Q4_0, 2, None, 256, 1) == LW_EINVAL
-    assert g(11, 2, Ms, 256, 1) == LW_EFMT
+    assert g(12, 2, Ms, 256, 1) == LW_EFMT
     assert g(Q4_0, 2, Ms, 300, 1) == LW_ESHAPE
 
 
@@ -338,7 +338,7 @@ def test_attn_errors_and_workspace(lib):
     def call(fmt=Q8_0, q=A16, K=A256, V=A256, out=A16, H=32, kv=8, D=128, L=2048, scale=0.088, ws=A16, wsb=1 << 30):
         return f(fmt, q, K, V, out, H, kv, D, L, scale, ws, wsb, None)
     assert call(fmt=Q4_K) == LW_EFMT                      # a super-block format: rows of 128 hold no block
-    assert call(fmt=11, q=None) == LW_EFMT
+    assert call(fmt=12, q=None) == LW_EFMT
     assert call(q=None) == LW_EINVAL
     assert call(ws=None) == LW_EINVAL
     assert call(H=12) == LW_EINVAL                         # 12 heads over 8

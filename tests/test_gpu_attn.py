@@ -10,11 +10,11 @@ import pytest
 
 from gpu_util import to_gpu
 from paper_2605_20706_amd import binding, synth
-from paper_2605_20706_amd.layout import F16, Q4_0, Q4_1, Q5_0, Q5_1, Q8_0
+from paper_2605_20706_amd.layout import F16, MXFP4, Q4_0, Q4_1, Q5_0, Q5_1, Q8_0
 
 pytestmark = pytest.mark.gpu
 
-KV_FMTS = [F16, Q8_0, Q4_0, Q4_1, Q5_0, Q5_1]
+KV_FMTS = [F16, Q8_0, Q4_0, Q4_1, Q5_0, Q5_1, MXFP4]
 
 
 def make(fmt, n_kv, L, D, seed, sigma=1.0):

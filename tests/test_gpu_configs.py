@@ -95,7 +95,7 @@ def test_workload_every_output(oracle_mod, key, idx):
 
 
 @pytest.mark.parametrize("key", ["q4_0_llama8b_ffn", "q4_1_llama8b_ffn", "q5_0_llama8b_ffn", "q5_1_llama8b_ffn",
-                                 "q5_k_llama8b_ffn", "q6_k_llama8b_ffn", "q2_k_llama8b_ffn"])
+                                 "q5_k_llama8b_ffn", "q6_k_llama8b_ffn", "q2_k_llama8b_ffn", "mxfp4_llama8b_ffn"])
 @pytest.mark.parametrize("n_tok", [1, 2, 4, 8, 512])
 def test_ffn_every_output(oracle_mod, key, n_tok):
     """The 8B gate, up and down matrices at every token count of the

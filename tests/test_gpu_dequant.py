@@ -5,7 +5,7 @@ import pytest
 
 from gpu_util import gpu_dequant, same_bits_or_both_zero
 from paper_2605_20706_amd import layout, synth
-from paper_2605_20706_amd.layout import F16, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
+from paper_2605_20706_amd.layout import F16, MXFP4, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
 
 pytestmark = pytest.mark.gpu
 
@@ -91,7 +91,7 @@ def test_q1_0_every_scale_and_signed_zero(oracle_mod):
 
 
 @pytest.mark.parametrize("n", [256, 512 + 256, 4096 * 3 + 256])
-@pytest.mark.parametrize("fmt", [F16, Q8_0, Q4_0, Q4_K, Q4_1, Q1_0, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K])
+@pytest.mark.parametrize("fmt", [F16, Q8_0, Q4_0, Q4_K, Q4_1, Q1_0, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K, MXFP4])
 def test_small_and_ragged(oracle_mod, fmt, n):
     check(oracle_mod, fmt, synth.gen_packed(fmt, n, np.random.default_rng(n + fmt)), n)
 
@@ -160,3 +160,11 @@ def test_q6_k_every_code_every_scale(oracle_mod):
     q = rng.integers(0, 64, 256 * d.size, dtype=np.uint8)
     sc = rng.integers(-128, 128, 16 * d.size).astype(np.int8)
     check(oracle_mod, Q6_K, layout.pack_q6_k(q, sc, d), q.size)
+
+
+def test_mxfp4_every_code_every_exponent(oracle_mod):
+    """16 codes x all 256 e8m0 exponents: subnormal scales, overflow to
+    infinity and the NaN exponent, bit for bit (NaN for NaN)."""
+    E = np.arange(256).astype(np.uint8)
+    codes = np.tile(np.concatenate([np.arange(16), np.arange(16)]).astype(np.uint8), E.size)
+    check(oracle_mod, MXFP4, layout.pack_mxfp4(codes, E), codes.size)

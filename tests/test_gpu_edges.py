@@ -25,7 +25,7 @@ from paper_2605_20706_amd import binding, synth
 
 pytestmark = pytest.mark.gpu
 
-FMTS = [0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10]
+FMTS = [0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11]
 # (M, K, n_tok): the single-token LDS kernel; the register kernel (one chunk,
 # two tokens, seven chunks over seven waves); the pair-step and few-token
 # matrix-core kernels; the 9..16-token kernels (multitok, Q8_0 skinny, VALU

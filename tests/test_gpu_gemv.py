@@ -13,11 +13,11 @@ import gate
 from gpu_util import gpu_matvec, to_gpu
 from parity import Ref, kernel_of, reference
 from paper_2605_20706_amd import synth
-from paper_2605_20706_amd.layout import F16, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
+from paper_2605_20706_amd.layout import F16, MXFP4, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
 
 pytestmark = pytest.mark.gpu
 
-FMTS = [F16, Q8_0, Q4_0, Q4_K, Q4_1, Q1_0, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K]
+FMTS = [F16, Q8_0, Q4_0, Q4_K, Q4_1, Q1_0, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K, MXFP4]
 # (M, K): single row; row tail below a workgroup's rows; K below one chunk;
 # K one chunk plus a ragged tail; several chunks; large K that needs x tiling.
 SHAPES = [(1, 256), (3, 768), (17, 2048), (67, 2304), (130, 4352), (33, 16640)]

@@ -11,7 +11,7 @@ import gate
 from gpu_util import to_gpu
 from parity import kernel_of, reference
 from paper_2605_20706_amd import binding, synth
-from paper_2605_20706_amd.layout import F16, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
+from paper_2605_20706_amd.layout import F16, MXFP4, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
 
 pytestmark = pytest.mark.gpu
 
@@ -36,7 +36,7 @@ def run_multi(oracle_mod, fmt, Ms, K, n_tok, seed):
                    f32_bound=1e-4, what=("vs single", i))
 
 
-@pytest.mark.parametrize("fmt", [F16, Q8_0, Q4_0, Q4_K, Q4_1, Q1_0, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K])
+@pytest.mark.parametrize("fmt", [F16, Q8_0, Q4_0, Q4_K, Q4_1, Q1_0, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K, MXFP4])
 @pytest.mark.parametrize("Ms,K", [((67, 130, 1), 2304), ((17, 5), 256), ((33, 40, 64, 3), 4352)])
 def test_multi_small(oracle_mod, fmt, Ms, K):
     """Ragged row counts (one launch over the LDS single-token kernel), up to

@@ -12,9 +12,9 @@ import numpy as np
 import pytest
 
 from paper_2605_20706_amd import synth
-from paper_2605_20706_amd.layout import F16, Q4_0, Q4_1, Q5_0, Q5_1, Q8_0
+from paper_2605_20706_amd.layout import F16, MXFP4, Q4_0, Q4_1, Q5_0, Q5_1, Q8_0
 
-KV_FMTS = [F16, Q8_0, Q4_0, Q4_1, Q5_0, Q5_1]
+KV_FMTS = [F16, Q8_0, Q4_0, Q4_1, Q5_0, Q5_1, MXFP4]
 
 
 def cache(fmt, n_kv, L, D, seed, sigma=1.0):
