@@ -50,6 +50,9 @@ C_FACTORED = 2.0 ** -17
 F32_BOUND = 1e-4
 MFMA_KERNELS = ("fewtok_kernel", "multitok_kernel", "multitok_pk_kernel", "skinny_kernel", "gemm_kernel",
                 "gemm32_kernel")
+METRIC_ATTN = "decode attention over a quantized KV cache, HBM GB/s of K and V read per decode step"
+# Llama-3-8B attention: 32 layers, 32 query heads over 8 key/value heads of 128
+ATTN_MODEL = {"n_layers": 32, "n_heads": 32, "n_kv": 8, "head_dim": 128}
 METRIC = "dequant-GEMV HBM GB/s (% of peak) and equiv. decode tok/s, Llama-1B/8B shapes"
 METRIC_DEQUANT = "standalone dequant HBM GB/s (packed read + float32 write), Llama-1B/8B shapes"
 
@@ -651,6 +654,152 @@ def run_sweep(out_path, n_seq=192, min_bytes=6e8):
     print(json.dumps({"sweep": out_path, "shapes": len(shapes)}))
 
 
+def run_attn(args):
+    """A decode step's attention: one lw_attn_decode per layer of a
+    Llama-3-8B-shaped model over a KV cache of --kv-len positions in the
+    --kv-fmt format (every layer its own K and V buffers, rotated over copies
+    above 1 GB), timed as the matrix-vector steps are. Prints one JSON line."""
+    import ctypes
+
+    import torch
+
+    lib = binding.library()
+    fmt = layout.FORMATS[args.kv_fmt]
+    Lkv = args.kv_len
+    nl, H, nkv, D = (ATTN_MODEL[k] for k in ("n_layers", "n_heads", "n_kv", "head_dim"))
+    n = nkv * Lkv * D
+    t0 = time.time()
+    host = []
+    Ks, Vs, qs, outs = [], [], [], []
+    for layer in range(nl):
+        rk = np.random.default_rng(np.random.SeedSequence([0, 20, layer, 0]))
+        rv = np.random.default_rng(np.random.SeedSequence([0, 20, layer, 1]))
+        Kh, Vh = synth.gen_packed(fmt, n, rk), synth.gen_packed(fmt, n, rv)
+        q = synth.gen_x_seeded([0, 20, layer, 2], D, H)
+        host.append((Kh, Vh, q))
+        Ks.append(torch.from_numpy(Kh).to("cuda"))
+        Vs.append(torch.from_numpy(Vh).to("cuda"))
+        qs.append(torch.from_numpy(q).to("cuda"))
+        outs.append(torch.empty((H, D), dtype=torch.float32, device="cuda"))
+    packed = sum(k.numel() + v.numel() for k, v in zip(Ks, Vs))
+    reps = max(1, int(-(-1e9 // packed)))
+    Kall = [Ks] + [[k.clone() for k in Ks] for _ in range(reps - 1)]
+    Vall = [Vs] + [[v.clone() for v in Vs] for _ in range(reps - 1)]
+    wsb = binding.attn_workspace_bytes(fmt, H, nkv, D, Lkv)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    log("attention: %d layers, %s cache of %d positions, %.3f GB (%d copies), generated in %.1fs"
+        % (nl, args.kv_fmt, Lkv, packed / 1e9, reps, time.time() - t0))
+    scale = ctypes.c_float(1.0 / np.sqrt(D))
+
+    def step(rep, s_):
+        for layer in range(nl):
+            rc = lib.lw_attn_decode(fmt, qs[layer].data_ptr(), Kall[rep][layer].data_ptr(),
+                                    Vall[rep][layer].data_ptr(), outs[layer].data_ptr(), H, nkv, D, Lkv, scale,
+                                    ws.data_ptr(), wsb, s_)
+            if rc != 0:
+                raise binding.LwError(rc, "lw_attn_decode")
+
+    def steps_on(first, count):
+        s_ = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        for i in range(first, first + count):
+            step(i % reps, s_)
+    nodes = 2 * nl
+    graphs = []
+    for first, count in ((0, args.warmup), (args.warmup, args.steps)):
+        gs = []
+        for f, c in graph_chunks(first, count, nodes) or []:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                steps_on(f, c)
+            gs.append(g)
+        graphs.append(gs)
+    for g in graphs[0]:
+        g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for g in graphs[1]:
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    y_timed = [o.cpu().numpy() for o in outs]
+    kv_bytes = packed  # one copy of every layer's K and V
+    alg = kv_bytes + nl * 2 * H * D * 4  # K, V, q, out
+    gbs = alg / (ms * 1e-3) / 1e9
+    # per call: the two kernels of one layer, 192 back to back, behind a device-side sleep
+    g2 = torch.cuda.CUDAGraph()
+    seq = 192
+
+    def sub():
+        s_ = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        for i in range(seq):
+            rep, layer = (i // nl) % reps, i % nl
+            rc = lib.lw_attn_decode(fmt, qs[layer].data_ptr(), Kall[rep][layer].data_ptr(),
+                                    Vall[rep][layer].data_ptr(), outs[layer].data_ptr(), H, nkv, D, Lkv, scale,
+                                    ws.data_ptr(), wsb, s_)
+            if rc != 0:
+                raise binding.LwError(rc, "lw_attn_decode")
+    with torch.cuda.graph(g2):
+        sub()
+    g2.replay()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    torch.cuda._sleep(int(2.4e6 * 5))
+    e0.record(stream)
+    g2.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    call_us = e0.elapsed_time(e1) * 1e3 / seq
+    call_bytes = alg / nl
+    kname = "attn_split_kernel<%d, %d, %d>" % (fmt, D, H // nkv)
+    roof = {"bound": "hbm", "achieved": round(call_bytes / (call_us * 1e-6) / 1e9, 1), "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": round(call_bytes / (call_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4), "traffic": None,
+            "kernel": kname + " + attn_combine_kernel<%d>" % D, "launches_per_step": 2 * nl,
+            "avg_call_us": round(call_us, 3), "alg_bytes_per_call": round(call_bytes),
+            "note": "achieved = one call's algorithmic bytes (K, V, q, out) over the call's duration (both kernels)"}
+    ceil, _ = ceilings(False, call_bytes, "graph")
+    out = {"metric": METRIC_ATTN, "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "f32",
+           "data": "synthetic (seeded; cache codes and scales drawn as for the weight formats, query N(0,1))",
+           "config": {"workload": "attn_llama8b_%s_kv%d" % (args.kv_fmt, Lkv),
+                      "description": "decode attention of a Llama-3-8B-shaped model (32 layers, 32 query heads over "
+                                     "8 key/value heads of 128) over a %s KV cache of %d positions" % (args.kv_fmt, Lkv),
+                      "format": args.kv_fmt, "kv_len": Lkv, "layers": nl, "bytes_per_step": round(alg),
+                      "mode": "graph", "op": "attn", "copies": reps},
+           "pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2), "roofline": roof, "stream_ceiling": ceil}
+    if not args.no_cpu_baseline:
+        import oracle
+        t_used, done, nb_ = 0.0, 0, 0
+        worst, ok, n_out = 0.0, True, 0
+        for layer in range(nl):
+            Kh, Vh, q = host[layer]
+            t1 = time.perf_counter()
+            ref, A, T = oracle.attn_decode(fmt, q, Kh, Vh, H, nkv, D, Lkv, 1.0 / np.sqrt(D))
+            t_used += time.perf_counter() - t1
+            done += 1
+            nb_ += alg / nl
+            err = np.abs(y_timed[layer].astype(np.float64) - ref)
+            bound = 2.0 ** -12 * (1 + T)[:, None] * A
+            with np.errstate(divide="ignore", invalid="ignore"):
+                worst = max(worst, float(np.where(bound > 0, err / bound, np.where(err > 0, np.inf, 0)).max()))
+            n_out += err.size
+            if t_used >= args.cpu_seconds:
+                break
+        ok = worst <= 1.0
+        out["cpu_baseline"] = {"value": round(nb_ / t_used / 1e9, 4), "unit": "GB/s", "cores": 1,
+                               "host_cpus": os.cpu_count() or 1, "kind": "oracle", "seconds": round(t_used, 2),
+                               "sample": "%d of %d layers, same inputs; oracle = plain C, double, one thread"
+                                         % (done, nl)}
+        out["parity"] = {"outputs_checked": n_out, "layers": done, "of_layers": nl,
+                         "what": "the last timed step's outputs vs the oracle",
+                         "bound": "|dout| <= 2^-12 (1 + T) sum_j p_j |v_j| per output",
+                         "bound_ratio_max": float("%.4g" % worst), "pass": ok}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -659,9 +808,12 @@ def main():
     ap.add_argument("--workload", default="q4_k_llama8b", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--n-tok", type=int, default=1)
     ap.add_argument("--mode", choices=["graph", "eager"], default="graph")
-    ap.add_argument("--op", choices=["matvec", "dequant"], default="matvec",
+    ap.add_argument("--kv-len", type=int, default=8192, help="--op attn: cached positions")
+    ap.add_argument("--kv-fmt", default="q8_0", choices=["f16", "q8_0", "q4_0", "q4_1", "q5_0", "q5_1", "mxfp4"],
+                    help="--op attn: KV cache format")
+    ap.add_argument("--op", choices=["matvec", "dequant", "attn"], default="matvec",
                     help="matvec: one lw_matvec per matrix (the decode step); dequant: one lw_dequant per "
-                         "matrix into float32 (eager, on the null stream)")
+                         "matrix into float32 (eager, on the null stream); attn: one lw_attn_decode per layer")
     ap.add_argument("--no-fuse", action="store_true",
                     help="one lw_matvec per matrix (default: a layer's gate and up share one lw_matvec_multi call)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -698,6 +850,10 @@ def main():
             torch.neg(src, out=dst)  # a plain elementwise kernel: reads n bytes, writes n bytes
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes": n, "copies": 20}))
+        return
+
+    if args.op == "attn":
+        run_attn(args)
         return
 
     wl = synth.WORKLOADS[args.workload]

@@ -83,11 +83,10 @@ __global__ void __launch_bounds__(kAttnThreads)
     }
 
     const int64_t head_base = (int64_t)g * kv_len;
-    for (int b = j0 + wave * RPW; b < j1; b += kAttnWaves * RPW) {
+    // one batch: positions b .. b + RPW - 1 (this lane: b + r), K and V decoded
+    auto load_batch = [&](int b, float* kk, float* vv) __attribute__((always_inline)) {
         const int row = b + r;
-        const bool valid = row < j1;
-        const int64_t e = (head_base + (valid ? row : j1 - 1)) * D + c * DPL;
-        float kk[DPL];
+        const int64_t e = (head_base + (row < j1 ? row : j1 - 1)) * D + c * DPL;
 #pragma unroll
         for (int i = 0; i < DPL / 4; ++i) {
             const float4 t = value4<FMT>(Kc, off1, off2, off3, e + 4 * i);
@@ -96,17 +95,6 @@ __global__ void __launch_bounds__(kAttnThreads)
             kk[4 * i + 2] = t.z;
             kk[4 * i + 3] = t.w;
         }
-        float s[G];
-#pragma unroll
-        for (int h = 0; h < G; ++h) {
-            float d = 0.f;
-#pragma unroll
-            for (int i = 0; i < DPL; ++i) d = __builtin_fmaf(qv[h][i], kk[i], d);
-#pragma unroll
-            for (int o = 1; o < LPR; o <<= 1) d = xor_sum(d, o);
-            s[h] = valid ? d * scale : -INFINITY;
-        }
-        float vv[DPL];
 #pragma unroll
         for (int i = 0; i < DPL / 4; ++i) {
             const float4 t = value4<FMT>(Vc, off1, off2, off3, e + 4 * i);
@@ -115,19 +103,45 @@ __global__ void __launch_bounds__(kAttnThreads)
             vv[4 * i + 2] = t.z;
             vv[4 * i + 3] = t.w;
         }
+    };
+    auto consume = [&](int b, const float* kk, const float* vv) __attribute__((always_inline)) {
+        const bool valid = b + r < j1;
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-            float mb = s[h];
+            float d = 0.f;
+#pragma unroll
+            for (int i = 0; i < DPL; ++i) d = __builtin_fmaf(qv[h][i], kk[i], d);
+#pragma unroll
+            for (int o = 1; o < LPR; o <<= 1) d = xor_sum(d, o);
+            const float s = valid ? d * scale : -INFINITY;
+            float mb = s;
 #pragma unroll
             for (int o = LPR; o < kWave; o <<= 1) mb = xor_max(mb, o);
             const float mn = fmaxf(m[h], mb);  // finite: the batch has a valid position
-            const float alpha = expf(m[h] - mn);  // m = -inf: 0
-            const float p = valid ? expf(s[h] - mn) : 0.f;
-            m[h] = mn;
-            l[h] = __builtin_fmaf(l[h], alpha, c == 0 ? p : 0.f);
+            if (mn != m[h]) {                  // wave-uniform: a new maximum rescales the partials
+                const float alpha = expf(m[h] - mn);  // m = -inf: 0
+                m[h] = mn;
+                l[h] *= alpha;
 #pragma unroll
-            for (int i = 0; i < DPL; ++i) acc[h][i] = __builtin_fmaf(p, vv[i], acc[h][i] * alpha);
+                for (int i = 0; i < DPL; ++i) acc[h][i] *= alpha;
+            }
+            const float p = valid ? expf(s - mn) : 0.f;
+            l[h] += c == 0 ? p : 0.f;
+#pragma unroll
+            for (int i = 0; i < DPL; ++i) acc[h][i] = __builtin_fmaf(p, vv[i], acc[h][i]);
         }
+    };
+    // two batches per round, both loaded before either is used (twice the
+    // bytes in flight per wave); the second only where it starts inside
+    // the split
+    constexpr int kStep = kAttnWaves * RPW;
+    for (int b = j0 + wave * RPW; b < j1; b += 2 * kStep) {
+        float k0[DPL], v0[DPL], k1[DPL], v1[DPL];
+        const bool two = b + kStep < j1;
+        load_batch(b, k0, v0);
+        load_batch(two ? b + kStep : b, k1, v1);
+        consume(b, k0, v0);
+        if (two) consume(b + kStep, k1, v1);
     }
 
     // the wave's totals: l over all lanes, the outputs over the positions
@@ -171,23 +185,74 @@ __global__ void __launch_bounds__(kAttnThreads)
     }
 }
 
-// out[h][d] = sum_s exp(m_s - M) acc_s[d] / sum_s exp(m_s - M) l_s
+// out[h][d] = sum_s exp(m_s - M) acc_s[d] / sum_s exp(m_s - M) l_s. One
+// workgroup per head: every thread loads the maxima of its splits at once
+// (one round trip for all of them), the weights w_s = exp(m_s - M) go to
+// LDS, then thread (d, sg) sums the splits sg, sg + SG, ... of output d
+// with eight loads in flight, and the SG partials are added through LDS.
+constexpr int kCombThreads = 256;
+constexpr int kMaxSplits = 1024;
+
 template <int D>
-__global__ void __launch_bounds__(D) attn_combine_kernel(const float* __restrict__ ws, float* __restrict__ out,
-                                                         int n_heads, int splits) {
-    const int h = blockIdx.x, d = threadIdx.x;
+__global__ void __launch_bounds__(kCombThreads) attn_combine_kernel(const float* __restrict__ ws,
+                                                                   float* __restrict__ out, int n_heads, int splits) {
+    constexpr int SG = kCombThreads / D;  // split groups
+    __shared__ float wsp[kMaxSplits];
+    __shared__ float part[SG][D + 1];
+    __shared__ float red[kCombThreads / kWave];
+    const int h = blockIdx.x, tid = threadIdx.x;
     const float* base = ws + (int64_t)h * (D + 2);
     const int64_t stride = (int64_t)n_heads * (D + 2);
-    float M = -INFINITY;
-    for (int s = 0; s < splits; ++s) M = fmaxf(M, base[s * stride + D]);
-    float L = 0.f, o = 0.f;
-    for (int s = 0; s < splits; ++s) {
-        const float ms = base[s * stride + D];
-        const float wgt = ms == -INFINITY ? 0.f : expf(ms - M);
-        L = __builtin_fmaf(wgt, base[s * stride + D + 1], L);
-        o = __builtin_fmaf(wgt, base[s * stride + d], o);
+    // maxima of the splits: all loads first, then the reduction
+    float mloc[kMaxSplits / kCombThreads];
+#pragma unroll
+    for (int i = 0; i < kMaxSplits / kCombThreads; ++i) {
+        const int s = tid + i * kCombThreads;
+        mloc[i] = s < splits ? base[s * stride + D] : -INFINITY;
     }
-    out[(int64_t)h * D + d] = o / L;
+    float M = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < kMaxSplits / kCombThreads; ++i) M = fmaxf(M, mloc[i]);
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) M = fmaxf(M, __shfl_xor(M, o, kWave));
+    if ((tid & (kWave - 1)) == 0) red[tid / kWave] = M;
+    __syncthreads();
+    M = red[0];
+#pragma unroll
+    for (int w = 1; w < kCombThreads / kWave; ++w) M = fmaxf(M, red[w]);
+#pragma unroll
+    for (int i = 0; i < kMaxSplits / kCombThreads; ++i) {
+        const int s = tid + i * kCombThreads;
+        if (s < splits) wsp[s] = mloc[i] == -INFINITY ? 0.f : expf(mloc[i] - M);
+    }
+    __syncthreads();
+    // thread (d, sg): d < D + 2 covers the outputs and l (slot D + 1; slot D
+    // is the maximum, unused here)
+    const int sg = tid / D, d0 = tid - sg * D;
+    for (int d = d0; d < D + 2; d += D) {
+        if (d == D) continue;
+        float o = 0.f;
+        int s = sg;
+        for (; s + 7 * SG < splits; s += 8 * SG) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = base[(s + u * SG) * stride + d];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) o = __builtin_fmaf(wsp[s + u * SG], v[u], o);
+        }
+        for (; s < splits; s += SG) o = __builtin_fmaf(wsp[s], base[s * stride + d], o);
+        part[sg][d == D + 1 ? D : d] = o;
+    }
+    __syncthreads();
+    if (tid < D) {
+        float o = 0.f, L = 0.f;
+#pragma unroll
+        for (int g = 0; g < SG; ++g) {
+            o += part[g][tid];
+            L += part[g][D];
+        }
+        out[(int64_t)h * D + tid] = o / L;
+    }
 }
 
 template <int FMT, int D, int G>
@@ -199,8 +264,8 @@ hipError_t launch_g(const float* q, const uint8_t* K, const uint8_t* V, float* o
                        0, stream, q, K, V, p.off1, p.off2, p.off3, (int)kv_len, (int)n_heads, scale, (int)pl.rps, ws);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
-    hipLaunchKernelGGL((attn_combine_kernel<D>), dim3((unsigned)n_heads), dim3(D), 0, stream, ws, out, (int)n_heads,
-                       (int)pl.splits);
+    hipLaunchKernelGGL((attn_combine_kernel<D>), dim3((unsigned)n_heads), dim3(kCombThreads), 0, stream, ws, out,
+                       (int)n_heads, (int)pl.splits);
     return hipGetLastError();
 }
 
@@ -229,8 +294,9 @@ hipError_t launch_f(const float* q, const uint8_t* K, const uint8_t* V, float* o
 
 AttnPlan attn_plan(int64_t n_kv, int64_t head_dim, int64_t kv_len, int64_t n_heads) {
     AttnPlan pl;
-    // about two workgroups per compute unit, at least 32 positions each
-    const int64_t by_len = (kv_len + 31) / 32;
+    // about two workgroups per compute unit, at least 64 positions each (two
+    // batches per wave: the per-wave reductions are paid once per split)
+    const int64_t by_len = (kv_len + 63) / 64;
     const int64_t by_chip = (512 + n_kv - 1) / n_kv;
     int64_t splits = by_len < by_chip ? by_len : by_chip;
     if (splits < 1) splits = 1;
