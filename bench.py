@@ -36,6 +36,9 @@ from paper_2605_20706_amd import binding, layout, synth  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFS = 2500.0  # dense bf16 matrix-core peak of MI355X
+MFMA_FP4_PEAK_TFS = 10100.0  # dense fp4 / fp6 matrix-core peak of MI355X
+# the fp4 matrix-core path's per-output bound (mxfp4 prefill through lw_matvec_ws)
+FP4_SPLIT, FP4_MFMA = 2.0 ** -16, 2.0 ** -11
 CSRC = os.path.join(ROOT, "paper_2605_20706_amd", "csrc")
 # Kernel nodes one captured HIP graph may hold. A 1-bit benchmark process
 # once ended in a segmentation fault while its graphs held 90 k and 180 k
@@ -113,6 +116,15 @@ class Workset:
                           m.M, m.K, n_tok) for r in range(self.reps) for i, m in enumerate(mats)]
             self.alg_bytes = [synth.algorithmic_bytes(wl.fmt, m.M, m.K, n_tok) for m in mats]
             self.flops = [2.0 * m.M * m.K * n_tok for m in mats]
+        # Calls whose fastest path needs a workspace (lw_matvec_workspace_bytes
+        # > 0: mxfp4 prefill on the fp4 matrix cores) go through lw_matvec_ws
+        # with one workspace shared by the step's calls (they run in order on
+        # one stream), one call per matrix.
+        need = [binding.matvec_workspace_bytes(wl.fmt, m.M, m.K, n_tok) for m in mats] if op == "matvec" else [0]
+        self.use_ws = max(need) > 0
+        self.wsbuf = torch.empty(max(need), dtype=torch.uint8, device="cuda") if self.use_ws else None
+        if self.use_ws:
+            fuse = False
         # Calls of a step: one per matrix, except that a layer's gate and up
         # projections (same input, independent outputs) are one
         # lw_matvec_multi call when fuse is set (op "matvec" only).
@@ -125,17 +137,20 @@ class Workset:
             else:
                 self.groups.append((i,))
         self._keep = []
-        self.calls = []  # (multi?, args) per weight copy and group
+        self.calls = []  # (kind "one" / "multi" / "ws", args) per weight copy and group
         for r in range(self.reps):
             for grp in self.groups:
-                if len(grp) == 1 or op != "matvec":
-                    self.calls.append((False, self.args[r * n + grp[0]]))
+                if self.use_ws:
+                    self.calls.append(("ws", self.args[r * n + grp[0]]
+                                       + (self.wsbuf.data_ptr(), self.wsbuf.numel())))
+                elif len(grp) == 1 or op != "matvec":
+                    self.calls.append(("one", self.args[r * n + grp[0]]))
                 else:
                     K = mats[grp[0]].K
                     arr = binding.multi_args([self.W[r * n + i].data_ptr() for i in grp],
                                              [self.y[i].data_ptr() for i in grp], [mats[i].M for i in grp])
                     self._keep.append(arr)
-                    self.calls.append((True, (wl.fmt, len(grp)) + arr + (self.x[K].data_ptr(), K, n_tok)))
+                    self.calls.append(("multi", (wl.fmt, len(grp)) + arr + (self.x[K].data_ptr(), K, n_tok)))
         self.fuse_used = any(len(g) > 1 for g in self.groups)
         # kernel launches per call: a multi call is one launch where the
         # library fuses it (lw_kernel_name_multi then names another kernel
@@ -155,6 +170,8 @@ class Workset:
             ms = [mats[i] for i in grp]
             if op == "dequant":
                 self.call_nodes.append(1)
+            elif self.use_ws:
+                self.call_nodes.append(binding.launch_count_ws(wl.fmt, ms[0].M, ms[0].K, n_tok))
             elif len(grp) == 1:
                 self.call_nodes.append(binding.launch_count(wl.fmt, ms[0].M, ms[0].K, n_tok))
             else:
@@ -176,12 +193,12 @@ class Workset:
                 if rc != 0:
                     raise binding.LwError(rc, "lw_dequant")
             return
-        f, fm = self.lib.lw_matvec, self.lib.lw_matvec_multi
+        fns = {"one": self.lib.lw_matvec, "multi": self.lib.lw_matvec_multi, "ws": self.lib.lw_matvec_ws}
         for i in calls:
-            multi, a = self.calls[i]
-            rc = fm(*a, stream) if multi else f(*a, stream)
+            kind, a = self.calls[i]
+            rc = fns[kind](*a, stream)
             if rc != 0:
-                raise binding.LwError(rc, "lw_matvec_multi" if multi else "lw_matvec")
+                raise binding.LwError(rc, "lw_matvec_" + kind)
 
     def kernel_names(self):
         """The kernel each call of a step launches (lw_kernel_name /
@@ -191,7 +208,9 @@ class Workset:
         out = []
         for grp in self.groups:
             ms = [self.mats[i] for i in grp]
-            if len(grp) == 1:
+            if self.use_ws:
+                out.append(binding.kernel_name_ws(self.wl.fmt, ms[0].M, ms[0].K, self.n_tok))
+            elif len(grp) == 1:
                 out.append(binding.kernel_name(self.wl.fmt, ms[0].M, ms[0].K, self.n_tok))
             else:
                 out.append(binding.kernel_name_multi(self.wl.fmt, [m.M for m in ms], ms[0].K, self.n_tok))
@@ -316,7 +335,7 @@ def run_gpu(ws, steps, warmup, mode):
 KERNEL_SOURCES = {"gemv_kernel": "gemv.hip", "gemv1_kernel": "gemv.hip", "gemv1r_kernel": "gemv.hip",
                   "multitok_kernel": "multitok.hip", "multitok_pk_kernel": "multitok.hip",
                   "fewtok_kernel": "fewtok.hip", "skinny_kernel": "skinny.hip", "gemm_kernel": "prefill.hip",
-                  "gemm32_kernel": "prefill.hip",
+                  "gemm32_kernel": "prefill.hip", "fp4mm_kernel": "fp4mm.hip",
                   "dequant_kernel": "dequant.hip"}
 
 
@@ -495,6 +514,20 @@ def cpu_baseline(ws, budget_s, y_timed=None):
     return out, parity
 
 
+def block_max_mass(oracle, fmt, W, x, M, K, rows=4096):
+    """Bm[t][r] = sum_k |w_rk| * (largest |x_t| of k's 32-block), from the
+    oracle's exact dequantization: the activation-split term of the fp4
+    matrix-core path's bound."""
+    x = np.atleast_2d(np.asarray(x, np.float64))
+    xm = np.abs(x).reshape(x.shape[0], K // 32, 32).max(axis=2)
+    Bm = np.empty((x.shape[0], M))
+    Wd = oracle.dequant(fmt, W, M * K).reshape(M, K)
+    for r0 in range(0, M, rows):
+        S = np.abs(Wd[r0:r0 + rows].astype(np.float64)).reshape(-1, K // 32, 32).sum(axis=2)
+        Bm[:, r0:r0 + rows] = xm @ S.T
+    return Bm
+
+
 def timed_parity(ws, refs, y_timed, n_threads):
     """Every output of the last timed step, for the matrices the CPU baseline
     covered, against the oracle: the float32 bound |dy| <= 1e-4 A + 2^-17 F
@@ -510,7 +543,7 @@ def timed_parity(ws, refs, y_timed, n_threads):
         for i in grp:
             kern_of[i] = names[j]
     worst = {"scaled": 0.0, "normwise": 0.0, "nmse": 0.0, "f32_bound_ratio": 0.0}
-    n_out, ok = 0, True
+    n_out, ok, fp4 = 0, True, False
     for i, (y_ref, A, _) in refs.items():
         m = ws.mats[i]
         y = y_timed[i].astype(np.float64).reshape(y_ref.shape)
@@ -521,6 +554,10 @@ def timed_parity(ws, refs, y_timed, n_threads):
             _, _, F, _ = oracle.matvec_f(wl.fmt, ws.host[i], ws.xh[m.K], m.M, m.K, beta, n_threads=n_threads)
         d = np.abs(y - y_ref)
         bound = F32_BOUND * A + C_FACTORED * F
+        if kern_of[i].split("<")[0] == "fp4mm_kernel":
+            fp4 = True
+            Bm = block_max_mass(oracle, wl.fmt, ws.host[i], ws.xh[m.K], m.M, m.K)
+            bound = FP4_SPLIT * Bm + FP4_MFMA * (A + Bm / 4)
         with np.errstate(divide="ignore", invalid="ignore"):
             r = np.where(bound > 0, d / bound, np.where(d > 0, np.inf, 0.0))
             sc = np.where(A > 0, d / A, 0.0)
@@ -534,7 +571,9 @@ def timed_parity(ws, refs, y_timed, n_threads):
         n_out += d.size
     return {"outputs_checked": int(n_out), "matrices": len(refs), "of_matrices": len(ws.mats),
             "what": "the last timed step's outputs vs the oracle",
-            "bound": "|dy| <= 1e-4*A + 2^-17*F per output; normwise <= 2e-3",
+            "bound": ("|dy| <= 2^-16*Bm + 2^-11*(A + Bm/4) per output (fp4 matrix cores: activations in four "
+                      "e2m3 pieces; Bm = sum |w| * block max |x|); normwise <= 2e-3" if fp4 else
+                      "|dy| <= 1e-4*A + 2^-17*F per output; normwise <= 2e-3"),
             "scaled_max": float("%.4g" % worst["scaled"]), "normwise_max": float("%.4g" % worst["normwise"]),
             "nmse_max": float("%.4g" % worst["nmse"]), "f32_bound_ratio_max": float("%.4g" % worst["f32_bound_ratio"]),
             "pass": ok}
@@ -881,9 +920,14 @@ def main():
     mfma = g["flop"] / g["bytes"] > ridge
     avg_launch_s = g["us"] * 1e-6 / g["launches"]
     if mfma:
+        # the contraction's own operand types: e2m1 x e2m3 on the fp4 path
+        # (four activation pieces, so its algorithmic flops are a quarter of
+        # the matrix-core flops it issues), else bf16
+        fp4 = kname.split("<")[0] == "fp4mm_kernel"
+        peak = MFMA_FP4_PEAK_TFS if fp4 else MFMA_BF16_PEAK_TFS
         kern_tfs = g["flop"] / (g["us"] * 1e-6) / 1e12
-        roof = {"bound": "mfma", "achieved": round(kern_tfs, 2), "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
-                "frac": round(kern_tfs / MFMA_BF16_PEAK_TFS, 4)}
+        roof = {"bound": "mfma", "achieved": round(kern_tfs, 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(kern_tfs / peak, 4), "mfma_operands": "fp4 x fp6" if fp4 else "bf16 x bf16"}
     else:
         kern_gbs = g["bytes"] / (g["us"] * 1e-6) / 1e9
         roof = {"bound": "hbm", "achieved": round(kern_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -907,7 +951,7 @@ def main():
     out = {
         "metric": METRIC if args.op == "matvec" else METRIC_DEQUANT, "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "scaling": "weak", "vs_baseline": None, "dtype": "fp4*fp6->f32" if ws.use_ws else "f32",
         "data": "synthetic (seeded; shapes and value distributions of the workload)",
         "config": {"workload": wl.key, "description": wl.description, "format": fmt_name,
                    "matrices": len(ws.mats), "calls_per_step": n_launch,

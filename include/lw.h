@@ -207,6 +207,46 @@ LW_API int lw_matvec_multi(int fmt, int n_mat, const void* const* W, float* cons
                            const float* x, int64_t K, int64_t n_tok, void* stream);
 
 /*
+ * lw_matvec_ws — lw_matvec with a device workspace from the caller, for the
+ * paths that need scratch memory. One path does: LW_MXFP4 weights with more
+ * than 16 tokens run on MI355X's native fp4 matrix cores (the mxfp4 format of
+ * Sec. 2.2 and Appendix B, which the paper emulates): e2m1 codes and their
+ * e8m0 exponents go to v_mfma_scale_f32_32x32x64_f8f6f4 as stored. The
+ * activations are split once per call into four e2m3 (6-bit float) pieces
+ * with one power-of-two scale per 32 values, kept in the workspace; per block,
+ * |x - sum of pieces| <= 2^-16 * the block's largest |x|. Error of that path:
+ *   |y - exact| <= 2^-16 * sum_k |w_k| * xmax_k + 2^-11 * sum_k |w_k * x_k|,
+ * xmax_k the largest |x| of k's 32-block (the second term bounds the matrix
+ * core's own summation, which is not float32's). Activations must be finite
+ * and below 2^126 in magnitude. Every other call ignores the workspace and
+ * is exactly lw_matvec (workspace may then be NULL).
+ *
+ *   workspace        device, 256-byte aligned, at least
+ *                    lw_matvec_workspace_bytes(fmt, M, K, n_tok) bytes, owned
+ *                    by the caller; needs no initialisation, undefined
+ *                    afterwards. Calls that overlap in time must not share a
+ *                    workspace.
+ *   workspace_bytes  its size in bytes.
+ *   fmt, W, x, y, M, K, n_tok, stream  as for lw_matvec.
+ *
+ * Checks as lw_matvec's, in the same order; LW_EINVAL also for a workspace
+ * that is needed and NULL or too small, LW_EALIGN for one not 256-byte
+ * aligned. The fp4 path makes two launches (three where a K split first
+ * zeroes y).
+ */
+LW_API int lw_matvec_ws(int fmt, const void* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
+                        void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
+ * lw_matvec_workspace_bytes — the workspace lw_matvec_ws needs for these
+ * sizes (0 where the call takes a path without one; for LW_MXFP4 above 16
+ * tokens 100 bytes per 32 activations of n_tok rounded up to 64 tokens), or
+ * the error lw_matvec would return on format, sizes or shape (negative).
+ * Host-only.
+ */
+LW_API int64_t lw_matvec_workspace_bytes(int fmt, int64_t M, int64_t K, int64_t n_tok);
+
+/*
  * lw_dequant — out[e] = value(W, e) for 0 <= e < n, bit-exact (see above).
  * Runs on the null stream. n == 0 is a no-op returning LW_OK.
  *
@@ -252,6 +292,13 @@ LW_API const char* lw_kernel_name(int fmt, int64_t M, int64_t K, int64_t n_tok);
  * Host-only: launches nothing.
  */
 LW_API const char* lw_kernel_name_multi(int fmt, int n_mat, const int64_t* M, int64_t K, int64_t n_tok);
+
+/*
+ * lw_kernel_name_ws, lw_launch_count_ws — lw_kernel_name and lw_launch_count
+ * for lw_matvec_ws with a large enough workspace. Host-only.
+ */
+LW_API const char* lw_kernel_name_ws(int fmt, int64_t M, int64_t K, int64_t n_tok);
+LW_API int64_t lw_launch_count_ws(int fmt, int64_t M, int64_t K, int64_t n_tok);
 
 /*
  * lw_attn_decode — one query token's attention over a KV cache stored in a

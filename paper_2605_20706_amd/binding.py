@@ -16,7 +16,8 @@ LIB_PATH = os.path.join(HERE, "liblw.so")
 LW_OK = 0
 EXPORTS = ("lw_matvec", "lw_matvec_multi", "lw_dequant", "lw_weight_bytes", "lw_strerror", "lw_kernel_name",
            "lw_kernel_name_multi", "lw_launch_count", "lw_launch_count_multi", "lw_attn_decode",
-           "lw_attn_workspace_bytes", "lw_attn_decode_noalloc")
+           "lw_attn_workspace_bytes", "lw_attn_decode_noalloc", "lw_matvec_ws", "lw_matvec_workspace_bytes",
+           "lw_kernel_name_ws", "lw_launch_count_ws")
 LW_MULTI_MAX = 4
 
 
@@ -72,6 +73,14 @@ def library() -> ctypes.CDLL:
         lib.lw_attn_workspace_bytes.restype = i64
         lib.lw_attn_decode_noalloc.argtypes = [ctypes.c_int, vp, vp, vp, vp, i64, i64, i64, i64, ctypes.c_float, vp]
         lib.lw_attn_decode_noalloc.restype = ctypes.c_int
+        lib.lw_matvec_ws.argtypes = [ctypes.c_int, vp, vp, vp, i64, i64, i64, vp, i64, vp]
+        lib.lw_matvec_ws.restype = ctypes.c_int
+        lib.lw_matvec_workspace_bytes.argtypes = [ctypes.c_int, i64, i64, i64]
+        lib.lw_matvec_workspace_bytes.restype = i64
+        lib.lw_kernel_name_ws.argtypes = [ctypes.c_int, i64, i64, i64]
+        lib.lw_kernel_name_ws.restype = ctypes.c_char_p
+        lib.lw_launch_count_ws.argtypes = [ctypes.c_int, i64, i64, i64]
+        lib.lw_launch_count_ws.restype = i64
         _lib = lib
     return _lib
 
@@ -128,6 +137,28 @@ def launch_count_multi(fmt: int, Ms, K: int, n_tok: int) -> int:
     return v
 
 
+def kernel_name_ws(fmt: int, M: int, K: int, n_tok: int):
+    """kernel_name for lw_matvec_ws with a large enough workspace."""
+    v = library().lw_kernel_name_ws(fmt, M, K, n_tok)
+    return None if v is None else v.decode()
+
+
+def launch_count_ws(fmt: int, M: int, K: int, n_tok: int) -> int:
+    """launch_count for lw_matvec_ws with a large enough workspace."""
+    v = library().lw_launch_count_ws(fmt, M, K, n_tok)
+    if v < 0:
+        raise LwError(v, "lw_launch_count_ws")
+    return v
+
+
+def matvec_workspace_bytes(fmt: int, M: int, K: int, n_tok: int) -> int:
+    """Workspace bytes lw_matvec_ws needs for these sizes (0: none)."""
+    v = library().lw_matvec_workspace_bytes(fmt, M, K, n_tok)
+    if v < 0:
+        raise LwError(v, "lw_matvec_workspace_bytes")
+    return v
+
+
 def _check_gpu(t, name):
     if not t.is_cuda:
         raise ValueError("%s must be a GPU tensor" % name)
@@ -162,6 +193,40 @@ def matvec(fmt: int, W, x, M: int, K: int, y=None, stream=None):
                              ctypes.c_void_p(stream.cuda_stream))
     if rc != LW_OK:
         raise LwError(rc, "lw_matvec")
+    return y
+
+
+def matvec_ws(fmt: int, W, x, M: int, K: int, y=None, workspace=None, stream=None):
+    """matvec through lw_matvec_ws: the same product, with a workspace (a
+    uint8 GPU tensor, allocated here when not given) for the paths that
+    need one."""
+    import torch
+
+    _check_gpu(W, "W")
+    _check_gpu(x, "x")
+    if x.dtype != torch.float32:
+        raise ValueError("x must be float32")
+    x2 = x.reshape(1, -1) if x.dim() == 1 else x
+    if x2.dim() != 2 or x2.shape[1] != K:
+        raise ValueError("x must be [n_tok, K] with K = %d" % K)
+    n_tok = x2.shape[0]
+    if y is None:
+        y = torch.empty((n_tok, M), dtype=torch.float32, device=x.device)
+    _check_gpu(y, "y")
+    if y.dtype != torch.float32 or y.numel() != n_tok * M:
+        raise ValueError("y must be float32 with n_tok*M elements")
+    nb = matvec_workspace_bytes(fmt, M, K, n_tok)
+    if workspace is None and nb > 0:
+        workspace = torch.empty(nb, dtype=torch.uint8, device=x.device)
+    if workspace is not None:
+        _check_gpu(workspace, "workspace")
+    if stream is None:
+        stream = torch.cuda.current_stream(x.device)
+    rc = library().lw_matvec_ws(fmt, W.data_ptr(), x2.data_ptr(), y.data_ptr(), M, K, n_tok,
+                                None if workspace is None else workspace.data_ptr(),
+                                0 if workspace is None else workspace.numel(), ctypes.c_void_p(stream.cuda_stream))
+    if rc != LW_OK:
+        raise LwError(rc, "lw_matvec_ws")
     return y
 
 

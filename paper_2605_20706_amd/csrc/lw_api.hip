@@ -11,7 +11,8 @@
 // LW_GEMV_MAX_TOK tokens -> the VALU kernels, up to 16 -> the matrix-core
 // kernel with K split across waves; more tokens -> the
 // tiled matrix-core (prefill) kernel. f16 weights use the VALU kernel in
-// token blocks of LW_GEMV_MAX_TOK for any token count.
+// token blocks of LW_GEMV_MAX_TOK for any token count. lw_matvec_ws (a
+// workspace) sends LW_MXFP4 prefill to the fp4 matrix cores.
 #include <cmath>
 
 #include "lw_internal.hpp"
@@ -50,9 +51,12 @@ hipError_t launch_family(int cand, int fmt, const uint8_t* Wb, const float* x, f
 
 // Kernel selection for a validated call: the swept table's candidate where
 // it names one (select.hpp), else the built-in rules below.
+// With a workspace (lw_matvec_ws), LW_MXFP4 prefill takes the fp4 matrix
+// cores; every other call ignores it.
 hipError_t dispatch(int fmt, const uint8_t* Wb, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
-                    hipStream_t s) {
+                    hipStream_t s, uint8_t* ws = nullptr) {
     const lw::Planes p = lw::planes_of(fmt, M * K);
+    if (ws && lw::fp4mm_takes(fmt, n_tok)) return lw::launch_fp4mm(Wb, x, y, M, K, n_tok, p, ws, s);
     hipError_t err = hipErrorNotSupported;
     const int cand = lw::select_cand(fmt, M, K, n_tok);
     if (cand >= lw::kCandFewtok) {
@@ -118,6 +122,28 @@ int lw_matvec(int fmt, const void* W, const float* x, float* y, int64_t M, int64
     return err == hipSuccess ? LW_OK : LW_EHIP;
 }
 
+int64_t lw_matvec_workspace_bytes(int fmt, int64_t M, int64_t K, int64_t n_tok) {
+    const int rc = check_shape(fmt, M, K, n_tok);
+    if (rc != LW_OK) return rc;
+    return lw::fp4mm_takes(fmt, n_tok) ? lw::fp4mm_workspace_bytes(K, n_tok) : 0;
+}
+
+int lw_matvec_ws(int fmt, const void* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
+                 void* workspace, int64_t workspace_bytes, void* stream) {
+    if (!known_fmt(fmt)) return LW_EFMT;
+    if (!W || !x || !y) return LW_EINVAL;
+    const int rc = check_shape(fmt, M, K, n_tok);
+    if (rc != LW_OK) return rc;
+    const int64_t need = lw::fp4mm_takes(fmt, n_tok) ? lw::fp4mm_workspace_bytes(K, n_tok) : 0;
+    if (need > 0 && (!workspace || workspace_bytes < need)) return LW_EINVAL;
+    if (!aligned(W, 256) || !aligned(x, 16) || !aligned(y, 16) || (need > 0 && !aligned(workspace, 256)))
+        return LW_EALIGN;
+    const hipError_t err = dispatch(fmt, static_cast<const uint8_t*>(W), x, y, M, K, n_tok,
+                                    reinterpret_cast<hipStream_t>(stream),
+                                    need > 0 ? static_cast<uint8_t*>(workspace) : nullptr);
+    return err == hipSuccess ? LW_OK : LW_EHIP;
+}
+
 int lw_matvec_multi(int fmt, int n_mat, const void* const* W, float* const* y, const int64_t* M, const float* x,
                     int64_t K, int64_t n_tok, void* stream) {
     if (!known_fmt(fmt)) return LW_EFMT;
@@ -157,7 +183,8 @@ namespace {
 // launch query active: nothing is launched or dereferenced, the launchers
 // stop at the launch. Returns false when the sizes fail the call's checks or
 // the selection fails.
-bool run_query(int fmt, int n_mat, const int64_t* Ms, int64_t M, int64_t K, int64_t n_tok, lw::LaunchQuery& out) {
+bool run_query(int fmt, int n_mat, const int64_t* Ms, int64_t M, int64_t K, int64_t n_tok, lw::LaunchQuery& out,
+               bool with_ws = false) {
     if (n_mat == 0) {
         if (check_shape(fmt, M, K, n_tok) != LW_OK) return false;
     } else {
@@ -174,7 +201,8 @@ bool run_query(int fmt, int n_mat, const int64_t* Ms, int64_t M, int64_t K, int6
     float* ys0 = const_cast<float*>(xs);
     hipError_t err;
     if (n_mat == 0) {
-        err = dispatch(fmt, stand_in, xs, ys0, M, K, n_tok, nullptr);
+        err = dispatch(fmt, stand_in, xs, ys0, M, K, n_tok, nullptr,
+                       with_ws ? const_cast<uint8_t*>(stand_in) : nullptr);
     } else {
         // the same routing as lw_matvec_multi
         const uint8_t* Ws[LW_MULTI_MAX];
@@ -217,6 +245,18 @@ int64_t lw_launch_count(int fmt, int64_t M, int64_t K, int64_t n_tok) {
     if (rc != LW_OK) return rc;
     lw::LaunchQuery r;
     return run_query(fmt, 0, nullptr, M, K, n_tok, r) ? r.count : LW_EHIP;
+}
+
+const char* lw_kernel_name_ws(int fmt, int64_t M, int64_t K, int64_t n_tok) {
+    lw::LaunchQuery r;
+    return run_query(fmt, 0, nullptr, M, K, n_tok, r, true) ? r.name : nullptr;
+}
+
+int64_t lw_launch_count_ws(int fmt, int64_t M, int64_t K, int64_t n_tok) {
+    const int rc = check_shape(fmt, M, K, n_tok);
+    if (rc != LW_OK) return rc;
+    lw::LaunchQuery r;
+    return run_query(fmt, 0, nullptr, M, K, n_tok, r, true) ? r.count : LW_EHIP;
 }
 
 int64_t lw_launch_count_multi(int fmt, int n_mat, const int64_t* M, int64_t K, int64_t n_tok) {

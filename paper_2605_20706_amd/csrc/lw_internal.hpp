@@ -181,8 +181,26 @@ int check_attn(int fmt, int64_t n_heads, int64_t n_kv, int64_t head_dim, int64_t
 hipError_t launch_attn(int fmt, const float* q, const uint8_t* K, const uint8_t* V, float* out, int64_t n_heads,
                        int64_t n_kv, int64_t head_dim, int64_t kv_len, float scale, const AttnPlan& pl, float* ws,
                        hipStream_t stream);
+// Work split of a tiled matrix-core launch: nrt x ntt (row tile, token tile)
+// pairs, ks K splits of sbp super-blocks each (the last one possibly
+// shorter); plan_split picks the fewest splits that keep the compute units
+// busy (prefill.hip). A K-split launch adds its partial results atomically
+// into y, which zero_fill clears first.
+struct GemmSplit {
+    int64_t nrt, ntt;
+    int ks, sbp;
+};
+GemmSplit plan_split(int64_t nrt, int64_t ntt, int64_t K);
+void zero_fill(float* y, int64_t n, hipStream_t stream);
 // Matrix-core path for larger token counts (prefill).
 hipError_t launch_prefill(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
                           int64_t n_tok, const Planes& p, hipStream_t stream);
+// LW_MXFP4 prefill on the fp4 x fp6 matrix cores (fp4mm.hip): the activations
+// are first split into e2m3 pieces in a caller-provided workspace of
+// fp4mm_workspace_bytes; fp4mm_takes says whether a call runs there.
+bool fp4mm_takes(int fmt, int64_t n_tok);
+int64_t fp4mm_workspace_bytes(int64_t K, int64_t n_tok);
+hipError_t launch_fp4mm(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
+                        const Planes& p, uint8_t* ws, hipStream_t stream);
 
 }  // namespace lw

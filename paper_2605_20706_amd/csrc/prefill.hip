@@ -302,13 +302,6 @@ __device__ __forceinline__ u32x4v transpose_quad(u32x4v w) {
     return u32x4v{s01[0], s01[1], s23[0], s23[1]};
 }
 
-// Work split of one launch: nrt x ntt tiles, ks K splits of sbp super-blocks
-// (the last one possibly shorter).
-struct GemmSplit {
-    int64_t nrt, ntt;
-    int ks, sbp;
-};
-
 template <int FMT, int WM, int TT>
 __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2, 2)))
     gemm_kernel(const uint8_t* __restrict__ W, const float* __restrict__ x, float* __restrict__ y, int64_t M,
@@ -1022,6 +1015,8 @@ __global__ void zero_kernel(float* __restrict__ y, int64_t n) {
     if (i0 < n - 4 * n4) y[4 * n4 + i0] = 0.f;
 }
 
+}  // namespace
+
 int cu_count_pf() {
     int dev = 0, v = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
@@ -1063,6 +1058,8 @@ void zero_fill(float* y, int64_t n, hipStream_t stream) {
     const int64_t zb = (n / 4 + 255) / 256 < 16384 ? (n / 4 + 255) / 256 + 1 : 16384;
     hipLaunchKernelGGL(zero_kernel, dim3((unsigned)zb), dim3(256), 0, stream, y, n);
 }
+
+namespace {
 
 template <int FMT, int WM, int TT>
 hipError_t launch_tile(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,

@@ -100,3 +100,44 @@ def check(y, y_ref, A, F=None, tol=TOL, f32_bound=None, what="", normwise=True):
         bad = d > _bounds(Aa, Fa, f32_bound)
         assert not bad.any(), (what, "exceeds float32-accumulation bound", int(bad.sum()), m)
     return m
+
+
+# The fp4 matrix-core path of lw_matvec_ws (mxfp4 weights, activations split
+# into four e2m3 pieces with a power-of-two scale per 32). Bound, from the
+# split and the instruction (include/lw.h, csrc/fp4mm.hip):
+#   split: per 32-block, |x_k - sum of pieces| <= 2^-16 * xmax_b, so the
+#     product of the pieces is within 2^-16 * Bm of W.x, where
+#     Bm = sum_k |w_k| * xmax_(block of k)                  (block-max mass);
+#   matrix core: each instruction's sum of its 64 products was measured within
+#     2^-12.5 of their absolute sum, and the float32 accumulation across the
+#     4 K / 64 instructions adds at most 2^-24 per instruction on the same
+#     mass; the pieces' absolute mass is at most A + Bm / 4 (piece p <= 2 *
+#     2^-4p xmax for p >= 1). 2^-11 covers both with a margin of about 3.
+# Hence every output must satisfy
+#   |y - y_ref| <= 2^-16 * Bm + 2^-11 * (A + Bm / 4).
+# The target's 2e-3 normwise reading (gate (ii) above) is checked as well.
+C_SPLIT = 2.0 ** -16
+C_MFMA = 2.0 ** -11
+
+
+def fp4_bound(A, Bm):
+    return C_SPLIT * Bm + C_MFMA * (A + Bm / 4)
+
+
+def check_fp4(y, y_ref, A, Bm, what="", normwise=True):
+    """Asserts the fp4 path's bound for every output (and gate (ii)); returns
+    the measures plus fp4_ratio, the largest error / bound."""
+    y_ref = np.asarray(y_ref, np.float64)
+    yy = np.asarray(y, np.float64).reshape(y_ref.shape)
+    Aa = np.asarray(A, np.float64).reshape(y_ref.shape)
+    Ba = np.asarray(Bm, np.float64).reshape(y_ref.shape)
+    m = measures(yy, y_ref, Aa)
+    assert np.isfinite(yy).all(), (what, "non-finite output")
+    d = np.abs(yy - y_ref)
+    bound = fp4_bound(Aa, Ba)
+    m["fp4_ratio"] = float(_ratio(d, bound).max())
+    bad = d > bound
+    assert not bad.any(), (what, "exceeds the fp4 path's bound", int(bad.sum()), m)
+    if normwise:
+        assert m["normwise"] <= TOL, (what, "gate (ii)", m)
+    return m

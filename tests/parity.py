@@ -58,3 +58,17 @@ def reference(oracle_mod, fmt, W, x, M, K, kernel, n_threads=0):
     """(y, A, F) for one call whose first kernel is `kernel`."""
     r = Ref(oracle_mod, fmt, W, x, M, K, betas=(beta_of(kernel),), n_threads=n_threads)
     return r.y, r.A, r.F(kernel)
+
+
+def block_max_mass(oracle_mod, fmt, W, x, M, K, rows=4096):
+    """Bm[t][r] = sum_k |w_rk| * max over k's 32-block of |x_t| (float64),
+    from the oracle's exact dequantization; the split term of the fp4 path's
+    bound (tests/gate.py)."""
+    x = np.atleast_2d(np.asarray(x, np.float64))
+    xm = np.abs(x).reshape(x.shape[0], K // 32, 32).max(axis=2)  # [n_tok, K/32]
+    Bm = np.empty((x.shape[0], M))
+    Wd = oracle_mod.dequant(fmt, W, M * K).reshape(M, K)
+    for r0 in range(0, M, rows):
+        S = np.abs(Wd[r0:r0 + rows].astype(np.float64)).reshape(-1, K // 32, 32).sum(axis=2)  # [rows, K/32]
+        Bm[:, r0:r0 + rows] = xm @ S.T
+    return Bm
