@@ -231,8 +231,9 @@ LW_API int lw_matvec_multi(int fmt, int n_mat, const void* const* W, float* cons
  *
  * Checks as lw_matvec's, in the same order; LW_EINVAL also for a workspace
  * that is needed and NULL or too small, LW_EALIGN for one not 256-byte
- * aligned. The fp4 path makes two launches (three where a K split first
- * zeroes y).
+ * aligned. The fp4 path makes two launches (three where it splits K: each
+ * split writes its partial results to the workspace and a last launch sums
+ * them into y).
  */
 LW_API int lw_matvec_ws(int fmt, const void* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
                         void* workspace, int64_t workspace_bytes, void* stream);
@@ -240,9 +241,10 @@ LW_API int lw_matvec_ws(int fmt, const void* W, const float* x, float* y, int64_
 /*
  * lw_matvec_workspace_bytes — the workspace lw_matvec_ws needs for these
  * sizes (0 where the call takes a path without one; for LW_MXFP4 above 16
- * tokens 100 bytes per 32 activations of n_tok rounded up to 64 tokens), or
- * the error lw_matvec would return on format, sizes or shape (negative).
- * Host-only.
+ * tokens 100 bytes per 32 activations of n_tok rounded up to 64 tokens, and
+ * where the call splits K, 4 bytes per output and split more), or the error
+ * lw_matvec would return on format, sizes or shape (negative). Host-only;
+ * the same on every device.
  */
 LW_API int64_t lw_matvec_workspace_bytes(int fmt, int64_t M, int64_t K, int64_t n_tok);
 

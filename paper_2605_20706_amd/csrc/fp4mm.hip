@@ -68,21 +68,31 @@ constexpr int kWS = kSB / 2;    // K windows of 64 per stage
 #define LW_FP4_NW 8
 #define LW_FP4_RT 2
 #endif
+constexpr int kNW = LW_FP4_NW;           // waves per workgroup
+constexpr int kRT = LW_FP4_RT;           // 32-row tiles per wave
+constexpr int kBM = 32 * kRT * kNW;      // weight rows per workgroup
 
-// Workspace layout, token-tile major so that one stage of one workgroup is
-// one contiguous run: codes [ntp / kBN][K/32][kPieces][kBN][24 bytes], then
-// the scale bytes [ntp / kBN][K/32][kPieces][kBN] at s_off; ntp = n_tok
-// rounded up to kBN (the padding tokens are split from zeros).
+// Tile and K-split plan of a call (row tiles of BM rows, token tiles of kBN)
+// and its workspace, token-tile major so that one stage of one workgroup is
+// one contiguous run: codes [ntp / kBN][K/32][kPieces][kBN][24 bytes], the
+// scale bytes [ntp / kBN][K/32][kPieces][kBN] at s_off, and with K splits
+// their float32 partial results [ks][n_tok][M] at p_off (summed into y by a
+// last launch). ntp = n_tok rounded up to kBN (the padding tokens are split
+// from zeros). The split count is planned for 256 compute units whatever the
+// device, so that lw_matvec_workspace_bytes needs no device.
 struct XLayout {
-    int64_t ntp, nb, s_off, total;
+    int64_t ntp, nb, s_off, p_off, total;
+    GemmSplit sp;
 };
 
-XLayout xlayout(int64_t K, int64_t n_tok) {
+XLayout xlayout(int64_t M, int64_t K, int64_t n_tok) {
     XLayout L;
     L.ntp = (n_tok + kBN - 1) / kBN * kBN;
     L.nb = K / 32;
+    L.sp = plan_split((M + kBM - 1) / kBM, L.ntp / kBN, K, 256);
     L.s_off = round_up_256(L.nb * kPieces * L.ntp * kPB);
-    L.total = L.s_off + round_up_256(L.nb * kPieces * L.ntp);
+    L.p_off = L.s_off + round_up_256(L.nb * kPieces * L.ntp);
+    L.total = L.p_off + (L.sp.ks > 1 ? round_up_256(4 * L.sp.ks * n_tok * M) : 0);
     return L;
 }
 
@@ -90,41 +100,45 @@ typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
 typedef int i32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-// One thread per (token t, block b); t runs fastest so that the stores of a
-// wave are contiguous.
-__global__ void __launch_bounds__(256) xsplit_kernel(const float* __restrict__ x, int64_t N, int64_t K, int64_t ntp,
-                                                     int64_t nb, uint8_t* __restrict__ q, uint8_t* __restrict__ s) {
+// Four threads per (token t, block b): thread q takes elements 4q .. 4q+3
+// and 16+4q .. 16+4q+3 of the block, which are fields 8q .. 8q+7 of its
+// pieces (field j is element j/2 + 16 (j % 2)); a piece's scale comes from
+// the block's largest |r| over the four threads (one lane quad). Thread
+// order: q fastest, then the token within its tile, the block, the token
+// tile, so that a quad writes one piece's 24 bytes and consecutive quads
+// consecutive tokens. The grid covers exactly 4 ntp nb threads.
+__global__ void __launch_bounds__(256) xsplit_kernel(const float* __restrict__ x, int64_t N, int64_t K, int64_t nb,
+                                                     uint8_t* __restrict__ q, uint8_t* __restrict__ s) {
     const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (gid >= ntp * nb) return;
-    const int64_t t = gid % ntp, b = gid / ntp;
-    float r[32];
+    const int qd = (int)(gid & 3);
+    const int64_t u = gid >> 2;
+    const int64_t tl = u % kBN, rest = u / kBN;
+    const int64_t b = rest % nb, ttile = rest / nb;
+    const int64_t t = ttile * kBN + tl;
+    float r[8];
     if (t < N) {
-        const float4* p = reinterpret_cast<const float4*>(x + t * K + 32 * b);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const float4 v = p[i];
-            r[4 * i] = v.x;
-            r[4 * i + 1] = v.y;
-            r[4 * i + 2] = v.z;
-            r[4 * i + 3] = v.w;
-        }
+        const float* p = x + t * K + 32 * b + 4 * qd;
+        const float4 v0 = *reinterpret_cast<const float4*>(p);
+        const float4 v1 = *reinterpret_cast<const float4*>(p + 16);
+        r[0] = v0.x, r[1] = v1.x, r[2] = v0.y, r[3] = v1.y, r[4] = v0.z, r[5] = v1.z, r[6] = v0.w, r[7] = v1.w;
     } else {
 #pragma unroll
-        for (int i = 0; i < 32; ++i) r[i] = 0.f;
+        for (int k = 0; k < 8; ++k) r[k] = 0.f;
     }
 #pragma unroll
     for (int pc = 0; pc < kPieces; ++pc) {
         float m = 0.f;
 #pragma unroll
-        for (int i = 0; i < 32; ++i) m = fmaxf(m, fabsf(r[i]));
+        for (int k = 0; k < 8; ++k) m = fmaxf(m, fabsf(r[k]));
+        m = fmaxf(m, dpp_move<0xB1>(m));  // quad lanes 1, 0, 3, 2
+        m = fmaxf(m, dpp_move<0x4E>(m));  // quad lanes 2, 3, 0, 1
         // m = f 2^e with f in [1/2, 1): floor(log2 m) = e - 1
         int S = m > 0.f ? __builtin_amdgcn_frexp_expf(m) - 2 : -127;
         S = S < -127 ? -127 : S;
-        uint32_t w[6] = {0u, 0u, 0u, 0u, 0u, 0u};
+        uint64_t w = 0;
 #pragma unroll
-        for (int j = 0; j < 32; ++j) {
-            const int i = j / 2 + 16 * (j % 2);
-            const float v = __builtin_ldexpf(r[i], -S);  // exact; |v| < 4
+        for (int k = 0; k < 8; ++k) {
+            const float v = __builtin_ldexpf(r[k], -S);  // exact; |v| < 4
             const float a = fabsf(v);
             const bool fine = a < 2.f;  // steps of 1/8 below 2, of 1/4 from 2 to 4
             const float g = __builtin_rintf(a * (fine ? 8.f : 4.f));
@@ -133,24 +147,48 @@ __global__ void __launch_bounds__(256) xsplit_kernel(const float* __restrict__ x
             // five bits themselves (subnormals included; 4.0 is code 24)
             const uint32_t code = ((uint32_t)g + (fine ? 0u : 8u)) | (v < 0.f ? 32u : 0u);
             const float qv = g * (fine ? 0.125f : 0.25f);
-            r[i] -= __builtin_ldexpf(__builtin_copysignf(qv, v), S);
-            const int bit = 6 * j, wd = bit / 32, sh = bit % 32;
-            w[wd] |= code << sh;
-            if (sh > 26) w[wd + 1] |= code >> (32 - sh);
+            r[k] -= __builtin_ldexpf(__builtin_copysignf(qv, v), S);
+            w |= (uint64_t)code << (6 * k);
         }
-        const int64_t slot = (((t / kBN) * nb + b) * kPieces + pc) * kBN + t % kBN;
-        uint2* qp = reinterpret_cast<uint2*>(q + slot * kPB);
-        qp[0] = make_uint2(w[0], w[1]);
-        qp[1] = make_uint2(w[2], w[3]);
-        qp[2] = make_uint2(w[4], w[5]);
-        s[slot] = (uint8_t)(S + 127);
+        const int64_t slot = ((ttile * nb + b) * kPieces + pc) * kBN + tl;
+        uint16_t* qp = reinterpret_cast<uint16_t*>(q + slot * kPB + 6 * qd);
+        qp[0] = (uint16_t)w;
+        qp[1] = (uint16_t)(w >> 16);
+        qp[2] = (uint16_t)(w >> 32);
+        if (qd == 0) s[slot] = (uint8_t)(S + 127);
+    }
+}
+
+// y[i] = sum over the ks K splits of part[split][i], i < n (float4 where
+// n % 4 == 0, whose slices are then 16-byte aligned).
+__global__ void __launch_bounds__(256) ksum_kernel(const float* __restrict__ part, int ks, int64_t n,
+                                                   float* __restrict__ y) {
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    const int64_t i0 = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if ((n & 3) == 0) {
+        const int64_t n4 = n / 4;
+        for (int64_t i = i0; i < n4; i += stride) {
+            float4 acc = reinterpret_cast<const float4*>(part)[i];
+            for (int sp = 1; sp < ks; ++sp) {
+                const float4 v = reinterpret_cast<const float4*>(part + sp * n)[i];
+                acc.x += v.x, acc.y += v.y, acc.z += v.z, acc.w += v.w;
+            }
+            reinterpret_cast<float4*>(y)[i] = acc;
+        }
+    } else {
+        for (int64_t i = i0; i < n; i += stride) {
+            float acc = part[i];
+            for (int sp = 1; sp < ks; ++sp) acc += part[sp * n + i];
+            y[i] = acc;
+        }
     }
 }
 
 template <int NW, int RT>
 __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(RT == 4 ? 1 : 2, RT == 4 ? 1 : 2)))
     fp4mm_kernel(const uint8_t* __restrict__ W, const uint8_t* __restrict__ xq, const uint8_t* __restrict__ xs,
-                 float* __restrict__ y, int64_t M, int64_t K, int64_t N, int64_t ntp, int64_t off1, GemmSplit sp) {
+                 float* __restrict__ y, float* __restrict__ part, int64_t M, int64_t K, int64_t N, int64_t off1,
+                 GemmSplit sp) {
     constexpr int NT = 64 * NW, BM = 32 * RT * NW;
     constexpr int kChunk = kBN * kPB;                // one (block, piece) of the token tile: 1536 bytes
     constexpr int kStageQ = kSB * kPieces * kChunk;  // codes of a stage
@@ -308,30 +346,26 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(RT
     }
 
     // store: lane (h, n32) holds token 32 tt + n32 of rows 32 (RT wm + rt) +
-    // 8 g + 4 h + e (register 4 g + e); K splits add into the zeroed y
-    const bool split_k = sp.ks > 1;
+    // 8 g + 4 h + e (register 4 g + e); a K split writes its own slice of
+    // the partial results (part), summed into y afterwards
+    float* const out = sp.ks > 1 ? part + (int64_t)split * N * M : y;
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt) {
         const int64_t t = tok0 + 32 * tt + n32;
         if (t >= N) continue;
-        float* const yt = y + t * M;
+        float* const yt = out + t * M;
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
                 const int64_t r = row0 + 32 * (RT * wm + rt) + 8 * g + 4 * h;
                 const f32x16& v = acc[rt][tt];
-                if (!split_k && (M & 3) == 0 && r + 3 < M) {
+                if ((M & 3) == 0 && r + 3 < M) {
                     *reinterpret_cast<float4*>(yt + r) = make_float4(v[4 * g], v[4 * g + 1], v[4 * g + 2], v[4 * g + 3]);
                 } else {
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
-                        if (r + e < M) {
-                            if (split_k)
-                                unsafeAtomicAdd(yt + r + e, v[4 * g + e]);
-                            else
-                                yt[r + e] = v[4 * g + e];
-                        }
+                        if (r + e < M) yt[r + e] = v[4 * g + e];
                 }
             }
     }
@@ -341,22 +375,24 @@ __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(RT
 
 bool fp4mm_takes(int fmt, int64_t n_tok) { return fmt == LW_MXFP4 && n_tok > 16; }
 
-int64_t fp4mm_workspace_bytes(int64_t K, int64_t n_tok) { return xlayout(K, n_tok).total; }
+int64_t fp4mm_workspace_bytes(int64_t M, int64_t K, int64_t n_tok) { return xlayout(M, K, n_tok).total; }
 
 hipError_t launch_fp4mm(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
                         const Planes& p, uint8_t* ws, hipStream_t stream) {
-    constexpr int NW = LW_FP4_NW, RT = LW_FP4_RT, BM = 32 * RT * NW;
-    const XLayout L = xlayout(K, n_tok);
-    const GemmSplit sp = plan_split((M + BM - 1) / BM, L.ntp / kBN, K);
+    const XLayout L = xlayout(M, K, n_tok);
+    const GemmSplit& sp = L.sp;
     const int64_t grid = sp.nrt * sp.ntt * sp.ks;
-    const int64_t sgrid = (L.ntp * L.nb + 255) / 256;
+    const int64_t sgrid = 4 * L.ntp * L.nb / 256;  // ntp is a multiple of 64: whole workgroups
+    const int64_t n = n_tok * M;
+    const int64_t rgrid = (n / 4 + 255) / 256 < 4096 ? (n / 4 + 255) / 256 + 1 : 4096;
     if (grid > 0x7fffffff || sgrid > 0x7fffffff) return hipErrorInvalidConfiguration;
-    if (query_only(kernel_name<Name_fp4mm_kernel, NW, RT>(), sp.ks > 1 ? 3 : 2)) return hipSuccess;
-    hipLaunchKernelGGL(xsplit_kernel, dim3((unsigned)sgrid), dim3(256), 0, stream, x, n_tok, K, L.ntp, L.nb, ws,
-                       ws + L.s_off);
-    if (sp.ks > 1) zero_fill(y, n_tok * M, stream);
-    hipLaunchKernelGGL((fp4mm_kernel<NW, RT>), dim3((unsigned)grid), dim3(64 * NW), 0, stream, W, ws, ws + L.s_off, y,
-                       M, K, n_tok, L.ntp, p.off1, sp);
+    if (query_only(kernel_name<Name_fp4mm_kernel, kNW, kRT>(), sp.ks > 1 ? 3 : 2)) return hipSuccess;
+    hipLaunchKernelGGL(xsplit_kernel, dim3((unsigned)sgrid), dim3(256), 0, stream, x, n_tok, K, L.nb, ws, ws + L.s_off);
+    float* part = reinterpret_cast<float*>(ws + L.p_off);
+    hipLaunchKernelGGL((fp4mm_kernel<kNW, kRT>), dim3((unsigned)grid), dim3(64 * kNW), 0, stream, W, ws,
+                       ws + L.s_off, y, part, M, K, n_tok, p.off1, sp);
+    if (sp.ks > 1)
+        hipLaunchKernelGGL(ksum_kernel, dim3((unsigned)rgrid), dim3(256), 0, stream, part, sp.ks, n, y);
     return hipGetLastError();
 }
 

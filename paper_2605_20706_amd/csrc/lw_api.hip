@@ -125,7 +125,7 @@ int lw_matvec(int fmt, const void* W, const float* x, float* y, int64_t M, int64
 int64_t lw_matvec_workspace_bytes(int fmt, int64_t M, int64_t K, int64_t n_tok) {
     const int rc = check_shape(fmt, M, K, n_tok);
     if (rc != LW_OK) return rc;
-    return lw::fp4mm_takes(fmt, n_tok) ? lw::fp4mm_workspace_bytes(K, n_tok) : 0;
+    return lw::fp4mm_takes(fmt, n_tok) ? lw::fp4mm_workspace_bytes(M, K, n_tok) : 0;
 }
 
 int lw_matvec_ws(int fmt, const void* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
@@ -134,7 +134,7 @@ int lw_matvec_ws(int fmt, const void* W, const float* x, float* y, int64_t M, in
     if (!W || !x || !y) return LW_EINVAL;
     const int rc = check_shape(fmt, M, K, n_tok);
     if (rc != LW_OK) return rc;
-    const int64_t need = lw::fp4mm_takes(fmt, n_tok) ? lw::fp4mm_workspace_bytes(K, n_tok) : 0;
+    const int64_t need = lw::fp4mm_takes(fmt, n_tok) ? lw::fp4mm_workspace_bytes(M, K, n_tok) : 0;
     if (need > 0 && (!workspace || workspace_bytes < need)) return LW_EINVAL;
     if (!aligned(W, 256) || !aligned(x, 16) || !aligned(y, 16) || (need > 0 && !aligned(workspace, 256)))
         return LW_EALIGN;

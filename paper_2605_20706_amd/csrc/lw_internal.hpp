@@ -190,7 +190,7 @@ struct GemmSplit {
     int64_t nrt, ntt;
     int ks, sbp;
 };
-GemmSplit plan_split(int64_t nrt, int64_t ntt, int64_t K);
+GemmSplit plan_split(int64_t nrt, int64_t ntt, int64_t K, int64_t cus = 0);  // cus 0: the device's
 void zero_fill(float* y, int64_t n, hipStream_t stream);
 // Matrix-core path for larger token counts (prefill).
 hipError_t launch_prefill(int fmt, const uint8_t* W, const float* x, float* y, int64_t M, int64_t K,
@@ -199,7 +199,7 @@ hipError_t launch_prefill(int fmt, const uint8_t* W, const float* x, float* y, i
 // are first split into e2m3 pieces in a caller-provided workspace of
 // fp4mm_workspace_bytes; fp4mm_takes says whether a call runs there.
 bool fp4mm_takes(int fmt, int64_t n_tok);
-int64_t fp4mm_workspace_bytes(int64_t K, int64_t n_tok);
+int64_t fp4mm_workspace_bytes(int64_t M, int64_t K, int64_t n_tok);
 hipError_t launch_fp4mm(const uint8_t* W, const float* x, float* y, int64_t M, int64_t K, int64_t n_tok,
                         const Planes& p, uint8_t* ws, hipStream_t stream);
 

@@ -1029,13 +1029,13 @@ int cu_count_pf() {
 // on super-block boundaries, the fewest that keep the compute units (one
 // workgroup each) at least 85 % busy over the launch's rounds, else the best
 // of them; every split keeps at least four super-blocks.
-GemmSplit plan_split(int64_t nrt, int64_t ntt, int64_t K) {
+GemmSplit plan_split(int64_t nrt, int64_t ntt, int64_t K, int64_t cus) {
     GemmSplit sp;
     sp.nrt = nrt;
     sp.ntt = ntt;
     const int nsb = (int)(K / 256);
     const int64_t tiles = nrt * ntt;
-    const int64_t cus = cu_count_pf();
+    if (cus <= 0) cus = cu_count_pf();
     const int kmax = nsb / 4 > 1 ? nsb / 4 : 1;
     int best = 1;
     double best_eff = 0.0;

@@ -356,20 +356,25 @@ def test_attn_errors_and_workspace(lib):
     assert lib.lw_attn_workspace_bytes(Q4_K, 32, 8, 128, 16) == LW_EFMT
 
 
-def _ws_bytes(K, n_tok):
+def _ws_bytes(M, K, n_tok, ks):
     """The fp4 path's workspace: four e2m3 pieces (24 bytes of codes and one
-    scale byte per 32 activations each) of n_tok rounded up to 64 tokens,
-    codes and scales each rounded up to 256 bytes."""
+    scale byte per 32 activations each) of n_tok rounded up to 64 tokens, and
+    with ks > 1 K splits their float32 partial results [ks][n_tok][M]; each
+    part rounded up to 256 bytes."""
     ntp = -(-n_tok // 64) * 64
     nb = K // 32
     r256 = lambda v: -(-v // 256) * 256
-    return r256(nb * 4 * ntp * 24) + r256(nb * 4 * ntp)
+    return r256(nb * 4 * ntp * 24) + r256(nb * 4 * ntp) + (r256(4 * ks * n_tok * M) if ks > 1 else 0)
 
 
 def test_matvec_workspace_bytes(lib):
     f = lib.lw_matvec_workspace_bytes
-    for M, K, n_tok in [(14336, 4096, 512), (4096, 14336, 512), (41, 256, 17), (1, 2048, 65)]:
-        assert f(layout.MXFP4, M, K, n_tok) == _ws_bytes(K, n_tok)
+    # K splits planned for 256 compute units (512 x 64 tiles): 28 x 8 tiles
+    # fill the chip unsplit; 8 x 8 tiles take 4 splits of 14 super-blocks; a
+    # K of one super-block cannot split; 1 x 2 tiles take the most splits
+    # that keep 4 super-blocks each (2)
+    for M, K, n_tok, ks in [(14336, 4096, 512, 1), (4096, 14336, 512, 4), (41, 256, 17, 1), (1, 2048, 65, 2)]:
+        assert f(layout.MXFP4, M, K, n_tok) == _ws_bytes(M, K, n_tok, ks), (M, K, n_tok)
     # every other call takes a path without a workspace
     for fmt in (F16, Q8_0, Q4_0, Q4_K, Q4_1, Q1_0, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K):
         assert f(fmt, 4096, 4096, 512) == 0
@@ -383,7 +388,7 @@ def test_matvec_workspace_bytes(lib):
 def test_matvec_ws_error_order(lib):
     f = lib.lw_matvec_ws
     MX = layout.MXFP4
-    need = _ws_bytes(256, 64)
+    need = _ws_bytes(64, 256, 64, 1)
     assert f(12, A256, A16, A16, 64, 256, 64, A256, need, None) == LW_EFMT
     assert f(MX, None, A16, A16, 64, 256, 64, A256, need, None) == LW_EINVAL
     assert f(MX, A256, A16, A16, 0, 256, 64, A256, need, None) == LW_EINVAL
@@ -399,12 +404,13 @@ def test_matvec_ws_error_order(lib):
 def test_kernel_name_and_launch_count_ws(lib):
     MX = layout.MXFP4
     # mxfp4 from 17 tokens: the split kernel and the fp4 matrix-core kernel
-    # (plus a fill kernel where the launch splits K)
+    # (plus the kernel that sums the partial results where K is split)
     for M, K, n_tok in [(14336, 4096, 512), (300, 1024, 17), (1100, 4352, 100)]:
         assert binding.kernel_name_ws(MX, M, K, n_tok).startswith("fp4mm_kernel<")
         assert binding.launch_count_ws(MX, M, K, n_tok) in (2, 3)
         assert binding.kernel_name(MX, M, K, n_tok) != binding.kernel_name_ws(MX, M, K, n_tok)
     assert binding.launch_count_ws(MX, 14336, 4096, 512) == 2
+    assert binding.launch_count_ws(MX, 4096, 14336, 512) == 3
     # elsewhere lw_matvec_ws is lw_matvec
     for fmt, n_tok in [(Q4_0, 512), (MX, 16), (MX, 1), (F16, 100), (Q4_K, 4)]:
         assert binding.kernel_name_ws(fmt, 4096, 4096, n_tok) == binding.kernel_name(fmt, 4096, 4096, n_tok)
