@@ -35,15 +35,16 @@
 // j / 2 + 16 (j % 2) (the Q4 byte order), so the pieces are packed in that
 // same element order and no weight code is moved or decoded.
 //
-// Two launches: xsplit_kernel writes the pieces of every (token, block) to the
-// caller's workspace once per call; fp4mm_kernel runs the tiled product.
-// Workgroup tile: 128 NW weight rows x 64 tokens; each wave 128 rows (four
-// 32-row tiles) x 64 tokens (two 32-token tiles). K advances in stages of four
-// blocks (two K windows of 64: lane half h takes blocks 2h + j of the stage in
-// window j); the stage's pieces of the 64 tokens are staged in LDS (double
-// buffered), the weight codes go from global memory straight to registers.
-// Tile order, K splits and the XCD grouping are those of the other prefill
-// kernels.
+// Launches: xsplit_kernel writes the pieces of every (token, block) to the
+// caller's workspace once per call; fp4mm_kernel runs the tiled product;
+// where K is split, each split writes its partial results to the workspace
+// and ksum_kernel adds them into y. Workgroup tile: 32 RT NW weight rows x 64
+// tokens (8 waves, two per SIMD); each wave 32 RT rows (RT 32-row tiles) x 64
+// tokens (two 32-token tiles). K advances in stages of four blocks (two K
+// windows of 64: lane half h takes blocks 2h + j of the stage in window j);
+// the stage's pieces of the 64 tokens are staged in LDS (double buffered),
+// the weight codes go from global memory straight to registers. Tile order
+// and the XCD grouping are those of the other prefill kernels.
 #include <type_traits>
 
 #include "lw_device.hpp"
