@@ -40,8 +40,49 @@ constexpr int dims_per_lane() {
     return G <= 4 ? 16 : 8;
 }
 
-__device__ __forceinline__ float xor_sum(float v, int mask) { return v + __shfl_xor(v, mask, kWave); }
-__device__ __forceinline__ float xor_max(float v, int mask) { return fmaxf(v, __shfl_xor(v, mask, kWave)); }
+// Lane reductions without LDS round trips. partner<MASK> gives, for masks 1
+// and 2, the DPP quad permutations (the lane's xor-MASK partner); for 4 and 8
+// the DPP half-row and row mirrors (lane i with 7 - i, 15 - i), which stand
+// in for the xor partner when the values are equal within groups of MASK
+// lanes; for 16 and 32 the permlane swaps of rows and halves (exact xor
+// partners).
+template <int MASK>
+__device__ __forceinline__ float partner(float v) {
+    if constexpr (MASK == 1) return dpp_move<0xB1>(v);
+    else if constexpr (MASK == 2) return dpp_move<0x4E>(v);
+    else if constexpr (MASK == 4) return dpp_move<0x141>(v);
+    else if constexpr (MASK == 8) return dpp_move<0x140>(v);
+    else {
+        const uint32_t b = __builtin_bit_cast(uint32_t, v);
+        const auto sw = MASK == 16 ? __builtin_amdgcn_permlane16_swap(b, b, false, false)
+                                   : __builtin_amdgcn_permlane32_swap(b, b, false, false);
+        // the upper group of each pair finds its partner in the first result
+        const int lane = threadIdx.x & (kWave - 1);
+        return __builtin_bit_cast(float, (lane & MASK) ? sw[0] : sw[1]);
+    }
+}
+// v summed (maximised) over the lanes that differ from this one in the mask
+// bits LO .. HI - 1, for values already equal within aligned groups of LO
+// lanes (LO a power of two; 1: no condition).
+template <int LO, int HI>
+__device__ __forceinline__ float group_sum(float v) {
+    if constexpr (LO < HI) return group_sum<2 * LO, HI>(v + partner<LO>(v));
+    else return v;
+}
+template <int LO, int HI>
+__device__ __forceinline__ float group_max(float v) {
+    if constexpr (LO < HI) return group_max<2 * LO, HI>(fmaxf(v, partner<LO>(v)));
+    else return v;
+}
+// v summed over all lanes congruent to this one modulo LO (LO = 4, 8 or 16),
+// whatever the values: rotations of each 16-lane row by LO, 2 LO, ..., 8
+// (DPP row_ror) reach every lane of the row in the same residue class, then
+// the row and half swaps add the other rows.
+template <int LO, int SH = LO>
+__device__ __forceinline__ float residue_sum(float v) {
+    if constexpr (SH < 16) return residue_sum<LO, 2 * SH>(v + dpp_move<0x120 + SH>(v));
+    else return group_sum<16, kWave>(v);
+}
 
 template <int FMT, int D, int G>
 __global__ void __launch_bounds__(kAttnThreads)
@@ -111,12 +152,9 @@ __global__ void __launch_bounds__(kAttnThreads)
             float d = 0.f;
 #pragma unroll
             for (int i = 0; i < DPL; ++i) d = __builtin_fmaf(qv[h][i], kk[i], d);
-#pragma unroll
-            for (int o = 1; o < LPR; o <<= 1) d = xor_sum(d, o);
+            d = group_sum<1, LPR>(d);
             const float s = valid ? d * scale : -INFINITY;
-            float mb = s;
-#pragma unroll
-            for (int o = LPR; o < kWave; o <<= 1) mb = xor_max(mb, o);
+            const float mb = group_max<LPR, kWave>(s);
             const float mn = fmaxf(m[h], mb);  // finite: the batch has a valid position
             if (mn != m[h]) {                  // wave-uniform: a new maximum rescales the partials
                 const float alpha = expf(m[h] - mn);  // m = -inf: 0
@@ -147,14 +185,10 @@ __global__ void __launch_bounds__(kAttnThreads)
     // the wave's totals: l over all lanes, the outputs over the positions
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-        float lt = l[h];
-#pragma unroll
-        for (int o = 1; o < kWave; o <<= 1) lt = xor_sum(lt, o);
+        const float lt = group_sum<1, kWave>(l[h]);
 #pragma unroll
         for (int i = 0; i < DPL; ++i) {
-            float a = acc[h][i];
-#pragma unroll
-            for (int o = LPR; o < kWave; o <<= 1) a = xor_sum(a, o);
+            const float a = residue_sum<LPR>(acc[h][i]);
             if (r == 0) red[wave][h][c * DPL + i] = a;
         }
         if (lane == 0) {
