@@ -11,13 +11,15 @@
 // query heads of key/value head g over positions [s*rps, (s+1)*rps) and
 // writes per head the running maximum m, the sum l of exp(s_j - m) and the
 // unnormalised output sum_j exp(s_j - m) v_j to the workspace; a second
-// kernel rescales the splits to their common maximum and divides. Inside a
+// kernel rescales the splits to their common maximum and divides (scores and
+// maxima are kept in base-2 units, s log2(e), so every exponential is one
+// v_exp_f32 of a non-positive argument). Inside a
 // workgroup each wave takes batches of RPW positions: lane (r, c) holds DPL
 // consecutive dimensions c*DPL .. of position r, its query slices for the G
 // heads in registers; scores are lane sums over the LPR = head_dim / DPL
 // lanes of a position, and the online softmax rescales the lane's G x DPL
 // output partials by exp(m_old - m_new) per batch. The wave's partials are
-// then summed over positions (lane shuffles) and the four waves combined
+// then summed over positions (DPP and permlane steps) and the four waves combined
 // through LDS. Everything is float32; every exp argument is <= 0.
 #include <cmath>
 
@@ -99,6 +101,8 @@ __global__ void __launch_bounds__(kAttnThreads)
     const int wave = threadIdx.x / kWave;
     const int r = lane / LPR, c = lane - r * LPR;
     const int j0 = split * rps;
+    // scores in base-2 units: exp(x) = exp2(x log2(e)), one v_exp_f32 each
+    const float scale2 = scale * 1.4426950408889634f;
     const int j1 = min(kv_len, j0 + rps);
 
     float qv[G][DPL];
@@ -153,17 +157,17 @@ __global__ void __launch_bounds__(kAttnThreads)
 #pragma unroll
             for (int i = 0; i < DPL; ++i) d = __builtin_fmaf(qv[h][i], kk[i], d);
             d = group_sum<1, LPR>(d);
-            const float s = valid ? d * scale : -INFINITY;
+            const float s = valid ? d * scale2 : -INFINITY;
             const float mb = group_max<LPR, kWave>(s);
             const float mn = fmaxf(m[h], mb);  // finite: the batch has a valid position
             if (mn != m[h]) {                  // wave-uniform: a new maximum rescales the partials
-                const float alpha = expf(m[h] - mn);  // m = -inf: 0
+                const float alpha = __builtin_amdgcn_exp2f(m[h] - mn);  // m = -inf: 0
                 m[h] = mn;
                 l[h] *= alpha;
 #pragma unroll
                 for (int i = 0; i < DPL; ++i) acc[h][i] *= alpha;
             }
-            const float p = valid ? expf(s - mn) : 0.f;
+            const float p = valid ? __builtin_amdgcn_exp2f(s - mn) : 0.f;
             l[h] += c == 0 ? p : 0.f;
 #pragma unroll
             for (int i = 0; i < DPL; ++i) acc[h][i] = __builtin_fmaf(p, vv[i], acc[h][i]);
@@ -211,7 +215,7 @@ __global__ void __launch_bounds__(kAttnThreads)
 #pragma unroll
             for (int w = 0; w < kAttnWaves; ++w) {
                 const float mw = red[w][h][D];
-                const float wgt = mw == -INFINITY ? 0.f : expf(mw - M);
+                const float wgt = mw == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mw - M);
                 v = __builtin_fmaf(wgt, red[w][h][d], v);
             }
         }
@@ -257,7 +261,7 @@ __global__ void __launch_bounds__(kCombThreads) attn_combine_kernel(const float*
 #pragma unroll
     for (int i = 0; i < kMaxSplits / kCombThreads; ++i) {
         const int s = tid + i * kCombThreads;
-        if (s < splits) wsp[s] = mloc[i] == -INFINITY ? 0.f : expf(mloc[i] - M);
+        if (s < splits) wsp[s] = mloc[i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mloc[i] - M);
     }
     __syncthreads();
     // thread (d, sg): d < D + 2 covers the outputs and l (slot D + 1; slot D
