@@ -227,7 +227,7 @@ __global__ void __launch_bounds__(kAttnThreads)
 // workgroup per head: every thread loads the maxima of its splits at once
 // (one round trip for all of them), the weights w_s = exp(m_s - M) go to
 // LDS, then thread (d, sg) sums the splits sg, sg + SG, ... of output d
-// with eight loads in flight, and the SG partials are added through LDS.
+// with sixteen loads in flight, and the SG partials are added through LDS.
 constexpr int kCombThreads = 256;
 constexpr int kMaxSplits = 1024;
 
@@ -264,23 +264,33 @@ __global__ void __launch_bounds__(kCombThreads) attn_combine_kernel(const float*
         if (s < splits) wsp[s] = mloc[i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mloc[i] - M);
     }
     __syncthreads();
-    // thread (d, sg): d < D + 2 covers the outputs and l (slot D + 1; slot D
-    // is the maximum, unused here)
+    // thread (d, sg) sums output d over the splits sg, sg + SG, ...; thread
+    // d = 1 also sums l (slot D + 1) in the same pass. Sixteen splits' loads
+    // (thirty-two for d = 1) are issued before any is used.
     const int sg = tid / D, d0 = tid - sg * D;
-    for (int d = d0; d < D + 2; d += D) {
-        if (d == D) continue;
-        float o = 0.f;
-        int s = sg;
-        for (; s + 7 * SG < splits; s += 8 * SG) {
-            float v[8];
+    const bool with_l = d0 == 1;
+    constexpr int U = 16;
+    float o = 0.f, ol = 0.f;
+    int s = sg;
+    for (; s + (U - 1) * SG < splits; s += U * SG) {
+        float v[U], vl[U];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) v[u] = base[(s + u * SG) * stride + d];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) o = __builtin_fmaf(wsp[s + u * SG], v[u], o);
+        for (int u = 0; u < U; ++u) {
+            v[u] = base[(s + u * SG) * stride + d0];
+            vl[u] = with_l ? base[(s + u * SG) * stride + D + 1] : 0.f;
         }
-        for (; s < splits; s += SG) o = __builtin_fmaf(wsp[s], base[s * stride + d], o);
-        part[sg][d == D + 1 ? D : d] = o;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            o = __builtin_fmaf(wsp[s + u * SG], v[u], o);
+            ol = __builtin_fmaf(wsp[s + u * SG], vl[u], ol);
+        }
     }
+    for (; s < splits; s += SG) {
+        o = __builtin_fmaf(wsp[s], base[s * stride + d0], o);
+        if (with_l) ol = __builtin_fmaf(wsp[s], base[s * stride + D + 1], ol);
+    }
+    part[sg][d0] = o;
+    if (with_l) part[sg][D] = ol;
     __syncthreads();
     if (tid < D) {
         float o = 0.f, L = 0.f;
