@@ -174,6 +174,40 @@ template <>
 struct MF<LW_Q4_K> : MF4<LW_Q4_K> {};
 template <>
 struct MF<LW_Q4_1> : MF4<LW_Q4_1> {};
+// The 5-bit formats share the 4-bit formats' scale data (read from their own
+// planes, passed in the same argument slots), and the biased code 128 + q with
+// q in [0, 31] is still an exact bfloat16: Q5_1 and Q5_K take Q4_1's and
+// Q4_K's coefficients as they are; Q5_0 is w = d (q - 16), so 128 + q =
+// (q - 16) + 144.
+template <>
+struct MF<LW_Q5_0> : MF4<LW_Q4_0> {
+    __device__ static void coef8(const uint32_t* r, int e, float* c1, float* c2) {
+        const float d = half_bits_to_float((r[e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
+        *c1 = d;
+        *c2 = -144.0f * d;
+    }
+};
+template <>
+struct MF<LW_Q5_1> : MF4<LW_Q4_1> {};
+template <>
+struct MF<LW_Q5_K> : MF4<LW_Q4_K> {};
+// MXFP4: the e2m1 values themselves are exact bfloat16 operands, so there is
+// no offset term: y += 2^(E - 127) * P, with the block's e8m0 exponent E.
+template <>
+struct MF<LW_MXFP4> {
+    static constexpr bool kSums = false;
+    static constexpr int kRaw = 2;  // the 8 exponent bytes of 8 blocks
+    __device__ static void load_scale8(const uint8_t* W, int64_t off1, int64_t, uint64_t row, uint32_t K, int blk0,
+                                       uint32_t* r) {
+        const uint2 v = *reinterpret_cast<const uint2*>(W + off1 + row * (K / 32u) + (uint32_t)blk0);
+        r[0] = v.x;
+        r[1] = v.y;
+    }
+    __device__ static void coef8(const uint32_t* r, int e, float* c1, float* c2) {
+        *c1 = e8m0_to_float((r[e >> 2] >> (8 * (e & 3))) & 0xFFu);
+        *c2 = 0.f;
+    }
+};
 
 template <>
 struct MF<LW_Q8_0> {
@@ -669,16 +703,59 @@ __device__ __forceinline__ void decode8(uint32_t w0, uint32_t w1, bf16x8* s0, bf
     *s1 = __builtin_bit_cast(bf16x8, b);
 }
 
+// The 5-bit formats: as decode8, with the fifth bits of the 16 elements
+// merged in first. hb holds them in element order: bits 0-7 for elements
+// 8h .. 8h+7 (K-step 0), bits 8-15 for 16 + 8h .. 16 + 8h + 7 (K-step 1).
+// spread4() moves the four bits at positions 4-7 of its argument to bit 4 of
+// each byte (one multiply: the four shifted copies do not overlap).
+__device__ __forceinline__ uint32_t spread4(uint32_t g) { return (g * 0x00204081u) & 0x10101010u; }
+__device__ __forceinline__ void decode8_q5(uint32_t w0, uint32_t w1, uint32_t hb, bf16x8* s0, bf16x8* s1) {
+    const uint32_t k43 = 0x43434343u;
+    const uint32_t l0 = opaque((w0 & 0x0F0F0F0Fu) | spread4((hb << 4) & 0xF0u));
+    const uint32_t l1 = opaque((w1 & 0x0F0F0F0Fu) | spread4(hb & 0xF0u));
+    const uint32_t h0 = opaque(((w0 >> 4) & 0x0F0F0F0Fu) | spread4((hb >> 4) & 0xF0u));
+    const uint32_t h1 = opaque(((w1 >> 4) & 0x0F0F0F0Fu) | spread4((hb >> 8) & 0xF0u));
+    const u32x4v a = {__builtin_amdgcn_perm(k43, l0, 0x04010400u), __builtin_amdgcn_perm(k43, l0, 0x04030402u),
+                      __builtin_amdgcn_perm(k43, l1, 0x04010400u), __builtin_amdgcn_perm(k43, l1, 0x04030402u)};
+    const u32x4v b = {__builtin_amdgcn_perm(k43, h0, 0x04010400u), __builtin_amdgcn_perm(k43, h0, 0x04030402u),
+                      __builtin_amdgcn_perm(k43, h1, 0x04010400u), __builtin_amdgcn_perm(k43, h1, 0x04030402u)};
+    *s0 = __builtin_bit_cast(bf16x8, a);
+    *s1 = __builtin_bit_cast(bf16x8, b);
+}
+
+// MXFP4: the bfloat16 of an e2m1 code from two 8-entry byte tables indexed
+// by its magnitude bits (high bytes 00 3F 3F 3F 40 40 40 40 and low bytes
+// 00 00 80 C0 00 40 80 C0: 0, 0.5, 1, 1.5, 2, 3, 4, 6), its sign bit moved
+// to bit 7 of the high byte; two more byte permutations interleave the low
+// and high bytes into bfloat16 pairs. Exact for every code.
+__device__ __forceinline__ void fp4_pairs(uint32_t idx, uint32_t sgn, uint32_t* p0, uint32_t* p1) {
+    const uint32_t hi = __builtin_amdgcn_perm(0x40404040u, 0x3F3F3F00u, idx) | sgn;
+    const uint32_t lo = __builtin_amdgcn_perm(0xC0804000u, 0xC0800000u, idx);
+    *p0 = __builtin_amdgcn_perm(hi, lo, 0x05010400u);
+    *p1 = __builtin_amdgcn_perm(hi, lo, 0x07030602u);
+}
+__device__ __forceinline__ void decode8_fp4(uint32_t w0, uint32_t w1, bf16x8* s0, bf16x8* s1) {
+    uint32_t a[4], b[4];
+    fp4_pairs(opaque(w0 & 0x07070707u), (w0 << 4) & 0x80808080u, &a[0], &a[1]);
+    fp4_pairs(opaque(w1 & 0x07070707u), (w1 << 4) & 0x80808080u, &a[2], &a[3]);
+    fp4_pairs(opaque((w0 >> 4) & 0x07070707u), w0 & 0x80808080u, &b[0], &b[1]);
+    fp4_pairs(opaque((w1 >> 4) & 0x07070707u), w1 & 0x80808080u, &b[2], &b[3]);
+    *s0 = __builtin_bit_cast(bf16x8, (u32x4v{a[0], a[1], a[2], a[3]}));
+    *s1 = __builtin_bit_cast(bf16x8, (u32x4v{b[0], b[1], b[2], b[3]}));
+}
+
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 template <int FMT, int WM>
 __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2, 2)))
     gemm32_kernel(const uint8_t* __restrict__ W, const float* __restrict__ x, float* __restrict__ y, int64_t M,
-                  int64_t K, int64_t N, int64_t off1, int64_t off2, GemmSplit sp) {
+                  int64_t K, int64_t N, int64_t off1, int64_t off2, int64_t offh, GemmSplit sp) {
     using T = MF<FMT>;
     using TL = Tile32<WM>;
     constexpr int BM = TL::BM, BN = TL::BN, NT = TL::NT, XI = TL::XI;
-    static_assert(FMT != LW_Q8_0 && T::kSums, "the 4-bit formats");
+    constexpr bool kQ5 = FMT == LW_Q5_0 || FMT == LW_Q5_1 || FMT == LW_Q5_K;
+    constexpr bool kFp4 = FMT == LW_MXFP4;
+    static_assert(FMT != LW_Q8_0 && (T::kSums || kFp4), "the formats over a 4-bit code plane");
     extern __shared__ bf16x8 smem[];
 
     const int tid = threadIdx.x;
@@ -727,11 +804,25 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
         wp[rt] = W + rr * (K32 / 2u) + 16u * (uint32_t)kb0 + 32u * (uint32_t)h;
     }
     u32x4v qraw[2][2], qcur[2][2];
+    // the 5-bit formats: the quad's 16 bytes of fifth bits of the lane's row
+    // (4 per block, byte j of a block for its elements 8j .. 8j+7)
+    const uint8_t* hp[2];
+    u32x4v hraw[2];
+    uint32_t hcur[2][2];
+    if constexpr (kQ5) {
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt) {
+            const int64_t r = row0 + 64 * wm + 32 * rt + n32;
+            const uint64_t rr = (uint64_t)(r < M ? r : M - 1);
+            hp[rt] = W + offh + rr * (K32 / 8u) + 4u * (uint32_t)kb0;
+        }
+    }
     auto load_quad = [&](int q) __attribute__((always_inline)) {
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt) {
             qraw[rt][0] = *reinterpret_cast<const u32x4v*>(wp[rt] + 64u * (uint32_t)q);
             qraw[rt][1] = *reinterpret_cast<const u32x4v*>(wp[rt] + 64u * (uint32_t)q + 16u);
+            if constexpr (kQ5) hraw[rt] = *reinterpret_cast<const u32x4v*>(hp[rt] + 16u * (uint32_t)q);
         }
     };
     // lanes 0-31 hold blocks 0, 1 of the quad and lanes 32-63 blocks 2, 3 (four
@@ -749,6 +840,16 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
                 const auto s13 = __builtin_amdgcn_permlane32_swap(v[1], v[3], false, false);
                 qcur[rt][hv] = u32x4v{s02[0], s13[0], s02[1], s13[1]};
             }
+        // fifth bits: bytes h and 2 + h of each block's word (the lane's
+        // elements of K-steps 0 and 1), two blocks per word
+        if constexpr (kQ5) {
+            const uint32_t hsel = 0x06040200u + 0x01010101u * (uint32_t)h;
+#pragma unroll
+            for (int rt = 0; rt < 2; ++rt) {
+                hcur[rt][0] = __builtin_amdgcn_perm(hraw[rt][1], hraw[rt][0], hsel);
+                hcur[rt][1] = __builtin_amdgcn_perm(hraw[rt][3], hraw[rt][2], hsel);
+            }
+        }
     };
 
     // ---- window coefficients: thread tid handles row tid, all 16 blocks ----
@@ -774,7 +875,7 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
                 float c1, c2;
                 T::coef8(sraw[hh], e, &c1, &c2);
                 c1w[b16 * BM + c_at] = c1;
-                c2_row[(b16 >> 2) * 128 + (b16 & 3)] = c2;
+                if constexpr (T::kSums) c2_row[(b16 >> 2) * 128 + (b16 & 3)] = c2;
             }
     };
 
@@ -811,12 +912,14 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
             float sum = split_bf16x8(v, &hv, &lv);
             xh[xo[i]] = hv;
             xl[xo[i]] = lv;
-            // the 4 quarters of (block, token) are one lane quad: after two
-            // exchanges every lane holds the block sum; all four store it
-            const int b16 = (st * kKB + xb_[i]) % kWin;
-            sum += dpp_move<0xB1>(sum);
-            sum += dpp_move<0x4E>(sum);
-            win_s(st * kKB / kWin)[so[i] + (b16 >> 2) * 4 * BN + (b16 & 3)] = sum;
+            if constexpr (T::kSums) {
+                // the 4 quarters of (block, token) are one lane quad: after two
+                // exchanges every lane holds the block sum; all four store it
+                const int b16 = (st * kKB + xb_[i]) % kWin;
+                sum += dpp_move<0xB1>(sum);
+                sum += dpp_move<0x4E>(sum);
+                win_s(st * kKB / kWin)[so[i] + (b16 >> 2) * 4 * BN + (b16 & 3)] = sum;
+            }
         }
     };
 
@@ -859,7 +962,14 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
             for (int rt = 0; rt < 2; ++rt) {
                 uint32_t w0, w1;
                 pair_of(rt, j0 + b, &w0, &w1);
-                decode8(w0, w1, &bw[rt][0], &bw[rt][1]);
+                if constexpr (kQ5) {
+                    const int jb = j0 + b;
+                    decode8_q5(w0, w1, (hcur[rt][jb >> 1] >> (16 * (jb & 1))) & 0xFFFFu, &bw[rt][0], &bw[rt][1]);
+                } else if constexpr (kFp4) {
+                    decode8_fp4(w0, w1, &bw[rt][0], &bw[rt][1]);
+                } else {
+                    decode8(w0, w1, &bw[rt][0], &bw[rt][1]);
+                }
             }
 #pragma unroll
             for (int tt = 0; tt < 2; ++tt) {
@@ -899,8 +1009,9 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
     };
     // acc += S(window) . c2(window)^T for window w: two K-steps of 8 blocks on
     // v_mfma_f32_32x32x8_bf16, S and c2 split three ways into bf16 parts
-    // (blocks past the split's end: S masked to zero)
+    // (blocks past the split's end: S masked to zero); none without offsets
     auto bias = [&](int w) __attribute__((always_inline)) {
+        if constexpr (!T::kSums) return;
         const int nv = nb - w * kWin < kWin ? nb - w * kWin : kWin;
         const float4* sw = reinterpret_cast<const float4*>(win_s(w));
         const float4* cw = reinterpret_cast<const float4*>(win_c2);
@@ -1084,8 +1195,15 @@ hipError_t launch_tile32(const uint8_t* W, const float* x, float* y, int64_t M, 
     if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
     if (query_only(kernel_name<Name_gemm32_kernel, FMT, WM>(), sp.ks > 1 ? 2 : 1)) return hipSuccess;
     if (sp.ks > 1) zero_fill(y, n_tok * M, stream);
+    // scale planes in the first two offset slots, the fifth-bit plane apart
+    int64_t o1 = p.off1, o2 = p.off2, oh = 0;
+    if constexpr (FMT == LW_Q5_0 || FMT == LW_Q5_1 || FMT == LW_Q5_K) {
+        o1 = p.off2;
+        o2 = p.off3;
+        oh = p.off1;
+    }
     hipLaunchKernelGGL((gemm32_kernel<FMT, WM>), dim3((unsigned)grid), dim3(TL::NT), TL::bytes(), stream, W, x, y,
-                       M, K, n_tok, p.off1, p.off2, sp);
+                       M, K, n_tok, o1, o2, oh, sp);
     return hipGetLastError();
 }
 
@@ -1109,6 +1227,10 @@ hipError_t launch_prefill(int fmt, const uint8_t* W, const float* x, float* y, i
     case LW_Q4_K: return launch_gemm<LW_Q4_K>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q4_1: return launch_gemm<LW_Q4_1>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q8_0: return launch_gemm<LW_Q8_0>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q5_0: return launch_gemm<LW_Q5_0>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q5_1: return launch_gemm<LW_Q5_1>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q5_K: return launch_gemm<LW_Q5_K>(W, x, y, M, K, n_tok, p, stream);
+    case LW_MXFP4: return launch_gemm<LW_MXFP4>(W, x, y, M, K, n_tok, p, stream);
     default:
         // f16 and q1_0 weights: token blocks of the matrix-vector kernel
         // (float32 throughout), all whole blocks in one launch
