@@ -141,9 +141,10 @@ enum {
 /* Token blocks of the VALU matrix-vector kernel: f16 and Q8_0 weights take
  * it for up to this many tokens (W streamed once, every token reusing each
  * decoded weight in registers). The 4-bit formats take a VALU kernel for one
- * or two tokens and the matrix cores from three tokens on; Q8_0 takes the
- * matrix cores above this bound; f16 stays on the VALU kernel, in blocks of
- * this many tokens. lw_kernel_name names the kernel a call selects. */
+ * or two tokens and the matrix cores from three tokens on; Q8_0, Q5_0, Q5_1,
+ * Q5_K, Q6_K, Q2_K and MXFP4 take the matrix cores above this bound; f16 and
+ * q1_0 stay on the VALU kernel, in token blocks. lw_kernel_name names the
+ * kernel a call selects. */
 #define LW_GEMV_MAX_TOK 8
 
 /*
@@ -167,10 +168,11 @@ enum {
  *
  * Arithmetic: products and sums in float32 with float32 accumulation (no
  * reduced-precision activations) on the VALU paths. The matrix-core paths
- * (4-bit formats from three tokens, Q8_0 above LW_GEMV_MAX_TOK tokens)
- * multiply exact integer codes by activations split into a bfloat16 high
- * part and a bfloat16 low part, accumulating in float32. Every path's error
- * relative to sum_k |w * x| stays below 1e-4.
+ * (4-bit formats from three tokens; Q8_0, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K and
+ * MXFP4 above LW_GEMV_MAX_TOK tokens) multiply exact bfloat16 codes (integer
+ * codes, or the e2m1 values of MXFP4) by activations split into a bfloat16
+ * high part and a bfloat16 low part, accumulating in float32. Every path's
+ * error relative to sum_k |w * x| stays below 1e-4.
  */
 LW_API int lw_matvec(int fmt, const void* W, const float* x, float* y,
               int64_t M, int64_t K, int64_t n_tok, void* stream);

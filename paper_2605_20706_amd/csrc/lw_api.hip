@@ -10,9 +10,11 @@
 // rows, one MFMA K step per 32-element block); Q8_0 with up to
 // LW_GEMV_MAX_TOK tokens -> the VALU kernels, up to 16 -> the matrix-core
 // kernel with K split across waves; more tokens -> the
-// tiled matrix-core (prefill) kernel. f16 weights use the VALU kernel in
-// token blocks of LW_GEMV_MAX_TOK for any token count. lw_matvec_ws (a
-// workspace) sends LW_MXFP4 prefill to the fp4 matrix cores.
+// tiled matrix-core (prefill) kernel. The other quantized formats (Q5_0,
+// Q5_1, Q5_K, Q6_K, Q2_K, MXFP4) run up to LW_GEMV_MAX_TOK tokens on the
+// VALU kernels and more on the tiled matrix-core kernel. f16 and q1_0
+// weights use the VALU kernel in token blocks for any token count.
+// lw_matvec_ws (a workspace) sends LW_MXFP4 prefill to the fp4 matrix cores.
 #include <cmath>
 
 #include "lw_internal.hpp"

@@ -1,31 +1,37 @@
-// Prefill product on the matrix cores (n_tok > 16; the 4-bit and 8-bit formats).
+// Prefill product on the matrix cores (many tokens; every quantized format
+// but q1_0).
 //
 // Y[t][r] = sum_k value(W, r*K + k) * X[t][k]. With many tokens the product is
-// a contraction over K with a token dimension, so it runs on
-// v_mfma_f32_16x16x32_bf16 (Sec. 3.2: matrix multiplication tiles through
-// shared memory and uses the cooperative matrix instructions of the device;
-// Sec. 3.3: quantized blocks are dequantized on the way in and each decoded
-// tile is reused for every token of the workgroup).
+// a contraction over K with a token dimension, so it runs on the matrix cores
+// (Sec. 3.2: matrix multiplication tiles through shared memory and uses the
+// cooperative matrix instructions of the device; Sec. 3.3: quantized blocks
+// are dequantized on the way in and each decoded tile is reused for every
+// token of the workgroup): gemm32_kernel on v_mfma_f32_32x32x16_bf16 for the
+// formats with at most 6-bit codes and MXFP4, gemm_kernel on
+// v_mfma_f32_16x16x32_bf16 for Q8_0.
 //
-// Precision. One MFMA K-step is one 32-element block. The weight operand holds
-// exact bfloat16 values derived from the integer codes only: for the 4-bit
-// formats the biased code 128 + q (bits 0x4300 | q), for Q8_0 the code q. X is
-// split into bf16 high and low parts (x = hi + lo to 2^-17 relative), two
-// MFMAs per tile and block, float32 accumulation. The block's scale, min and
-// bias are applied to its float32 partial P:
-//   Q4_0:   y += d * P - 136 * d * S     (128 + q = (q - 8) + 136)
-//   Q4_K:   y += d*sc * P - (128*d*sc + dmin*m) * S
-//   Q4_1:   y += d * P + (m - 128*d) * S
-//   Q8_0:   y += d * P
-// where S = sum over the block of (hi + lo), the very values fed to the
+// Precision. The weight operand holds exact bfloat16 values derived from the
+// integer codes only: the biased code 128 + q (bits 0x4300 | q, q < 64) for
+// the formats with an offset, the code q for Q8_0, the e2m1 value for MXFP4.
+// X is split into bf16 high and low parts (x = hi + lo to 2^-17 relative),
+// two MFMAs per tile and K-step, float32 accumulation. A coefficient unit
+// (a 32-element block, or a 16-element sub-block for Q6_K and Q2_K) applies
+// its scale, min and bias to its float32 partial P:
+//   Q4_0:   y += d * P - 136 * d * S             (128 + q = (q - 8) + 136)
+//   Q5_0:   y += d * P - 144 * d * S             (128 + q = (q - 16) + 144)
+//   Q4_1, Q5_1:  y += d * P + (m - 128*d) * S
+//   Q4_K, Q5_K:  y += d*sc * P - (128*d*sc + dmin*m) * S
+//   Q6_K:   y += d*sc * P - 160 * d*sc * S       (128 + q = (q - 32) + 160)
+//   Q2_K:   y += d*sc * P - (128*d*sc + dmin*m) * S
+//   Q8_0:   y += d * P;   MXFP4:  y += 2^(E - 127) * P
+// where S = sum over the unit of (hi + lo), the very values fed to the
 // matrix core, so the bias cancels to float32 rounding. The error relative
 // to sum_k |w * x| stays near 1e-5.
 //
-// Layout of one block in the MFMA operands: lane slice s (lanes 16s..16s+15)
-// holds 8 of the block's 32 elements. For the 4-bit formats slice s takes the
-// 32-bit word s of the block's 16 code bytes, i.e. elements 4s..4s+3 (low
-// nibbles) and 16+4s..16+4s+3 (high nibbles); for Q8_0, elements 8s..8s+7.
-// The X operand in LDS uses the same order of k.
+// Layout of one block in the 16 x 16 x 32 operands: lane slice s (lanes
+// 16s..16s+15) holds 8 of the block's 32 elements (Q8_0: elements 8s..8s+7).
+// The 32 x 32 x 16 layout is described at gemm32_kernel. The X operand in LDS
+// uses the same order of k.
 #include "lw_device.hpp"
 #include "lw_internal.hpp"
 
@@ -191,6 +197,51 @@ template <>
 struct MF<LW_Q5_1> : MF4<LW_Q4_1> {};
 template <>
 struct MF<LW_Q5_K> : MF4<LW_Q4_K> {};
+// The formats with 16-element sub-blocks: one coefficient pair per sub-block
+// (one MFMA K-step), read for the 16 sub-blocks of 8 blocks (one super-block)
+// at a time. Q6_K: w = d sc (q - 32), 6-bit q, signed 8-bit sc, so 128 + q =
+// (q - 32) + 160. Q2_K: w = d sc q - dmin m, 2-bit q, 4-bit sc and m.
+template <>
+struct MF<LW_Q6_K> {
+    static constexpr bool kSums = true;
+    static constexpr int kRaw = 5;  // 16 scale bytes, then d
+    __device__ static void load_scale16(const uint8_t* W, int64_t off1, int64_t off2, uint64_t row, uint32_t K,
+                                        int blk0, uint32_t* r) {
+        const uint4 v = *reinterpret_cast<const uint4*>(W + off1 + row * (K / 16u) + 2u * (uint32_t)blk0);
+        r[0] = v.x;
+        r[1] = v.y;
+        r[2] = v.z;
+        r[3] = v.w;
+        r[4] = *reinterpret_cast<const uint16_t*>(W + off2 + 2u * (row * (K / 256u) + (uint32_t)(blk0 >> 3)));
+    }
+    __device__ static void coef16(const uint32_t* r, int u, float* c1, float* c2) {
+        const float ds = half_bits_to_float(r[4]) * (float)sbyte_at(r[u >> 2], u & 3);  // exact
+        *c1 = ds;
+        *c2 = -160.0f * ds;  // exact
+    }
+    __device__ static int sbyte_at(uint32_t w, int i) { return (int)(int8_t)(uint8_t)(w >> (8 * i)); }
+};
+template <>
+struct MF<LW_Q2_K> {
+    static constexpr bool kSums = true;
+    static constexpr int kRaw = 5;  // 16 {scale, min} bytes, then {d, dmin}
+    __device__ static void load_scale16(const uint8_t* W, int64_t off1, int64_t off2, uint64_t row, uint32_t K,
+                                        int blk0, uint32_t* r) {
+        const uint4 v = *reinterpret_cast<const uint4*>(W + off1 + row * (K / 16u) + 2u * (uint32_t)blk0);
+        r[0] = v.x;
+        r[1] = v.y;
+        r[2] = v.z;
+        r[3] = v.w;
+        r[4] = *reinterpret_cast<const uint32_t*>(W + off2 + 4u * (row * (K / 256u) + (uint32_t)(blk0 >> 3)));
+    }
+    __device__ static void coef16(const uint32_t* r, int u, float* c1, float* c2) {
+        const uint32_t scm = (r[u >> 2] >> (8 * (u & 3))) & 0xFFu;
+        const float ds = half_bits_to_float(r[4] & 0xFFFFu) * (float)(scm & 15u);  // exact
+        const float dm = half_bits_to_float(r[4] >> 16) * (float)(scm >> 4);       // exact
+        *c1 = ds;
+        *c2 = -__builtin_fmaf(128.0f, ds, dm);
+    }
+};
 // MXFP4: the e2m1 values themselves are exact bfloat16 operands, so there is
 // no offset term: y += 2^(E - 127) * P, with the block's e8m0 exponent E.
 template <>
@@ -723,6 +774,47 @@ __device__ __forceinline__ void decode8_q5(uint32_t w0, uint32_t w1, uint32_t hb
     *s1 = __builtin_bit_cast(bf16x8, b);
 }
 
+// Four 2-bit fields (bits 0-7 of g) to bits 4-5 (spread2_hi) or 0-1
+// (spread2_lo) of the four bytes: two shift-or-mask steps, no carries.
+__device__ __forceinline__ uint32_t spread2_hi(uint32_t g) {
+    const uint32_t u = ((g << 4) | (g << 16)) & 0x00F000F0u;  // fields 0, 1 at bits 4-7; 2, 3 at 20-23
+    return (u | (u << 6)) & 0x30303030u;
+}
+__device__ __forceinline__ uint32_t spread2_lo(uint32_t g) {
+    const uint32_t u = (g | (g << 12)) & 0x000F000Fu;  // fields 0, 1 at bits 0-3; 2, 3 at 16-19
+    return (u | (u << 6)) & 0x03030303u;
+}
+// Q6_K: as decode8, with the two high bits of the 16 elements merged in. hw
+// holds them in element order, two bits each: bits 0-15 for elements 8h ..
+// 8h+7 (K-step 0), bits 16-31 for 16 + 8h .. 16 + 8h + 7 (K-step 1).
+__device__ __forceinline__ void decode8_q6(uint32_t w0, uint32_t w1, uint32_t hw, bf16x8* s0, bf16x8* s1) {
+    const uint32_t k43 = 0x43434343u;
+    const uint32_t l0 = opaque((w0 & 0x0F0F0F0Fu) | spread2_hi(hw & 0xFFu));
+    const uint32_t l1 = opaque((w1 & 0x0F0F0F0Fu) | spread2_hi((hw >> 8) & 0xFFu));
+    const uint32_t h0 = opaque(((w0 >> 4) & 0x0F0F0F0Fu) | spread2_hi((hw >> 16) & 0xFFu));
+    const uint32_t h1 = opaque(((w1 >> 4) & 0x0F0F0F0Fu) | spread2_hi(hw >> 24));
+    const u32x4v a = {__builtin_amdgcn_perm(k43, l0, 0x04010400u), __builtin_amdgcn_perm(k43, l0, 0x04030402u),
+                      __builtin_amdgcn_perm(k43, l1, 0x04010400u), __builtin_amdgcn_perm(k43, l1, 0x04030402u)};
+    const u32x4v b = {__builtin_amdgcn_perm(k43, h0, 0x04010400u), __builtin_amdgcn_perm(k43, h0, 0x04030402u),
+                      __builtin_amdgcn_perm(k43, h1, 0x04010400u), __builtin_amdgcn_perm(k43, h1, 0x04030402u)};
+    *s0 = __builtin_bit_cast(bf16x8, a);
+    *s1 = __builtin_bit_cast(bf16x8, b);
+}
+// Q2_K: the 2-bit codes alone, in the same layout as decode8_q6's hw.
+__device__ __forceinline__ void decode8_q2(uint32_t hw, bf16x8* s0, bf16x8* s1) {
+    const uint32_t k43 = 0x43434343u;
+    const uint32_t l0 = opaque(spread2_lo(hw & 0xFFu));
+    const uint32_t l1 = opaque(spread2_lo((hw >> 8) & 0xFFu));
+    const uint32_t h0 = opaque(spread2_lo((hw >> 16) & 0xFFu));
+    const uint32_t h1 = opaque(spread2_lo(hw >> 24));
+    const u32x4v a = {__builtin_amdgcn_perm(k43, l0, 0x04010400u), __builtin_amdgcn_perm(k43, l0, 0x04030402u),
+                      __builtin_amdgcn_perm(k43, l1, 0x04010400u), __builtin_amdgcn_perm(k43, l1, 0x04030402u)};
+    const u32x4v b = {__builtin_amdgcn_perm(k43, h0, 0x04010400u), __builtin_amdgcn_perm(k43, h0, 0x04030402u),
+                      __builtin_amdgcn_perm(k43, h1, 0x04010400u), __builtin_amdgcn_perm(k43, h1, 0x04030402u)};
+    *s0 = __builtin_bit_cast(bf16x8, a);
+    *s1 = __builtin_bit_cast(bf16x8, b);
+}
+
 // MXFP4: the bfloat16 of an e2m1 code from two 8-entry byte tables indexed
 // by its magnitude bits (high bytes 00 3F 3F 3F 40 40 40 40 and low bytes
 // 00 00 80 C0 00 40 80 C0: 0, 0.5, 1, 1.5, 2, 3, 4, 6), its sign bit moved
@@ -755,7 +847,11 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
     constexpr int BM = TL::BM, BN = TL::BN, NT = TL::NT, XI = TL::XI;
     constexpr bool kQ5 = FMT == LW_Q5_0 || FMT == LW_Q5_1 || FMT == LW_Q5_K;
     constexpr bool kFp4 = FMT == LW_MXFP4;
-    static_assert(FMT != LW_Q8_0 && (T::kSums || kFp4), "the formats over a 4-bit code plane");
+    constexpr bool kQ6 = FMT == LW_Q6_K, kQ2 = FMT == LW_Q2_K;
+    constexpr bool kSub16 = kQ6 || kQ2;  // one coefficient pair per 16-element K-step
+    // a window holds kWin coefficient units: blocks, or the sub-blocks of kWin / 2 blocks
+    constexpr int KWB = kSub16 ? kWin / 2 : kWin;
+    static_assert(FMT != LW_Q8_0 && (T::kSums || kFp4), "the formats with 32-element K-steps of bf16 codes");
     extern __shared__ bf16x8 smem[];
 
     const int tid = threadIdx.x;
@@ -780,7 +876,7 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
     const int kb0 = 8 * sb0;
     const int nb = 8 * (sb1 - sb0);
     const int nst = nb / kKB;
-    const int nwin = (nb + kWin - 1) / kWin;
+    const int nwin = (nb + KWB - 1) / KWB;
 
     char* lds = reinterpret_cast<char*>(smem);
     auto st_xh = [&](int bf) __attribute__((always_inline)) { return reinterpret_cast<bf16x8*>(lds + bf * TL::kStage); };
@@ -806,23 +902,31 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
     u32x4v qraw[2][2], qcur[2][2];
     // the 5-bit formats: the quad's 16 bytes of fifth bits of the lane's row
     // (4 per block, byte j of a block for its elements 8j .. 8j+7)
+    // the 2-bit planes (Q6_K high bits, Q2_K codes): 8 bytes per block, lane
+    // (h, n) reads blocks 2h, 2h + 1 of the quad (16 bytes)
     const uint8_t* hp[2];
     u32x4v hraw[2];
-    uint32_t hcur[2][2];
-    if constexpr (kQ5) {
+    uint32_t hcur[2][kSub16 ? 4 : 2];
+    if constexpr (kQ5 || kSub16) {
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt) {
             const int64_t r = row0 + 64 * wm + 32 * rt + n32;
             const uint64_t rr = (uint64_t)(r < M ? r : M - 1);
-            hp[rt] = W + offh + rr * (K32 / 8u) + 4u * (uint32_t)kb0;
+            if constexpr (kQ5)
+                hp[rt] = W + offh + rr * (K32 / 8u) + 4u * (uint32_t)kb0;
+            else
+                hp[rt] = W + offh + rr * (K32 / 4u) + 8u * (uint32_t)kb0 + 16u * (uint32_t)h;
         }
     }
     auto load_quad = [&](int q) __attribute__((always_inline)) {
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt) {
-            qraw[rt][0] = *reinterpret_cast<const u32x4v*>(wp[rt] + 64u * (uint32_t)q);
-            qraw[rt][1] = *reinterpret_cast<const u32x4v*>(wp[rt] + 64u * (uint32_t)q + 16u);
+            if constexpr (!kQ2) {
+                qraw[rt][0] = *reinterpret_cast<const u32x4v*>(wp[rt] + 64u * (uint32_t)q);
+                qraw[rt][1] = *reinterpret_cast<const u32x4v*>(wp[rt] + 64u * (uint32_t)q + 16u);
+            }
             if constexpr (kQ5) hraw[rt] = *reinterpret_cast<const u32x4v*>(hp[rt] + 16u * (uint32_t)q);
+            if constexpr (kSub16) hraw[rt] = *reinterpret_cast<const u32x4v*>(hp[rt] + 32u * (uint32_t)q);
         }
     };
     // lanes 0-31 hold blocks 0, 1 of the quad and lanes 32-63 blocks 2, 3 (four
@@ -834,7 +938,7 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-            for (int hv = 0; hv < 2; ++hv) {
+            for (int hv = 0; hv < (kQ2 ? 0 : 2); ++hv) {
                 const u32x4v v = qraw[rt][hv];
                 const auto s02 = __builtin_amdgcn_permlane32_swap(v[0], v[2], false, false);
                 const auto s13 = __builtin_amdgcn_permlane32_swap(v[1], v[3], false, false);
@@ -850,6 +954,25 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
                 hcur[rt][1] = __builtin_amdgcn_perm(hraw[rt][3], hraw[rt][2], hsel);
             }
         }
+        // 2-bit planes: block k of the lane's pair as words (w0, w1) = bytes
+        // 0-3, 4-7; lanes of half h need bytes 2h, 2h+1 of each (elements 8h ..
+        // 8h+7 and 16 + 8h .. 16 + 8h + 7). Each lane packs the bytes the
+        // lower half needs (0, 1, 4, 5) and those the upper half needs (2, 3,
+        // 6, 7) of its own block k; one swap across the halves then leaves
+        // every lane its bytes of block k and of block 2 + k.
+        if constexpr (kSub16) {
+#pragma unroll
+            for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+                for (int k = 0; k < 2; ++k) {
+                    const uint32_t w0 = hraw[rt][2 * k], w1 = hraw[rt][2 * k + 1];
+                    const uint32_t lo = __builtin_amdgcn_perm(w1, w0, 0x05040100u);
+                    const uint32_t hi = __builtin_amdgcn_perm(w1, w0, 0x07060302u);
+                    const auto r = __builtin_amdgcn_permlane32_swap(lo, hi, false, false);
+                    hcur[rt][k] = r[0];
+                    hcur[rt][2 + k] = r[1];
+                }
+        }
     };
 
     // ---- window coefficients: thread tid handles row tid, all 16 blocks ----
@@ -859,10 +982,13 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
     uint32_t sraw[2][T::kRaw];
     auto load_win_scales = [&](int w) __attribute__((always_inline)) {
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-            int blk0 = kb0 + w * kWin + 8 * hh;
+        for (int hh = 0; hh < (kSub16 ? 1 : 2); ++hh) {
+            int blk0 = kb0 + w * KWB + 8 * hh;
             blk0 = blk0 < kb0 + nb ? blk0 : kb0 + nb - 8;  // past the split: a valid copy, never used
-            T::load_scale8(W, off1, off2, (uint64_t)crow, K32, blk0, sraw[hh]);
+            if constexpr (kSub16)
+                T::load_scale16(W, off1, off2, (uint64_t)crow, K32, blk0, sraw[hh]);
+            else
+                T::load_scale8(W, off1, off2, (uint64_t)crow, K32, blk0, sraw[hh]);
         }
     };
     auto put_win_scales = [&](int w) __attribute__((always_inline)) {
@@ -871,9 +997,12 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
         for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                const int b16 = 8 * hh + e;
+                const int b16 = 8 * hh + e;  // coefficient unit of the window
                 float c1, c2;
-                T::coef8(sraw[hh], e, &c1, &c2);
+                if constexpr (kSub16)
+                    T::coef16(sraw[0], b16, &c1, &c2);
+                else
+                    T::coef8(sraw[hh], e, &c1, &c2);
                 c1w[b16 * BM + c_at] = c1;
                 if constexpr (T::kSums) c2_row[(b16 >> 2) * 128 + (b16 & 3)] = c2;
             }
@@ -882,7 +1011,7 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
     // ---- X stage producer: item (block b, token t, quarter q = 2s + hx):
     // elements 16s + 8hx .. +7 of the block for token t ----
     const float* xp[XI];
-    int xo[XI], so[XI], xb_[XI];
+    int xo[XI], so[XI], xb_[XI], xs_[XI];
 #pragma unroll
     for (int i = 0; i < XI; ++i) {
         const int it = tid + i * NT;
@@ -890,8 +1019,9 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
         const int64_t tk = tok0 + t < N ? tok0 + t : N - 1;  // past N: the last token, never stored
         xp[i] = x + tk * K + 32 * (int64_t)(kb0 + b) + 8 * q;
         xo[i] = (b * 4 + q) * BN + (t ^ (q << 2));  // the four quarters of a token in four bank groups
-        so[i] = t * 4;                               // S slot of (t, block 0); + (b16 >> 2) * 4 BN + (b16 & 3)
+        so[i] = t * 4;                               // S slot of (t, unit 0); + (u >> 2) * 4 BN + (u & 3)
         xb_[i] = b;
+        xs_[i] = q >> 1;                             // the K-step (sub-block) of the quarter
     }
     float4 xa[XI], xb[XI];
     auto fetch = [&](int st) __attribute__((always_inline)) {
@@ -912,7 +1042,13 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
             float sum = split_bf16x8(v, &hv, &lv);
             xh[xo[i]] = hv;
             xl[xo[i]] = lv;
-            if constexpr (T::kSums) {
+            if constexpr (kSub16) {
+                // quarters 2s, 2s + 1 of (block, token) are a lane pair: one
+                // exchange gives both the sum of sub-block s; both store it
+                const int u = 2 * ((st * kKB + xb_[i]) % KWB) + xs_[i];
+                sum += dpp_move<0xB1>(sum);
+                win_s(st * kKB / KWB)[so[i] + (u >> 2) * 4 * BN + (u & 3)] = sum;
+            } else if constexpr (T::kSums) {
                 // the 4 quarters of (block, token) are one lane quad: after two
                 // exchanges every lane holds the block sum; all four store it
                 const int b16 = (st * kKB + xb_[i]) % kWin;
@@ -944,7 +1080,7 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
     auto compute = [&](int bf, int st, int j0) __attribute__((always_inline)) {
         const bf16x8* xh = st_xh(bf);
         const bf16x8* xl = st_xl(bf);
-        const float2* c1w = reinterpret_cast<const float2*>(win_c1(st * kKB / kWin));
+        const float2* c1w = reinterpret_cast<const float2*>(win_c1(st * kKB / KWB));
         // A operands one token tile ahead (across the block boundary too)
         bf16x8 an[2][2];  // [s][hi, lo]
 #pragma unroll
@@ -954,17 +1090,33 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
         }
 #pragma unroll
         for (int b = 0; b < kKB; ++b) {
-            const int b16 = (st * kKB + b) % kWin;
-            const float2 c1v = c1w[(b16 * BM + 64 * wm) / 2 + n32];
-            const float c1[2] = {c1v.x, c1v.y};
+            const int b16 = (st * kKB + b) % KWB;
+            // c1 of K-step 0 (the block's, or its first sub-block's) and, with
+            // 16-element sub-blocks, c1b of K-step 1; [rt]
+            float c1[2], c1b[2];
+            {
+                const int u0 = kSub16 ? 2 * b16 : b16;
+                const float2 c1v = c1w[(u0 * BM + 64 * wm) / 2 + n32];
+                c1[0] = c1v.x;
+                c1[1] = c1v.y;
+                if constexpr (kSub16) {
+                    const float2 c1u = c1w[((u0 + 1) * BM + 64 * wm) / 2 + n32];
+                    c1b[0] = c1u.x;
+                    c1b[1] = c1u.y;
+                }
+            }
             bf16x8 bw[2][2];  // [rt][s]
 #pragma unroll
             for (int rt = 0; rt < 2; ++rt) {
-                uint32_t w0, w1;
-                pair_of(rt, j0 + b, &w0, &w1);
+                uint32_t w0 = 0, w1 = 0;
+                if constexpr (!kQ2) pair_of(rt, j0 + b, &w0, &w1);
                 if constexpr (kQ5) {
                     const int jb = j0 + b;
                     decode8_q5(w0, w1, (hcur[rt][jb >> 1] >> (16 * (jb & 1))) & 0xFFFFu, &bw[rt][0], &bw[rt][1]);
+                } else if constexpr (kQ6) {
+                    decode8_q6(w0, w1, hcur[rt][j0 + b], &bw[rt][0], &bw[rt][1]);
+                } else if constexpr (kQ2) {
+                    decode8_q2(hcur[rt][j0 + b], &bw[rt][0], &bw[rt][1]);
                 } else if constexpr (kFp4) {
                     decode8_fp4(w0, w1, &bw[rt][0], &bw[rt][1]);
                 } else {
@@ -999,10 +1151,20 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
                     for (int v = 0; v < 16; ++v) pz[v] = 0.f;
                     f32x16 p = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0][0], bw[rt][0], pz, 0, 0, 0);
                     p = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0][1], bw[rt][0], p, 0, 0, 0);
-                    p = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[1][0], bw[rt][1], p, 0, 0, 0);
-                    p = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[1][1], bw[rt][1], p, 0, 0, 0);
+                    if constexpr (kSub16) {
+                        // each K-step is a sub-block with its own scale
 #pragma unroll
-                    for (int v = 0; v < 16; ++v) acc[rt][tt][v] = __builtin_fmaf(c1[rt], p[v], acc[rt][tt][v]);
+                        for (int v = 0; v < 16; ++v) acc[rt][tt][v] = __builtin_fmaf(c1[rt], p[v], acc[rt][tt][v]);
+                        p = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[1][0], bw[rt][1], pz, 0, 0, 0);
+                        p = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[1][1], bw[rt][1], p, 0, 0, 0);
+#pragma unroll
+                        for (int v = 0; v < 16; ++v) acc[rt][tt][v] = __builtin_fmaf(c1b[rt], p[v], acc[rt][tt][v]);
+                    } else {
+                        p = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[1][0], bw[rt][1], p, 0, 0, 0);
+                        p = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[1][1], bw[rt][1], p, 0, 0, 0);
+#pragma unroll
+                        for (int v = 0; v < 16; ++v) acc[rt][tt][v] = __builtin_fmaf(c1[rt], p[v], acc[rt][tt][v]);
+                    }
                 }
             }
         }
@@ -1012,7 +1174,8 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
     // (blocks past the split's end: S masked to zero); none without offsets
     auto bias = [&](int w) __attribute__((always_inline)) {
         if constexpr (!T::kSums) return;
-        const int nv = nb - w * kWin < kWin ? nb - w * kWin : kWin;
+        const int nvb = nb - w * KWB < KWB ? nb - w * KWB : KWB;  // valid blocks of the window
+        const int nv = kSub16 ? 2 * nvb : nvb;                    // valid coefficient units
         const float4* sw = reinterpret_cast<const float4*>(win_s(w));
         const float4* cw = reinterpret_cast<const float4*>(win_c2);
 #pragma unroll
@@ -1053,8 +1216,8 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
             for (int tt = 0; tt < 2; ++tt) asm volatile("" : "+v"(acc[rt][tt]));
     };
     auto window_end = [&](int st) __attribute__((always_inline)) {
-        if (((st + 1) * kKB) % kWin == 0 || st == nst - 1) {
-            const int w = st * kKB / kWin;
+        if (((st + 1) * kKB) % KWB == 0 || st == nst - 1) {
+            const int w = st * kKB / KWB;
             bias(w);
             __syncthreads();
             if (w + 1 < nwin) put_win_scales(w + 1);
@@ -1197,11 +1360,11 @@ hipError_t launch_tile32(const uint8_t* W, const float* x, float* y, int64_t M, 
     if (sp.ks > 1) zero_fill(y, n_tok * M, stream);
     // scale planes in the first two offset slots, the fifth-bit plane apart
     int64_t o1 = p.off1, o2 = p.off2, oh = 0;
-    if constexpr (FMT == LW_Q5_0 || FMT == LW_Q5_1 || FMT == LW_Q5_K) {
+    if constexpr (FMT == LW_Q5_0 || FMT == LW_Q5_1 || FMT == LW_Q5_K || FMT == LW_Q6_K) {
         o1 = p.off2;
         o2 = p.off3;
         oh = p.off1;
-    }
+    }  // Q2_K: its 2-bit code plane is plane 0 (oh = 0), the scales planes 1 and 2
     hipLaunchKernelGGL((gemm32_kernel<FMT, WM>), dim3((unsigned)grid), dim3(TL::NT), TL::bytes(), stream, W, x, y,
                        M, K, n_tok, o1, o2, oh, sp);
     return hipGetLastError();
@@ -1231,6 +1394,8 @@ hipError_t launch_prefill(int fmt, const uint8_t* W, const float* x, float* y, i
     case LW_Q5_1: return launch_gemm<LW_Q5_1>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q5_K: return launch_gemm<LW_Q5_K>(W, x, y, M, K, n_tok, p, stream);
     case LW_MXFP4: return launch_gemm<LW_MXFP4>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q6_K: return launch_gemm<LW_Q6_K>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q2_K: return launch_gemm<LW_Q2_K>(W, x, y, M, K, n_tok, p, stream);
     default:
         // f16 and q1_0 weights: token blocks of the matrix-vector kernel
         // (float32 throughout), all whole blocks in one launch

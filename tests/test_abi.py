@@ -214,11 +214,9 @@ def test_kernel_selection_table(lib):
     for fmt in (Q5_0, Q5_1, Q5_K, Q6_K, Q2_K, 11):            # the VALU kernels up to 8 tokens
         assert kind(fmt, 14336, 4096, 1) == "gemv1_kernel"
         assert kind(fmt, 14336, 4096, 4) == "gemv_kernel"
-    for fmt in (Q5_0, Q5_1, Q5_K, 11):                        # over a 4-bit code plane: the tiled matrix cores
+    for fmt in (Q5_0, Q5_1, Q5_K, Q6_K, Q2_K, 11):            # from 9 tokens: the tiled matrix cores
         assert kind(fmt, 14336, 4096, 12) == "gemm32_kernel"
         assert kind(fmt, 14336, 4096, 512) == "gemm32_kernel"
-    for fmt in (Q6_K, Q2_K):                                  # 16-element sub-blocks: VALU token blocks
-        assert kind(fmt, 14336, 4096, 512) == "gemv_kernel"
 
 
 def test_ceiling_library_exports_and_checks():
