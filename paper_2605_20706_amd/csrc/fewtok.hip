@@ -1,5 +1,6 @@
-// Few-token product (2 <= n_tok <= 8) over the 4-bit formats on the matrix
-// cores, with the activations converted once per workgroup.
+// Few-token product (2 <= n_tok <= 8) on the matrix cores for the formats
+// with 32-element blocks over a 4-bit code plane (Q4_0, Q4_K, Q4_1, Q5_0,
+// Q5_1, Q5_K, MXFP4), with the activations converted once per workgroup.
 //
 // Y[t][r] = sum_k value(W, r*K + k) * X[t][k]: the decode product of Sec. 2.1
 // for a small batch of tokens. The weights are read from HBM exactly once and
@@ -32,14 +33,17 @@
 // weight loads in flight.
 //
 // Precision (the reading shared by the matrix-core paths): the codes enter as
-// the exact bf16 of 128 + q; X = high + low to 16 significant bits; per block
+// the exact bf16 of 128 + q (the 5-bit formats: the fifth bit merged into q
+// first); X = high + low to 16 significant bits; per block
 // y += c1 * (P + k * S) + dm * (k * S)-term, with S the block sum of the
 // multiplied operand, computed by the same MFMA against a B of the constant k
 // and used as P's accumulator:
 //   Q4_0:     w = d (q - 8)         -> c1 = d,    k = -136, dm = 0
-//   Q4_K:     w = d sc q - dmin m   -> c1 = d sc, k = -128, dm = dmin m / 128
-//   Q4_1:     w = d q + m           -> c1 = d,    k = -128, dm = -m / 128
-// Accumulation is f32 throughout.
+//   Q5_0:     w = d (q - 16)        -> c1 = d,    k = -144, dm = 0
+//   Q4_K, Q5_K: w = d sc q - dmin m -> c1 = d sc, k = -128, dm = dmin m / 128
+//   Q4_1, Q5_1: w = d q + m         -> c1 = d,    k = -128, dm = -m / 128
+// MXFP4 multiplies the exact bf16 of its e2m1 values (no offset, no k * S):
+// y += 2^(E - 127) * P. Accumulation is f32 throughout.
 #include "lw_internal.hpp"
 #include "lw_mfma.hpp"
 
@@ -55,6 +59,8 @@ constexpr int kFtWinSB = 16;     // super-blocks per window: 16 x 8 blocks x 1 K
 constexpr int kFtMaxTpw = 4;     // tiles per wave when the waves do not split K
 template <int FMT>
 constexpr int kFtRing = FMT == LW_Q4_0 ? 3 : 2;  // units in flight per wave (fewer where the scales take more registers)
+template <int FMT>
+constexpr bool kFtQ5 = FMT == LW_Q5_0 || FMT == LW_Q5_1 || FMT == LW_Q5_K;
 
 // Scale data of one super-block (8 blocks, 256 columns) of one weight row.
 template <int FMT>
@@ -121,12 +127,59 @@ struct SbScale<LW_Q4_K> {
     }
 };
 
+// The 5-bit formats read Q4_0's, Q4_1's and Q4_K's scale data from their own
+// planes (the kernel passes those planes).
+template <>
+struct SbScale<LW_Q5_0> : SbScale<LW_Q4_0> {};
+template <>
+struct SbScale<LW_Q5_1> : SbScale<LW_Q4_1> {};
+template <>
+struct SbScale<LW_Q5_K> : SbScale<LW_Q4_K> {};
+
+template <>
+struct SbScale<LW_MXFP4> {
+    uint32_t e[2];  // the e8m0 exponent bytes of the 8 blocks
+    __device__ void load(const uint8_t* P1, const uint8_t*, uint64_t sbi) {
+        const uint2 v = *reinterpret_cast<const uint2*>(P1 + 8 * sbi);
+        e[0] = v.x;
+        e[1] = v.y;
+    }
+    // c1 = 2^(E - 127) of blocks 4h .. 4h+3; dm is unused
+    __device__ void coef(int h, float* c1, float*) const {
+        const uint32_t w = h ? e[1] : e[0];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) c1[i] = e8m0_to_float((w >> (8 * i)) & 0xFFu);
+    }
+};
+
 template <int FMT>
 struct Unit {
-    u32x4 c[2];  // code lines: block 8s + 4h + g of the lane's row, h = 0, 1
+    u32x4 c[2];   // code lines: block 8s + 4h + g of the lane's row, h = 0, 1
+    u32x4 qh[2];  // the 5-bit formats: fifth bits of blocks 8s + 4h .. 8s + 4h + 3 (one word each)
     SbScale<FMT> sc;
     int i, s;  // tile (of the wave), super-block
 };
+
+// Code word w of a block (lane group g: elements 4g .. 4g+3 in the low
+// nibbles, 16 + 4g .. 16 + 4g + 3 in the high ones) with its fifth bits from
+// the block's bit word qw (bit e for element e) -> the 8 bf16 values 128 + q.
+__device__ __forceinline__ bf16x8 biased_codes5(uint32_t w, uint32_t qw, uint32_t g4) {
+    const uint32_t lo = opaque((w & 0x0F0F0F0Fu) | spread4((qw >> g4) << 4 & 0xF0u));
+    const uint32_t hi = opaque(((w >> 4) & 0x0F0F0F0Fu) | spread4((qw >> (16u + g4)) << 4 & 0xF0u));
+    const uint32_t k43 = 0x43434343u;
+    const u32x4 v = {__builtin_amdgcn_perm(k43, lo, 0x04010400u), __builtin_amdgcn_perm(k43, lo, 0x04030402u),
+                     __builtin_amdgcn_perm(k43, hi, 0x04010400u), __builtin_amdgcn_perm(k43, hi, 0x04030402u)};
+    return __builtin_bit_cast(bf16x8, v);
+}
+
+// Code word w of an MXFP4 block -> the bf16 values of its 8 e2m1 codes, in
+// the same element order.
+__device__ __forceinline__ bf16x8 fp4_codes(uint32_t w) {
+    uint32_t p[4];
+    fp4_pairs(opaque(w & 0x07070707u), (w << 4) & 0x80808080u, &p[0], &p[1]);
+    fp4_pairs(opaque((w >> 4) & 0x07070707u), w & 0x80808080u, &p[2], &p[3]);
+    return __builtin_bit_cast(bf16x8, (u32x4{p[0], p[1], p[2], p[3]}));
+}
 
 // LDS-only barrier: waits for this wave's LDS traffic, not for its global
 // loads (the weight units in flight stay in flight).
@@ -162,8 +215,12 @@ __global__ void __launch_bounds__(64 * kFtMaxWaves)
     const int nwin = (nsb + ws - 1) / ws;
     const int64_t r0 = wgi * rpw;
     const int64_t rl = (r0 + rpw < (int64_t)M ? r0 + rpw : (int64_t)M) - 1;  // last row of the workgroup
-    const uint8_t* P1 = W + sg.off1[si];
-    const uint8_t* P2 = W + sg.off2[si];
+    // scale planes (the 5-bit formats: planes 2 and 3; plane 1 holds the fifth bits)
+    constexpr bool kQ5 = kFtQ5<FMT>;
+    constexpr bool kFp4 = FMT == LW_MXFP4;
+    const uint8_t* PH = W + sg.off1[si];
+    const uint8_t* P1 = W + (kQ5 ? sg.off2[si] : sg.off1[si]);
+    const uint8_t* P2 = W + (kQ5 ? sg.off3[si] : sg.off2[si]);
     const uint64_t rowb = (uint64_t)K / 2u;  // code bytes per row
 
     // the wave's tiles: the lane's row in each (past the workgroup's last row:
@@ -203,6 +260,11 @@ __global__ void __launch_bounds__(64 * kFtMaxWaves)
         const uint8_t* cp = W + r * rowb + 128u * (uint32_t)sb + 16u * (uint32_t)g;
         st.c[0] = *reinterpret_cast<const u32x4*>(cp);
         st.c[1] = *reinterpret_cast<const u32x4*>(cp + 64);
+        if constexpr (kQ5) {
+            const uint8_t* hq = PH + r * ((uint64_t)K / 8u) + 32u * (uint32_t)sb;
+            st.qh[0] = *reinterpret_cast<const u32x4*>(hq);
+            st.qh[1] = *reinterpret_cast<const u32x4*>(hq + 16);
+        }
         st.sc.load(P1, P2, r * (uint64_t)nsb + (uint64_t)sb);
         st.i = i;
         st.s = sb;
@@ -219,7 +281,7 @@ __global__ void __launch_bounds__(64 * kFtMaxWaves)
     // kXb items per thread before it converts any. The division by n_tok
     // (<= 8) is a multiplication by ceil(2^20 / n_tok), exact for the item
     // counts here (below 2^13 per window).
-    constexpr int kXb = TPW >= 4 ? 2 : 4;
+    constexpr int kXb = (TPW >= 4 || kQ5) ? 2 : 4;  // the 5-bit formats hold more per unit
     const uint32_t tmag = ((1u << 20) + (uint32_t)ntok - 1u) / (uint32_t)ntok;
     auto win_items = [&](int win) __attribute__((always_inline)) {
         const int w0 = win * ws;
@@ -284,8 +346,10 @@ __global__ void __launch_bounds__(64 * kFtMaxWaves)
         }
     };
 
-    // bf16 k: -136 (Q4_0: code bias 128 plus the format's offset 8) or -128
-    const uint32_t kb = FMT == LW_Q4_0 ? 0xC308C308u : 0xC300C300u;
+    // bf16 k: -136 (Q4_0: code bias 128 plus the format's offset 8), -144
+    // (Q5_0: offset 16) or -128
+    const uint32_t kb = FMT == LW_Q4_0 ? 0xC308C308u : FMT == LW_Q5_0 ? 0xC310C310u : 0xC300C300u;
+    const uint32_t g4 = 4u * (uint32_t)g;  // the lane group's first bit in a fifth-bit word
     const bf16x8 bias_b = __builtin_bit_cast(bf16x8, u32x4{kb, kb, kb, kb});
     // the lane's A slot within a block: g * 16 + ((n + 4g) & 15)
     const int aoff = g * 16 + ((n + 4 * g) & 15);
@@ -309,10 +373,20 @@ __global__ void __launch_bounds__(64 * kFtMaxWaves)
             for (int j = 0; j < 4; ++j) a[j] = __builtin_bit_cast(bf16x8, lds[(b0 + 4 * h + j) * 64 + aoff]);
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-                C[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[j], bias_b, f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                C[j] = kFp4 ? f32x4{0.f, 0.f, 0.f, 0.f}
+                            : __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[j], bias_b, f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
             const u32x4 wq = quad_transpose(u.c[h]);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) Pm[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[j], biased_codes(wq[j]), C[j], 0, 0, 0);
+            for (int j = 0; j < 4; ++j) {
+                bf16x8 cb;
+                if constexpr (kQ5)
+                    cb = biased_codes5(wq[j], u.qh[h][j], g4);
+                else if constexpr (kFp4)
+                    cb = fp4_codes(wq[j]);
+                else
+                    cb = biased_codes(wq[j]);
+                Pm[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[j], cb, C[j], 0, 0, 0);
+            }
             float c1[4], dm[4];
             u.sc.coef(h, c1, dm);
 #pragma unroll
@@ -320,7 +394,7 @@ __global__ void __launch_bounds__(64 * kFtMaxWaves)
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
                     float o = __builtin_fmaf(c1[j], Pm[j][v], t[v]);
-                    if constexpr (FMT != LW_Q4_0) o = __builtin_fmaf(dm[j], C[j][v], o);
+                    if constexpr (FMT != LW_Q4_0 && FMT != LW_Q5_0 && !kFp4) o = __builtin_fmaf(dm[j], C[j][v], o);
                     t[v] = o;
                 }
         }
@@ -462,18 +536,23 @@ hipError_t launch_f(const RowSegs<NS>& sg, const float* x, int64_t M, int64_t K,
     // takes a few tiles per workgroup to amortize: it is taken from two tiles
     // per workgroup with K >= 4096 (Q4_K-style: any K) and for very tall
     // matrices (more tiles than waves); other shapes go to the other kernel.
-    const bool take = ntq > kFtMaxWaves || (ntq >= 2 && (K >= 4096 || FMT == LW_Q4_K));
+    // The formats without that other kernel (the 5-bit ones, MXFP4) take this
+    // one for every shape, a single tile with K split over up to 16 waves.
+    constexpr bool only = kFtQ5<FMT> || FMT == LW_MXFP4;
+    const bool take = only || ntq > kFtMaxWaves || (ntq >= 2 && (K >= 4096 || FMT == LW_Q4_K));
     if (!take) return hipErrorNotSupported;
     int nw, P, tpw;
+    // tiles per wave at most (the 5-bit formats, which hold more per unit: 2)
+    constexpr int max_tpw = kFtQ5<FMT> ? 2 : kFtMaxTpw;
     if (ntq > kFtMaxWaves) {
         // more tiles than waves: each wave owns whole tiles
         nw = kFtMaxWaves;
         P = 1;
         tpw = (ntq + nw - 1) / nw;
-        if (tpw > kFtMaxTpw) {
-            rpw = 16 * kFtMaxWaves * kFtMaxTpw;
-            ntq = kFtMaxWaves * kFtMaxTpw;
-            tpw = kFtMaxTpw;
+        if (tpw > max_tpw) {
+            rpw = 16 * kFtMaxWaves * max_tpw;
+            ntq = kFtMaxWaves * max_tpw;
+            tpw = max_tpw;
         }
     } else {
         // waves split K: P parts per tile, preferring a P that divides the
@@ -496,7 +575,11 @@ hipError_t launch_f(const RowSegs<NS>& sg, const float* x, int64_t M, int64_t K,
     switch (tp) {
     case 1: return launch_tpw<FMT, 1, NS>(sg, x, K, n_tok, nw, (int)rpw, ntq, P, ws, lds, stream);
     case 2: return launch_tpw<FMT, 2, NS>(sg, x, K, n_tok, nw, (int)rpw, ntq, P, ws, lds, stream);
-    default: return launch_tpw<FMT, 4, NS>(sg, x, K, n_tok, nw, (int)rpw, ntq, P, ws, lds, stream);
+    default:
+        if constexpr (max_tpw < 4)
+            return hipErrorNotSupported;  // not reached: tpw <= max_tpw
+        else
+            return launch_tpw<FMT, 4, NS>(sg, x, K, n_tok, nw, (int)rpw, ntq, P, ws, lds, stream);
     }
 }
 
@@ -508,6 +591,7 @@ hipError_t launch_one(const uint8_t* W, const float* x, float* y, int64_t M, int
     sg.y[0] = y;
     sg.off1[0] = p.off1;
     sg.off2[0] = p.off2;
+    sg.off3[0] = p.off3;
     sg.start[0] = 0;
     sg.M[0] = M;
     return launch_f<FMT, 1>(sg, x, M, K, n_tok, stream);
@@ -525,6 +609,7 @@ hipError_t launch_segs(int n, const uint8_t* const* W, float* const* y, const in
         sg.y[i] = used ? y[i] : y[0];
         sg.off1[i] = p.off1;
         sg.off2[i] = p.off2;
+        sg.off3[i] = p.off3;
         sg.start[i] = used ? tot : INT64_MAX;
         sg.M[i] = used ? M[i] : 0;
         if (used) tot += M[i];
@@ -547,6 +632,10 @@ hipError_t launch_fewtok(int fmt, const uint8_t* W, const float* x, float* y, in
     case LW_Q4_0: return launch_one<LW_Q4_0>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q4_K: return launch_one<LW_Q4_K>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q4_1: return launch_one<LW_Q4_1>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q5_0: return launch_one<LW_Q5_0>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q5_1: return launch_one<LW_Q5_1>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q5_K: return launch_one<LW_Q5_K>(W, x, y, M, K, n_tok, p, stream);
+    case LW_MXFP4: return launch_one<LW_MXFP4>(W, x, y, M, K, n_tok, p, stream);
     default: return hipErrorNotSupported;
     }
 }
@@ -557,6 +646,10 @@ hipError_t launch_fewtok_multi(int fmt, int n, const uint8_t* const* W, float* c
     case LW_Q4_0: return launch_multi_ft<LW_Q4_0>(n, W, y, M, x, K, n_tok, stream);
     case LW_Q4_K: return launch_multi_ft<LW_Q4_K>(n, W, y, M, x, K, n_tok, stream);
     case LW_Q4_1: return launch_multi_ft<LW_Q4_1>(n, W, y, M, x, K, n_tok, stream);
+    case LW_Q5_0: return launch_multi_ft<LW_Q5_0>(n, W, y, M, x, K, n_tok, stream);
+    case LW_Q5_1: return launch_multi_ft<LW_Q5_1>(n, W, y, M, x, K, n_tok, stream);
+    case LW_Q5_K: return launch_multi_ft<LW_Q5_K>(n, W, y, M, x, K, n_tok, stream);
+    case LW_MXFP4: return launch_multi_ft<LW_MXFP4>(n, W, y, M, x, K, n_tok, stream);
     default: return hipErrorNotSupported;
     }
 }

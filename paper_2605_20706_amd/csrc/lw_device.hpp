@@ -76,4 +76,23 @@ __device__ __forceinline__ float e8m0_to_float(uint32_t E) {
 // in the binary16 subnormals).
 __device__ __forceinline__ uint32_t e2m1_half_bits(uint32_t c) { return ((c & 7u) << 9) | ((c & 8u) << 12); }
 
+// Four bits at positions 4-7 of g moved to bit 4 of each byte (the fifth bit
+// of four 5-bit codes held one per byte): one multiply, whose four shifted
+// copies of g do not overlap.
+__device__ __forceinline__ uint32_t spread4(uint32_t g) { return (g * 0x00204081u) & 0x10101010u; }
+
+// Four e2m1 codes, one per byte (idx: the magnitude bits; sgn: the sign bits,
+// at bit 7 of each byte) -> their four bfloat16 values as two pairs (p0:
+// bytes 0, 1; p1: bytes 2, 3). Two 8-entry byte tables indexed by the
+// magnitude give the high bytes (00 3F 3F 3F 40 40 40 40) and the low bytes
+// (00 00 80 C0 00 40 80 C0) of 0, 0.5, 1, 1.5, 2, 3, 4, 6; the sign goes to
+// bit 7 of the high byte; two more byte permutations interleave low and high
+// bytes. Exact for every code.
+__device__ __forceinline__ void fp4_pairs(uint32_t idx, uint32_t sgn, uint32_t* p0, uint32_t* p1) {
+    const uint32_t hi = __builtin_amdgcn_perm(0x40404040u, 0x3F3F3F00u, idx) | sgn;
+    const uint32_t lo = __builtin_amdgcn_perm(0xC0804000u, 0xC0800000u, idx);
+    *p0 = __builtin_amdgcn_perm(hi, lo, 0x05010400u);
+    *p1 = __builtin_amdgcn_perm(hi, lo, 0x07030602u);
+}
+
 }  // namespace lw

@@ -755,11 +755,9 @@ __device__ __forceinline__ void decode8(uint32_t w0, uint32_t w1, bf16x8* s0, bf
 }
 
 // The 5-bit formats: as decode8, with the fifth bits of the 16 elements
-// merged in first. hb holds them in element order: bits 0-7 for elements
-// 8h .. 8h+7 (K-step 0), bits 8-15 for 16 + 8h .. 16 + 8h + 7 (K-step 1).
-// spread4() moves the four bits at positions 4-7 of its argument to bit 4 of
-// each byte (one multiply: the four shifted copies do not overlap).
-__device__ __forceinline__ uint32_t spread4(uint32_t g) { return (g * 0x00204081u) & 0x10101010u; }
+// merged in first (spread4). hb holds them in element order: bits 0-7 for
+// elements 8h .. 8h+7 (K-step 0), bits 8-15 for 16 + 8h .. 16 + 8h + 7
+// (K-step 1).
 __device__ __forceinline__ void decode8_q5(uint32_t w0, uint32_t w1, uint32_t hb, bf16x8* s0, bf16x8* s1) {
     const uint32_t k43 = 0x43434343u;
     const uint32_t l0 = opaque((w0 & 0x0F0F0F0Fu) | spread4((hb << 4) & 0xF0u));
@@ -815,17 +813,7 @@ __device__ __forceinline__ void decode8_q2(uint32_t hw, bf16x8* s0, bf16x8* s1) 
     *s1 = __builtin_bit_cast(bf16x8, b);
 }
 
-// MXFP4: the bfloat16 of an e2m1 code from two 8-entry byte tables indexed
-// by its magnitude bits (high bytes 00 3F 3F 3F 40 40 40 40 and low bytes
-// 00 00 80 C0 00 40 80 C0: 0, 0.5, 1, 1.5, 2, 3, 4, 6), its sign bit moved
-// to bit 7 of the high byte; two more byte permutations interleave the low
-// and high bytes into bfloat16 pairs. Exact for every code.
-__device__ __forceinline__ void fp4_pairs(uint32_t idx, uint32_t sgn, uint32_t* p0, uint32_t* p1) {
-    const uint32_t hi = __builtin_amdgcn_perm(0x40404040u, 0x3F3F3F00u, idx) | sgn;
-    const uint32_t lo = __builtin_amdgcn_perm(0xC0804000u, 0xC0800000u, idx);
-    *p0 = __builtin_amdgcn_perm(hi, lo, 0x05010400u);
-    *p1 = __builtin_amdgcn_perm(hi, lo, 0x07030602u);
-}
+// MXFP4: both K-steps through fp4_pairs (lw_device.hpp).
 __device__ __forceinline__ void decode8_fp4(uint32_t w0, uint32_t w1, bf16x8* s0, bf16x8* s1) {
     uint32_t a[4], b[4];
     fp4_pairs(opaque(w0 & 0x07070707u), (w0 << 4) & 0x80808080u, &a[0], &a[1]);

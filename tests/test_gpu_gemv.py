@@ -55,13 +55,14 @@ def test_parity_many_rows(oracle_mod, fmt):
         gate.check(y, ref.y[:nt], ref.A[:nt], ref.F(kern, nt), f32_bound=1e-4, what=(fmt, M, K, nt, kern))
 
 
-@pytest.mark.parametrize("fmt", [Q4_0, Q4_K, Q4_1])
+@pytest.mark.parametrize("fmt", [Q4_0, Q4_K, Q4_1, Q5_0, Q5_1, Q5_K, MXFP4])
 @pytest.mark.parametrize("M,K", [(70000, 512), (300000, 256), (8200, 14336)])
 def test_parity_few_tokens_tiles(oracle_mod, fmt, M, K):
     """Few-token matrix-core kernel with the activations in LDS: more 16-row
     tiles per workgroup than waves (two and four tiles per wave, a ragged last
-    workgroup), and three tiles per workgroup with a long K that takes four
-    activation windows (the last one partial), each split over four waves."""
+    workgroup; the 5-bit formats at most two, their row groups capped), and
+    three tiles per workgroup with a long K that takes four activation
+    windows (the last one partial), each split over four waves."""
     W = synth.gen_packed(fmt, M * K, np.random.default_rng([fmt, M, K, 21]))
     Wg = to_gpu(W)
     x = synth.gen_x_seeded([22, fmt, M, K], K, 8)
