@@ -1,6 +1,6 @@
-// Few-token product (2 <= n_tok <= 8) on the matrix cores for the formats
-// with 32-element blocks over a 4-bit code plane (Q4_0, Q4_K, Q4_1, Q5_0,
-// Q5_1, Q5_K, MXFP4), with the activations converted once per workgroup.
+// Few-token product (2 <= n_tok <= 8) on the matrix cores for every quantized
+// format but Q8_0 and q1_0, with the activations converted once per
+// workgroup.
 //
 // Y[t][r] = sum_k value(W, r*K + k) * X[t][k]: the decode product of Sec. 2.1
 // for a small batch of tokens. The weights are read from HBM exactly once and
@@ -43,7 +43,13 @@
 //   Q4_K, Q5_K: w = d sc q - dmin m -> c1 = d sc, k = -128, dm = dmin m / 128
 //   Q4_1, Q5_1: w = d q + m         -> c1 = d,    k = -128, dm = -m / 128
 // MXFP4 multiplies the exact bf16 of its e2m1 values (no offset, no k * S):
-// y += 2^(E - 127) * P. Accumulation is f32 throughout.
+// y += 2^(E - 127) * P. Q6_K and Q2_K scale 16-element sub-blocks: a block
+// is two v_mfma_f32_16x16x16_bf16 (the low and the high half of each lane's
+// 8 operand values, elements 0..15 and 16..31 of the block), each with its
+// own coefficients:
+//   Q6_K:     w = d sc (q - 32)     -> c1 = d sc, k = -160, dm = 0
+//   Q2_K:     w = d sc q - dmin m   -> c1 = d sc, k = -128, dm = dmin m / 128
+// Accumulation is f32 throughout.
 #include "lw_internal.hpp"
 #include "lw_mfma.hpp"
 
@@ -54,6 +60,9 @@ struct Name_fewtok_kernel {
     static constexpr const char* base = "fewtok_kernel";
 };
 
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
 constexpr int kFtMaxWaves = 16;  // waves per workgroup
 constexpr int kFtWinSB = 16;     // super-blocks per window: 16 x 8 blocks x 1 KiB of A = 128 KiB of LDS
 constexpr int kFtMaxTpw = 4;     // tiles per wave when the waves do not split K
@@ -61,6 +70,8 @@ template <int FMT>
 constexpr int kFtRing = FMT == LW_Q4_0 ? 3 : 2;  // units in flight per wave (fewer where the scales take more registers)
 template <int FMT>
 constexpr bool kFtQ5 = FMT == LW_Q5_0 || FMT == LW_Q5_1 || FMT == LW_Q5_K;
+template <int FMT>
+constexpr bool kFtSub16 = FMT == LW_Q6_K || FMT == LW_Q2_K;
 
 // Scale data of one super-block (8 blocks, 256 columns) of one weight row.
 template <int FMT>
@@ -152,10 +163,51 @@ struct SbScale<LW_MXFP4> {
     }
 };
 
+// 16-element sub-blocks: the 16 coefficient units of a super-block, read at
+// once (16 bytes of scales, then d or {d, dmin}).
+template <>
+struct SbScale<LW_Q6_K> {
+    u32x4 sc;     // signed 8-bit sub-block scales
+    uint32_t d;   // binary16 d
+    __device__ void load(const uint8_t* P1, const uint8_t* P2, uint64_t sbi) {
+        sc = *reinterpret_cast<const u32x4*>(P1 + 16 * sbi);
+        d = *reinterpret_cast<const uint16_t*>(P2 + 2 * sbi);
+    }
+    // c1 = d * sc of sub-blocks 8h .. 8h+7; dm is unused
+    __device__ void coef16(int h, float* c1, float*) const {
+        const float dv = half_bits_to_float(d);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const uint32_t w = sc[2 * h + (i >> 2)];
+            c1[i] = dv * (float)(int)(int8_t)(uint8_t)(w >> (8 * (i & 3)));
+        }
+    }
+};
+template <>
+struct SbScale<LW_Q2_K> {
+    u32x4 scm;    // {scale, min} nibbles of the sub-blocks
+    uint32_t dd;  // {binary16 d, binary16 dmin}
+    __device__ void load(const uint8_t* P1, const uint8_t* P2, uint64_t sbi) {
+        scm = *reinterpret_cast<const u32x4*>(P1 + 16 * sbi);
+        dd = *reinterpret_cast<const uint32_t*>(P2 + 4 * sbi);
+    }
+    // c1 = d * sc and dm = dmin * m / 128 of sub-blocks 8h .. 8h+7
+    __device__ void coef16(int h, float* c1, float* dm) const {
+        const float dv = half_bits_to_float(dd & 0xFFFFu), mv = half_bits_to_float(dd >> 16) * (1.0f / 128.0f);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const uint32_t b = (scm[2 * h + (i >> 2)] >> (8 * (i & 3))) & 0xFFu;
+            c1[i] = dv * (float)(b & 15u);
+            dm[i] = mv * (float)(b >> 4);
+        }
+    }
+};
+
 template <int FMT>
 struct Unit {
     u32x4 c[2];   // code lines: block 8s + 4h + g of the lane's row, h = 0, 1
     u32x4 qh[2];  // the 5-bit formats: fifth bits of blocks 8s + 4h .. 8s + 4h + 3 (one word each)
+    u32x4 two;    // Q6_K high bits, Q2_K codes: blocks 8s + 2g, 8s + 2g + 1 (8 bytes each)
     SbScale<FMT> sc;
     int i, s;  // tile (of the wave), super-block
 };
@@ -170,6 +222,42 @@ __device__ __forceinline__ bf16x8 biased_codes5(uint32_t w, uint32_t qw, uint32_
     const u32x4 v = {__builtin_amdgcn_perm(k43, lo, 0x04010400u), __builtin_amdgcn_perm(k43, lo, 0x04030402u),
                      __builtin_amdgcn_perm(k43, hi, 0x04010400u), __builtin_amdgcn_perm(k43, hi, 0x04030402u)};
     return __builtin_bit_cast(bf16x8, v);
+}
+
+// Q6_K: code word w and the 16 bits hw of the two high bits of its elements
+// (bits 0-7: elements 4g .. 4g+3; bits 8-15: 16 + 4g .. 16 + 4g + 3) -> the
+// 8 bf16 values 128 + q. Q2_K: the 2-bit codes alone.
+__device__ __forceinline__ bf16x8 biased_codes6(uint32_t w, uint32_t hw) {
+    const uint32_t lo = opaque((w & 0x0F0F0F0Fu) | spread2_hi(hw & 0xFFu));
+    const uint32_t hi = opaque(((w >> 4) & 0x0F0F0F0Fu) | spread2_hi((hw >> 8) & 0xFFu));
+    const uint32_t k43 = 0x43434343u;
+    const u32x4 v = {__builtin_amdgcn_perm(k43, lo, 0x04010400u), __builtin_amdgcn_perm(k43, lo, 0x04030402u),
+                     __builtin_amdgcn_perm(k43, hi, 0x04010400u), __builtin_amdgcn_perm(k43, hi, 0x04030402u)};
+    return __builtin_bit_cast(bf16x8, v);
+}
+__device__ __forceinline__ bf16x8 biased_codes2(uint32_t hw) {
+    const uint32_t lo = opaque(spread2_lo(hw & 0xFFu));
+    const uint32_t hi = opaque(spread2_lo((hw >> 8) & 0xFFu));
+    const uint32_t k43 = 0x43434343u;
+    const u32x4 v = {__builtin_amdgcn_perm(k43, lo, 0x04010400u), __builtin_amdgcn_perm(k43, lo, 0x04030402u),
+                     __builtin_amdgcn_perm(k43, hi, 0x04010400u), __builtin_amdgcn_perm(k43, hi, 0x04030402u)};
+    return __builtin_bit_cast(bf16x8, v);
+}
+
+// The 2-bit plane of a super-block (lane group L holds the 8-byte records
+// of blocks 2L, 2L + 1 as words s0..s3) -> for lane group g the word R_L,
+// L = 0..3, holding byte g of each of s0..s3 of lane group L: bytes 0, 1 are
+// the two bytes of block 2L its elements need, bytes 2, 3 those of block
+// 2L + 1. A byte transpose within the lane (P_d = byte d of s0..s3), then the
+// word transpose across the lane groups.
+__device__ __forceinline__ u32x4 two_bit_transpose(u32x4 s) {
+    const uint32_t t01l = __builtin_amdgcn_perm(s[1], s[0], 0x05010400u);  // s0[0] s1[0] s0[1] s1[1]
+    const uint32_t t01h = __builtin_amdgcn_perm(s[1], s[0], 0x07030602u);  // s0[2] s1[2] s0[3] s1[3]
+    const uint32_t t23l = __builtin_amdgcn_perm(s[3], s[2], 0x05010400u);
+    const uint32_t t23h = __builtin_amdgcn_perm(s[3], s[2], 0x07030602u);
+    const u32x4 p = {__builtin_amdgcn_perm(t23l, t01l, 0x05040100u), __builtin_amdgcn_perm(t23l, t01l, 0x07060302u),
+                     __builtin_amdgcn_perm(t23h, t01h, 0x05040100u), __builtin_amdgcn_perm(t23h, t01h, 0x07060302u)};
+    return quad_transpose(p);
 }
 
 // Code word w of an MXFP4 block -> the bf16 values of its 8 e2m1 codes, in
@@ -216,11 +304,16 @@ __global__ void __launch_bounds__(64 * kFtMaxWaves)
     const int64_t r0 = wgi * rpw;
     const int64_t rl = (r0 + rpw < (int64_t)M ? r0 + rpw : (int64_t)M) - 1;  // last row of the workgroup
     // scale planes (the 5-bit formats: planes 2 and 3; plane 1 holds the fifth bits)
+    // (Q6_K: plane 1 holds the high bits, planes 2 and 3 the scales; Q2_K:
+    // plane 0 holds its 2-bit codes, planes 1 and 2 the scales)
     constexpr bool kQ5 = kFtQ5<FMT>;
     constexpr bool kFp4 = FMT == LW_MXFP4;
-    const uint8_t* PH = W + sg.off1[si];
-    const uint8_t* P1 = W + (kQ5 ? sg.off2[si] : sg.off1[si]);
-    const uint8_t* P2 = W + (kQ5 ? sg.off3[si] : sg.off2[si]);
+    constexpr bool kSub16 = kFtSub16<FMT>;
+    constexpr bool kQ2 = FMT == LW_Q2_K;
+    const bool hi_planes = kQ5 || FMT == LW_Q6_K;
+    const uint8_t* PH = W + (kQ2 ? 0 : sg.off1[si]);
+    const uint8_t* P1 = W + (hi_planes ? sg.off2[si] : sg.off1[si]);
+    const uint8_t* P2 = W + (hi_planes ? sg.off3[si] : sg.off2[si]);
     const uint64_t rowb = (uint64_t)K / 2u;  // code bytes per row
 
     // the wave's tiles: the lane's row in each (past the workgroup's last row:
@@ -257,9 +350,13 @@ __global__ void __launch_bounds__(64 * kFtMaxWaves)
             sb = wa + (ue - i * wlen);
         }
         const uint64_t r = row_of(i);
-        const uint8_t* cp = W + r * rowb + 128u * (uint32_t)sb + 16u * (uint32_t)g;
-        st.c[0] = *reinterpret_cast<const u32x4*>(cp);
-        st.c[1] = *reinterpret_cast<const u32x4*>(cp + 64);
+        if constexpr (!kQ2) {
+            const uint8_t* cp = W + r * rowb + 128u * (uint32_t)sb + 16u * (uint32_t)g;
+            st.c[0] = *reinterpret_cast<const u32x4*>(cp);
+            st.c[1] = *reinterpret_cast<const u32x4*>(cp + 64);
+        }
+        if constexpr (kSub16)
+            st.two = *reinterpret_cast<const u32x4*>(PH + r * ((uint64_t)K / 4u) + 64u * (uint32_t)sb + 16u * (uint32_t)g);
         if constexpr (kQ5) {
             const uint8_t* hq = PH + r * ((uint64_t)K / 8u) + 32u * (uint32_t)sb;
             st.qh[0] = *reinterpret_cast<const u32x4*>(hq);
@@ -348,7 +445,12 @@ __global__ void __launch_bounds__(64 * kFtMaxWaves)
 
     // bf16 k: -136 (Q4_0: code bias 128 plus the format's offset 8), -144
     // (Q5_0: offset 16) or -128
-    const uint32_t kb = FMT == LW_Q4_0 ? 0xC308C308u : FMT == LW_Q5_0 ? 0xC310C310u : 0xC300C300u;
+    // (Q6_K: offset 32, -160)
+    const uint32_t kb = FMT == LW_Q4_0   ? 0xC308C308u
+                        : FMT == LW_Q5_0 ? 0xC310C310u
+                        : FMT == LW_Q6_K ? 0xC320C320u
+                                         : 0xC300C300u;
+    const bf16x4 bias_b4 = __builtin_bit_cast(bf16x4, (u32x2{kb, kb}));
     const uint32_t g4 = 4u * (uint32_t)g;  // the lane group's first bit in a fifth-bit word
     const bf16x8 bias_b = __builtin_bit_cast(bf16x8, u32x4{kb, kb, kb, kb});
     // the lane's A slot within a block: g * 16 + ((n + 4g) & 15)
@@ -362,6 +464,39 @@ __global__ void __launch_bounds__(64 * kFtMaxWaves)
     auto consume = [&](const Unit<FMT>& u) __attribute__((always_inline)) {
         const int b0 = 8 * (u.s - cur * ws);  // window block of the super-block's first block
         f32x4 t = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (kSub16) {
+            const u32x4 R = two_bit_transpose(u.two);
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                // four blocks, each two sub-blocks: K-steps of 16 over the low
+                // and the high half of the lane's operand values
+                u32x4 wq = {0u, 0u, 0u, 0u};
+                if constexpr (!kQ2) wq = quad_transpose(u.c[h]);
+                float c1[8], dm[8];
+                u.sc.coef16(h, c1, dm);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int jb = 4 * h + j;
+                    const uint32_t hw = (R[jb >> 1] >> (16 * (jb & 1))) & 0xFFFFu;
+                    const u32x4 av = __builtin_bit_cast(u32x4, lds[(b0 + jb) * 64 + aoff]);
+                    const u32x4 cv = __builtin_bit_cast(u32x4, kQ2 ? biased_codes2(hw) : biased_codes6(wq[j], hw));
+#pragma unroll
+                    for (int sh = 0; sh < 2; ++sh) {
+                        const bf16x4 a4 = __builtin_bit_cast(bf16x4, (u32x2{av[2 * sh], av[2 * sh + 1]}));
+                        const bf16x4 c4 = __builtin_bit_cast(bf16x4, (u32x2{cv[2 * sh], cv[2 * sh + 1]}));
+                        const f32x4 Cs =
+                            __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a4, bias_b4, f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                        const f32x4 Ps = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a4, c4, Cs, 0, 0, 0);
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) {
+                            float o = __builtin_fmaf(c1[2 * j + sh], Ps[v], t[v]);
+                            if constexpr (kQ2) o = __builtin_fmaf(dm[2 * j + sh], Cs[v], o);
+                            t[v] = o;
+                        }
+                    }
+                }
+            }
+        } else
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             // four blocks: A slices from LDS, the bias term k * S as an MFMA
@@ -536,9 +671,10 @@ hipError_t launch_f(const RowSegs<NS>& sg, const float* x, int64_t M, int64_t K,
     // takes a few tiles per workgroup to amortize: it is taken from two tiles
     // per workgroup with K >= 4096 (Q4_K-style: any K) and for very tall
     // matrices (more tiles than waves); other shapes go to the other kernel.
-    // The formats without that other kernel (the 5-bit ones, MXFP4) take this
+    // The formats without that other kernel (the 5-bit ones, Q6_K, Q2_K,
+    // MXFP4) take this
     // one for every shape, a single tile with K split over up to 16 waves.
-    constexpr bool only = kFtQ5<FMT> || FMT == LW_MXFP4;
+    constexpr bool only = kFtQ5<FMT> || kFtSub16<FMT> || FMT == LW_MXFP4;
     const bool take = only || ntq > kFtMaxWaves || (ntq >= 2 && (K >= 4096 || FMT == LW_Q4_K));
     if (!take) return hipErrorNotSupported;
     int nw, P, tpw;
@@ -636,6 +772,8 @@ hipError_t launch_fewtok(int fmt, const uint8_t* W, const float* x, float* y, in
     case LW_Q5_1: return launch_one<LW_Q5_1>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q5_K: return launch_one<LW_Q5_K>(W, x, y, M, K, n_tok, p, stream);
     case LW_MXFP4: return launch_one<LW_MXFP4>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q6_K: return launch_one<LW_Q6_K>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q2_K: return launch_one<LW_Q2_K>(W, x, y, M, K, n_tok, p, stream);
     default: return hipErrorNotSupported;
     }
 }
@@ -650,6 +788,8 @@ hipError_t launch_fewtok_multi(int fmt, int n, const uint8_t* const* W, float* c
     case LW_Q5_1: return launch_multi_ft<LW_Q5_1>(n, W, y, M, x, K, n_tok, stream);
     case LW_Q5_K: return launch_multi_ft<LW_Q5_K>(n, W, y, M, x, K, n_tok, stream);
     case LW_MXFP4: return launch_multi_ft<LW_MXFP4>(n, W, y, M, x, K, n_tok, stream);
+    case LW_Q6_K: return launch_multi_ft<LW_Q6_K>(n, W, y, M, x, K, n_tok, stream);
+    case LW_Q2_K: return launch_multi_ft<LW_Q2_K>(n, W, y, M, x, K, n_tok, stream);
     default: return hipErrorNotSupported;
     }
 }

@@ -81,6 +81,17 @@ __device__ __forceinline__ uint32_t e2m1_half_bits(uint32_t c) { return ((c & 7u
 // copies of g do not overlap.
 __device__ __forceinline__ uint32_t spread4(uint32_t g) { return (g * 0x00204081u) & 0x10101010u; }
 
+// Four 2-bit fields (bits 0-7 of g) to bits 4-5 (spread2_hi) or 0-1
+// (spread2_lo) of the four bytes: two shift-or-mask steps, no carries.
+__device__ __forceinline__ uint32_t spread2_hi(uint32_t g) {
+    const uint32_t u = ((g << 4) | (g << 16)) & 0x00F000F0u;  // fields 0, 1 at bits 4-7; 2, 3 at 20-23
+    return (u | (u << 6)) & 0x30303030u;
+}
+__device__ __forceinline__ uint32_t spread2_lo(uint32_t g) {
+    const uint32_t u = (g | (g << 12)) & 0x000F000Fu;  // fields 0, 1 at bits 0-3; 2, 3 at 16-19
+    return (u | (u << 6)) & 0x03030303u;
+}
+
 // Four e2m1 codes, one per byte (idx: the magnitude bits; sgn: the sign bits,
 // at bit 7 of each byte) -> their four bfloat16 values as two pairs (p0:
 // bytes 0, 1; p1: bytes 2, 3). Two 8-entry byte tables indexed by the

@@ -772,16 +772,6 @@ __device__ __forceinline__ void decode8_q5(uint32_t w0, uint32_t w1, uint32_t hb
     *s1 = __builtin_bit_cast(bf16x8, b);
 }
 
-// Four 2-bit fields (bits 0-7 of g) to bits 4-5 (spread2_hi) or 0-1
-// (spread2_lo) of the four bytes: two shift-or-mask steps, no carries.
-__device__ __forceinline__ uint32_t spread2_hi(uint32_t g) {
-    const uint32_t u = ((g << 4) | (g << 16)) & 0x00F000F0u;  // fields 0, 1 at bits 4-7; 2, 3 at 20-23
-    return (u | (u << 6)) & 0x30303030u;
-}
-__device__ __forceinline__ uint32_t spread2_lo(uint32_t g) {
-    const uint32_t u = (g | (g << 12)) & 0x000F000Fu;  // fields 0, 1 at bits 0-3; 2, 3 at 16-19
-    return (u | (u << 6)) & 0x03030303u;
-}
 // Q6_K: as decode8, with the two high bits of the 16 elements merged in. hw
 // holds them in element order, two bits each: bits 0-15 for elements 8h ..
 // 8h+7 (K-step 0), bits 16-31 for 16 + 8h .. 16 + 8h + 7 (K-step 1).

@@ -184,9 +184,9 @@ def test_kernel_selection_table(lib):
     activations in LDS for matrices with at least two 16-row tiles per
     workgroup (and K >= 4096 for Q4_0), else the pair-step matrix-core kernel;
     9..16 the few-token one with two MFMAs per block; more: the tiled
-    matrix-core kernel. The 5-bit formats and MXFP4 take the first
-    matrix-core kernel for 2..8 tokens at every shape; Q6_K and Q2_K the
-    VALU kernels up to 8 tokens; all of them the tiled kernel beyond."""
+    matrix-core kernel. The formats without the pair-step kernel
+    (Q5_0, Q5_1, Q5_K, Q6_K, Q2_K, MXFP4) take the first matrix-core kernel
+    for 2..8 tokens at every shape and the tiled kernel beyond."""
     from paper_2605_20706_amd import synth
 
     def kind(fmt, M, K, nt):
@@ -215,13 +215,11 @@ def test_kernel_selection_table(lib):
     assert kind(F16, 2048, 2048, 20) == "gemv_kernel"
     for fmt in (Q5_0, Q5_1, Q5_K, Q6_K, Q2_K, 11):            # one token: the LDS kernel
         assert kind(fmt, 14336, 4096, 1) == "gemv1_kernel"
-    for fmt in (Q5_0, Q5_1, Q5_K, 11):                        # 2..8 tokens: the few-token matrix-core kernel
+    for fmt in (Q5_0, Q5_1, Q5_K, Q6_K, Q2_K, 11):            # 2..8 tokens: the few-token matrix-core kernel
         for nt in (2, 4, 8):
             assert kind(fmt, 14336, 4096, nt) == "fewtok_kernel"
         assert kind(fmt, 100, 2304, 4) == "fewtok_kernel"     # one tile, K split over the waves
         assert kind(fmt, 4096, 14336, 8) == "fewtok_kernel"   # the 8B down projection
-    for fmt in (Q6_K, Q2_K):                                  # 16-element sub-blocks: VALU up to 8 tokens
-        assert kind(fmt, 14336, 4096, 4) == "gemv_kernel"
     for fmt in (Q5_0, Q5_1, Q5_K, Q6_K, Q2_K, 11):            # from 9 tokens: the tiled matrix cores
         assert kind(fmt, 14336, 4096, 12) == "gemm32_kernel"
         assert kind(fmt, 14336, 4096, 512) == "gemm32_kernel"
