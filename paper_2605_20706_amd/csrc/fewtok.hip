@@ -1,6 +1,5 @@
 // Few-token product (2 <= n_tok <= 8) on the matrix cores for every quantized
-// format but Q8_0 and q1_0, with the activations converted once per
-// workgroup.
+// format but Q8_0, with the activations converted once per workgroup.
 //
 // Y[t][r] = sum_k value(W, r*K + k) * X[t][k]: the decode product of Sec. 2.1
 // for a small batch of tokens. The weights are read from HBM exactly once and
@@ -46,7 +45,7 @@
 // y += 2^(E - 127) * P. Q6_K and Q2_K scale 16-element sub-blocks: a block
 // is two v_mfma_f32_16x16x16_bf16 (the low and the high half of each lane's
 // 8 operand values, elements 0..15 and 16..31 of the block), each with its
-// own coefficients:
+// own coefficients (q1_0: the bf16 +-1 of each bit, y += d * P):
 //   Q6_K:     w = d sc (q - 32)     -> c1 = d sc, k = -160, dm = 0
 //   Q2_K:     w = d sc q - dmin m   -> c1 = d sc, k = -128, dm = dmin m / 128
 // Accumulation is f32 throughout.
@@ -146,6 +145,20 @@ template <>
 struct SbScale<LW_Q5_1> : SbScale<LW_Q4_1> {};
 template <>
 struct SbScale<LW_Q5_K> : SbScale<LW_Q4_K> {};
+
+template <>
+struct SbScale<LW_Q1_0> {
+    uint32_t d2;  // the binary16 d of the super-block's two 128-element groups
+    __device__ void load(const uint8_t* P1, const uint8_t*, uint64_t sbi) {
+        d2 = *reinterpret_cast<const uint32_t*>(P1 + 4 * sbi);
+    }
+    // c1 = d of blocks 4h .. 4h+3 (all in group h); dm is unused
+    __device__ void coef(int h, float* c1, float*) const {
+        const float d = half_bits_to_float(h ? d2 >> 16 : d2 & 0xFFFFu);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) c1[i] = d;
+    }
+};
 
 template <>
 struct SbScale<LW_MXFP4> {
@@ -260,6 +273,15 @@ __device__ __forceinline__ u32x4 two_bit_transpose(u32x4 s) {
     return quad_transpose(p);
 }
 
+// q1_0: the block's code bits qw (bit e for element e) -> the bf16 +-1 of
+// the lane group's 8 elements, in the order above.
+__device__ __forceinline__ bf16x8 sign_codes(uint32_t qw, uint32_t g4) {
+    uint32_t p[4];
+    sign_pairs((qw >> g4) & 15u, &p[0], &p[1]);
+    sign_pairs((qw >> (16u + g4)) & 15u, &p[2], &p[3]);
+    return __builtin_bit_cast(bf16x8, (u32x4{p[0], p[1], p[2], p[3]}));
+}
+
 // Code word w of an MXFP4 block -> the bf16 values of its 8 e2m1 codes, in
 // the same element order.
 __device__ __forceinline__ bf16x8 fp4_codes(uint32_t w) {
@@ -310,8 +332,9 @@ __global__ void __launch_bounds__(64 * kFtMaxWaves)
     constexpr bool kFp4 = FMT == LW_MXFP4;
     constexpr bool kSub16 = kFtSub16<FMT>;
     constexpr bool kQ2 = FMT == LW_Q2_K;
+    constexpr bool kQ1 = FMT == LW_Q1_0;  // its code bits are read as the fifth-bit words
     const bool hi_planes = kQ5 || FMT == LW_Q6_K;
-    const uint8_t* PH = W + (kQ2 ? 0 : sg.off1[si]);
+    const uint8_t* PH = W + (kQ2 || kQ1 ? 0 : sg.off1[si]);
     const uint8_t* P1 = W + (hi_planes ? sg.off2[si] : sg.off1[si]);
     const uint8_t* P2 = W + (hi_planes ? sg.off3[si] : sg.off2[si]);
     const uint64_t rowb = (uint64_t)K / 2u;  // code bytes per row
@@ -350,14 +373,14 @@ __global__ void __launch_bounds__(64 * kFtMaxWaves)
             sb = wa + (ue - i * wlen);
         }
         const uint64_t r = row_of(i);
-        if constexpr (!kQ2) {
+        if constexpr (!kQ2 && !kQ1) {
             const uint8_t* cp = W + r * rowb + 128u * (uint32_t)sb + 16u * (uint32_t)g;
             st.c[0] = *reinterpret_cast<const u32x4*>(cp);
             st.c[1] = *reinterpret_cast<const u32x4*>(cp + 64);
         }
         if constexpr (kSub16)
             st.two = *reinterpret_cast<const u32x4*>(PH + r * ((uint64_t)K / 4u) + 64u * (uint32_t)sb + 16u * (uint32_t)g);
-        if constexpr (kQ5) {
+        if constexpr (kQ5 || kQ1) {
             const uint8_t* hq = PH + r * ((uint64_t)K / 8u) + 32u * (uint32_t)sb;
             st.qh[0] = *reinterpret_cast<const u32x4*>(hq);
             st.qh[1] = *reinterpret_cast<const u32x4*>(hq + 16);
@@ -508,13 +531,16 @@ __global__ void __launch_bounds__(64 * kFtMaxWaves)
             for (int j = 0; j < 4; ++j) a[j] = __builtin_bit_cast(bf16x8, lds[(b0 + 4 * h + j) * 64 + aoff]);
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-                C[j] = kFp4 ? f32x4{0.f, 0.f, 0.f, 0.f}
+                C[j] = kFp4 || kQ1 ? f32x4{0.f, 0.f, 0.f, 0.f}
                             : __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[j], bias_b, f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-            const u32x4 wq = quad_transpose(u.c[h]);
+            u32x4 wq = {0u, 0u, 0u, 0u};
+            if constexpr (!kQ1) wq = quad_transpose(u.c[h]);
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 bf16x8 cb;
-                if constexpr (kQ5)
+                if constexpr (kQ1)
+                    cb = sign_codes(u.qh[h][j], g4);
+                else if constexpr (kQ5)
                     cb = biased_codes5(wq[j], u.qh[h][j], g4);
                 else if constexpr (kFp4)
                     cb = fp4_codes(wq[j]);
@@ -529,7 +555,8 @@ __global__ void __launch_bounds__(64 * kFtMaxWaves)
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
                     float o = __builtin_fmaf(c1[j], Pm[j][v], t[v]);
-                    if constexpr (FMT != LW_Q4_0 && FMT != LW_Q5_0 && !kFp4) o = __builtin_fmaf(dm[j], C[j][v], o);
+                    if constexpr (FMT != LW_Q4_0 && FMT != LW_Q5_0 && !kFp4 && !kQ1)
+                        o = __builtin_fmaf(dm[j], C[j][v], o);
                     t[v] = o;
                 }
         }
@@ -672,9 +699,9 @@ hipError_t launch_f(const RowSegs<NS>& sg, const float* x, int64_t M, int64_t K,
     // per workgroup with K >= 4096 (Q4_K-style: any K) and for very tall
     // matrices (more tiles than waves); other shapes go to the other kernel.
     // The formats without that other kernel (the 5-bit ones, Q6_K, Q2_K,
-    // MXFP4) take this
+    // MXFP4, q1_0) take this
     // one for every shape, a single tile with K split over up to 16 waves.
-    constexpr bool only = kFtQ5<FMT> || kFtSub16<FMT> || FMT == LW_MXFP4;
+    constexpr bool only = kFtQ5<FMT> || kFtSub16<FMT> || FMT == LW_MXFP4 || FMT == LW_Q1_0;
     const bool take = only || ntq > kFtMaxWaves || (ntq >= 2 && (K >= 4096 || FMT == LW_Q4_K));
     if (!take) return hipErrorNotSupported;
     int nw, P, tpw;
@@ -774,6 +801,7 @@ hipError_t launch_fewtok(int fmt, const uint8_t* W, const float* x, float* y, in
     case LW_MXFP4: return launch_one<LW_MXFP4>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q6_K: return launch_one<LW_Q6_K>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q2_K: return launch_one<LW_Q2_K>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q1_0: return launch_one<LW_Q1_0>(W, x, y, M, K, n_tok, p, stream);
     default: return hipErrorNotSupported;
     }
 }
@@ -790,6 +818,7 @@ hipError_t launch_fewtok_multi(int fmt, int n, const uint8_t* const* W, float* c
     case LW_MXFP4: return launch_multi_ft<LW_MXFP4>(n, W, y, M, x, K, n_tok, stream);
     case LW_Q6_K: return launch_multi_ft<LW_Q6_K>(n, W, y, M, x, K, n_tok, stream);
     case LW_Q2_K: return launch_multi_ft<LW_Q2_K>(n, W, y, M, x, K, n_tok, stream);
+    case LW_Q1_0: return launch_multi_ft<LW_Q1_0>(n, W, y, M, x, K, n_tok, stream);
     default: return hipErrorNotSupported;
     }
 }

@@ -92,6 +92,17 @@ __device__ __forceinline__ uint32_t spread2_lo(uint32_t g) {
     return (u | (u << 6)) & 0x03030303u;
 }
 
+// Four 1-bit codes (bits 0-3 of b4: 1 for +1, 0 for -1) -> their bfloat16
+// values as two pairs (p0: codes 0, 1; p1: codes 2, 3). One multiply moves
+// bit i to bit 7 of byte i (the shifted copies do not overlap); those bits
+// clear the sign of the high bytes 0xBF; byte permutations pair the high
+// bytes with the low byte 0x80 of +-1.
+__device__ __forceinline__ void sign_pairs(uint32_t b4, uint32_t* p0, uint32_t* p1) {
+    const uint32_t hi = 0xBFBFBFBFu ^ (((b4 << 7) * 0x00204081u) & 0x80808080u);
+    *p0 = __builtin_amdgcn_perm(hi, 0x80808080u, 0x05010400u);
+    *p1 = __builtin_amdgcn_perm(hi, 0x80808080u, 0x07030602u);
+}
+
 // Four e2m1 codes, one per byte (idx: the magnitude bits; sgn: the sign bits,
 // at bit 7 of each byte) -> their four bfloat16 values as two pairs (p0:
 // bytes 0, 1; p1: bytes 2, 3). Two 8-entry byte tables indexed by the

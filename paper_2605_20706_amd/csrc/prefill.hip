@@ -242,6 +242,21 @@ struct MF<LW_Q2_K> {
         *c2 = -__builtin_fmaf(128.0f, ds, dm);
     }
 };
+// q1_0: w = +-d, the operand the exact bfloat16 +-1 of each bit; one d per
+// 128 elements (4 blocks); no offset term.
+template <>
+struct MF<LW_Q1_0> {
+    static constexpr bool kSums = false;
+    static constexpr int kRaw = 1;  // the two binary16 d of 8 blocks
+    __device__ static void load_scale8(const uint8_t* W, int64_t off1, int64_t, uint64_t row, uint32_t K, int blk0,
+                                       uint32_t* r) {
+        r[0] = *reinterpret_cast<const uint32_t*>(W + off1 + 2u * (row * (K / 128u) + (uint32_t)(blk0 >> 2)));
+    }
+    __device__ static void coef8(const uint32_t* r, int e, float* c1, float* c2) {
+        *c1 = half_bits_to_float((r[0] >> (16 * (e >> 2))) & 0xFFFFu);
+        *c2 = 0.f;
+    }
+};
 // MXFP4: the e2m1 values themselves are exact bfloat16 operands, so there is
 // no offset term: y += 2^(E - 127) * P, with the block's e8m0 exponent E.
 template <>
@@ -803,6 +818,17 @@ __device__ __forceinline__ void decode8_q2(uint32_t hw, bf16x8* s0, bf16x8* s1) 
     *s1 = __builtin_bit_cast(bf16x8, b);
 }
 
+// q1_0: the 16 bits hb (as decode8_q5's) as bfloat16 +-1.
+__device__ __forceinline__ void decode8_q1(uint32_t hb, bf16x8* s0, bf16x8* s1) {
+    uint32_t a[4], b[4];
+    sign_pairs(hb & 15u, &a[0], &a[1]);
+    sign_pairs((hb >> 4) & 15u, &a[2], &a[3]);
+    sign_pairs((hb >> 8) & 15u, &b[0], &b[1]);
+    sign_pairs((hb >> 12) & 15u, &b[2], &b[3]);
+    *s0 = __builtin_bit_cast(bf16x8, (u32x4v{a[0], a[1], a[2], a[3]}));
+    *s1 = __builtin_bit_cast(bf16x8, (u32x4v{b[0], b[1], b[2], b[3]}));
+}
+
 // MXFP4: both K-steps through fp4_pairs (lw_device.hpp).
 __device__ __forceinline__ void decode8_fp4(uint32_t w0, uint32_t w1, bf16x8* s0, bf16x8* s1) {
     uint32_t a[4], b[4];
@@ -826,10 +852,11 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
     constexpr bool kQ5 = FMT == LW_Q5_0 || FMT == LW_Q5_1 || FMT == LW_Q5_K;
     constexpr bool kFp4 = FMT == LW_MXFP4;
     constexpr bool kQ6 = FMT == LW_Q6_K, kQ2 = FMT == LW_Q2_K;
+    constexpr bool kQ1 = FMT == LW_Q1_0;  // its 1-bit plane is laid out as the fifth-bit planes
     constexpr bool kSub16 = kQ6 || kQ2;  // one coefficient pair per 16-element K-step
     // a window holds kWin coefficient units: blocks, or the sub-blocks of kWin / 2 blocks
     constexpr int KWB = kSub16 ? kWin / 2 : kWin;
-    static_assert(FMT != LW_Q8_0 && (T::kSums || kFp4), "the formats with 32-element K-steps of bf16 codes");
+    static_assert(FMT != LW_Q8_0 && (T::kSums || kFp4 || kQ1), "the formats with 32-element K-steps of bf16 codes");
     extern __shared__ bf16x8 smem[];
 
     const int tid = threadIdx.x;
@@ -885,12 +912,12 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
     const uint8_t* hp[2];
     u32x4v hraw[2];
     uint32_t hcur[2][kSub16 ? 4 : 2];
-    if constexpr (kQ5 || kSub16) {
+    if constexpr (kQ5 || kQ1 || kSub16) {
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt) {
             const int64_t r = row0 + 64 * wm + 32 * rt + n32;
             const uint64_t rr = (uint64_t)(r < M ? r : M - 1);
-            if constexpr (kQ5)
+            if constexpr (kQ5 || kQ1)
                 hp[rt] = W + offh + rr * (K32 / 8u) + 4u * (uint32_t)kb0;
             else
                 hp[rt] = W + offh + rr * (K32 / 4u) + 8u * (uint32_t)kb0 + 16u * (uint32_t)h;
@@ -899,11 +926,11 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
     auto load_quad = [&](int q) __attribute__((always_inline)) {
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt) {
-            if constexpr (!kQ2) {
+            if constexpr (!kQ2 && !kQ1) {
                 qraw[rt][0] = *reinterpret_cast<const u32x4v*>(wp[rt] + 64u * (uint32_t)q);
                 qraw[rt][1] = *reinterpret_cast<const u32x4v*>(wp[rt] + 64u * (uint32_t)q + 16u);
             }
-            if constexpr (kQ5) hraw[rt] = *reinterpret_cast<const u32x4v*>(hp[rt] + 16u * (uint32_t)q);
+            if constexpr (kQ5 || kQ1) hraw[rt] = *reinterpret_cast<const u32x4v*>(hp[rt] + 16u * (uint32_t)q);
             if constexpr (kSub16) hraw[rt] = *reinterpret_cast<const u32x4v*>(hp[rt] + 32u * (uint32_t)q);
         }
     };
@@ -916,15 +943,15 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-            for (int hv = 0; hv < (kQ2 ? 0 : 2); ++hv) {
+            for (int hv = 0; hv < (kQ2 || kQ1 ? 0 : 2); ++hv) {
                 const u32x4v v = qraw[rt][hv];
                 const auto s02 = __builtin_amdgcn_permlane32_swap(v[0], v[2], false, false);
                 const auto s13 = __builtin_amdgcn_permlane32_swap(v[1], v[3], false, false);
                 qcur[rt][hv] = u32x4v{s02[0], s13[0], s02[1], s13[1]};
             }
-        // fifth bits: bytes h and 2 + h of each block's word (the lane's
-        // elements of K-steps 0 and 1), two blocks per word
-        if constexpr (kQ5) {
+        // fifth bits (q1_0: the code bits): bytes h and 2 + h of each block's
+        // word (the lane's elements of K-steps 0 and 1), two blocks per word
+        if constexpr (kQ5 || kQ1) {
             const uint32_t hsel = 0x06040200u + 0x01010101u * (uint32_t)h;
 #pragma unroll
             for (int rt = 0; rt < 2; ++rt) {
@@ -1087,8 +1114,11 @@ __global__ void __launch_bounds__(64 * WM) __attribute__((amdgpu_waves_per_eu(2,
 #pragma unroll
             for (int rt = 0; rt < 2; ++rt) {
                 uint32_t w0 = 0, w1 = 0;
-                if constexpr (!kQ2) pair_of(rt, j0 + b, &w0, &w1);
-                if constexpr (kQ5) {
+                if constexpr (!kQ2 && !kQ1) pair_of(rt, j0 + b, &w0, &w1);
+                if constexpr (kQ1) {
+                    const int jb = j0 + b;
+                    decode8_q1((hcur[rt][jb >> 1] >> (16 * (jb & 1))) & 0xFFFFu, &bw[rt][0], &bw[rt][1]);
+                } else if constexpr (kQ5) {
                     const int jb = j0 + b;
                     decode8_q5(w0, w1, (hcur[rt][jb >> 1] >> (16 * (jb & 1))) & 0xFFFFu, &bw[rt][0], &bw[rt][1]);
                 } else if constexpr (kQ6) {
@@ -1374,8 +1404,9 @@ hipError_t launch_prefill(int fmt, const uint8_t* W, const float* x, float* y, i
     case LW_MXFP4: return launch_gemm<LW_MXFP4>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q6_K: return launch_gemm<LW_Q6_K>(W, x, y, M, K, n_tok, p, stream);
     case LW_Q2_K: return launch_gemm<LW_Q2_K>(W, x, y, M, K, n_tok, p, stream);
+    case LW_Q1_0: return launch_gemm<LW_Q1_0>(W, x, y, M, K, n_tok, p, stream);
     default:
-        // f16 and q1_0 weights: token blocks of the matrix-vector kernel
+        // f16 weights: token blocks of the matrix-vector kernel
         // (float32 throughout), all whole blocks in one launch
         return launch_gemv_blocks(fmt, W, x, y, M, K, n_tok, p, stream);
     }

@@ -84,7 +84,10 @@ def check(y, y_ref, A, F=None, tol=TOL, f32_bound=None, what="", normwise=True):
     float32 bound |y - y_ref| <= f32_bound * A + 2^-17 * F for every output.
     F: the oracle's term mass for the evaluated form (None: a plain sum).
     normwise=False skips (ii), for inputs built to cancel (all-zero rows)
-    where max |y_ref| says nothing about the kernel."""
+    where max |y_ref| says nothing about the kernel. (ii) needs a column of
+    several outputs: for a one-row matrix it is the elementwise relative
+    error of that one output, which no float32 evaluation bounds where the
+    row cancels; such columns are held to (i) and the float32 bound."""
     y_ref = np.asarray(y_ref, np.float64)
     yy = np.asarray(y, np.float64).reshape(y_ref.shape)
     Aa = np.asarray(A, np.float64).reshape(y_ref.shape)
@@ -94,7 +97,7 @@ def check(y, y_ref, A, F=None, tol=TOL, f32_bound=None, what="", normwise=True):
     d = np.abs(yy - y_ref)
     bad = d > _bounds(Aa, Fa, tol)
     assert not bad.any(), (what, "gate (i)", int(bad.sum()), m)
-    if normwise:
+    if normwise and y_ref.shape[-1] > 1:
         assert m["normwise"] <= tol, (what, "gate (ii)", m)
     if f32_bound is not None:
         bad = d > _bounds(Aa, Fa, f32_bound)
@@ -138,6 +141,6 @@ def check_fp4(y, y_ref, A, Bm, what="", normwise=True):
     m["fp4_ratio"] = float(_ratio(d, bound).max())
     bad = d > bound
     assert not bad.any(), (what, "exceeds the fp4 path's bound", int(bad.sum()), m)
-    if normwise:
+    if normwise and y_ref.shape[-1] > 1:
         assert m["normwise"] <= TOL, (what, "gate (ii)", m)
     return m

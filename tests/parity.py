@@ -4,12 +4,13 @@ of the form the selected kernel evaluates (gate.py derives the bound).
 The VALU kernels evaluate the formats with an offset as s * sum q x +
 mu * sum x (beta = 0); the matrix-core kernels multiply the bfloat16 of
 128 + q (beta = 128). f16, Q8_0 and mxfp4 are plain sums of products (mxfp4
-scaled by powers of two only): F is None.
+scaled by powers of two only): F is None. So is q1_0 on the matrix cores,
+which multiply the exact bfloat16 +-1 of each bit and scale by d.
 lw_kernel_name / lw_kernel_name_multi say which kernel a call launches."""
 import numpy as np
 
 from paper_2605_20706_amd import binding
-from paper_2605_20706_amd.layout import F16, MXFP4, Q8_0
+from paper_2605_20706_amd.layout import F16, MXFP4, Q1_0, Q8_0
 
 MFMA_KERNELS = frozenset({"fewtok_kernel", "multitok_kernel", "multitok_pk_kernel", "skinny_kernel",
                           "gemm_kernel", "gemm32_kernel"})
@@ -21,6 +22,11 @@ def beta_of(kernel):
 
 def plain(fmt):
     return fmt in (F16, Q8_0, MXFP4)
+
+
+def plain_on(fmt, kernel):
+    """The kernel's evaluation is a plain sum of products (no offset term)."""
+    return plain(fmt) or (fmt == Q1_0 and beta_of(kernel) == 128)
 
 
 def kernel_of(fmt, M, K, n_tok, Ms=None):
@@ -48,7 +54,7 @@ class Ref:
             self.y, self.A, self.Fs[b] = y, A, F
 
     def F(self, kernel, nt=None):
-        if plain(self.fmt):
+        if plain_on(self.fmt, kernel):
             return None
         F = self.Fs[beta_of(kernel)]
         return F if nt is None else F[:nt]

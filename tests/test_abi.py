@@ -272,7 +272,8 @@ def test_launch_count(lib):
     assert binding.launch_count(Q4_0, 14336, 4096, 512) == 1
     assert binding.launch_count(F16, 2048, 2048, 17) == 2         # two blocks of 8, then one token
     assert binding.launch_count(F16, 2048, 2048, 16) == 1
-    assert binding.launch_count(Q1_0, 2048, 2048, 512) == 1       # 128 blocks of 4 in one launch
+    assert binding.launch_count(Q1_0, 2048, 2048, 512) == 2       # tiled: K split over a zeroed y
+    assert binding.launch_count(F16, 2048, 2048, 512) == 1        # 64 blocks of 8 in one launch
     assert binding.launch_count_multi(Q4_K, [14336, 14336], 4096, 1) == 1   # fused gate + up
     assert binding.launch_count_multi(Q4_K, [14336, 14336], 4096, 2) == 2   # one per matrix
     assert binding.launch_count_multi(Q4_0, [14336, 14336], 4096, 4) == 1

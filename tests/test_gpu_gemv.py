@@ -55,7 +55,7 @@ def test_parity_many_rows(oracle_mod, fmt):
         gate.check(y, ref.y[:nt], ref.A[:nt], ref.F(kern, nt), f32_bound=1e-4, what=(fmt, M, K, nt, kern))
 
 
-@pytest.mark.parametrize("fmt", [Q4_0, Q4_K, Q4_1, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K, MXFP4])
+@pytest.mark.parametrize("fmt", [Q4_0, Q4_K, Q4_1, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K, MXFP4, Q1_0])
 @pytest.mark.parametrize("M,K", [(70000, 512), (300000, 256), (8200, 14336)])
 def test_parity_few_tokens_tiles(oracle_mod, fmt, M, K):
     """Few-token matrix-core kernel with the activations in LDS: more 16-row

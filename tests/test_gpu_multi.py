@@ -62,7 +62,7 @@ def test_multi_lds_kernel_full_size(oracle_mod, fmt):
     run_multi(oracle_mod, fmt, [8192, 8192], 2048, 1, 33)
 
 
-@pytest.mark.parametrize("fmt", [Q4_0, Q4_K, Q4_1, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K, MXFP4])
+@pytest.mark.parametrize("fmt", [Q4_0, Q4_K, Q4_1, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K, MXFP4, Q1_0])
 @pytest.mark.parametrize("Ms,K", [((14336, 14336), 4096), ((3000, 3000, 2048), 4096), ((40000, 37, 40000), 256),
                                   ((70000, 70000), 256)])
 def test_multi_fewtok_kernel(oracle_mod, fmt, Ms, K):

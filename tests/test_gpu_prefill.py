@@ -1,5 +1,5 @@
-"""Prefill (more than 16 tokens; every quantized format but q1_0) on the
-matrix cores against the oracle: several row and token tiles with ragged tails, the
+"""Prefill (more than 16 tokens; every quantized format) on the matrix
+cores against the oracle: several row and token tiles with ragged tails, the
 K-split launch (partial products added into a zeroed y) with an uneven last
 split and a half coefficient window, and the unsplit launch.
 
@@ -28,7 +28,7 @@ def run(oracle_mod, fmt, M, K, n_tok, seed):
     gate.check(y, y_ref, A, F, f32_bound=1e-4, what=(fmt, M, K, n_tok))
 
 
-@pytest.mark.parametrize("fmt", [Q4_0, Q4_K, Q4_1, Q8_0, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K, MXFP4])
+@pytest.mark.parametrize("fmt", [Q4_0, Q4_K, Q4_1, Q8_0, Q5_0, Q5_1, Q5_K, Q6_K, Q2_K, MXFP4, Q1_0])
 @pytest.mark.parametrize("M,K,n_tok", [
     (1100, 4352, 100),  # 3 x 2 tiles (ragged rows and tokens); K split 5 + 5 + 5 + 2 super-blocks
     (300, 1024, 17),    # one tile, 17 tokens (one past the few-token paths); unsplit (4 super-blocks)
@@ -39,13 +39,13 @@ def test_prefill_tiles(oracle_mod, fmt, M, K, n_tok):
     run(oracle_mod, fmt, M, K, n_tok, 50)
 
 
-@pytest.mark.parametrize("fmt", [F16, Q1_0])
+@pytest.mark.parametrize("fmt", [F16])
 @pytest.mark.parametrize("M,K,n_tok", [(300, 2304, 517), (1, 256, 64)])
 def test_token_blocks_one_launch(oracle_mod, fmt, M, K, n_tok):
-    """f16 and q1_0 run many tokens as blocks of the matrix-vector kernel, all
-    whole blocks in one launch (grid.y = block) and the remaining tokens in
-    one more: 517 tokens are 64 blocks of 8 plus 5 (f16) or 129 blocks of 4
-    plus 1 (q1_0); 64 tokens leave no remainder."""
+    """f16 runs many tokens as blocks of the matrix-vector kernel, all whole
+    blocks in one launch (grid.y = block) and the remaining tokens in one
+    more: 517 tokens are 64 blocks of 8 plus 5; 64 tokens leave no
+    remainder."""
     run(oracle_mod, fmt, M, K, n_tok, 70)
 
 
