@@ -187,10 +187,12 @@ LW_API int lw_matvec(int fmt, const void* W, const float* x, float* y,
  * decode step of Sec. 2.1. Results equal n_mat lw_matvec calls, up to float32
  * summation order. With one token the rows of all matrices form one row space
  * and the call is a single kernel launch (the single-token kernels, selected
- * as for lw_matvec with M = the sum of the M_i). With 3 to 8 tokens and a
- * 4-bit format it is one launch of the few-token matrix-core kernel where
- * that kernel takes the summed row count (each workgroup then works on rows
- * of one matrix). Otherwise it enqueues one lw_matvec per matrix.
+ * as for lw_matvec with M = the sum of the M_i). With 3 to 8 tokens (2 to 8
+ * for the formats without the two-token register kernel: all but Q4_0, Q4_K,
+ * Q4_1 and q1_0) and a format the few-token matrix-core kernel serves (all
+ * quantized formats but Q8_0), it is one launch of that kernel where it
+ * takes the summed row count (each workgroup then works on rows of one
+ * matrix). Otherwise it enqueues one lw_matvec per matrix.
  *
  *   fmt      one of lw_fmt, shared by all matrices.
  *   n_mat    1 <= n_mat <= LW_MULTI_MAX.

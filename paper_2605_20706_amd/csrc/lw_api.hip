@@ -28,6 +28,14 @@ bool known_fmt(int fmt) {
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
+// lw_matvec_multi takes the fused few-token launch from three tokens for the
+// formats whose two-token calls run the register kernel (one launch per
+// matrix is faster there at every shape), from two for the others.
+bool fused_few(int fmt, int n_mat, int64_t n_tok) {
+    const bool reg2 = fmt == LW_Q4_0 || fmt == LW_Q4_K || fmt == LW_Q4_1 || fmt == LW_Q1_0;
+    return n_mat > 1 && n_tok <= 8 && n_tok >= (reg2 ? 3 : 2);
+}
+
 // The checks of lw_matvec that need no pointer, in the documented order.
 int check_shape(int fmt, int64_t M, int64_t K, int64_t n_tok) {
     if (!known_fmt(fmt)) return LW_EFMT;
@@ -166,9 +174,7 @@ int lw_matvec_multi(int fmt, int n_mat, const void* const* W, float* const* y, c
     hipError_t err = hipErrorNotSupported;
     const uint8_t* const* Wb = reinterpret_cast<const uint8_t* const*>(W);
     if (n_tok == 1 && n_mat > 1) err = lw::launch_gemv_multi(fmt, n_mat, Wb, y, M, x, K, s);
-    // two tokens: the register kernel, one launch per matrix, is faster than
-    // the few-token kernel at every shape (and takes one matrix only)
-    if (n_tok >= 3 && n_tok <= 8 && n_mat > 1) err = lw::launch_fewtok_multi(fmt, n_mat, Wb, y, M, x, K, n_tok, s);
+    if (fused_few(fmt, n_mat, n_tok)) err = lw::launch_fewtok_multi(fmt, n_mat, Wb, y, M, x, K, n_tok, s);
     if (err == hipErrorNotSupported) {
         err = hipSuccess;
         for (int i = 0; i < n_mat && err == hipSuccess; ++i)
@@ -215,8 +221,7 @@ bool run_query(int fmt, int n_mat, const int64_t* Ms, int64_t M, int64_t K, int6
         }
         err = hipErrorNotSupported;
         if (n_tok == 1 && n_mat > 1) err = lw::launch_gemv_multi(fmt, n_mat, Ws, ys, Ms, xs, K, nullptr);
-        if (n_tok >= 3 && n_tok <= 8 && n_mat > 1)
-            err = lw::launch_fewtok_multi(fmt, n_mat, Ws, ys, Ms, xs, K, n_tok, nullptr);
+        if (fused_few(fmt, n_mat, n_tok)) err = lw::launch_fewtok_multi(fmt, n_mat, Ws, ys, Ms, xs, K, n_tok, nullptr);
         if (err == hipErrorNotSupported) {
             err = hipSuccess;
             for (int i = 0; i < n_mat && err == hipSuccess; ++i)

@@ -277,6 +277,9 @@ def test_launch_count(lib):
     assert binding.launch_count_multi(Q4_K, [14336, 14336], 4096, 1) == 1   # fused gate + up
     assert binding.launch_count_multi(Q4_K, [14336, 14336], 4096, 2) == 2   # one per matrix
     assert binding.launch_count_multi(Q4_0, [14336, 14336], 4096, 4) == 1
+    assert binding.launch_count_multi(Q5_K, [14336, 14336], 4096, 2) == 1   # no register kernel: fused
+    assert binding.launch_count_multi(Q1_0, [6144, 6144], 2048, 2) == 2     # the register kernel per matrix
+    assert binding.launch_count_multi(Q1_0, [6144, 6144], 2048, 4) == 1
     f = lib.lw_launch_count
     assert f(12, 4, 256, 1) == LW_EFMT
     assert f(Q4_0, 0, 256, 1) == LW_EINVAL

@@ -69,7 +69,8 @@ def test_multi_fewtok_kernel(oracle_mod, fmt, Ms, K):
     """The few-token kernel over two to four matrices in one launch: the 8B
     gate/up pair, ragged segments whose last workgroup is short, a segment
     smaller than one workgroup's rows, and two or three tiles per wave."""
-    for n_tok in (3, 8):
+    # two tokens are fused too where no register kernel takes them
+    for n_tok in ((3, 8) if fmt in (Q4_0, Q4_K, Q4_1, Q1_0) else (2, 3, 8)):
         name = binding.kernel_name_multi(fmt, list(Ms), K, n_tok)
         assert name.startswith("fewtok_kernel<%d, " % fmt), name
         run_multi(oracle_mod, fmt, list(Ms), K, n_tok, 34)
