@@ -19,8 +19,10 @@
 // heads in registers; scores are lane sums over the LPR = head_dim / DPL
 // lanes of a position, and the online softmax rescales the lane's G x DPL
 // output partials by exp(m_old - m_new) per batch. The wave's partials are
-// then summed over positions (DPP and permlane steps) and the four waves combined
-// through LDS. Everything is float32; every exp argument is <= 0.
+// then summed over positions by a reduce-scatter (two permlane swap steps,
+// each halving the values a lane holds, then DPP row rotations), and the
+// four waves combined through LDS. Everything is float32; every exp
+// argument is <= 0.
 #include <cmath>
 
 #include "lw_device.hpp"
@@ -84,6 +86,45 @@ template <int LO, int SH = LO>
 __device__ __forceinline__ float residue_sum(float v) {
     if constexpr (SH < 16) return residue_sum<LO, 2 * SH>(v + dpp_move<0x120 + SH>(v));
     else return group_sum<16, kWave>(v);
+}
+
+// v summed over the lanes of its 16-lane row congruent to this one modulo LO
+// (LO = 1 .. 16, a power of two; 16: v itself).
+template <int LO, int SH = LO>
+__device__ __forceinline__ float row_residue_sum(float v) {
+    if constexpr (SH < 16) return row_residue_sum<LO, 2 * SH>(v + dpp_move<0x120 + SH>(v));
+    else return v;
+}
+
+// Reduce-scatter of N per-lane values over the lanes that share this lane's
+// value set apart from the row bits LO (a power of two, at most 16) .. 32 of
+// the lane index: the halves of the set are exchanged across the 32-lane and
+// the 16-lane halves with one permlane swap per two values (each lane then
+// adds the half it keeps), and the row bits below 16 are summed with DPP row
+// rotations. Afterwards out[j], j < N / 4, holds the total of value
+// j + (N / 4) (bit 4) + (N / 2) (bit 5) of the lane index.
+template <int N, int LO>
+__device__ __forceinline__ void reduce_scatter(const float* v, float* out) {
+    static_assert(N % 4 == 0 && LO >= 1 && LO <= 16, "whole quarters, row bits from LO");
+    float w[N / 2];
+#pragma unroll
+    for (int j = 0; j < N / 2; ++j) {
+        const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, v[j]),
+                                                        __builtin_bit_cast(uint32_t, v[j + N / 2]), false, false);
+        uint32_t r0 = r[0], r1 = r[1];
+        asm("" : "+v"(r0), "+v"(r1));  // else the compiler folds r[1] into r[0] when both are summed
+        w[j] = __builtin_bit_cast(float, r0) + __builtin_bit_cast(float, r1);
+    }
+#pragma unroll
+    for (int j = 0; j < N / 4; ++j) {
+        const auto r = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(uint32_t, w[j]),
+                                                        __builtin_bit_cast(uint32_t, w[j + N / 4]), false, false);
+        uint32_t r0 = r[0], r1 = r[1];
+        asm("" : "+v"(r0), "+v"(r1));  // else the compiler folds r[1] into r[0] when both are summed
+        out[j] = __builtin_bit_cast(float, r0) + __builtin_bit_cast(float, r1);
+    }
+#pragma unroll
+    for (int j = 0; j < N / 4; ++j) out[j] = row_residue_sum<LO>(out[j]);
 }
 
 template <int FMT, int D, int G>
@@ -187,14 +228,29 @@ __global__ void __launch_bounds__(kAttnThreads)
     }
 
     // the wave's totals: l over all lanes, the outputs over the positions
+    // (the G * DPL sums over the wave's positions: a reduce-scatter leaves a
+    // quarter of them in each lane, which the first LPR lanes of each
+    // 16-lane row store)
+    {
+        constexpr int N = G * DPL;
+        float v[N], tot[N / 4];
+#pragma unroll
+        for (int h = 0; h < G; ++h)
+#pragma unroll
+            for (int i = 0; i < DPL; ++i) v[h * DPL + i] = acc[h][i];
+        reduce_scatter<N, LPR>(v, tot);
+        const int J0 = ((lane >> 4) & 1) * (N / 4) + ((lane >> 5) & 1) * (N / 2);
+        if ((lane & 15) < LPR) {
+#pragma unroll
+            for (int j = 0; j < N / 4; ++j) {
+                const int J = J0 + j;
+                red[wave][J / DPL][c * DPL + J % DPL] = tot[j];
+            }
+        }
+    }
 #pragma unroll
     for (int h = 0; h < G; ++h) {
         const float lt = group_sum<1, kWave>(l[h]);
-#pragma unroll
-        for (int i = 0; i < DPL; ++i) {
-            const float a = residue_sum<LPR>(acc[h][i]);
-            if (r == 0) red[wave][h][c * DPL + i] = a;
-        }
         if (lane == 0) {
             red[wave][h][D] = m[h];
             red[wave][h][D + 1] = lt;
