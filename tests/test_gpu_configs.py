@@ -8,7 +8,9 @@ kernel evaluates.
 Workloads: the single Q8_0 2048x2048 matrix; the Llama-3.2-1B-shaped f16 set
 (80 matrices); the 1B Q4_0 set with its lm_head (81); the Llama-3-8B-shaped
 Q4_K-style set with its lm_head (161, in five parts); the 8B Q4_0 and Q4_1
-FFN sets at 1, 2, 4, 8 and 512 tokens; the 1.7B q1_0 set (141, in two parts)."""
+FFN sets at 1, 2, 4, 8 and 512 tokens, and the other formats' 8B FFN sets at
+the same counts; the 1.7B q1_0 set (141, in two parts) and its first layer
+at 2, 4, 8 and 512 tokens."""
 import os
 
 import numpy as np
@@ -103,6 +105,16 @@ def test_ffn_every_output(oracle_mod, key, n_tok):
     wl = synth.WORKLOADS[key]
     n = run_calls(oracle_mod, wl, range(len(wl.matrices)), n_tok)
     assert n == n_tok * sum(m.M for m in wl.matrices)
+
+
+@pytest.mark.parametrize("n_tok", [2, 4, 8, 512])
+def test_q1_0_layer_tokens_every_output(oracle_mod, n_tok):
+    """The 1.7B q1_0 set's first layer (qkv, o, gate + up fused, down) at the
+    multi-token counts of the benchmark: the register kernel (2 tokens), the
+    few-token matrix-core kernel (4, 8) and the tiled one (512); every output."""
+    wl = synth.WORKLOADS["q1_0_1b7"]
+    n = run_calls(oracle_mod, wl, range(5), n_tok)
+    assert n == n_tok * sum(wl.matrices[i].M for i in range(5))
 
 
 @pytest.mark.parametrize("key", ["q4_0_llama8b_ffn"])
