@@ -17,12 +17,17 @@
 // workgroup each wave takes batches of RPW positions: lane (r, c) holds DPL
 // consecutive dimensions c*DPL .. of position r, its query slices for the G
 // heads in registers; scores are lane sums over the LPR = head_dim / DPL
-// lanes of a position, and the online softmax rescales the lane's G x DPL
-// output partials by exp(m_old - m_new) per batch. The wave's partials are
-// then summed over positions by a reduce-scatter (two permlane swap steps,
-// each halving the values a lane holds, then DPP row rotations), and the
-// four waves combined through LDS. Everything is float32; every exp
-// argument is <= 0.
+// lanes of a position. Batches come in sets of NB, two sets in flight per
+// wave: the next set's loads are issued before the current set is decoded
+// (f16, Q8_0 and Q4_0 keep the raw words until then; Q8_0 and Q4_0 decode
+// to codes with one affine scale per lane and row, applied once per head
+// to the score and the weight instead of once per element). The online
+// softmax takes one maximum per head over the whole set and rescales the
+// lane's G x DPL output partials by exp(m_old - m_new) only when a maximum
+// grew. The wave's partials are then summed over positions by a
+// reduce-scatter (two permlane swap steps, each halving the values a lane
+// holds, then DPP row rotations), and the four waves combined through LDS.
+// Everything is float32; every exp argument is <= 0.
 #include <cmath>
 
 #include "lw_device.hpp"
@@ -38,6 +43,11 @@ struct Name_attn_split_kernel {
 
 constexpr int kAttnWaves = 4;
 constexpr int kAttnThreads = kAttnWaves * kWave;
+#ifndef LW_ATTN_RAW_BATCHES
+#define LW_ATTN_RAW_BATCHES 2
+#endif
+// batches of raw K/V loads in flight per wave (f16, Q8_0, Q4_0)
+constexpr int kAttnRawBatches = LW_ATTN_RAW_BATCHES;
 
 template <int G>
 constexpr int dims_per_lane() {
@@ -127,6 +137,85 @@ __device__ __forceinline__ void reduce_scatter(const float* v, float* out) {
     for (int j = 0; j < N / 4; ++j) out[j] = row_residue_sum<LO>(out[j]);
 }
 
+// Raw K/V loads for f16, Q8_0 and Q4_0: the lane's DPL elements of a row
+// (consecutive, inside one 32-element block) are kept as loaded, a few
+// words per row, and decoded only when the batch is used, so that further
+// batches stay in flight meanwhile. Q8_0 and Q4_0 decode to codes c_i with
+// value a * c_i + b (a and b the block's), so the scale multiplies once per
+// lane and head instead of once per element: Q8_0 c = code + 128 (the code
+// with its sign bit flipped, one v_cvt_f32_ubyte), a = d, b = -128 d; Q4_0
+// c = the nibble, a = d, b = -8 d (both b exact).
+template <int FMT, int DPL>
+struct AttnRaw {
+    static constexpr bool kOn = FMT == LW_F16 || FMT == LW_Q8_0 || FMT == LW_Q4_0;
+    static constexpr bool kAffine = FMT == LW_Q8_0 || FMT == LW_Q4_0;
+    static constexpr int kWords = FMT == LW_F16 ? DPL / 2 : DPL / 4;
+    // the other formats: the values, decoded by the element routine on load
+    struct Raw {
+        uint32_t w[kOn ? kWords : DPL];
+        uint32_t s;
+    };
+    // element e of the plane (e a multiple of DPL)
+    __device__ static void load(const uint8_t* __restrict__ P, int64_t off1, int64_t off2, int64_t off3, int64_t e,
+                                Raw& x) {
+        if constexpr (kOn) {
+            // Q4_0: block e / 32 holds element 32g + i in the low nibble of
+            // byte i and 32g + i + 16 in the high nibble of the same byte
+            const uint8_t* p = FMT == LW_F16 ? P + 2 * e : FMT == LW_Q8_0 ? P + e : P + 16 * (e >> 5) + (e & 15);
+#pragma unroll
+            for (int k = 0; k < kWords; k += 4) {
+                if constexpr (kWords >= 4) {
+                    const uint4 t = *reinterpret_cast<const uint4*>(p + 4 * k);
+                    x.w[k] = t.x;
+                    x.w[k + 1] = t.y;
+                    x.w[k + 2] = t.z;
+                    x.w[k + 3] = t.w;
+                } else {
+                    const uint2 t = *reinterpret_cast<const uint2*>(p);
+                    x.w[0] = t.x;
+                    x.w[1] = t.y;
+                }
+            }
+            if constexpr (kAffine) x.s = *reinterpret_cast<const uint16_t*>(P + off1 + 2 * (e >> 5));
+        } else {
+#pragma unroll
+            for (int i = 0; i < DPL / 4; ++i) {
+                const float4 t = value4<FMT>(P, off1, off2, off3, e + 4 * i);
+                x.w[4 * i] = __builtin_bit_cast(uint32_t, t.x);
+                x.w[4 * i + 1] = __builtin_bit_cast(uint32_t, t.y);
+                x.w[4 * i + 2] = __builtin_bit_cast(uint32_t, t.z);
+                x.w[4 * i + 3] = __builtin_bit_cast(uint32_t, t.w);
+            }
+        }
+    }
+    // sh: the Q4_0 nibble (0 or 4), the same for every row of a lane
+    __device__ static void decode(const Raw& x, int sh, float* c, float& a, float& b) {
+        a = 1.f;
+        b = 0.f;
+        if constexpr (FMT == LW_F16) {
+#pragma unroll
+            for (int k = 0; k < kWords; ++k) {
+                c[2 * k] = half_bits_to_float(x.w[k] & 0xFFFFu);
+                c[2 * k + 1] = half_bits_to_float(x.w[k] >> 16);
+            }
+        } else if constexpr (kAffine) {
+#pragma unroll
+            for (int k = 0; k < kWords; ++k) {
+                const uint32_t w = FMT == LW_Q8_0 ? x.w[k] ^ 0x80808080u : opaque((x.w[k] >> sh) & 0x0F0F0F0Fu);
+                c[4 * k] = ubyte<0>(w);
+                c[4 * k + 1] = ubyte<1>(w);
+                c[4 * k + 2] = ubyte<2>(w);
+                c[4 * k + 3] = ubyte<3>(w);
+            }
+            a = half_bits_to_float(x.s);
+            b = (FMT == LW_Q8_0 ? -128.0f : -8.0f) * a;
+        } else {
+#pragma unroll
+            for (int i = 0; i < DPL; ++i) c[i] = __builtin_bit_cast(float, x.w[i]);
+        }
+    }
+};
+
 template <int FMT, int D, int G>
 __global__ void __launch_bounds__(kAttnThreads)
     attn_split_kernel(const float* __restrict__ q, const uint8_t* __restrict__ Kc, const uint8_t* __restrict__ Vc,
@@ -139,7 +228,9 @@ __global__ void __launch_bounds__(kAttnThreads)
 
     const int g = blockIdx.x, split = blockIdx.y;
     const int lane = threadIdx.x & (kWave - 1);
-    const int wave = threadIdx.x / kWave;
+    // wave-uniform in a scalar register: the loop over the sets below
+    // then branches on scalars, and its waits can leave loads in flight
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int r = lane / LPR, c = lane - r * LPR;
     const int j0 = split * rps;
     // scores in base-2 units: exp(x) = exp2(x log2(e)), one v_exp_f32 each
@@ -159,72 +250,128 @@ __global__ void __launch_bounds__(kAttnThreads)
             qv[h][4 * i + 3] = t.w;
         }
     }
+    using RW = AttnRaw<FMT, DPL>;
+    constexpr bool kAff = RW::kAffine;
+    // affine loads: the lane's query sums (the b term of a score) and the
+    // b terms of the output, accb (the same for all the lane's dimensions)
+    float qsum[G], accb[G];
     float m[G], l[G], acc[G][DPL];
 #pragma unroll
     for (int h = 0; h < G; ++h) {
         m[h] = -INFINITY;
         l[h] = 0.f;
+        accb[h] = 0.f;
+        qsum[h] = 0.f;
 #pragma unroll
-        for (int i = 0; i < DPL; ++i) acc[h][i] = 0.f;
+        for (int i = 0; i < DPL; ++i) {
+            acc[h][i] = 0.f;
+            qsum[h] += qv[h][i];
+        }
     }
 
     const int64_t head_base = (int64_t)g * kv_len;
-    // one batch: positions b .. b + RPW - 1 (this lane: b + r), K and V decoded
-    auto load_batch = [&](int b, float* kk, float* vv) __attribute__((always_inline)) {
+    // a batch: positions b .. b + RPW - 1 (this lane: b + r; rows past the
+    // split repeat its last row and are masked)
+    constexpr int kStep = kAttnWaves * RPW;
+    auto elem = [&](int b) __attribute__((always_inline)) {
         const int row = b + r;
-        const int64_t e = (head_base + (row < j1 ? row : j1 - 1)) * D + c * DPL;
+        return (head_base + (row < j1 ? row : j1 - 1)) * D + c * DPL;
+    };
+    // a set: NB batches b, b + kStep, ... loaded together. K and V of f16,
+    // Q8_0 and Q4_0 stay as loaded until the set is used; the other formats
+    // are decoded on load (their values take more registers: one batch)
+    constexpr int NB = RW::kOn ? kAttnRawBatches : 1;
+    using Raw = typename RW::Raw;
+    const int sh = (c * DPL) & 16 ? 4 : 0;
+    auto load_set = [&](int b, Raw* kr, Raw* vr) __attribute__((always_inline)) {
 #pragma unroll
-        for (int i = 0; i < DPL / 4; ++i) {
-            const float4 t = value4<FMT>(Kc, off1, off2, off3, e + 4 * i);
-            kk[4 * i] = t.x;
-            kk[4 * i + 1] = t.y;
-            kk[4 * i + 2] = t.z;
-            kk[4 * i + 3] = t.w;
-        }
-#pragma unroll
-        for (int i = 0; i < DPL / 4; ++i) {
-            const float4 t = value4<FMT>(Vc, off1, off2, off3, e + 4 * i);
-            vv[4 * i] = t.x;
-            vv[4 * i + 1] = t.y;
-            vv[4 * i + 2] = t.z;
-            vv[4 * i + 3] = t.w;
+        for (int i = 0; i < NB; ++i) {
+            const int64_t e = elem(b + i * kStep);
+            RW::load(Kc, off1, off2, off3, e, kr[i]);
+            RW::load(Vc, off1, off2, off3, e, vr[i]);
         }
     };
-    auto consume = [&](int b, const float* kk, const float* vv) __attribute__((always_inline)) {
-        const bool valid = b + r < j1;
+    // the set's scores for every head, then one maximum per head over the
+    // set (one rescale test per set, no branch between the heads), then
+    // the weights and the output partials
+    auto use_set = [&](int b, const Raw* kr, const Raw* vr) __attribute__((always_inline)) {
+        float s[NB][G];
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            float kk[DPL], ka, kb;
+            RW::decode(kr[i], sh, kk, ka, kb);
+            const bool valid = b + i * kStep + r < j1;
+#pragma unroll
+            for (int h = 0; h < G; ++h) {
+                float d = 0.f;
+#pragma unroll
+                for (int k = 0; k < DPL; ++k) d = __builtin_fmaf(qv[h][k], kk[k], d);
+                if constexpr (kAff) d = __builtin_fmaf(kb, qsum[h], ka * d);
+                d = group_sum<1, LPR>(d);
+                s[i][h] = valid ? d * scale2 : -INFINITY;
+            }
+        }
+        float mn[G];
+        bool grow = false;
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-            float d = 0.f;
+            float mb = s[0][h];
 #pragma unroll
-            for (int i = 0; i < DPL; ++i) d = __builtin_fmaf(qv[h][i], kk[i], d);
-            d = group_sum<1, LPR>(d);
-            const float s = valid ? d * scale2 : -INFINITY;
-            const float mb = group_max<LPR, kWave>(s);
-            const float mn = fmaxf(m[h], mb);  // finite: the batch has a valid position
-            if (mn != m[h]) {                  // wave-uniform: a new maximum rescales the partials
-                const float alpha = __builtin_amdgcn_exp2f(m[h] - mn);  // m = -inf: 0
-                m[h] = mn;
+            for (int i = 1; i < NB; ++i) mb = fmaxf(mb, s[i][h]);
+            mb = group_max<LPR, kWave>(mb);
+            mn[h] = fmaxf(m[h], mb);  // finite: the first set has a valid position
+            grow |= mn[h] != m[h];
+        }
+        if (__builtin_amdgcn_readfirstlane((int)grow)) {  // wave-uniform: a new maximum rescales the partials
+#pragma unroll
+            for (int h = 0; h < G; ++h) {
+                const float alpha = __builtin_amdgcn_exp2f(m[h] - mn[h]);  // m = -inf: 0; unchanged: 1
+                m[h] = mn[h];
                 l[h] *= alpha;
+                if constexpr (kAff) accb[h] *= alpha;
 #pragma unroll
-                for (int i = 0; i < DPL; ++i) acc[h][i] *= alpha;
+                for (int k = 0; k < DPL; ++k) acc[h][k] *= alpha;
             }
-            const float p = valid ? __builtin_amdgcn_exp2f(s - mn) : 0.f;
-            l[h] += c == 0 ? p : 0.f;
+        }
 #pragma unroll
-            for (int i = 0; i < DPL; ++i) acc[h][i] = __builtin_fmaf(p, vv[i], acc[h][i]);
+        for (int i = 0; i < NB; ++i) {
+            float vv[DPL], va, vb;
+            RW::decode(vr[i], sh, vv, va, vb);
+#pragma unroll
+            for (int h = 0; h < G; ++h) {
+                const float p = __builtin_amdgcn_exp2f(s[i][h] - m[h]);  // masked (s = -inf): 0
+                l[h] += p;  // in all LPR lanes of the position: LPR times the sum
+                float pa = p;
+                if constexpr (kAff) {
+                    pa = p * va;
+                    accb[h] = __builtin_fmaf(p, vb, accb[h]);
+                }
+#pragma unroll
+                for (int k = 0; k < DPL; ++k) acc[h][k] = __builtin_fmaf(pa, vv[k], acc[h][k]);
+            }
         }
     };
-    // two batches per round, both loaded before either is used (twice the
-    // bytes in flight per wave); the second only where it starts inside
-    // the split
-    constexpr int kStep = kAttnWaves * RPW;
-    for (int b = j0 + wave * RPW; b < j1; b += 2 * kStep) {
-        float k0[DPL], v0[DPL], k1[DPL], v1[DPL];
-        const bool two = b + kStep < j1;
-        load_batch(b, k0, v0);
-        load_batch(two ? b + kStep : b, k1, v1);
-        consume(b, k0, v0);
-        if (two) consume(b + kStep, k1, v1);
+    // two sets alternate: the next is issued before the current one is
+    // used, so a set per wave is in flight while it computes (unrolled by
+    // hand over the two: no register copies of data still in flight). The
+    // next set is loaded unconditionally (past the split: its last row
+    // again, from the cache), and the loop has one exit and a wave-uniform
+    // trip count, so that every wait for the current set can leave the
+    // next one's loads outstanding.
+    int b = j0 + wave * RPW;
+    if (b < j1) {
+        constexpr int kSet = NB * kStep;
+        const int n = (j1 - b + kSet - 1) / kSet;  // the wave's sets
+        Raw ka[NB], va[NB], kb[NB], vb[NB];
+        load_set(b, ka, va);
+        for (int t = 2; t <= n; t += 2) {
+            load_set(b + kSet, kb, vb);
+            use_set(b, ka, va);
+            load_set(b + 2 * kSet, ka, va);
+            use_set(b + kSet, kb, vb);
+            b += 2 * kSet;
+        }
+        if (n & 1) use_set(b, ka, va);
     }
 
     // the wave's totals: l over all lanes, the outputs over the positions
@@ -237,7 +384,7 @@ __global__ void __launch_bounds__(kAttnThreads)
 #pragma unroll
         for (int h = 0; h < G; ++h)
 #pragma unroll
-            for (int i = 0; i < DPL; ++i) v[h * DPL + i] = acc[h][i];
+            for (int i = 0; i < DPL; ++i) v[h * DPL + i] = kAff ? acc[h][i] + accb[h] : acc[h][i];
         reduce_scatter<N, LPR>(v, tot);
         const int J0 = ((lane >> 4) & 1) * (N / 4) + ((lane >> 5) & 1) * (N / 2);
         if ((lane & 15) < LPR) {
@@ -250,7 +397,9 @@ __global__ void __launch_bounds__(kAttnThreads)
     }
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-        const float lt = group_sum<1, kWave>(l[h]);
+        // each position's weight counted once per lane of the position:
+        // LPR (a power of 2) times the sum, the scaling exact
+        const float lt = group_sum<1, kWave>(l[h]) * (1.0f / LPR);
         if (lane == 0) {
             red[wave][h][D] = m[h];
             red[wave][h][D + 1] = lt;
@@ -280,82 +429,68 @@ __global__ void __launch_bounds__(kAttnThreads)
 }
 
 // out[h][d] = sum_s exp(m_s - M) acc_s[d] / sum_s exp(m_s - M) l_s. One
-// workgroup per head: every thread loads the maxima of its splits at once
-// (one round trip for all of them), the weights w_s = exp(m_s - M) go to
-// LDS, then thread (d, sg) sums the splits sg, sg + SG, ... of output d
-// with sixteen loads in flight, and the SG partials are added through LDS.
-constexpr int kCombThreads = 256;
-constexpr int kMaxSplits = 1024;
+// workgroup per head; thread (d, sg) takes output d of the splits sg,
+// sg + SG, ...: their maxima and partials are loaded together (one round
+// trip for up to U splits per thread), summed against the thread's own
+// running maximum, and the SG groups merged through LDS with one more
+// rescale each (the same merge as the split kernel's waves).
+constexpr int kCombThreads = 512;
 
 template <int D>
 __global__ void __launch_bounds__(kCombThreads) attn_combine_kernel(const float* __restrict__ ws,
                                                                    float* __restrict__ out, int n_heads, int splits) {
     constexpr int SG = kCombThreads / D;  // split groups
-    __shared__ float wsp[kMaxSplits];
-    __shared__ float part[SG][D + 1];
-    __shared__ float red[kCombThreads / kWave];
+    constexpr int U = 16;                 // splits per thread and round
+    __shared__ float part[SG][D + 2];     // group sums of output d; [D]: the group's maximum, [D + 1]: its l
     const int h = blockIdx.x, tid = threadIdx.x;
     const float* base = ws + (int64_t)h * (D + 2);
     const int64_t stride = (int64_t)n_heads * (D + 2);
-    // maxima of the splits: all loads first, then the reduction
-    float mloc[kMaxSplits / kCombThreads];
-#pragma unroll
-    for (int i = 0; i < kMaxSplits / kCombThreads; ++i) {
-        const int s = tid + i * kCombThreads;
-        mloc[i] = s < splits ? base[s * stride + D] : -INFINITY;
-    }
-    float M = -INFINITY;
-#pragma unroll
-    for (int i = 0; i < kMaxSplits / kCombThreads; ++i) M = fmaxf(M, mloc[i]);
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) M = fmaxf(M, __shfl_xor(M, o, kWave));
-    if ((tid & (kWave - 1)) == 0) red[tid / kWave] = M;
-    __syncthreads();
-    M = red[0];
-#pragma unroll
-    for (int w = 1; w < kCombThreads / kWave; ++w) M = fmaxf(M, red[w]);
-#pragma unroll
-    for (int i = 0; i < kMaxSplits / kCombThreads; ++i) {
-        const int s = tid + i * kCombThreads;
-        if (s < splits) wsp[s] = mloc[i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mloc[i] - M);
-    }
-    __syncthreads();
-    // thread (d, sg) sums output d over the splits sg, sg + SG, ...; thread
-    // d = 1 also sums l (slot D + 1) in the same pass. Sixteen splits' loads
-    // (thirty-two for d = 1) are issued before any is used.
     const int sg = tid / D, d0 = tid - sg * D;
-    const bool with_l = d0 == 1;
-    constexpr int U = 16;
-    float o = 0.f, ol = 0.f;
-    int s = sg;
-    for (; s + (U - 1) * SG < splits; s += U * SG) {
-        float v[U], vl[U];
+    const bool with_l = d0 == 1;  // thread d = 1 also sums l (slot D + 1)
+    float M = -INFINITY, o = 0.f, ol = 0.f;
+    for (int s = sg; s < splits; s += U * SG) {
+        float mv[U], v[U], vl[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            v[u] = base[(s + u * SG) * stride + d0];
-            vl[u] = with_l ? base[(s + u * SG) * stride + D + 1] : 0.f;
+            const int su = s + u * SG;
+            const bool ok = su < splits;
+            const float* p = base + (int64_t)(ok ? su : 0) * stride;
+            mv[u] = ok ? p[D] : -INFINITY;
+            v[u] = ok ? p[d0] : 0.f;
+            vl[u] = ok && with_l ? p[D + 1] : 0.f;
         }
+        float mc = M;
+#pragma unroll
+        for (int u = 0; u < U; ++u) mc = fmaxf(mc, mv[u]);
+        // every split has a position, so mc is finite from the first round on
+        const float a = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(M - mc);
+        o *= a;
+        ol *= a;
+        M = mc;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            o = __builtin_fmaf(wsp[s + u * SG], v[u], o);
-            ol = __builtin_fmaf(wsp[s + u * SG], vl[u], ol);
+            const float w = mv[u] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mv[u] - M);
+            o = __builtin_fmaf(w, v[u], o);
+            ol = __builtin_fmaf(w, vl[u], ol);
         }
-    }
-    for (; s < splits; s += SG) {
-        o = __builtin_fmaf(wsp[s], base[s * stride + d0], o);
-        if (with_l) ol = __builtin_fmaf(wsp[s], base[s * stride + D + 1], ol);
     }
     part[sg][d0] = o;
-    if (with_l) part[sg][D] = ol;
+    if (d0 == 0) part[sg][D] = M;  // -inf for a group without splits
+    if (with_l) part[sg][D + 1] = ol;
     __syncthreads();
     if (tid < D) {
-        float o = 0.f, L = 0.f;
+        float Mh = -INFINITY;
+#pragma unroll
+        for (int g = 0; g < SG; ++g) Mh = fmaxf(Mh, part[g][D]);
+        float y = 0.f, L = 0.f;
 #pragma unroll
         for (int g = 0; g < SG; ++g) {
-            o += part[g][tid];
-            L += part[g][D];
+            const float mg = part[g][D];
+            const float w = mg == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mg - Mh);
+            y = __builtin_fmaf(w, part[g][tid], y);
+            L = __builtin_fmaf(w, part[g][D + 1], L);
         }
-        out[(int64_t)h * D + tid] = o / L;
+        out[(int64_t)h * D + tid] = y / L;
     }
 }
 
