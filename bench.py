@@ -792,7 +792,7 @@ def run_attn(args):
     torch.cuda.synchronize()
     call_us = e0.elapsed_time(e1) * 1e3 / seq
     call_bytes = alg / nl
-    kname = "attn_split_kernel<%d, %d, %d>" % (fmt, D, H // nkv)
+    kname = binding.attn_kernel_name(fmt, H, nkv, D, Lkv)
     roof = {"bound": "hbm", "achieved": round(call_bytes / (call_us * 1e-6) / 1e9, 1), "peak": HBM_PEAK_GBS,
             "unit": "GB/s", "frac": round(call_bytes / (call_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4), "traffic": None,
             "kernel": kname + " + attn_combine_kernel<%d>" % D, "launches_per_step": 2 * nl,

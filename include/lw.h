@@ -337,10 +337,14 @@ LW_API int64_t lw_launch_count_ws(int fmt, int64_t M, int64_t K, int64_t n_tok);
  * Errors in the usual order: LW_EFMT (fmt not one of the above), LW_EINVAL
  * (null pointer, sizes out of range, a head ratio or head_dim not listed,
  * scale not finite, workspace too small), LW_ESHAPE (n_kv_heads * kv_len *
- * head_dim not a multiple of 256), LW_EALIGN, LW_EHIP. Two kernel launches.
- * Arithmetic in float32: each output is within 2^-12 * (1 + T) * sum_j p_j
- * |v[g][j][d]| of the exact value, T the largest scale * sum_d |q k| of the
- * head (the score error enters the weights through exp).
+ * head_dim not a multiple of 256), LW_EALIGN, LW_EHIP. Two kernel launches
+ * (lw_attn_kernel_name names the first). Arithmetic in float32, except that
+ * f16, Q8_0 and Q4_0 scores on the matrix cores take the query as two f16
+ * parts (22 significant bits, after an exact power-of-two scaling per head)
+ * times exact f16 forms of the cache elements, with float32 accumulation:
+ * each output is within 2^-12 * (1 + T) * sum_j p_j |v[g][j][d]| of the
+ * exact value, T the largest scale * sum_d |q k| of the head (the score error
+ * enters the weights through exp).
  */
 LW_API int lw_attn_decode(int fmt, const float* q, const void* K, const void* V, float* out, int64_t n_heads,
                           int64_t n_kv_heads, int64_t head_dim, int64_t kv_len, float scale, void* workspace,
@@ -352,6 +356,17 @@ LW_API int lw_attn_decode(int fmt, const float* q, const void* K, const void* V,
  * of the positions), or the size error of the call (negative). Host-only.
  */
 LW_API int64_t lw_attn_workspace_bytes(int fmt, int64_t n_heads, int64_t n_kv_heads, int64_t head_dim,
+                                       int64_t kv_len);
+
+/*
+ * lw_attn_kernel_name — the first of the two kernels lw_attn_decode launches
+ * for these sizes, as "attn_mf_kernel<fmt, head_dim, G>" (f16, Q8_0 and Q4_0
+ * caches when the library's split gives more than 64 positions per
+ * workgroup: scores on the matrix cores) or "attn_split_kernel<...>" (the
+ * vector kernel), G = n_heads / n_kv_heads; NULL when the sizes fail
+ * lw_attn_decode's checks. Host-only; the string is static.
+ */
+LW_API const char* lw_attn_kernel_name(int fmt, int64_t n_heads, int64_t n_kv_heads, int64_t head_dim,
                                        int64_t kv_len);
 
 /*

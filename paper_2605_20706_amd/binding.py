@@ -17,7 +17,7 @@ LW_OK = 0
 EXPORTS = ("lw_matvec", "lw_matvec_multi", "lw_dequant", "lw_weight_bytes", "lw_strerror", "lw_kernel_name",
            "lw_kernel_name_multi", "lw_launch_count", "lw_launch_count_multi", "lw_attn_decode",
            "lw_attn_workspace_bytes", "lw_attn_decode_noalloc", "lw_matvec_ws", "lw_matvec_workspace_bytes",
-           "lw_kernel_name_ws", "lw_launch_count_ws")
+           "lw_kernel_name_ws", "lw_launch_count_ws", "lw_attn_kernel_name")
 LW_MULTI_MAX = 4
 
 
@@ -71,6 +71,8 @@ def library() -> ctypes.CDLL:
         lib.lw_attn_decode.restype = ctypes.c_int
         lib.lw_attn_workspace_bytes.argtypes = [ctypes.c_int, i64, i64, i64, i64]
         lib.lw_attn_workspace_bytes.restype = i64
+        lib.lw_attn_kernel_name.argtypes = [ctypes.c_int, i64, i64, i64, i64]
+        lib.lw_attn_kernel_name.restype = ctypes.c_char_p
         lib.lw_attn_decode_noalloc.argtypes = [ctypes.c_int, vp, vp, vp, vp, i64, i64, i64, i64, ctypes.c_float, vp]
         lib.lw_attn_decode_noalloc.restype = ctypes.c_int
         lib.lw_matvec_ws.argtypes = [ctypes.c_int, vp, vp, vp, i64, i64, i64, vp, i64, vp]
@@ -291,6 +293,13 @@ def attn_workspace_bytes(fmt: int, n_heads: int, n_kv_heads: int, head_dim: int,
     if v < 0:
         raise LwError(v, "lw_attn_workspace_bytes")
     return v
+
+
+def attn_kernel_name(fmt: int, n_heads: int, n_kv_heads: int, head_dim: int, kv_len: int):
+    """The first kernel lw_attn_decode launches for these sizes (None when
+    they fail its checks)."""
+    v = library().lw_attn_kernel_name(fmt, n_heads, n_kv_heads, head_dim, kv_len)
+    return None if v is None else v.decode()
 
 
 def attn_decode(fmt: int, q, K, V, n_heads: int, n_kv_heads: int, head_dim: int, kv_len: int, scale: float,

@@ -28,6 +28,12 @@
 // reduce-scatter (two permlane swap steps, each halving the values a lane
 // holds, then DPP row rotations), and the four waves combined through LDS.
 // Everything is float32; every exp argument is <= 0.
+//
+// f16, Q8_0 and Q4_0 caches whose splits hold more than 64 positions take
+// attn_mf_kernel instead: the same split, online softmax and output
+// accumulation, with the scores of 16-position tiles on the matrix cores
+// (f16 operands: exact forms of the cache elements and the query as two f16
+// parts; its header below states the exactness argument).
 #include <cmath>
 
 #include "lw_device.hpp"
@@ -40,6 +46,9 @@ namespace {
 struct Name_attn_split_kernel {
     static constexpr const char* base = "attn_split_kernel";
 };
+struct Name_attn_mf_kernel {
+    static constexpr const char* base = "attn_mf_kernel";
+};
 
 constexpr int kAttnWaves = 4;
 constexpr int kAttnThreads = kAttnWaves * kWave;
@@ -48,6 +57,9 @@ constexpr int kAttnThreads = kAttnWaves * kWave;
 #endif
 // batches of raw K/V loads in flight per wave (f16, Q8_0, Q4_0)
 constexpr int kAttnRawBatches = LW_ATTN_RAW_BATCHES;
+// positions per split above which f16, Q8_0 and Q4_0 take the matrix-core
+// score kernel (one round of 64 positions: the vector kernel)
+constexpr int64_t kMfMinRps = 64;
 
 template <int G>
 constexpr int dims_per_lane() {
@@ -188,6 +200,26 @@ struct AttnRaw {
             }
         }
     }
+    // the same from the lane's code bytes cp and its block's scale sp
+    // (f16, Q8_0, Q4_0)
+    __device__ static void load_ptr(const uint8_t* __restrict__ cp, const uint8_t* __restrict__ sp, Raw& x) {
+        static_assert(kOn, "raw formats");
+#pragma unroll
+        for (int k = 0; k < kWords; k += 4) {
+            if constexpr (kWords >= 4) {
+                const uint4 t = *reinterpret_cast<const uint4*>(cp + 4 * k);
+                x.w[k] = t.x;
+                x.w[k + 1] = t.y;
+                x.w[k + 2] = t.z;
+                x.w[k + 3] = t.w;
+            } else {
+                const uint2 t = *reinterpret_cast<const uint2*>(cp);
+                x.w[0] = t.x;
+                x.w[1] = t.y;
+            }
+        }
+        if constexpr (kAffine) x.s = *reinterpret_cast<const uint16_t*>(sp);
+    }
     // sh: the Q4_0 nibble (0 or 4), the same for every row of a lane
     __device__ static void decode(const Raw& x, int sh, float* c, float& a, float& b) {
         a = 1.f;
@@ -215,6 +247,50 @@ struct AttnRaw {
         }
     }
 };
+
+// The G x DPL output partials of a wave (lane (r, c): position r, dimensions
+// c*DPL ..), summed over the wave's positions into row[h][0 .. D): a
+// reduce-scatter leaves a quarter of the sums in each lane, which the first
+// LPR lanes of each 16-lane row store.
+template <int D, int G, int DPL>
+__device__ __forceinline__ void wave_outputs_to_lds(const float* v, float (*row)[D + 2], int lane, int c) {
+    constexpr int N = G * DPL, LPR = D / DPL;
+    float tot[N / 4];
+    reduce_scatter<N, LPR>(v, tot);
+    const int J0 = ((lane >> 4) & 1) * (N / 4) + ((lane >> 5) & 1) * (N / 2);
+    if ((lane & 15) < LPR) {
+#pragma unroll
+        for (int j = 0; j < N / 4; ++j) {
+            const int J = J0 + j;
+            row[J / DPL][c * DPL + J % DPL] = tot[j];
+        }
+    }
+}
+
+// The workgroup's waves merged (red[w][h]: outputs, then m and l; a wave
+// without positions has m = -inf, l = 0, outputs 0) into the split's
+// workspace record out[h][0 .. D + 2).
+template <int D, int G>
+__device__ __forceinline__ void merge_waves(float (*red)[G][D + 2], float* __restrict__ out) {
+    for (int idx = threadIdx.x; idx < G * (D + 2); idx += kAttnThreads) {
+        const int h = idx / (D + 2), d = idx - h * (D + 2);
+        float M = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < kAttnWaves; ++w) M = fmaxf(M, red[w][h][D]);
+        float v = 0.f;
+        if (d == D) {
+            v = M;
+        } else {
+#pragma unroll
+            for (int w = 0; w < kAttnWaves; ++w) {
+                const float mw = red[w][h][D];
+                const float wgt = mw == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mw - M);
+                v = __builtin_fmaf(wgt, red[w][h][d], v);
+            }
+        }
+        out[(int64_t)h * (D + 2) + d] = v;
+    }
+}
 
 template <int FMT, int D, int G>
 __global__ void __launch_bounds__(kAttnThreads)
@@ -375,25 +451,13 @@ __global__ void __launch_bounds__(kAttnThreads)
     }
 
     // the wave's totals: l over all lanes, the outputs over the positions
-    // (the G * DPL sums over the wave's positions: a reduce-scatter leaves a
-    // quarter of them in each lane, which the first LPR lanes of each
-    // 16-lane row store)
     {
-        constexpr int N = G * DPL;
-        float v[N], tot[N / 4];
+        float v[G * DPL];
 #pragma unroll
         for (int h = 0; h < G; ++h)
 #pragma unroll
             for (int i = 0; i < DPL; ++i) v[h * DPL + i] = kAff ? acc[h][i] + accb[h] : acc[h][i];
-        reduce_scatter<N, LPR>(v, tot);
-        const int J0 = ((lane >> 4) & 1) * (N / 4) + ((lane >> 5) & 1) * (N / 2);
-        if ((lane & 15) < LPR) {
-#pragma unroll
-            for (int j = 0; j < N / 4; ++j) {
-                const int J = J0 + j;
-                red[wave][J / DPL][c * DPL + J % DPL] = tot[j];
-            }
-        }
+        wave_outputs_to_lds<D, G, DPL>(v, red[wave], lane, c);
     }
 #pragma unroll
     for (int h = 0; h < G; ++h) {
@@ -406,26 +470,319 @@ __global__ void __launch_bounds__(kAttnThreads)
         }
     }
     __syncthreads();
-    // combine the waves (a wave without positions has m = -inf, l = 0, sums 0)
-    float* out = ws + ((int64_t)split * n_heads + (int64_t)g * G) * (D + 2);
-    for (int idx = threadIdx.x; idx < G * (D + 2); idx += kAttnThreads) {
-        const int h = idx / (D + 2), d = idx - h * (D + 2);
-        float M = -INFINITY;
+    merge_waves<D, G>(red, ws + ((int64_t)split * n_heads + (int64_t)g * G) * (D + 2));
+}
+
+// Scores on the matrix cores (f16, Q8_0 and Q4_0 caches). A wave takes
+// tiles of 16 positions; v_mfma_f32_16x16x32_f16 multiplies the tile's K
+// rows (A: row n = position n of the tile, one 32-element block per
+// instruction) by the query (B: column n < G the high f16 part of head n,
+// column G + n its low part, the other columns zero), so lane (gq, n)
+// receives column n of rows 4gq .. 4gq + 3. Each lane group gq supplies 8
+// elements of every block: f16 and Q8_0 elements 8gq .. 8gq + 7, Q4_0 the low
+// and then the high nibbles of bytes 4gq .. 4gq + 3 (elements 4gq .. and
+// 16 + 4gq ..); the query columns follow the same order.
+//
+// Exactness. Q8_0 codes enter as the f16 1024 + (q + 128) (bits 0x64 and the
+// code with its sign bit flipped, one v_perm per two codes), Q4_0 nibbles as
+// 1024 + c: the accumulator starts at -1152 (Q8_0) or -1032 (Q4_0) times the
+// block's sum of the query part, so it ends at the sum of the query part
+// times the signed code, and the block scale multiplies it afterwards. The
+// query is first scaled by a power of two per head (its largest magnitude
+// into [2^13, 2^14), so no f16 part overflows) and split into high and low
+// f16 parts, 22 significant bits; products are exact in the float32
+// accumulation and the scaling is undone exactly with the score scale.
+// The weights p then go through LDS to the value layout of the vector path
+// (lane (r, c): position r, dimensions c*DPL ..), which accumulates the
+// outputs as the split kernel does.
+template <int FMT, int D, int G>
+__global__ void __launch_bounds__(kAttnThreads)
+    attn_mf_kernel(const float* __restrict__ q, const uint8_t* __restrict__ Kc, const uint8_t* __restrict__ Vc,
+                   int64_t off1, int kv_len, int n_heads, float scale, int rps, float* __restrict__ ws) {
+    typedef _Float16 h16x8 __attribute__((ext_vector_type(8)));
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    static_assert(FMT == LW_F16 || FMT == LW_Q8_0 || FMT == LW_Q4_0, "f16, Q8_0 and Q4_0 caches");
+    static_assert(2 * G <= 16, "high and low parts of every head in 16 columns");
+    constexpr int NBK = D / 32;                          // blocks per row
+    constexpr int DPL = dims_per_lane<G>();
+    constexpr int LPR = D / DPL;                          // value layout: lanes per position
+    constexpr int RPW = kWave / LPR;                      // positions per value batch
+    constexpr int BPT = 16 / RPW;                         // value batches per tile
+    constexpr int KW = FMT == LW_F16 ? 4 : FMT == LW_Q8_0 ? 2 : 1;  // K words per block and lane
+    constexpr int SW = NBK / 2;                           // scale words per row (two f16 each)
+    constexpr bool kScaled = FMT != LW_F16;
+    constexpr float kBias = FMT == LW_Q8_0 ? 1152.0f : 1032.0f;
+    using RW = AttnRaw<FMT, DPL>;
+    using Raw = typename RW::Raw;
+    __shared__ float red[kAttnWaves][G][D + 2];
+    __shared__ float pw[kAttnWaves][16][G];              // the tile's weights [position][head]
+
+    const int g = blockIdx.x, split = blockIdx.y;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int n = lane & 15, gq = lane >> 4;             // score layout
+    const int r = lane / LPR, c = lane - r * LPR;        // value layout
+    const int j0 = split * rps;
+    const int j1 = min(kv_len, j0 + rps);
+    const int64_t head_base = (int64_t)g * kv_len;
+
+    // the query operand, its per-head power-of-two scaling, the bias sums
+    h16x8 bq[NBK];
+    float cb[NBK];
+    float sc;  // column n < G: the score factor scale * log2(e) * 2^-shift
+    {
+        const bool qcol = n < 2 * G;
+        const int hq = n < G ? n : n - G;
+        const float* qh = q + (int64_t)(g * G + (qcol ? hq : 0)) * D;
+        float qf[NBK][8];
 #pragma unroll
-        for (int w = 0; w < kAttnWaves; ++w) M = fmaxf(M, red[w][h][D]);
-        float v = 0.f;
-        if (d == D) {
-            v = M;
-        } else {
+        for (int bk = 0; bk < NBK; ++bk) {
+            const int d0 = 32 * bk + (FMT == LW_Q4_0 ? 4 * gq : 8 * gq);
+            const float4 a = *reinterpret_cast<const float4*>(qh + d0);
+            const float4 b = *reinterpret_cast<const float4*>(qh + d0 + (FMT == LW_Q4_0 ? 16 : 4));
+            qf[bk][0] = a.x;
+            qf[bk][1] = a.y;
+            qf[bk][2] = a.z;
+            qf[bk][3] = a.w;
+            qf[bk][4] = b.x;
+            qf[bk][5] = b.y;
+            qf[bk][6] = b.z;
+            qf[bk][7] = b.w;
+        }
+        float amax = 0.f;
 #pragma unroll
-            for (int w = 0; w < kAttnWaves; ++w) {
-                const float mw = red[w][h][D];
-                const float wgt = mw == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mw - M);
-                v = __builtin_fmaf(wgt, red[w][h][d], v);
+        for (int bk = 0; bk < NBK; ++bk)
+#pragma unroll
+            for (int k = 0; k < 8; ++k) amax = fmaxf(amax, fabsf(qf[bk][k]));
+        amax = fmaxf(amax, partner<16>(amax));
+        amax = fmaxf(amax, partner<32>(amax));  // the head's largest magnitude, in its four lane groups
+        int ex;
+        (void)frexpf(amax, &ex);  // amax < 2^ex (amax = 0: ex = 0)
+        const int shift = 14 - ex;
+        sc = scale * 1.4426950408889634f * ldexpf(1.0f, -shift);
+#pragma unroll
+        for (int bk = 0; bk < NBK; ++bk) {
+            float part = 0.f;
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const float qs = ldexpf(qf[bk][k], shift);  // exact
+                const _Float16 hi = (_Float16)qs;
+                const _Float16 lo = (_Float16)(qs - (float)hi);
+                const _Float16 v = !qcol ? (_Float16)0.0f : n < G ? hi : lo;
+                bq[bk][k] = v;
+                part += (float)v;
+            }
+            part += partner<16>(part);
+            part += partner<32>(part);  // the block's sum of this column's part
+            cb[bk] = kScaled ? -kBias * part : 0.f;
+        }
+    }
+
+    float m_l = -INFINITY, l_l = 0.f;  // lane (gq, n < G): head n's running maximum; its rows' weight sum
+    float acc[G][DPL], accb[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        accb[h] = 0.f;
+#pragma unroll
+        for (int i = 0; i < DPL; ++i) acc[h][i] = 0.f;
+    }
+    const int sh = (c * DPL) & 16 ? 4 : 0;
+
+    struct Tile {
+        uint32_t kw[NBK][KW];     // K: the lane's row, its 8 elements of each block
+        uint32_t ks[4][SW];       // K scales of rows 4gq .. 4gq + 3
+        Raw v[BPT];               // V in the value layout
+    };
+    // per-row byte strides of the code and scale planes, and the lane's
+    // base addresses in this head's rows (row j at base + j * stride)
+    constexpr uint32_t kRowB = FMT == LW_F16 ? 2 * D : FMT == LW_Q8_0 ? D : D / 2;
+    constexpr uint32_t kRowS = 2 * NBK;
+    const uint8_t* kbase = Kc + head_base * kRowB +
+                           (FMT == LW_F16 ? 16 * gq : FMT == LW_Q8_0 ? 8 * gq : 4 * gq);
+    const uint8_t* ksbase = Kc + off1 + head_base * kRowS;
+    const int ce = c * DPL;  // the lane's first dimension in the value layout
+    const uint8_t* vbase = Vc + head_base * kRowB +
+                           (FMT == LW_F16 ? 2 * ce : FMT == LW_Q8_0 ? ce : 16 * (ce >> 5) + (ce & 15));
+    const uint8_t* vsbase = Vc + off1 + head_base * kRowS + 2 * (ce >> 5);
+    const uint32_t jl = (uint32_t)(j1 - 1);
+    auto clamp = [&](int row) __attribute__((always_inline)) {
+        return (uint64_t)min((uint32_t)row, jl);
+    };
+    // a tile: positions b .. b + 15 (rows past the split repeat its last row
+    // and are masked)
+    auto load_tile = [&](int b, Tile& t) __attribute__((always_inline)) {
+        const uint8_t* kp = kbase + clamp(b + n) * kRowB;
+#pragma unroll
+        for (int bk = 0; bk < NBK; ++bk) {
+            if constexpr (FMT == LW_F16) {
+                const uint4 w = *reinterpret_cast<const uint4*>(kp + 64 * bk);
+                t.kw[bk][0] = w.x;
+                t.kw[bk][1] = w.y;
+                t.kw[bk][2] = w.z;
+                t.kw[bk][3] = w.w;
+            } else if constexpr (FMT == LW_Q8_0) {
+                const uint2 w = *reinterpret_cast<const uint2*>(kp + 32 * bk);
+                t.kw[bk][0] = w.x;
+                t.kw[bk][1] = w.y;
+            } else {
+                t.kw[bk][0] = *reinterpret_cast<const uint32_t*>(kp + 16 * bk);
             }
         }
-        out[(int64_t)h * (D + 2) + d] = v;
+        if constexpr (kScaled) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint8_t* sp = ksbase + clamp(b + 4 * gq + i) * kRowS;
+                if constexpr (SW == 2) {
+                    const uint2 w = *reinterpret_cast<const uint2*>(sp);
+                    t.ks[i][0] = w.x;
+                    t.ks[i][1] = w.y;
+                } else {
+                    t.ks[i][0] = *reinterpret_cast<const uint32_t*>(sp);
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < BPT; ++j) {
+            const uint64_t row = clamp(b + j * RPW + r);
+            RW::load_ptr(vbase + row * kRowB, vsbase + row * kRowS, t.v[j]);
+        }
+    };
+    auto use_tile = [&](int b, const Tile& t) __attribute__((always_inline)) {
+        // scores of rows 4gq + i, column n
+        float S[4];
+        if constexpr (FMT == LW_F16) {
+            f32x4 C = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int bk = 0; bk < NBK; ++bk) {
+                const uint32_t w[4] = {t.kw[bk][0], t.kw[bk][1], t.kw[bk][2], t.kw[bk][3]};
+                C = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h16x8, w), bq[bk], C, 0, 0, 0);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) S[i] = C[i];
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) S[i] = 0.f;
+            const uint32_t k64 = 0x64646464u;
+#pragma unroll
+            for (int bk = 0; bk < NBK; ++bk) {
+                uint32_t a[4];
+                if constexpr (FMT == LW_Q8_0) {
+                    const uint32_t w0 = t.kw[bk][0] ^ 0x80808080u, w1 = t.kw[bk][1] ^ 0x80808080u;
+                    a[0] = __builtin_amdgcn_perm(k64, w0, 0x04010400u);
+                    a[1] = __builtin_amdgcn_perm(k64, w0, 0x04030402u);
+                    a[2] = __builtin_amdgcn_perm(k64, w1, 0x04010400u);
+                    a[3] = __builtin_amdgcn_perm(k64, w1, 0x04030402u);
+                } else {
+                    const uint32_t lo = opaque(t.kw[bk][0] & 0x0F0F0F0Fu);
+                    const uint32_t hi = opaque((t.kw[bk][0] >> 4) & 0x0F0F0F0Fu);
+                    a[0] = __builtin_amdgcn_perm(k64, lo, 0x04010400u);
+                    a[1] = __builtin_amdgcn_perm(k64, lo, 0x04030402u);
+                    a[2] = __builtin_amdgcn_perm(k64, hi, 0x04010400u);
+                    a[3] = __builtin_amdgcn_perm(k64, hi, 0x04030402u);
+                }
+                const f32x4 C0 = {cb[bk], cb[bk], cb[bk], cb[bk]};
+                const f32x4 C = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h16x8, a), bq[bk], C0, 0, 0, 0);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const uint32_t sw = t.ks[i][bk >> 1];
+                    const float d = half_bits_to_float((bk & 1) ? sw >> 16 : sw & 0xFFFFu);
+                    S[i] = __builtin_fmaf(d, C[i], S[i]);
+                }
+            }
+        }
+        // the high part's column n plus the low part's column G + n
+        float s[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float tot = S[i] + dpp_move<0x100 + G>(S[i]);  // row_shl: lane n reads lane n + G
+            s[i] = b + 4 * gq + i < j1 ? tot * sc : -INFINITY;
+        }
+        float mx = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
+        mx = fmaxf(mx, partner<16>(mx));
+        mx = fmaxf(mx, partner<32>(mx));  // the tile's maximum of head n (its first row is valid)
+        const float mn = fmaxf(m_l, mx);
+        if (__builtin_amdgcn_ballot_w64(n < G && mn != m_l)) {  // a head's maximum grew
+            const float alpha = __builtin_amdgcn_exp2f(m_l - mn);  // m = -inf: 0; unchanged: 1
+            l_l *= alpha;
+#pragma unroll
+            for (int h = 0; h < G; ++h) {
+                const float ah = __builtin_bit_cast(
+                    float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, alpha), h));  // lane h: head h
+                accb[h] *= ah;
+#pragma unroll
+                for (int i = 0; i < DPL; ++i) acc[h][i] *= ah;
+            }
+        }
+        m_l = mn;
+        float p[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) p[i] = __builtin_amdgcn_exp2f(s[i] - m_l);  // masked: 0
+        l_l += (p[0] + p[1]) + (p[2] + p[3]);
+        if (n < G) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) pw[wave][4 * gq + i][n] = p[i];
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        // outputs: the value layout, BPT batches of RPW positions
+#pragma unroll
+        for (int j = 0; j < BPT; ++j) {
+            float ph[G];
+#pragma unroll
+            for (int h = 0; h < G; ++h) ph[h] = pw[wave][j * RPW + r][h];
+            float vv[DPL], va, vb;
+            RW::decode(t.v[j], sh, vv, va, vb);
+#pragma unroll
+            for (int h = 0; h < G; ++h) {
+                float pa = ph[h];
+                if constexpr (RW::kAffine) {
+                    pa = ph[h] * va;
+                    accb[h] = __builtin_fmaf(ph[h], vb, accb[h]);
+                }
+#pragma unroll
+                for (int i = 0; i < DPL; ++i) acc[h][i] = __builtin_fmaf(pa, vv[i], acc[h][i]);
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    };
+    // tiles b, b + 64, ... of this wave, two in flight (as the split kernel's
+    // sets: unconditional loads, one exit, wave-uniform trip count)
+    constexpr int kTileStep = kAttnWaves * 16;
+    int b = j0 + wave * 16;
+    if (b < j1) {
+        const int nt = (j1 - b + kTileStep - 1) / kTileStep;
+        Tile ta, tb;
+        load_tile(b, ta);
+        for (int t = 2; t <= nt; t += 2) {
+            load_tile(b + kTileStep, tb);
+            use_tile(b, ta);
+            load_tile(b + 2 * kTileStep, ta);
+            use_tile(b + kTileStep, tb);
+            b += 2 * kTileStep;
+        }
+        if (nt & 1) use_tile(b, ta);
     }
+
+    {
+        float v[G * DPL];
+#pragma unroll
+        for (int h = 0; h < G; ++h)
+#pragma unroll
+            for (int i = 0; i < DPL; ++i) v[h * DPL + i] = RW::kAffine ? acc[h][i] + accb[h] : acc[h][i];
+        wave_outputs_to_lds<D, G, DPL>(v, red[wave], lane, c);
+    }
+    // head n's weight sum over the four lane groups; lane h < G (gq = 0) writes head h
+    l_l += partner<16>(l_l);
+    l_l += partner<32>(l_l);
+    if (lane < G) {
+        red[wave][lane][D] = m_l;
+        red[wave][lane][D + 1] = l_l;
+    }
+    __syncthreads();
+    merge_waves<D, G>(red, ws + ((int64_t)split * n_heads + (int64_t)g * G) * (D + 2));
 }
 
 // out[h][d] = sum_s exp(m_s - M) acc_s[d] / sum_s exp(m_s - M) l_s. One
@@ -498,9 +855,22 @@ template <int FMT, int D, int G>
 hipError_t launch_g(const float* q, const uint8_t* K, const uint8_t* V, float* out, int64_t n_heads, int64_t n_kv,
                     int64_t kv_len, float scale, const AttnPlan& pl, float* ws, hipStream_t stream) {
     const Planes p = planes_of(FMT, n_kv * kv_len * D);
-    if (query_only(kernel_name<Name_attn_split_kernel, FMT, D, G>(), 2)) return hipSuccess;
-    hipLaunchKernelGGL((attn_split_kernel<FMT, D, G>), dim3((unsigned)n_kv, (unsigned)pl.splits), dim3(kAttnThreads),
-                       0, stream, q, K, V, p.off1, p.off2, p.off3, (int)kv_len, (int)n_heads, scale, (int)pl.rps, ws);
+    // f16, Q8_0 and Q4_0 caches with more than one 64-position round per
+    // workgroup: scores on the matrix cores (with a single round its query
+    // preparation is not repaid)
+    constexpr bool kMf = FMT == LW_F16 || FMT == LW_Q8_0 || FMT == LW_Q4_0;
+    if (kMf && pl.rps > kMfMinRps) {
+        constexpr int FM = kMf ? FMT : LW_F16;  // instantiated for the three formats only
+        if (query_only(kernel_name<Name_attn_mf_kernel, FM, D, G>(), 2)) return hipSuccess;
+        hipLaunchKernelGGL((attn_mf_kernel<FM, D, G>), dim3((unsigned)n_kv, (unsigned)pl.splits),
+                           dim3(kAttnThreads), 0, stream, q, K, V, p.off1, (int)kv_len, (int)n_heads, scale,
+                           (int)pl.rps, ws);
+    } else {
+        if (query_only(kernel_name<Name_attn_split_kernel, FMT, D, G>(), 2)) return hipSuccess;
+        hipLaunchKernelGGL((attn_split_kernel<FMT, D, G>), dim3((unsigned)n_kv, (unsigned)pl.splits),
+                           dim3(kAttnThreads), 0, stream, q, K, V, p.off1, p.off2, p.off3, (int)kv_len, (int)n_heads,
+                           scale, (int)pl.rps, ws);
+    }
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     hipLaunchKernelGGL((attn_combine_kernel<D>), dim3((unsigned)n_heads), dim3(kCombThreads), 0, stream, ws, out,

@@ -313,6 +313,22 @@ int64_t lw_attn_workspace_bytes(int fmt, int64_t n_heads, int64_t n_kv_heads, in
     return lw::attn_plan(n_kv_heads, head_dim, kv_len, n_heads).ws_bytes;
 }
 
+const char* lw_attn_kernel_name(int fmt, int64_t n_heads, int64_t n_kv_heads, int64_t head_dim, int64_t kv_len) {
+    if (lw::check_attn(fmt, n_heads, n_kv_heads, head_dim, kv_len, 1.0f) != LW_OK) return nullptr;
+    const lw::AttnPlan pl = lw::attn_plan(n_kv_heads, head_dim, kv_len, n_heads);
+    lw::LaunchQuery& q = lw::launch_query();
+    q.active = true;
+    q.name = nullptr;
+    q.count = 0;
+    alignas(256) static const uint8_t stand_in[256] = {};
+    float* fs = reinterpret_cast<float*>(const_cast<uint8_t*>(stand_in));
+    const hipError_t err = lw::launch_attn(fmt, fs, stand_in, stand_in, fs, n_heads, n_kv_heads, head_dim, kv_len,
+                                           1.0f, pl, fs, nullptr);
+    const char* name = q.name;
+    q.active = false;
+    return err == hipSuccess ? name : nullptr;
+}
+
 int lw_attn_decode(int fmt, const float* q, const void* K, const void* V, float* out, int64_t n_heads,
                    int64_t n_kv_heads, int64_t head_dim, int64_t kv_len, float scale, void* workspace,
                    int64_t workspace_bytes, void* stream) {

@@ -1,5 +1,4 @@
-// Prefill product on the matrix cores (many tokens; every quantized format
-// but q1_0).
+// Prefill product on the matrix cores (many tokens; every quantized format).
 //
 // Y[t][r] = sum_k value(W, r*K + k) * X[t][k]. With many tokens the product is
 // a contraction over K with a token dimension, so it runs on the matrix cores
@@ -12,7 +11,8 @@
 //
 // Precision. The weight operand holds exact bfloat16 values derived from the
 // integer codes only: the biased code 128 + q (bits 0x4300 | q, q < 64) for
-// the formats with an offset, the code q for Q8_0, the e2m1 value for MXFP4.
+// the formats with an offset, the code q for Q8_0, the e2m1 value for MXFP4,
+// +-1 for q1_0.
 // X is split into bf16 high and low parts (x = hi + lo to 2^-17 relative),
 // two MFMAs per tile and K-step, float32 accumulation. A coefficient unit
 // (a 32-element block, or a 16-element sub-block for Q6_K and Q2_K) applies
@@ -23,7 +23,7 @@
 //   Q4_K, Q5_K:  y += d*sc * P - (128*d*sc + dmin*m) * S
 //   Q6_K:   y += d*sc * P - 160 * d*sc * S       (128 + q = (q - 32) + 160)
 //   Q2_K:   y += d*sc * P - (128*d*sc + dmin*m) * S
-//   Q8_0:   y += d * P;   MXFP4:  y += 2^(E - 127) * P
+//   Q8_0, q1_0:  y += d * P;   MXFP4:  y += 2^(E - 127) * P
 // where S = sum over the unit of (hi + lo), the very values fed to the
 // matrix core, so the bias cancels to float32 rounding. The error relative
 // to sum_k |w * x| stays near 1e-5.

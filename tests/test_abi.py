@@ -9,7 +9,7 @@ import pytest
 
 import golden_io
 from paper_2605_20706_amd import binding, layout
-from paper_2605_20706_amd.layout import F16, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
+from paper_2605_20706_amd.layout import F16, MXFP4, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 LW_OK, LW_EINVAL, LW_EFMT, LW_ESHAPE, LW_EALIGN = 0, -1, -2, -3, -4
@@ -366,6 +366,22 @@ def test_attn_errors_and_workspace(lib):
     assert wb > 0 and wb % (32 * 130 * 4) == 0
     assert binding.attn_workspace_bytes(Q8_0, 32, 8, 128, 1) == 32 * 130 * 4   # one split
     assert lib.lw_attn_workspace_bytes(Q4_K, 32, 8, 128, 16) == LW_EFMT
+
+
+def test_attn_kernel_routing(lib):
+    """f16, Q8_0 and Q4_0 caches take the matrix-core score kernel when the
+    split leaves more than 64 positions per workgroup (32 heads over 8:
+    64 splits from 4096 positions on), the other formats the vector kernel."""
+    name = binding.attn_kernel_name
+    assert name(Q8_0, 32, 8, 128, 2048) == "attn_split_kernel<1, 128, 4>"     # 32 splits of 64
+    assert name(Q8_0, 32, 8, 128, 4096) == "attn_split_kernel<1, 128, 4>"     # 64 splits of 64
+    assert name(Q8_0, 32, 8, 128, 4160) == "attn_mf_kernel<1, 128, 4>"        # 64 splits of 65
+    assert name(F16, 64, 8, 64, 32768) == "attn_mf_kernel<0, 64, 8>"
+    assert name(Q4_0, 8, 8, 128, 8192) == "attn_mf_kernel<2, 128, 1>"
+    assert name(Q4_1, 32, 8, 128, 32768) == "attn_split_kernel<4, 128, 4>"
+    assert name(MXFP4, 32, 8, 128, 32768) == "attn_split_kernel<11, 128, 4>"
+    assert name(Q4_K, 32, 8, 128, 32768) is None
+    assert name(Q8_0, 12, 8, 128, 2048) is None
 
 
 def _ws_bytes(M, K, n_tok, ks):

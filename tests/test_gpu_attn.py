@@ -61,6 +61,43 @@ def test_attn_peaked_and_flat(oracle_mod, fmt):
     check(oracle_mod, fmt, np.zeros((H, D), np.float32), Kc, Vc, H, n_kv, D, L, 1 / np.sqrt(D), "flat")
 
 
+MF_FMTS = [F16, Q8_0, Q4_0]
+
+
+@pytest.mark.parametrize("fmt", MF_FMTS)
+@pytest.mark.parametrize("H,n_kv,D,L", [(8, 8, 128, 4160), (16, 8, 128, 9000), (32, 8, 128, 12345),
+                                        (64, 8, 128, 9000), (32, 8, 64, 9000), (64, 8, 64, 5000),
+                                        (16, 2, 64, 20000), (4, 1, 128, 40000)])
+def test_attn_matrix_core_scores(oracle_mod, fmt, H, n_kv, D, L):
+    """The matrix-core score kernel (more than 64 positions per split) over
+    every head ratio and head size: 65-position splits whose last tile holds
+    one position, ragged last splits, one key/value head."""
+    assert binding.attn_kernel_name(fmt, H, n_kv, D, L).startswith("attn_mf_kernel")
+    Kc, Vc = make(fmt, n_kv, L, D, 21), make(fmt, n_kv, L, D, 22)
+    q = np.random.default_rng([23, H, D]).standard_normal((H, D)).astype(np.float32)
+    r, nmse = check(oracle_mod, fmt, q, Kc, Vc, H, n_kv, D, L, 1 / np.sqrt(D), (fmt, H, n_kv, D, L))
+    print("  bound ratio %.3g NMSE %.3g" % (r, nmse), flush=True)
+
+
+@pytest.mark.parametrize("fmt", MF_FMTS)
+def test_attn_matrix_core_query_range(oracle_mod, fmt):
+    """The query's per-head power-of-two scaling of the matrix-core kernel:
+    queries scaled by 2^60 and 2^-60, one with elements spread over 2^-20 ..
+    2^20 within a head, peaked and zero queries."""
+    H, n_kv, D, L = 32, 8, 128, 9000
+    assert binding.attn_kernel_name(fmt, H, n_kv, D, L).startswith("attn_mf_kernel")
+    Kc, Vc = make(fmt, n_kv, L, D, 24), make(fmt, n_kv, L, D, 25)
+    rng = np.random.default_rng(26)
+    q = rng.standard_normal((H, D)).astype(np.float32)
+    spread = (q * np.exp2(rng.integers(-20, 21, (H, D)))).astype(np.float32)
+    sc = 1 / np.sqrt(D)
+    check(oracle_mod, fmt, (q * 2.0 ** 60).astype(np.float32), Kc, Vc, H, n_kv, D, L, sc * 2.0 ** -60, "2^60")
+    check(oracle_mod, fmt, (q * 2.0 ** -60).astype(np.float32), Kc, Vc, H, n_kv, D, L, sc * 2.0 ** 60, "2^-60")
+    check(oracle_mod, fmt, spread, Kc, Vc, H, n_kv, D, L, sc * 2.0 ** -16, "spread")
+    check(oracle_mod, fmt, (q * 16).astype(np.float32), Kc, Vc, H, n_kv, D, L, sc, "peaked")
+    check(oracle_mod, fmt, np.zeros((H, D), np.float32), Kc, Vc, H, n_kv, D, L, sc, "flat")
+
+
 def test_attn_stream_and_workspace_reuse(oracle_mod):
     """Two calls on one stream sharing a workspace, the second smaller; each
     output matches the oracle."""
