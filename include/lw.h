@@ -373,10 +373,10 @@ LW_API const char* lw_attn_kernel_name(int fmt, int64_t n_heads, int64_t n_kv_he
  * lw_attn_decode_noalloc — lw_attn_decode without a workspace argument, for
  * callers that cannot allocate device memory (code under HIP graph capture,
  * tight serving loops, harnesses that forbid allocation). It allocates
- * nothing: the partial results go to a fixed 4 MiB array of the library's
+ * nothing: the partial results go to a fixed 2 MiB array of the library's
  * own on each GPU (held until the process ends), so calls whose
- * lw_attn_workspace_bytes exceeds 4 MiB return LW_EINVAL (32 heads over 8
- * key/value heads of 128 need about 1 MiB at any length). Every call on a
+ * lw_attn_workspace_bytes exceeds 2 MiB return LW_EINVAL (32 heads over 8
+ * key/value heads of 128 need about 0.5 MiB at any length). Every call on a
  * GPU shares that GPU's array: calls that overlap in time on one GPU race.
  * Arguments, checks and results otherwise as lw_attn_decode's.
  */

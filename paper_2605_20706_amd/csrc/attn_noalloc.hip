@@ -17,7 +17,7 @@
 
 namespace {
 
-constexpr int64_t kAttnScratchBytes = 4 << 20;  // 4 MiB per GPU
+constexpr int64_t kAttnScratchBytes = 2 << 20;  // 2 MiB per GPU
 constexpr int kMaxDevices = 64;
 
 static __device__ __align__(256) unsigned char scratch[kAttnScratchBytes];

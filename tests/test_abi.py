@@ -371,11 +371,11 @@ def test_attn_errors_and_workspace(lib):
 def test_attn_kernel_routing(lib):
     """f16, Q8_0 and Q4_0 caches take the matrix-core score kernel when the
     split leaves more than 64 positions per workgroup (32 heads over 8:
-    64 splits from 4096 positions on), the other formats the vector kernel."""
+    32 splits from 2048 positions on), the other formats the vector kernel."""
     name = binding.attn_kernel_name
+    assert name(Q8_0, 32, 8, 128, 1000) == "attn_split_kernel<1, 128, 4>"     # 16 splits of 63
     assert name(Q8_0, 32, 8, 128, 2048) == "attn_split_kernel<1, 128, 4>"     # 32 splits of 64
-    assert name(Q8_0, 32, 8, 128, 4096) == "attn_split_kernel<1, 128, 4>"     # 64 splits of 64
-    assert name(Q8_0, 32, 8, 128, 4160) == "attn_mf_kernel<1, 128, 4>"        # 64 splits of 65
+    assert name(Q8_0, 32, 8, 128, 2080) == "attn_mf_kernel<1, 128, 4>"        # 32 splits of 65
     assert name(F16, 64, 8, 64, 32768) == "attn_mf_kernel<0, 64, 8>"
     assert name(Q4_0, 8, 8, 128, 8192) == "attn_mf_kernel<2, 128, 1>"
     assert name(Q4_1, 32, 8, 128, 32768) == "attn_split_kernel<4, 128, 4>"

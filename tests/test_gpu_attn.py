@@ -65,7 +65,7 @@ MF_FMTS = [F16, Q8_0, Q4_0]
 
 
 @pytest.mark.parametrize("fmt", MF_FMTS)
-@pytest.mark.parametrize("H,n_kv,D,L", [(8, 8, 128, 4160), (16, 8, 128, 9000), (32, 8, 128, 12345),
+@pytest.mark.parametrize("H,n_kv,D,L", [(8, 8, 128, 2080), (16, 8, 128, 9000), (32, 8, 128, 12345),
                                         (64, 8, 128, 9000), (32, 8, 64, 9000), (64, 8, 64, 5000),
                                         (16, 2, 64, 20000), (4, 1, 128, 40000)])
 def test_attn_matrix_core_scores(oracle_mod, fmt, H, n_kv, D, L):

@@ -2,7 +2,7 @@
 partials in the library's fixed per-GPU array) against lw_attn_decode with a
 caller workspace, through the C ABI: two calls in a row, the second smaller,
 each bit for bit the workspace call's output and within the oracle's bound;
-and a call needing more than the array's 4 MiB is refused before any launch."""
+and a call needing more than the array's 2 MiB is refused before any launch."""
 import ctypes
 
 import numpy as np
@@ -51,9 +51,9 @@ def test_noalloc_matches_workspace_call(oracle_mod):
 
 def test_noalloc_refuses_beyond_its_array():
     lib = binding.library()
-    # 4088 heads over 511 key/value heads of 128 at 4096 positions: two splits of 4088 x 130 floats,
-    # above the array's 4 MiB; refused by the size check, before any pointer is used or kernel launched
-    assert binding.attn_workspace_bytes(Q8_0, 4088, 511, 128, 4096) > 4 << 20
+    # 4088 heads over 511 key/value heads of 128 at 4096 positions: one split of 4088 x 130 floats,
+    # above the array's 2 MiB; refused by the size check, before any pointer is used or kernel launched
+    assert binding.attn_workspace_bytes(Q8_0, 4088, 511, 128, 4096) > 2 << 20
     A256, A16 = 0x7F0000000000, 0x7F0000000010
     rc = lib.lw_attn_decode_noalloc(Q8_0, A16, A256, A256, A16, 4088, 511, 128, 4096, ctypes.c_float(0.1), None)
     assert rc == LW_EINVAL
