@@ -52,11 +52,9 @@ struct Name_attn_mf_kernel {
 
 constexpr int kAttnWaves = 4;
 constexpr int kAttnThreads = kAttnWaves * kWave;
-#ifndef LW_ATTN_RAW_BATCHES
-#define LW_ATTN_RAW_BATCHES 2
-#endif
-// batches of raw K/V loads in flight per wave (f16, Q8_0, Q4_0)
-constexpr int kAttnRawBatches = LW_ATTN_RAW_BATCHES;
+// batches per set of the vector kernel's raw K/V loads (f16, Q8_0, Q4_0):
+// four would take more than 256 registers with four heads per KV head
+constexpr int kAttnRawBatches = 2;
 // positions per split above which f16, Q8_0 and Q4_0 take the matrix-core
 // score kernel (one round of 64 positions: the vector kernel)
 constexpr int64_t kMfMinRps = 64;
