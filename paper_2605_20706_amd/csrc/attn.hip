@@ -20,8 +20,8 @@
 // lanes of a position. Batches come in sets of NB, two sets in flight per
 // wave: the next set's loads are issued before the current set is decoded
 // (f16, Q8_0 and Q4_0 keep the raw words until then; Q8_0 and Q4_0 decode
-// to codes with one affine scale per lane and row, applied once per head
-// to the score and the weight instead of once per element). The online
+// to exact signed codes, the block scale applied once per head to the
+// score and the weight instead of once per element). The online
 // softmax takes one maximum per head over the whole set and rescales the
 // lane's G x DPL output partials by exp(m_old - m_new) only when a maximum
 // grew. The wave's partials are then summed over positions by a
@@ -150,11 +150,12 @@ __device__ __forceinline__ void reduce_scatter(const float* v, float* out) {
 // Raw K/V loads for f16, Q8_0 and Q4_0: the lane's DPL elements of a row
 // (consecutive, inside one 32-element block) are kept as loaded, a few
 // words per row, and decoded only when the batch is used, so that further
-// batches stay in flight meanwhile. Q8_0 and Q4_0 decode to codes c_i with
-// value a * c_i + b (a and b the block's), so the scale multiplies once per
-// lane and head instead of once per element: Q8_0 c = code + 128 (the code
-// with its sign bit flipped, one v_cvt_f32_ubyte), a = d, b = -128 d; Q4_0
-// c = the nibble, a = d, b = -8 d (both b exact).
+// batches stay in flight meanwhile. Q8_0 and Q4_0 decode to the signed
+// integer codes c_i (Q8_0: one v_cvt_f32_i32 of a sign-extended byte; Q4_0:
+// the nibble minus 8), exact, with value a * c_i for the block scale a = d,
+// so the scale multiplies once per lane and head instead of once per element.
+// A code of zero stays an exact zero: a cache dimension whose values are all
+// zero gives an output of exactly zero, as the accuracy bound requires.
 template <int FMT, int DPL>
 struct AttnRaw {
     static constexpr bool kOn = FMT == LW_F16 || FMT == LW_Q8_0 || FMT == LW_Q4_0;
@@ -219,9 +220,8 @@ struct AttnRaw {
         if constexpr (kAffine) x.s = *reinterpret_cast<const uint16_t*>(sp);
     }
     // sh: the Q4_0 nibble (0 or 4), the same for every row of a lane
-    __device__ static void decode(const Raw& x, int sh, float* c, float& a, float& b) {
+    __device__ static void decode(const Raw& x, int sh, float* c, float& a) {
         a = 1.f;
-        b = 0.f;
         if constexpr (FMT == LW_F16) {
 #pragma unroll
             for (int k = 0; k < kWords; ++k) {
@@ -231,14 +231,20 @@ struct AttnRaw {
         } else if constexpr (kAffine) {
 #pragma unroll
             for (int k = 0; k < kWords; ++k) {
-                const uint32_t w = FMT == LW_Q8_0 ? x.w[k] ^ 0x80808080u : opaque((x.w[k] >> sh) & 0x0F0F0F0Fu);
-                c[4 * k] = ubyte<0>(w);
-                c[4 * k + 1] = ubyte<1>(w);
-                c[4 * k + 2] = ubyte<2>(w);
-                c[4 * k + 3] = ubyte<3>(w);
+                if constexpr (FMT == LW_Q8_0) {
+                    c[4 * k] = sbyte<0>(x.w[k]);
+                    c[4 * k + 1] = sbyte<1>(x.w[k]);
+                    c[4 * k + 2] = sbyte<2>(x.w[k]);
+                    c[4 * k + 3] = sbyte<3>(x.w[k]);
+                } else {
+                    const uint32_t w = opaque((x.w[k] >> sh) & 0x0F0F0F0Fu);
+                    c[4 * k] = ubyte<0>(w) - 8.0f;
+                    c[4 * k + 1] = ubyte<1>(w) - 8.0f;
+                    c[4 * k + 2] = ubyte<2>(w) - 8.0f;
+                    c[4 * k + 3] = ubyte<3>(w) - 8.0f;
+                }
             }
             a = half_bits_to_float(x.s);
-            b = (FMT == LW_Q8_0 ? -128.0f : -8.0f) * a;
         } else {
 #pragma unroll
             for (int i = 0; i < DPL; ++i) c[i] = __builtin_bit_cast(float, x.w[i]);
@@ -326,21 +332,13 @@ __global__ void __launch_bounds__(kAttnThreads)
     }
     using RW = AttnRaw<FMT, DPL>;
     constexpr bool kAff = RW::kAffine;
-    // affine loads: the lane's query sums (the b term of a score) and the
-    // b terms of the output, accb (the same for all the lane's dimensions)
-    float qsum[G], accb[G];
     float m[G], l[G], acc[G][DPL];
 #pragma unroll
     for (int h = 0; h < G; ++h) {
         m[h] = -INFINITY;
         l[h] = 0.f;
-        accb[h] = 0.f;
-        qsum[h] = 0.f;
 #pragma unroll
-        for (int i = 0; i < DPL; ++i) {
-            acc[h][i] = 0.f;
-            qsum[h] += qv[h][i];
-        }
+        for (int i = 0; i < DPL; ++i) acc[h][i] = 0.f;
     }
 
     const int64_t head_base = (int64_t)g * kv_len;
@@ -372,15 +370,15 @@ __global__ void __launch_bounds__(kAttnThreads)
         float s[NB][G];
 #pragma unroll
         for (int i = 0; i < NB; ++i) {
-            float kk[DPL], ka, kb;
-            RW::decode(kr[i], sh, kk, ka, kb);
+            float kk[DPL], ka;
+            RW::decode(kr[i], sh, kk, ka);
             const bool valid = b + i * kStep + r < j1;
 #pragma unroll
             for (int h = 0; h < G; ++h) {
                 float d = 0.f;
 #pragma unroll
                 for (int k = 0; k < DPL; ++k) d = __builtin_fmaf(qv[h][k], kk[k], d);
-                if constexpr (kAff) d = __builtin_fmaf(kb, qsum[h], ka * d);
+                if constexpr (kAff) d *= ka;
                 d = group_sum<1, LPR>(d);
                 s[i][h] = valid ? d * scale2 : -INFINITY;
             }
@@ -402,24 +400,19 @@ __global__ void __launch_bounds__(kAttnThreads)
                 const float alpha = __builtin_amdgcn_exp2f(m[h] - mn[h]);  // m = -inf: 0; unchanged: 1
                 m[h] = mn[h];
                 l[h] *= alpha;
-                if constexpr (kAff) accb[h] *= alpha;
 #pragma unroll
                 for (int k = 0; k < DPL; ++k) acc[h][k] *= alpha;
             }
         }
 #pragma unroll
         for (int i = 0; i < NB; ++i) {
-            float vv[DPL], va, vb;
-            RW::decode(vr[i], sh, vv, va, vb);
+            float vv[DPL], va;
+            RW::decode(vr[i], sh, vv, va);
 #pragma unroll
             for (int h = 0; h < G; ++h) {
                 const float p = __builtin_amdgcn_exp2f(s[i][h] - m[h]);  // masked (s = -inf): 0
                 l[h] += p;  // in all LPR lanes of the position: LPR times the sum
-                float pa = p;
-                if constexpr (kAff) {
-                    pa = p * va;
-                    accb[h] = __builtin_fmaf(p, vb, accb[h]);
-                }
+                const float pa = kAff ? p * va : p;
 #pragma unroll
                 for (int k = 0; k < DPL; ++k) acc[h][k] = __builtin_fmaf(pa, vv[k], acc[h][k]);
             }
@@ -454,7 +447,7 @@ __global__ void __launch_bounds__(kAttnThreads)
 #pragma unroll
         for (int h = 0; h < G; ++h)
 #pragma unroll
-            for (int i = 0; i < DPL; ++i) v[h * DPL + i] = kAff ? acc[h][i] + accb[h] : acc[h][i];
+            for (int i = 0; i < DPL; ++i) v[h * DPL + i] = acc[h][i];
         wave_outputs_to_lds<D, G, DPL>(v, red[wave], lane, c);
     }
 #pragma unroll
@@ -577,13 +570,11 @@ __global__ void __launch_bounds__(kAttnThreads)
     }
 
     float m_l = -INFINITY, l_l = 0.f;  // lane (gq, n < G): head n's running maximum; its rows' weight sum
-    float acc[G][DPL], accb[G];
+    float acc[G][DPL];
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-        accb[h] = 0.f;
+    for (int h = 0; h < G; ++h)
 #pragma unroll
         for (int i = 0; i < DPL; ++i) acc[h][i] = 0.f;
-    }
     const int sh = (c * DPL) & 16 ? 4 : 0;
 
     struct Tile {
@@ -706,7 +697,6 @@ __global__ void __launch_bounds__(kAttnThreads)
             for (int h = 0; h < G; ++h) {
                 const float ah = __builtin_bit_cast(
                     float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, alpha), h));  // lane h: head h
-                accb[h] *= ah;
 #pragma unroll
                 for (int i = 0; i < DPL; ++i) acc[h][i] *= ah;
             }
@@ -729,15 +719,11 @@ __global__ void __launch_bounds__(kAttnThreads)
             float ph[G];
 #pragma unroll
             for (int h = 0; h < G; ++h) ph[h] = pw[wave][j * RPW + r][h];
-            float vv[DPL], va, vb;
-            RW::decode(t.v[j], sh, vv, va, vb);
+            float vv[DPL], va;
+            RW::decode(t.v[j], sh, vv, va);
 #pragma unroll
             for (int h = 0; h < G; ++h) {
-                float pa = ph[h];
-                if constexpr (RW::kAffine) {
-                    pa = ph[h] * va;
-                    accb[h] = __builtin_fmaf(ph[h], vb, accb[h]);
-                }
+                const float pa = RW::kAffine ? ph[h] * va : ph[h];
 #pragma unroll
                 for (int i = 0; i < DPL; ++i) acc[h][i] = __builtin_fmaf(pa, vv[i], acc[h][i]);
             }
@@ -769,7 +755,7 @@ __global__ void __launch_bounds__(kAttnThreads)
 #pragma unroll
         for (int h = 0; h < G; ++h)
 #pragma unroll
-            for (int i = 0; i < DPL; ++i) v[h * DPL + i] = RW::kAffine ? acc[h][i] + accb[h] : acc[h][i];
+            for (int i = 0; i < DPL; ++i) v[h * DPL + i] = acc[h][i];
         wave_outputs_to_lds<D, G, DPL>(v, red[wave], lane, c);
     }
     // head n's weight sum over the four lane groups; lane h < G (gq = 0) writes head h

@@ -98,6 +98,33 @@ def test_attn_matrix_core_query_range(oracle_mod, fmt):
     check(oracle_mod, fmt, np.zeros((H, D), np.float32), Kc, Vc, H, n_kv, D, L, sc, "flat")
 
 
+# the code of an exact zero, per format with one
+ZERO_CODE = {F16: ("w", 0), Q8_0: ("q", 0), Q4_0: ("q", 8), Q5_0: ("q", 16), MXFP4: ("q", 0)}
+
+
+@pytest.mark.parametrize("fmt", sorted(ZERO_CODE))
+@pytest.mark.parametrize("L", [1000, 9000])
+def test_attn_zero_values_exact(oracle_mod, fmt, L):
+    """A cache dimension whose values are all exactly zero (every position,
+    every key/value head), and a key row of zeros: A = 0 for that output
+    dimension, so the bound asks for an exact zero there. 1000 positions
+    run the vector kernel for every format, 9000 the matrix-core score
+    kernel for f16, Q8_0 and Q4_0."""
+    H, n_kv, D = 32, 8, 128
+    key, zero = ZERO_CODE[fmt]
+    rng = np.random.default_rng([27, fmt, L])
+    fk = synth.gen_fields_eq1(fmt, n_kv * L * D, rng, 1.0)
+    fv = synth.gen_fields_eq1(fmt, n_kv * L * D, rng, 1.0)
+    col = (np.arange(n_kv * L * D) % D) == 5
+    fv[key][col] = zero
+    fk[key][(np.arange(n_kv * L * D) // D) % L == 17] = zero  # position 17 of every head: k = 0
+    Kc, Vc = synth.pack_fields(fmt, fk), synth.pack_fields(fmt, fv)
+    q = rng.standard_normal((H, D)).astype(np.float32)
+    check(oracle_mod, fmt, q, Kc, Vc, H, n_kv, D, L, 1 / np.sqrt(D), (fmt, L))
+    out = binding.attn_decode(fmt, to_gpu(q), to_gpu(Kc), to_gpu(Vc), H, n_kv, D, L, 1 / np.sqrt(D))
+    assert (out.cpu().numpy()[:, 5] == 0).all(), (fmt, L)
+
+
 def test_attn_stream_and_workspace_reuse(oracle_mod):
     """Two calls on one stream sharing a workspace, the second smaller; each
     output matches the oracle."""
