@@ -380,7 +380,8 @@ def stored_traffic(workload, n_tok, kernel):
 
 def traffic_method(workload, n_tok):
     """How the stored traffic figure was taken: the counters and the
-    calibration factors (from one plain 1 GiB elementwise copy)."""
+    calibration factors (a plain 1 GiB elementwise copy, confirmed by a 1 GiB
+    read of the 128-bit non-temporal read kernel)."""
     path = os.path.join(ROOT, "profiles", "hbm_traffic_%s_nt%d.txt" % (workload, n_tok))
     if not os.path.exists(path):
         return None
@@ -388,7 +389,8 @@ def traffic_method(workload, n_tok):
         for line in fh:
             if "bytes = FETCH_SIZE" in line:
                 return ("rocprofv3 --pmc, one counter per run; " + line.strip("# \n")
-                        + "; factors from one 1 GiB elementwise copy (%s)" % os.path.relpath(path, ROOT))
+                        + "; factors from a 1 GiB elementwise copy, confirmed by a 1 GiB 128-bit read (%s)"
+                        % os.path.relpath(path, ROOT))
     return None
 
 
@@ -862,6 +864,9 @@ def main():
                          "(the committed copy is profiles/sweep_select.json, which generates the table)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain copy kernel over MIB MiB 20 times (HBM counter calibration)")
+    ap.add_argument("--calibrate-read", type=int, default=0, metavar="MIB",
+                    help="only run libceiling's 128-bit non-temporal read kernel over MIB MiB 20 times "
+                         "(a second, read-only HBM counter calibration)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -889,6 +894,25 @@ def main():
             torch.neg(src, out=dst)  # a plain elementwise kernel: reads n bytes, writes n bytes
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes": n, "copies": 20}))
+        return
+
+    if args.calibrate_read:
+        # reads exactly n bytes per launch and writes nothing (the sink word
+        # is stored only if the folded value hits a fixed constant)
+        import ctypes
+        n = args.calibrate_read * (1 << 20)
+        lib = ctypes.CDLL(os.path.join(ROOT, "paper_2605_20706_amd", "libceiling.so"))
+        lib.lw_ceiling_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+        torch.cuda.synchronize()
+        s = torch.cuda.current_stream().cuda_stream
+        for _ in range(20):
+            rc = lib.lw_ceiling_read(src.data_ptr(), n, sink.data_ptr(), s)
+            if rc != 0:
+                raise RuntimeError("libceiling: code %d" % rc)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_read_bytes": n, "reads": 20}))
         return
 
     if args.op == "attn":
