@@ -264,6 +264,49 @@ __device__ __forceinline__ float bit_dot(uint32_t w, const float4* xv) {
     return (lo_s + hi_s) * 16777216.0f;  // 2^24
 }
 
+// One AND per bit pair for the 1-bit format. A single set bit i < 12 of a
+// binary16 half is exactly 2^(i - 24) (bits 0..9 subnormal, bits 10 and 11
+// the lowest exponent bits); bits 12..15, shifted down by 4, are bits 8..11.
+// So with the lane's x pre-multiplied by 2^-s(e), s(e) = e mod 16 below 12
+// and e mod 16 - 4 from 12 (q1_prescale, exact: powers of two), the masked
+// bit times the pre-scaled x is b * x * 2^-24, the same product bit_dot
+// forms. 16 ANDs and one shift per 32 bits instead of 16 shifts and 16 ANDs.
+__device__ __forceinline__ int q1_shift(int e) {
+    const int i = e & 15;
+    return i < 12 ? i : i - 4;
+}
+
+__device__ __forceinline__ void q1_prescale(float4* xv) {  // the lane's 8 float4 (32 elements)
+#pragma unroll
+    for (int j4 = 0; j4 < 8; ++j4) {
+        xv[j4].x = __builtin_ldexpf(xv[j4].x, -q1_shift(4 * j4 + 0));
+        xv[j4].y = __builtin_ldexpf(xv[j4].y, -q1_shift(4 * j4 + 1));
+        xv[j4].z = __builtin_ldexpf(xv[j4].z, -q1_shift(4 * j4 + 2));
+        xv[j4].w = __builtin_ldexpf(xv[j4].w, -q1_shift(4 * j4 + 3));
+    }
+}
+
+// The mask of bit pair i (elements i and 16 + i) of w, w4 = w >> 4.
+__device__ __forceinline__ uint32_t q1_mask(uint32_t w, uint32_t w4, int i) {
+    return opaque((i < 12 ? w : w4) & (0x00010001u << q1_shift(i)));
+}
+
+// bit_dot over pre-scaled x (q1_prescale)
+__device__ __forceinline__ float bit_dot_pre(uint32_t w, const float4* xv) {
+    float lo_s = 0.f, hi_s = 0.f;
+    const uint32_t w4 = w >> 4;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+        const uint32_t m = q1_mask(w, w4, i);
+        const float4& xl = xv[i >> 2];
+        const float4& xh = xv[4 + (i >> 2)];
+        const int c = i & 3;
+        lo_s = __builtin_fmaf(half_of<0>(m), c == 0 ? xl.x : c == 1 ? xl.y : c == 2 ? xl.z : xl.w, lo_s);
+        hi_s = __builtin_fmaf(half_of<1>(m), c == 0 ? xh.x : c == 1 ? xh.y : c == 2 ? xh.z : xh.w, hi_s);
+    }
+    return (lo_s + hi_s) * 16777216.0f;  // 2^24
+}
+
 // q1_0 (Sec. 2.2: one bit per weight, one binary16 scale per 128): a lane
 // holds 32 consecutive bits (one 32-bit word; a wave-wide load is 256
 // contiguous bytes) and its block's scale, shared by four lanes.
@@ -297,6 +340,10 @@ struct Traits<LW_Q1_0> {
     // sum (2b - 1) * d * x = d * (2 * sum b*x - sum x)
     __device__ static float dot(const Packet& p, const float4* xv, float sx, int) {
         return half_bits_to_float(p.d) * __builtin_fmaf(2.0f, bit_dot(p.b, xv), -sx);
+    }
+    // the same over x pre-scaled by q1_prescale (sx the sum of the plain x)
+    __device__ static float dot_pre(const Packet& p, const float4* xv, float sx) {
+        return half_bits_to_float(p.d) * __builtin_fmaf(2.0f, bit_dot_pre(p.b, xv), -sx);
     }
 };
 
@@ -759,16 +806,18 @@ __device__ __forceinline__ void dot24(const Traits<LW_Q4_0>::Packet& p, const fl
 
 // acc[t] += (q1_0 contribution of the lane for token t) * 2^-24:
 // d * (2 * sum b*x_t - sum x_t); the masks of the 16 bit pairs serve every
-// token (a bit masked into bit 0 of a half is b * 2^-24, as in bit_dot).
+// token, x_t pre-scaled by q1_prescale (so each masked bit times its x is
+// b * x * 2^-24, as in bit_dot_pre).
 template <int NTK>
 __device__ __forceinline__ void dot24(const Traits<LW_Q1_0>::Packet& p, const float4* const* xv,
                                       const float* sx24, const SubBlock&, float* acc) {
     float lo_s[NTK], hi_s[NTK];
 #pragma unroll
     for (int t = 0; t < NTK; ++t) lo_s[t] = hi_s[t] = 0.f;
+    const uint32_t w4 = p.b >> 4;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-        const uint32_t m = opaque((p.b >> i) & 0x00010001u);
+        const uint32_t m = q1_mask(p.b, w4, i);
         const int c = i & 3;
 #pragma unroll
         for (int t = 0; t < NTK; ++t) {
@@ -1067,9 +1116,18 @@ __global__ void __launch_bounds__(NW * kWave)
         const int c = t / kWave, l = t - c * kWave;
         float sum = 0.f;
 #pragma unroll
-        for (int j4 = 0; j4 < J4; ++j4) {
-            xs[(c * J4 + j4) * kWave + l] = v[j4];
-            sum += (v[j4].x + v[j4].y) + (v[j4].z + v[j4].w);
+        for (int j4 = 0; j4 < J4; ++j4) sum += (v[j4].x + v[j4].y) + (v[j4].z + v[j4].w);
+        if constexpr (FMT == LW_Q1_0) {
+            // the 1-bit dot reads x pre-scaled (the sums stay those of x)
+            float4 u[J4];
+#pragma unroll
+            for (int j4 = 0; j4 < J4; ++j4) u[j4] = v[j4];
+            q1_prescale(u);
+#pragma unroll
+            for (int j4 = 0; j4 < J4; ++j4) xs[(c * J4 + j4) * kWave + l] = u[j4];
+        } else {
+#pragma unroll
+            for (int j4 = 0; j4 < J4; ++j4) xs[(c * J4 + j4) * kWave + l] = v[j4];
         }
         if (T::kGroupSums) sxs[t] = sum;
     };
@@ -1098,7 +1156,11 @@ __global__ void __launch_bounds__(NW * kWave)
         const float sx = T::kGroupSums ? sxs[c * kWave + lane] : 0.f;
 #pragma unroll
         for (int r = 0; r < R; ++r) {
-            const float v = T::dot(pk[r], xv, sx, j);
+            float v;
+            if constexpr (FMT == LW_Q1_0)
+                v = T::dot_pre(pk[r], xv, sx);
+            else
+                v = T::dot(pk[r], xv, sx, j);
             acc[r] += ok ? v : 0.f;
         }
     };
@@ -1254,6 +1316,7 @@ __global__ void __launch_bounds__(G * WPR * kWave)
             const int tc = t * NC + w * CPW + cc;
 #pragma unroll
             for (int j4 = 0; j4 < J4; ++j4) xr[t][cc][j4] = xs[(tc * J4 + j4) * kWave + (lane ^ j4)];
+            if constexpr (FMT == LW_Q1_0) q1_prescale(xr[t][cc]);  // the 1-bit dot's form
             sx24[t][cc] = sxs[tc * kWave + lane] * 5.9604644775390625e-8f;  // 2^-24
         }
 
