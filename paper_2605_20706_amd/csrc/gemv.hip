@@ -462,6 +462,45 @@ __device__ __forceinline__ float sum16(const float4* x4) {
            (((x4[2].x + x4[2].y) + (x4[2].z + x4[2].w)) + ((x4[3].x + x4[3].y) + (x4[3].z + x4[3].w)));
 }
 
+// One AND per pair of 2-bit codes. A 2-bit field at bits 2j, 2j+1 <= 9 of a
+// binary16 half lies in the mantissa, so it reads as c * 2^(2j - 24)
+// exactly; fields 5..7 (bits 10..15) are shifted down by 6 first (bits
+// 4..9). With the lane's x pre-multiplied by 2^-t(e) (q2_prescale: t = 2j
+// for fields 0..4, 2j - 6 for 5..7, j = (e mod 16) mod 8 the field of element
+// e), each masked field times its x is c * x * 2^-24, the product
+// two_bit_dot forms. 9 instead of 16 mask instructions per 16 codes.
+__device__ __forceinline__ int q2_shift(int e) {
+    const int j = (e & 15) & 7;
+    return j <= 4 ? 2 * j : 2 * j - 6;
+}
+
+__device__ __forceinline__ void q2_prescale(float4* xv) {  // the lane's 8 float4 (32 elements)
+#pragma unroll
+    for (int j4 = 0; j4 < 8; ++j4) {
+        xv[j4].x = __builtin_ldexpf(xv[j4].x, -q2_shift(4 * j4 + 0));
+        xv[j4].y = __builtin_ldexpf(xv[j4].y, -q2_shift(4 * j4 + 1));
+        xv[j4].z = __builtin_ldexpf(xv[j4].z, -q2_shift(4 * j4 + 2));
+        xv[j4].w = __builtin_ldexpf(xv[j4].w, -q2_shift(4 * j4 + 3));
+    }
+}
+
+// two_bit_dot over x pre-scaled by q2_prescale
+__device__ __forceinline__ float two_bit_dot_pre(uint32_t w, const float4* x4) {
+    float a = 0.f, b = 0.f;
+    const uint32_t w6 = w >> 6;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const uint32_t m = opaque((j <= 4 ? w : w6) & (0x00030003u << (j <= 4 ? 2 * j : 2 * j - 6)));
+        const float4& xl = x4[j >> 2];
+        const float4& xh = x4[2 + (j >> 2)];
+        const float vl = (j & 3) == 0 ? xl.x : (j & 3) == 1 ? xl.y : (j & 3) == 2 ? xl.z : xl.w;
+        const float vh = (j & 3) == 0 ? xh.x : (j & 3) == 1 ? xh.y : (j & 3) == 2 ? xh.z : xh.w;
+        a = __builtin_fmaf(half_of<0>(m), vl, a);
+        b = __builtin_fmaf(half_of<1>(m), vh, b);
+    }
+    return (a + b) * 16777216.0f;  // 2^24
+}
+
 // The 6-bit sub-block fields of a K-quant record {r0, r1, r2} (sc_j at bit
 // 6j, m_j at bit 48 + 6j), as floats.
 __device__ __forceinline__ void record_fields(uint32_t r0, uint32_t r1, uint32_t r2, int j, float& sc, float& m) {
@@ -678,6 +717,16 @@ struct Traits<LW_Q2_K> {
     __device__ static float dot(const Packet& p, const float4* xv, float sx, int) {
         const float qa = two_bit_dot(p.c.x, xv), qb = two_bit_dot(p.c.y, xv + 4);
         const float sxa = sum16(xv), sxb = sx - sxa;
+        const float d = half_bits_to_float(p.dd & 0xFFFFu), dmin = half_bits_to_float(p.dd >> 16);
+        const float dsa = d * (float)(p.scm & 15u), dma = dmin * (float)((p.scm >> 4) & 15u);
+        const float dsb = d * (float)((p.scm >> 8) & 15u), dmb = dmin * (float)((p.scm >> 12) & 15u);
+        return __builtin_fmaf(dsa, qa, -dma * sxa) + __builtin_fmaf(dsb, qb, -dmb * sxb);
+    }
+    // the same over x pre-scaled by q2_prescale, sxa the sum of the plain x's
+    // first 16 elements (staged once with x)
+    __device__ static float dot_pre(const Packet& p, const float4* xv, float sx, float sxa) {
+        const float qa = two_bit_dot_pre(p.c.x, xv), qb = two_bit_dot_pre(p.c.y, xv + 4);
+        const float sxb = sx - sxa;
         const float d = half_bits_to_float(p.dd & 0xFFFFu), dmin = half_bits_to_float(p.dd >> 16);
         const float dsa = d * (float)(p.scm & 15u), dma = dmin * (float)((p.scm >> 4) & 15u);
         const float dsb = d * (float)((p.scm >> 8) & 15u), dmb = dmin * (float)((p.scm >> 12) & 15u);
@@ -1064,6 +1113,7 @@ __global__ void __launch_bounds__(NW * kWave)
     const int nc = (int)((K + E - 1) / E);  // chunks per row = steps per batch
     float4* xs = smem;                                          // nc * E floats, lane-interleaved
     float* sxs = reinterpret_cast<float*>(smem + nc * (E / 4));  // nc * 64 group sums (4-bit formats)
+    float* sxs16 = sxs + nc * kWave;                              // Q2_K: sums of each group's first 16
     const int64_t nbatch = (M + R - 1) / R;
     const int64_t bstride = (int64_t)gridDim.x * NW;
     const int64_t b0 = (int64_t)blockIdx.x * NW + wave;
@@ -1117,12 +1167,17 @@ __global__ void __launch_bounds__(NW * kWave)
         float sum = 0.f;
 #pragma unroll
         for (int j4 = 0; j4 < J4; ++j4) sum += (v[j4].x + v[j4].y) + (v[j4].z + v[j4].w);
-        if constexpr (FMT == LW_Q1_0) {
-            // the 1-bit dot reads x pre-scaled (the sums stay those of x)
+        if constexpr (FMT == LW_Q1_0 || FMT == LW_Q2_K) {
+            // the 1- and 2-bit dots read x pre-scaled (the sums stay those of x)
             float4 u[J4];
 #pragma unroll
             for (int j4 = 0; j4 < J4; ++j4) u[j4] = v[j4];
-            q1_prescale(u);
+            if constexpr (FMT == LW_Q1_0) {
+                q1_prescale(u);
+            } else {
+                sxs16[t] = sum16(v);
+                q2_prescale(u);
+            }
 #pragma unroll
             for (int j4 = 0; j4 < J4; ++j4) xs[(c * J4 + j4) * kWave + l] = u[j4];
         } else {
@@ -1159,6 +1214,8 @@ __global__ void __launch_bounds__(NW * kWave)
             float v;
             if constexpr (FMT == LW_Q1_0)
                 v = T::dot_pre(pk[r], xv, sx);
+            else if constexpr (FMT == LW_Q2_K)
+                v = T::dot_pre(pk[r], xv, sx, sxs16[c * kWave + lane]);
             else
                 v = T::dot(pk[r], xv, sx, j);
             acc[r] += ok ? v : 0.f;
@@ -1453,7 +1510,8 @@ hipError_t launch_single_segs(const RowSegs<NS>& sg, const float* x, int64_t M, 
     constexpr int NW = 8;
     constexpr int E = kWave * Traits<FMT>::EPL;
     const int64_t nc = (K + E - 1) / E;
-    const int64_t lds = nc * E * 4 + (Traits<FMT>::kGroupSums ? nc * kWave * 4 : 0);
+    const int64_t lds = nc * E * 4 + (Traits<FMT>::kGroupSums ? nc * kWave * 4 : 0) +
+                        (FMT == LW_Q2_K ? nc * kWave * 4 : 0);  // Q2_K: the first-16 sums
     if (lds > kLdsBytes || max_total >= ((int64_t)1 << 32) || M >= ((int64_t)1 << 31)) return hipErrorNotSupported;
     const int64_t nbatch = (M + R - 1) / R;
     int64_t grid = (nbatch + NW - 1) / NW;
