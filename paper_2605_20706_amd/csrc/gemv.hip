@@ -900,8 +900,10 @@ __device__ __forceinline__ void dot24(const Traits<LW_Q4_K>::Packet& p, const fl
                                       const float* sx24, const SubBlock& sb, float* acc) {
     const uint32_t sc_w = __builtin_amdgcn_alignbit(p.r1, sb.sl ? p.r0 : p.r1, sb.ts & 31u);
     const uint32_t m_w = __builtin_amdgcn_alignbit(p.r2, sb.ml ? p.r1 : p.r2, sb.tm & 31u);
-    const float ds = half_bits_to_float(p.dd & 0xFFFFu) * (float)(sc_w & 63u);
-    const float dm = half_bits_to_float(p.dd >> 16) * (float)(m_w & 63u);
+    // d * sc and dmin * m, each one v_fma_mix with the binary16 operand (a +0
+    // addend, which the compiler keeps; only an exact -0 product turns +0)
+    const float ds = __builtin_fmaf(half_of<0>(p.dd), (float)(sc_w & 63u), 0.0f);
+    const float dm = __builtin_fmaf(half_of<1>(p.dd), (float)(m_w & 63u), 0.0f);
     float qx[NTK];
     nibble_dot24<NTK>(p.c, xv, qx);
 #pragma unroll
