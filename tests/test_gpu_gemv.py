@@ -12,7 +12,7 @@ import pytest
 import gate
 from gpu_util import gpu_matvec, to_gpu
 from parity import Ref, kernel_of, reference
-from paper_2605_20706_amd import synth
+from paper_2605_20706_amd import binding, synth
 from paper_2605_20706_amd.layout import F16, MXFP4, Q1_0, Q2_K, Q4_0, Q4_1, Q4_K, Q5_0, Q5_1, Q5_K, Q6_K, Q8_0
 
 pytestmark = pytest.mark.gpu
@@ -117,6 +117,27 @@ def test_one_hot_columns(oracle_mod, fmt):
     for i, k in enumerate(ks):
         err = np.abs(y[i].astype(np.float64) - Wd[:, k]).max()
         assert err <= 1e-6 * np.abs(Wd[:, k]).max(), (fmt, k, err)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("K", [2048, 2304])
+def test_one_hot_every_lane_position(oracle_mod, fmt, K):
+    """x = e_k for every element position k of two lanes' 32-element slices
+    (and the last two of the row) returns column k of the dequantized matrix
+    bit-exactly, on the register kernel (K = 2048) and the LDS kernel
+    (K = 2304): pins the per-position handling of the one-token dots,
+    including the 1- and 2-bit dots that pre-scale x by the power of two of
+    each code's bit position."""
+    M = 70
+    W = synth.gen_packed(fmt, M * K, np.random.default_rng([4, fmt, K]))
+    Wd = oracle_mod.dequant(fmt, W, M * K).reshape(M, K)
+    Wg = to_gpu(W)
+    print("one-hot fmt=%d K=%d kernel=%s" % (fmt, K, binding.kernel_name(fmt, M, K, 1)), flush=True)
+    for k in list(range(64)) + [K - 2, K - 1]:
+        x = np.zeros(K, np.float32)
+        x[k] = 1.0
+        y = gpu_matvec(fmt, W, x, M, K, Wg=Wg)
+        assert np.array_equal(y[0], Wd[:, k]), (fmt, K, k)
 
 
 @pytest.mark.parametrize("fmt", FMTS)
